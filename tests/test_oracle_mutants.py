@@ -1,0 +1,79 @@
+"""Pin strength: each plausible mistake planted in a copy of the oracle must be
+caught by at least one pin.  CPU only; the mutants live here, not in oracle/."""
+import numpy as np
+import pytest
+
+import pins
+
+
+class Mutant:
+    """The oracle's pack/unpack with one planted mistake selected by `bug`."""
+
+    def __init__(self, bug):
+        self.bug = bug
+
+    def _index(self, bt, n, P):
+        t = np.arange(n)
+        if self.bug == "div_mod_swapped":
+            return np.asarray(bt)[t % P], t // P
+        if self.bug == "token_off_by_one":
+            return np.asarray(bt)[np.minimum(t + 1, n - 1) // P], (np.minimum(t + 1, n - 1)) % P
+        if self.bug == "slot_reversed":
+            return np.asarray(bt)[t // P], (P - 1) - t % P
+        return np.asarray(bt)[t // P], t % P
+
+    def pack_request(self, pool, layer, bt, n):
+        P = pool.shape[3]
+        n = int(n)
+        pages, slots = self._index(bt, n, P)
+        if self.bug == "wrong_layer":
+            layer = 0
+        g = pool[layer][pages, :, slots]                      # (n, C, H, D)
+        if self.bug == "no_plane_transpose":
+            out = g
+        elif self.bug == "heads_dims_swapped":
+            out = g.transpose(1, 0, 3, 2)
+        else:
+            out = g.transpose(1, 0, 2, 3)
+        if self.bug == "drops_v_plane":
+            out = out[:1]
+        return np.ascontiguousarray(out)
+
+    def pack_layer(self, pool, layer, bts, lens):
+        order = range(len(lens))
+        if self.bug == "requests_reversed":
+            order = reversed(list(order))
+        parts = [self.pack_request(pool, layer, bts[r], lens[r]).reshape(-1) for r in order]
+        return np.concatenate(parts) if parts else np.empty(0, pool.dtype)
+
+    def unpack_layer(self, packed, pool, layer, bts, lens):
+        C, P, H, D = pool.shape[2], pool.shape[3], pool.shape[4], pool.shape[5]
+        if self.bug == "unpack_assumes_page16":
+            P = 16
+        off = 0
+        for r in range(len(lens)):
+            n = int(lens[r])
+            size = C * n * H * D
+            start = 0 if self.bug == "unpack_no_request_offset" else off
+            block = packed[start:start + size].reshape(C, n, H, D)
+            pages, slots = self._index(bts[r], n, P)
+            pool[layer][pages, :, slots % pool.shape[3]] = block.transpose(1, 0, 2, 3)
+            if self.bug == "unpack_zero_fills_tail" and n % pool.shape[3]:
+                pool[layer][bts[r][(n - 1) // pool.shape[3]], :, n % pool.shape[3]:] = 0
+            off += size
+        return pool
+
+
+BUGS = ["div_mod_swapped", "token_off_by_one", "slot_reversed", "wrong_layer",
+        "no_plane_transpose", "heads_dims_swapped", "drops_v_plane", "requests_reversed",
+        "unpack_assumes_page16", "unpack_no_request_offset", "unpack_zero_fills_tail"]
+
+
+def test_unmutated_copy_passes():
+    assert pins.failing_pins(Mutant(None)) == []
+
+
+@pytest.mark.parametrize("bug", BUGS)
+def test_mutant_is_caught(bug):
+    failed = pins.failing_pins(Mutant(bug))
+    assert failed, f"no pin catches the planted mistake {bug!r}"
