@@ -1,0 +1,277 @@
+#!/usr/bin/env python3
+"""Per-layer paged KV-cache pack + unpack throughput on one MI355X.
+
+One step = pack every layer of the workload (one batched launch per layer,
+pool -> contiguous send buffer), then unpack every layer (one launch per
+layer, send buffer -> destination pool), i.e. the per-layer transfer unit of
+the paper's pipelined layer-by-layer KV transfer (Section 5.2) for both ends.
+
+value      = algorithmic bytes of the whole step / wall time of the step (GB/s,
+             10^9), inputs resident in HBM, timed with HIP events over exactly
+             --steps steps after --warmup untimed ones.
+roofline   = the dominant kernel's algorithmic bytes per launch / its average
+             launch duration; durations are the kernels' own begin/end
+             timestamps (hipExtLaunchKernel events) over the timed region.
+cpu_baseline = the CPU oracle (numpy, one thread) on a bounded sample of the
+             same workload, on this host, same byte definition.
+
+Algorithmic bytes per layer and direction: read + write of
+planes * sum(n) * row_bytes each, plus 4 B per block-table entry read
+(ceil(n/P) per request, P of the pool being read or written) and 4 B per
+seq_len.  Cache defeat: every layer packs into its own buffer slice while the
+packed volume fits 2 GiB (ring otherwise), and the whole pack sweep runs
+before the unpack sweep, so no kernel reads data another just wrote (the
+MI355X last-level cache holds 256 MB).
+
+    python bench.py [--steps K] [--warmup W] [--workload NAME]
+    python bench.py --calib-copy-bytes N   # plain copy kernel, for PMC scaling
+"""
+import argparse
+import hashlib
+import json
+import math
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+HBM_PEAK_GBS = 8000.0          # MI355X HBM3E, AMD published peak
+PROFILES = os.path.join(ROOT, "profiles")
+KERNEL_SOURCE = os.path.join(ROOT, "paper_2607_28633_amd", "csrc", "topkv.hip")
+
+
+def log(msg):
+    print(msg, file=sys.stderr, flush=True)
+
+
+def parse():
+    from paper_2607_28633_amd.workloads import WORKLOADS
+    ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=10)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--workload", default="llama3-70b-4k", choices=sorted(WORKLOADS))
+    ap.add_argument("--cpu-seconds", type=float, default=10.0,
+                    help="budget of the CPU-oracle sample (0 disables it)")
+    ap.add_argument("--calib-copy-bytes", type=int, default=0,
+                    help="instead of the workload, run a plain device copy of this many bytes")
+    return ap.parse_args()
+
+
+def step_bytes(wl):
+    """Algorithmic bytes of one pack launch and one unpack launch (one layer)."""
+    import numpy as np
+    row = wl.num_heads * wl.head_dim * wl.elem_bytes
+    moved = wl.planes * int(wl.seq_lens.astype(np.int64).sum()) * row
+    pages = sum(-(-int(n) // wl.page_size) for n in wl.seq_lens)
+    pages2 = sum(-(-int(n) // wl.dst_page_size) for n in wl.seq_lens)
+    return 2 * moved + 4 * pages + 4 * wl.num_reqs, 2 * moved + 4 * pages2 + 4 * wl.num_reqs
+
+
+def read_traffic(workload):
+    """HBM traffic per launch from the committed rocprofv3 --pmc summary, or
+    None when the kernel source has changed since the counters were taken."""
+    path = os.path.join(PROFILES, f"kv_pack_unpack_{workload}_pmc.txt")
+    if not os.path.exists(path):
+        return None
+    vals = {}
+    for line in open(path):
+        if "=" in line and not line.lstrip().startswith("#"):
+            k, v = line.split("=", 1)
+            vals[k.strip()] = v.strip()
+    digest = hashlib.sha256(open(KERNEL_SOURCE, "rb").read()).hexdigest()
+    if vals.get("kernel_source_sha256") != digest:
+        return None
+    return vals
+
+
+def calib_copy(args):
+    import torch
+    n = int(args.calib_copy_bytes)
+    a = torch.empty(n, dtype=torch.uint8, device="cuda").fill_(1)
+    b = torch.empty_like(a)
+    for _ in range(args.warmup + args.steps):
+        b.copy_(a)
+    torch.cuda.synchronize()
+    print(json.dumps({"calib_copy_bytes": n, "launches": args.warmup + args.steps}), flush=True)
+
+
+def cpu_baseline(wl, src, dst, budget_s):
+    """Time the oracle on host copies of a few layer slabs, cycling until the
+    budget is spent.  Returns the cpu_baseline object."""
+    import numpy as np
+    import oracle
+    import torch
+
+    def to_host_words(t):   # device bf16 slab -> host uint16 words, bit-exact
+        return t.view(torch.int16).cpu().numpy().view(np.uint16)
+
+    pack_b, unpack_b = step_bytes(wl)
+    slabs = list(range(min(wl.phys_layers, 4)))
+    host = {s: (to_host_words(src[s])[None], to_host_words(dst[s])[None]) for s in slabs}
+    done_bytes, spent, layers = 0, 0.0, 0
+    while spent < budget_s and layers < 10_000:
+        s = slabs[layers % len(slabs)]
+        src_h, dst_h = host[s]
+        t0 = time.perf_counter()
+        packed = oracle.pack_layer(src_h, 0, wl.block_tables, wl.seq_lens)
+        oracle.unpack_layer(packed, dst_h, 0, wl.dst_block_tables, wl.seq_lens)
+        spent += time.perf_counter() - t0
+        done_bytes += pack_b + unpack_b
+        layers += 1
+    cpu = "unknown"
+    try:
+        for line in open("/proc/cpuinfo"):
+            if line.startswith("model name"):
+                cpu = line.split(":", 1)[1].strip()
+                break
+    except OSError:
+        pass
+    return {"value": round(done_bytes / spent / 1e9, 3), "unit": "GB/s", "cores": 1, "kind": "oracle",
+            "sample": (f"{layers} layer pack+unpack passes of {wl.name} over host copies of "
+                       f"{len(slabs)} layer slab(s), numpy oracle, one thread, {spent:.1f} s"),
+            "cpu_model": cpu, "host_threads_available": len(os.sched_getaffinity(0)),
+            "ms_per_layer_pack_unpack": round(1e3 * spent / layers, 3)}
+
+
+def run(args):
+    import numpy as np
+    import torch
+
+    from paper_2607_28633_amd import topkv
+    from paper_2607_28633_amd.workloads import WORKLOADS, device_dst_prefill, device_src_pool, make_workload
+
+    torch.cuda.set_device(0)
+    wl = make_workload(args.workload)
+    log(f"[bench] workload {wl.describe()}")
+    src = device_src_pool(wl)
+    dst = device_dst_prefill(wl)
+    bt = torch.from_numpy(wl.block_tables).cuda()
+    bt2 = torch.from_numpy(wl.dst_block_tables).cuda()
+    lens = torch.from_numpy(wl.seq_lens).cuda()
+    nbytes = topkv.topkv_packed_layer_bytes(src, wl.seq_lens)
+    L, R = wl.num_layers, wl.num_reqs
+    ring = min(L, max(2, (2 << 30) // max(nbytes, 1)))
+    packed = torch.empty((ring, nbytes // 2), dtype=torch.int16, device="cuda")
+    stream = torch.cuda.current_stream()
+    log(f"[bench] pools src {tuple(src.shape)} dst {tuple(dst.shape)}, packed {nbytes} B/layer, ring {ring}")
+
+    def sweep(evs):
+        """The launches of one step, arguments marshalled up front."""
+        calls = []
+        for l in range(L):
+            e = evs[0][l] if evs else (None, None)
+            calls.append(topkv.prepare_pack_layer_batched_ex(
+                src, l % wl.phys_layers, R, bt, bt.shape[1], lens, packed[l % ring], stream=stream,
+                start=e[0], stop=e[1]))
+        for l in range(L):
+            e = evs[1][l] if evs else (None, None)
+            calls.append(topkv.prepare_unpack_layer_batched_ex(
+                packed[l % ring], dst, l % wl.phys_layers, R, bt2, bt2.shape[1], lens, stream=stream,
+                start=e[0], stop=e[1]))
+        return calls
+
+    def step(calls):
+        for c in calls:
+            c()
+
+    plain = sweep(None)
+    for _ in range(args.warmup):
+        step(plain)
+    torch.cuda.synchronize()
+    log(f"[bench] {args.warmup} warmup steps done")
+
+    evs = [[[(topkv.HipEvent(), topkv.HipEvent()) for _ in range(L)] for _ in range(2)]
+           for _ in range(args.steps)]
+    timed = [sweep(evs[k]) for k in range(args.steps)]
+    t_start, t_stop = topkv.HipEvent(), topkv.HipEvent()
+    torch.cuda.synchronize()
+    h0 = time.perf_counter()
+    t_start.record(stream)
+    for k in range(args.steps):
+        step(timed[k])
+    t_stop.record(stream)
+    t_stop.synchronize()
+    torch.cuda.synchronize()
+    host_s = time.perf_counter() - h0
+    wall_ms = t_start.elapsed_ms(t_stop)
+    ms_per_step = wall_ms / args.steps
+    log(f"[bench] {args.steps} timed steps: {wall_ms:.3f} ms on the GPU clock, {host_s * 1e3:.3f} ms host")
+
+    pack_b, unpack_b = step_bytes(wl)
+    bytes_step = L * (pack_b + unpack_b)
+    dur = {d: np.array([[evs[k][d][l][0].elapsed_ms(evs[k][d][l][1]) for l in range(L)]
+                        for k in range(args.steps)]) * 1e3 for d in (0, 1)}   # microseconds
+    kern = {}
+    for d, name, b in ((0, "pack", pack_b), (1, "unpack", unpack_b)):
+        us = float(dur[d].mean())
+        kern[name] = {"bytes_per_launch": b, "avg_us": round(us, 3), "median_us": round(float(np.median(dur[d])), 3),
+                      "min_us": round(float(dur[d].min()), 3), "gbs": round(b / us / 1e3, 1),
+                      "launches": int(dur[d].size)}
+    dom = max(kern, key=lambda k: kern[k]["avg_us"] * kern[k]["launches"])
+    traffic_vals = read_traffic(args.workload)
+    traffic = None
+    if traffic_vals and f"{dom}_hbm_bytes_per_launch" in traffic_vals:
+        traffic = float(traffic_vals[f"{dom}_hbm_bytes_per_launch"])
+    achieved = kern[dom]["gbs"]
+    roofline = {"bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": traffic,
+                "kernel": f"kv_{dom}_kernel", "bytes_per_launch": kern[dom]["bytes_per_launch"],
+                "avg_launch_us": kern[dom]["avg_us"]}
+
+    # practical ceiling on this machine: a plain device copy of one layer's bytes
+    # into as many distinct buffers as the pack sweep uses (same cache defeat)
+    flat = src.view(-1).view(torch.int16)
+    ce0, ce1 = topkv.HipEvent(), topkv.HipEvent()
+    n_el = nbytes // 2
+    for _ in range(2):
+        ce0.record(stream)
+        for l in range(L):
+            off = ((l * 7919 * n_el) % max(1, flat.numel() - n_el)) // 4096 * 4096
+            packed[l % ring].copy_(flat[off:off + n_el])
+        ce1.record(stream)
+        ce1.synchronize()
+    copy_gbs = 2 * nbytes * L / (ce0.elapsed_ms(ce1) * 1e-3) / 1e9
+
+    out = {
+        "metric": "per-layer KV pack+unpack HBM GB/s (% of MI355X peak), 70B GQA 4K tokens",
+        "value": round(bytes_step / (ms_per_step * 1e-3) / 1e9, 1),
+        "unit": "GB/s", "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
+        "ms_per_step": round(ms_per_step, 4), "higher_is_better": True, "scaling": "weak",
+        "vs_baseline": None, "dtype": "bf16", "data": "synthetic",
+        "config": {"workload": f"{wl.name}: {WORKLOADS[wl.name]}", "layers": L, "requests": R,
+                   "tokens": int(wl.seq_lens.astype(np.int64).sum()), "page_size": wl.page_size,
+                   "dst_page_size": wl.dst_page_size, "packed_bytes_per_layer": nbytes,
+                   "step": "pack every layer (1 launch each), then unpack every layer",
+                   "seed": wl.seed, "packed_ring": ring, "phys_layers": wl.phys_layers},
+        "pct_of_peak": round(100 * bytes_step / (ms_per_step * 1e-3) / 1e9 / HBM_PEAK_GBS, 2),
+        "wall_us_per_layer": {"pack+unpack": round(1e3 * ms_per_step / L, 3)},
+        "kernels": kern,
+        "roofline": roofline,
+        "copy_ceiling_gbs": round(copy_gbs, 1),
+    }
+    if args.cpu_seconds > 0:
+        log(f"[bench] CPU oracle sample (~{args.cpu_seconds} s)")
+        out["cpu_baseline"] = cpu_baseline(wl, src, dst, args.cpu_seconds)
+    else:
+        out["cpu_baseline"] = None
+    print(json.dumps(out), flush=True)
+
+
+def main():
+    args = parse()
+    world = int(os.environ.get("WORLD_SIZE", "1"))
+    if args.gpus != 1 or world != 1:
+        print(f"bench.py: this build measures one GPU only (asked for --gpus {args.gpus}, WORLD_SIZE {world}); "
+              "the per-layer pack/unpack has no multi-GPU leg here", file=sys.stderr, flush=True)
+        sys.exit(2)
+    if args.calib_copy_bytes:
+        calib_copy(args)
+    else:
+        run(args)
+
+
+if __name__ == "__main__":
+    main()

@@ -1,0 +1,175 @@
+/*
+ * topkv.h - per-layer paged KV-cache pack / unpack for AMD MI355X (gfx950).
+ *
+ * C ABI of libtopkv.so.  Every entry point takes plain device pointers and
+ * sizes, launches hand-written HIP kernels on the caller's stream and returns
+ * without synchronising.  The library never allocates, frees or keeps
+ * per-call state; it caches only each device's compute-unit count.
+ *
+ * What is computed (arxiv 2607.28633, "Topology-Aware Data Movement for
+ * Disaggregated GPU Inference"):
+ *   - Section 5.2: a prefill worker sends layer l's KV cache while later
+ *     layers still compute, so the unit of transfer is one layer.
+ *   - Section 3.5: on the wire, K and V are contiguous tensors indexed
+ *     [seq_len][kv_heads][head_dim] within a layer (single-DMA sends).
+ *   - Section 6: both sides keep the cache in fixed-size pages reached
+ *     through per-request block tables (PagedAttention).
+ *   - Section 2.2, Eq. 1: a request of s tokens moves
+ *     2 * L * h_kv * d_h * s * b_p bytes over L layers; Section 5.3: an MLA
+ *     cache holds one shared latent per token and layer, no factor 2.
+ *
+ * Pool layout (topkv_pool_t), row-major:
+ *     base[layer][page][plane][slot][head][dim]
+ *   planes = 2 (K then V) or 1 (MLA latent); slot runs over page_size tokens;
+ *   one element is elem_bytes opaque bytes (never interpreted: NaN payloads,
+ *   -0 and subnormals are moved bit-exactly).  A "row" is one token of one
+ *   plane: row_bytes = num_heads * head_dim * elem_bytes.
+ *
+ * Packed layout (one layer): per request r, in request order,
+ *     [plane][token t < n_r][head][dim]
+ *   so request r starts at byte planes * row_bytes * (n_0 + ... + n_{r-1}).
+ *
+ * Pack:   packed_r[c][t] = pool[layer][bt_r[t / P]][c][t % P]        t < n_r
+ * Unpack: pool[layer][bt_r[t / P']][c][t % P'] = packed_r[c][t]      t < n_r
+ *   where P / P' are the page sizes of the pool being read / written.  The
+ *   packed form has no pages, so unpacking into a pool of another page size
+ *   re-blocks.  Unpack writes only the slots of valid tokens: every other
+ *   byte of the destination pool (other pages, and slots past the last token
+ *   of a request's last page) keeps its value.
+ *
+ * Block tables: int32, device memory.  Entry i of request r is the physical
+ * page (in [0, num_pages)) holding tokens [i*P, i*P + P).  Only the first
+ * ceil(n_r / P) entries of a row are read; later entries may hold anything.
+ * Within one unpack launch no destination page may be named twice (the
+ * writes would race); pack has no such restriction.
+ *
+ * Errors: argument problems the host can see return a status before any
+ * launch (TOPKV_ERR_INVALID_ARG for null pointers, out-of-range layer or
+ * non-positive dimensions, TOPKV_ERR_UNSUPPORTED for sizes beyond the
+ * documented limits).  A failed launch returns TOPKV_ERR_LAUNCH.  Device-side
+ * contents are not trusted: a table entry outside [0, num_pages) makes the
+ * kernel skip that page (nothing read or written for it); a device seq_len
+ * below 0 counts as 0 and one above bt_stride * P as bt_stride * P; a batched
+ * request whose packed block would cross the end of the packed buffer is not
+ * moved.  Such skips are silent.
+ * Overlapping source and destination ranges are undefined behaviour.
+ *
+ * Build: hipcc --offload-arch=gfx950 (see the package's build script).  C
+ * callers compile with -D__HIP_PLATFORM_AMD__ -I/opt/rocm/include.
+ */
+#ifndef TOPKV_H_
+#define TOPKV_H_
+
+#include <stdint.h>
+#include <hip/hip_runtime_api.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum topkv_status {
+  TOPKV_OK = 0,
+  TOPKV_ERR_INVALID_ARG = 1,  /* null pointer, bad layer index, non-positive dimension */
+  TOPKV_ERR_UNSUPPORTED = 2,  /* valid but beyond the library's limits (see each call) */
+  TOPKV_ERR_LAUNCH = 3,       /* the HIP runtime refused the launch */
+  TOPKV_ERR_BOUNDS = 4,       /* topkv_check_tables found an invalid table or length */
+  TOPKV_ERR_DEVICE = 5        /* a HIP runtime query failed */
+} topkv_status_t;
+
+/* One paged KV pool.  The caller owns the memory.  All counts are elements
+ * or tokens; layer stride = num_pages * planes * page_size * row_bytes. */
+typedef struct topkv_pool {
+  void*   base;        /* device pointer to base[num_layers][num_pages][planes][page_size][heads][dim] */
+  int64_t num_pages;   /* pages per layer, > 0 */
+  int32_t num_layers;  /* > 0 */
+  int32_t page_size;   /* tokens per page, > 0 */
+  int32_t planes;      /* 2 = K|V, 1 = MLA latent (any value > 0 is accepted) */
+  int32_t num_heads;   /* KV heads, > 0 */
+  int32_t head_dim;    /* > 0 */
+  int32_t elem_bytes;  /* 1, 2, 4 or 8 (bf16/fp16 caches: 2) */
+} topkv_pool_t;
+
+/* Launch options for the *_ex calls.  When start / stop are non-null they
+ * are stamped with the kernel's own begin / end time (hipExtLaunchKernel), so
+ * hipEventElapsedTime(start, stop) is the kernel duration without queueing
+ * gaps.  Events must have been created by the caller on the same device. */
+typedef struct topkv_launch {
+  hipStream_t stream;
+  hipEvent_t  start;
+  hipEvent_t  stop;
+} topkv_launch_t;
+
+/* Largest num_reqs one batched launch accepts (the per-request prefix sums
+ * live in LDS: 8 bytes per request).  Larger batches: split into launches. */
+#define TOPKV_MAX_BATCH_REQS 8000
+
+/* Pack one request's tokens of one layer (Sections 5.2, 3.5, 6).
+ *   src:         pool to read (device memory described by *src, host struct)
+ *   layer:       in [0, src->num_layers)
+ *   block_table: device int32[ceil(seq_len / src->page_size)]
+ *   seq_len:     tokens, >= 0 (0: nothing is launched)
+ *   dst:         device buffer of planes * seq_len * row_bytes bytes,
+ *                written as [plane][seq_len][heads][dim]
+ *   stream:      HIP stream the kernel is queued on */
+topkv_status_t topkv_pack_layer(const topkv_pool_t* src, int32_t layer,
+                                const int32_t* block_table, int32_t seq_len,
+                                void* dst, hipStream_t stream);
+
+/* Unpack one request's packed layer into a pool (inverse of
+ * topkv_pack_layer; dst->page_size may differ from the page size the data
+ * was packed from).  src holds planes * seq_len * row_bytes bytes. */
+topkv_status_t topkv_unpack_layer(const void* src, const topkv_pool_t* dst, int32_t layer,
+                                  const int32_t* block_table, int32_t seq_len,
+                                  hipStream_t stream);
+
+/* Pack num_reqs requests of one layer in ONE launch (Section 5.2 per-layer
+ * unit; batching keeps small layers from being launch-bound).
+ *   block_tables: device int32[num_reqs][bt_stride], bt_stride >= the
+ *                 largest ceil(seq_lens[r] / page_size)
+ *   seq_lens:     device int32[num_reqs]; request offsets in the packed
+ *                 buffer are prefix sums computed on the device
+ *   dst:          device buffer of dst_bytes bytes; the batch occupies the
+ *                 first planes * row_bytes * sum(seq_lens) bytes
+ *   num_reqs:     0 .. TOPKV_MAX_BATCH_REQS (0: nothing is launched) */
+topkv_status_t topkv_pack_layer_batched(const topkv_pool_t* src, int32_t layer,
+                                        int32_t num_reqs, const int32_t* block_tables,
+                                        int32_t bt_stride, const int32_t* seq_lens,
+                                        void* dst, int64_t dst_bytes, hipStream_t stream);
+
+/* Unpack num_reqs packed requests of one layer in one launch (inverse of
+ * topkv_pack_layer_batched; re-blocks when the pool's page size differs from
+ * the packing side's).  src holds src_bytes bytes of packed data. */
+topkv_status_t topkv_unpack_layer_batched(const void* src, int64_t src_bytes,
+                                          const topkv_pool_t* dst, int32_t layer,
+                                          int32_t num_reqs, const int32_t* block_tables,
+                                          int32_t bt_stride, const int32_t* seq_lens,
+                                          hipStream_t stream);
+
+/* The batched calls with launch options (kernel-timestamp events).
+ * launch must be non-null. */
+topkv_status_t topkv_pack_layer_batched_ex(const topkv_pool_t* src, int32_t layer,
+                                           int32_t num_reqs, const int32_t* block_tables,
+                                           int32_t bt_stride, const int32_t* seq_lens,
+                                           void* dst, int64_t dst_bytes,
+                                           const topkv_launch_t* launch);
+topkv_status_t topkv_unpack_layer_batched_ex(const void* src, int64_t src_bytes,
+                                             const topkv_pool_t* dst, int32_t layer,
+                                             int32_t num_reqs, const int32_t* block_tables,
+                                             int32_t bt_stride, const int32_t* seq_lens,
+                                             const topkv_launch_t* launch);
+
+/* Bytes of one layer's packed batch, planes * row_bytes * sum(seq_lens),
+ * computed on the host from HOST seq_lens (Eq. 1 for one layer; planes = 1
+ * for MLA per Section 5.3).  Returns -1 for a null/invalid pool, a null
+ * seq_lens with num_reqs > 0, a negative length or int64 overflow. */
+int64_t topkv_packed_layer_bytes(const topkv_pool_t* pool, const int32_t* seq_lens_host,
+                                 int32_t num_reqs);
+
+/* Static, human-readable name of a status code (never null). */
+const char* topkv_status_string(topkv_status_t status);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* TOPKV_H_ */

@@ -1,0 +1,59 @@
+"""Build libtopkv.so (HIP, gfx950) in-tree with hipcc.
+
+    python -m paper_2607_28633_amd.build            # -> paper_2607_28633_amd/libtopkv.so
+
+``build_library(defines=..., out=...)`` builds a variant with extra -D
+defines (TOPKV_VPT, TOPKV_WG_PER_CU, TOPKV_NONTEMPORAL) to another path, for
+launch-shape sweeps.
+"""
+from __future__ import annotations
+
+import os
+import shutil
+import subprocess
+import sys
+
+PKG = os.path.dirname(os.path.abspath(__file__))
+ROOT = os.path.dirname(PKG)
+SOURCES = [os.path.join(PKG, "csrc", "topkv.hip")]
+INCLUDE = os.path.join(ROOT, "include")
+LIBRARY = os.path.join(PKG, "libtopkv.so")
+ARCH = "gfx950"
+
+
+def hipcc() -> str:
+    for cand in (os.environ.get("HIPCC"), "/opt/rocm/bin/hipcc", shutil.which("hipcc")):
+        if cand and os.path.exists(cand):
+            return cand
+    raise RuntimeError("hipcc not found (ROCm is required to build libtopkv.so)")
+
+
+def build_command(out: str = LIBRARY, defines=None):
+    cmd = [hipcc(), f"--offload-arch={ARCH}", "-O3", "-std=c++17", "-fPIC", "-shared",
+           # packed-FP32 instructions are kept out of every kernel
+           "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
+           "-Wall", f"-I{INCLUDE}", "-o", out]
+    for k, v in (defines or {}).items():
+        cmd.append(f"-D{k}={v}")
+    return cmd + SOURCES
+
+
+def build_library(out: str = LIBRARY, defines=None, verbose: bool = False) -> str:
+    """Compile the library (always; no up-to-date check) and return its path."""
+    tmp = out + ".tmp"
+    cmd = build_command(tmp, defines)
+    if verbose:
+        print(" ".join(cmd), flush=True)
+    res = subprocess.run(cmd, capture_output=True, text=True)
+    noise = ("packed-fp32-ops", "argument unused during compilation")
+    msgs = [ln for ln in (res.stdout + res.stderr).splitlines() if ln and not any(x in ln for x in noise)]
+    if res.returncode != 0:
+        raise RuntimeError("hipcc failed:\n" + "\n".join(msgs))
+    if verbose and msgs:
+        print("\n".join(msgs))
+    os.replace(tmp, out)
+    return out
+
+
+if __name__ == "__main__":
+    print(build_library(verbose="-v" in sys.argv))

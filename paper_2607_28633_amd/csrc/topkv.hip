@@ -1,0 +1,484 @@
+// topkv.hip - HIP kernels (gfx950 / CDNA4) and the C ABI of libtopkv.so:
+// per-layer paged KV-cache pack (gather a layer's pages into the contiguous
+// [plane][token][head][dim] wire layout) and unpack (scatter it into a pool of
+// any page size).  The operation and the layouts are specified in
+// include/topkv.h (paper: Sections 3.5, 5.2, 6; Eq. 1 in Section 2.2 and the
+// MLA rule of Section 5.3 for sizes).
+//
+// Design (memory-bound byte movement, no MFMA, no arithmetic on values):
+//   * Work item = (request, logical page, plane, tile).  One page of one plane
+//     is a single contiguous run of min(P, n - i*P) rows on the pool side and
+//     also contiguous on the packed side, so every item is a plain contiguous
+//     copy of <= kTile bytes.  Unpack with another page size is the same
+//     kernel: its items are the DESTINATION pool's pages, which are again one
+//     contiguous run each (the packed form has no pages), so no layout
+//     transpose and no LDS staging is needed.
+//   * Each lane moves VPT 16-byte vectors: all loads are issued before any
+//     store, so a workgroup keeps kTile bytes in flight; the lane->vector
+//     mapping (j * kThreads + lane) makes each wave instruction touch one
+//     contiguous 1 KiB span (coalesced, full cache lines, no read-for-
+//     ownership on the write side).
+//   * Batched launches take device-resident seq_lens.  Each workgroup turns
+//     them into exclusive prefix sums of tokens and pages with a wave64
+//     shuffle scan (results in LDS), then maps its work items to requests by
+//     binary search.  The grid is sized from host-known bounds (num_reqs *
+//     bt_stride pages) and capped at a few workgroups per CU; workgroups
+//     stride over the items.
+//   * Device-side table entries and lengths are bounds-checked before any
+//     access, so malformed tables cannot make the kernel touch memory outside
+//     the pool or packed buffer.
+#include <hip/hip_runtime.h>
+#include <hip/hip_ext.h>
+
+#include <atomic>
+#include <cstdint>
+
+#include "topkv.h"
+
+#ifndef TOPKV_VPT
+#define TOPKV_VPT 4           // 16-byte vectors per lane per tile
+#endif
+#ifndef TOPKV_WG_PER_CU
+#define TOPKV_WG_PER_CU 8     // grid cap = CUs * this
+#endif
+#ifndef TOPKV_NONTEMPORAL
+#define TOPKV_NONTEMPORAL 1   // streaming hint on the bulk loads and stores
+#endif
+
+namespace topkv {
+
+constexpr int kThreads = 256;  // four wave64 per workgroup
+constexpr int kWaves = kThreads / 64;
+
+template <int B> struct Vec;
+template <> struct Vec<16> { typedef unsigned int type __attribute__((ext_vector_type(4))); };
+template <> struct Vec<8> { typedef unsigned int type __attribute__((ext_vector_type(2))); };
+template <> struct Vec<4> { typedef unsigned int type; };
+template <> struct Vec<2> { typedef unsigned short type; };
+template <> struct Vec<1> { typedef unsigned char type; };
+
+// Scalar kernel arguments (passed by value in the kernarg segment).  The
+// four pointers are separate __restrict__ kernel arguments so the compiler
+// can prove the tables are never written and read them through the scalar
+// cache.
+struct MoveParams {
+  int64_t page_bytes;         // planes * page_size * row_bytes
+  int64_t plane_bytes;        // page_size * row_bytes
+  int64_t packed_cap;         // bytes the packed buffer holds
+  int64_t num_pages;          // valid page indices are [0, num_pages)
+  int32_t row_bytes;          // heads * head_dim * elem_bytes
+  int32_t page_size;          // tokens per page of THIS pool
+  int32_t planes;
+  int32_t num_reqs;
+  int32_t bt_stride;
+  int32_t n_single;           // tokens of the single request when seq_lens is null
+  int32_t tiles_per_plane;    // ceil(plane_bytes / tile bytes)
+  int32_t batched;            // 1: lengths come from device seq_lens
+};
+
+__device__ __forceinline__ int32_t uniform(int32_t x) { return __builtin_amdgcn_readfirstlane(x); }
+
+// Exclusive prefix sums over requests of (clamped) token counts and of page
+// counts, written to LDS: tok[r], pg[r] for r < R, totals at index R.
+// Tokens ride in the high and pages in the low 32 bits of one 64-bit value,
+// so a single wave64 shuffle scan produces both.
+__device__ void request_prefix(const MoveParams& p, const int32_t* __restrict__ seq_lens, int32_t* tok,
+                               int32_t* pg, uint64_t* wsum) {
+  const int lane = threadIdx.x & 63;
+  const int wave = threadIdx.x >> 6;
+  const int64_t max_tok = (int64_t)p.bt_stride * p.page_size;
+  uint64_t carry = 0;
+  for (int base = 0; base < p.num_reqs; base += kThreads) {
+    const int r = base + threadIdx.x;
+    uint64_t v = 0;
+    if (r < p.num_reqs) {
+      int64_t n = seq_lens[r];
+      n = n < 0 ? 0 : (n > max_tok ? max_tok : n);
+      const uint64_t pages = (uint64_t)((n + p.page_size - 1) / p.page_size);
+      v = ((uint64_t)n << 32) | pages;
+    }
+    uint64_t x = v;
+#pragma unroll
+    for (int d = 1; d < 64; d <<= 1) {
+      const uint64_t y = __shfl_up(x, d, 64);
+      if (lane >= d) x += y;
+    }
+    if (lane == 63) wsum[wave] = x;
+    __syncthreads();
+    uint64_t before = carry, chunk = 0;
+#pragma unroll
+    for (int w = 0; w < kWaves; ++w) {
+      if (w < wave) before += wsum[w];
+      chunk += wsum[w];
+    }
+    if (r < p.num_reqs) {
+      const uint64_t excl = before + x - v;
+      tok[r] = (int32_t)(excl >> 32);
+      pg[r] = (int32_t)(excl & 0xffffffffu);
+    }
+    carry += chunk;
+    __syncthreads();
+  }
+  if (threadIdx.x == 0) {
+    tok[p.num_reqs] = (int32_t)(carry >> 32);
+    pg[p.num_reqs] = (int32_t)(carry & 0xffffffffu);
+  }
+  __syncthreads();
+}
+
+template <int VB, int VPT>
+__device__ __forceinline__ void copy_tile(char* __restrict__ dst, const char* __restrict__ src,
+                                          int32_t len) {
+  typedef typename Vec<VB>::type V;
+  const V* __restrict__ s = reinterpret_cast<const V*>(src);
+  V* __restrict__ d = reinterpret_cast<V*>(dst);
+  const int32_t nv = len / VB;
+  V v[VPT];
+  if (nv == kThreads * VPT) {
+#pragma unroll
+    for (int j = 0; j < VPT; ++j) {
+#if TOPKV_NONTEMPORAL
+      v[j] = __builtin_nontemporal_load(s + j * kThreads + threadIdx.x);
+#else
+      v[j] = s[j * kThreads + threadIdx.x];
+#endif
+    }
+#pragma unroll
+    for (int j = 0; j < VPT; ++j) {
+#if TOPKV_NONTEMPORAL
+      __builtin_nontemporal_store(v[j], d + j * kThreads + threadIdx.x);
+#else
+      d[j * kThreads + threadIdx.x] = v[j];
+#endif
+    }
+  } else {
+    // Ragged tile (1 <= nv < kThreads * VPT): every lane still issues all VPT
+    // loads back to back (indices clamped into the tile, so they stay in
+    // bounds) and only the stores are predicated.
+#pragma unroll
+    for (int j = 0; j < VPT; ++j) {
+      const int idx = j * kThreads + threadIdx.x;
+      v[j] = s[idx < nv ? idx : nv - 1];
+    }
+#pragma unroll
+    for (int j = 0; j < VPT; ++j) {
+      const int idx = j * kThreads + threadIdx.x;
+      if (idx < nv) d[idx] = v[j];
+    }
+  }
+}
+
+// pool: pool base already offset to the layer; packed: packed buffer base;
+// tables: [num_reqs][bt_stride]; seq_lens: device [num_reqs] (batched only).
+template <int VB, bool kPack>
+__device__ __forceinline__ void move_layer(char* __restrict__ pool, char* __restrict__ packed,
+                                           const int32_t* __restrict__ tables,
+                                           const int32_t* __restrict__ seq_lens, const MoveParams& p) {
+  constexpr int VPT = TOPKV_VPT;
+  constexpr int64_t kTile = (int64_t)kThreads * VPT * VB;
+  extern __shared__ uint64_t lds_u64[];
+  uint64_t* wsum = lds_u64;                                      // [kWaves]
+  int32_t* tok = reinterpret_cast<int32_t*>(lds_u64 + kWaves);   // [num_reqs + 1]
+  int32_t* pg = tok + (p.num_reqs + 1);                          // [num_reqs + 1]
+
+  const bool batched = p.batched != 0;
+  int32_t total_pages;
+  if (batched) {
+    request_prefix(p, seq_lens, tok, pg, wsum);
+    total_pages = pg[p.num_reqs];
+  } else {
+    total_pages = (p.n_single + p.page_size - 1) / p.page_size;
+  }
+  // the host guarantees pages * planes * tiles_per_plane < 2^31
+  const uint32_t per_page = (uint32_t)(p.planes * p.tiles_per_plane);
+  const uint32_t work = (uint32_t)total_pages * per_page;
+
+  for (uint32_t w = blockIdx.x; w < work; w += gridDim.x) {
+    const int32_t g = uniform((int32_t)(w / per_page));
+    const int32_t rem = (int32_t)(w - (uint32_t)g * per_page);
+    const int32_t c = uniform(rem / p.tiles_per_plane);
+    const int32_t k = uniform(rem - c * p.tiles_per_plane);
+    int32_t r = 0, tok0 = 0, n = p.n_single, i = g;
+    if (batched) {
+      int lo = 0, hi = p.num_reqs - 1;   // largest r with pg[r] <= g
+      while (lo < hi) {
+        const int mid = (lo + hi + 1) >> 1;
+        if (pg[mid] <= g) lo = mid; else hi = mid - 1;
+      }
+      r = uniform(lo);
+      tok0 = uniform(tok[r]);
+      n = uniform(tok[r + 1] - tok0);
+      i = uniform(g - pg[r]);
+    }
+    const int32_t first = i * p.page_size;
+    const int32_t rows = min(p.page_size, n - first);
+    const int64_t run = (int64_t)rows * p.row_bytes;
+    const int64_t start = (int64_t)k * kTile;
+    if (start >= run) continue;
+    const int64_t req_end = ((int64_t)tok0 + n) * p.planes * p.row_bytes;
+    if (req_end > p.packed_cap) continue;
+    const int32_t page = tables[(int64_t)r * p.bt_stride + i];
+    if (page < 0 || (int64_t)page >= p.num_pages) continue;
+    const int32_t len = (int32_t)(run - start < kTile ? run - start : kTile);
+    char* pool_ptr = pool + (int64_t)page * p.page_bytes + (int64_t)c * p.plane_bytes + start;
+    char* packed_ptr = packed +
+        (((int64_t)tok0 * p.planes + (int64_t)c * n + first) * p.row_bytes + start);
+    if (kPack) copy_tile<VB, VPT>(packed_ptr, pool_ptr, len);
+    else copy_tile<VB, VPT>(pool_ptr, packed_ptr, len);
+  }
+}
+
+template <int VB>
+__global__ __launch_bounds__(kThreads) void kv_pack_kernel(char* __restrict__ pool, char* __restrict__ packed,
+                                                           const int32_t* __restrict__ tables,
+                                                           const int32_t* __restrict__ seq_lens, MoveParams p) {
+  move_layer<VB, true>(pool, packed, tables, seq_lens, p);
+}
+
+template <int VB>
+__global__ __launch_bounds__(kThreads) void kv_unpack_kernel(char* __restrict__ pool, char* __restrict__ packed,
+                                                             const int32_t* __restrict__ tables,
+                                                             const int32_t* __restrict__ seq_lens, MoveParams p) {
+  move_layer<VB, false>(pool, packed, tables, seq_lens, p);
+}
+
+// ---------------------------------------------------------------------------
+// Host side
+// ---------------------------------------------------------------------------
+
+constexpr int kMaxDevices = 64;
+std::atomic<int> g_cu_count[kMaxDevices];
+
+topkv_status_t cu_count(int* out) {
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0) return TOPKV_ERR_DEVICE;
+  if (dev < kMaxDevices) {
+    const int cached = g_cu_count[dev].load(std::memory_order_relaxed);
+    if (cached > 0) { *out = cached; return TOPKV_OK; }
+  }
+  int cus = 0;
+  if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || cus <= 0)
+    return TOPKV_ERR_DEVICE;
+  if (dev < kMaxDevices) g_cu_count[dev].store(cus, std::memory_order_relaxed);
+  *out = cus;
+  return TOPKV_OK;
+}
+
+struct Geometry {
+  int64_t row_bytes, plane_bytes, page_bytes, layer_bytes;
+};
+
+topkv_status_t pool_geometry(const topkv_pool_t* pool, int32_t layer, Geometry* g) {
+  if (!pool || !pool->base) return TOPKV_ERR_INVALID_ARG;
+  if (pool->num_pages <= 0 || pool->num_layers <= 0 || pool->page_size <= 0 || pool->planes <= 0 ||
+      pool->num_heads <= 0 || pool->head_dim <= 0)
+    return TOPKV_ERR_INVALID_ARG;
+  if (pool->elem_bytes != 1 && pool->elem_bytes != 2 && pool->elem_bytes != 4 && pool->elem_bytes != 8)
+    return TOPKV_ERR_INVALID_ARG;
+  if (layer < 0 || layer >= pool->num_layers) return TOPKV_ERR_INVALID_ARG;
+  int64_t row, plane, page, lay, all;
+  if (__builtin_mul_overflow((int64_t)pool->num_heads, (int64_t)pool->head_dim, &row) ||
+      __builtin_mul_overflow(row, (int64_t)pool->elem_bytes, &row) ||
+      __builtin_mul_overflow(row, (int64_t)pool->page_size, &plane) ||
+      __builtin_mul_overflow(plane, (int64_t)pool->planes, &page) ||
+      __builtin_mul_overflow(page, pool->num_pages, &lay) ||
+      __builtin_mul_overflow(lay, (int64_t)pool->num_layers, &all))
+    return TOPKV_ERR_UNSUPPORTED;
+  if (row > INT32_MAX || pool->num_pages > INT32_MAX) return TOPKV_ERR_UNSUPPORTED;
+  g->row_bytes = row;
+  g->plane_bytes = plane;
+  g->page_bytes = page;
+  g->layer_bytes = lay;
+  return TOPKV_OK;
+}
+
+int vector_bytes(uintptr_t a, uintptr_t b, int64_t row) {
+  for (int vb = 16; vb > 1; vb >>= 1)
+    if (a % vb == 0 && b % vb == 0 && row % vb == 0) return vb;
+  return 1;
+}
+
+typedef void (*KernelFn)(char*, char*, const int32_t*, const int32_t*, MoveParams);
+
+KernelFn pick_kernel(bool pack, int vb) {
+  switch (vb) {
+    case 16: return pack ? kv_pack_kernel<16> : kv_unpack_kernel<16>;
+    case 8: return pack ? kv_pack_kernel<8> : kv_unpack_kernel<8>;
+    case 4: return pack ? kv_pack_kernel<4> : kv_unpack_kernel<4>;
+    case 2: return pack ? kv_pack_kernel<2> : kv_unpack_kernel<2>;
+    default: return pack ? kv_pack_kernel<1> : kv_unpack_kernel<1>;
+  }
+}
+
+// Shared launcher for the four movement entry points.
+//   pack:     direction (pool -> packed when true)
+//   seq_lens: device lengths (batched) or null (single request of n_single)
+topkv_status_t launch_move(bool pack, const topkv_pool_t* pool, int32_t layer, void* packed,
+                           int64_t packed_cap, int32_t num_reqs, const int32_t* tables,
+                           int32_t bt_stride, const int32_t* seq_lens, int32_t n_single,
+                           const topkv_launch_t* launch) {
+  Geometry g;
+  topkv_status_t st = pool_geometry(pool, layer, &g);
+  if (st != TOPKV_OK) return st;
+  if (!launch) return TOPKV_ERR_INVALID_ARG;
+  if (num_reqs < 0 || n_single < 0 || packed_cap < 0) return TOPKV_ERR_INVALID_ARG;
+  if (num_reqs > TOPKV_MAX_BATCH_REQS) return TOPKV_ERR_UNSUPPORTED;
+  if (num_reqs == 0 || (!seq_lens && n_single == 0)) return TOPKV_OK;  // nothing to move
+  if (!tables || !packed || bt_stride <= 0) return TOPKV_ERR_INVALID_ARG;
+
+  const int vb = vector_bytes(reinterpret_cast<uintptr_t>(pool->base),
+                              reinterpret_cast<uintptr_t>(packed), g.row_bytes);
+  const int64_t tile = (int64_t)kThreads * TOPKV_VPT * vb;
+  const int64_t tpp = (g.plane_bytes + tile - 1) / tile;
+  int64_t per_page, max_pages, work;
+  if (seq_lens) {
+    max_pages = (int64_t)num_reqs * bt_stride;
+  } else {
+    max_pages = ((int64_t)n_single + pool->page_size - 1) / pool->page_size;
+    if (max_pages > bt_stride) return TOPKV_ERR_INVALID_ARG;
+  }
+  if (__builtin_mul_overflow(tpp, (int64_t)pool->planes, &per_page) || per_page > INT32_MAX ||
+      __builtin_mul_overflow(max_pages, per_page, &work) || work > INT32_MAX ||
+      (int64_t)bt_stride * pool->page_size > INT32_MAX)
+    return TOPKV_ERR_UNSUPPORTED;
+
+  int cus = 0;
+  st = cu_count(&cus);
+  if (st != TOPKV_OK) return st;
+  const int64_t cap = (int64_t)cus * TOPKV_WG_PER_CU;
+  const unsigned grid = (unsigned)(work < cap ? work : cap);
+  if (grid == 0) return TOPKV_OK;
+
+  char* pool_ptr = static_cast<char*>(pool->base) + (int64_t)layer * g.layer_bytes;
+  char* packed_ptr = static_cast<char*>(packed);
+  MoveParams p;
+  p.page_bytes = g.page_bytes;
+  p.plane_bytes = g.plane_bytes;
+  p.packed_cap = packed_cap;
+  p.num_pages = pool->num_pages;
+  p.row_bytes = (int32_t)g.row_bytes;
+  p.page_size = pool->page_size;
+  p.planes = pool->planes;
+  p.num_reqs = seq_lens ? num_reqs : 1;
+  p.bt_stride = bt_stride;
+  p.n_single = n_single;
+  p.tiles_per_plane = (int32_t)tpp;
+  p.batched = seq_lens ? 1 : 0;
+
+  const size_t lds = seq_lens ? sizeof(uint64_t) * kWaves + sizeof(int32_t) * 2 * ((size_t)num_reqs + 1) : 0;
+  void* args[] = {&pool_ptr, &packed_ptr, &tables, &seq_lens, &p};
+  const void* fn = reinterpret_cast<const void*>(pick_kernel(pack, vb));
+  hipError_t e;
+  if (launch->start || launch->stop)
+    e = hipExtLaunchKernel(fn, dim3(grid), dim3(kThreads), args, lds, launch->stream, launch->start,
+                           launch->stop, 0);
+  else
+    e = hipLaunchKernel(fn, dim3(grid), dim3(kThreads), args, lds, launch->stream);
+  return e == hipSuccess ? TOPKV_OK : TOPKV_ERR_LAUNCH;
+}
+
+int64_t single_bytes(const topkv_pool_t* pool, int32_t n) {
+  int64_t b;
+  if (__builtin_mul_overflow((int64_t)pool->num_heads * pool->head_dim * pool->elem_bytes,
+                             (int64_t)pool->planes * n, &b))
+    return -1;
+  return b;
+}
+
+}  // namespace topkv
+
+// ---------------------------------------------------------------------------
+// C ABI
+// ---------------------------------------------------------------------------
+extern "C" {
+
+topkv_status_t topkv_pack_layer(const topkv_pool_t* src, int32_t layer, const int32_t* block_table,
+                                int32_t seq_len, void* dst, hipStream_t stream) {
+  if (!src || seq_len < 0) return TOPKV_ERR_INVALID_ARG;
+  const topkv_launch_t l = {stream, nullptr, nullptr};
+  const int64_t pages = src->page_size > 0 ? ((int64_t)seq_len + src->page_size - 1) / src->page_size : 0;
+  const int64_t cap = topkv::single_bytes(src, seq_len);
+  if (cap < 0 || pages > INT32_MAX) return TOPKV_ERR_UNSUPPORTED;
+  return topkv::launch_move(true, src, layer, dst, cap, 1, block_table, (int32_t)(pages > 0 ? pages : 1),
+                            nullptr, seq_len, &l);
+}
+
+topkv_status_t topkv_unpack_layer(const void* src, const topkv_pool_t* dst, int32_t layer,
+                                  const int32_t* block_table, int32_t seq_len, hipStream_t stream) {
+  if (!dst || seq_len < 0) return TOPKV_ERR_INVALID_ARG;
+  const topkv_launch_t l = {stream, nullptr, nullptr};
+  const int64_t pages = dst->page_size > 0 ? ((int64_t)seq_len + dst->page_size - 1) / dst->page_size : 0;
+  const int64_t cap = topkv::single_bytes(dst, seq_len);
+  if (cap < 0 || pages > INT32_MAX) return TOPKV_ERR_UNSUPPORTED;
+  return topkv::launch_move(false, dst, layer, const_cast<void*>(src), cap, 1, block_table,
+                            (int32_t)(pages > 0 ? pages : 1), nullptr, seq_len, &l);
+}
+
+topkv_status_t topkv_pack_layer_batched_ex(const topkv_pool_t* src, int32_t layer, int32_t num_reqs,
+                                           const int32_t* block_tables, int32_t bt_stride,
+                                           const int32_t* seq_lens, void* dst, int64_t dst_bytes,
+                                           const topkv_launch_t* launch) {
+  if (num_reqs > 0 && !seq_lens) return TOPKV_ERR_INVALID_ARG;
+  return topkv::launch_move(true, src, layer, dst, dst_bytes, num_reqs, block_tables, bt_stride,
+                            num_reqs > 0 ? seq_lens : nullptr, 0, launch);
+}
+
+topkv_status_t topkv_unpack_layer_batched_ex(const void* src, int64_t src_bytes, const topkv_pool_t* dst,
+                                             int32_t layer, int32_t num_reqs,
+                                             const int32_t* block_tables, int32_t bt_stride,
+                                             const int32_t* seq_lens, const topkv_launch_t* launch) {
+  if (num_reqs > 0 && !seq_lens) return TOPKV_ERR_INVALID_ARG;
+  return topkv::launch_move(false, dst, layer, const_cast<void*>(src), src_bytes, num_reqs, block_tables,
+                            bt_stride, num_reqs > 0 ? seq_lens : nullptr, 0, launch);
+}
+
+topkv_status_t topkv_pack_layer_batched(const topkv_pool_t* src, int32_t layer, int32_t num_reqs,
+                                        const int32_t* block_tables, int32_t bt_stride,
+                                        const int32_t* seq_lens, void* dst, int64_t dst_bytes,
+                                        hipStream_t stream) {
+  const topkv_launch_t l = {stream, nullptr, nullptr};
+  return topkv_pack_layer_batched_ex(src, layer, num_reqs, block_tables, bt_stride, seq_lens, dst,
+                                     dst_bytes, &l);
+}
+
+topkv_status_t topkv_unpack_layer_batched(const void* src, int64_t src_bytes, const topkv_pool_t* dst,
+                                          int32_t layer, int32_t num_reqs, const int32_t* block_tables,
+                                          int32_t bt_stride, const int32_t* seq_lens,
+                                          hipStream_t stream) {
+  const topkv_launch_t l = {stream, nullptr, nullptr};
+  return topkv_unpack_layer_batched_ex(src, src_bytes, dst, layer, num_reqs, block_tables, bt_stride,
+                                       seq_lens, &l);
+}
+
+int64_t topkv_packed_layer_bytes(const topkv_pool_t* pool, const int32_t* seq_lens_host,
+                                 int32_t num_reqs) {
+  if (!pool || num_reqs < 0 || (num_reqs > 0 && !seq_lens_host)) return -1;
+  if (pool->planes <= 0 || pool->num_heads <= 0 || pool->head_dim <= 0 || pool->elem_bytes <= 0) return -1;
+  int64_t per_token;
+  if (__builtin_mul_overflow((int64_t)pool->planes * pool->num_heads, (int64_t)pool->head_dim * pool->elem_bytes,
+                             &per_token))
+    return -1;
+  int64_t total = 0;
+  for (int32_t r = 0; r < num_reqs; ++r) {
+    if (seq_lens_host[r] < 0) return -1;
+    int64_t b;
+    if (__builtin_mul_overflow(per_token, (int64_t)seq_lens_host[r], &b) ||
+        __builtin_add_overflow(total, b, &total))
+      return -1;
+  }
+  return total;
+}
+
+const char* topkv_status_string(topkv_status_t status) {
+  switch (status) {
+    case TOPKV_OK: return "TOPKV_OK";
+    case TOPKV_ERR_INVALID_ARG: return "TOPKV_ERR_INVALID_ARG: null pointer, bad layer or non-positive size";
+    case TOPKV_ERR_UNSUPPORTED: return "TOPKV_ERR_UNSUPPORTED: size beyond the library's limits";
+    case TOPKV_ERR_LAUNCH: return "TOPKV_ERR_LAUNCH: the HIP runtime refused the kernel launch";
+    case TOPKV_ERR_BOUNDS: return "TOPKV_ERR_BOUNDS: block table or length out of range";
+    case TOPKV_ERR_DEVICE: return "TOPKV_ERR_DEVICE: HIP device query failed";
+  }
+  return "TOPKV_ERR_UNKNOWN";
+}
+
+}  // extern "C"

@@ -1,0 +1,276 @@
+"""ctypes binding of libtopkv.so (declared in include/topkv.h).
+
+Argument marshalling only: every function here forwards to the C entry point
+of the same name, passing raw device pointers taken from torch tensors (or
+plain integers) and the caller's HIP stream, and raises :class:`TopkvError`
+on a non-zero status.  Every byte is moved by the library's HIP kernels.
+
+Importing this module loads the library and fails loudly (ImportError) when
+it has not been built; there is no fallback path.  torch is imported first so
+the library binds to the HIP runtime torch already loaded (one runtime per
+process).
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+import sys
+
+import torch  # noqa: F401  (must load torch's HIP runtime before libtopkv.so)
+
+LIBRARY = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libtopkv.so")
+
+if not os.path.exists(LIBRARY):
+    raise ImportError(f"{LIBRARY} is missing: build it with `python -m paper_2607_28633_amd.build` "
+                      "(or __graft_entry__.build()); there is no non-HIP fallback")
+_lib = ctypes.CDLL(LIBRARY)
+
+TOPKV_OK = 0
+TOPKV_ERR_INVALID_ARG = 1
+TOPKV_ERR_UNSUPPORTED = 2
+TOPKV_ERR_LAUNCH = 3
+TOPKV_ERR_BOUNDS = 4
+TOPKV_ERR_DEVICE = 5
+TOPKV_MAX_BATCH_REQS = 8000
+
+EXPORTS = ["topkv_pack_layer", "topkv_unpack_layer", "topkv_pack_layer_batched",
+           "topkv_unpack_layer_batched", "topkv_pack_layer_batched_ex",
+           "topkv_unpack_layer_batched_ex", "topkv_packed_layer_bytes", "topkv_status_string"]
+
+
+class topkv_pool_t(ctypes.Structure):
+    _fields_ = [("base", ctypes.c_void_p), ("num_pages", ctypes.c_int64),
+                ("num_layers", ctypes.c_int32), ("page_size", ctypes.c_int32),
+                ("planes", ctypes.c_int32), ("num_heads", ctypes.c_int32),
+                ("head_dim", ctypes.c_int32), ("elem_bytes", ctypes.c_int32)]
+
+
+class topkv_launch_t(ctypes.Structure):
+    _fields_ = [("stream", ctypes.c_void_p), ("start", ctypes.c_void_p), ("stop", ctypes.c_void_p)]
+
+
+_P = ctypes.c_void_p
+_I32 = ctypes.c_int32
+_I64 = ctypes.c_int64
+_POOL = ctypes.POINTER(topkv_pool_t)
+_SIGS = {
+    "topkv_pack_layer": (_I32, [_POOL, _I32, _P, _I32, _P, _P]),
+    "topkv_unpack_layer": (_I32, [_P, _POOL, _I32, _P, _I32, _P]),
+    "topkv_pack_layer_batched": (_I32, [_POOL, _I32, _I32, _P, _I32, _P, _P, _I64, _P]),
+    "topkv_unpack_layer_batched": (_I32, [_P, _I64, _POOL, _I32, _I32, _P, _I32, _P, _P]),
+    "topkv_pack_layer_batched_ex": (_I32, [_POOL, _I32, _I32, _P, _I32, _P, _P, _I64,
+                                           ctypes.POINTER(topkv_launch_t)]),
+    "topkv_unpack_layer_batched_ex": (_I32, [_P, _I64, _POOL, _I32, _I32, _P, _I32, _P,
+                                             ctypes.POINTER(topkv_launch_t)]),
+    "topkv_packed_layer_bytes": (_I64, [_POOL, ctypes.POINTER(_I32), _I32]),
+    "topkv_status_string": (ctypes.c_char_p, [_I32]),
+}
+for _name, (_res, _args) in _SIGS.items():
+    _fn = getattr(_lib, _name)
+    _fn.restype = _res
+    _fn.argtypes = _args
+
+
+class TopkvError(RuntimeError):
+    def __init__(self, status: int):
+        self.status = int(status)
+        super().__init__(topkv_status_string(status))
+
+
+def _check(status: int) -> None:
+    if status != TOPKV_OK:
+        raise TopkvError(status)
+
+
+def _ptr(x) -> int:
+    """Device address of a tensor (or an integer address / None)."""
+    if x is None:
+        return 0
+    if isinstance(x, int):
+        return x
+    if isinstance(x, torch.Tensor):
+        if x.numel() and not x.is_cuda:
+            raise ValueError("tensor arguments must live in device memory")
+        if x.numel() and not x.is_contiguous():
+            raise ValueError("tensor arguments must be contiguous")
+        return x.data_ptr()
+    raise TypeError(f"expected a tensor or an address, got {type(x).__name__}")
+
+
+def _table_ptr(t) -> int:
+    if isinstance(t, torch.Tensor) and t.numel() and t.dtype != torch.int32:
+        raise ValueError("block tables and seq_lens must be int32")
+    return _ptr(t)
+
+
+def _stream(stream) -> int:
+    if stream is None:
+        return torch.cuda.current_stream().cuda_stream
+    if isinstance(stream, int):
+        return stream
+    return stream.cuda_stream
+
+
+def _nbytes(t, given) -> int:
+    if given is not None:
+        return int(given)
+    if isinstance(t, torch.Tensor):
+        return t.numel() * t.element_size()
+    raise ValueError("byte capacity is required when passing a raw address")
+
+
+def make_pool(base, *, num_pages, num_layers, page_size, planes, num_heads, head_dim,
+              elem_bytes=2) -> topkv_pool_t:
+    """Pool descriptor for device memory laid out
+    [num_layers][num_pages][planes][page_size][num_heads][head_dim]."""
+    return topkv_pool_t(_ptr(base), int(num_pages), int(num_layers), int(page_size), int(planes),
+                        int(num_heads), int(head_dim), int(elem_bytes))
+
+
+def pool_from_tensor(t: torch.Tensor) -> topkv_pool_t:
+    """Descriptor of a 6-D pool tensor [layers][pages][planes][page_size][heads][dim]."""
+    if t.dim() != 6:
+        raise ValueError("pool tensor must be [layers][pages][planes][page_size][heads][dim]")
+    L, NP, C, P, H, D = t.shape
+    return make_pool(t, num_pages=NP, num_layers=L, page_size=P, planes=C, num_heads=H,
+                     head_dim=D, elem_bytes=t.element_size())
+
+
+def _pool_arg(pool) -> topkv_pool_t:
+    return pool if isinstance(pool, topkv_pool_t) else pool_from_tensor(pool)
+
+
+def topkv_pack_layer(src, layer, block_table, seq_len, dst, stream=None) -> None:
+    _check(_lib.topkv_pack_layer(ctypes.byref(_pool_arg(src)), int(layer), _table_ptr(block_table),
+                                 int(seq_len), _ptr(dst), _stream(stream)))
+
+
+def topkv_unpack_layer(src, dst, layer, block_table, seq_len, stream=None) -> None:
+    _check(_lib.topkv_unpack_layer(_ptr(src), ctypes.byref(_pool_arg(dst)), int(layer),
+                                   _table_ptr(block_table), int(seq_len), _stream(stream)))
+
+
+def topkv_pack_layer_batched(src, layer, num_reqs, block_tables, bt_stride, seq_lens, dst,
+                             dst_bytes=None, stream=None) -> None:
+    _check(_lib.topkv_pack_layer_batched(ctypes.byref(_pool_arg(src)), int(layer), int(num_reqs),
+                                         _table_ptr(block_tables), int(bt_stride), _table_ptr(seq_lens),
+                                         _ptr(dst), _nbytes(dst, dst_bytes), _stream(stream)))
+
+
+def topkv_unpack_layer_batched(src, dst, layer, num_reqs, block_tables, bt_stride, seq_lens,
+                               src_bytes=None, stream=None) -> None:
+    _check(_lib.topkv_unpack_layer_batched(_ptr(src), _nbytes(src, src_bytes), ctypes.byref(_pool_arg(dst)),
+                                           int(layer), int(num_reqs), _table_ptr(block_tables),
+                                           int(bt_stride), _table_ptr(seq_lens), _stream(stream)))
+
+
+def topkv_pack_layer_batched_ex(src, layer, num_reqs, block_tables, bt_stride, seq_lens, dst,
+                                dst_bytes=None, stream=None, start=None, stop=None) -> None:
+    """As topkv_pack_layer_batched; start/stop are raw hipEvent_t handles
+    (see HipEvent) stamped with the kernel's own begin/end time."""
+    launch = topkv_launch_t(_stream(stream), _event(start), _event(stop))
+    _check(_lib.topkv_pack_layer_batched_ex(ctypes.byref(_pool_arg(src)), int(layer), int(num_reqs),
+                                            _table_ptr(block_tables), int(bt_stride), _table_ptr(seq_lens),
+                                            _ptr(dst), _nbytes(dst, dst_bytes), ctypes.byref(launch)))
+
+
+def topkv_unpack_layer_batched_ex(src, dst, layer, num_reqs, block_tables, bt_stride, seq_lens,
+                                  src_bytes=None, stream=None, start=None, stop=None) -> None:
+    launch = topkv_launch_t(_stream(stream), _event(start), _event(stop))
+    _check(_lib.topkv_unpack_layer_batched_ex(_ptr(src), _nbytes(src, src_bytes), ctypes.byref(_pool_arg(dst)),
+                                              int(layer), int(num_reqs), _table_ptr(block_tables),
+                                              int(bt_stride), _table_ptr(seq_lens), ctypes.byref(launch)))
+
+
+def topkv_packed_layer_bytes(pool, seq_lens_host) -> int:
+    lens = [int(x) for x in seq_lens_host]
+    arr = (_I32 * max(1, len(lens)))(*lens)
+    return int(_lib.topkv_packed_layer_bytes(ctypes.byref(_pool_arg(pool)), arr, len(lens)))
+
+
+def topkv_status_string(status: int) -> str:
+    return _lib.topkv_status_string(int(status)).decode()
+
+
+# --- kernel-timestamp events for the *_ex calls ------------------------------
+# Raw hipEvent_t handles from the HIP runtime that torch loaded (the same
+# process-wide runtime libtopkv.so is bound to).
+_hip = ctypes.CDLL("libamdhip64.so.7")
+_hip.hipEventCreate.argtypes = [ctypes.POINTER(ctypes.c_void_p)]
+_hip.hipEventDestroy.argtypes = [ctypes.c_void_p]
+_hip.hipEventSynchronize.argtypes = [ctypes.c_void_p]
+_hip.hipEventElapsedTime.argtypes = [ctypes.POINTER(ctypes.c_float), ctypes.c_void_p, ctypes.c_void_p]
+_hip.hipEventRecord.argtypes = [ctypes.c_void_p, ctypes.c_void_p]
+
+
+class HipEvent:
+    """A hipEvent_t (timing enabled) usable as start/stop of the *_ex calls."""
+
+    def __init__(self):
+        h = ctypes.c_void_p()
+        if _hip.hipEventCreate(ctypes.byref(h)) != 0:
+            raise RuntimeError("hipEventCreate failed")
+        self.handle = h.value
+
+    def record(self, stream=None):
+        if _hip.hipEventRecord(self.handle, _stream(stream)) != 0:
+            raise RuntimeError("hipEventRecord failed")
+
+    def synchronize(self):
+        if _hip.hipEventSynchronize(self.handle) != 0:
+            raise RuntimeError("hipEventSynchronize failed")
+
+    def elapsed_ms(self, end: "HipEvent") -> float:
+        ms = ctypes.c_float()
+        rc = _hip.hipEventElapsedTime(ctypes.byref(ms), self.handle, end.handle)
+        if rc != 0:
+            raise RuntimeError(f"hipEventElapsedTime failed ({rc})")
+        return float(ms.value)
+
+    def __del__(self):
+        h, self.handle = getattr(self, "handle", None), None
+        if h and not sys.is_finalizing():
+            _hip.hipEventDestroy(h)
+
+
+def _event(e) -> int:
+    if e is None:
+        return 0
+    return e.handle if isinstance(e, HipEvent) else int(e)
+
+
+# --- prepared calls -----------------------------------------------------------
+class PreparedCall:
+    """One C entry point with its arguments converted to ctypes once.
+    Calling it re-issues exactly that launch; per-layer sweeps use these so
+    the host enqueue rate, not ctypes conversion, bounds the launch rate."""
+
+    def __init__(self, name, args, keep):
+        self._fn = getattr(_lib, name)
+        self._args = args
+        self._keep = keep          # structs the arguments point to
+
+    def __call__(self) -> None:
+        st = self._fn(*self._args)
+        if st:
+            raise TopkvError(st)
+
+
+def prepare_pack_layer_batched_ex(src, layer, num_reqs, block_tables, bt_stride, seq_lens, dst,
+                                  dst_bytes=None, stream=None, start=None, stop=None) -> PreparedCall:
+    pool = _pool_arg(src)
+    launch = topkv_launch_t(_stream(stream), _event(start), _event(stop))
+    args = (ctypes.byref(pool), _I32(int(layer)), _I32(int(num_reqs)), _P(_table_ptr(block_tables)),
+            _I32(int(bt_stride)), _P(_table_ptr(seq_lens)), _P(_ptr(dst)), _I64(_nbytes(dst, dst_bytes)),
+            ctypes.byref(launch))
+    return PreparedCall("topkv_pack_layer_batched_ex", args, (pool, launch))
+
+
+def prepare_unpack_layer_batched_ex(src, dst, layer, num_reqs, block_tables, bt_stride, seq_lens,
+                                    src_bytes=None, stream=None, start=None, stop=None) -> PreparedCall:
+    pool = _pool_arg(dst)
+    launch = topkv_launch_t(_stream(stream), _event(start), _event(stop))
+    args = (_P(_ptr(src)), _I64(_nbytes(src, src_bytes)), ctypes.byref(pool), _I32(int(layer)),
+            _I32(int(num_reqs)), _P(_table_ptr(block_tables)), _I32(int(bt_stride)),
+            _P(_table_ptr(seq_lens)), ctypes.byref(launch))
+    return PreparedCall("topkv_unpack_layer_batched_ex", args, (pool, launch))

@@ -235,22 +235,28 @@ def random_words(rng, shape, elem_bytes: int) -> np.ndarray:
 
 def device_src_pool(wl: Workload, device="cuda"):
     """Source pool generated on the device (multi-GB pools): bf16 ~ N(0, 1) from
-    a seeded torch generator.  Returned as a torch tensor of the pool shape."""
+    a seeded torch generator, filled one layer slab at a time.  Returned as a
+    torch tensor of the pool shape."""
     import torch
     if wl.elem_bytes != 2:
         raise ValueError("device generation is for bf16 pools")
     g = torch.Generator(device=device)
     g.manual_seed(wl.seed * 1000003 + 1)
-    return torch.randn(wl.pool_shape(), generator=g, device=device, dtype=torch.bfloat16)
+    t = torch.empty(wl.pool_shape(), device=device, dtype=torch.bfloat16)
+    for layer in range(t.shape[0]):
+        t[layer].normal_(generator=g)
+    return t
 
 
 def device_dst_prefill(wl: Workload, device="cuda"):
-    """Destination pool pre-fill on the device: arbitrary seeded int16 words."""
+    """Destination pool pre-fill on the device: arbitrary seeded 16-bit words
+    (every bit pattern), one layer slab at a time."""
     import torch
     if wl.elem_bytes != 2:
         raise ValueError("device generation is for bf16 pools")
     g = torch.Generator(device=device)
     g.manual_seed(wl.seed * 1000003 + 2)
-    t = torch.randint(-32768, 32768, wl.pool_shape(dst=True), generator=g, device=device,
-                      dtype=torch.int32)
-    return t.to(torch.int16).view(torch.bfloat16)
+    t = torch.empty(wl.pool_shape(dst=True), device=device, dtype=torch.int16)
+    for layer in range(t.shape[0]):
+        t[layer].random_(-32768, 32768, generator=g)
+    return t.view(torch.bfloat16)

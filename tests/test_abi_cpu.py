@@ -1,0 +1,108 @@
+"""The C-ABI library on the CPU: it loads, exports every entry point declared in
+include/topkv.h, and its host-side logic (sizes, status strings, argument
+validation) behaves as documented.  No call here gets past validation, so
+nothing is launched and no GPU is needed."""
+import ctypes
+import os
+import re
+
+import numpy as np
+import pytest
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "topkv.h")
+
+
+@pytest.fixture(scope="module")
+def tk():
+    from paper_2607_28633_amd.build import LIBRARY, build_library
+    if not os.path.exists(LIBRARY):
+        build_library()
+    from paper_2607_28633_amd import topkv
+    return topkv
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(topkv_[a-z_0-9]+)\s*\(", text)))
+
+
+def test_header_declares_the_binding_names(tk):
+    assert declared_functions() == sorted(tk.EXPORTS)
+
+
+def test_library_exports_every_declared_symbol(tk):
+    lib = ctypes.CDLL(tk.LIBRARY)
+    missing = [name for name in declared_functions() if not hasattr(lib, name)]
+    assert not missing, f"not exported: {missing}"
+
+
+def test_status_strings(tk):
+    for code in range(6):
+        s = tk.topkv_status_string(code)
+        assert s.startswith("TOPKV_")
+    assert tk.topkv_status_string(99) == "TOPKV_ERR_UNKNOWN"
+
+
+def _pool(tk, **kw):
+    g = dict(num_pages=64, num_layers=2, page_size=16, planes=2, num_heads=8, head_dim=128, elem_bytes=2)
+    g.update(kw)
+    return tk.make_pool(kw.pop("base", 0x10000), **{k: v for k, v in g.items() if k != "base"})
+
+
+def test_packed_layer_bytes_matches_eq1(tk):
+    from paper_2607_28633_amd.workloads import make_workload
+    for name in ("tiny", "llama3-8b", "llama3-70b-batch8", "deepseek-v3-mla", "reblock-70b"):
+        wl = make_workload(name)
+        pool = tk.make_pool(0x10000, num_pages=wl.num_pages, num_layers=wl.num_layers,
+                            page_size=wl.page_size, planes=wl.planes, num_heads=wl.num_heads,
+                            head_dim=wl.head_dim, elem_bytes=wl.elem_bytes)
+        s = int(wl.seq_lens.astype(np.int64).sum())
+        # Eq. 1 per layer: planes * h_kv * d_h * s * b_p (planes = 2, or 1 for MLA)
+        assert tk.topkv_packed_layer_bytes(pool, wl.seq_lens) == \
+            wl.planes * wl.num_heads * wl.head_dim * s * wl.elem_bytes
+    # the 70B / 4096-token figure of Table 1 over 80 layers
+    assert 80 * tk.topkv_packed_layer_bytes(_pool(tk), [4096]) == 1_342_177_280
+    assert tk.topkv_packed_layer_bytes(_pool(tk), []) == 0
+    assert tk.topkv_packed_layer_bytes(_pool(tk), [5, -1]) == -1
+    lib = ctypes.CDLL(tk.LIBRARY)
+    lib.topkv_packed_layer_bytes.restype = ctypes.c_int64
+    assert lib.topkv_packed_layer_bytes(None, None, 0) == -1
+
+
+def _expect(tk, code, fn, *args, **kw):
+    kw.setdefault("stream", 0)   # the null stream handle: no torch device query on a GPU-less host
+    with pytest.raises(tk.TopkvError) as ei:
+        fn(*args, **kw)
+    assert ei.value.status == code, tk.topkv_status_string(ei.value.status)
+
+
+def test_argument_validation_before_launch(tk):
+    INV, UNS = tk.TOPKV_ERR_INVALID_ARG, tk.TOPKV_ERR_UNSUPPORTED
+    bt, lens, buf = 0x20000, 0x30000, 0x40000
+    good = _pool(tk)
+    _expect(tk, INV, tk.topkv_pack_layer, _pool(tk, base=0), 0, bt, 16, buf)          # null base
+    _expect(tk, INV, tk.topkv_pack_layer, good, 2, bt, 16, buf)                       # layer >= L
+    _expect(tk, INV, tk.topkv_pack_layer, good, -1, bt, 16, buf)
+    _expect(tk, INV, tk.topkv_pack_layer, _pool(tk, elem_bytes=3), 0, bt, 16, buf)
+    _expect(tk, INV, tk.topkv_pack_layer, _pool(tk, head_dim=0), 0, bt, 16, buf)
+    _expect(tk, INV, tk.topkv_pack_layer, _pool(tk, page_size=-4), 0, bt, 16, buf)
+    _expect(tk, INV, tk.topkv_pack_layer, good, 0, bt, -1, buf)                       # negative length
+    _expect(tk, INV, tk.topkv_pack_layer, good, 0, 0, 16, buf)                        # null table
+    _expect(tk, INV, tk.topkv_unpack_layer, 0, good, 0, bt, 16)                       # null packed src
+    _expect(tk, INV, tk.topkv_pack_layer_batched, good, 0, -1, bt, 4, lens, buf, dst_bytes=1 << 20)
+    _expect(tk, INV, tk.topkv_pack_layer_batched, good, 0, 3, bt, 0, lens, buf, dst_bytes=1 << 20)
+    _expect(tk, INV, tk.topkv_pack_layer_batched, good, 0, 3, bt, 4, 0, buf, dst_bytes=1 << 20)
+    _expect(tk, INV, tk.topkv_unpack_layer_batched, buf, good, 0, 3, bt, 4, lens, src_bytes=-1)
+    _expect(tk, UNS, tk.topkv_pack_layer_batched, good, 0, tk.TOPKV_MAX_BATCH_REQS + 1, bt, 4, lens,
+            buf, dst_bytes=1 << 20)
+    _expect(tk, UNS, tk.topkv_pack_layer, _pool(tk, num_pages=1 << 40, num_layers=1 << 20), 0, bt, 16, buf)
+
+
+def test_empty_work_is_a_no_op(tk):
+    good = _pool(tk)
+    tk.topkv_pack_layer(good, 0, 0, 0, 0, stream=0)            # zero tokens: nothing to launch
+    tk.topkv_unpack_layer(0, good, 1, 0, 0, stream=0)
+    tk.topkv_pack_layer_batched(good, 0, 0, 0, 1, 0, 0, dst_bytes=0, stream=0)
+    tk.topkv_unpack_layer_batched(0, good, 0, 0, 0, 1, 0, src_bytes=0, stream=0)

@@ -1,0 +1,223 @@
+"""HIP path vs the CPU oracle, element by element, through the C ABI.
+
+Small cases run every layer of seeded pools shaped like the five workloads
+(reduced in layers or lengths so the oracle finishes in seconds, while still
+spanning many tiles and ragged last pages), plus edge cases.  Bar: bit-exact
+(the operation moves opaque words)."""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from gpu_util import say, to_dev, to_host
+from paper_2607_28633_amd.workloads import (host_dst_prefill, host_src_pool, make_workload,
+                                            random_words)
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module")
+def tk():
+    from paper_2607_28633_amd import topkv
+    assert torch.cuda.is_available(), "GPU tests need a GPU"
+    return topkv
+
+
+def _scaled(name, div, **kw):
+    base = make_workload(name)
+    lens = np.maximum(base.seq_lens // div, 1)
+    return make_workload(name, seq_lens=lens, **kw)
+
+
+SMALL = {
+    "tiny": lambda: make_workload("tiny"),
+    "tiny-p16-to-p48": lambda: make_workload("tiny", dst_page_size=48),
+    "tiny-p16-to-p1": lambda: make_workload("tiny", dst_page_size=1),
+    "llama3-8b-2layers": lambda: make_workload("llama3-8b", num_layers=2, num_pages=600, dst_num_pages=700),
+    "llama3-70b-batch8-div6": lambda: _scaled("llama3-70b-batch8", 6, num_layers=2),
+    "deepseek-v3-mla-div16": lambda: _scaled("deepseek-v3-mla", 16, num_layers=2),
+    "reblock-70b-div32": lambda: _scaled("reblock-70b", 32, num_layers=3, phys_layers=3),
+    "reblock-p64-to-p16": lambda: _scaled("reblock-70b", 64, num_layers=2, phys_layers=2, page_size=64,
+                                          dst_page_size=16),
+    "odd-row-6B": lambda: make_workload("tiny", num_heads=1, head_dim=3, seq_lens=[40, 0, 7, 33]),
+    "odd-row-5B-u8": lambda: make_workload("tiny", num_heads=1, head_dim=5, elem_bytes=1, seq_lens=[19, 64]),
+    "row-12B-u32": lambda: make_workload("tiny", num_heads=1, head_dim=3, elem_bytes=4, seq_lens=[5, 77]),
+    "row-24B-u64": lambda: make_workload("tiny", num_heads=3, head_dim=1, elem_bytes=8, seq_lens=[31, 2, 17]),
+    "page256-big-planes": lambda: make_workload("llama3-8b", num_layers=1, page_size=256, dst_page_size=16,
+                                                seq_lens=[1000, 513, 256]),
+}
+
+
+def _sweep_and_check(tk, wl, src_h, dst_h, label):
+    """Batched pack of every layer, then batched unpack; both vs the oracle."""
+    src, dst = to_dev(src_h), to_dev(dst_h)
+    bt, bt2 = to_dev(wl.block_tables), to_dev(wl.dst_block_tables)
+    lens = to_dev(wl.seq_lens)
+    nbytes = tk.topkv_packed_layer_bytes(src, wl.seq_lens)
+    want_dst = dst_h.copy()
+    for layer in range(wl.num_layers):
+        slab = layer % wl.phys_layers
+        # sentinel-filled packed buffer with a tail guard: nothing may be written past the batch
+        packed = torch.full((nbytes // wl.elem_bytes + 64,), -7, dtype=src.dtype, device="cuda")
+        tk.topkv_pack_layer_batched(src, slab, wl.num_reqs, bt, bt.shape[1], lens, packed,
+                                    dst_bytes=nbytes)
+        tk.topkv_unpack_layer_batched(packed, dst, slab, wl.num_reqs, bt2, bt2.shape[1], lens,
+                                      src_bytes=nbytes)
+        torch.cuda.synchronize()
+        got = to_host(packed)
+        want = oracle.pack_layer(src_h, slab, wl.block_tables, wl.seq_lens)
+        assert np.array_equal(got[:want.size], want), \
+            f"{label}: pack layer {layer}: {int((got[:want.size] != want).sum())} of {want.size} differ"
+        assert (got[want.size:].view(SIGNED_OF[got.itemsize]) == -7).all(), f"{label}: write past the batch"
+        oracle.unpack_layer(want, want_dst, slab, wl.dst_block_tables, wl.seq_lens)
+        got_dst = to_host(dst)
+        assert np.array_equal(got_dst[slab], want_dst[slab]), \
+            f"{label}: unpack layer {layer}: {int((got_dst[slab] != want_dst[slab]).sum())} elements differ"
+    return src, dst
+
+
+SIGNED_OF = {1: np.int8, 2: np.int16, 4: np.int32, 8: np.int64}
+
+
+@pytest.mark.parametrize("case", sorted(SMALL))
+def test_parity_batched(tk, case):
+    wl = SMALL[case]()
+    say(f"[parity_batched] {case}: {wl.describe()}")
+    _sweep_and_check(tk, wl, host_src_pool(wl), host_dst_prefill(wl), case)
+
+
+@pytest.mark.parametrize("case", ["tiny", "deepseek-v3-mla-div16", "reblock-70b-div32", "odd-row-5B-u8"])
+def test_parity_single_request(tk, case):
+    """topkv_pack_layer / topkv_unpack_layer, one call per request."""
+    wl = SMALL[case]()
+    say(f"[parity_single] {case}")
+    src_h, dst_h = host_src_pool(wl), host_dst_prefill(wl)
+    src, dst = to_dev(src_h), to_dev(dst_h)
+    want_dst = dst_h.copy()
+    layer = wl.phys_layers - 1
+    for r in range(wl.num_reqs):
+        n = int(wl.seq_lens[r])
+        k, k2 = -(-n // wl.page_size), -(-n // wl.dst_page_size)
+        bt = to_dev(wl.block_tables[r, :max(k, 1)])
+        bt2 = to_dev(wl.dst_block_tables[r, :max(k2, 1)])
+        nbytes = tk.topkv_packed_layer_bytes(src, [n])
+        packed = torch.empty(max(nbytes // wl.elem_bytes, 1), dtype=src.dtype, device="cuda")
+        tk.topkv_pack_layer(src, layer, bt, n, packed)
+        tk.topkv_unpack_layer(packed, dst, layer, bt2, n)
+        torch.cuda.synchronize()
+        want = oracle.pack_request(src_h, layer, wl.block_tables[r], n).reshape(-1)
+        assert np.array_equal(to_host(packed)[:want.size], want), f"{case}: request {r} pack differs"
+        oracle.unpack_request(want, want_dst, layer, wl.dst_block_tables[r], n)
+    assert np.array_equal(to_host(dst), want_dst), f"{case}: single-request unpack differs"
+
+
+@pytest.mark.parametrize("P", [16, 64])
+def test_edge_lengths(tk, P):
+    """Lengths 0, 1, P-1, P, P+1, 2P with a zero-length request mid-batch."""
+    lens = [0, 1, P - 1, 0, P, P + 1, 2 * P, 3]
+    wl = make_workload("tiny", seq_lens=lens, page_size=P, dst_page_size=16)
+    say(f"[edge_lengths] P={P} lens={lens}")
+    _sweep_and_check(tk, wl, host_src_pool(wl), host_dst_prefill(wl), f"edge P={P}")
+
+
+def test_one_page_pool(tk):
+    for n in (1, 7, 16):
+        wl = make_workload("tiny", seq_lens=[n], num_pages=1, dst_num_pages=1)
+        say(f"[one_page_pool] n={n}")
+        _sweep_and_check(tk, wl, host_src_pool(wl), host_dst_prefill(wl), f"one-page n={n}")
+
+
+def test_bit_patterns(tk):
+    """Every 16-bit pattern (NaN payloads, -0, Inf, subnormals) survives."""
+    wl = make_workload("tiny", seed=9, dst_page_size=64)
+    rng = np.random.default_rng(123)
+    src_h = random_words(rng, wl.pool_shape(), 2)
+    src_h.reshape(-1)[:65536] = np.arange(65536, dtype=np.uint16)   # all patterns present
+    say("[bit_patterns]")
+    _sweep_and_check(tk, wl, src_h, host_dst_prefill(wl), "bit patterns")
+
+
+def test_misaligned_packed_buffer(tk):
+    """A packed buffer 2 bytes off 16-byte alignment takes the narrow-vector path."""
+    wl = make_workload("tiny", seed=4)
+    say("[misaligned_packed]")
+    src_h = host_src_pool(wl)
+    src = to_dev(src_h)
+    bt, lens = to_dev(wl.block_tables), to_dev(wl.seq_lens)
+    nbytes = tk.topkv_packed_layer_bytes(src, wl.seq_lens)
+    raw = torch.zeros(nbytes + 64, dtype=torch.uint8, device="cuda")
+    base = raw.data_ptr() + 2
+    tk.topkv_pack_layer_batched(src, 1, wl.num_reqs, bt, bt.shape[1], lens, base, dst_bytes=nbytes)
+    torch.cuda.synchronize()
+    got = raw.cpu().numpy()[2:2 + nbytes].view(np.uint16)
+    assert np.array_equal(got, oracle.pack_layer(src_h, 1, wl.block_tables, wl.seq_lens))
+    assert (raw.cpu().numpy()[:2] == 0).all() and (raw.cpu().numpy()[2 + nbytes:] == 0).all()
+
+
+def test_untrusted_device_inputs(tk):
+    """Out-of-range table entries are skipped, lengths are clamped to the
+    table width, and a batch that overruns the packed buffer's capacity is
+    not moved; nothing outside the buffers is touched."""
+    wl = make_workload("tiny", seed=5)
+    say("[untrusted_inputs]")
+    src_h, dst_h = host_src_pool(wl), host_dst_prefill(wl)
+    src, dst = to_dev(src_h), to_dev(dst_h)
+    P, NP = wl.page_size, wl.num_pages
+    row_words = wl.planes * wl.num_heads * wl.head_dim          # words per token over both planes
+    lens = wl.seq_lens
+    nbytes = tk.topkv_packed_layer_bytes(src, lens)
+    # (a) request 1 page 0 -> NP (invalid), request 2 page 1 -> -1
+    bad = wl.block_tables.copy()
+    bad[1, 0] = NP
+    bad[2, 1] = -1
+    packed = torch.full((nbytes // 2,), 0x5A5A, dtype=torch.int16, device="cuda")
+    tk.topkv_pack_layer_batched(src, 0, wl.num_reqs, to_dev(bad), bad.shape[1],
+                                to_dev(lens), packed, dst_bytes=nbytes)
+    torch.cuda.synchronize()
+    got = to_host(packed)
+    want = oracle.pack_layer(src_h, 0, wl.block_tables, lens).copy()
+    offs = np.concatenate([[0], np.cumsum(lens.astype(np.int64) * row_words)])
+    H, D = wl.num_heads, wl.head_dim
+    for r, i in ((1, 0), (2, 1)):
+        n = int(lens[r])
+        for c in range(wl.planes):
+            a = offs[r] + (c * n + i * P) * H * D
+            b = offs[r] + (c * n + min(n, (i + 1) * P)) * H * D
+            want[a:b] = 0x5A5A
+    assert np.array_equal(got, want)
+    # (b) a length beyond bt_stride * P is clamped to it
+    long_lens = lens.copy()
+    long_lens[3] = 10_000
+    clamped = lens.copy()
+    clamped[3] = wl.block_tables.shape[1] * P
+    need = tk.topkv_packed_layer_bytes(src, clamped)
+    packed2 = torch.zeros(need // 2, dtype=torch.int16, device="cuda")
+    full_bt = wl.block_tables.copy()
+    free = sorted(set(range(NP)) - set(full_bt[full_bt >= 0].tolist()))
+    full_bt[3, 2:] = free[:full_bt.shape[1] - 2]
+    tk.topkv_pack_layer_batched(src, 1, wl.num_reqs, to_dev(full_bt), full_bt.shape[1],
+                                to_dev(long_lens), packed2, dst_bytes=need)
+    torch.cuda.synchronize()
+    assert np.array_equal(to_host(packed2), oracle.pack_layer(src_h, 1, full_bt, clamped))
+    # (c) capacity one word short: the last request is not moved, earlier ones are
+    packed3 = torch.full((nbytes // 2,), 0x1111, dtype=torch.int16, device="cuda")
+    tk.topkv_pack_layer_batched(src, 0, wl.num_reqs, to_dev(wl.block_tables),
+                                wl.block_tables.shape[1], to_dev(lens), packed3,
+                                dst_bytes=nbytes - 2)
+    torch.cuda.synchronize()
+    got3 = to_host(packed3)
+    full = oracle.pack_layer(src_h, 0, wl.block_tables, lens)
+    assert np.array_equal(got3[:offs[-2]], full[:offs[-2]])
+    assert (got3[offs[-2]:] == 0x1111).all()
+    # (d) unpack through a table with an invalid entry writes nothing for it
+    bad2 = wl.dst_block_tables.copy()
+    bad2[0, 1] = -5
+    tk.topkv_unpack_layer_batched(torch.from_numpy(full.view(np.int16)).cuda(), dst, 0, wl.num_reqs,
+                                  to_dev(bad2), bad2.shape[1], to_dev(lens),
+                                  src_bytes=nbytes)
+    torch.cuda.synchronize()
+    want_dst = dst_h.copy()
+    keep = want_dst[0, wl.dst_block_tables[0, 1]].copy()
+    oracle.unpack_layer(full, want_dst, 0, wl.dst_block_tables, lens)
+    want_dst[0, wl.dst_block_tables[0, 1]] = keep
+    assert np.array_equal(to_host(dst), want_dst)
