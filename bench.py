@@ -7,11 +7,17 @@ layer, send buffer -> destination pool), i.e. the per-layer transfer unit of
 the paper's pipelined layer-by-layer KV transfer (Section 5.2) for both ends.
 
 value      = algorithmic bytes of the whole step / wall time of the step (GB/s,
-             10^9), inputs resident in HBM, timed with HIP events over exactly
-             --steps steps after --warmup untimed ones.
+             10^9), inputs resident in HBM, timed with HIP events on the launch
+             stream over exactly --steps steps after --warmup untimed ones.
+             Each sweep (L launches of one direction) is replayed from a
+             captured HIP graph (--launch graph, default) or issued from the
+             host (--launch eager).
 roofline   = the dominant kernel's algorithmic bytes per launch / its average
-             launch duration; durations are the kernels' own begin/end
-             timestamps (hipExtLaunchKernel events) over the timed region.
+             launch duration, i.e. the time between HIP events at that
+             direction's sweep boundaries over the timed region divided by
+             the launches in it (includes the sub-microsecond gaps between
+             graph-launched kernels).  --kernel-events adds per-launch
+             kernel-timestamp events as a diagnostic.
 cpu_baseline = the CPU oracle (numpy, one thread) on a bounded sample of the
              same workload, on this host, same byte definition.
 
@@ -55,6 +61,10 @@ def parse():
     ap.add_argument("--workload", default="llama3-70b-4k", choices=sorted(WORKLOADS))
     ap.add_argument("--cpu-seconds", type=float, default=10.0,
                     help="budget of the CPU-oracle sample (0 disables it)")
+    ap.add_argument("--launch", choices=["eager", "graph"], default="graph",
+                    help="issue each sweep as L host launches, or replay it as a captured HIP graph")
+    ap.add_argument("--kernel-events", action="store_true",
+                    help="also time every launch with its own kernel-timestamp events (diagnostic)")
     ap.add_argument("--calib-copy-bytes", type=int, default=0,
                     help="instead of the workload, run a plain device copy of this many bytes")
     return ap.parse_args()
@@ -158,58 +168,89 @@ def run(args):
     stream = torch.cuda.current_stream()
     log(f"[bench] pools src {tuple(src.shape)} dst {tuple(dst.shape)}, packed {nbytes} B/layer, ring {ring}")
 
-    def sweep(evs):
-        """The launches of one step, arguments marshalled up front."""
+    def sweep(direction, evs=None, on=stream):
+        """One direction's launches (every layer), arguments marshalled up front,
+        bound to stream `on` (None: the stream current when called)."""
         calls = []
         for l in range(L):
-            e = evs[0][l] if evs else (None, None)
-            calls.append(topkv.prepare_pack_layer_batched_ex(
-                src, l % wl.phys_layers, R, bt, bt.shape[1], lens, packed[l % ring], stream=stream,
-                start=e[0], stop=e[1]))
-        for l in range(L):
-            e = evs[1][l] if evs else (None, None)
-            calls.append(topkv.prepare_unpack_layer_batched_ex(
-                packed[l % ring], dst, l % wl.phys_layers, R, bt2, bt2.shape[1], lens, stream=stream,
-                start=e[0], stop=e[1]))
+            e = evs[l] if evs else (None, None)
+            if direction == 0:
+                calls.append(topkv.prepare_pack_layer_batched_ex(
+                    src, l % wl.phys_layers, R, bt, bt.shape[1], lens, packed[l % ring], stream=on,
+                    start=e[0], stop=e[1]))
+            else:
+                calls.append(topkv.prepare_unpack_layer_batched_ex(
+                    packed[l % ring], dst, l % wl.phys_layers, R, bt2, bt2.shape[1], lens, stream=on,
+                    start=e[0], stop=e[1]))
         return calls
 
-    def step(calls):
+    def run_calls(calls):
         for c in calls:
             c()
 
-    plain = sweep(None)
+    sweeps = [sweep(0), sweep(1)]
     for _ in range(args.warmup):
-        step(plain)
+        run_calls(sweeps[0])
+        run_calls(sweeps[1])
     torch.cuda.synchronize()
-    log(f"[bench] {args.warmup} warmup steps done")
+    if args.launch == "graph":
+        # each direction's sweep captured once; replays launch the L kernels from the GPU side
+        graphs = []
+        for d in (0, 1):
+            g = torch.cuda.CUDAGraph()
+            with torch.cuda.graph(g):
+                run_calls(sweep(d, on=None))   # bound to the capture stream
+            graphs.append(g)
+        for _ in range(max(1, args.warmup)):
+            graphs[0].replay()
+            graphs[1].replay()
+        torch.cuda.synchronize()
+        issue = [graphs[0].replay, graphs[1].replay]
+    else:
+        issue = [lambda: run_calls(sweeps[0]), lambda: run_calls(sweeps[1])]
+    log(f"[bench] {args.warmup} warmup steps done ({args.launch} launches)")
 
-    evs = [[[(topkv.HipEvent(), topkv.HipEvent()) for _ in range(L)] for _ in range(2)]
-           for _ in range(args.steps)]
-    timed = [sweep(evs[k]) for k in range(args.steps)]
-    t_start, t_stop = topkv.HipEvent(), topkv.HipEvent()
+    # timed region: events on the launch stream at the sweep boundaries
+    marks = [[topkv.HipEvent() for _ in range(3)] for _ in range(args.steps)]
     torch.cuda.synchronize()
     h0 = time.perf_counter()
-    t_start.record(stream)
     for k in range(args.steps):
-        step(timed[k])
-    t_stop.record(stream)
-    t_stop.synchronize()
+        marks[k][0].record(stream)
+        issue[0]()
+        marks[k][1].record(stream)
+        issue[1]()
+        marks[k][2].record(stream)
+    marks[-1][2].synchronize()
     torch.cuda.synchronize()
     host_s = time.perf_counter() - h0
-    wall_ms = t_start.elapsed_ms(t_stop)
+    wall_ms = marks[0][0].elapsed_ms(marks[-1][2])
     ms_per_step = wall_ms / args.steps
+    sweep_us = [1e3 * sum(marks[k][d].elapsed_ms(marks[k][d + 1]) for k in range(args.steps)) for d in (0, 1)]
     log(f"[bench] {args.steps} timed steps: {wall_ms:.3f} ms on the GPU clock, {host_s * 1e3:.3f} ms host")
 
     pack_b, unpack_b = step_bytes(wl)
     bytes_step = L * (pack_b + unpack_b)
-    dur = {d: np.array([[evs[k][d][l][0].elapsed_ms(evs[k][d][l][1]) for l in range(L)]
-                        for k in range(args.steps)]) * 1e3 for d in (0, 1)}   # microseconds
     kern = {}
     for d, name, b in ((0, "pack", pack_b), (1, "unpack", unpack_b)):
-        us = float(dur[d].mean())
-        kern[name] = {"bytes_per_launch": b, "avg_us": round(us, 3), "median_us": round(float(np.median(dur[d])), 3),
-                      "min_us": round(float(dur[d].min()), 3), "gbs": round(b / us / 1e3, 1),
-                      "launches": int(dur[d].size)}
+        us = sweep_us[d] / (args.steps * L)
+        kern[name] = {"bytes_per_launch": b, "avg_us": round(us, 3), "gbs": round(b / us / 1e3, 1),
+                      "launches": args.steps * L}
+
+    if args.kernel_events:
+        # diagnostic: each launch stamped with its own begin/end (host launch path is slower)
+        evs = [[(topkv.HipEvent(), topkv.HipEvent()) for _ in range(L)] for _ in range(2)]
+        stamped = [sweep(0, evs[0]), sweep(1, evs[1])]
+        per = [[], []]
+        for _ in range(3):
+            run_calls(stamped[0])
+            run_calls(stamped[1])
+            torch.cuda.synchronize()
+            for d in (0, 1):
+                per[d] += [evs[d][l][0].elapsed_ms(evs[d][l][1]) * 1e3 for l in range(L)]
+        for d, name in ((0, "pack"), (1, "unpack")):
+            kern[name]["kernel_stamp_avg_us"] = round(float(np.mean(per[d])), 3)
+            kern[name]["kernel_stamp_median_us"] = round(float(np.median(per[d])), 3)
+
     dom = max(kern, key=lambda k: kern[k]["avg_us"] * kern[k]["launches"])
     traffic_vals = read_traffic(args.workload)
     traffic = None
@@ -242,6 +283,7 @@ def run(args):
         "ms_per_step": round(ms_per_step, 4), "higher_is_better": True, "scaling": "weak",
         "vs_baseline": None, "dtype": "bf16", "data": "synthetic",
         "config": {"workload": f"{wl.name}: {WORKLOADS[wl.name]}", "layers": L, "requests": R,
+                   "launch": args.launch,
                    "tokens": int(wl.seq_lens.astype(np.int64).sum()), "page_size": wl.page_size,
                    "dst_page_size": wl.dst_page_size, "packed_bytes_per_layer": nbytes,
                    "step": "pack every layer (1 launch each), then unpack every layer",

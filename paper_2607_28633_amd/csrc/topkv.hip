@@ -36,18 +36,24 @@
 #include "topkv.h"
 
 #ifndef TOPKV_VPT
-#define TOPKV_VPT 4           // 16-byte vectors per lane per tile
+#define TOPKV_VPT 8           // vectors per lane per tile (16-byte vectors: 32 KiB tiles)
 #endif
 #ifndef TOPKV_WG_PER_CU
-#define TOPKV_WG_PER_CU 8     // grid cap = CUs * this
+#define TOPKV_WG_PER_CU 8     // persistent grid cap = CUs * this
+#endif
+#ifndef TOPKV_DIRECT_MAX
+#define TOPKV_DIRECT_MAX 65536  // largest one-shot direct-mapped grid (slots)
 #endif
 #ifndef TOPKV_NONTEMPORAL
 #define TOPKV_NONTEMPORAL 1   // streaming hint on the bulk loads and stores
 #endif
+#ifndef TOPKV_THREADS
+#define TOPKV_THREADS 256     // threads per workgroup (a multiple of 64)
+#endif
 
 namespace topkv {
 
-constexpr int kThreads = 256;  // four wave64 per workgroup
+constexpr int kThreads = TOPKV_THREADS;
 constexpr int kWaves = kThreads / 64;
 
 template <int B> struct Vec;
@@ -126,14 +132,13 @@ __device__ void request_prefix(const MoveParams& p, const int32_t* __restrict__ 
   __syncthreads();
 }
 
+// A tile is up to kThreads * VPT vectors of VB bytes.  Lane t handles vectors
+// t, t + kThreads, ... so each wave instruction covers one contiguous span.
 template <int VB, int VPT>
-__device__ __forceinline__ void copy_tile(char* __restrict__ dst, const char* __restrict__ src,
-                                          int32_t len) {
+__device__ __forceinline__ void load_tile(typename Vec<VB>::type (&v)[VPT], const char* __restrict__ src,
+                                          int32_t nv) {
   typedef typename Vec<VB>::type V;
   const V* __restrict__ s = reinterpret_cast<const V*>(src);
-  V* __restrict__ d = reinterpret_cast<V*>(dst);
-  const int32_t nv = len / VB;
-  V v[VPT];
   if (nv == kThreads * VPT) {
 #pragma unroll
     for (int j = 0; j < VPT; ++j) {
@@ -143,6 +148,24 @@ __device__ __forceinline__ void copy_tile(char* __restrict__ dst, const char* __
       v[j] = s[j * kThreads + threadIdx.x];
 #endif
     }
+  } else {
+    // Ragged tile (1 <= nv < kThreads * VPT): every lane still issues all VPT
+    // loads back to back (indices clamped into the tile, so they stay in
+    // bounds); only the stores are predicated.
+#pragma unroll
+    for (int j = 0; j < VPT; ++j) {
+      const int idx = j * kThreads + threadIdx.x;
+      v[j] = s[idx < nv ? idx : nv - 1];
+    }
+  }
+}
+
+template <int VB, int VPT>
+__device__ __forceinline__ void store_tile(char* __restrict__ dst, const typename Vec<VB>::type (&v)[VPT],
+                                           int32_t nv) {
+  typedef typename Vec<VB>::type V;
+  V* __restrict__ d = reinterpret_cast<V*>(dst);
+  if (nv == kThreads * VPT) {
 #pragma unroll
     for (int j = 0; j < VPT; ++j) {
 #if TOPKV_NONTEMPORAL
@@ -152,14 +175,6 @@ __device__ __forceinline__ void copy_tile(char* __restrict__ dst, const char* __
 #endif
     }
   } else {
-    // Ragged tile (1 <= nv < kThreads * VPT): every lane still issues all VPT
-    // loads back to back (indices clamped into the tile, so they stay in
-    // bounds) and only the stores are predicated.
-#pragma unroll
-    for (int j = 0; j < VPT; ++j) {
-      const int idx = j * kThreads + threadIdx.x;
-      v[j] = s[idx < nv ? idx : nv - 1];
-    }
 #pragma unroll
     for (int j = 0; j < VPT; ++j) {
       const int idx = j * kThreads + threadIdx.x;
@@ -168,10 +183,90 @@ __device__ __forceinline__ void copy_tile(char* __restrict__ dst, const char* __
   }
 }
 
+template <int VB, int VPT>
+__device__ __forceinline__ void copy_tile(char* __restrict__ dst, const char* __restrict__ src, int32_t len) {
+  typename Vec<VB>::type v[VPT];
+  load_tile<VB, VPT>(v, src, len / VB);
+  store_tile<VB, VPT>(dst, v, len / VB);
+}
+
+// Sum of the (clamped) lengths of requests [0, r): the token offset of
+// request r in the packed batch.  Block-wide; every thread must call it.
+__device__ __forceinline__ int64_t tokens_before(const int32_t* __restrict__ seq_lens, int32_t r,
+                                                 int64_t max_tok, int64_t* red) {
+  int64_t s = 0;
+  for (int j = threadIdx.x; j < r; j += kThreads) {
+    const int64_t n = seq_lens[j];
+    s += n < 0 ? 0 : (n > max_tok ? max_tok : n);
+  }
+#pragma unroll
+  for (int off = 32; off > 0; off >>= 1) s += __shfl_xor(s, off, 64);
+  if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = s;
+  __syncthreads();
+  int64_t t = 0;
+#pragma unroll
+  for (int w = 0; w < kWaves; ++w) t += red[w];
+  return t;
+}
+
+// Direct mapping: one workgroup per (request, table entry, plane, tile)
+// slot, w = ((r * bt_stride + i) * planes + c) * tiles_per_plane + k, so the
+// slot's lengths and page index are two independent scalar loads issued at
+// once; slots past a request's last page exit.  The token offset of the
+// request is a block sum over the earlier lengths.  For pack the pool loads
+// are issued before that sum, so they overlap it.  Used when the slot count
+// is small enough for a one-shot grid.
+template <int VB, bool kPack, bool kBatched>
+__device__ __forceinline__ void move_direct(char* __restrict__ pool, char* __restrict__ packed,
+                                            const int32_t* __restrict__ tables,
+                                            const int32_t* __restrict__ seq_lens, const MoveParams& p) {
+  constexpr int VPT = TOPKV_VPT;
+  constexpr int32_t kTile = kThreads * VPT * VB;
+  __shared__ int64_t red[kWaves];
+  const uint32_t per_page = (uint32_t)(p.planes * p.tiles_per_plane);
+  const uint32_t per_req = (uint32_t)p.bt_stride * per_page;
+  const uint32_t w = blockIdx.x;
+  const int32_t r = (int32_t)(w / per_req);
+  const uint32_t rem = w - (uint32_t)r * per_req;
+  const int32_t i = (int32_t)(rem / per_page);
+  const uint32_t rem2 = rem - (uint32_t)i * per_page;
+  const int32_t c = (int32_t)(rem2 / (uint32_t)p.tiles_per_plane);
+  const int32_t k = (int32_t)(rem2 - (uint32_t)c * p.tiles_per_plane);
+  const int64_t max_tok = (int64_t)p.bt_stride * p.page_size;
+
+  const int32_t page = tables[(int64_t)r * p.bt_stride + i];
+  int64_t n = kBatched ? (int64_t)seq_lens[r] : (int64_t)p.n_single;
+  n = n < 0 ? 0 : (n > max_tok ? max_tok : n);
+  const int32_t first = i * p.page_size;
+  const int64_t rows = n - first < p.page_size ? n - first : p.page_size;
+  const int64_t run = rows * p.row_bytes;
+  const int64_t start = (int64_t)k * kTile;
+  const bool live = rows > 0 && start < run && page >= 0 && (int64_t)page < p.num_pages;
+  const int32_t nv = live ? (int32_t)((run - start < kTile ? run - start : kTile) / VB) : 0;
+  char* pool_ptr = pool + (int64_t)page * p.page_bytes + (int64_t)c * p.plane_bytes + start;
+
+  typename Vec<VB>::type v[VPT];
+  if (kPack && live) load_tile<VB, VPT>(v, pool_ptr, nv);
+  const int64_t tok0 = (kBatched && r > 0) ? tokens_before(seq_lens, r, max_tok, red) : 0;
+  if (!live) return;
+  if ((tok0 + n) * p.planes * p.row_bytes > p.packed_cap) return;
+  char* packed_ptr = packed + ((tok0 * p.planes + (int64_t)c * n + first) * p.row_bytes + start);
+  if (kPack) {
+    store_tile<VB, VPT>(packed_ptr, v, nv);
+  } else {
+    load_tile<VB, VPT>(v, packed_ptr, nv);
+    store_tile<VB, VPT>(pool_ptr, v, nv);
+  }
+}
+
+// Persistent mapping for large batches: every workgroup scans the lengths
+// into per-request token and page prefix sums (LDS), then strides over the
+// live (request, page, plane, tile) items, locating each item's request by
+// binary search.  Work is spread evenly however long the requests are.
 // pool: pool base already offset to the layer; packed: packed buffer base;
 // tables: [num_reqs][bt_stride]; seq_lens: device [num_reqs] (batched only).
 template <int VB, bool kPack>
-__device__ __forceinline__ void move_layer(char* __restrict__ pool, char* __restrict__ packed,
+__device__ __forceinline__ void move_strided(char* __restrict__ pool, char* __restrict__ packed,
                                            const int32_t* __restrict__ tables,
                                            const int32_t* __restrict__ seq_lens, const MoveParams& p) {
   constexpr int VPT = TOPKV_VPT;
@@ -228,18 +323,24 @@ __device__ __forceinline__ void move_layer(char* __restrict__ pool, char* __rest
   }
 }
 
-template <int VB>
+// kMode: 0 = persistent (strided) grid, 1 = direct grid for one request with
+// a host-side length, 2 = direct grid for a batch with device lengths.
+enum { kStrided = 0, kDirectSingle = 1, kDirectBatched = 2 };
+
+template <int VB, int kMode>
 __global__ __launch_bounds__(kThreads) void kv_pack_kernel(char* __restrict__ pool, char* __restrict__ packed,
                                                            const int32_t* __restrict__ tables,
                                                            const int32_t* __restrict__ seq_lens, MoveParams p) {
-  move_layer<VB, true>(pool, packed, tables, seq_lens, p);
+  if (kMode == kStrided) move_strided<VB, true>(pool, packed, tables, seq_lens, p);
+  else move_direct<VB, true, kMode == kDirectBatched>(pool, packed, tables, seq_lens, p);
 }
 
-template <int VB>
+template <int VB, int kMode>
 __global__ __launch_bounds__(kThreads) void kv_unpack_kernel(char* __restrict__ pool, char* __restrict__ packed,
                                                              const int32_t* __restrict__ tables,
                                                              const int32_t* __restrict__ seq_lens, MoveParams p) {
-  move_layer<VB, false>(pool, packed, tables, seq_lens, p);
+  if (kMode == kStrided) move_strided<VB, false>(pool, packed, tables, seq_lens, p);
+  else move_direct<VB, false, kMode == kDirectBatched>(pool, packed, tables, seq_lens, p);
 }
 
 // ---------------------------------------------------------------------------
@@ -300,14 +401,20 @@ int vector_bytes(uintptr_t a, uintptr_t b, int64_t row) {
 
 typedef void (*KernelFn)(char*, char*, const int32_t*, const int32_t*, MoveParams);
 
-KernelFn pick_kernel(bool pack, int vb) {
+template <int kMode>
+KernelFn pick_kernel_mode(bool pack, int vb) {
   switch (vb) {
-    case 16: return pack ? kv_pack_kernel<16> : kv_unpack_kernel<16>;
-    case 8: return pack ? kv_pack_kernel<8> : kv_unpack_kernel<8>;
-    case 4: return pack ? kv_pack_kernel<4> : kv_unpack_kernel<4>;
-    case 2: return pack ? kv_pack_kernel<2> : kv_unpack_kernel<2>;
-    default: return pack ? kv_pack_kernel<1> : kv_unpack_kernel<1>;
+    case 16: return pack ? kv_pack_kernel<16, kMode> : kv_unpack_kernel<16, kMode>;
+    case 8: return pack ? kv_pack_kernel<8, kMode> : kv_unpack_kernel<8, kMode>;
+    case 4: return pack ? kv_pack_kernel<4, kMode> : kv_unpack_kernel<4, kMode>;
+    case 2: return pack ? kv_pack_kernel<2, kMode> : kv_unpack_kernel<2, kMode>;
+    default: return pack ? kv_pack_kernel<1, kMode> : kv_unpack_kernel<1, kMode>;
   }
+}
+
+KernelFn pick_kernel(bool pack, int vb, bool direct, bool batched) {
+  if (!direct) return pick_kernel_mode<kStrided>(pack, vb);
+  return batched ? pick_kernel_mode<kDirectBatched>(pack, vb) : pick_kernel_mode<kDirectSingle>(pack, vb);
 }
 
 // Shared launcher for the four movement entry points.
@@ -342,11 +449,20 @@ topkv_status_t launch_move(bool pack, const topkv_pool_t* pool, int32_t layer, v
       (int64_t)bt_stride * pool->page_size > INT32_MAX)
     return TOPKV_ERR_UNSUPPORTED;
 
-  int cus = 0;
-  st = cu_count(&cus);
-  if (st != TOPKV_OK) return st;
-  const int64_t cap = (int64_t)cus * TOPKV_WG_PER_CU;
-  const unsigned grid = (unsigned)(work < cap ? work : cap);
+  // Direct mapping when every (request, table entry, plane, tile) slot can
+  // get its own workgroup; otherwise a persistent grid over the live items.
+  const int64_t slots = (seq_lens ? (int64_t)num_reqs : 1) * bt_stride * per_page;
+  const bool direct = slots <= TOPKV_DIRECT_MAX;
+  unsigned grid;
+  if (direct) {
+    grid = (unsigned)slots;
+  } else {
+    int cus = 0;
+    st = cu_count(&cus);
+    if (st != TOPKV_OK) return st;
+    const int64_t cap = (int64_t)cus * TOPKV_WG_PER_CU;
+    grid = (unsigned)(work < cap ? work : cap);
+  }
   if (grid == 0) return TOPKV_OK;
 
   char* pool_ptr = static_cast<char*>(pool->base) + (int64_t)layer * g.layer_bytes;
@@ -365,9 +481,10 @@ topkv_status_t launch_move(bool pack, const topkv_pool_t* pool, int32_t layer, v
   p.tiles_per_plane = (int32_t)tpp;
   p.batched = seq_lens ? 1 : 0;
 
-  const size_t lds = seq_lens ? sizeof(uint64_t) * kWaves + sizeof(int32_t) * 2 * ((size_t)num_reqs + 1) : 0;
+  const size_t lds = (seq_lens && !direct) ? sizeof(uint64_t) * kWaves + sizeof(int32_t) * 2 * ((size_t)num_reqs + 1)
+                                           : 0;
   void* args[] = {&pool_ptr, &packed_ptr, &tables, &seq_lens, &p};
-  const void* fn = reinterpret_cast<const void*>(pick_kernel(pack, vb));
+  const void* fn = reinterpret_cast<const void*>(pick_kernel(pack, vb, direct, seq_lens != nullptr));
   hipError_t e;
   if (launch->start || launch->stop)
     e = hipExtLaunchKernel(fn, dim3(grid), dim3(kThreads), args, lds, launch->stream, launch->start,

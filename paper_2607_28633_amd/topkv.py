@@ -227,10 +227,10 @@ class HipEvent:
             raise RuntimeError(f"hipEventElapsedTime failed ({rc})")
         return float(ms.value)
 
-    def __del__(self):
+    def __del__(self, _finalizing=sys.is_finalizing, _destroy=_hip.hipEventDestroy):
         h, self.handle = getattr(self, "handle", None), None
-        if h and not sys.is_finalizing():
-            _hip.hipEventDestroy(h)
+        if h and not _finalizing():
+            _destroy(h)
 
 
 def _event(e) -> int:
