@@ -51,7 +51,7 @@
  * kernel skip that page (nothing read or written for it); a device seq_len
  * below 0 counts as 0 and one above bt_stride * P as bt_stride * P; a batched
  * request whose packed block would cross the end of the packed buffer is not
- * moved.  Such skips are silent.
+ * moved.  Such skips are silent; topkv_check_tables reports them.
  * Overlapping source and destination ranges are undefined behaviour.
  *
  * Build: hipcc --offload-arch=gfx950 (see the package's build script).  C
@@ -164,6 +164,33 @@ topkv_status_t topkv_unpack_layer_batched_ex(const void* src, int64_t src_bytes,
  * seq_lens with num_reqs > 0, a negative length or int64 overflow. */
 int64_t topkv_packed_layer_bytes(const topkv_pool_t* pool, const int32_t* seq_lens_host,
                                  int32_t num_reqs);
+
+/* Checked path: validate block tables and lengths on the device before a
+ * pack or unpack (the movement calls skip bad entries silently).  For every
+ * request r and entry i < ceil(seq_lens[r] / pool->page_size) it checks
+ * 0 <= entry < pool->num_pages, that seq_lens[r] lies in
+ * [0, bt_stride * page_size], and, when check_duplicates != 0, that no page
+ * is named twice in the batch (required of an unpack destination, where two
+ * writers of one page would race; a pack source may repeat pages).
+ *   pool:       geometry only (num_pages, page_size); base is not accessed
+ *   workspace:  device memory of topkv_check_workspace_bytes(pool) bytes (a
+ *               page bitmap), owned by the caller, cleared by this call; may
+ *               be null when check_duplicates == 0
+ *   result:     device int32[4], written on the stream: [0] TOPKV_OK or
+ *               TOPKV_ERR_BOUNDS, [1] entries out of range, [2] repeated
+ *               pages, [3] lengths out of range.  Read it after the stream
+ *               has synchronised.
+ * Launches three small kernels; the call itself does not synchronise.
+ * Calls sharing a workspace on overlapping streams race. */
+topkv_status_t topkv_check_tables(const topkv_pool_t* pool, int32_t num_reqs,
+                                  const int32_t* block_tables, int32_t bt_stride,
+                                  const int32_t* seq_lens, int32_t check_duplicates,
+                                  void* workspace, int64_t workspace_bytes,
+                                  int32_t* result, hipStream_t stream);
+
+/* Workspace bytes topkv_check_tables needs for this pool (a bitmap of
+ * num_pages bits, in 4-byte words); -1 for a null or empty pool. */
+int64_t topkv_check_workspace_bytes(const topkv_pool_t* pool);
 
 /* Static, human-readable name of a status code (never null). */
 const char* topkv_status_string(topkv_status_t status);

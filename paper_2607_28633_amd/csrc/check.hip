@@ -1,0 +1,95 @@
+// check.hip - checked path of libtopkv.so: device-side validation of block
+// tables and lengths (declared in include/topkv.h).  The movement kernels in
+// topkv.hip never depend on it; they bounds-check what they read and skip
+// bad entries silently, and this call reports them.
+#include <hip/hip_runtime.h>
+
+#include <cstdint>
+
+#include "topkv.h"
+
+namespace {
+
+// result[0] status, [1] entries outside [0, num_pages), [2] pages named more
+// than once, [3] lengths outside [0, bt_stride * page_size].
+__global__ __launch_bounds__(256) void kv_check_clear_kernel(uint32_t* __restrict__ bitmap, int64_t words,
+                                                             int32_t* __restrict__ result) {
+  const int64_t stride = (int64_t)gridDim.x * blockDim.x;
+  for (int64_t w = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; w < words; w += stride) bitmap[w] = 0u;
+  if (blockIdx.x == 0 && threadIdx.x < 4) result[threadIdx.x] = 0;
+}
+
+// One thread per (request, table entry) slot.
+__global__ __launch_bounds__(256) void kv_check_tables_kernel(const int32_t* __restrict__ tables,
+                                                              const int32_t* __restrict__ seq_lens,
+                                                              int32_t num_reqs, int32_t bt_stride,
+                                                              int32_t page_size, int64_t num_pages,
+                                                              int32_t check_duplicates,
+                                                              uint32_t* __restrict__ bitmap,
+                                                              int32_t* __restrict__ result) {
+  const int64_t slot = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (slot >= (int64_t)num_reqs * bt_stride) return;
+  const int32_t r = (int32_t)(slot / bt_stride);
+  const int32_t i = (int32_t)(slot - (int64_t)r * bt_stride);
+  int64_t n = seq_lens[r];
+  const int64_t max_tok = (int64_t)bt_stride * page_size;
+  if (n < 0 || n > max_tok) {
+    if (i == 0) atomicAdd(&result[3], 1);
+    n = n < 0 ? 0 : max_tok;
+  }
+  if ((int64_t)i * page_size >= n) return;     // past the request's last page: never read
+  const int32_t e = tables[slot];
+  if (e < 0 || (int64_t)e >= num_pages) {
+    atomicAdd(&result[1], 1);
+    return;
+  }
+  if (check_duplicates) {
+    const uint32_t bit = 1u << (e & 31);
+    const uint32_t old = atomicOr(&bitmap[e >> 5], bit);
+    if (old & bit) atomicAdd(&result[2], 1);
+  }
+}
+
+__global__ void kv_check_finish_kernel(int32_t* __restrict__ result) {
+  if (threadIdx.x == 0)
+    result[0] = (result[1] | result[2] | result[3]) ? (int32_t)TOPKV_ERR_BOUNDS : (int32_t)TOPKV_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+int64_t topkv_check_workspace_bytes(const topkv_pool_t* pool) {
+  if (!pool || pool->num_pages <= 0) return -1;
+  return ((pool->num_pages + 31) / 32) * (int64_t)sizeof(uint32_t);
+}
+
+topkv_status_t topkv_check_tables(const topkv_pool_t* pool, int32_t num_reqs, const int32_t* block_tables,
+                                  int32_t bt_stride, const int32_t* seq_lens, int32_t check_duplicates,
+                                  void* workspace, int64_t workspace_bytes, int32_t* result,
+                                  hipStream_t stream) {
+  if (!pool || pool->num_pages <= 0 || pool->page_size <= 0 || num_reqs < 0 || !result) return TOPKV_ERR_INVALID_ARG;
+  if (num_reqs > 0 && (!block_tables || !seq_lens || bt_stride <= 0)) return TOPKV_ERR_INVALID_ARG;
+  if ((int64_t)bt_stride * pool->page_size > INT32_MAX) return TOPKV_ERR_UNSUPPORTED;
+  const int64_t words = (pool->num_pages + 31) / 32;
+  const bool dup = check_duplicates != 0;
+  if (dup && (!workspace || workspace_bytes < words * (int64_t)sizeof(uint32_t))) return TOPKV_ERR_INVALID_ARG;
+  uint32_t* bitmap = dup ? static_cast<uint32_t*>(workspace) : nullptr;
+  const int64_t clear_words = dup ? words : 0;
+  const unsigned clear_grid = (unsigned)(clear_words / 256 + 1 < 1024 ? clear_words / 256 + 1 : 1024);
+  hipLaunchKernelGGL(kv_check_clear_kernel, dim3(clear_grid), dim3(256), 0, stream, bitmap, clear_words,
+                     result);
+  if (hipGetLastError() != hipSuccess) return TOPKV_ERR_LAUNCH;
+  const int64_t slots = (int64_t)num_reqs * bt_stride;
+  if (slots > 0) {
+    if (slots / 256 + 1 > INT32_MAX) return TOPKV_ERR_UNSUPPORTED;
+    hipLaunchKernelGGL(kv_check_tables_kernel, dim3((unsigned)((slots + 255) / 256)), dim3(256), 0, stream,
+                       block_tables, seq_lens, num_reqs, bt_stride, pool->page_size, pool->num_pages,
+                       (int32_t)dup, bitmap, result);
+    if (hipGetLastError() != hipSuccess) return TOPKV_ERR_LAUNCH;
+  }
+  hipLaunchKernelGGL(kv_check_finish_kernel, dim3(1), dim3(64), 0, stream, result);
+  return hipGetLastError() == hipSuccess ? TOPKV_OK : TOPKV_ERR_LAUNCH;
+}
+
+}  // extern "C"

@@ -32,10 +32,12 @@ TOPKV_ERR_LAUNCH = 3
 TOPKV_ERR_BOUNDS = 4
 TOPKV_ERR_DEVICE = 5
 TOPKV_MAX_BATCH_REQS = 8000
+TOPKV_CHECK_RESULT_WORDS = 4
 
 EXPORTS = ["topkv_pack_layer", "topkv_unpack_layer", "topkv_pack_layer_batched",
            "topkv_unpack_layer_batched", "topkv_pack_layer_batched_ex",
-           "topkv_unpack_layer_batched_ex", "topkv_packed_layer_bytes", "topkv_status_string"]
+           "topkv_unpack_layer_batched_ex", "topkv_packed_layer_bytes", "topkv_status_string",
+           "topkv_check_tables", "topkv_check_workspace_bytes"]
 
 
 class topkv_pool_t(ctypes.Structure):
@@ -64,6 +66,8 @@ _SIGS = {
                                              ctypes.POINTER(topkv_launch_t)]),
     "topkv_packed_layer_bytes": (_I64, [_POOL, ctypes.POINTER(_I32), _I32]),
     "topkv_status_string": (ctypes.c_char_p, [_I32]),
+    "topkv_check_tables": (_I32, [_POOL, _I32, _P, _I32, _P, _I32, _P, _I64, _P, _P]),
+    "topkv_check_workspace_bytes": (_I64, [_POOL]),
 }
 for _name, (_res, _args) in _SIGS.items():
     _fn = getattr(_lib, _name)
@@ -186,6 +190,21 @@ def topkv_packed_layer_bytes(pool, seq_lens_host) -> int:
     lens = [int(x) for x in seq_lens_host]
     arr = (_I32 * max(1, len(lens)))(*lens)
     return int(_lib.topkv_packed_layer_bytes(ctypes.byref(_pool_arg(pool)), arr, len(lens)))
+
+
+def topkv_check_tables(pool, num_reqs, block_tables, bt_stride, seq_lens, check_duplicates, workspace,
+                       result, workspace_bytes=None, stream=None) -> None:
+    """Queue the device-side table check; `result` (device int32[4]) holds
+    [status, entries out of range, repeated pages, lengths out of range]
+    once the stream has synchronised."""
+    ws_bytes = 0 if workspace is None else _nbytes(workspace, workspace_bytes)
+    _check(_lib.topkv_check_tables(ctypes.byref(_pool_arg(pool)), int(num_reqs), _table_ptr(block_tables),
+                                   int(bt_stride), _table_ptr(seq_lens), int(check_duplicates), _ptr(workspace),
+                                   ws_bytes, _table_ptr(result), _stream(stream)))
+
+
+def topkv_check_workspace_bytes(pool) -> int:
+    return int(_lib.topkv_check_workspace_bytes(ctypes.byref(_pool_arg(pool))))
 
 
 def topkv_status_string(status: int) -> str:

@@ -106,3 +106,18 @@ def test_empty_work_is_a_no_op(tk):
     tk.topkv_unpack_layer(0, good, 1, 0, 0, stream=0)
     tk.topkv_pack_layer_batched(good, 0, 0, 0, 1, 0, 0, dst_bytes=0, stream=0)
     tk.topkv_unpack_layer_batched(0, good, 0, 0, 0, 1, 0, src_bytes=0, stream=0)
+
+
+def test_check_tables_validation(tk):
+    INV = tk.TOPKV_ERR_INVALID_ARG
+    good = _pool(tk)
+    bt, lens, ws, res = 0x20000, 0x30000, 0x40000, 0x50000
+    assert tk.topkv_check_workspace_bytes(good) == 64 // 32 * 4
+    assert tk.topkv_check_workspace_bytes(_pool(tk, num_pages=33)) == 8
+    assert tk.topkv_check_workspace_bytes(_pool(tk, num_pages=0)) == -1
+    _expect(tk, INV, tk.topkv_check_tables, good, 2, bt, 4, lens, 1, ws, 0, workspace_bytes=8)      # null result
+    _expect(tk, INV, tk.topkv_check_tables, good, 2, bt, 4, lens, 1, 0, res, workspace_bytes=8)     # no workspace
+    _expect(tk, INV, tk.topkv_check_tables, good, 2, bt, 4, lens, 1, ws, res, workspace_bytes=4)    # too small
+    _expect(tk, INV, tk.topkv_check_tables, good, 2, 0, 4, lens, 0, None, res)                      # null tables
+    _expect(tk, INV, tk.topkv_check_tables, good, -1, bt, 4, lens, 0, None, res)
+    _expect(tk, INV, tk.topkv_check_tables, _pool(tk, page_size=0), 2, bt, 4, lens, 0, None, res)
