@@ -5,7 +5,7 @@ benchmark's CPU-baseline leg, never by the product path.  It shares no code
 with the HIP library.
 """
 from .kvpack import (pack_layer, pack_request, packed_layer_elems, unpack_layer,
-                     unpack_request)
+                     unpack_request, window_start)
 
 __all__ = ["pack_layer", "pack_request", "packed_layer_elems", "unpack_layer",
-           "unpack_request"]
+           "unpack_request", "window_start"]

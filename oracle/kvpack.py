@@ -18,7 +18,9 @@ Disaggregated GPU Inference"):
 * Section 2.2, Eq. 1: the bytes moved for a request of s tokens are
   2 * L * h_kv * d_h * s * b_p; Section 5.3: an MLA cache keeps one shared
   576-wide latent per token and layer, so the factor 2 (separate K and V)
-  is dropped.
+  is dropped.  Section 2.2 extends Eq. 1 per layer kind: a windowed
+  (sliding-window attention) layer holds only its last W tokens, so its
+  transfer moves tokens [max(0, s - W), s) only.
 
 Hence, for one layer ``l`` (pool ``[L][NP][C][P][H][D]``, C planes = 2 for K|V
 and 1 for an MLA latent):
@@ -26,8 +28,10 @@ and 1 for an MLA latent):
   pack    out_r[c][t][h][d] = pool[l][bt_r[t div P]][c][t mod P][h][d]  for t < n_r
   unpack  pool'[l][bt'_r[t div P']][c][t mod P'][h][d] = in_r[c][t][h][d] for t < n_r
 
-A batch concatenates the per-request blocks ``[C][n_r][H][D]`` in request
-order.  Unpack writes only the slots of valid tokens: every other element of
+A windowed layer (``window`` W > 0) keeps tokens t in [max(0, n_r - W), n_r)
+only: the packed block is ``[C][min(n_r, W)][H][D]`` and unpack writes those
+tokens at their own positions.  A batch concatenates the per-request blocks
+in request order.  Unpack writes only the slots of valid tokens: every other element of
 the destination pool (other pages, and slots >= n_r mod P' of a request's last
 page) keeps its prior value.  Entries of a block table past the request's
 ``ceil(n_r / P)`` pages are never read.  Elements are opaque words: the
@@ -49,17 +53,26 @@ def _check_pool(pool):
         raise ValueError("pool must be [layers][pages][planes][page_size][heads][dim]")
 
 
-def pack_request(pool: np.ndarray, layer: int, block_table: np.ndarray, seq_len: int) -> np.ndarray:
+def window_start(seq_len: int, window: int) -> int:
+    """First token a windowed layer keeps: the last `window` tokens survive
+    (Section 2.2); window 0 keeps every token."""
+    n = int(seq_len)
+    return n - int(window) if 0 < int(window) < n else 0
+
+
+def pack_request(pool: np.ndarray, layer: int, block_table: np.ndarray, seq_len: int,
+                 window: int = 0) -> np.ndarray:
     """One request, one layer: gather its pages into ``[C][n][H][D]``.
 
     Token t of the request sits in physical page ``block_table[t // P]`` at
     slot ``t % P`` (paged layout, Section 6); the result lists K then V
     (planes), each token-major with heads and dims inside (Section 3.5).
+    With a window only tokens [window_start, n) are gathered.
     """
     _check_pool(pool)
     P = pool.shape[3]
     n = int(seq_len)
-    t = np.arange(n)
+    t = np.arange(window_start(n, window), n)
     pages = np.asarray(block_table)[t // P]
     slots = t % P
     # advanced indices on axes 0 and 2 of pool[layer] -> result (n, C, H, D)
@@ -68,11 +81,11 @@ def pack_request(pool: np.ndarray, layer: int, block_table: np.ndarray, seq_len:
 
 
 def pack_layer(pool: np.ndarray, layer: int, block_tables: np.ndarray,
-               seq_lens: np.ndarray) -> np.ndarray:
+               seq_lens: np.ndarray, window: int = 0) -> np.ndarray:
     """A batch of requests, one layer: flat buffer of the per-request
     ``[C][n_r][H][D]`` blocks in request order."""
     _check_pool(pool)
-    parts = [pack_request(pool, layer, block_tables[r], int(seq_lens[r])).reshape(-1)
+    parts = [pack_request(pool, layer, block_tables[r], int(seq_lens[r]), window).reshape(-1)
              for r in range(len(seq_lens))]
     if not parts:
         return np.empty(0, dtype=pool.dtype)
@@ -80,7 +93,7 @@ def pack_layer(pool: np.ndarray, layer: int, block_tables: np.ndarray,
 
 
 def unpack_request(packed_r: np.ndarray, pool: np.ndarray, layer: int,
-                   block_table: np.ndarray, seq_len: int) -> None:
+                   block_table: np.ndarray, seq_len: int, window: int = 0) -> None:
     """Inverse of :func:`pack_request` into ``pool`` (modified in place).
 
     The destination page size P' is the pool's own; it need not equal the
@@ -89,8 +102,8 @@ def unpack_request(packed_r: np.ndarray, pool: np.ndarray, layer: int,
     _check_pool(pool)
     C, P, H, D = pool.shape[2], pool.shape[3], pool.shape[4], pool.shape[5]
     n = int(seq_len)
-    block = np.asarray(packed_r).reshape(C, n, H, D)
-    t = np.arange(n)
+    t = np.arange(window_start(n, window), n)
+    block = np.asarray(packed_r).reshape(C, t.size, H, D)
     pages = np.asarray(block_table)[t // P]
     slots = t % P
     view = pool[layer]
@@ -98,7 +111,7 @@ def unpack_request(packed_r: np.ndarray, pool: np.ndarray, layer: int,
 
 
 def unpack_layer(packed: np.ndarray, pool: np.ndarray, layer: int,
-                 block_tables: np.ndarray, seq_lens: np.ndarray) -> np.ndarray:
+                 block_tables: np.ndarray, seq_lens: np.ndarray, window: int = 0) -> np.ndarray:
     """A batch of requests, one layer, scattered into ``pool`` (in place;
     also returned).  Request r's block starts where requests < r end."""
     _check_pool(pool)
@@ -106,14 +119,15 @@ def unpack_layer(packed: np.ndarray, pool: np.ndarray, layer: int,
     off = 0
     for r in range(len(seq_lens)):
         n = int(seq_lens[r])
-        size = C * n * H * D
-        unpack_request(packed[off:off + size], pool, layer, block_tables[r], n)
+        size = C * (n - window_start(n, window)) * H * D
+        unpack_request(packed[off:off + size], pool, layer, block_tables[r], n, window)
         off += size
     if off != packed.size:
         raise ValueError(f"packed buffer holds {packed.size} elements, requests need {off}")
     return pool
 
 
-def packed_layer_elems(planes: int, heads: int, dim: int, seq_lens) -> int:
-    """Elements in one layer's packed batch: C * H * D * sum(n_r)."""
-    return int(planes) * int(heads) * int(dim) * int(np.sum(np.asarray(seq_lens, dtype=np.int64)))
+def packed_layer_elems(planes: int, heads: int, dim: int, seq_lens, window: int = 0) -> int:
+    """Elements in one layer's packed batch: C * H * D * sum(kept tokens)."""
+    kept = sum(int(n) - window_start(int(n), window) for n in np.asarray(seq_lens).reshape(-1))
+    return int(planes) * int(heads) * int(dim) * kept

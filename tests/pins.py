@@ -245,9 +245,64 @@ def pin_zero_and_opaque(impl):
         assert empty.size == 0
 
 
+# ----------------------------------------------------------------------------
+# Windowed layers (Section 2.2 per-layer-kind extension of Eq. 1)
+# ----------------------------------------------------------------------------
+
+def pin_window_slice(impl):
+    """A windowed pack equals the full pack cut to each request's last W
+    tokens (a library slice of a result the pins above fix)."""
+    wl = make_workload("tiny", seed=8, seq_lens=[64, 48, 33, 17, 1, 0])
+    src = host_src_pool(wl)
+    C, H, D = wl.planes, wl.num_heads, wl.head_dim
+    for W in (1, 15, 16, 17, 40, 64, 100):
+        got = impl.pack_layer(src, 1, wl.block_tables, wl.seq_lens, window=W)
+        parts = []
+        for r, n in enumerate(wl.seq_lens):
+            full = impl.pack_layer(src, 1, wl.block_tables[r:r + 1], wl.seq_lens[r:r + 1]).reshape(C, int(n), H, D)
+            parts.append(full[:, max(0, int(n) - W):].reshape(-1))
+        assert np.array_equal(got, np.concatenate(parts)), f"window {W}: != last-W slice of the full pack"
+
+
+def pin_window_roundtrip(impl):
+    """Windowed unpack into another page size, windowed pack back: same words;
+    only the window's slots change in the destination."""
+    for P2, W in ((16, 20), (64, 33), (5, 1), (48, 64)):
+        wl = make_workload("tiny", seed=6, dst_page_size=P2)
+        src = host_src_pool(wl)
+        first = impl.pack_layer(src, 0, wl.block_tables, wl.seq_lens, window=W)
+        dst0 = host_dst_prefill(wl)
+        dst = impl.unpack_layer(first.copy(), dst0.copy(), 0, wl.dst_block_tables, wl.seq_lens, window=W)
+        again = impl.pack_layer(dst, 0, wl.dst_block_tables, wl.seq_lens, window=W)
+        assert np.array_equal(first, again), f"windowed round trip differs (P'={P2}, W={W})"
+        m = np.zeros(dst.shape, dtype=bool)
+        for r, n in enumerate(wl.seq_lens):
+            for t in range(max(0, int(n) - W), int(n)):
+                m[0, wl.dst_block_tables[r][t // P2], :, t % P2] = True
+        assert np.array_equal(dst[~m], dst0[~m]), f"windowed unpack touched other slots (P'={P2}, W={W})"
+
+
+def pin_layer_kind_sizes(impl):
+    """Section 2.2: the 2026-model figures (Kimi K2 MLA, gpt-oss-120b with 18
+    window-capped layers) from packed bytes summed over every layer."""
+    for model, full_l, win_l, W, C, H, D, s, printed in read_golden("layer_kinds.txt"):
+        full_l, win_l, W, C, H, D, s = map(int, (full_l, win_l, W, C, H, D, s))
+        k = _pages(s, 16)
+        pool = np.zeros((1, k, C, 16, H, D), dtype=np.uint16)
+        bt = np.arange(k, dtype=np.int32)[None, :]
+        lens = np.array([s], dtype=np.int32)
+        total = full_l * impl.pack_layer(pool, 0, bt, lens).nbytes
+        total += win_l * impl.pack_layer(pool, 0, bt, lens, window=W).nbytes
+        eq1 = C * H * D * 2 * (full_l * s + win_l * min(s, W))
+        assert total == eq1, f"{model}: {total} B != per-kind Eq. 1 {eq1} B"
+        decimals = len(printed.split(".")[1])
+        assert any(math.isclose(round(total / u, decimals), float(printed), abs_tol=1e-12)
+                   for u in (1e9, 2.0 ** 30)), f"{model}: {total} B does not round to {printed} GB"
+
+
 QUICK_PINS = [pin_mla_ratio, pin_bruteforce_tiny, pin_page_take_transpose, pin_request_concat,
-              pin_roundtrip, pin_multiset, pin_zero_and_opaque]
-FULL_PINS = QUICK_PINS + [pin_table1_sizes, pin_eq1_workloads]
+              pin_roundtrip, pin_multiset, pin_zero_and_opaque, pin_window_slice, pin_window_roundtrip]
+FULL_PINS = QUICK_PINS + [pin_table1_sizes, pin_eq1_workloads, pin_layer_kind_sizes]
 
 
 def failing_pins(impl, pins=QUICK_PINS):
