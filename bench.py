@@ -70,14 +70,27 @@ def parse():
     return ap.parse_args()
 
 
-def step_bytes(wl):
-    """Algorithmic bytes of one pack launch and one unpack launch (one layer)."""
-    import numpy as np
+def layer_bytes(wl, layer):
+    """Algorithmic bytes of layer `layer`'s pack launch and unpack launch:
+    read + write of the kept tokens' rows, 4 B per table entry covering them
+    (P of the pool being read or written), 4 B per length."""
     row = wl.num_heads * wl.head_dim * wl.elem_bytes
-    moved = wl.planes * int(wl.seq_lens.astype(np.int64).sum()) * row
-    pages = sum(-(-int(n) // wl.page_size) for n in wl.seq_lens)
-    pages2 = sum(-(-int(n) // wl.dst_page_size) for n in wl.seq_lens)
+    W = wl.window(layer)
+    kept = moved = pages = pages2 = 0
+    for n in (int(x) for x in wl.seq_lens):
+        s = n - W if 0 < W < n else 0
+        kept += n - s
+        if n > s:
+            pages += (n - 1) // wl.page_size - s // wl.page_size + 1
+            pages2 += (n - 1) // wl.dst_page_size - s // wl.dst_page_size + 1
+    moved = wl.planes * kept * row
     return 2 * moved + 4 * pages + 4 * wl.num_reqs, 2 * moved + 4 * pages2 + 4 * wl.num_reqs
+
+
+def step_bytes(wl):
+    """Algorithmic bytes of one pack and one unpack launch, averaged over layers."""
+    per = [layer_bytes(wl, l) for l in range(wl.num_layers)]
+    return (sum(p for p, _ in per) // wl.num_layers, sum(u for _, u in per) // wl.num_layers)
 
 
 def read_traffic(workload):
@@ -118,18 +131,18 @@ def cpu_baseline(wl, src, dst, budget_s):
     def to_host_words(t):   # device bf16 slab -> host uint16 words, bit-exact
         return t.view(torch.int16).cpu().numpy().view(np.uint16)
 
-    pack_b, unpack_b = step_bytes(wl)
     slabs = list(range(min(wl.phys_layers, 4)))
     host = {s: (to_host_words(src[s])[None], to_host_words(dst[s])[None]) for s in slabs}
     done_bytes, spent, layers = 0, 0.0, 0
     while spent < budget_s and layers < 10_000:
         s = slabs[layers % len(slabs)]
         src_h, dst_h = host[s]
+        W = wl.window(layers % wl.num_layers)
         t0 = time.perf_counter()
-        packed = oracle.pack_layer(src_h, 0, wl.block_tables, wl.seq_lens)
-        oracle.unpack_layer(packed, dst_h, 0, wl.dst_block_tables, wl.seq_lens)
+        packed = oracle.pack_layer(src_h, 0, wl.block_tables, wl.seq_lens, window=W)
+        oracle.unpack_layer(packed, dst_h, 0, wl.dst_block_tables, wl.seq_lens, window=W)
         spent += time.perf_counter() - t0
-        done_bytes += pack_b + unpack_b
+        done_bytes += sum(layer_bytes(wl, layers % wl.num_layers))
         layers += 1
     cpu = "unknown"
     try:
@@ -175,13 +188,13 @@ def run(args):
         for l in range(L):
             e = evs[l] if evs else (None, None)
             if direction == 0:
-                calls.append(topkv.prepare_pack_layer_batched_ex(
-                    src, l % wl.phys_layers, R, bt, bt.shape[1], lens, packed[l % ring], stream=on,
-                    start=e[0], stop=e[1]))
+                calls.append(topkv.prepare_pack_layer_window(
+                    src, l % wl.phys_layers, R, bt, bt.shape[1], lens, wl.window(l), packed[l % ring],
+                    stream=on, start=e[0], stop=e[1]))
             else:
-                calls.append(topkv.prepare_unpack_layer_batched_ex(
-                    packed[l % ring], dst, l % wl.phys_layers, R, bt2, bt2.shape[1], lens, stream=on,
-                    start=e[0], stop=e[1]))
+                calls.append(topkv.prepare_unpack_layer_window(
+                    packed[l % ring], dst, l % wl.phys_layers, R, bt2, bt2.shape[1], lens, wl.window(l),
+                    stream=on, start=e[0], stop=e[1]))
         return calls
 
     def run_calls(calls):
@@ -228,12 +241,14 @@ def run(args):
     sweep_us = [1e3 * sum(marks[k][d].elapsed_ms(marks[k][d + 1]) for k in range(args.steps)) for d in (0, 1)]
     log(f"[bench] {args.steps} timed steps: {wall_ms:.3f} ms on the GPU clock, {host_s * 1e3:.3f} ms host")
 
-    pack_b, unpack_b = step_bytes(wl)
-    bytes_step = L * (pack_b + unpack_b)
+    per_layer = [layer_bytes(wl, l) for l in range(L)]
+    dir_bytes = [sum(b[d] for b in per_layer) for d in (0, 1)]     # one sweep
+    bytes_step = dir_bytes[0] + dir_bytes[1]
     kern = {}
-    for d, name, b in ((0, "pack", pack_b), (1, "unpack", unpack_b)):
+    for d, name in ((0, "pack"), (1, "unpack")):
         us = sweep_us[d] / (args.steps * L)
-        kern[name] = {"bytes_per_launch": b, "avg_us": round(us, 3), "gbs": round(b / us / 1e3, 1),
+        b = dir_bytes[d] / L
+        kern[name] = {"bytes_per_launch": int(round(b)), "avg_us": round(us, 3), "gbs": round(b / us / 1e3, 1),
                       "launches": args.steps * L}
 
     if args.kernel_events:

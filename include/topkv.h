@@ -99,9 +99,11 @@ typedef struct topkv_launch {
   hipEvent_t  stop;
 } topkv_launch_t;
 
-/* Largest num_reqs one batched launch accepts (the per-request prefix sums
- * live in LDS: 8 bytes per request).  Larger batches: split into launches. */
-#define TOPKV_MAX_BATCH_REQS 8000
+/* Largest num_reqs one batched launch accepts (per-request prefix sums live
+ * in LDS: 12 bytes per request).  Larger batches: split into launches.  A
+ * launch's token capacity, num_reqs * bt_stride * page_size, must also stay
+ * below 2^31 (TOPKV_ERR_UNSUPPORTED otherwise). */
+#define TOPKV_MAX_BATCH_REQS 4096
 
 /* Pack one request's tokens of one layer (Sections 5.2, 3.5, 6).
  *   src:         pool to read (device memory described by *src, host struct)
@@ -158,12 +160,35 @@ topkv_status_t topkv_unpack_layer_batched_ex(const void* src, int64_t src_bytes,
                                              int32_t bt_stride, const int32_t* seq_lens,
                                              const topkv_launch_t* launch);
 
+/* Windowed layers (Section 2.2 extends Eq. 1 per layer kind: a sliding-
+ * window attention layer holds only its last `window` tokens).  As the
+ * batched calls, but only tokens [max(0, n_r - window), n_r) of request r
+ * move; window 0 moves every token (identical to the batched calls).  The
+ * packed block of request r is [planes][min(n_r, window)][heads][dim];
+ * unpack writes those tokens at their own positions t (page t / P', slot
+ * t % P') and nothing else.  window < 0 is TOPKV_ERR_INVALID_ARG.
+ * launch must be non-null. */
+topkv_status_t topkv_pack_layer_window(const topkv_pool_t* src, int32_t layer, int32_t num_reqs,
+                                       const int32_t* block_tables, int32_t bt_stride,
+                                       const int32_t* seq_lens, int32_t window, void* dst,
+                                       int64_t dst_bytes, const topkv_launch_t* launch);
+topkv_status_t topkv_unpack_layer_window(const void* src, int64_t src_bytes,
+                                         const topkv_pool_t* dst, int32_t layer, int32_t num_reqs,
+                                         const int32_t* block_tables, int32_t bt_stride,
+                                         const int32_t* seq_lens, int32_t window,
+                                         const topkv_launch_t* launch);
+
 /* Bytes of one layer's packed batch, planes * row_bytes * sum(seq_lens),
  * computed on the host from HOST seq_lens (Eq. 1 for one layer; planes = 1
  * for MLA per Section 5.3).  Returns -1 for a null/invalid pool, a null
  * seq_lens with num_reqs > 0, a negative length or int64 overflow. */
 int64_t topkv_packed_layer_bytes(const topkv_pool_t* pool, const int32_t* seq_lens_host,
                                  int32_t num_reqs);
+
+/* The same for a windowed layer: planes * row_bytes * sum(min(n_r, window))
+ * (window 0: every token).  -1 also for window < 0. */
+int64_t topkv_packed_window_bytes(const topkv_pool_t* pool, const int32_t* seq_lens_host,
+                                  int32_t num_reqs, int32_t window);
 
 /* Checked path: validate block tables and lengths on the device before a
  * pack or unpack (the movement calls skip bad entries silently).  For every

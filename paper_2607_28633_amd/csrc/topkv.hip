@@ -80,16 +80,36 @@ struct MoveParams {
   int32_t n_single;           // tokens of the single request when seq_lens is null
   int32_t tiles_per_plane;    // ceil(plane_bytes / tile bytes)
   int32_t batched;            // 1: lengths come from device seq_lens
+  int32_t window;             // > 0: only the last `window` tokens of each request move
+  int32_t pad_;
 };
+
+// First token a windowed layer keeps (window 0 keeps all): the last
+// `window` tokens of a request of n tokens.
+__device__ __forceinline__ int64_t window_start(int64_t n, int32_t window) {
+  return (window > 0 && n > window) ? n - window : 0;
+}
 
 __device__ __forceinline__ int32_t uniform(int32_t x) { return __builtin_amdgcn_readfirstlane(x); }
 
-// Exclusive prefix sums over requests of (clamped) token counts and of page
-// counts, written to LDS: tok[r], pg[r] for r < R, totals at index R.
-// Tokens ride in the high and pages in the low 32 bits of one 64-bit value,
-// so a single wave64 shuffle scan produces both.
+// Two small words that every lane needs, fetched as vector loads issued back
+// to back (vector loads retire in order, so one wait covers both), then
+// broadcast from lane 0.  Scalar loads of the same words would be waited on
+// one at a time, since scalar loads may complete out of order.
+__device__ __forceinline__ void load_pair(const int32_t* a, const int32_t* b, int32_t* va, int32_t* vb) {
+  const int32_t x = __builtin_nontemporal_load(a);
+  const int32_t y = __builtin_nontemporal_load(b);
+  *va = uniform(x);
+  *vb = uniform(y);
+}
+
+// Exclusive prefix sums over requests of kept token counts (lengths clamped,
+// then cut to the window) and of the pages those tokens occupy, written to
+// LDS: tok[r], pg[r] for r < R with totals at index R, and each request's
+// first kept token in st[r].  Tokens ride in the high and pages in the low
+// 32 bits of one 64-bit value, so a single wave64 shuffle scan yields both.
 __device__ void request_prefix(const MoveParams& p, const int32_t* __restrict__ seq_lens, int32_t* tok,
-                               int32_t* pg, uint64_t* wsum) {
+                               int32_t* pg, int32_t* st, uint64_t* wsum) {
   const int lane = threadIdx.x & 63;
   const int wave = threadIdx.x >> 6;
   const int64_t max_tok = (int64_t)p.bt_stride * p.page_size;
@@ -100,8 +120,11 @@ __device__ void request_prefix(const MoveParams& p, const int32_t* __restrict__ 
     if (r < p.num_reqs) {
       int64_t n = seq_lens[r];
       n = n < 0 ? 0 : (n > max_tok ? max_tok : n);
-      const uint64_t pages = (uint64_t)((n + p.page_size - 1) / p.page_size);
-      v = ((uint64_t)n << 32) | pages;
+      const int64_t start = window_start(n, p.window);
+      const int64_t cnt = n - start;
+      const uint64_t pages = cnt > 0 ? (uint64_t)((n - 1) / p.page_size - start / p.page_size + 1) : 0;
+      v = ((uint64_t)cnt << 32) | pages;
+      st[r] = (int32_t)start;
     }
     uint64_t x = v;
 #pragma unroll
@@ -190,67 +213,71 @@ __device__ __forceinline__ void copy_tile(char* __restrict__ dst, const char* __
   store_tile<VB, VPT>(dst, v, len / VB);
 }
 
-// Sum of the (clamped) lengths of requests [0, r): the token offset of
-// request r in the packed batch.  Block-wide; every thread must call it.
-__device__ __forceinline__ int64_t tokens_before(const int32_t* __restrict__ seq_lens, int32_t r,
-                                                 int64_t max_tok, int64_t* red) {
-  int64_t s = 0;
-  for (int j = threadIdx.x; j < r; j += kThreads) {
-    const int64_t n = seq_lens[j];
-    s += n < 0 ? 0 : (n > max_tok ? max_tok : n);
+// Sum of the kept token counts of requests [0, r): the token offset of
+// request r in the packed batch.  Each wave computes it on its own (lanes
+// stride over the lengths, then a butterfly of 32-bit shuffles), so no LDS
+// and no barrier are involved.  The host keeps one launch's token capacity
+// (num_reqs * bt_stride * page_size) below 2^31, so 32 bits suffice.
+__device__ __forceinline__ int32_t tokens_before(const int32_t* __restrict__ seq_lens, int32_t r,
+                                                 int32_t max_tok, int32_t window) {
+  int32_t s = 0;
+  for (int j = threadIdx.x & 63; j < r; j += 64) {
+    int32_t n = seq_lens[j];
+    n = n < 0 ? 0 : (n > max_tok ? max_tok : n);
+    s += (window > 0 && n > window) ? window : n;
   }
 #pragma unroll
   for (int off = 32; off > 0; off >>= 1) s += __shfl_xor(s, off, 64);
-  if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = s;
-  __syncthreads();
-  int64_t t = 0;
-#pragma unroll
-  for (int w = 0; w < kWaves; ++w) t += red[w];
-  return t;
+  return uniform(s);
 }
 
 // Direct mapping: one workgroup per (request, table entry, plane, tile)
-// slot, w = ((r * bt_stride + i) * planes + c) * tiles_per_plane + k, so the
-// slot's lengths and page index are two independent scalar loads issued at
-// once; slots past a request's last page exit.  The token offset of the
-// request is a block sum over the earlier lengths.  For pack the pool loads
-// are issued before that sum, so they overlap it.  Used when the slot count
-// is small enough for a one-shot grid.
-template <int VB, bool kPack, bool kBatched>
+// slot, read straight from a 3-D grid (z, y, x) = (r, i, c * tiles + k), so the
+// slot's length and page index are independent scalar loads issued at once,
+// next to the loads of the earlier lengths that give the request's token
+// offset; slots past a request's last page exit.  Used when the slot count is
+// small enough for a one-shot grid.
+template <int VB, int VPT, bool kPack, bool kBatched>
 __device__ __forceinline__ void move_direct(char* __restrict__ pool, char* __restrict__ packed,
                                             const int32_t* __restrict__ tables,
                                             const int32_t* __restrict__ seq_lens, const MoveParams& p) {
-  constexpr int VPT = TOPKV_VPT;
   constexpr int32_t kTile = kThreads * VPT * VB;
-  __shared__ int64_t red[kWaves];
-  const uint32_t per_page = (uint32_t)(p.planes * p.tiles_per_plane);
-  const uint32_t per_req = (uint32_t)p.bt_stride * per_page;
-  const uint32_t w = blockIdx.x;
-  const int32_t r = (int32_t)(w / per_req);
-  const uint32_t rem = w - (uint32_t)r * per_req;
-  const int32_t i = (int32_t)(rem / per_page);
-  const uint32_t rem2 = rem - (uint32_t)i * per_page;
-  const int32_t c = (int32_t)(rem2 / (uint32_t)p.tiles_per_plane);
-  const int32_t k = (int32_t)(rem2 - (uint32_t)c * p.tiles_per_plane);
-  const int64_t max_tok = (int64_t)p.bt_stride * p.page_size;
+  // grid: z = request, y = table entry, x = plane * tiles_per_plane + tile
+  const int32_t r = blockIdx.z;
+  const int32_t i = blockIdx.y;
+  const int32_t c = (int32_t)(blockIdx.x / (uint32_t)p.tiles_per_plane);
+  const int32_t k = (int32_t)(blockIdx.x - (uint32_t)c * p.tiles_per_plane);
+  const int32_t max_tok = p.bt_stride * p.page_size;   // < 2^31 (host check)
 
-  const int32_t page = tables[(int64_t)r * p.bt_stride + i];
-  int64_t n = kBatched ? (int64_t)seq_lens[r] : (int64_t)p.n_single;
+  // This slot's table entry and length, loaded together.
+  int32_t page, n;
+  if (kBatched) {
+    load_pair(tables + (int64_t)r * p.bt_stride + i, seq_lens + r, &page, &n);
+  } else {
+    page = tables[(int64_t)r * p.bt_stride + i];
+    n = p.n_single;
+  }
   n = n < 0 ? 0 : (n > max_tok ? max_tok : n);
-  const int32_t first = i * p.page_size;
-  const int64_t rows = n - first < p.page_size ? n - first : p.page_size;
-  const int64_t run = rows * p.row_bytes;
-  const int64_t start = (int64_t)k * kTile;
-  const bool live = rows > 0 && start < run && page >= 0 && (int64_t)page < p.num_pages;
-  const int32_t nv = live ? (int32_t)((run - start < kTile ? run - start : kTile) / VB) : 0;
-  char* pool_ptr = pool + (int64_t)page * p.page_bytes + (int64_t)c * p.plane_bytes + start;
-
-  typename Vec<VB>::type v[VPT];
-  if (kPack && live) load_tile<VB, VPT>(v, pool_ptr, nv);
-  const int64_t tok0 = (kBatched && r > 0) ? tokens_before(seq_lens, r, max_tok, red) : 0;
+  const int32_t start = (p.window > 0 && n > p.window) ? n - p.window : 0;   // first kept token
+  const int32_t cnt = n - start;
+  const int32_t first = i * p.page_size;              // page i holds tokens [first, first + P)
+  const int32_t lo = first > start ? first : start;
+  const int32_t hi = first + p.page_size < n ? first + p.page_size : n;
+  const int64_t run = (int64_t)(hi - lo) * p.row_bytes;
+  const int64_t tstart = (int64_t)k * kTile;
+  // bitwise, not short-circuit: keeps the table load ahead of the first branch
+  const bool live = (hi > lo) & (tstart < run) & (page >= 0) & ((int64_t)page < p.num_pages);
   if (!live) return;
-  if ((tok0 + n) * p.planes * p.row_bytes > p.packed_cap) return;
-  char* packed_ptr = packed + ((tok0 * p.planes + (int64_t)c * n + first) * p.row_bytes + start);
+  const int32_t nv = (int32_t)((run - tstart < kTile ? run - tstart : kTile) / VB);
+  char* pool_ptr = pool + (int64_t)page * p.page_bytes + (int64_t)c * p.plane_bytes +
+                   (int64_t)(lo - first) * p.row_bytes + tstart;
+  typename Vec<VB>::type v[VPT];
+  // Pack: the pool loads go out before the token offset is known (their
+  // addresses do not depend on it), so the offset sum overlaps them.
+  if (kPack) load_tile<VB, VPT>(v, pool_ptr, nv);
+  const int32_t tok0 = (kBatched && r > 0) ? tokens_before(seq_lens, r, max_tok, p.window) : 0;
+  if (((int64_t)tok0 + cnt) * p.planes * p.row_bytes > p.packed_cap) return;
+  char* packed_ptr = packed + (((int64_t)tok0 * p.planes + (int64_t)c * cnt + (lo - start)) * p.row_bytes + tstart);
   if (kPack) {
     store_tile<VB, VPT>(packed_ptr, v, nv);
   } else {
@@ -265,24 +292,26 @@ __device__ __forceinline__ void move_direct(char* __restrict__ pool, char* __res
 // binary search.  Work is spread evenly however long the requests are.
 // pool: pool base already offset to the layer; packed: packed buffer base;
 // tables: [num_reqs][bt_stride]; seq_lens: device [num_reqs] (batched only).
-template <int VB, bool kPack>
+template <int VB, int VPT, bool kPack>
 __device__ __forceinline__ void move_strided(char* __restrict__ pool, char* __restrict__ packed,
                                            const int32_t* __restrict__ tables,
                                            const int32_t* __restrict__ seq_lens, const MoveParams& p) {
-  constexpr int VPT = TOPKV_VPT;
   constexpr int64_t kTile = (int64_t)kThreads * VPT * VB;
   extern __shared__ uint64_t lds_u64[];
   uint64_t* wsum = lds_u64;                                      // [kWaves]
   int32_t* tok = reinterpret_cast<int32_t*>(lds_u64 + kWaves);   // [num_reqs + 1]
   int32_t* pg = tok + (p.num_reqs + 1);                          // [num_reqs + 1]
+  int32_t* st = pg + (p.num_reqs + 1);                           // [num_reqs + 1]
 
   const bool batched = p.batched != 0;
   int32_t total_pages;
+  const int64_t single_start = window_start(p.n_single, p.window);
   if (batched) {
-    request_prefix(p, seq_lens, tok, pg, wsum);
+    request_prefix(p, seq_lens, tok, pg, st, wsum);
     total_pages = pg[p.num_reqs];
   } else {
-    total_pages = (p.n_single + p.page_size - 1) / p.page_size;
+    total_pages = p.n_single > single_start
+                      ? (int32_t)((p.n_single - 1) / p.page_size - single_start / p.page_size + 1) : 0;
   }
   // the host guarantees pages * planes * tiles_per_plane < 2^31
   const uint32_t per_page = (uint32_t)(p.planes * p.tiles_per_plane);
@@ -293,7 +322,9 @@ __device__ __forceinline__ void move_strided(char* __restrict__ pool, char* __re
     const int32_t rem = (int32_t)(w - (uint32_t)g * per_page);
     const int32_t c = uniform(rem / p.tiles_per_plane);
     const int32_t k = uniform(rem - c * p.tiles_per_plane);
-    int32_t r = 0, tok0 = 0, n = p.n_single, i = g;
+    int32_t r = 0, tok0 = 0;
+    int64_t start = single_start, cnt = p.n_single - single_start;
+    int32_t i = (int32_t)(start / p.page_size) + g;
     if (batched) {
       int lo = 0, hi = p.num_reqs - 1;   // largest r with pg[r] <= g
       while (lo < hi) {
@@ -302,22 +333,25 @@ __device__ __forceinline__ void move_strided(char* __restrict__ pool, char* __re
       }
       r = uniform(lo);
       tok0 = uniform(tok[r]);
-      n = uniform(tok[r + 1] - tok0);
-      i = uniform(g - pg[r]);
+      cnt = uniform(tok[r + 1] - tok0);
+      start = uniform(st[r]);
+      i = uniform((int32_t)(start / p.page_size) + g - pg[r]);
     }
-    const int32_t first = i * p.page_size;
-    const int32_t rows = min(p.page_size, n - first);
-    const int64_t run = (int64_t)rows * p.row_bytes;
-    const int64_t start = (int64_t)k * kTile;
-    if (start >= run) continue;
-    const int64_t req_end = ((int64_t)tok0 + n) * p.planes * p.row_bytes;
+    const int64_t n = start + cnt;
+    const int64_t first = (int64_t)i * p.page_size;
+    const int64_t lo_t = first > start ? first : start;
+    const int64_t hi_t = first + p.page_size < n ? first + p.page_size : n;
+    const int64_t run = (hi_t - lo_t) * p.row_bytes;
+    const int64_t tstart = (int64_t)k * kTile;
+    if (tstart >= run) continue;
+    const int64_t req_end = ((int64_t)tok0 + cnt) * p.planes * p.row_bytes;
     if (req_end > p.packed_cap) continue;
     const int32_t page = tables[(int64_t)r * p.bt_stride + i];
     if (page < 0 || (int64_t)page >= p.num_pages) continue;
-    const int32_t len = (int32_t)(run - start < kTile ? run - start : kTile);
-    char* pool_ptr = pool + (int64_t)page * p.page_bytes + (int64_t)c * p.plane_bytes + start;
-    char* packed_ptr = packed +
-        (((int64_t)tok0 * p.planes + (int64_t)c * n + first) * p.row_bytes + start);
+    const int32_t len = (int32_t)(run - tstart < kTile ? run - tstart : kTile);
+    char* pool_ptr = pool + (int64_t)page * p.page_bytes + (int64_t)c * p.plane_bytes + (lo_t - first) * p.row_bytes +
+                     tstart;
+    char* packed_ptr = packed + (((int64_t)tok0 * p.planes + (int64_t)c * cnt + (lo_t - start)) * p.row_bytes + tstart);
     if (kPack) copy_tile<VB, VPT>(packed_ptr, pool_ptr, len);
     else copy_tile<VB, VPT>(pool_ptr, packed_ptr, len);
   }
@@ -327,20 +361,22 @@ __device__ __forceinline__ void move_strided(char* __restrict__ pool, char* __re
 // a host-side length, 2 = direct grid for a batch with device lengths.
 enum { kStrided = 0, kDirectSingle = 1, kDirectBatched = 2 };
 
-template <int VB, int kMode>
+// VB: bytes per vector (16 on the fast path); VPT: vectors per lane per tile,
+// so a tile is kThreads * VPT * VB bytes (chosen per launch to fit a page plane).
+template <int VB, int VPT, int kMode>
 __global__ __launch_bounds__(kThreads) void kv_pack_kernel(char* __restrict__ pool, char* __restrict__ packed,
                                                            const int32_t* __restrict__ tables,
                                                            const int32_t* __restrict__ seq_lens, MoveParams p) {
-  if (kMode == kStrided) move_strided<VB, true>(pool, packed, tables, seq_lens, p);
-  else move_direct<VB, true, kMode == kDirectBatched>(pool, packed, tables, seq_lens, p);
+  if (kMode == kStrided) move_strided<VB, VPT, true>(pool, packed, tables, seq_lens, p);
+  else move_direct<VB, VPT, true, kMode == kDirectBatched>(pool, packed, tables, seq_lens, p);
 }
 
-template <int VB, int kMode>
+template <int VB, int VPT, int kMode>
 __global__ __launch_bounds__(kThreads) void kv_unpack_kernel(char* __restrict__ pool, char* __restrict__ packed,
                                                              const int32_t* __restrict__ tables,
                                                              const int32_t* __restrict__ seq_lens, MoveParams p) {
-  if (kMode == kStrided) move_strided<VB, false>(pool, packed, tables, seq_lens, p);
-  else move_direct<VB, false, kMode == kDirectBatched>(pool, packed, tables, seq_lens, p);
+  if (kMode == kStrided) move_strided<VB, VPT, false>(pool, packed, tables, seq_lens, p);
+  else move_direct<VB, VPT, false, kMode == kDirectBatched>(pool, packed, tables, seq_lens, p);
 }
 
 // ---------------------------------------------------------------------------
@@ -401,20 +437,42 @@ int vector_bytes(uintptr_t a, uintptr_t b, int64_t row) {
 
 typedef void (*KernelFn)(char*, char*, const int32_t*, const int32_t*, MoveParams);
 
+template <int VB, int VPT, int kMode>
+KernelFn kernel_for(bool pack) {
+  return pack ? kv_pack_kernel<VB, VPT, kMode> : kv_unpack_kernel<VB, VPT, kMode>;
+}
+
 template <int kMode>
-KernelFn pick_kernel_mode(bool pack, int vb) {
+KernelFn pick_kernel_mode(bool pack, int vb, int vpt) {
   switch (vb) {
-    case 16: return pack ? kv_pack_kernel<16, kMode> : kv_unpack_kernel<16, kMode>;
-    case 8: return pack ? kv_pack_kernel<8, kMode> : kv_unpack_kernel<8, kMode>;
-    case 4: return pack ? kv_pack_kernel<4, kMode> : kv_unpack_kernel<4, kMode>;
-    case 2: return pack ? kv_pack_kernel<2, kMode> : kv_unpack_kernel<2, kMode>;
-    default: return pack ? kv_pack_kernel<1, kMode> : kv_unpack_kernel<1, kMode>;
+    case 16:
+      if (vpt == TOPKV_VPT) return kernel_for<16, TOPKV_VPT, kMode>(pack);
+      switch (vpt) {
+        case 8: return kernel_for<16, 8, kMode>(pack);
+        case 4: return kernel_for<16, 4, kMode>(pack);
+        case 2: return kernel_for<16, 2, kMode>(pack);
+        default: return kernel_for<16, 1, kMode>(pack);
+      }
+    case 8: return kernel_for<8, TOPKV_VPT, kMode>(pack);
+    case 4: return kernel_for<4, TOPKV_VPT, kMode>(pack);
+    case 2: return kernel_for<2, TOPKV_VPT, kMode>(pack);
+    default: return kernel_for<1, TOPKV_VPT, kMode>(pack);
   }
 }
 
-KernelFn pick_kernel(bool pack, int vb, bool direct, bool batched) {
-  if (!direct) return pick_kernel_mode<kStrided>(pack, vb);
-  return batched ? pick_kernel_mode<kDirectBatched>(pack, vb) : pick_kernel_mode<kDirectSingle>(pack, vb);
+KernelFn pick_kernel(bool pack, int vb, int vpt, bool direct, bool batched) {
+  if (!direct) return pick_kernel_mode<kStrided>(pack, vb, vpt);
+  return batched ? pick_kernel_mode<kDirectBatched>(pack, vb, vpt) : pick_kernel_mode<kDirectSingle>(pack, vb, vpt);
+}
+
+// Vectors per lane for 16-byte vectors: the largest of TOPKV_VPT, 4, 2, 1
+// whose tile still fits in one page plane, so small planes (e.g. 16 KiB for
+// 1 KiB rows in 16-token pages) get full tiles instead of half-empty ones.
+int vectors_per_lane(int vb, int64_t plane_bytes) {
+  if (vb != 16) return TOPKV_VPT;
+  for (int v = TOPKV_VPT; v > 1; v >>= 1)
+    if ((int64_t)kThreads * v * 16 <= plane_bytes) return v;
+  return 1;
 }
 
 // Shared launcher for the four movement entry points.
@@ -422,20 +480,21 @@ KernelFn pick_kernel(bool pack, int vb, bool direct, bool batched) {
 //   seq_lens: device lengths (batched) or null (single request of n_single)
 topkv_status_t launch_move(bool pack, const topkv_pool_t* pool, int32_t layer, void* packed,
                            int64_t packed_cap, int32_t num_reqs, const int32_t* tables,
-                           int32_t bt_stride, const int32_t* seq_lens, int32_t n_single,
+                           int32_t bt_stride, const int32_t* seq_lens, int32_t n_single, int32_t window,
                            const topkv_launch_t* launch) {
   Geometry g;
   topkv_status_t st = pool_geometry(pool, layer, &g);
   if (st != TOPKV_OK) return st;
   if (!launch) return TOPKV_ERR_INVALID_ARG;
-  if (num_reqs < 0 || n_single < 0 || packed_cap < 0) return TOPKV_ERR_INVALID_ARG;
+  if (num_reqs < 0 || n_single < 0 || packed_cap < 0 || window < 0) return TOPKV_ERR_INVALID_ARG;
   if (num_reqs > TOPKV_MAX_BATCH_REQS) return TOPKV_ERR_UNSUPPORTED;
   if (num_reqs == 0 || (!seq_lens && n_single == 0)) return TOPKV_OK;  // nothing to move
   if (!tables || !packed || bt_stride <= 0) return TOPKV_ERR_INVALID_ARG;
 
   const int vb = vector_bytes(reinterpret_cast<uintptr_t>(pool->base),
                               reinterpret_cast<uintptr_t>(packed), g.row_bytes);
-  const int64_t tile = (int64_t)kThreads * TOPKV_VPT * vb;
+  const int vpt = vectors_per_lane(vb, g.plane_bytes);
+  const int64_t tile = (int64_t)kThreads * vpt * vb;
   const int64_t tpp = (g.plane_bytes + tile - 1) / tile;
   int64_t per_page, max_pages, work;
   if (seq_lens) {
@@ -444,17 +503,21 @@ topkv_status_t launch_move(bool pack, const topkv_pool_t* pool, int32_t layer, v
     max_pages = ((int64_t)n_single + pool->page_size - 1) / pool->page_size;
     if (max_pages > bt_stride) return TOPKV_ERR_INVALID_ARG;
   }
+  // one launch's token capacity (requests x table width x page size) must stay below 2^31
+  const int64_t tok_cap = (seq_lens ? (int64_t)num_reqs : 1) * bt_stride * (int64_t)pool->page_size;
   if (__builtin_mul_overflow(tpp, (int64_t)pool->planes, &per_page) || per_page > INT32_MAX ||
-      __builtin_mul_overflow(max_pages, per_page, &work) || work > INT32_MAX ||
-      (int64_t)bt_stride * pool->page_size > INT32_MAX)
+      __builtin_mul_overflow(max_pages, per_page, &work) || work > INT32_MAX || tok_cap > INT32_MAX)
     return TOPKV_ERR_UNSUPPORTED;
 
   // Direct mapping when every (request, table entry, plane, tile) slot can
   // get its own workgroup; otherwise a persistent grid over the live items.
-  const int64_t slots = (seq_lens ? (int64_t)num_reqs : 1) * bt_stride * per_page;
-  const bool direct = slots <= TOPKV_DIRECT_MAX;
-  unsigned grid;
+  const int64_t reqs = seq_lens ? (int64_t)num_reqs : 1;
+  const int64_t slots = reqs * bt_stride * per_page;
+  const bool direct = slots <= TOPKV_DIRECT_MAX && bt_stride <= 65535 && reqs <= 65535;
+  dim3 grid3;
+  unsigned grid = 0;
   if (direct) {
+    grid3 = dim3((unsigned)per_page, (unsigned)bt_stride, (unsigned)reqs);
     grid = (unsigned)slots;
   } else {
     int cus = 0;
@@ -462,6 +525,7 @@ topkv_status_t launch_move(bool pack, const topkv_pool_t* pool, int32_t layer, v
     if (st != TOPKV_OK) return st;
     const int64_t cap = (int64_t)cus * TOPKV_WG_PER_CU;
     grid = (unsigned)(work < cap ? work : cap);
+    grid3 = dim3(grid);
   }
   if (grid == 0) return TOPKV_OK;
 
@@ -480,17 +544,19 @@ topkv_status_t launch_move(bool pack, const topkv_pool_t* pool, int32_t layer, v
   p.n_single = n_single;
   p.tiles_per_plane = (int32_t)tpp;
   p.batched = seq_lens ? 1 : 0;
+  p.window = window;
+  p.pad_ = 0;
 
-  const size_t lds = (seq_lens && !direct) ? sizeof(uint64_t) * kWaves + sizeof(int32_t) * 2 * ((size_t)num_reqs + 1)
+  const size_t lds = (seq_lens && !direct) ? sizeof(uint64_t) * kWaves + sizeof(int32_t) * 3 * ((size_t)num_reqs + 1)
                                            : 0;
   void* args[] = {&pool_ptr, &packed_ptr, &tables, &seq_lens, &p};
-  const void* fn = reinterpret_cast<const void*>(pick_kernel(pack, vb, direct, seq_lens != nullptr));
+  const void* fn = reinterpret_cast<const void*>(pick_kernel(pack, vb, vpt, direct, seq_lens != nullptr));
   hipError_t e;
   if (launch->start || launch->stop)
-    e = hipExtLaunchKernel(fn, dim3(grid), dim3(kThreads), args, lds, launch->stream, launch->start,
+    e = hipExtLaunchKernel(fn, grid3, dim3(kThreads), args, lds, launch->stream, launch->start,
                            launch->stop, 0);
   else
-    e = hipLaunchKernel(fn, dim3(grid), dim3(kThreads), args, lds, launch->stream);
+    e = hipLaunchKernel(fn, grid3, dim3(kThreads), args, lds, launch->stream);
   return e == hipSuccess ? TOPKV_OK : TOPKV_ERR_LAUNCH;
 }
 
@@ -517,7 +583,7 @@ topkv_status_t topkv_pack_layer(const topkv_pool_t* src, int32_t layer, const in
   const int64_t cap = topkv::single_bytes(src, seq_len);
   if (cap < 0 || pages > INT32_MAX) return TOPKV_ERR_UNSUPPORTED;
   return topkv::launch_move(true, src, layer, dst, cap, 1, block_table, (int32_t)(pages > 0 ? pages : 1),
-                            nullptr, seq_len, &l);
+                            nullptr, seq_len, 0, &l);
 }
 
 topkv_status_t topkv_unpack_layer(const void* src, const topkv_pool_t* dst, int32_t layer,
@@ -528,25 +594,39 @@ topkv_status_t topkv_unpack_layer(const void* src, const topkv_pool_t* dst, int3
   const int64_t cap = topkv::single_bytes(dst, seq_len);
   if (cap < 0 || pages > INT32_MAX) return TOPKV_ERR_UNSUPPORTED;
   return topkv::launch_move(false, dst, layer, const_cast<void*>(src), cap, 1, block_table,
-                            (int32_t)(pages > 0 ? pages : 1), nullptr, seq_len, &l);
+                            (int32_t)(pages > 0 ? pages : 1), nullptr, seq_len, 0, &l);
+}
+
+topkv_status_t topkv_pack_layer_window(const topkv_pool_t* src, int32_t layer, int32_t num_reqs,
+                                       const int32_t* block_tables, int32_t bt_stride, const int32_t* seq_lens,
+                                       int32_t window, void* dst, int64_t dst_bytes, const topkv_launch_t* launch) {
+  if (num_reqs > 0 && !seq_lens) return TOPKV_ERR_INVALID_ARG;
+  return topkv::launch_move(true, src, layer, dst, dst_bytes, num_reqs, block_tables, bt_stride,
+                            num_reqs > 0 ? seq_lens : nullptr, 0, window, launch);
+}
+
+topkv_status_t topkv_unpack_layer_window(const void* src, int64_t src_bytes, const topkv_pool_t* dst, int32_t layer,
+                                         int32_t num_reqs, const int32_t* block_tables, int32_t bt_stride,
+                                         const int32_t* seq_lens, int32_t window, const topkv_launch_t* launch) {
+  if (num_reqs > 0 && !seq_lens) return TOPKV_ERR_INVALID_ARG;
+  return topkv::launch_move(false, dst, layer, const_cast<void*>(src), src_bytes, num_reqs, block_tables,
+                            bt_stride, num_reqs > 0 ? seq_lens : nullptr, 0, window, launch);
 }
 
 topkv_status_t topkv_pack_layer_batched_ex(const topkv_pool_t* src, int32_t layer, int32_t num_reqs,
                                            const int32_t* block_tables, int32_t bt_stride,
                                            const int32_t* seq_lens, void* dst, int64_t dst_bytes,
                                            const topkv_launch_t* launch) {
-  if (num_reqs > 0 && !seq_lens) return TOPKV_ERR_INVALID_ARG;
-  return topkv::launch_move(true, src, layer, dst, dst_bytes, num_reqs, block_tables, bt_stride,
-                            num_reqs > 0 ? seq_lens : nullptr, 0, launch);
+  return topkv_pack_layer_window(src, layer, num_reqs, block_tables, bt_stride, seq_lens, 0, dst, dst_bytes,
+                                 launch);
 }
 
 topkv_status_t topkv_unpack_layer_batched_ex(const void* src, int64_t src_bytes, const topkv_pool_t* dst,
                                              int32_t layer, int32_t num_reqs,
                                              const int32_t* block_tables, int32_t bt_stride,
                                              const int32_t* seq_lens, const topkv_launch_t* launch) {
-  if (num_reqs > 0 && !seq_lens) return TOPKV_ERR_INVALID_ARG;
-  return topkv::launch_move(false, dst, layer, const_cast<void*>(src), src_bytes, num_reqs, block_tables,
-                            bt_stride, num_reqs > 0 ? seq_lens : nullptr, 0, launch);
+  return topkv_unpack_layer_window(src, src_bytes, dst, layer, num_reqs, block_tables, bt_stride, seq_lens, 0,
+                                   launch);
 }
 
 topkv_status_t topkv_pack_layer_batched(const topkv_pool_t* src, int32_t layer, int32_t num_reqs,
@@ -567,9 +647,9 @@ topkv_status_t topkv_unpack_layer_batched(const void* src, int64_t src_bytes, co
                                        seq_lens, &l);
 }
 
-int64_t topkv_packed_layer_bytes(const topkv_pool_t* pool, const int32_t* seq_lens_host,
-                                 int32_t num_reqs) {
-  if (!pool || num_reqs < 0 || (num_reqs > 0 && !seq_lens_host)) return -1;
+int64_t topkv_packed_window_bytes(const topkv_pool_t* pool, const int32_t* seq_lens_host, int32_t num_reqs,
+                                  int32_t window) {
+  if (!pool || num_reqs < 0 || window < 0 || (num_reqs > 0 && !seq_lens_host)) return -1;
   if (pool->planes <= 0 || pool->num_heads <= 0 || pool->head_dim <= 0 || pool->elem_bytes <= 0) return -1;
   int64_t per_token;
   if (__builtin_mul_overflow((int64_t)pool->planes * pool->num_heads, (int64_t)pool->head_dim * pool->elem_bytes,
@@ -577,13 +657,17 @@ int64_t topkv_packed_layer_bytes(const topkv_pool_t* pool, const int32_t* seq_le
     return -1;
   int64_t total = 0;
   for (int32_t r = 0; r < num_reqs; ++r) {
-    if (seq_lens_host[r] < 0) return -1;
+    const int64_t n = seq_lens_host[r];
+    if (n < 0) return -1;
+    const int64_t kept = (window > 0 && n > window) ? window : n;
     int64_t b;
-    if (__builtin_mul_overflow(per_token, (int64_t)seq_lens_host[r], &b) ||
-        __builtin_add_overflow(total, b, &total))
-      return -1;
+    if (__builtin_mul_overflow(per_token, kept, &b) || __builtin_add_overflow(total, b, &total)) return -1;
   }
   return total;
+}
+
+int64_t topkv_packed_layer_bytes(const topkv_pool_t* pool, const int32_t* seq_lens_host, int32_t num_reqs) {
+  return topkv_packed_window_bytes(pool, seq_lens_host, num_reqs, 0);
 }
 
 const char* topkv_status_string(topkv_status_t status) {

@@ -31,13 +31,14 @@ TOPKV_ERR_UNSUPPORTED = 2
 TOPKV_ERR_LAUNCH = 3
 TOPKV_ERR_BOUNDS = 4
 TOPKV_ERR_DEVICE = 5
-TOPKV_MAX_BATCH_REQS = 8000
+TOPKV_MAX_BATCH_REQS = 4096
 TOPKV_CHECK_RESULT_WORDS = 4
 
 EXPORTS = ["topkv_pack_layer", "topkv_unpack_layer", "topkv_pack_layer_batched",
            "topkv_unpack_layer_batched", "topkv_pack_layer_batched_ex",
            "topkv_unpack_layer_batched_ex", "topkv_packed_layer_bytes", "topkv_status_string",
-           "topkv_check_tables", "topkv_check_workspace_bytes"]
+           "topkv_check_tables", "topkv_check_workspace_bytes", "topkv_pack_layer_window",
+           "topkv_unpack_layer_window", "topkv_packed_window_bytes"]
 
 
 class topkv_pool_t(ctypes.Structure):
@@ -68,6 +69,11 @@ _SIGS = {
     "topkv_status_string": (ctypes.c_char_p, [_I32]),
     "topkv_check_tables": (_I32, [_POOL, _I32, _P, _I32, _P, _I32, _P, _I64, _P, _P]),
     "topkv_check_workspace_bytes": (_I64, [_POOL]),
+    "topkv_pack_layer_window": (_I32, [_POOL, _I32, _I32, _P, _I32, _P, _I32, _P, _I64,
+                                       ctypes.POINTER(topkv_launch_t)]),
+    "topkv_unpack_layer_window": (_I32, [_P, _I64, _POOL, _I32, _I32, _P, _I32, _P, _I32,
+                                         ctypes.POINTER(topkv_launch_t)]),
+    "topkv_packed_window_bytes": (_I64, [_POOL, ctypes.POINTER(_I32), _I32, _I32]),
 }
 for _name, (_res, _args) in _SIGS.items():
     _fn = getattr(_lib, _name)
@@ -186,6 +192,28 @@ def topkv_unpack_layer_batched_ex(src, dst, layer, num_reqs, block_tables, bt_st
                                               int(bt_stride), _table_ptr(seq_lens), ctypes.byref(launch)))
 
 
+def topkv_pack_layer_window(src, layer, num_reqs, block_tables, bt_stride, seq_lens, window, dst,
+                            dst_bytes=None, stream=None, start=None, stop=None) -> None:
+    launch = topkv_launch_t(_stream(stream), _event(start), _event(stop))
+    _check(_lib.topkv_pack_layer_window(ctypes.byref(_pool_arg(src)), int(layer), int(num_reqs),
+                                        _table_ptr(block_tables), int(bt_stride), _table_ptr(seq_lens), int(window),
+                                        _ptr(dst), _nbytes(dst, dst_bytes), ctypes.byref(launch)))
+
+
+def topkv_unpack_layer_window(src, dst, layer, num_reqs, block_tables, bt_stride, seq_lens, window,
+                              src_bytes=None, stream=None, start=None, stop=None) -> None:
+    launch = topkv_launch_t(_stream(stream), _event(start), _event(stop))
+    _check(_lib.topkv_unpack_layer_window(_ptr(src), _nbytes(src, src_bytes), ctypes.byref(_pool_arg(dst)),
+                                          int(layer), int(num_reqs), _table_ptr(block_tables), int(bt_stride),
+                                          _table_ptr(seq_lens), int(window), ctypes.byref(launch)))
+
+
+def topkv_packed_window_bytes(pool, seq_lens_host, window) -> int:
+    lens = [int(x) for x in seq_lens_host]
+    arr = (_I32 * max(1, len(lens)))(*lens)
+    return int(_lib.topkv_packed_window_bytes(ctypes.byref(_pool_arg(pool)), arr, len(lens), int(window)))
+
+
 def topkv_packed_layer_bytes(pool, seq_lens_host) -> int:
     lens = [int(x) for x in seq_lens_host]
     arr = (_I32 * max(1, len(lens)))(*lens)
@@ -275,21 +303,33 @@ class PreparedCall:
             raise TopkvError(st)
 
 
-def prepare_pack_layer_batched_ex(src, layer, num_reqs, block_tables, bt_stride, seq_lens, dst,
-                                  dst_bytes=None, stream=None, start=None, stop=None) -> PreparedCall:
+def prepare_pack_layer_window(src, layer, num_reqs, block_tables, bt_stride, seq_lens, window, dst,
+                              dst_bytes=None, stream=None, start=None, stop=None) -> PreparedCall:
     pool = _pool_arg(src)
     launch = topkv_launch_t(_stream(stream), _event(start), _event(stop))
     args = (ctypes.byref(pool), _I32(int(layer)), _I32(int(num_reqs)), _P(_table_ptr(block_tables)),
-            _I32(int(bt_stride)), _P(_table_ptr(seq_lens)), _P(_ptr(dst)), _I64(_nbytes(dst, dst_bytes)),
-            ctypes.byref(launch))
-    return PreparedCall("topkv_pack_layer_batched_ex", args, (pool, launch))
+            _I32(int(bt_stride)), _P(_table_ptr(seq_lens)), _I32(int(window)), _P(_ptr(dst)),
+            _I64(_nbytes(dst, dst_bytes)), ctypes.byref(launch))
+    return PreparedCall("topkv_pack_layer_window", args, (pool, launch))
+
+
+def prepare_unpack_layer_window(src, dst, layer, num_reqs, block_tables, bt_stride, seq_lens, window,
+                                src_bytes=None, stream=None, start=None, stop=None) -> PreparedCall:
+    pool = _pool_arg(dst)
+    launch = topkv_launch_t(_stream(stream), _event(start), _event(stop))
+    args = (_P(_ptr(src)), _I64(_nbytes(src, src_bytes)), ctypes.byref(pool), _I32(int(layer)),
+            _I32(int(num_reqs)), _P(_table_ptr(block_tables)), _I32(int(bt_stride)), _P(_table_ptr(seq_lens)),
+            _I32(int(window)), ctypes.byref(launch))
+    return PreparedCall("topkv_unpack_layer_window", args, (pool, launch))
+
+
+def prepare_pack_layer_batched_ex(src, layer, num_reqs, block_tables, bt_stride, seq_lens, dst,
+                                  dst_bytes=None, stream=None, start=None, stop=None) -> PreparedCall:
+    return prepare_pack_layer_window(src, layer, num_reqs, block_tables, bt_stride, seq_lens, 0, dst,
+                                     dst_bytes, stream, start, stop)
 
 
 def prepare_unpack_layer_batched_ex(src, dst, layer, num_reqs, block_tables, bt_stride, seq_lens,
                                     src_bytes=None, stream=None, start=None, stop=None) -> PreparedCall:
-    pool = _pool_arg(dst)
-    launch = topkv_launch_t(_stream(stream), _event(start), _event(stop))
-    args = (_P(_ptr(src)), _I64(_nbytes(src, src_bytes)), ctypes.byref(pool), _I32(int(layer)),
-            _I32(int(num_reqs)), _P(_table_ptr(block_tables)), _I32(int(bt_stride)),
-            _P(_table_ptr(seq_lens)), ctypes.byref(launch))
-    return PreparedCall("topkv_unpack_layer_batched_ex", args, (pool, launch))
+    return prepare_unpack_layer_window(src, dst, layer, num_reqs, block_tables, bt_stride, seq_lens, 0,
+                                       src_bytes, stream, start, stop)

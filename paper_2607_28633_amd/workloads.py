@@ -64,6 +64,10 @@ class Workload:
     seq_lens: np.ndarray     # int32 [R]
     block_tables: np.ndarray       # int32 [R, max_pages_src]
     dst_block_tables: np.ndarray   # int32 [R, max_pages_dst]
+    layer_windows: tuple = ()      # per logical layer: 0 = full attention, W > 0 = last-W-token window
+
+    def window(self, layer: int) -> int:
+        return int(self.layer_windows[layer]) if self.layer_windows else 0
 
     @property
     def num_reqs(self) -> int:
@@ -90,6 +94,7 @@ class Workload:
             "dst_page_size": self.dst_page_size, "pool_pages": self.num_pages,
             "dst_pool_pages": self.dst_num_pages, "requests": self.num_reqs,
             "tokens": int(self.seq_lens.astype(np.int64).sum()),
+            "windowed_layers": sum(1 for w in self.layer_windows if w),
         }
 
 
@@ -128,10 +133,11 @@ WORKLOADS = {
     "llama3-70b-batch8": "80 layers, 8 KV heads, head_dim 128, page 16, 8 requests (4096 + 7 x U[1024,8192]), pools 1.25x pages",
     "deepseek-v3-mla": "61 layers, 1 x 576 latent (no K/V split), page 64, 32 requests lognormal(median 4096, sigma 1) in [512,16384], pools 1.25x pages",
     "reblock-70b": "80 layers, 8 KV heads, head_dim 128, page 16 -> 64, 100 requests lognormal(median 4096, sigma 1) in [256,32768], pools 1.25x pages, 8 physical layer slabs",
+    "gpt-oss-120b": "36 layers alternating 128-token sliding window / full attention, 8 KV heads, head_dim 64, page 16, 32 requests lognormal(median 4096, sigma 1) in [512,16384], pools 1.25x pages",
 }
 
 DEFAULT_SEEDS = {"tiny": 0, "llama3-8b": 1, "llama3-70b-batch8": 2, "deepseek-v3-mla": 3,
-                 "reblock-70b": 4, "llama3-70b-4k": 5}
+                 "reblock-70b": 4, "llama3-70b-4k": 5, "gpt-oss-120b": 6}
 
 
 def make_workload(name: str, seed: Optional[int] = None, *,
@@ -165,6 +171,10 @@ def make_workload(name: str, seed: Optional[int] = None, *,
         shape = dict(L=61, C=1, H=1, D=576, P=64, P2=64)
         lens = _lognormal_lengths(rng, 32, 4096, 1.0, 512, 16384)
         pools = None
+    elif name == "gpt-oss-120b":
+        shape = dict(L=36, C=2, H=8, D=64, P=16, P2=16)
+        lens = _lognormal_lengths(rng, 32, 4096, 1.0, 512, 16384)
+        pools = None
     else:  # reblock-70b
         shape = dict(L=80, C=2, H=8, D=128, P=16, P2=64)
         lens = _lognormal_lengths(rng, 100, 4096, 1.0, 256, 32768)
@@ -194,10 +204,11 @@ def make_workload(name: str, seed: Optional[int] = None, *,
 
     bt = _tables(rng, lens, P, np_src)
     bt2 = _tables(rng, lens, P2, np_dst)
+    windows = tuple(128 if l % 2 == 0 else 0 for l in range(L)) if name == "gpt-oss-120b" else ()
     return Workload(name=name, seed=seed, num_layers=L, phys_layers=int(phys_layers),
                     planes=C, num_heads=H, head_dim=D, elem_bytes=int(elem_bytes),
                     page_size=P, num_pages=np_src, dst_page_size=P2, dst_num_pages=np_dst,
-                    seq_lens=lens, block_tables=bt, dst_block_tables=bt2)
+                    seq_lens=lens, block_tables=bt, dst_block_tables=bt2, layer_windows=windows)
 
 
 def bf16_bits_from_f32(x: np.ndarray) -> np.ndarray:
