@@ -65,6 +65,9 @@ def parse():
                     help="issue each sweep as L host launches, or replay it as a captured HIP graph")
     ap.add_argument("--kernel-events", action="store_true",
                     help="also time every launch with its own kernel-timestamp events (diagnostic)")
+    ap.add_argument("--mode", choices=["layers", "kvcache1"], default="layers",
+                    help="layers: per-layer pack/unpack sweep (the headline); kvcache1: whole-request "
+                         "serialization (pack every layer into a KVCACHE1 blob, seal, verify, unpack)")
     ap.add_argument("--calib-copy-bytes", type=int, default=0,
                     help="instead of the workload, run a plain device copy of this many bytes")
     return ap.parse_args()
@@ -317,6 +320,65 @@ def run(args):
     print(json.dumps(out), flush=True)
 
 
+def run_kvcache1(args):
+    """Whole-request serialization of request 0 (Section 3.5 KVCACHE1 format):
+    per step, pack every layer into the blob, seal (CRC-64 of K and V + header),
+    verify on the receiving side, unpack every layer into the decode pool."""
+    import torch
+
+    from paper_2607_28633_amd import topkv
+    from paper_2607_28633_amd.workloads import WORKLOADS, device_dst_prefill, device_src_pool, make_workload
+
+    torch.cuda.set_device(0)
+    wl = make_workload(args.workload)
+    if wl.phys_layers != wl.num_layers:
+        raise SystemExit("kvcache1 mode needs one pool slab per layer")
+    src, dst = device_src_pool(wl), device_dst_prefill(wl)
+    n = int(wl.seq_lens[0])
+    bt = torch.from_numpy(wl.block_tables[0].copy()).cuda()
+    bt2 = torch.from_numpy(wl.dst_block_tables[0].copy()).cuda()
+    geo = topkv.pool_from_tensor(src)
+    nbytes = topkv.topkv_kvcache1_bytes(geo, n)
+    blob = torch.empty(nbytes, dtype=torch.uint8, device="cuda")
+    ws = torch.empty(topkv.topkv_kvcache1_workspace_bytes(geo, n) // 8, dtype=torch.int64, device="cuda")
+    res = torch.empty(4, dtype=torch.int32, device="cuda")
+    stream = torch.cuda.current_stream()
+    L = wl.num_layers
+    phases = {
+        "pack_layers": lambda: [topkv.topkv_kvcache1_pack_layer(src, l, bt, n, blob, stream=stream) for l in range(L)],
+        "seal": lambda: topkv.topkv_kvcache1_seal(geo, n, 1, 2, blob, ws, stream=stream),
+        "verify": lambda: topkv.topkv_kvcache1_verify(geo, n, 1, 2, blob, ws, res, stream=stream),
+        "unpack_layers": lambda: [topkv.topkv_kvcache1_unpack_layer(blob, dst, l, bt2, n, stream=stream)
+                                  for l in range(L)],
+    }
+    for _ in range(args.warmup):
+        for f in phases.values():
+            f()
+    torch.cuda.synchronize()
+    marks = [[topkv.HipEvent() for _ in range(len(phases) + 1)] for _ in range(args.steps)]
+    for k in range(args.steps):
+        marks[k][0].record(stream)
+        for j, f in enumerate(phases.values()):
+            f()
+            marks[k][j + 1].record(stream)
+    marks[-1][-1].synchronize()
+    ok = res.cpu().tolist()[0] == topkv.TOPKV_OK
+    body = nbytes - 128
+    moved = {"pack_layers": 2 * body, "seal": body, "verify": body, "unpack_layers": 2 * body}
+    out_ph = {}
+    for j, name in enumerate(phases):
+        us = 1e3 * sum(marks[k][j].elapsed_ms(marks[k][j + 1]) for k in range(args.steps)) / args.steps
+        out_ph[name] = {"us": round(us, 2), "bytes": moved[name], "gbs": round(moved[name] / us / 1e3, 1)}
+    total_us = 1e3 * marks[0][0].elapsed_ms(marks[-1][-1]) / args.steps
+    print(json.dumps({
+        "metric": "KVCACHE1 whole-request serialize + verify + deserialize GB/s", "mode": "kvcache1",
+        "value": round(sum(moved.values()) / total_us / 1e3, 1), "unit": "GB/s", "n_gpus": 1,
+        "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(total_us / 1e3, 4),
+        "higher_is_better": True, "dtype": "bf16", "data": "synthetic", "verified": ok,
+        "config": {"workload": f"{wl.name}: {WORKLOADS[wl.name]}", "request_tokens": n, "blob_bytes": nbytes},
+        "phases": out_ph}), flush=True)
+
+
 def main():
     args = parse()
     world = int(os.environ.get("WORLD_SIZE", "1"))
@@ -326,6 +388,8 @@ def main():
         sys.exit(2)
     if args.calib_copy_bytes:
         calib_copy(args)
+    elif args.mode == "kvcache1":
+        run_kvcache1(args)
     else:
         run(args)
 

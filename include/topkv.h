@@ -73,7 +73,8 @@ typedef enum topkv_status {
   TOPKV_ERR_UNSUPPORTED = 2,  /* valid but beyond the library's limits (see each call) */
   TOPKV_ERR_LAUNCH = 3,       /* the HIP runtime refused the launch */
   TOPKV_ERR_BOUNDS = 4,       /* topkv_check_tables found an invalid table or length */
-  TOPKV_ERR_DEVICE = 5        /* a HIP runtime query failed */
+  TOPKV_ERR_DEVICE = 5,       /* a HIP runtime query failed */
+  TOPKV_ERR_CHECKSUM = 6      /* topkv_kvcache1_verify: header or checksum mismatch */
 } topkv_status_t;
 
 /* One paged KV pool.  The caller owns the memory.  All counts are elements
@@ -189,6 +190,85 @@ int64_t topkv_packed_layer_bytes(const topkv_pool_t* pool, const int32_t* seq_le
  * (window 0: every token).  -1 also for window < 0. */
 int64_t topkv_packed_window_bytes(const topkv_pool_t* pool, const int32_t* seq_lens_host,
                                   int32_t num_reqs, int32_t window);
+
+/* One request with caller-placed planes: plane c of the packed request
+ * (c < planes) is written to / read from dst + c * plane_stride as
+ * [n][heads][dim] rows (plane_stride > 0; 16-byte multiples keep the wide
+ * path).  With plane_stride = tensor bytes this writes one layer's K and V
+ * rows straight into the K and V tensors of a serialized request
+ * (Section 3.5).  dst_bytes / src_bytes: bytes available from dst / src;
+ * the last plane must end within it, or nothing is moved. */
+topkv_status_t topkv_pack_layer_planes(const topkv_pool_t* src, int32_t layer,
+                                       const int32_t* block_table, int32_t seq_len, void* dst,
+                                       int64_t plane_stride, int64_t dst_bytes, hipStream_t stream);
+topkv_status_t topkv_unpack_layer_planes(const void* src, int64_t plane_stride, int64_t src_bytes,
+                                         const topkv_pool_t* dst, int32_t layer,
+                                         const int32_t* block_table, int32_t seq_len,
+                                         hipStream_t stream);
+
+/* ---- Whole-request serialization: KVCACHE1 (Section 3.5) --------------------
+ * A blob is a 128-byte header followed by the K tensor and the V tensor,
+ * each [layers][seq_len][kv_heads][head_dim] (the V tensor is empty for an
+ * MLA cache, planes = 1, Section 5.3).  The paper fixes the fields but not
+ * their widths, byte order or the CRC; this library writes, little-endian:
+ *   0 "KVCACHE1"   8 request_id u64   16 model_id u64
+ *   24 seq_len u32 28 layers u32      32 kv_heads u32   36 head_dim u32
+ *   40 elem_bytes u32                 44 planes u32
+ *   48 k_bytes u64 56 v_bytes u64     64 crc64(K) u64   72 crc64(V) u64
+ *   80..127 zero
+ * CRC-64/XZ: ECMA-182 polynomial 0x42F0E1EBA9EA3693, reflected, preset and
+ * final complement all ones (CRC of "123456789" = 0x995DC9BBDF1939FA).
+ * The pool descriptor gives the geometry (all num_layers layers go in the
+ * blob); rows must be a multiple of 16 bytes and the blob 16-byte aligned
+ * (TOPKV_ERR_UNSUPPORTED otherwise).  Typical sender: topkv_kvcache1_pack_
+ * layer for each layer as it is produced, then topkv_kvcache1_seal; receiver:
+ * topkv_kvcache1_verify, then topkv_kvcache1_unpack_layer per layer. */
+
+/* Blob bytes for seq_len tokens (128 + planes * layers * seq_len * row); -1
+ * for bad geometry. */
+int64_t topkv_kvcache1_bytes(const topkv_pool_t* geometry, int32_t seq_len);
+
+/* Workspace bytes seal / verify need (checksum partials); -1 on bad input. */
+int64_t topkv_kvcache1_workspace_bytes(const topkv_pool_t* geometry, int32_t seq_len);
+
+/* Pack layer `layer` of one request into its rows of the blob's K and V
+ * tensors (one launch; block_table as for topkv_pack_layer). */
+topkv_status_t topkv_kvcache1_pack_layer(const topkv_pool_t* src, int32_t layer,
+                                         const int32_t* block_table, int32_t seq_len, void* blob,
+                                         int64_t blob_bytes, hipStream_t stream);
+
+/* After every layer is packed: checksum both tensors on the device and write
+ * the header.  workspace: topkv_kvcache1_workspace_bytes() bytes of device
+ * memory owned by the caller (contents on return are scratch).  Queued on
+ * stream; the blob is complete once the stream reaches this point. */
+topkv_status_t topkv_kvcache1_seal(const topkv_pool_t* geometry, int32_t seq_len,
+                                   uint64_t request_id, uint64_t model_id, void* blob,
+                                   int64_t blob_bytes, void* workspace, int64_t workspace_bytes,
+                                   hipStream_t stream);
+
+/* Receiver check: recompute both checksums and compare them, and the header
+ * fields, with what the caller expects.  result: device int32[4] written on
+ * the stream: [0] TOPKV_OK or TOPKV_ERR_CHECKSUM, [1] bit mask of header
+ * words 0-7 that differ, [2] K checksum mismatch, [3] V checksum mismatch.
+ * A mismatch is the paper's trigger for a retry. */
+topkv_status_t topkv_kvcache1_verify(const topkv_pool_t* geometry, int32_t seq_len,
+                                     uint64_t request_id, uint64_t model_id, const void* blob,
+                                     int64_t blob_bytes, void* workspace, int64_t workspace_bytes,
+                                     int32_t* result, hipStream_t stream);
+
+/* Scatter layer `layer` of a blob into a pool (any page size; the blob's
+ * geometry is the pool descriptor's, seq_len tokens). */
+topkv_status_t topkv_kvcache1_unpack_layer(const void* blob, int64_t blob_bytes,
+                                           const topkv_pool_t* dst, int32_t layer,
+                                           const int32_t* block_table, int32_t seq_len,
+                                           hipStream_t stream);
+
+/* CRC-64/XZ (as above) of nbytes of device memory at data (16-byte aligned,
+ * any length), written to the device word *crc_out on the stream.
+ * workspace: topkv_crc64_workspace_bytes(nbytes) bytes, caller-owned. */
+topkv_status_t topkv_crc64(const void* data, int64_t nbytes, void* workspace,
+                           int64_t workspace_bytes, uint64_t* crc_out, hipStream_t stream);
+int64_t topkv_crc64_workspace_bytes(int64_t nbytes);
 
 /* Checked path: validate block tables and lengths on the device before a
  * pack or unpack (the movement calls skip bad entries silently).  For every

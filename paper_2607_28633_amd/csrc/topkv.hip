@@ -82,6 +82,7 @@ struct MoveParams {
   int32_t batched;            // 1: lengths come from device seq_lens
   int32_t window;             // > 0: only the last `window` tokens of each request move
   int32_t pad_;
+  int64_t plane_stride;       // single request only: > 0 places plane c at packed + c * plane_stride
 };
 
 // First token a windowed layer keeps (window 0 keeps all): the last
@@ -276,8 +277,16 @@ __device__ __forceinline__ void move_direct(char* __restrict__ pool, char* __res
   // addresses do not depend on it), so the offset sum overlaps them.
   if (kPack) load_tile<VB, VPT>(v, pool_ptr, nv);
   const int32_t tok0 = (kBatched && r > 0) ? tokens_before(seq_lens, r, max_tok, p.window) : 0;
-  if (((int64_t)tok0 + cnt) * p.planes * p.row_bytes > p.packed_cap) return;
-  char* packed_ptr = packed + (((int64_t)tok0 * p.planes + (int64_t)c * cnt + (lo - start)) * p.row_bytes + tstart);
+  int64_t plane_off, end;
+  if (!kBatched && p.plane_stride > 0) {          // caller-placed planes (one request)
+    plane_off = (int64_t)c * p.plane_stride;
+    end = (int64_t)(p.planes - 1) * p.plane_stride + (int64_t)cnt * p.row_bytes;
+  } else {
+    plane_off = ((int64_t)tok0 * p.planes + (int64_t)c * cnt) * p.row_bytes;
+    end = ((int64_t)tok0 + cnt) * p.planes * p.row_bytes;
+  }
+  if (end > p.packed_cap) return;
+  char* packed_ptr = packed + plane_off + (int64_t)(lo - start) * p.row_bytes + tstart;
   if (kPack) {
     store_tile<VB, VPT>(packed_ptr, v, nv);
   } else {
@@ -344,14 +353,18 @@ __device__ __forceinline__ void move_strided(char* __restrict__ pool, char* __re
     const int64_t run = (hi_t - lo_t) * p.row_bytes;
     const int64_t tstart = (int64_t)k * kTile;
     if (tstart >= run) continue;
-    const int64_t req_end = ((int64_t)tok0 + cnt) * p.planes * p.row_bytes;
+    const bool placed = !batched && p.plane_stride > 0;   // caller-placed planes (one request)
+    const int64_t req_end = placed ? (int64_t)(p.planes - 1) * p.plane_stride + cnt * p.row_bytes
+                                   : ((int64_t)tok0 + cnt) * p.planes * p.row_bytes;
     if (req_end > p.packed_cap) continue;
     const int32_t page = tables[(int64_t)r * p.bt_stride + i];
     if (page < 0 || (int64_t)page >= p.num_pages) continue;
     const int32_t len = (int32_t)(run - tstart < kTile ? run - tstart : kTile);
     char* pool_ptr = pool + (int64_t)page * p.page_bytes + (int64_t)c * p.plane_bytes + (lo_t - first) * p.row_bytes +
                      tstart;
-    char* packed_ptr = packed + (((int64_t)tok0 * p.planes + (int64_t)c * cnt + (lo_t - start)) * p.row_bytes + tstart);
+    const int64_t plane_off = placed ? (int64_t)c * p.plane_stride
+                                     : ((int64_t)tok0 * p.planes + (int64_t)c * cnt) * p.row_bytes;
+    char* packed_ptr = packed + plane_off + (lo_t - start) * p.row_bytes + tstart;
     if (kPack) copy_tile<VB, VPT>(packed_ptr, pool_ptr, len);
     else copy_tile<VB, VPT>(pool_ptr, packed_ptr, len);
   }
@@ -481,18 +494,19 @@ int vectors_per_lane(int vb, int64_t plane_bytes) {
 topkv_status_t launch_move(bool pack, const topkv_pool_t* pool, int32_t layer, void* packed,
                            int64_t packed_cap, int32_t num_reqs, const int32_t* tables,
                            int32_t bt_stride, const int32_t* seq_lens, int32_t n_single, int32_t window,
-                           const topkv_launch_t* launch) {
+                           int64_t plane_stride, const topkv_launch_t* launch) {
   Geometry g;
   topkv_status_t st = pool_geometry(pool, layer, &g);
   if (st != TOPKV_OK) return st;
   if (!launch) return TOPKV_ERR_INVALID_ARG;
-  if (num_reqs < 0 || n_single < 0 || packed_cap < 0 || window < 0) return TOPKV_ERR_INVALID_ARG;
+  if (num_reqs < 0 || n_single < 0 || packed_cap < 0 || window < 0 || plane_stride < 0) return TOPKV_ERR_INVALID_ARG;
+  if (plane_stride > 0 && seq_lens) return TOPKV_ERR_INVALID_ARG;   // placed planes: one request only
   if (num_reqs > TOPKV_MAX_BATCH_REQS) return TOPKV_ERR_UNSUPPORTED;
   if (num_reqs == 0 || (!seq_lens && n_single == 0)) return TOPKV_OK;  // nothing to move
   if (!tables || !packed || bt_stride <= 0) return TOPKV_ERR_INVALID_ARG;
 
-  const int vb = vector_bytes(reinterpret_cast<uintptr_t>(pool->base),
-                              reinterpret_cast<uintptr_t>(packed), g.row_bytes);
+  int vb = vector_bytes(reinterpret_cast<uintptr_t>(pool->base), reinterpret_cast<uintptr_t>(packed), g.row_bytes);
+  while (plane_stride % vb) vb >>= 1;             // placed planes keep every run vector-aligned
   const int vpt = vectors_per_lane(vb, g.plane_bytes);
   const int64_t tile = (int64_t)kThreads * vpt * vb;
   const int64_t tpp = (g.plane_bytes + tile - 1) / tile;
@@ -546,6 +560,7 @@ topkv_status_t launch_move(bool pack, const topkv_pool_t* pool, int32_t layer, v
   p.batched = seq_lens ? 1 : 0;
   p.window = window;
   p.pad_ = 0;
+  p.plane_stride = plane_stride;
 
   const size_t lds = (seq_lens && !direct) ? sizeof(uint64_t) * kWaves + sizeof(int32_t) * 3 * ((size_t)num_reqs + 1)
                                            : 0;
@@ -583,7 +598,7 @@ topkv_status_t topkv_pack_layer(const topkv_pool_t* src, int32_t layer, const in
   const int64_t cap = topkv::single_bytes(src, seq_len);
   if (cap < 0 || pages > INT32_MAX) return TOPKV_ERR_UNSUPPORTED;
   return topkv::launch_move(true, src, layer, dst, cap, 1, block_table, (int32_t)(pages > 0 ? pages : 1),
-                            nullptr, seq_len, 0, &l);
+                            nullptr, seq_len, 0, 0, &l);
 }
 
 topkv_status_t topkv_unpack_layer(const void* src, const topkv_pool_t* dst, int32_t layer,
@@ -594,7 +609,29 @@ topkv_status_t topkv_unpack_layer(const void* src, const topkv_pool_t* dst, int3
   const int64_t cap = topkv::single_bytes(dst, seq_len);
   if (cap < 0 || pages > INT32_MAX) return TOPKV_ERR_UNSUPPORTED;
   return topkv::launch_move(false, dst, layer, const_cast<void*>(src), cap, 1, block_table,
-                            (int32_t)(pages > 0 ? pages : 1), nullptr, seq_len, 0, &l);
+                            (int32_t)(pages > 0 ? pages : 1), nullptr, seq_len, 0, 0, &l);
+}
+
+topkv_status_t topkv_pack_layer_planes(const topkv_pool_t* src, int32_t layer, const int32_t* block_table,
+                                       int32_t seq_len, void* dst, int64_t plane_stride, int64_t dst_bytes,
+                                       hipStream_t stream) {
+  if (!src || seq_len < 0 || plane_stride <= 0) return TOPKV_ERR_INVALID_ARG;
+  const topkv_launch_t l = {stream, nullptr, nullptr};
+  const int64_t pages = src->page_size > 0 ? ((int64_t)seq_len + src->page_size - 1) / src->page_size : 0;
+  if (pages > INT32_MAX) return TOPKV_ERR_UNSUPPORTED;
+  return topkv::launch_move(true, src, layer, dst, dst_bytes, 1, block_table, (int32_t)(pages > 0 ? pages : 1),
+                            nullptr, seq_len, 0, plane_stride, &l);
+}
+
+topkv_status_t topkv_unpack_layer_planes(const void* src, int64_t plane_stride, int64_t src_bytes,
+                                         const topkv_pool_t* dst, int32_t layer, const int32_t* block_table,
+                                         int32_t seq_len, hipStream_t stream) {
+  if (!dst || seq_len < 0 || plane_stride <= 0) return TOPKV_ERR_INVALID_ARG;
+  const topkv_launch_t l = {stream, nullptr, nullptr};
+  const int64_t pages = dst->page_size > 0 ? ((int64_t)seq_len + dst->page_size - 1) / dst->page_size : 0;
+  if (pages > INT32_MAX) return TOPKV_ERR_UNSUPPORTED;
+  return topkv::launch_move(false, dst, layer, const_cast<void*>(src), src_bytes, 1, block_table,
+                            (int32_t)(pages > 0 ? pages : 1), nullptr, seq_len, 0, plane_stride, &l);
 }
 
 topkv_status_t topkv_pack_layer_window(const topkv_pool_t* src, int32_t layer, int32_t num_reqs,
@@ -602,7 +639,7 @@ topkv_status_t topkv_pack_layer_window(const topkv_pool_t* src, int32_t layer, i
                                        int32_t window, void* dst, int64_t dst_bytes, const topkv_launch_t* launch) {
   if (num_reqs > 0 && !seq_lens) return TOPKV_ERR_INVALID_ARG;
   return topkv::launch_move(true, src, layer, dst, dst_bytes, num_reqs, block_tables, bt_stride,
-                            num_reqs > 0 ? seq_lens : nullptr, 0, window, launch);
+                            num_reqs > 0 ? seq_lens : nullptr, 0, window, 0, launch);
 }
 
 topkv_status_t topkv_unpack_layer_window(const void* src, int64_t src_bytes, const topkv_pool_t* dst, int32_t layer,
@@ -610,7 +647,7 @@ topkv_status_t topkv_unpack_layer_window(const void* src, int64_t src_bytes, con
                                          const int32_t* seq_lens, int32_t window, const topkv_launch_t* launch) {
   if (num_reqs > 0 && !seq_lens) return TOPKV_ERR_INVALID_ARG;
   return topkv::launch_move(false, dst, layer, const_cast<void*>(src), src_bytes, num_reqs, block_tables,
-                            bt_stride, num_reqs > 0 ? seq_lens : nullptr, 0, window, launch);
+                            bt_stride, num_reqs > 0 ? seq_lens : nullptr, 0, window, 0, launch);
 }
 
 topkv_status_t topkv_pack_layer_batched_ex(const topkv_pool_t* src, int32_t layer, int32_t num_reqs,
@@ -678,6 +715,7 @@ const char* topkv_status_string(topkv_status_t status) {
     case TOPKV_ERR_LAUNCH: return "TOPKV_ERR_LAUNCH: the HIP runtime refused the kernel launch";
     case TOPKV_ERR_BOUNDS: return "TOPKV_ERR_BOUNDS: block table or length out of range";
     case TOPKV_ERR_DEVICE: return "TOPKV_ERR_DEVICE: HIP device query failed";
+    case TOPKV_ERR_CHECKSUM: return "TOPKV_ERR_CHECKSUM: serialized header or checksum mismatch";
   }
   return "TOPKV_ERR_UNKNOWN";
 }

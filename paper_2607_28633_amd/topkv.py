@@ -31,6 +31,7 @@ TOPKV_ERR_UNSUPPORTED = 2
 TOPKV_ERR_LAUNCH = 3
 TOPKV_ERR_BOUNDS = 4
 TOPKV_ERR_DEVICE = 5
+TOPKV_ERR_CHECKSUM = 6
 TOPKV_MAX_BATCH_REQS = 4096
 TOPKV_CHECK_RESULT_WORDS = 4
 
@@ -38,7 +39,10 @@ EXPORTS = ["topkv_pack_layer", "topkv_unpack_layer", "topkv_pack_layer_batched",
            "topkv_unpack_layer_batched", "topkv_pack_layer_batched_ex",
            "topkv_unpack_layer_batched_ex", "topkv_packed_layer_bytes", "topkv_status_string",
            "topkv_check_tables", "topkv_check_workspace_bytes", "topkv_pack_layer_window",
-           "topkv_unpack_layer_window", "topkv_packed_window_bytes"]
+           "topkv_unpack_layer_window", "topkv_packed_window_bytes", "topkv_pack_layer_planes",
+           "topkv_unpack_layer_planes", "topkv_kvcache1_bytes", "topkv_kvcache1_workspace_bytes",
+           "topkv_kvcache1_pack_layer", "topkv_kvcache1_seal", "topkv_kvcache1_verify",
+           "topkv_kvcache1_unpack_layer", "topkv_crc64", "topkv_crc64_workspace_bytes"]
 
 
 class topkv_pool_t(ctypes.Structure):
@@ -74,6 +78,16 @@ _SIGS = {
     "topkv_unpack_layer_window": (_I32, [_P, _I64, _POOL, _I32, _I32, _P, _I32, _P, _I32,
                                          ctypes.POINTER(topkv_launch_t)]),
     "topkv_packed_window_bytes": (_I64, [_POOL, ctypes.POINTER(_I32), _I32, _I32]),
+    "topkv_pack_layer_planes": (_I32, [_POOL, _I32, _P, _I32, _P, _I64, _I64, _P]),
+    "topkv_unpack_layer_planes": (_I32, [_P, _I64, _I64, _POOL, _I32, _P, _I32, _P]),
+    "topkv_kvcache1_bytes": (_I64, [_POOL, _I32]),
+    "topkv_kvcache1_workspace_bytes": (_I64, [_POOL, _I32]),
+    "topkv_kvcache1_pack_layer": (_I32, [_POOL, _I32, _P, _I32, _P, _I64, _P]),
+    "topkv_kvcache1_seal": (_I32, [_POOL, _I32, ctypes.c_uint64, ctypes.c_uint64, _P, _I64, _P, _I64, _P]),
+    "topkv_kvcache1_verify": (_I32, [_POOL, _I32, ctypes.c_uint64, ctypes.c_uint64, _P, _I64, _P, _I64, _P, _P]),
+    "topkv_kvcache1_unpack_layer": (_I32, [_P, _I64, _POOL, _I32, _P, _I32, _P]),
+    "topkv_crc64": (_I32, [_P, _I64, _P, _I64, _P, _P]),
+    "topkv_crc64_workspace_bytes": (_I64, [_I64]),
 }
 for _name, (_res, _args) in _SIGS.items():
     _fn = getattr(_lib, _name)
@@ -212,6 +226,60 @@ def topkv_packed_window_bytes(pool, seq_lens_host, window) -> int:
     lens = [int(x) for x in seq_lens_host]
     arr = (_I32 * max(1, len(lens)))(*lens)
     return int(_lib.topkv_packed_window_bytes(ctypes.byref(_pool_arg(pool)), arr, len(lens), int(window)))
+
+
+def topkv_pack_layer_planes(src, layer, block_table, seq_len, dst, plane_stride, dst_bytes=None, stream=None) -> None:
+    _check(_lib.topkv_pack_layer_planes(ctypes.byref(_pool_arg(src)), int(layer), _table_ptr(block_table),
+                                        int(seq_len), _ptr(dst), int(plane_stride), _nbytes(dst, dst_bytes),
+                                        _stream(stream)))
+
+
+def topkv_unpack_layer_planes(src, plane_stride, dst, layer, block_table, seq_len, src_bytes=None,
+                              stream=None) -> None:
+    _check(_lib.topkv_unpack_layer_planes(_ptr(src), int(plane_stride), _nbytes(src, src_bytes),
+                                          ctypes.byref(_pool_arg(dst)), int(layer), _table_ptr(block_table),
+                                          int(seq_len), _stream(stream)))
+
+
+def topkv_kvcache1_bytes(geometry, seq_len) -> int:
+    return int(_lib.topkv_kvcache1_bytes(ctypes.byref(_pool_arg(geometry)), int(seq_len)))
+
+
+def topkv_kvcache1_workspace_bytes(geometry, seq_len) -> int:
+    return int(_lib.topkv_kvcache1_workspace_bytes(ctypes.byref(_pool_arg(geometry)), int(seq_len)))
+
+
+def topkv_kvcache1_pack_layer(src, layer, block_table, seq_len, blob, blob_bytes=None, stream=None) -> None:
+    _check(_lib.topkv_kvcache1_pack_layer(ctypes.byref(_pool_arg(src)), int(layer), _table_ptr(block_table),
+                                          int(seq_len), _ptr(blob), _nbytes(blob, blob_bytes), _stream(stream)))
+
+
+def topkv_kvcache1_seal(geometry, seq_len, request_id, model_id, blob, workspace, blob_bytes=None,
+                        workspace_bytes=None, stream=None) -> None:
+    _check(_lib.topkv_kvcache1_seal(ctypes.byref(_pool_arg(geometry)), int(seq_len), int(request_id),
+                                    int(model_id), _ptr(blob), _nbytes(blob, blob_bytes), _ptr(workspace),
+                                    _nbytes(workspace, workspace_bytes), _stream(stream)))
+
+
+def topkv_kvcache1_verify(geometry, seq_len, request_id, model_id, blob, workspace, result, blob_bytes=None,
+                          workspace_bytes=None, stream=None) -> None:
+    _check(_lib.topkv_kvcache1_verify(ctypes.byref(_pool_arg(geometry)), int(seq_len), int(request_id),
+                                      int(model_id), _ptr(blob), _nbytes(blob, blob_bytes), _ptr(workspace),
+                                      _nbytes(workspace, workspace_bytes), _table_ptr(result), _stream(stream)))
+
+
+def topkv_kvcache1_unpack_layer(blob, dst, layer, block_table, seq_len, blob_bytes=None, stream=None) -> None:
+    _check(_lib.topkv_kvcache1_unpack_layer(_ptr(blob), _nbytes(blob, blob_bytes), ctypes.byref(_pool_arg(dst)),
+                                            int(layer), _table_ptr(block_table), int(seq_len), _stream(stream)))
+
+
+def topkv_crc64(data, nbytes, workspace, crc_out, workspace_bytes=None, stream=None) -> None:
+    _check(_lib.topkv_crc64(_ptr(data), int(nbytes), _ptr(workspace), _nbytes(workspace, workspace_bytes),
+                            _ptr(crc_out), _stream(stream)))
+
+
+def topkv_crc64_workspace_bytes(nbytes) -> int:
+    return int(_lib.topkv_crc64_workspace_bytes(int(nbytes)))
 
 
 def topkv_packed_layer_bytes(pool, seq_lens_host) -> int:

@@ -1,0 +1,136 @@
+"""KVCACHE1 serialization and the device CRC-64 through the C ABI vs the CPU
+oracle (serializer and C CRC), bit for bit."""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import oracle.kvcache1 as okv
+from gpu_util import say, to_dev, to_host
+from oracle.crc64 import crc64
+from paper_2607_28633_amd.workloads import (device_dst_prefill, device_src_pool, host_dst_prefill,
+                                            host_src_pool, make_workload)
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module")
+def tk():
+    from paper_2607_28633_amd import topkv
+    assert torch.cuda.is_available(), "GPU tests need a GPU"
+    return topkv
+
+
+def _device_crc(tk, buf: torch.Tensor, nbytes: int) -> int:
+    ws = torch.empty(max(8, tk.topkv_crc64_workspace_bytes(nbytes)) // 8, dtype=torch.int64, device="cuda")
+    out = torch.zeros(1, dtype=torch.int64, device="cuda")
+    tk.topkv_crc64(buf, nbytes, ws, out)
+    torch.cuda.synchronize()
+    return int(out.cpu().numpy().view(np.uint64)[0])
+
+
+@pytest.mark.parametrize("n", [0, 1, 9, 15, 16, 17, 4096, 65536, 65536 + 21, 3 * 65536 + 999,
+                               (10 << 20) + 3, 300 << 20])
+def test_device_crc64(tk, n):
+    say(f"[crc64] {n} bytes")
+    host = np.random.default_rng(n).integers(0, 256, max(n, 1), dtype=np.uint8)
+    if n == 9:
+        host[:9] = np.frombuffer(b"123456789", dtype=np.uint8)
+    dev = torch.from_numpy(host).cuda()
+    got = _device_crc(tk, dev, n)
+    assert got == crc64(host[:n]), f"{n} bytes: {got:#x} != {crc64(host[:n]):#x}"
+    if n == 9:
+        assert got == 0x995DC9BBDF1939FA
+
+
+def _blob_run(tk, wl, src, dst, r, rid=0x1234, mid=0x77):
+    """Serialize request r from src, verify, unpack into dst; returns the blob."""
+    n = int(wl.seq_lens[r])
+    geo = tk.pool_from_tensor(src)
+    nbytes = tk.topkv_kvcache1_bytes(geo, n)
+    blob = torch.full((nbytes,), 0xAB, dtype=torch.uint8, device="cuda")
+    ws = torch.empty(tk.topkv_kvcache1_workspace_bytes(geo, n) // 8, dtype=torch.int64, device="cuda")
+    bt = to_dev(wl.block_tables[r])
+    for layer in range(wl.num_layers):
+        tk.topkv_kvcache1_pack_layer(src, layer, bt, n, blob)
+    tk.topkv_kvcache1_seal(geo, n, rid, mid, blob, ws)
+    res = torch.full((4,), 99, dtype=torch.int32, device="cuda")
+    tk.topkv_kvcache1_verify(geo, n, rid, mid, blob, ws, res)
+    bt2 = to_dev(wl.dst_block_tables[r])
+    for layer in range(wl.num_layers):
+        tk.topkv_kvcache1_unpack_layer(blob, dst, layer, bt2, n)
+    torch.cuda.synchronize()
+    assert res.cpu().tolist() == [tk.TOPKV_OK, 0, 0, 0]
+    return blob, ws
+
+
+@pytest.mark.parametrize("case", ["tiny", "mla", "reblock"])
+def test_kvcache1_matches_oracle(tk, case):
+    if case == "tiny":
+        wl = make_workload("tiny", dst_page_size=48)
+    elif case == "mla":
+        wl = make_workload("deepseek-v3-mla", num_layers=3, seq_lens=[700, 1, 64, 129])
+    else:
+        wl = make_workload("reblock-70b", num_layers=2, phys_layers=2, seq_lens=[300, 17, 4096])
+    say(f"[kvcache1] {case}: {wl.describe()}")
+    src_h, dst_h = host_src_pool(wl), host_dst_prefill(wl)
+    src, dst = to_dev(src_h), to_dev(dst_h)
+    want_dst = dst_h.copy()
+    for r in range(wl.num_reqs):
+        n = int(wl.seq_lens[r])
+        blob, _ = _blob_run(tk, wl, src, dst, r, rid=r + 1, mid=len(case))
+        want = okv.serialize(src_h, wl.block_tables[r], n, r + 1, len(case))
+        assert blob.cpu().numpy().tobytes() == want, f"{case} request {r}: blob differs from the oracle"
+        for layer in range(wl.num_layers):
+            okv.unpack_layer(want, want_dst, layer, wl.dst_block_tables[r])
+    assert np.array_equal(to_host(dst), want_dst), f"{case}: unpacked pool differs"
+
+
+def test_kvcache1_detects_corruption(tk):
+    wl = make_workload("tiny", seed=2)
+    src, dst = to_dev(host_src_pool(wl)), to_dev(host_dst_prefill(wl))
+    geo = tk.pool_from_tensor(src)
+    n = int(wl.seq_lens[0])
+    blob, ws = _blob_run(tk, wl, src, dst, 0, rid=5, mid=6)
+    res = torch.zeros(4, dtype=torch.int32, device="cuda")
+    k_bytes = wl.num_layers * n * wl.num_heads * wl.head_dim * 2
+    for pos, want in ((128 + 7, [tk.TOPKV_ERR_CHECKSUM, 0, 1, 0]),            # a K byte
+                      (128 + k_bytes + 3, [tk.TOPKV_ERR_CHECKSUM, 0, 0, 1]),  # a V byte
+                      (24, [tk.TOPKV_ERR_CHECKSUM, 1 << 3, 0, 0])):           # seq_len field
+        bad = blob.clone()
+        bad[pos] ^= 0x40
+        tk.topkv_kvcache1_verify(geo, n, 5, 6, bad, ws, res)
+        torch.cuda.synchronize()
+        assert res.cpu().tolist() == want, f"corruption at byte {pos}"
+    tk.topkv_kvcache1_verify(geo, n, 5, 7, blob, ws, res)      # wrong model id expected
+    torch.cuda.synchronize()
+    assert res.cpu().tolist() == [tk.TOPKV_ERR_CHECKSUM, 1 << 2, 0, 0]
+    roomy = torch.zeros(blob.numel() + 64, dtype=torch.uint8, device="cuda")   # misaligned blob
+    with pytest.raises(tk.TopkvError) as e:
+        tk.topkv_kvcache1_seal(geo, n, 5, 6, roomy.data_ptr() + 8, ws, blob_bytes=blob.numel())
+    assert e.value.status == tk.TOPKV_ERR_UNSUPPORTED
+
+
+def test_kvcache1_fullsize_70b(tk):
+    """One 4096-token request of the 80-layer 70B pool: 1.34 GB blob (Eq. 1)."""
+    wl = make_workload("llama3-70b-4k")
+    say(f"[kvcache1] full size: {wl.describe()}")
+    src, dst = device_src_pool(wl), device_dst_prefill(wl)
+    n = int(wl.seq_lens[0])
+    blob, ws = _blob_run(tk, wl, src, dst, 0, rid=42, mid=70)
+    assert blob.numel() == 128 + 1_342_177_280
+    hdr = okv.parse_header(blob[:128].cpu().numpy().tobytes())
+    body = blob[128:].cpu().numpy()
+    kb = hdr["k_bytes"]
+    assert hdr["crc_k"] == crc64(body[:kb]) and hdr["crc_v"] == crc64(body[kb:])
+    assert (hdr["seq_len"], hdr["layers"], hdr["kv_heads"], hdr["head_dim"]) == (4096, 80, 8, 128)
+    row = 8 * 128 * 2
+    for layer in (0, 41, 79):
+        want = oracle.pack_request(to_host(src[layer])[None], 0, wl.block_tables[0], n)
+        got_k = body[layer * n * row:(layer + 1) * n * row].view(np.uint16)
+        got_v = body[kb + layer * n * row:kb + (layer + 1) * n * row].view(np.uint16)
+        assert np.array_equal(got_k, want[0].reshape(-1)) and np.array_equal(got_v, want[1].reshape(-1))
+        again = oracle.pack_request(to_host(dst[layer])[None], 0, wl.dst_block_tables[0], n)
+        assert np.array_equal(again, want), f"layer {layer}: unpacked pool does not hold the request"
+    del src, dst, blob
+    torch.cuda.empty_cache()
