@@ -15,12 +15,16 @@
 // complement), R(A || B) = R(A) * x^(8|B|) + R(B) over GF(2), leading zero
 // bytes leave R unchanged, and the CRC proper is
 // ~(~0 * x^(8N) + R(data)).  Work split:
-//   kernel 1: each workgroup owns a 64 KiB chunk; each lane computes R of its
-//     256-byte piece with slicing-by-8 tables built in LDS, then a tree of
-//     shift-and-add steps combines the 256 pieces.  The data is front-padded
-//     with zero bytes to whole chunks (free, by the property above);
-//   kernel 2: one workgroup combines the chunk values (each lane a run of
-//     2^q chunks, then a tree), appends the sub-16-byte tail and applies the
+//   kernel 0: byte tables into the caller's workspace (slicing-by-8, and
+//     multiply-by-constant tables for the two fixed shifts below);
+//   kernel 1: each workgroup owns a 256 KiB chunk = 16 sub-chunks of 16 KiB;
+//     lane t takes bytes [64t, 64t + 64) of every sub-chunk (adjacent loads),
+//     runs them through the slicing tables (in LDS), advances its running
+//     register by one sub-chunk per step with a table multiply, and a tree
+//     of shift-and-add steps joins the lanes.  The data is front-padded with
+//     zero bytes to whole chunks (free, by the property above);
+//   kernel 2: one workgroup folds the chunk values (each lane a run of 2^q
+//     chunks, then a tree), appends the sub-16-byte tail and applies the
 //     preset and complement.
 // Shift constants x^(8 * 2^k) mod P are computed once on the host.
 #include <hip/hip_runtime.h>
@@ -34,9 +38,14 @@ namespace {
 
 constexpr uint64_t kPolyReflected = 0xC96C5795D7870F42ull;   // ECMA-182, bit-reversed
 constexpr int kCrcThreads = 256;
-constexpr int kPiece = 256;                                     // bytes per lane
-constexpr int64_t kChunk = (int64_t)kCrcThreads * kPiece;       // 64 KiB per workgroup
-constexpr int kChunkLog2 = 16;
+constexpr int kPiece = 64;                                      // bytes per lane per sub-chunk
+constexpr int kSubLog2 = 14;                                    // 16 KiB sub-chunk = 256 lanes x 64 B
+constexpr int kSubs = 16;                                       // sub-chunks per workgroup
+constexpr int kChunkLog2 = 18;                                  // 256 KiB per workgroup
+constexpr int64_t kChunk = (int64_t)1 << kChunkLog2;
+constexpr int kTableWords = 8 * 256;                            // one set of 8 byte tables
+// workspace: [slicing tables][x^(8*16K) tables][x^(8*256K) tables][chunk registers...]
+constexpr int64_t kWsTables = 3 * kTableWords;
 
 struct ShiftConsts {
   uint64_t x8pow2[64];    // x^(8 * 2^k) mod P, reflected
@@ -75,76 +84,126 @@ uint64_t x8n(const ShiftConsts& c, uint64_t n) {
   return r;
 }
 
-// Slicing-by-8 tables in LDS: t[k][i] is byte i followed by k zero bytes.
-__device__ void build_tables(uint64_t (*t)[256]) {
-  const int i = threadIdx.x;                                   // kCrcThreads == 256 entries
-  uint64_t c = (uint64_t)i;
-  for (int b = 0; b < 8; ++b) c = mul_x(c);
-  t[0][i] = c;
-  __syncthreads();
-  for (int k = 1; k < 8; ++k) {
-    const uint64_t prev = t[k - 1][i];
-    t[k][i] = (prev >> 8) ^ t[0][prev & 0xff];
-    __syncthreads();
+// Kernel 0: the byte tables every other kernel copies into LDS.
+//   [0, 2048):     slicing-by-8, t[k][b] = byte b followed by k zero bytes
+//   [2048, 4096):  b << 8k times x^(8 * 16 KiB)   (advance one sub-chunk)
+//   [4096, 6144):  b << 8k times x^(8 * 256 KiB)  (advance one chunk)
+// Multiplying a register by a constant is linear, so it is the XOR of one
+// lookup per register byte in such a table.
+__global__ __launch_bounds__(256) void crc64_tables_kernel(uint64_t* __restrict__ tables, uint64_t sub_shift,
+                                                           uint64_t chunk_shift) {
+  const int g = blockIdx.x * 256 + threadIdx.x;              // grid covers exactly 3 * 2048 entries
+  const int set = g / kTableWords, k = (g / 256) % 8, b = g % 256;
+  uint64_t v;
+  if (set == 0) {
+    v = (uint64_t)b;
+    for (int i = 0; i < 8 * (k + 1); ++i) v = mul_x(v);
+  } else {
+    v = mulmod((uint64_t)b << (8 * k), set == 1 ? sub_shift : chunk_shift);
   }
+  tables[g] = v;
 }
 
-__device__ inline uint64_t crc_word(uint64_t reg, uint64_t w, const uint64_t (*t)[256]) {
+__device__ inline uint64_t lookup8(uint64_t v, const uint64_t* t) {   // t: 8 x 256 words
+  return t[0 * 256 + (v & 0xff)] ^ t[1 * 256 + ((v >> 8) & 0xff)] ^ t[2 * 256 + ((v >> 16) & 0xff)] ^
+         t[3 * 256 + ((v >> 24) & 0xff)] ^ t[4 * 256 + ((v >> 32) & 0xff)] ^ t[5 * 256 + ((v >> 40) & 0xff)] ^
+         t[6 * 256 + ((v >> 48) & 0xff)] ^ t[7 * 256 + (v >> 56)];
+}
+
+// Eight bytes (little-endian word w) into the register: with the slicing
+// tables, byte 0 is followed by 7 more bytes, byte 7 by none.
+__device__ inline uint64_t crc_word(uint64_t reg, uint64_t w, const uint64_t* t) {
   reg ^= w;
-  return t[7][reg & 0xff] ^ t[6][(reg >> 8) & 0xff] ^ t[5][(reg >> 16) & 0xff] ^ t[4][(reg >> 24) & 0xff] ^
-         t[3][(reg >> 32) & 0xff] ^ t[2][(reg >> 40) & 0xff] ^ t[1][(reg >> 48) & 0xff] ^ t[0][reg >> 56];
+  return t[7 * 256 + (reg & 0xff)] ^ t[6 * 256 + ((reg >> 8) & 0xff)] ^ t[5 * 256 + ((reg >> 16) & 0xff)] ^
+         t[4 * 256 + ((reg >> 24) & 0xff)] ^ t[3 * 256 + ((reg >> 32) & 0xff)] ^
+         t[2 * 256 + ((reg >> 40) & 0xff)] ^ t[1 * 256 + ((reg >> 48) & 0xff)] ^ t[0 * 256 + (reg >> 56)];
+}
+
+__device__ inline void copy_words(uint64_t* lds, const uint64_t* __restrict__ src, int words) {
+  for (int i = threadIdx.x; i < words; i += blockDim.x) lds[i] = src[i];
 }
 
 typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
 
-// Kernel 1: raw register of each 64 KiB chunk of the front-padded stream.
+// Kernel 1: raw register of each 256 KiB chunk of the front-padded stream.
 // data: 16-byte aligned, `head` bytes (a multiple of 16); `pad` leading zero
-// bytes (a multiple of 16) make head + pad a whole number of chunks.
+// bytes (a multiple of 16) make head + pad a whole number of chunks.  Lane t
+// owns bytes [t*64, t*64 + 64) of each 16 KiB sub-chunk (four adjacent
+// 16-byte loads, so every line is used at once), folds its pieces across the
+// 16 sub-chunks (advance by 16 KiB = one table multiply), and a tree of
+// shift-and-add steps joins the 256 lanes.
 __global__ __launch_bounds__(kCrcThreads) void crc64_chunks_kernel(const u32x4* __restrict__ data, int64_t head,
-                                                                   int64_t pad, uint64_t* __restrict__ partial,
-                                                                   ShiftConsts sc) {
-  __shared__ uint64_t tables[8][256];
+                                                                   int64_t pad, const uint64_t* __restrict__ tables,
+                                                                   uint64_t* __restrict__ partial, ShiftConsts sc) {
+  __shared__ uint64_t t_slice[kTableWords];
+  __shared__ uint64_t t_sub[kTableWords];
   __shared__ uint64_t acc[kCrcThreads];
-  build_tables(tables);
-  const int64_t vbase = (int64_t)blockIdx.x * kChunk + (int64_t)threadIdx.x * kPiece - pad;   // data offset
-  uint64_t reg = 0;
-#pragma unroll 4
-  for (int j = 0; j < kPiece / 16; ++j) {
-    const int64_t off = vbase + 16 * j;
-    u32x4 v = {0u, 0u, 0u, 0u};
-    if (off >= 0) v = __builtin_nontemporal_load(data + off / 16);   // off < head by construction
-    reg = crc_word(reg, ((uint64_t)v.y << 32) | v.x, tables);
-    reg = crc_word(reg, ((uint64_t)v.w << 32) | v.z, tables);
-  }
-  acc[threadIdx.x] = reg;
+  copy_words(t_slice, tables, kTableWords);
+  copy_words(t_sub, tables + kTableWords, kTableWords);
   __syncthreads();
-  // combine pieces t and t + s (the later piece is s * 256 bytes long)
+  const int64_t base = (int64_t)blockIdx.x * kChunk + (int64_t)threadIdx.x * kPiece - pad;   // data offset
+  u32x4 cur[4], nxt[4];
+  auto load = [&](u32x4 (&v)[4], int sub) {
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const int64_t off = base + ((int64_t)sub << kSubLog2) + 16 * j;
+      v[j] = off >= 0 ? __builtin_nontemporal_load(data + off / 16) : u32x4{0u, 0u, 0u, 0u};   // off < head
+    }
+  };
+  load(cur, 0);
+  uint64_t fold = 0;
+#pragma unroll 2
+  for (int sub = 0; sub < kSubs; ++sub) {
+    if (sub + 1 < kSubs) load(nxt, sub + 1);
+    uint64_t reg = 0;
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      reg = crc_word(reg, ((uint64_t)cur[j].y << 32) | cur[j].x, t_slice);
+      reg = crc_word(reg, ((uint64_t)cur[j].w << 32) | cur[j].z, t_slice);
+    }
+    fold = lookup8(fold, t_sub) ^ reg;
+#pragma unroll
+    for (int j = 0; j < 4; ++j) cur[j] = nxt[j];
+  }
+  acc[threadIdx.x] = fold;
+  __syncthreads();
+  // join lanes t and t + s: the later group holds s lanes x 64 bytes of every sub-chunk
   for (int lvl = 0; lvl < 8; ++lvl) {
     const int s = 1 << lvl;
     const int t = threadIdx.x;
-    if ((t & (2 * s - 1)) == 0) acc[t] = mulmod(sc.x8pow2[8 + lvl], acc[t]) ^ acc[t + s];
+    if ((t & (2 * s - 1)) == 0) acc[t] = mulmod(sc.x8pow2[6 + lvl], acc[t]) ^ acc[t + s];
     __syncthreads();
   }
   if (threadIdx.x == 0) partial[blockIdx.x] = acc[0];
 }
 
 // Kernel 2 (one workgroup): fold `chunks` chunk registers, each lane a run of
-// 2^run_log2 of them (front-padded with zero registers), then append the
-// tail bytes and finish: out = ~(preset_shift + R).
-__global__ __launch_bounds__(kCrcThreads) void crc64_finish_kernel(const uint64_t* __restrict__ partial,
+// 2^run_log2 of them (front-padded with zero registers; advancing one chunk is
+// one table multiply), join the lanes, append the tail bytes and finish:
+// out = ~(preset_shift + R).
+__global__ __launch_bounds__(kCrcThreads) void crc64_finish_kernel(const uint64_t* __restrict__ tables,
+                                                                   const uint64_t* __restrict__ partial,
                                                                    int64_t chunks, int run_log2,
                                                                    const unsigned char* __restrict__ tail,
                                                                    int tail_len, uint64_t preset_shift,
                                                                    uint64_t* __restrict__ out, ShiftConsts sc) {
-  __shared__ uint64_t tables[8][256];
+  __shared__ uint64_t t_chunk[kTableWords];
   __shared__ uint64_t acc[kCrcThreads];
-  build_tables(tables);
+  copy_words(t_chunk, tables + 2 * kTableWords, kTableWords);
+  __syncthreads();
   const int64_t run = (int64_t)1 << run_log2;
   const int64_t lead = (int64_t)kCrcThreads * run - chunks;    // leading zero chunks
   uint64_t reg = 0;
-  for (int64_t j = 0; j < run; ++j) {
-    const int64_t v = (int64_t)threadIdx.x * run + j - lead;
-    reg = mulmod(sc.x8pow2[kChunkLog2], reg) ^ (v >= 0 ? partial[v] : 0ull);
+  for (int64_t j0 = 0; j0 < run; j0 += 8) {
+    uint64_t vals[8];   // issue the loads of eight chunk registers, then fold them
+#pragma unroll
+    for (int j = 0; j < 8; ++j) {
+      const int64_t v = (int64_t)threadIdx.x * run + j0 + j - lead;
+      vals[j] = (j0 + j < run && v >= 0) ? partial[v] : 0ull;
+    }
+#pragma unroll
+    for (int j = 0; j < 8; ++j)
+      if (j0 + j < run) reg = lookup8(reg, t_chunk) ^ vals[j];
   }
   acc[threadIdx.x] = reg;
   __syncthreads();
@@ -156,23 +215,28 @@ __global__ __launch_bounds__(kCrcThreads) void crc64_finish_kernel(const uint64_
   }
   if (threadIdx.x == 0) {
     uint64_t r = acc[0];
-    for (int b = 0; b < tail_len; ++b) r = tables[0][(r ^ tail[b]) & 0xff] ^ (r >> 8);
+    for (int b = 0; b < tail_len; ++b) r = tables[(r ^ tail[b]) & 0xff] ^ (r >> 8);   // slicing table 0
     out[0] = ~(preset_shift ^ r);
   }
 }
 
-int64_t crc_chunks(int64_t head) {
-  return (head + kChunk - 1) / kChunk;
+int64_t crc_chunks(int64_t head) { return (head + kChunk - 1) / kChunk; }
+
+// Workspace words one CRC of n bytes needs: tables + chunk registers.
+int64_t crc_words(int64_t n) { return kWsTables + crc_chunks(n - n % 16) + 1; }
+
+// Queue the byte tables into ws (first kWsTables words).
+topkv_status_t crc64_tables(uint64_t* ws, hipStream_t stream) {
+  const ShiftConsts& sc = shift_consts();
+  hipLaunchKernelGGL(crc64_tables_kernel, dim3((unsigned)(kWsTables / 256)), dim3(256), 0, stream, ws,
+                     sc.x8pow2[kSubLog2], sc.x8pow2[kChunkLog2]);
+  return hipGetLastError() == hipSuccess ? TOPKV_OK : TOPKV_ERR_LAUNCH;
 }
 
-// Workspace words one CRC of n bytes needs (chunk registers).
-int64_t crc_words(int64_t n) {
-  return crc_chunks(n - n % 16) + 1;
-}
-
-// Queue the CRC-64/XZ of data[0, n) into out (device).  data 16-byte aligned.
-topkv_status_t crc64_launch(const unsigned char* data, int64_t n, uint64_t* partial, uint64_t* out,
-                            hipStream_t stream) {
+// Queue the CRC-64/XZ of data[0, n) into out (device).  data 16-byte aligned;
+// ws holds the tables (crc64_tables) followed by room for the chunk registers.
+topkv_status_t crc64_launch(const unsigned char* data, int64_t n, const uint64_t* tables, uint64_t* partial,
+                            uint64_t* out, hipStream_t stream) {
   const ShiftConsts& sc = shift_consts();
   const int64_t head = n - n % 16;
   const int64_t chunks = crc_chunks(head);
@@ -180,13 +244,13 @@ topkv_status_t crc64_launch(const unsigned char* data, int64_t n, uint64_t* part
   if (chunks > 0) {
     if (chunks > INT32_MAX) return TOPKV_ERR_UNSUPPORTED;
     hipLaunchKernelGGL(crc64_chunks_kernel, dim3((unsigned)chunks), dim3(kCrcThreads), 0, stream,
-                       reinterpret_cast<const u32x4*>(data), head, pad, partial, sc);
+                       reinterpret_cast<const u32x4*>(data), head, pad, tables, partial, sc);
     if (hipGetLastError() != hipSuccess) return TOPKV_ERR_LAUNCH;
   }
   int run_log2 = 0;
   while (((int64_t)kCrcThreads << run_log2) < chunks) ++run_log2;
   if (kChunkLog2 + run_log2 + 8 > 63) return TOPKV_ERR_UNSUPPORTED;
-  hipLaunchKernelGGL(crc64_finish_kernel, dim3(1), dim3(kCrcThreads), 0, stream, partial, chunks, run_log2,
+  hipLaunchKernelGGL(crc64_finish_kernel, dim3(1), dim3(kCrcThreads), 0, stream, tables, partial, chunks, run_log2,
                      data + head, (int)(n - head), mulmod(x8n(sc, (uint64_t)n), ~0ull), out, sc);
   return hipGetLastError() == hipSuccess ? TOPKV_OK : TOPKV_ERR_LAUNCH;
 }
@@ -283,17 +347,21 @@ HeaderFields fields(const topkv_pool_t* g, int32_t seq_len, uint64_t request_id,
   return f;
 }
 
-// Both checksums of a blob body into ws[0..1]; chunk registers after them.
+// Both checksums of a blob body into ws[0..1]; then the byte tables, then
+// the chunk registers of K and of V.
 topkv_status_t blob_crcs(const unsigned char* blob, const Blob& b, uint64_t* ws, hipStream_t stream) {
-  uint64_t* partial_k = ws + 2;
-  uint64_t* partial_v = partial_k + crc_words(b.k_bytes);
-  topkv_status_t st = crc64_launch(blob + kHeaderBytes, b.k_bytes, partial_k, ws, stream);
+  uint64_t* tables = ws + 2;
+  uint64_t* partial_k = tables + kWsTables;
+  uint64_t* partial_v = partial_k + crc_words(b.k_bytes) - kWsTables;
+  topkv_status_t st = crc64_tables(tables, stream);
   if (st != TOPKV_OK) return st;
-  return crc64_launch(blob + kHeaderBytes + b.k_bytes, b.v_bytes, partial_v, ws + 1, stream);
+  st = crc64_launch(blob + kHeaderBytes, b.k_bytes, tables, partial_k, ws, stream);
+  if (st != TOPKV_OK) return st;
+  return crc64_launch(blob + kHeaderBytes + b.k_bytes, b.v_bytes, tables, partial_v, ws + 1, stream);
 }
 
 int64_t blob_ws_bytes(const Blob& b) {
-  return (int64_t)sizeof(uint64_t) * (2 + crc_words(b.k_bytes) + crc_words(b.v_bytes));
+  return (int64_t)sizeof(uint64_t) * (2 + crc_words(b.k_bytes) + crc_words(b.v_bytes) - kWsTables);
 }
 
 bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15) == 0; }
@@ -312,8 +380,10 @@ topkv_status_t topkv_crc64(const void* data, int64_t nbytes, void* workspace, in
   if (nbytes < 0 || !crc_out || (nbytes > 0 && !data) || !workspace) return TOPKV_ERR_INVALID_ARG;
   if (workspace_bytes < topkv_crc64_workspace_bytes(nbytes)) return TOPKV_ERR_INVALID_ARG;
   if (nbytes > 0 && !aligned16(data)) return TOPKV_ERR_UNSUPPORTED;
-  return crc64_launch(static_cast<const unsigned char*>(data), nbytes, static_cast<uint64_t*>(workspace), crc_out,
-                      stream);
+  uint64_t* ws = static_cast<uint64_t*>(workspace);
+  const topkv_status_t st = crc64_tables(ws, stream);
+  if (st != TOPKV_OK) return st;
+  return crc64_launch(static_cast<const unsigned char*>(data), nbytes, ws, ws + kWsTables, crc_out, stream);
 }
 
 int64_t topkv_kvcache1_bytes(const topkv_pool_t* geometry, int32_t seq_len) {
