@@ -297,6 +297,37 @@ topkv_status_t topkv_check_tables(const topkv_pool_t* pool, int32_t num_reqs,
  * num_pages bits, in 4-byte words); -1 for a null or empty pool. */
 int64_t topkv_check_workspace_bytes(const topkv_pool_t* pool);
 
+/* Layer shipper (Sec. 5.2: layer l's cache leaves while layers l+1 .. L still
+ * compute).  Copies run on the GPU's DMA engines (ROCr asynchronous copies),
+ * so they take no compute unit from the kernels still running; a worker
+ * thread starts each copy once its `ready` event has completed.
+ *
+ * topkv_dma_create: a shipper for the current HIP device, returned in *out
+ *   (owned by the caller; free it with topkv_dma_destroy).  TOPKV_ERR_DEVICE
+ *   if the HSA runtime or its signals cannot be set up.
+ * topkv_dma_submit: queue a copy of `bytes` from src to dst and return its
+ *   ticket (1, 2, 3, ... in submission order) in *ticket.  Both pointers must
+ *   lie, with all `bytes`, inside one hipMalloc or hipHostMalloc allocation
+ *   (device memory or pinned, mapped host memory), else TOPKV_ERR_BOUNDS; the
+ *   ranges must not overlap.  `ready` (may be null) is a recorded event that
+ *   marks the moment src holds the data; it must have been recorded before
+ *   this call and without hipEventDisableSystemFence, so the producer's writes
+ *   are visible to the DMA engine.  bytes == 0 queues an ordering point.
+ *   Returns at once; the caller keeps both buffers and the event alive, and
+ *   the buffers unchanged, until the ticket completes.
+ * topkv_dma_wait: block the calling host thread until every ticket up to and
+ *   including `ticket` has completed.  After a failed copy every later wait
+ *   and submit returns TOPKV_ERR_DEVICE and queued copies are dropped.
+ * topkv_dma_destroy: finish every queued copy, stop the worker, free the
+ *   shipper; returns the shipper's status.
+ * Any number of host threads may submit and wait on one shipper. */
+typedef struct topkv_dma topkv_dma_t;
+topkv_status_t topkv_dma_create(topkv_dma_t** out);
+topkv_status_t topkv_dma_submit(topkv_dma_t* dma, hipEvent_t ready, void* dst, const void* src,
+                                int64_t bytes, int64_t* ticket);
+topkv_status_t topkv_dma_wait(topkv_dma_t* dma, int64_t ticket);
+topkv_status_t topkv_dma_destroy(topkv_dma_t* dma);
+
 /* Static, human-readable name of a status code (never null). */
 const char* topkv_status_string(topkv_status_t status);
 

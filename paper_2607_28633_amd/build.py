@@ -15,7 +15,7 @@ import sys
 
 PKG = os.path.dirname(os.path.abspath(__file__))
 ROOT = os.path.dirname(PKG)
-SOURCES = [os.path.join(PKG, "csrc", n) for n in ("topkv.hip", "check.hip", "kvcache1.hip")]
+SOURCES = [os.path.join(PKG, "csrc", n) for n in ("topkv.hip", "check.hip", "kvcache1.hip", "dma.hip")]
 INCLUDE = os.path.join(ROOT, "include")
 LIBRARY = os.path.join(PKG, "libtopkv.so")
 ARCH = "gfx950"
@@ -35,7 +35,7 @@ def build_command(out: str = LIBRARY, defines=None):
            "-Wall", f"-I{INCLUDE}", "-o", out]
     for k, v in (defines or {}).items():
         cmd.append(f"-D{k}={v}")
-    return cmd + SOURCES
+    return cmd + SOURCES + ["-L/opt/rocm/lib", "-lhsa-runtime64"]
 
 
 def build_library(out: str = LIBRARY, defines=None, verbose: bool = False) -> str:

@@ -42,7 +42,8 @@ EXPORTS = ["topkv_pack_layer", "topkv_unpack_layer", "topkv_pack_layer_batched",
            "topkv_unpack_layer_window", "topkv_packed_window_bytes", "topkv_pack_layer_planes",
            "topkv_unpack_layer_planes", "topkv_kvcache1_bytes", "topkv_kvcache1_workspace_bytes",
            "topkv_kvcache1_pack_layer", "topkv_kvcache1_seal", "topkv_kvcache1_verify",
-           "topkv_kvcache1_unpack_layer", "topkv_crc64", "topkv_crc64_workspace_bytes"]
+           "topkv_kvcache1_unpack_layer", "topkv_crc64", "topkv_crc64_workspace_bytes", "topkv_dma_create",
+           "topkv_dma_submit", "topkv_dma_wait", "topkv_dma_destroy"]
 
 
 class topkv_pool_t(ctypes.Structure):
@@ -88,6 +89,10 @@ _SIGS = {
     "topkv_kvcache1_unpack_layer": (_I32, [_P, _I64, _POOL, _I32, _P, _I32, _P]),
     "topkv_crc64": (_I32, [_P, _I64, _P, _I64, _P, _P]),
     "topkv_crc64_workspace_bytes": (_I64, [_I64]),
+    "topkv_dma_create": (_I32, [ctypes.POINTER(_P)]),
+    "topkv_dma_submit": (_I32, [_P, _P, _P, _P, _I64, ctypes.POINTER(_I64)]),
+    "topkv_dma_wait": (_I32, [_P, _I64]),
+    "topkv_dma_destroy": (_I32, [_P]),
 }
 for _name, (_res, _args) in _SIGS.items():
     _fn = getattr(_lib, _name)
@@ -348,10 +353,66 @@ class HipEvent:
             _destroy(h)
 
 
+# --- mapped host memory and the DMA layer shipper ----------------------------
+_hip.hipHostGetDevicePointer.argtypes = [ctypes.POINTER(ctypes.c_void_p), ctypes.c_void_p, ctypes.c_uint]
+
+
+def host_device_pointer(t: torch.Tensor) -> int:
+    """Device address of pinned (hipHostMalloc'd) host memory, for kernels
+    that write straight into it; raises for memory the device cannot map."""
+    if t.is_cuda or not t.is_pinned():
+        raise ValueError("expected a pinned host tensor")
+    d = ctypes.c_void_p()
+    rc = _hip.hipHostGetDevicePointer(ctypes.byref(d), ctypes.c_void_p(t.data_ptr()), 0)
+    if rc != 0 or not d.value:
+        raise RuntimeError(f"hipHostGetDevicePointer failed ({rc}): host memory is not mapped")
+    return int(d.value)
+
+
+def _any_ptr(x) -> int:
+    """Address of device memory or of pinned host memory (the shipper's ends)."""
+    if isinstance(x, torch.Tensor):
+        if x.numel() and not (x.is_cuda or x.is_pinned()):
+            raise ValueError("shipper buffers must be device memory or pinned host memory")
+        if x.numel() and not x.is_contiguous():
+            raise ValueError("tensor arguments must be contiguous")
+        return x.data_ptr()
+    return _ptr(x)
+
+
+def topkv_dma_create() -> int:
+    h = _P()
+    _check(_lib.topkv_dma_create(ctypes.byref(h)))
+    return int(h.value)
+
+
+def topkv_dma_submit(dma, ready, dst, src, nbytes=None) -> int:
+    """Queue a DMA copy src -> dst that starts once `ready` (a recorded
+    HipEvent / torch.cuda.Event / raw handle / None) has completed; returns
+    the ticket."""
+    t = _I64()
+    n = _nbytes(src, nbytes)
+    _check(_lib.topkv_dma_submit(_P(int(dma)), _P(_event(ready)), _P(_any_ptr(dst)), _P(_any_ptr(src)),
+                                 n, ctypes.byref(t)))
+    return int(t.value)
+
+
+def topkv_dma_wait(dma, ticket) -> None:
+    _check(_lib.topkv_dma_wait(_P(int(dma)), int(ticket)))
+
+
+def topkv_dma_destroy(dma) -> None:
+    _check(_lib.topkv_dma_destroy(_P(int(dma))))
+
+
 def _event(e) -> int:
     if e is None:
         return 0
-    return e.handle if isinstance(e, HipEvent) else int(e)
+    if isinstance(e, HipEvent):
+        return e.handle
+    if isinstance(e, torch.cuda.Event):
+        return int(e.cuda_event)
+    return int(e)
 
 
 # --- prepared calls -----------------------------------------------------------

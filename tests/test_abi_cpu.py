@@ -121,3 +121,15 @@ def test_check_tables_validation(tk):
     _expect(tk, INV, tk.topkv_check_tables, good, 2, 0, 4, lens, 0, None, res)                      # null tables
     _expect(tk, INV, tk.topkv_check_tables, good, -1, bt, 4, lens, 0, None, res)
     _expect(tk, INV, tk.topkv_check_tables, _pool(tk, page_size=0), 2, bt, 4, lens, 0, None, res)
+
+
+def test_dma_shipper_validation(tk):
+    """Null handles and bad sizes are refused before any runtime call."""
+    INV = tk.TOPKV_ERR_INVALID_ARG
+    lib, P, I64 = tk._lib, ctypes.c_void_p, ctypes.c_int64
+    t = I64(-7)
+    assert lib.topkv_dma_create(None) == INV
+    assert lib.topkv_dma_submit(None, None, P(0x1000), P(0x2000), 16, ctypes.byref(t)) == INV
+    assert lib.topkv_dma_wait(None, 1) == INV
+    assert lib.topkv_dma_destroy(None) == INV
+    assert t.value == -7
