@@ -65,10 +65,11 @@ def parse():
                     help="issue each sweep as L host launches, or replay it as a captured HIP graph")
     ap.add_argument("--kernel-events", action="store_true",
                     help="also time every launch with its own kernel-timestamp events (diagnostic)")
-    ap.add_argument("--mode", choices=["layers", "kvcache1", "pipeline"], default="layers",
+    ap.add_argument("--mode", choices=["layers", "kvcache1", "pipeline", "reshard"], default="layers",
                     help="layers: per-layer pack/unpack sweep (the headline); kvcache1: whole-request "
                          "serialization (pack every layer into a KVCACHE1 blob, seal, verify, unpack); "
-                         "pipeline: layer-by-layer transfer overlapped with a synthetic prefill")
+                         "pipeline: layer-by-layer transfer overlapped with a synthetic prefill; "
+                         "reshard: head-sliced pack, head-major unpack, pool-to-pool re-blocking")
     ap.add_argument("--layer-ms", type=float, default=0.5,
                     help="pipeline mode: synthetic prefill time per layer (the paper's 0.5 ms for 70B)")
     ap.add_argument("--calib-copy-bytes", type=int, default=0,
@@ -382,6 +383,96 @@ def run_kvcache1(args):
         "phases": out_ph}), flush=True)
 
 
+def run_reshard(args):
+    """Layout moves, per layer, as graph-captured sweeps over every layer:
+    head-sliced pack of the two tensor-parallel halves (heads [0, H/2) and
+    [H/2, H), two launches per layer) beside the full-head pack; unpack into a
+    head-major pool beside the slot-major unpack; and pool-to-pool re-blocking
+    (P -> P', one launch, no staging buffer) beside the pack + unpack pair.
+    GB/s counts algorithmic bytes: each moved byte read once and written once
+    per launch that moves it (the pair moves every byte twice)."""
+    import torch
+
+    from paper_2607_28633_amd import topkv
+    from paper_2607_28633_amd.workloads import WORKLOADS, device_dst_prefill, device_src_pool, make_workload
+
+    torch.cuda.set_device(0)
+    wl = make_workload(args.workload)
+    if any(wl.window(l) for l in range(wl.num_layers)):
+        raise SystemExit("reshard mode measures full-attention layers")
+    log(f"[bench] reshard {wl.describe()}")
+    src, dst = device_src_pool(wl), device_dst_prefill(wl)
+    L, R, H = wl.num_layers, wl.num_reqs, wl.num_heads
+    bt = torch.from_numpy(wl.block_tables).cuda()
+    bt2 = torch.from_numpy(wl.dst_block_tables).cuda()
+    lens = torch.from_numpy(wl.seq_lens).cuda()
+    nbytes = topkv.topkv_packed_layer_bytes(src, wl.seq_lens)
+    ring = min(L, max(2, (2 << 30) // max(nbytes, 1)))
+    packed = torch.empty((ring, nbytes // 2), dtype=torch.int16, device="cuda")
+    half = torch.empty((ring, 2, nbytes // 4), dtype=torch.int16, device="cuda")
+    hm = dst.view(wl.phys_layers, wl.dst_num_pages, wl.planes, H, wl.dst_page_size, wl.head_dim)
+    row = H * wl.head_dim * wl.elem_bytes
+    moved = wl.planes * int(wl.seq_lens.astype("int64").sum()) * row          # bytes of one layer
+
+    def slab(l):
+        return l % wl.phys_layers
+
+    sweeps = {
+        "pack_full": lambda: [topkv.prepare_pack_layer_batched_ex(
+            src, slab(l), R, bt, bt.shape[1], lens, packed[l % ring], stream=None) for l in range(L)],
+        "pack_heads_tp2": lambda: [topkv.prepare_pack_layer_heads(
+            src, slab(l), R, bt, bt.shape[1], lens, i * (H // 2), H // 2, half[l % ring, i]) for l in range(L)
+            for i in range(2)],
+        "unpack_full": lambda: [topkv.prepare_unpack_layer_batched_ex(
+            packed[l % ring], dst, slab(l), R, bt2, bt2.shape[1], lens, stream=None) for l in range(L)],
+        "unpack_head_major": lambda: [topkv.prepare_move_layer(
+            topkv.packed_view(packed[l % ring]), topkv.pool_view(hm, slab(l), bt2, bt2.shape[1], head_major=True),
+            R, lens, H) for l in range(L)],
+        "reblock_fused": lambda: [topkv.prepare_move_layer(
+            topkv.pool_view(src, slab(l), bt, bt.shape[1]), topkv.pool_view(dst, slab(l), bt2, bt2.shape[1]),
+            R, lens, H) for l in range(L)],
+    }
+    graphs = {}
+    for name, make in sweeps.items():
+        for c in make():
+            c()                                           # eager warm-up (and argument check)
+        torch.cuda.synchronize()
+        g = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(g):
+            calls = make()
+            for c in calls:
+                c()
+        graphs[name] = g
+    stream = torch.cuda.current_stream()
+    res = {}
+    for name, g in graphs.items():
+        for _ in range(max(1, args.warmup)):
+            g.replay()
+        e0, e1 = topkv.HipEvent(), topkv.HipEvent()
+        torch.cuda.synchronize()
+        e0.record(stream)
+        for _ in range(args.steps):
+            g.replay()
+        e1.record(stream)
+        e1.synchronize()
+        us = 1e3 * e0.elapsed_ms(e1) / (args.steps * L)
+        b = 2 * moved
+        res[name] = {"us_per_layer": round(us, 3), "bytes_per_layer": b, "gbs": round(b / us / 1e3, 1),
+                     "frac": round(b / us / 1e3 / HBM_PEAK_GBS, 4)}
+    pair = res["pack_full"]["us_per_layer"] + res["unpack_full"]["us_per_layer"]
+    res["reblock_two_step"] = {"us_per_layer": round(pair, 3), "bytes_per_layer": 4 * moved,
+                               "gbs": round(4 * moved / pair / 1e3, 1)}
+    print(json.dumps({
+        "metric": "per-layer layout moves: GB/s of algorithmic bytes", "mode": "reshard",
+        "value": res["reblock_fused"]["gbs"], "unit": "GB/s", "n_gpus": 1, "steps": args.steps,
+        "warmup": args.warmup, "higher_is_better": True, "dtype": "bf16", "data": "synthetic",
+        "config": {"workload": f"{wl.name}: {WORKLOADS[wl.name]}", "layers": L, "requests": R,
+                   "page_size": wl.page_size, "dst_page_size": wl.dst_page_size, "bytes_per_layer": moved,
+                   "launch": "graph"},
+        "ops": res,
+        "reblock_fused_speedup_vs_pair": round(pair / res["reblock_fused"]["us_per_layer"], 3)}), flush=True)
+
+
 def run_pipeline(args, check=None):
     """Section 5.2 on one GPU.  A prefill stream computes layer after layer
     (one bf16 GEMM per layer, sized to --layer-ms); as each layer finishes its
@@ -560,6 +651,8 @@ def main():
         run_kvcache1(args)
     elif args.mode == "pipeline":
         print(json.dumps(run_pipeline(args)), flush=True)
+    elif args.mode == "reshard":
+        run_reshard(args)
     else:
         run(args)
 

@@ -297,6 +297,89 @@ topkv_status_t topkv_check_tables(const topkv_pool_t* pool, int32_t num_reqs,
  * num_pages bits, in 4-byte words); -1 for a null or empty pool. */
 int64_t topkv_check_workspace_bytes(const topkv_pool_t* pool);
 
+/* Layer moves between cache layouts (one layer, a batch of requests).
+ *
+ * A view is one side of a move:
+ *   TOPKV_LAYOUT_PACKED           `data`/`bytes`: per request a block
+ *                                 [planes][kept tokens][head_count][head_dim],
+ *                                 blocks in request order (the pack/unpack
+ *                                 wire order, restricted to the moved heads)
+ *   TOPKV_LAYOUT_POOL             `pool`: the slot-major pool of topkv_pool_t,
+ *                                 [layer][page][plane][slot][head][dim]
+ *   TOPKV_LAYOUT_POOL_HEAD_MAJOR  `pool` geometry, but each page plane is
+ *                                 [head][slot][dim] (each head's slots adjacent)
+ * Pool views also give `layer`, `block_tables` (device int32
+ * [num_reqs][bt_stride]) and `head_begin`, the first of the head_count moved
+ * heads.  Packed views ignore those fields.
+ *
+ * For every request r, kept token t (the last `window` tokens when window > 0,
+ * Sec. 2.2; all of them when 0), plane c, j < head_count and dim d:
+ *   dst(r, t, c, dst.head_begin + j, d) = src(r, t, c, src.head_begin + j, d).
+ * Token t of a pool view is page block_tables[r][t / page_size], slot
+ * t % page_size of that pool (Sec. 6).  Nothing else in a destination pool is
+ * written.  Cases: head-sliced pack (pool -> packed, the heads of one
+ * tensor-parallel shard), head-sliced unpack (packed -> pool), re-blocking
+ * between page sizes with no staging buffer (pool -> pool), and head-major
+ * pools on either side.
+ *
+ * Requirements: at least one side is a pool; pool sides agree on planes,
+ * head_dim and elem_bytes (page size, page count, head count and layer count
+ * may differ); 1 <= head_count <= num_heads - head_begin on each pool side;
+ * 0 <= num_reqs <= TOPKV_MAX_BATCH_REQS; seq_lens is device int32 [num_reqs].
+ * Lengths are clamped on the device to [0, min over pool sides of
+ * bt_stride * page_size]; entries outside [0, num_pages) are skipped, and so
+ * are packed pieces past `bytes`.  src and dst must not overlap.
+ * Errors: TOPKV_ERR_INVALID_ARG for bad descriptors or arguments,
+ * TOPKV_ERR_UNSUPPORTED when a launch would address 2^31 or more pieces
+ * (num_reqs * max tokens * planes * head_count * head_dim * elem_bytes / piece
+ * width), TOPKV_ERR_LAUNCH if the launch fails.  One kernel on the stream;
+ * the call does not synchronise. */
+typedef enum topkv_layout {
+    TOPKV_LAYOUT_PACKED = 0,
+    TOPKV_LAYOUT_POOL = 1,
+    TOPKV_LAYOUT_POOL_HEAD_MAJOR = 2
+} topkv_layout_t;
+
+typedef struct topkv_view {
+    int32_t layout;               /* topkv_layout_t */
+    int32_t layer;                /* pool views: layer index */
+    int32_t head_begin;           /* pool views: first moved head */
+    int32_t bt_stride;            /* pool views: entries per block-table row */
+    const int32_t* block_tables;  /* pool views: device [num_reqs][bt_stride] */
+    topkv_pool_t pool;            /* pool views: geometry and base */
+    void* data;                   /* packed views: device buffer */
+    int64_t bytes;                /* packed views: capacity in bytes */
+} topkv_view_t;
+
+topkv_status_t topkv_move_layer(const topkv_view_t* src, const topkv_view_t* dst, int32_t num_reqs,
+                                const int32_t* seq_lens, int32_t head_count, int32_t window,
+                                hipStream_t stream);
+
+/* Head-sliced pack: heads [head_begin, head_begin + head_count) of layer
+ * `layer` of a slot-major pool into dst ([planes][n_r][head_count][dim] per
+ * request, requests concatenated; dst_bytes is its capacity).  Same as
+ * topkv_move_layer(pool view, packed view, ..., window 0). */
+topkv_status_t topkv_pack_layer_heads(const topkv_pool_t* src, int32_t layer, int32_t num_reqs,
+                                      const int32_t* block_tables, int32_t bt_stride, const int32_t* seq_lens,
+                                      int32_t head_begin, int32_t head_count, void* dst, int64_t dst_bytes,
+                                      hipStream_t stream);
+
+/* Head-sliced unpack: the inverse, into heads [head_begin, +head_count) of a
+ * slot-major pool; the pool's other heads are not written. */
+topkv_status_t topkv_unpack_layer_heads(const void* src, int64_t src_bytes, const topkv_pool_t* dst,
+                                        int32_t layer, int32_t num_reqs, const int32_t* block_tables,
+                                        int32_t bt_stride, const int32_t* seq_lens, int32_t head_begin,
+                                        int32_t head_count, hipStream_t stream);
+
+/* Pool-to-pool re-blocking: every head of layer src_layer of `src` (page size
+ * P, tables src_tables) into layer dst_layer of `dst` (page size P', tables
+ * dst_tables), with no packed staging buffer.  Both pools have the same
+ * planes, heads, head_dim and elem_bytes. */
+topkv_status_t topkv_reblock_layer(const topkv_pool_t* src, int32_t src_layer, const int32_t* src_tables,
+                                   int32_t src_stride, const topkv_pool_t* dst, int32_t dst_layer,
+                                   const int32_t* dst_tables, int32_t dst_stride, int32_t num_reqs,
+                                   const int32_t* seq_lens, hipStream_t stream);
+
 /* Layer shipper (Sec. 5.2: layer l's cache leaves while layers l+1 .. L still
  * compute).  Copies run on the GPU's DMA engines (ROCr asynchronous copies),
  * so they take no compute unit from the kernels still running; a worker

@@ -1,0 +1,527 @@
+// reshard.hip - one layer moved between cache layouts on gfx950: head-sliced
+// pack and unpack (a tensor-parallel shard's heads), pool-to-pool
+// re-blocking between page sizes without a staging buffer, and pools whose
+// pages are head-major.  The layouts and the entry points are specified in
+// include/topkv.h (per-layer unit: Section 5.2; K-then-V token-major wire
+// order: Section 3.5; paged pools: Section 6; KV heads per layer: Sections
+// 2.2 and 5.3).
+//
+// Design.  Every move copies, per request, kept token and plane, the moved
+// heads' values.  The unit of contiguity is a granule: one head's head_dim
+// values, or all moved heads at once when both sides keep heads adjacent (a
+// packed buffer and a slot-major pool do, a head-major pool does not).  The
+// work is flattened in the packed order (request, plane, token, granule,
+// 16-byte piece), so
+//   * a packed side's address is simply piece index * piece bytes, and both
+//     sides walk consecutive bytes across consecutive lanes wherever their
+//     layout allows (a head-major side still gets whole granules);
+//   * the request comes from a binary search over per-request prefix sums
+//     held in LDS (built with a wave64 shuffle scan from the device lengths),
+//     every other index from multiply-high divisions by launch constants;
+//   * when a token's pieces fill whole wave spans (every 70B-class shape),
+//     request, plane, token and page are wave-uniform: they are computed once
+//     per wave in scalar registers and the block-table entries come through
+//     scalar loads, the last one reused while the page does not change.
+// Granules are at least one head's values (256 bytes for head_dim 128 in
+// bf16), so both sides touch whole cache lines: no LDS staging of the data is
+// needed even where the layout transposes (slot-major <-> head-major).
+// Each lane issues all of its loads before its stores; workgroups stride over
+// tiles on a grid capped at a few workgroups per CU.  Table entries and
+// lengths are bounds-checked on the device before any access.
+#include <hip/hip_runtime.h>
+
+#include <atomic>
+#include <cstdint>
+
+#include "topkv.h"
+
+namespace topkv_reshard {
+
+#ifndef TOPKV_RS_VPT
+#define TOPKV_RS_VPT 8            // pieces per lane per tile
+#endif
+#ifndef TOPKV_RS_WG_PER_CU
+#define TOPKV_RS_WG_PER_CU 16     // grid cap = CUs * this
+#endif
+
+constexpr int kThreads = 256;
+constexpr int kWaves = kThreads / 64;
+constexpr int kVpt = TOPKV_RS_VPT;
+constexpr int kWgPerCu = TOPKV_RS_WG_PER_CU;
+
+template <int B> struct Vec;
+template <> struct Vec<16> { typedef unsigned int type __attribute__((ext_vector_type(4))); };
+template <> struct Vec<8> { typedef unsigned int type __attribute__((ext_vector_type(2))); };
+template <> struct Vec<4> { typedef unsigned int type; };
+template <> struct Vec<2> { typedef unsigned short type; };
+template <> struct Vec<1> { typedef unsigned char type; };
+
+// n / d for 0 <= n < 2^31 by a multiply-high (Granlund and Montgomery, 1994):
+// with s = ceil(log2 d) and m = floor(2^32 (2^s - d) / d) + 1, the quotient is
+// (mulhi(n, m) + n) >> s; the sum cannot overflow because mulhi(n, m) <= n.
+struct FastDiv {
+  uint32_t d, m, s;
+};
+
+FastDiv make_div(uint32_t d) {
+  uint32_t s = 0;
+  while ((1ull << s) < d) ++s;
+  const uint64_t m = (((1ull << 32) * ((1ull << s) - d)) / d) + 1;
+  return FastDiv{d, (uint32_t)m, s};
+}
+
+__device__ __forceinline__ uint32_t fdiv(uint32_t n, const FastDiv& f) {
+  return (__umulhi(n, f.m) + n) >> f.s;
+}
+
+// One side of a move (kernel argument, by value).
+struct Side {
+  char* base;               // pool: the layer slab; packed: the buffer
+  const int32_t* tables;    // pool: [num_reqs][bt_stride]
+  int64_t page_bytes;
+  int64_t plane_bytes;
+  int64_t head0_bytes;      // offset of the first moved head within a slot
+  int64_t num_pages;        // valid page indices are [0, num_pages)
+  int32_t slot_bytes;       // stride between slots of a page plane
+  int32_t gran_stride;      // stride between consecutive granules of a slot
+  int32_t bt_stride;
+  int32_t packed;           // 1: packed buffer, address = piece index * VB
+  FastDiv page;             // tokens per page
+};
+
+struct Params {
+  Side src, dst;
+  int64_t packed_cap;       // bytes of the packed side (if any)
+  FastDiv vpg;              // pieces per granule
+  FastDiv gpt;              // granules per (token, plane)
+  FastDiv ktp;              // pieces per (token, plane) = gpt * vpg
+  int32_t num_reqs;
+  int32_t planes;
+  int32_t window;
+  int32_t max_tok;          // lengths are clamped to [0, max_tok]
+};
+
+// Per-request kept-token counts and first kept tokens, and the exclusive
+// prefix of planes * count (token-planes before request r), into LDS.
+__device__ void request_prefix(const Params& p, const int32_t* __restrict__ seq_lens, int32_t* tp,
+                               int32_t* st, int32_t* cnt, int32_t* wsum) {
+  const int lane = threadIdx.x & 63;
+  const int wave = threadIdx.x >> 6;
+  int32_t carry = 0;
+  for (int base = 0; base < p.num_reqs; base += kThreads) {
+    const int r = base + threadIdx.x;
+    int32_t v = 0;
+    if (r < p.num_reqs) {
+      int32_t n = seq_lens[r];
+      n = n < 0 ? 0 : (n > p.max_tok ? p.max_tok : n);
+      const int32_t start = (p.window > 0 && n > p.window) ? n - p.window : 0;
+      st[r] = start;
+      cnt[r] = n - start;
+      v = (n - start) * p.planes;
+    }
+    int32_t x = v;
+#pragma unroll
+    for (int d = 1; d < 64; d <<= 1) {
+      const int32_t y = __shfl_up(x, d, 64);
+      if (lane >= d) x += y;
+    }
+    if (lane == 63) wsum[wave] = x;
+    __syncthreads();
+    int32_t before = carry, chunk = 0;
+#pragma unroll
+    for (int w = 0; w < kWaves; ++w) {
+      if (w < wave) before += wsum[w];
+      chunk += wsum[w];
+    }
+    if (r < p.num_reqs) tp[r] = before + x - v;
+    carry += chunk;
+    __syncthreads();
+  }
+  if (threadIdx.x == 0) tp[p.num_reqs] = carry;
+  __syncthreads();
+}
+
+// Byte offset of piece (r, c, t, k, e) on a pool side; false if the table
+// entry is out of range.
+__device__ __forceinline__ bool pool_offset(const Side& s, int32_t r, uint32_t c, uint32_t t, uint32_t k,
+                                            uint32_t e_bytes, int64_t* off) {
+  const uint32_t i = fdiv(t, s.page);
+  const uint32_t slot = t - i * s.page.d;
+  const int32_t page = s.tables[(int64_t)r * s.bt_stride + i];
+  if (page < 0 || (int64_t)page >= s.num_pages) return false;
+  *off = (int64_t)page * s.page_bytes + (int64_t)c * s.plane_bytes + (int64_t)slot * s.slot_bytes +
+         s.head0_bytes + (int64_t)k * s.gran_stride + e_bytes;
+  return true;
+}
+
+struct Loc {
+  int32_t r;                // request
+  uint32_t c, t;            // plane, token
+};
+
+// Request, plane and token of global (request, plane, token) index q2: the
+// largest r with tp[r] <= q2 owns it (its count is then > 0), and the plane
+// is the number of whole token runs below q2 within the request.
+__device__ __forceinline__ Loc locate(uint32_t q2, const int32_t* tp, const int32_t* st, const int32_t* cnt,
+                                      int32_t num_reqs) {
+  int lo = 0, hi = num_reqs - 1;
+  while (lo < hi) {
+    const int mid = (lo + hi + 1) >> 1;
+    if ((uint32_t)tp[mid] <= q2) lo = mid; else hi = mid - 1;
+  }
+  uint32_t local = q2 - (uint32_t)tp[lo];
+  const uint32_t n_r = (uint32_t)cnt[lo];
+  uint32_t c = 0;
+  while (local >= n_r) { local -= n_r; ++c; }
+  return Loc{lo, c, (uint32_t)st[lo] + local};
+}
+
+// Page lookups of one side for wave-uniform tokens.  Block tables are never
+// written while a move runs, so they are read through the constant address
+// space (scalar loads and the scalar cache); consecutive wave spans of a tile
+// usually sit on the same page, so the last entry is kept.
+struct PageCache {
+  int32_t r = -1;
+  uint32_t i = 0;
+  int32_t page = -1;
+};
+
+typedef __attribute__((address_space(4))) const int32_t ConstInt;
+
+// pool_offset for a wave-uniform (request, plane, token): the page lookup and
+// everything but the piece's place inside the token's granules are uniform.
+__device__ __forceinline__ bool pool_offset_wave(const Side& s, const Loc& at, uint32_t k, uint32_t e_bytes,
+                                                 PageCache& pc, int64_t* off) {
+  const uint32_t i = fdiv(at.t, s.page);
+  const uint32_t slot = at.t - i * s.page.d;
+  if (at.r != pc.r || i != pc.i) {
+    const ConstInt* tab = (const ConstInt*)s.tables;
+    pc.page = __builtin_amdgcn_readfirstlane(tab[(int64_t)at.r * s.bt_stride + i]);
+    pc.r = at.r;
+    pc.i = i;
+  }
+  const int32_t page = pc.page;
+  if (page < 0 || (int64_t)page >= s.num_pages) return false;
+  const int64_t base = (int64_t)page * s.page_bytes + (int64_t)at.c * s.plane_bytes +
+                       (int64_t)slot * s.slot_bytes + s.head0_bytes;
+  *off = base + (int64_t)k * s.gran_stride + e_bytes;
+  return true;
+}
+
+// kWave: the pieces of one (request, plane, token) fill whole 64-piece wave
+// spans (pieces per token-plane divisible by 64), so every wave instruction
+// has one request, plane, token and page per side: those are found once per
+// wave, with uniform (scalar) arithmetic and loads, and only the piece's
+// place inside the token's granules varies across lanes.  Otherwise every
+// lane locates its own piece.
+template <int VB, bool kWave>
+__global__ __launch_bounds__(kThreads) void kv_reshard_kernel(Params p, const int32_t* __restrict__ seq_lens) {
+  typedef typename Vec<VB>::type V;
+  extern __shared__ int32_t lds_i32[];
+  int32_t* wsum = lds_i32;                     // [kWaves]
+  int32_t* tp = wsum + kWaves;                 // [num_reqs + 1]
+  int32_t* st = tp + (p.num_reqs + 1);         // [num_reqs]
+  int32_t* cnt = st + p.num_reqs;              // [num_reqs]
+  request_prefix(p, seq_lens, tp, st, cnt, wsum);
+
+  const uint32_t per_tp = p.ktp.d;                            // pieces per (token, plane)
+  const uint32_t total = (uint32_t)tp[p.num_reqs] * per_tp;   // the host keeps this below 2^31
+  constexpr uint32_t kTile = (uint32_t)kThreads * kVpt;
+  const uint32_t lane = threadIdx.x & 63u;
+  const uint32_t wave_first = __builtin_amdgcn_readfirstlane(threadIdx.x & ~63u);
+
+  PageCache src_pc, dst_pc;
+  for (uint32_t base = blockIdx.x * kTile; base < total; base += gridDim.x * kTile) {
+    V v[kVpt];
+    int64_t doff[kVpt];
+    bool ok[kVpt];
+#pragma unroll
+    for (int j = 0; j < kVpt; ++j) {
+      doff[j] = 0;
+      ok[j] = false;
+      if (kWave) {
+        const uint32_t wbase = base + j * kThreads + wave_first;   // uniform
+        if (wbase >= total) continue;                               // the whole span is past the end
+        const uint32_t q2 = fdiv(wbase, p.ktp);
+        const uint32_t m = wbase - q2 * per_tp + lane;              // < per_tp
+        const uint32_t k = fdiv(m, p.vpg);
+        const uint32_t e = m - k * p.vpg.d;
+        Loc at = locate(q2, tp, st, cnt, p.num_reqs);
+        at.r = __builtin_amdgcn_readfirstlane(at.r);
+        at.c = __builtin_amdgcn_readfirstlane(at.c);
+        at.t = __builtin_amdgcn_readfirstlane(at.t);
+        const uint32_t idx = wbase + lane;
+        int64_t soff = (int64_t)idx * VB, o = (int64_t)idx * VB;
+        bool good = true;
+        if (!p.src.packed) good = pool_offset_wave(p.src, at, k, e * VB, src_pc, &soff);
+        else good = soff + VB <= p.packed_cap;
+        if (!p.dst.packed) good = good && pool_offset_wave(p.dst, at, k, e * VB, dst_pc, &o);
+        else good = good && o + VB <= p.packed_cap;
+        ok[j] = good;
+        doff[j] = o;
+        if (good) v[j] = __builtin_nontemporal_load(reinterpret_cast<const V*>(p.src.base + soff));
+      } else {
+        const uint32_t idx = base + j * kThreads + threadIdx.x;
+        if (idx >= total) continue;
+        const uint32_t q = fdiv(idx, p.vpg);
+        const uint32_t e = idx - q * p.vpg.d;
+        const uint32_t q2 = fdiv(q, p.gpt);
+        const uint32_t k = q - q2 * p.gpt.d;
+        const Loc at = locate(q2, tp, st, cnt, p.num_reqs);
+        int64_t soff = (int64_t)idx * VB, o = (int64_t)idx * VB;
+        bool good = true;
+        if (!p.src.packed) good = pool_offset(p.src, at.r, at.c, at.t, k, e * VB, &soff);
+        else good = soff + VB <= p.packed_cap;
+        if (!p.dst.packed) good = good && pool_offset(p.dst, at.r, at.c, at.t, k, e * VB, &o);
+        else good = good && o + VB <= p.packed_cap;
+        ok[j] = good;
+        doff[j] = o;
+        if (good) v[j] = __builtin_nontemporal_load(reinterpret_cast<const V*>(p.src.base + soff));
+      }
+    }
+#pragma unroll
+    for (int j = 0; j < kVpt; ++j)
+      if (ok[j]) __builtin_nontemporal_store(v[j], reinterpret_cast<V*>(p.dst.base + doff[j]));
+  }
+}
+
+// ---------------------------------------------------------------------------
+// Host side
+// ---------------------------------------------------------------------------
+
+constexpr int kMaxDevices = 64;
+std::atomic<int> g_cus[kMaxDevices];
+
+topkv_status_t cu_count(int* out) {
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0) return TOPKV_ERR_DEVICE;
+  const int cached = dev < kMaxDevices ? g_cus[dev].load(std::memory_order_relaxed) : 0;
+  if (cached > 0) { *out = cached; return TOPKV_OK; }
+  int cus = 0;
+  if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || cus <= 0)
+    return TOPKV_ERR_DEVICE;
+  if (dev < kMaxDevices) g_cus[dev].store(cus, std::memory_order_relaxed);
+  *out = cus;
+  return TOPKV_OK;
+}
+
+struct PoolInfo {
+  int64_t head_bytes, slot_bytes, plane_bytes, page_bytes, layer_bytes;
+};
+
+// Strides of a pool view in its layout, after validating the descriptor.
+topkv_status_t pool_info(const topkv_view_t* v, int32_t head_count, PoolInfo* g) {
+  const topkv_pool_t& pl = v->pool;
+  if (!pl.base || pl.num_pages <= 0 || pl.num_layers <= 0 || pl.page_size <= 0 || pl.planes <= 0 ||
+      pl.num_heads <= 0 || pl.head_dim <= 0)
+    return TOPKV_ERR_INVALID_ARG;
+  if (pl.elem_bytes != 1 && pl.elem_bytes != 2 && pl.elem_bytes != 4 && pl.elem_bytes != 8)
+    return TOPKV_ERR_INVALID_ARG;
+  if (v->layer < 0 || v->layer >= pl.num_layers || v->bt_stride <= 0 || v->head_begin < 0 ||
+      head_count > pl.num_heads - v->head_begin)
+    return TOPKV_ERR_INVALID_ARG;
+  int64_t head, row, plane, page, layer, all;
+  if (__builtin_mul_overflow((int64_t)pl.head_dim, (int64_t)pl.elem_bytes, &head) ||
+      __builtin_mul_overflow(head, (int64_t)pl.num_heads, &row) ||
+      __builtin_mul_overflow(row, (int64_t)pl.page_size, &plane) ||
+      __builtin_mul_overflow(plane, (int64_t)pl.planes, &page) ||
+      __builtin_mul_overflow(page, pl.num_pages, &layer) ||
+      __builtin_mul_overflow(layer, (int64_t)pl.num_layers, &all))
+    return TOPKV_ERR_UNSUPPORTED;
+  if (plane > INT32_MAX || pl.num_pages > INT32_MAX) return TOPKV_ERR_UNSUPPORTED;
+  const bool head_major = v->layout == TOPKV_LAYOUT_POOL_HEAD_MAJOR;
+  g->head_bytes = head_major ? head * pl.page_size : head;
+  g->slot_bytes = head_major ? head : row;
+  g->plane_bytes = plane;
+  g->page_bytes = page;
+  g->layer_bytes = layer;
+  return TOPKV_OK;
+}
+
+bool valid_layout(int32_t l) {
+  return l == TOPKV_LAYOUT_PACKED || l == TOPKV_LAYOUT_POOL || l == TOPKV_LAYOUT_POOL_HEAD_MAJOR;
+}
+
+typedef void (*KernelFn)(Params, const int32_t*);
+
+template <bool kWave>
+KernelFn kernel_for_mode(int vb) {
+  switch (vb) {
+    case 16: return kv_reshard_kernel<16, kWave>;
+    case 8: return kv_reshard_kernel<8, kWave>;
+    case 4: return kv_reshard_kernel<4, kWave>;
+    case 2: return kv_reshard_kernel<2, kWave>;
+    default: return kv_reshard_kernel<1, kWave>;
+  }
+}
+
+KernelFn kernel_for(int vb, bool wave) { return wave ? kernel_for_mode<true>(vb) : kernel_for_mode<false>(vb); }
+
+topkv_status_t move_layer(const topkv_view_t* src, const topkv_view_t* dst, int32_t num_reqs,
+                          const int32_t* seq_lens, int32_t head_count, int32_t window, hipStream_t stream) {
+  if (!src || !dst || !valid_layout(src->layout) || !valid_layout(dst->layout)) return TOPKV_ERR_INVALID_ARG;
+  if (src->layout == TOPKV_LAYOUT_PACKED && dst->layout == TOPKV_LAYOUT_PACKED) return TOPKV_ERR_INVALID_ARG;
+  if (num_reqs < 0 || head_count <= 0 || window < 0 || (num_reqs > 0 && !seq_lens)) return TOPKV_ERR_INVALID_ARG;
+  if (num_reqs > TOPKV_MAX_BATCH_REQS) return TOPKV_ERR_UNSUPPORTED;
+
+  const topkv_view_t* sides[2] = {src, dst};
+  const topkv_pool_t* geo = nullptr;     // geometry both pool sides share
+  PoolInfo info[2] = {};
+  int64_t packed_cap = 0;
+  int64_t max_tok = INT32_MAX;
+  for (int i = 0; i < 2; ++i) {
+    const topkv_view_t* v = sides[i];
+    if (v->layout == TOPKV_LAYOUT_PACKED) {
+      if (v->bytes < 0 || (v->bytes > 0 && !v->data)) return TOPKV_ERR_INVALID_ARG;
+      packed_cap = v->bytes;
+      continue;
+    }
+    const topkv_status_t st = pool_info(v, head_count, &info[i]);
+    if (st != TOPKV_OK) return st;
+    if (num_reqs > 0 && !v->block_tables) return TOPKV_ERR_INVALID_ARG;
+    if (geo && (geo->planes != v->pool.planes || geo->head_dim != v->pool.head_dim ||
+                geo->elem_bytes != v->pool.elem_bytes))
+      return TOPKV_ERR_INVALID_ARG;
+    geo = &v->pool;
+    const int64_t cap = (int64_t)v->bt_stride * v->pool.page_size;
+    if (cap < max_tok) max_tok = cap;
+  }
+  if (num_reqs == 0) return TOPKV_OK;
+
+  // Heads ride together in one granule when both sides keep them adjacent.
+  const int64_t head = (int64_t)geo->head_dim * geo->elem_bytes;
+  bool adjacent = true;
+  for (int i = 0; i < 2; ++i)
+    if (sides[i]->layout == TOPKV_LAYOUT_POOL_HEAD_MAJOR) adjacent = false;
+  const int64_t heads_per_gran = adjacent ? head_count : 1;
+  const int64_t gran = heads_per_gran * head;
+  // Piece width: every stride and base the pieces are addressed with.
+  int vb = 16;
+  for (; vb > 1; vb >>= 1) {
+    bool fits = gran % vb == 0;
+    for (int i = 0; i < 2 && fits; ++i) {
+      const topkv_view_t* v = sides[i];
+      if (v->layout == TOPKV_LAYOUT_PACKED) {
+        fits = reinterpret_cast<uintptr_t>(v->data) % vb == 0;
+      } else {
+        const uintptr_t b = reinterpret_cast<uintptr_t>(v->pool.base);
+        fits = b % vb == 0 && info[i].layer_bytes % vb == 0 && info[i].page_bytes % vb == 0 &&
+               info[i].plane_bytes % vb == 0 && info[i].slot_bytes % vb == 0 && info[i].head_bytes % vb == 0;
+      }
+    }
+    if (fits) break;
+  }
+  const int64_t vpg = gran / vb;
+  const int64_t gpt = head_count / heads_per_gran;
+  // Upper bound of pieces in the launch; indices are 32-bit in the kernel.
+  const int64_t bound = (int64_t)num_reqs * max_tok * geo->planes * gpt * vpg;
+  if (max_tok <= 0) return TOPKV_OK;
+  if (bound >= ((int64_t)1 << 31) || vpg >= ((int64_t)1 << 31)) return TOPKV_ERR_UNSUPPORTED;
+
+  Params p = {};
+  for (int i = 0; i < 2; ++i) {
+    const topkv_view_t* v = sides[i];
+    Side& s = i == 0 ? p.src : p.dst;
+    if (v->layout == TOPKV_LAYOUT_PACKED) {
+      s.base = static_cast<char*>(v->data);
+      s.packed = 1;
+      s.page = make_div(1);
+      continue;
+    }
+    s.base = static_cast<char*>(v->pool.base) + (int64_t)v->layer * info[i].layer_bytes;
+    s.tables = v->block_tables;
+    s.page_bytes = info[i].page_bytes;
+    s.plane_bytes = info[i].plane_bytes;
+    s.head0_bytes = (int64_t)v->head_begin * info[i].head_bytes;
+    s.num_pages = v->pool.num_pages;
+    s.slot_bytes = (int32_t)info[i].slot_bytes;
+    s.gran_stride = (int32_t)(heads_per_gran * info[i].head_bytes);
+    s.bt_stride = v->bt_stride;
+    s.page = make_div((uint32_t)v->pool.page_size);
+  }
+  p.packed_cap = packed_cap;
+  p.vpg = make_div((uint32_t)vpg);
+  p.gpt = make_div((uint32_t)gpt);
+  p.ktp = make_div((uint32_t)(gpt * vpg));
+  p.num_reqs = num_reqs;
+  p.planes = geo->planes;
+  p.window = window;
+  p.max_tok = (int32_t)max_tok;
+
+  int cus = 0;
+  const topkv_status_t st = cu_count(&cus);
+  if (st != TOPKV_OK) return st;
+  const int64_t tile = (int64_t)kThreads * kVpt;
+  int64_t blocks = (bound + tile - 1) / tile;
+  if (blocks > (int64_t)cus * kWgPerCu) blocks = (int64_t)cus * kWgPerCu;
+  if (blocks < 1) blocks = 1;
+  const size_t lds = sizeof(int32_t) * (kWaves + 3 * (size_t)num_reqs + 1);
+  const bool wave = (gpt * vpg) % 64 == 0;
+  hipLaunchKernelGGL(kernel_for(vb, wave), dim3((unsigned)blocks), dim3(kThreads), lds, stream, p, seq_lens);
+  return hipGetLastError() == hipSuccess ? TOPKV_OK : TOPKV_ERR_LAUNCH;
+}
+
+topkv_view_t pool_view(int32_t layout, const topkv_pool_t* pool, int32_t layer, const int32_t* tables,
+                       int32_t bt_stride, int32_t head_begin) {
+  topkv_view_t v = {};
+  v.layout = layout;
+  v.layer = layer;
+  v.head_begin = head_begin;
+  v.bt_stride = bt_stride;
+  v.block_tables = tables;
+  v.pool = *pool;
+  return v;
+}
+
+topkv_view_t packed_view(const void* data, int64_t bytes) {
+  topkv_view_t v = {};
+  v.layout = TOPKV_LAYOUT_PACKED;
+  v.data = const_cast<void*>(data);
+  v.bytes = bytes;
+  return v;
+}
+
+}  // namespace topkv_reshard
+
+using namespace topkv_reshard;
+
+extern "C" {
+
+topkv_status_t topkv_move_layer(const topkv_view_t* src, const topkv_view_t* dst, int32_t num_reqs,
+                                const int32_t* seq_lens, int32_t head_count, int32_t window,
+                                hipStream_t stream) {
+  return move_layer(src, dst, num_reqs, seq_lens, head_count, window, stream);
+}
+
+topkv_status_t topkv_pack_layer_heads(const topkv_pool_t* src, int32_t layer, int32_t num_reqs,
+                                      const int32_t* block_tables, int32_t bt_stride, const int32_t* seq_lens,
+                                      int32_t head_begin, int32_t head_count, void* dst, int64_t dst_bytes,
+                                      hipStream_t stream) {
+  if (!src) return TOPKV_ERR_INVALID_ARG;
+  const topkv_view_t s = pool_view(TOPKV_LAYOUT_POOL, src, layer, block_tables, bt_stride, head_begin);
+  const topkv_view_t d = packed_view(dst, dst_bytes);
+  return move_layer(&s, &d, num_reqs, seq_lens, head_count, 0, stream);
+}
+
+topkv_status_t topkv_unpack_layer_heads(const void* src, int64_t src_bytes, const topkv_pool_t* dst,
+                                        int32_t layer, int32_t num_reqs, const int32_t* block_tables,
+                                        int32_t bt_stride, const int32_t* seq_lens, int32_t head_begin,
+                                        int32_t head_count, hipStream_t stream) {
+  if (!dst) return TOPKV_ERR_INVALID_ARG;
+  const topkv_view_t s = packed_view(src, src_bytes);
+  const topkv_view_t d = pool_view(TOPKV_LAYOUT_POOL, dst, layer, block_tables, bt_stride, head_begin);
+  return move_layer(&s, &d, num_reqs, seq_lens, head_count, 0, stream);
+}
+
+topkv_status_t topkv_reblock_layer(const topkv_pool_t* src, int32_t src_layer, const int32_t* src_tables,
+                                   int32_t src_stride, const topkv_pool_t* dst, int32_t dst_layer,
+                                   const int32_t* dst_tables, int32_t dst_stride, int32_t num_reqs,
+                                   const int32_t* seq_lens, hipStream_t stream) {
+  if (!src || !dst) return TOPKV_ERR_INVALID_ARG;
+  if (src->num_heads != dst->num_heads) return TOPKV_ERR_INVALID_ARG;
+  const topkv_view_t s = pool_view(TOPKV_LAYOUT_POOL, src, src_layer, src_tables, src_stride, 0);
+  const topkv_view_t d = pool_view(TOPKV_LAYOUT_POOL, dst, dst_layer, dst_tables, dst_stride, 0);
+  return move_layer(&s, &d, num_reqs, seq_lens, src->num_heads, 0, stream);
+}
+
+}  // extern "C"

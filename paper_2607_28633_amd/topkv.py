@@ -43,7 +43,12 @@ EXPORTS = ["topkv_pack_layer", "topkv_unpack_layer", "topkv_pack_layer_batched",
            "topkv_unpack_layer_planes", "topkv_kvcache1_bytes", "topkv_kvcache1_workspace_bytes",
            "topkv_kvcache1_pack_layer", "topkv_kvcache1_seal", "topkv_kvcache1_verify",
            "topkv_kvcache1_unpack_layer", "topkv_crc64", "topkv_crc64_workspace_bytes", "topkv_dma_create",
-           "topkv_dma_submit", "topkv_dma_wait", "topkv_dma_destroy"]
+           "topkv_dma_submit", "topkv_dma_wait", "topkv_dma_destroy", "topkv_move_layer",
+           "topkv_pack_layer_heads", "topkv_unpack_layer_heads", "topkv_reblock_layer"]
+
+TOPKV_LAYOUT_PACKED = 0
+TOPKV_LAYOUT_POOL = 1
+TOPKV_LAYOUT_POOL_HEAD_MAJOR = 2
 
 
 class topkv_pool_t(ctypes.Structure):
@@ -51,6 +56,12 @@ class topkv_pool_t(ctypes.Structure):
                 ("num_layers", ctypes.c_int32), ("page_size", ctypes.c_int32),
                 ("planes", ctypes.c_int32), ("num_heads", ctypes.c_int32),
                 ("head_dim", ctypes.c_int32), ("elem_bytes", ctypes.c_int32)]
+
+
+class topkv_view_t(ctypes.Structure):
+    _fields_ = [("layout", ctypes.c_int32), ("layer", ctypes.c_int32), ("head_begin", ctypes.c_int32),
+                ("bt_stride", ctypes.c_int32), ("block_tables", ctypes.c_void_p), ("pool", topkv_pool_t),
+                ("data", ctypes.c_void_p), ("bytes", ctypes.c_int64)]
 
 
 class topkv_launch_t(ctypes.Structure):
@@ -89,6 +100,11 @@ _SIGS = {
     "topkv_kvcache1_unpack_layer": (_I32, [_P, _I64, _POOL, _I32, _P, _I32, _P]),
     "topkv_crc64": (_I32, [_P, _I64, _P, _I64, _P, _P]),
     "topkv_crc64_workspace_bytes": (_I64, [_I64]),
+    "topkv_move_layer": (_I32, [ctypes.POINTER(topkv_view_t), ctypes.POINTER(topkv_view_t), _I32, _P, _I32,
+                                _I32, _P]),
+    "topkv_pack_layer_heads": (_I32, [_POOL, _I32, _I32, _P, _I32, _P, _I32, _I32, _P, _I64, _P]),
+    "topkv_unpack_layer_heads": (_I32, [_P, _I64, _POOL, _I32, _I32, _P, _I32, _P, _I32, _I32, _P]),
+    "topkv_reblock_layer": (_I32, [_POOL, _I32, _P, _I32, _POOL, _I32, _P, _I32, _I32, _P, _P]),
     "topkv_dma_create": (_I32, [ctypes.POINTER(_P)]),
     "topkv_dma_submit": (_I32, [_P, _P, _P, _P, _I64, ctypes.POINTER(_I64)]),
     "topkv_dma_wait": (_I32, [_P, _I64]),
@@ -167,6 +183,30 @@ def pool_from_tensor(t: torch.Tensor) -> topkv_pool_t:
 
 def _pool_arg(pool) -> topkv_pool_t:
     return pool if isinstance(pool, topkv_pool_t) else pool_from_tensor(pool)
+
+
+def head_major_pool_from_tensor(t: torch.Tensor) -> topkv_pool_t:
+    """Descriptor of a 6-D head-major pool tensor [layers][pages][planes][heads][page_size][dim]."""
+    if t.dim() != 6:
+        raise ValueError("head-major pool tensor must be [layers][pages][planes][heads][page_size][dim]")
+    L, NP, C, H, P, D = t.shape
+    return make_pool(t, num_pages=NP, num_layers=L, page_size=P, planes=C, num_heads=H,
+                     head_dim=D, elem_bytes=t.element_size())
+
+
+def pool_view(pool, layer, block_tables, bt_stride, head_begin=0, head_major=False) -> topkv_view_t:
+    """A pool side of topkv_move_layer (a tensor in its layout, or a descriptor)."""
+    if isinstance(pool, topkv_pool_t):
+        desc = pool
+    else:
+        desc = head_major_pool_from_tensor(pool) if head_major else pool_from_tensor(pool)
+    layout = TOPKV_LAYOUT_POOL_HEAD_MAJOR if head_major else TOPKV_LAYOUT_POOL
+    return topkv_view_t(layout, int(layer), int(head_begin), int(bt_stride), _table_ptr(block_tables), desc, 0, 0)
+
+
+def packed_view(buf, nbytes=None) -> topkv_view_t:
+    """A packed side of topkv_move_layer."""
+    return topkv_view_t(TOPKV_LAYOUT_PACKED, 0, 0, 0, 0, topkv_pool_t(), _ptr(buf), _nbytes(buf, nbytes))
 
 
 def topkv_pack_layer(src, layer, block_table, seq_len, dst, stream=None) -> None:
@@ -380,6 +420,35 @@ def _any_ptr(x) -> int:
     return _ptr(x)
 
 
+def topkv_move_layer(src: topkv_view_t, dst: topkv_view_t, num_reqs, seq_lens, head_count, window=0,
+                     stream=None) -> None:
+    _check(_lib.topkv_move_layer(ctypes.byref(src), ctypes.byref(dst), int(num_reqs), _table_ptr(seq_lens),
+                                 int(head_count), int(window), _stream(stream)))
+
+
+def topkv_pack_layer_heads(src, layer, num_reqs, block_tables, bt_stride, seq_lens, head_begin, head_count, dst,
+                           dst_bytes=None, stream=None) -> None:
+    _check(_lib.topkv_pack_layer_heads(ctypes.byref(_pool_arg(src)), int(layer), int(num_reqs),
+                                       _table_ptr(block_tables), int(bt_stride), _table_ptr(seq_lens),
+                                       int(head_begin), int(head_count), _ptr(dst), _nbytes(dst, dst_bytes),
+                                       _stream(stream)))
+
+
+def topkv_unpack_layer_heads(src, dst, layer, num_reqs, block_tables, bt_stride, seq_lens, head_begin, head_count,
+                             src_bytes=None, stream=None) -> None:
+    _check(_lib.topkv_unpack_layer_heads(_ptr(src), _nbytes(src, src_bytes), ctypes.byref(_pool_arg(dst)),
+                                         int(layer), int(num_reqs), _table_ptr(block_tables), int(bt_stride),
+                                         _table_ptr(seq_lens), int(head_begin), int(head_count), _stream(stream)))
+
+
+def topkv_reblock_layer(src, src_layer, src_tables, src_stride, dst, dst_layer, dst_tables, dst_stride, num_reqs,
+                        seq_lens, stream=None) -> None:
+    _check(_lib.topkv_reblock_layer(ctypes.byref(_pool_arg(src)), int(src_layer), _table_ptr(src_tables),
+                                    int(src_stride), ctypes.byref(_pool_arg(dst)), int(dst_layer),
+                                    _table_ptr(dst_tables), int(dst_stride), int(num_reqs), _table_ptr(seq_lens),
+                                    _stream(stream)))
+
+
 def topkv_dma_create() -> int:
     h = _P()
     _check(_lib.topkv_dma_create(ctypes.byref(h)))
@@ -462,3 +531,19 @@ def prepare_unpack_layer_batched_ex(src, dst, layer, num_reqs, block_tables, bt_
                                     src_bytes=None, stream=None, start=None, stop=None) -> PreparedCall:
     return prepare_unpack_layer_window(src, dst, layer, num_reqs, block_tables, bt_stride, seq_lens, 0,
                                        src_bytes, stream, start, stop)
+
+
+def prepare_pack_layer_heads(src, layer, num_reqs, block_tables, bt_stride, seq_lens, head_begin, head_count, dst,
+                             dst_bytes=None, stream=None) -> PreparedCall:
+    pool = _pool_arg(src)
+    args = (ctypes.byref(pool), _I32(int(layer)), _I32(int(num_reqs)), _P(_table_ptr(block_tables)),
+            _I32(int(bt_stride)), _P(_table_ptr(seq_lens)), _I32(int(head_begin)), _I32(int(head_count)),
+            _P(_ptr(dst)), _I64(_nbytes(dst, dst_bytes)), _P(_stream(stream)))
+    return PreparedCall("topkv_pack_layer_heads", args, (pool,))
+
+
+def prepare_move_layer(src: topkv_view_t, dst: topkv_view_t, num_reqs, seq_lens, head_count, window=0,
+                       stream=None) -> PreparedCall:
+    args = (ctypes.byref(src), ctypes.byref(dst), _I32(int(num_reqs)), _P(_table_ptr(seq_lens)),
+            _I32(int(head_count)), _I32(int(window)), _P(_stream(stream)))
+    return PreparedCall("topkv_move_layer", args, (src, dst))

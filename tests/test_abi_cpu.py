@@ -133,3 +133,33 @@ def test_dma_shipper_validation(tk):
     assert lib.topkv_dma_wait(None, 1) == INV
     assert lib.topkv_dma_destroy(None) == INV
     assert t.value == -7
+
+
+def test_move_layer_validation(tk):
+    """Layout moves refuse bad views and arguments before any launch."""
+    INV, UNS = tk.TOPKV_ERR_INVALID_ARG, tk.TOPKV_ERR_UNSUPPORTED
+    bt, lens, buf = 0x20000, 0x30000, 0x40000
+    good = _pool(tk)
+    pv = tk.pool_view(good, 1, bt, 4)
+    pk = tk.packed_view(buf, 1 << 20)
+    _expect(tk, INV, tk.topkv_move_layer, pk, tk.packed_view(buf + 64, 1 << 20), 2, lens, 8)   # no pool side
+    bad = tk.pool_view(good, 1, bt, 4)
+    bad.layout = 7
+    _expect(tk, INV, tk.topkv_move_layer, bad, pk, 2, lens, 8)
+    _expect(tk, INV, tk.topkv_move_layer, pv, pk, 2, lens, 0)                  # head_count 0
+    _expect(tk, INV, tk.topkv_move_layer, tk.pool_view(good, 1, bt, 4, head_begin=5), pk, 2, lens, 4)
+    _expect(tk, INV, tk.topkv_move_layer, tk.pool_view(good, 2, bt, 4), pk, 2, lens, 8)   # layer >= L
+    _expect(tk, INV, tk.topkv_move_layer, tk.pool_view(good, 1, bt, 0), pk, 2, lens, 8)   # bt_stride 0
+    _expect(tk, INV, tk.topkv_move_layer, tk.pool_view(good, 1, 0, 4), pk, 2, lens, 8)    # null tables
+    _expect(tk, INV, tk.topkv_move_layer, pv, pk, 2, 0, 8)                     # null lengths
+    _expect(tk, INV, tk.topkv_move_layer, pv, pk, 2, lens, 8, window=-1)
+    _expect(tk, INV, tk.topkv_move_layer, pv, tk.packed_view(0, 64), 2, lens, 8)         # null packed data
+    _expect(tk, INV, tk.topkv_move_layer, pv, tk.pool_view(_pool(tk, base=0x900000, planes=1), 0, bt, 4),
+            2, lens, 8)                                                        # planes differ
+    _expect(tk, UNS, tk.topkv_move_layer, pv, pk, tk.TOPKV_MAX_BATCH_REQS + 1, lens, 8)
+    _expect(tk, UNS, tk.topkv_move_layer, tk.pool_view(good, 1, bt, 1 << 20), pk, 4096, lens, 8)  # 2^31 pieces
+    _expect(tk, INV, tk.topkv_pack_layer_heads, good, 1, 2, bt, 4, lens, 6, 3, buf, dst_bytes=1 << 20)
+    _expect(tk, INV, tk.topkv_unpack_layer_heads, buf, good, 1, 2, bt, 4, lens, -1, 2, src_bytes=1 << 20)
+    _expect(tk, INV, tk.topkv_reblock_layer, good, 0, bt, 4, _pool(tk, base=0x900000, num_heads=4), 0, bt, 4,
+            2, lens)
+    tk.topkv_move_layer(pv, pk, 0, 0, 8, stream=0)                             # no requests: nothing to launch

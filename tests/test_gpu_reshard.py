@@ -1,0 +1,258 @@
+"""Layer moves between layouts (head-sliced pack/unpack, pool-to-pool
+re-blocking, head-major pools) through the C ABI vs the CPU oracle, bit for
+bit: reduced pools element by element across tiles and ragged tails, edge
+cases (empty and one-token requests, odd widths, windows, malformed tables),
+and the 70B shapes at full size in the benchmark's launch configuration
+(sampled layers vs the oracle, the rest vs the full-head pack kernel)."""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import oracle.reshard as rs
+from gpu_util import say, to_dev, to_host
+from paper_2607_28633_amd.workloads import (device_dst_prefill, device_src_pool, host_dst_prefill,
+                                            host_src_pool, make_workload)
+
+pytestmark = pytest.mark.gpu
+
+SENTINEL = -9
+
+
+@pytest.fixture(scope="module")
+def tk():
+    from paper_2607_28633_amd import topkv
+    assert torch.cuda.is_available(), "GPU tests need a GPU"
+    return topkv
+
+
+def _heads_wl(**kw):
+    base = dict(num_layers=2, num_heads=8, head_dim=16, seq_lens=[37, 16, 0, 1, 50, 9, 300])
+    base.update(kw)
+    return make_workload("tiny", **base)
+
+
+WORKLOADS = {
+    "h8-d16": lambda: _heads_wl(),
+    "h8-d16-p5": lambda: _heads_wl(dst_page_size=5),
+    "h8-d128-p16-p64": lambda: _heads_wl(head_dim=128, dst_page_size=64, seq_lens=[700, 1, 64, 129]),
+    "h3-d3-odd": lambda: _heads_wl(num_heads=3, head_dim=3, dst_page_size=48),
+    "h4-d5-u8": lambda: _heads_wl(num_heads=4, head_dim=5, elem_bytes=1, dst_page_size=7),
+    "mla-p64-p16": lambda: make_workload("deepseek-v3-mla", num_layers=2, seq_lens=[700, 1, 64, 129, 0],
+                                         dst_page_size=16),
+}
+
+
+def _geom(wl):
+    return wl.planes, wl.num_heads, wl.head_dim
+
+
+@pytest.mark.parametrize("case", sorted(WORKLOADS))
+def test_pack_heads_parity(tk, case):
+    wl = WORKLOADS[case]()
+    say(f"[reshard] pack heads {case}: {wl.describe()}")
+    C, H, D = _geom(wl)
+    src_h = host_src_pool(wl)
+    src, bt, lens = to_dev(src_h), to_dev(wl.block_tables), to_dev(wl.seq_lens)
+    slices = sorted({(0, H), (H - 1, 1), (H // 2, H - H // 2), (0, 1), (min(1, H - 1), max(1, H - 2))})
+    for h0, hc in slices:
+        for layer in range(wl.num_layers):
+            n = rs.packed_heads_elems(C, hc, D, wl.seq_lens)
+            out = torch.full((n + 64,), SENTINEL, dtype=src.dtype, device="cuda")
+            tk.topkv_pack_layer_heads(src, layer, wl.num_reqs, bt, bt.shape[1], lens, h0, hc, out,
+                                      dst_bytes=n * wl.elem_bytes)
+            torch.cuda.synchronize()
+            got = to_host(out)
+            want = rs.pack_layer_heads(src_h, layer, wl.block_tables, wl.seq_lens, h0, hc)
+            assert np.array_equal(got[:n], want), f"{case} heads [{h0}, +{hc}) layer {layer}"
+            assert torch.equal(out[n:], torch.full_like(out[n:], SENTINEL)), f"{case}: write past the packed batch"
+
+
+@pytest.mark.parametrize("case", sorted(WORKLOADS))
+def test_unpack_heads_parity(tk, case):
+    wl = WORKLOADS[case]()
+    say(f"[reshard] unpack heads {case}")
+    C, H, D = _geom(wl)
+    dst_h = host_dst_prefill(wl)
+    dst, bt2, lens = to_dev(dst_h), to_dev(wl.dst_block_tables), to_dev(wl.seq_lens)
+    want = dst_h.copy()
+    rng = np.random.default_rng(5)
+    for h0, hc in sorted({(0, H), (H - 1, 1), (H // 2, H - H // 2)}):
+        n = rs.packed_heads_elems(C, hc, D, wl.seq_lens)
+        packed_h = rng.integers(0, 1 << (8 * wl.elem_bytes), n, dtype=np.uint64).astype(want.dtype)
+        layer = (h0 + hc) % wl.num_layers
+        tk.topkv_unpack_layer_heads(to_dev(packed_h), dst, layer, wl.num_reqs, bt2, bt2.shape[1], lens, h0, hc)
+        rs.unpack_layer_heads(packed_h, want, layer, wl.dst_block_tables, wl.seq_lens, h0, hc)
+    torch.cuda.synchronize()
+    assert np.array_equal(to_host(dst), want), f"{case}: pool after head-sliced unpacks differs"
+
+
+@pytest.mark.parametrize("case", sorted(WORKLOADS))
+@pytest.mark.parametrize("window", [0, 40])
+def test_reblock_parity(tk, case, window):
+    wl = WORKLOADS[case]()
+    say(f"[reshard] re-block {case} P={wl.page_size}->{wl.dst_page_size} W={window}")
+    src_h, dst_h = host_src_pool(wl), host_dst_prefill(wl)
+    src, dst = to_dev(src_h), to_dev(dst_h)
+    bt, bt2, lens = to_dev(wl.block_tables), to_dev(wl.dst_block_tables), to_dev(wl.seq_lens)
+    want = dst_h.copy()
+    for layer in range(wl.num_layers):
+        dl = (layer + 1) % wl.num_layers
+        if window:
+            tk.topkv_move_layer(tk.pool_view(src, layer, bt, bt.shape[1]), tk.pool_view(dst, dl, bt2, bt2.shape[1]),
+                                wl.num_reqs, lens, wl.num_heads, window)
+        else:
+            tk.topkv_reblock_layer(src, layer, bt, bt.shape[1], dst, dl, bt2, bt2.shape[1], wl.num_reqs, lens)
+        rs.reblock_layer(src_h, layer, wl.block_tables, want, dl, wl.dst_block_tables, wl.seq_lens, window)
+    torch.cuda.synchronize()
+    assert np.array_equal(to_host(dst), want), f"{case} W={window}: re-blocked pool differs"
+
+
+HM_CASES = [("pool", "hm", 0, 0, 0), ("hm", "packed", 1, 0, 0), ("hm", "pool", 2, 1, 7), ("hm", "hm", 0, 3, 0),
+            ("packed", "hm", 0, 2, 13), ("pool", "hm", 3, 5, 0)]
+
+
+@pytest.mark.parametrize("case", ["h8-d16-p5", "h8-d128-p16-p64", "h3-d3-odd", "h4-d5-u8"])
+def test_head_major_parity(tk, case):
+    wl = WORKLOADS[case]()
+    C, H, D = _geom(wl)
+    src_sm = host_src_pool(wl)
+    src_hm = rs.to_head_major(src_sm)
+    dst_sm = host_dst_prefill(wl)
+    dst_hm = rs.to_head_major(dst_sm)
+    tabs = {"src": wl.block_tables, "dst": wl.dst_block_tables}
+    for sk, dk, h0s, h0d, window in HM_CASES:
+        hc = max(1, min(H - h0s, H - h0d, 3 if (h0s or h0d) else H))
+        if h0s >= H or h0d >= H:
+            continue
+        say(f"[reshard] head-major {case}: {sk} -> {dk}, heads {h0s}/{h0d} +{hc}, W={window}")
+        n = rs.packed_heads_elems(C, hc, D, wl.seq_lens, window)
+        if sk == "packed":
+            s_h = rs.pack_layer_heads(src_sm, 1, wl.block_tables, wl.seq_lens, 0, hc, window)
+        else:
+            s_h = src_hm if sk == "hm" else src_sm
+        d_h = np.zeros(n, dtype=src_sm.dtype) if dk == "packed" else (dst_hm if dk == "hm" else dst_sm).copy()
+        lay = {"packed": rs.PACKED, "pool": rs.POOL, "hm": rs.POOL_HEAD_MAJOR}
+        want = rs.move_layer(rs.View(lay[sk], s_h, 1, tabs["src"], h0s if sk != "packed" else 0),
+                             rs.View(lay[dk], d_h.copy(), 0, tabs["dst"], h0d if dk != "packed" else 0),
+                             wl.seq_lens, hc, window)
+        s_d, d_d = to_dev(s_h), to_dev(d_h)
+        bt, bt2, lens = to_dev(wl.block_tables), to_dev(wl.dst_block_tables), to_dev(wl.seq_lens)
+        sv = (tk.packed_view(s_d) if sk == "packed" else
+              tk.pool_view(s_d, 1, bt, bt.shape[1], h0s, head_major=sk == "hm"))
+        dv = (tk.packed_view(d_d) if dk == "packed" else
+              tk.pool_view(d_d, 0, bt2, bt2.shape[1], h0d, head_major=dk == "hm"))
+        tk.topkv_move_layer(sv, dv, wl.num_reqs, lens, hc, window)
+        torch.cuda.synchronize()
+        assert np.array_equal(to_host(d_d), want), f"{case}: {sk} -> {dk} differs"
+
+
+def test_untrusted_tables_and_lengths(tk):
+    """Out-of-range table entries are skipped, lengths are clamped to the
+    table capacity and negative lengths count as zero; nothing else moves."""
+    wl = _heads_wl(seq_lens=[37, 16, 50, 9])
+    C, H, D = _geom(wl)
+    src_h = host_src_pool(wl)
+    bt_h = wl.block_tables.copy()
+    bt_h[0, 1] = -1                      # tokens 16..31 of request 0
+    bt_h[2, 0] = wl.num_pages            # tokens 0..15 of request 2
+    lens_h = np.array([37, -5, 10_000, 9], dtype=np.int32)
+    clamp = np.clip(lens_h, 0, bt_h.shape[1] * wl.page_size).astype(np.int32)
+    src, bt, lens = to_dev(src_h), to_dev(bt_h), to_dev(lens_h)
+    h0, hc = 2, 3
+    n = rs.packed_heads_elems(C, hc, D, clamp)
+    out = torch.full((n,), SENTINEL, dtype=src.dtype, device="cuda")
+    tk.topkv_pack_layer_heads(src, 0, 4, bt, bt.shape[1], lens, h0, hc, out)
+    torch.cuda.synchronize()
+    got = to_host(out).view(np.int16)
+    good_bt = bt_h.copy()
+    good_bt[0, 1] = 0
+    good_bt[2, 0] = 0
+    want = rs.pack_layer_heads(src_h, 0, good_bt, clamp, h0, hc).view(np.int16).copy()
+    # blank the skipped tokens in the expectation
+    off = 0
+    for r, nr in enumerate(clamp):
+        blk = want[off:off + C * nr * hc * D].reshape(C, nr, hc, D)
+        if r == 0:
+            blk[:, 16:32] = SENTINEL
+        if r == 2:
+            blk[:, 0:16] = SENTINEL
+        off += blk.size
+    assert np.array_equal(got, want)
+
+
+def test_fullsize_70b_head_slices(tk):
+    """70B, 4096 tokens: the two tensor-parallel halves (heads 0-3, 4-7) put
+    side by side are the full-head packed layer of the fast pack kernel, on
+    every layer; sampled layers also vs the oracle."""
+    wl = make_workload("llama3-70b-4k")
+    say(f"[reshard] 70B head slices full size: {wl.describe()}")
+    src = device_src_pool(wl)
+    bt, lens = to_dev(wl.block_tables), to_dev(wl.seq_lens)
+    n = int(wl.seq_lens[0])
+    full = torch.empty(2 * n * 8 * 128, dtype=torch.int16, device="cuda")
+    halves = [torch.empty(2 * n * 4 * 128, dtype=torch.int16, device="cuda") for _ in range(2)]
+    for layer in range(wl.num_layers):
+        tk.topkv_pack_layer_batched(src, layer, 1, bt, bt.shape[1], lens, full)
+        for i in range(2):
+            tk.topkv_pack_layer_heads(src, layer, 1, bt, bt.shape[1], lens, 4 * i, 4, halves[i])
+        joined = torch.cat([h.view(2, n, 4, 128) for h in halves], dim=2).reshape(-1)
+        assert torch.equal(joined, full), f"layer {layer}: head halves do not tile the layer"
+        if layer in (0, 79):
+            want = rs.pack_layer_heads(to_host(src[layer])[None], 0, wl.block_tables, wl.seq_lens, 4, 4)
+            assert np.array_equal(to_host(halves[1]), want), f"layer {layer}: heads 4-7 vs oracle"
+    del src
+    torch.cuda.empty_cache()
+
+
+def test_fullsize_reblock_70b(tk):
+    """reblock-70b (100 requests, page 16 -> 64) at full size: the fused
+    pool-to-pool move equals the fast pack + unpack pair on sampled layers,
+    and one layer equals the oracle."""
+    wl = make_workload("reblock-70b")
+    say(f"[reshard] re-block full size: {wl.describe()}")
+    src, dst = device_src_pool(wl), device_dst_prefill(wl)
+    dst2 = dst.clone()
+    bt, bt2, lens = to_dev(wl.block_tables), to_dev(wl.dst_block_tables), to_dev(wl.seq_lens)
+    nbytes = tk.topkv_packed_layer_bytes(src, wl.seq_lens)
+    packed = torch.empty(nbytes // 2, dtype=torch.int16, device="cuda")
+    for layer in (0, 5, 7):
+        tk.topkv_reblock_layer(src, layer, bt, bt.shape[1], dst, layer, bt2, bt2.shape[1], wl.num_reqs, lens)
+        tk.topkv_pack_layer_batched(src, layer, wl.num_reqs, bt, bt.shape[1], lens, packed)
+        tk.topkv_unpack_layer_batched(packed, dst2, layer, wl.num_reqs, bt2, bt2.shape[1], lens)
+        torch.cuda.synchronize()
+        same = torch.equal(dst[layer].view(torch.int16), dst2[layer].view(torch.int16))   # bits: NaNs included
+        assert same, f"layer {layer}: fused re-block differs from pack+unpack"
+    want = oracle.unpack_layer(oracle.pack_layer(to_host(src[5])[None], 0, wl.block_tables, wl.seq_lens),
+                               to_host(device_dst_prefill(wl)[5])[None], 0, wl.dst_block_tables, wl.seq_lens)
+    assert np.array_equal(to_host(dst[5]), want[0]), "layer 5 vs oracle"
+    del src, dst, dst2, packed
+    torch.cuda.empty_cache()
+
+
+def test_fullsize_head_major_70b(tk):
+    """70B, 4096 tokens, page 16 -> head-major page 64 and back to packed:
+    equals the fast pack on every layer."""
+    wl = make_workload("llama3-70b-4k", dst_page_size=64)
+    say(f"[reshard] head-major full size: {wl.describe()}")
+    src = device_src_pool(wl)
+    hm = torch.zeros((wl.phys_layers, wl.dst_num_pages, 2, 8, 64, 128), dtype=torch.int16, device="cuda")
+    bt, bt2, lens = to_dev(wl.block_tables), to_dev(wl.dst_block_tables), to_dev(wl.seq_lens)
+    n = int(wl.seq_lens[0])
+    full = torch.empty(2 * n * 8 * 128, dtype=torch.int16, device="cuda")
+    back = torch.empty_like(full)
+    for layer in range(0, wl.num_layers, 7):
+        tk.topkv_move_layer(tk.pool_view(src, layer, bt, bt.shape[1]),
+                            tk.pool_view(hm, layer, bt2, bt2.shape[1], head_major=True), 1, lens, 8)
+        tk.topkv_move_layer(tk.pool_view(hm, layer, bt2, bt2.shape[1], head_major=True), tk.packed_view(back),
+                            1, lens, 8)
+        tk.topkv_pack_layer_batched(src, layer, 1, bt, bt.shape[1], lens, full)
+        assert torch.equal(back, full), f"layer {layer}: head-major round trip differs"
+    page0 = int(wl.dst_block_tables[0][3])
+    want = rs.to_head_major(
+        oracle.unpack_layer(oracle.pack_layer(to_host(src[0])[None], 0, wl.block_tables, wl.seq_lens),
+                            np.zeros((1, wl.dst_num_pages, 2, 64, 8, 128), np.uint16), 0, wl.dst_block_tables,
+                            wl.seq_lens))
+    assert np.array_equal(to_host(hm[0, page0]), want[0, page0]), "head-major page vs oracle"
+    del src, hm
+    torch.cuda.empty_cache()
