@@ -487,8 +487,9 @@ def run_pipeline(args, check=None):
               layer's event has completed (no compute unit used).
     Measured: compute alone, transfer alone (side placement), both back to
     back (serial), and each placement alone and overlapped.
-    hidden = 1 - (pipelined - compute) / transfer, beside the paper's model
-    T_eff = max(T_last, T_xfer - T_rem).  With `check(placement, host)`, the
+    hidden = 1 - exposed / transfer with exposed = pipelined - compute, beside
+    the paper's model T_eff = max(T_last, T_xfer - T_rem) (T_last: the final
+    layer's prefill compute; T_rem: the compute after the first layer).  With `check(placement, host)`, the
     staging buffer and host buffer are poisoned before every run and the
     hook sees the host buffer after each placement's last run."""
     import time
@@ -514,24 +515,26 @@ def run_pipeline(args, check=None):
     N = 8192
     b = torch.randn(N, N, dtype=torch.bfloat16, device="cuda")
 
-    def gemm_ms(m):
+    def gemm_ms(m, reps=20):
         a = torch.randn(m, N, dtype=torch.bfloat16, device="cuda")
         c = torch.empty(m, N, dtype=torch.bfloat16, device="cuda")
         for _ in range(3):
             torch.matmul(a, b, out=c)
         e0, e1 = topkv.HipEvent(), topkv.HipEvent()
         e0.record(main)
-        for _ in range(10):
+        for _ in range(reps):
             torch.matmul(a, b, out=c)
         e1.record(main)
         e1.synchronize()
-        return e0.elapsed_ms(e1) / 10, a, c
+        return e0.elapsed_ms(e1) / reps, a, c
 
-    M, t = N, None
-    for _ in range(3):                            # time scales with M: refine twice
-        t, a, c = gemm_ms(M)
-        M = int(min(65536, max(256, round(M * args.layer_ms / t / 256) * 256)))
-    t, a, c = gemm_ms(M)
+    # GEMM time is not linear in M (tile quantisation): search M in steps of
+    # 256 around the proportional guess for the time closest to --layer-ms
+    t8k, _, _ = gemm_ms(N, 5)
+    guess = max(256, round(N * args.layer_ms / t8k / 256) * 256)
+    cands = sorted({m for m in range(guess // 2, guess * 2 + 1, 256) if 256 <= m <= 65536})
+    M = min(cands, key=lambda m: abs(gemm_ms(m, 5)[0] - args.layer_ms))
+    _, a, c = gemm_ms(M)
 
     def compute(l):
         torch.matmul(a, b, out=c)                  # on the current (prefill) stream
@@ -611,7 +614,8 @@ def run_pipeline(args, check=None):
     variants = {}
     for name, (alone, overlapped) in plans.items():
         v = {"transfer_ms": best(alone), "pipelined_ms": best(overlapped)}
-        v["hidden"] = 1 - max(0.0, v["pipelined_ms"] - runs["compute"]) / runs["transfer"]
+        v["exposed_ms"] = max(0.0, v["pipelined_ms"] - runs["compute"])
+        v["hidden"] = 1 - v["exposed_ms"] / runs["transfer"]
         variants[name] = {key: round(x, 4) for key, x in v.items()}
         if check is not None:
             check(name, host)
@@ -621,7 +625,7 @@ def run_pipeline(args, check=None):
     layer_ms = runs["compute"] / L
     t_xfer = runs["transfer"]
     t_rem = (L - 1) * layer_ms
-    t_eff = max(t_xfer / L, t_xfer - t_rem)
+    t_eff = max(layer_ms, t_xfer - t_rem)          # T_last: the final layer's prefill compute
     return {
         "metric": "pipelined layer-by-layer KV transfer: hidden fraction of transfer time", "mode": "pipeline",
         "value": variants[top]["hidden"], "unit": "fraction", "n_gpus": 1, "steps": args.steps,
