@@ -134,10 +134,11 @@ WORKLOADS = {
     "deepseek-v3-mla": "61 layers, 1 x 576 latent (no K/V split), page 64, 32 requests lognormal(median 4096, sigma 1) in [512,16384], pools 1.25x pages",
     "reblock-70b": "80 layers, 8 KV heads, head_dim 128, page 16 -> 64, 100 requests lognormal(median 4096, sigma 1) in [256,32768], pools 1.25x pages, 8 physical layer slabs",
     "gpt-oss-120b": "36 layers alternating 128-token sliding window / full attention, 8 KV heads, head_dim 64, page 16, 32 requests lognormal(median 4096, sigma 1) in [512,16384], pools 1.25x pages",
+    "llama3-70b-tp8": "one GPU's share of 70B at tensor parallelism 8: 80 layers, 1 KV head, head_dim 128, page 16, one 4096-token request, 4096-page pools",
 }
 
 DEFAULT_SEEDS = {"tiny": 0, "llama3-8b": 1, "llama3-70b-batch8": 2, "deepseek-v3-mla": 3,
-                 "reblock-70b": 4, "llama3-70b-4k": 5, "gpt-oss-120b": 6}
+                 "reblock-70b": 4, "llama3-70b-4k": 5, "gpt-oss-120b": 6, "llama3-70b-tp8": 7}
 
 
 def make_workload(name: str, seed: Optional[int] = None, *,
@@ -158,8 +159,9 @@ def make_workload(name: str, seed: Optional[int] = None, *,
         shape = dict(L=2, C=2, H=2, D=64, P=16, P2=16)
         lens = np.array([64, 48, 33, 17], dtype=np.int32)
         pools = (64, 64)
-    elif name in ("llama3-8b", "llama3-70b-4k"):
-        shape = dict(L=32 if name == "llama3-8b" else 80, C=2, H=8, D=128, P=16, P2=16)
+    elif name in ("llama3-8b", "llama3-70b-4k", "llama3-70b-tp8"):
+        shape = dict(L=32 if name == "llama3-8b" else 80, C=2, H=1 if name == "llama3-70b-tp8" else 8,
+                     D=128, P=16, P2=16)
         lens = np.array([4096], dtype=np.int32)
         pools = (4096, 4096)
     elif name == "llama3-70b-batch8":

@@ -16,7 +16,7 @@ from paper_2607_28633_amd.workloads import device_dst_prefill, device_src_pool, 
 
 pytestmark = pytest.mark.gpu
 
-FULL = ["llama3-70b-4k", "llama3-8b", "llama3-70b-batch8", "deepseek-v3-mla", "reblock-70b"]
+FULL = ["llama3-70b-4k", "llama3-8b", "llama3-70b-batch8", "deepseek-v3-mla", "reblock-70b", "llama3-70b-tp8"]
 
 
 @pytest.fixture(scope="module")

@@ -47,6 +47,8 @@ def test_workload_shapes():
     assert 2500 < np.median(rb.seq_lens) < 6500
     h = make_workload("llama3-70b-4k")
     assert h.num_layers == 80 and h.seq_lens.tolist() == [4096] and h.num_pages == 4096
+    tp8 = make_workload("llama3-70b-tp8")      # one GPU's eighth of the 70B heads
+    assert tp8.num_heads * 8 == h.num_heads and tp8.pool_shape()[1:] == (4096, 2, 16, 1, 128)
 
 
 def test_bf16_rounding_and_values():
