@@ -252,11 +252,13 @@ __global__ __launch_bounds__(kThreads) void kv_reshard_kernel(Params p, const in
         at.t = __builtin_amdgcn_readfirstlane(at.t);
         const uint32_t idx = wbase + lane;
         int64_t soff = (int64_t)idx * VB, o = (int64_t)idx * VB;
-        bool good = true;
-        if (!p.src.packed) good = pool_offset_wave(p.src, at, k, e * VB, src_pc, &soff);
-        else good = soff + VB <= p.packed_cap;
-        if (!p.dst.packed) good = good && pool_offset_wave(p.dst, at, k, e * VB, dst_pc, &o);
-        else good = good && o + VB <= p.packed_cap;
+        // both sides' table entries are in-bounds reads whatever the other side
+        // holds, so both lookups issue before either is tested (bitwise &)
+        const bool s_ok = p.src.packed ? soff + VB <= p.packed_cap
+                                       : pool_offset_wave(p.src, at, k, e * VB, src_pc, &soff);
+        const bool d_ok = p.dst.packed ? o + VB <= p.packed_cap
+                                       : pool_offset_wave(p.dst, at, k, e * VB, dst_pc, &o);
+        const bool good = s_ok & d_ok;
         ok[j] = good;
         doff[j] = o;
         if (good) v[j] = __builtin_nontemporal_load(reinterpret_cast<const V*>(p.src.base + soff));
@@ -269,11 +271,11 @@ __global__ __launch_bounds__(kThreads) void kv_reshard_kernel(Params p, const in
         const uint32_t k = q - q2 * p.gpt.d;
         const Loc at = locate(q2, tp, st, cnt, p.num_reqs);
         int64_t soff = (int64_t)idx * VB, o = (int64_t)idx * VB;
-        bool good = true;
-        if (!p.src.packed) good = pool_offset(p.src, at.r, at.c, at.t, k, e * VB, &soff);
-        else good = soff + VB <= p.packed_cap;
-        if (!p.dst.packed) good = good && pool_offset(p.dst, at.r, at.c, at.t, k, e * VB, &o);
-        else good = good && o + VB <= p.packed_cap;
+        const bool s_ok = p.src.packed ? soff + VB <= p.packed_cap
+                                       : pool_offset(p.src, at.r, at.c, at.t, k, e * VB, &soff);
+        const bool d_ok = p.dst.packed ? o + VB <= p.packed_cap
+                                       : pool_offset(p.dst, at.r, at.c, at.t, k, e * VB, &o);
+        const bool good = s_ok & d_ok;
         ok[j] = good;
         doff[j] = o;
         if (good) v[j] = __builtin_nontemporal_load(reinterpret_cast<const V*>(p.src.base + soff));
