@@ -1,0 +1,36 @@
+"""bench.py on the CPU: its byte accounting follows Eq. 1 and the SURVEY's
+per-launch definition, and it refuses more than one GPU before touching one."""
+import os
+import subprocess
+import sys
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+sys.path.insert(0, ROOT)
+
+
+def test_headline_bytes_per_launch():
+    import bench
+    from paper_2607_28633_amd.workloads import make_workload
+    wl = make_workload("llama3-70b-4k")
+    # read + write of 2 planes x 4096 tokens x 2 KiB rows, 256 table entries, one length
+    assert bench.layer_bytes(wl, 0) == (2 * 16_777_216 + 4 * 256 + 4,) * 2
+    assert bench.step_bytes(wl) == (33_555_460, 33_555_460)
+
+
+def test_windowed_bytes_count_kept_tokens_only():
+    import bench
+    from paper_2607_28633_amd.workloads import make_workload
+    wl = make_workload("gpt-oss-120b")
+    row = 8 * 64 * 2
+    kept = int(np.minimum(wl.seq_lens, 128).sum())
+    pack, _ = bench.layer_bytes(wl, 0)                   # layer 0 is windowed (W = 128)
+    assert pack - 4 * wl.num_reqs - 2 * 2 * kept * row == 4 * sum(
+        (int(n) - 1) // 16 - max(0, int(n) - 128) // 16 + 1 for n in wl.seq_lens)
+
+
+def test_more_than_one_gpu_is_refused():
+    r = subprocess.run([sys.executable, os.path.join(ROOT, "bench.py"), "--gpus", "2"],
+                       capture_output=True, text=True, cwd=ROOT, timeout=120)
+    assert r.returncode == 2 and "one GPU" in r.stderr
