@@ -402,7 +402,8 @@ topkv_status_t topkv_reblock_layer(const topkv_pool_t* src, int32_t src_layer, c
  *   including `ticket` has completed.  After a failed copy every later wait
  *   and submit returns TOPKV_ERR_DEVICE and queued copies are dropped.
  * topkv_dma_destroy: finish every queued copy, stop the worker, free the
- *   shipper; returns the shipper's status.
+ *   shipper; returns the shipper's status.  No other call on the same shipper
+ *   may be in progress or follow it.
  * Any number of host threads may submit and wait on one shipper. */
 typedef struct topkv_dma topkv_dma_t;
 topkv_status_t topkv_dma_create(topkv_dma_t** out);
