@@ -12,7 +12,10 @@ KV heads: with grouped-query attention a layer holds h_kv heads of d_h
 values per token and plane.  A layer can be moved between:
 
 * a packed buffer: per request a block ``[C][n_r][hc][D]`` of the moved heads,
-  blocks concatenated in request order (the pack/unpack wire order);
+  blocks concatenated in request order (the pack/unpack wire order); with S
+  shards (tensor-parallel receivers) the moved heads split into S equal runs,
+  and shard s is such a buffer of its own ``hc / S`` heads, at element offset
+  ``s * shard_elems``;
 * a slot-major pool ``[L][NP][C][P][H][D]``: token t of request r lives at
   page ``bt_r[t div P]``, slot ``t mod P``;
 * a head-major pool ``[L][NP][C][H][P][D]``: the same page and slot, but each
@@ -54,16 +57,31 @@ class View:
     layer: int = 0
     block_tables: np.ndarray | None = None
     head_begin: int = 0
+    shards: int = 1               # packed: shard regions of shard_elems elements each
+    shard_elems: int = 0
 
 
 def _page_size(v: View) -> int:
     return v.data.shape[3] if v.kind == POOL else v.data.shape[4]
 
 
+def _shard_slices(v: View, off: int, n: int, hc: int, D: int, C: int):
+    """(region slice, head slice) per shard of a packed view; `off` is this
+    request's element offset inside one shard's buffer."""
+    S = max(1, v.shards)
+    hs = hc // S
+    size = C * n * hs * D
+    for s in range(S):
+        base = s * v.shard_elems if S > 1 else 0
+        yield slice(base + off, base + off + size), slice(s * hs, (s + 1) * hs)
+
+
 def _gather(v: View, r: int, t: np.ndarray, hc: int, off: int, C: int, D: int) -> np.ndarray:
     """Request r's tokens t, heads [head_begin, head_begin + hc): ``[C][len(t)][hc][D]``."""
     if v.kind == PACKED:
-        return v.data[off:off + C * t.size * hc * D].reshape(C, t.size, hc, D)
+        S = max(1, v.shards)
+        parts = [v.data[reg].reshape(C, t.size, hc // S, D) for reg, _ in _shard_slices(v, off, t.size, hc, D, C)]
+        return np.concatenate(parts, axis=2)
     P = _page_size(v)
     pages, slots = np.asarray(v.block_tables[r])[t // P], t % P
     heads = slice(v.head_begin, v.head_begin + hc)
@@ -76,7 +94,9 @@ def _gather(v: View, r: int, t: np.ndarray, hc: int, off: int, C: int, D: int) -
 
 def _scatter(v: View, r: int, t: np.ndarray, hc: int, off: int, block: np.ndarray) -> None:
     if v.kind == PACKED:
-        v.data[off:off + block.size] = block.reshape(-1)
+        C, D = block.shape[0], block.shape[3]
+        for reg, heads in _shard_slices(v, off, t.size, hc, D, C):
+            v.data[reg] = block[:, :, heads].reshape(-1)
         return
     P = _page_size(v)
     pages, slots = np.asarray(v.block_tables[r])[t // P], t % P
@@ -112,18 +132,21 @@ def move_layer(src: View, dst: View, seq_lens, head_count: int, window: int = 0)
             c, H, d = _geometry(v)
             if (c, d) != (C, D) or not (0 <= v.head_begin and v.head_begin + hc <= H):
                 raise ValueError("planes, head_dim or the head slice do not fit a pool")
-        elif v.head_begin != 0:
-            raise ValueError("a packed side holds exactly the moved heads")
-    off = 0
+        elif v.head_begin != 0 or hc % max(1, v.shards):
+            raise ValueError("a packed side holds exactly the moved heads, in equal shards")
+    off = 0                                      # elements into one shard's buffer
     for r in range(len(seq_lens)):
         n = int(seq_lens[r])
         t = np.arange(window_start(n, window), n)
+        shards = max([1] + [v.shards for v in (src, dst) if v.kind == PACKED])
         block = _gather(src, r, t, hc, off, C, D)
         _scatter(dst, r, t, hc, off, block)
-        off += block.size
+        off += block.size // shards
     for v in (src, dst):
-        if v.kind == PACKED and off != v.data.size:
+        if v.kind == PACKED and not v.shard_elems and off != v.data.size:
             raise ValueError(f"packed buffer holds {v.data.size} elements, requests need {off}")
+        if v.kind == PACKED and v.shard_elems and off > v.shard_elems:
+            raise ValueError(f"shards hold {v.shard_elems} elements each, requests need {off}")
     return dst.data
 
 
@@ -145,6 +168,16 @@ def unpack_layer_heads(packed, pool, layer, block_tables, seq_lens, head_begin, 
     """Scatter head-sliced packed blocks into heads [head_begin, +head_count)
     of a slot-major pool (in place; also returned)."""
     return move_layer(View(PACKED, packed), View(POOL, pool, layer, block_tables, head_begin),
+                      seq_lens, head_count, window)
+
+
+def pack_layer_shards(pool, layer, block_tables, seq_lens, head_begin, head_count, shards, shard_elems, window=0):
+    """Heads [head_begin, +head_count) of one layer split into `shards` equal
+    runs; shard s (heads head_begin + s*hc/S ...) packed into elements
+    [s * shard_elems, ...) of the result."""
+    out = np.zeros(int(shards) * int(shard_elems), dtype=pool.dtype)
+    return move_layer(View(POOL, pool, layer, block_tables, head_begin),
+                      View(PACKED, out, shards=int(shards), shard_elems=int(shard_elems)),
                       seq_lens, head_count, window)
 
 

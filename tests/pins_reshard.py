@@ -191,8 +191,46 @@ def pin_head_major_identity_is_swapaxes(impl):
     assert np.array_equal(hm, np.swapaxes(src, 3, 4)), "head-major pool is not the axis swap"
 
 
+def pin_shards_are_head_slices(impl):
+    """S shards of heads [h0, h0 + hc): shard s is the head-sliced pack of
+    heads h0 + s*hc/S ... (itself pinned by brute force), at s * shard_elems;
+    the gap after each shard keeps its prior words."""
+    wl = _wl()
+    pool = host_src_pool(wl)
+    for h0, hc, S, window in ((0, 8, 2, 0), (0, 8, 4, 9), (2, 6, 3, 0), (0, 8, 8, 0), (4, 4, 1, 3)):
+        per = oracle.packed_layer_elems(wl.planes, hc // S, wl.head_dim, wl.seq_lens, window)
+        cap = per + 7
+        out = np.full(S * cap, 0xABCD, dtype=pool.dtype)
+        got = impl.move_layer(impl.View(impl.POOL, pool, 1, wl.block_tables, h0),
+                              impl.View(impl.PACKED, out, shards=S, shard_elems=cap), wl.seq_lens, hc, window)
+        for sh in range(S):
+            want = _brute_pack(pool, 1, wl.block_tables, wl.seq_lens, h0 + sh * (hc // S), hc // S, window)
+            region = got[sh * cap:(sh + 1) * cap]
+            assert np.array_equal(region[:per], want), f"shard {sh} of {S} (heads {h0}+{hc}, W={window})"
+            assert (region[per:] == 0xABCD).all(), f"shard {sh}: words past the shard's data changed"
+
+
+def pin_shards_unpack(impl):
+    """Unpacking S shards into a pool equals unpacking each shard's head
+    slice on its own (brute force)."""
+    wl = _wl(dst_page_size=7)
+    rng = np.random.default_rng(11)
+    for h0, hc, S in ((0, 8, 2), (1, 6, 3), (0, 8, 8)):
+        per = oracle.packed_layer_elems(wl.planes, hc // S, wl.head_dim, wl.seq_lens)
+        packed = random_words(rng, (S * per,), 2)
+        base = host_dst_prefill(wl)
+        got = impl.move_layer(impl.View(impl.PACKED, packed, shards=S, shard_elems=per),
+                              impl.View(impl.POOL, base.copy(), 0, wl.dst_block_tables, h0), wl.seq_lens, hc)
+        want = base.copy()
+        for sh in range(S):
+            _brute_unpack(packed[sh * per:(sh + 1) * per], want, 0, wl.dst_block_tables, wl.seq_lens,
+                          h0 + sh * (hc // S), hc // S, 0)
+        assert np.array_equal(got, want), f"{S} shards of heads {h0}+{hc} unpacked"
+
+
 RESHARD_PINS = [pin_heads_bruteforce, pin_heads_partition, pin_unpack_heads_bruteforce, pin_reblock_two_step,
-                pin_reblock_bruteforce, pin_head_major_bruteforce, pin_head_major_identity_is_swapaxes]
+                pin_reblock_bruteforce, pin_head_major_bruteforce, pin_head_major_identity_is_swapaxes,
+                pin_shards_are_head_slices, pin_shards_unpack]
 
 
 def failing_pins(impl):

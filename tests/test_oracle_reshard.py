@@ -52,7 +52,11 @@ class Mutant:
                 start = 0
             t = np.arange(start, n)
             size = C * t.size * hc * D
-            if src.kind == rs.PACKED:
+            S = max([1] + [v.shards for v in (src, dst) if v.kind == rs.PACKED])
+            if src.kind == rs.PACKED and S > 1:
+                block = np.concatenate([src.data[self._shard_base(src, sh, off, size // S)].reshape(
+                    C, t.size, hc // S, D) for sh in self._shard_order(S)], axis=2)
+            elif src.kind == rs.PACKED:
                 if self.bug == "packed_token_major":
                     block = src.data[off:off + size].reshape(t.size, C, hc, D).transpose(1, 0, 2, 3)
                 else:
@@ -61,7 +65,11 @@ class Mutant:
                 pages, slots = self._where(src, r, t)
                 g, _ = self._sel(src, pages, slots)
                 block = g[:, :, self._heads(src, hc)].transpose(1, 0, 2, 3)
-            if dst.kind == rs.PACKED:
+            if dst.kind == rs.PACKED and S > 1:
+                for i, sh in enumerate(self._shard_order(S)):
+                    dst.data[self._shard_base(dst, sh, off, size // S)] = \
+                        block[:, :, i * (hc // S):(i + 1) * (hc // S)].reshape(-1)
+            elif dst.kind == rs.PACKED:
                 out = block.transpose(1, 0, 2, 3) if self.bug == "packed_token_major" else block
                 dst.data[off:off + size] = out.reshape(-1)
             else:
@@ -73,8 +81,17 @@ class Mutant:
                 else:
                     sel[:, :, heads] = block.transpose(1, 0, 2, 3)
                 dst.data[dst.layer][idx] = sel
-            off += size
+            off += size // S
         return dst.data
+
+    def _shard_order(self, S):
+        return list(reversed(range(S))) if self.bug == "shards_reversed" else list(range(S))
+
+    def _shard_base(self, v, sh, off, size):
+        base = sh * v.shard_elems
+        if self.bug == "shard_offset_total":
+            off = off * v.shards
+        return slice(base + off, base + off + size)
 
     def pack_layer_heads(self, pool, layer, bts, lens, h0, hc, window=0):
         out = np.empty(rs.packed_heads_elems(pool.shape[2], hc, pool.shape[5], lens,
@@ -90,7 +107,8 @@ class Mutant:
 
 
 BUGS = ["head_begin_ignored", "dst_head_begin_ignored", "reblock_uses_src_page_size",
-        "head_major_read_as_slot_major", "window_ignored", "packed_token_major", "unpack_writes_all_heads"]
+        "head_major_read_as_slot_major", "window_ignored", "packed_token_major", "unpack_writes_all_heads",
+        "shards_reversed", "shard_offset_total"]
 
 
 def test_unmutated_copy_passes():
