@@ -386,7 +386,8 @@ def run_kvcache1(args):
 def run_reshard(args):
     """Layout moves, per layer, as graph-captured sweeps over every layer:
     head-sliced pack of the two tensor-parallel halves (heads [0, H/2) and
-    [H/2, H), two launches per layer) beside the full-head pack; unpack into a
+    [H/2, H), two launches per layer, or one launch writing both shards)
+    beside the full-head pack; unpack into a
     head-major pool beside the slot-major unpack; and pool-to-pool re-blocking
     (P -> P', one launch, no staging buffer) beside the pack + unpack pair.
     GB/s counts algorithmic bytes: each moved byte read once and written once
@@ -423,6 +424,8 @@ def run_reshard(args):
         "pack_heads_tp2": lambda: [topkv.prepare_pack_layer_heads(
             src, slab(l), R, bt, bt.shape[1], lens, i * (H // 2), H // 2, half[l % ring, i]) for l in range(L)
             for i in range(2)],
+        "pack_shards_tp2": lambda: [topkv.prepare_pack_layer_shards(
+            src, slab(l), R, bt, bt.shape[1], lens, 0, H, 2, half[l % ring]) for l in range(L)],
         "unpack_full": lambda: [topkv.prepare_unpack_layer_batched_ex(
             packed[l % ring], dst, slab(l), R, bt2, bt2.shape[1], lens, stream=None) for l in range(L)],
         "unpack_head_major": lambda: [topkv.prepare_move_layer(

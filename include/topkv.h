@@ -303,14 +303,20 @@ int64_t topkv_check_workspace_bytes(const topkv_pool_t* pool);
  *   TOPKV_LAYOUT_PACKED           `data`/`bytes`: per request a block
  *                                 [planes][kept tokens][head_count][head_dim],
  *                                 blocks in request order (the pack/unpack
- *                                 wire order, restricted to the moved heads)
+ *                                 wire order, restricted to the moved heads).
+ *                                 With `shards` = S > 1 (tensor-parallel
+ *                                 receivers) the moved heads split into S equal
+ *                                 runs and shard s is such a buffer of its
+ *                                 head_count / S heads at data + s * bytes
+ *                                 (`bytes` is then each shard's capacity)
  *   TOPKV_LAYOUT_POOL             `pool`: the slot-major pool of topkv_pool_t,
  *                                 [layer][page][plane][slot][head][dim]
  *   TOPKV_LAYOUT_POOL_HEAD_MAJOR  `pool` geometry, but each page plane is
  *                                 [head][slot][dim] (each head's slots adjacent)
  * Pool views also give `layer`, `block_tables` (device int32
  * [num_reqs][bt_stride]) and `head_begin`, the first of the head_count moved
- * heads.  Packed views ignore those fields.
+ * heads, and ignore `shards`.  Packed views ignore the pool fields; shards 0
+ * or 1 means one region.
  *
  * For every request r, kept token t (the last `window` tokens when window > 0,
  * Sec. 2.2; all of them when 0), plane c, j < head_count and dim d:
@@ -322,7 +328,8 @@ int64_t topkv_check_workspace_bytes(const topkv_pool_t* pool);
  * between page sizes with no staging buffer (pool -> pool), and head-major
  * pools on either side.
  *
- * Requirements: at least one side is a pool; pool sides agree on planes,
+ * Requirements: at least one side is a pool; a packed side's shards divide
+ * head_count (and, if S > 1, its piece width divides `bytes`); pool sides agree on planes,
  * head_dim and elem_bytes (page size, page count, head count and layer count
  * may differ); 1 <= head_count <= num_heads - head_begin on each pool side;
  * 0 <= num_reqs <= TOPKV_MAX_BATCH_REQS; seq_lens is device int32 [num_reqs].
@@ -348,7 +355,9 @@ typedef struct topkv_view {
     const int32_t* block_tables;  /* pool views: device [num_reqs][bt_stride] */
     topkv_pool_t pool;            /* pool views: geometry and base */
     void* data;                   /* packed views: device buffer */
-    int64_t bytes;                /* packed views: capacity in bytes */
+    int64_t bytes;                /* packed views: capacity in bytes (of each shard) */
+    int32_t shards;               /* packed views: 0 or 1 = one region, S > 1 = S shard regions */
+    int32_t reserved;             /* set to 0 */
 } topkv_view_t;
 
 topkv_status_t topkv_move_layer(const topkv_view_t* src, const topkv_view_t* dst, int32_t num_reqs,
@@ -370,6 +379,23 @@ topkv_status_t topkv_unpack_layer_heads(const void* src, int64_t src_bytes, cons
                                         int32_t layer, int32_t num_reqs, const int32_t* block_tables,
                                         int32_t bt_stride, const int32_t* seq_lens, int32_t head_begin,
                                         int32_t head_count, hipStream_t stream);
+
+/* Packing for S tensor-parallel receivers in one launch: heads
+ * [head_begin, head_begin + head_count) split into S equal runs; shard s (its
+ * head_count / S heads, [planes][n_r][head_count / S][dim] per request,
+ * requests concatenated) goes to dst + s * shard_bytes.  Same as
+ * topkv_move_layer(pool view, packed view with `shards` = S, ..., window 0). */
+topkv_status_t topkv_pack_layer_shards(const topkv_pool_t* src, int32_t layer, int32_t num_reqs,
+                                      const int32_t* block_tables, int32_t bt_stride, const int32_t* seq_lens,
+                                      int32_t head_begin, int32_t head_count, int32_t shards, void* dst,
+                                      int64_t shard_bytes, hipStream_t stream);
+
+/* The inverse: S shard buffers (at src + s * shard_bytes) into heads
+ * [head_begin, head_begin + head_count) of a slot-major pool. */
+topkv_status_t topkv_unpack_layer_shards(const void* src, int64_t shard_bytes, int32_t shards,
+                                        const topkv_pool_t* dst, int32_t layer, int32_t num_reqs,
+                                        const int32_t* block_tables, int32_t bt_stride, const int32_t* seq_lens,
+                                        int32_t head_begin, int32_t head_count, hipStream_t stream);
 
 /* Pool-to-pool re-blocking: every head of layer src_layer of `src` (page size
  * P, tables src_tables) into layer dst_layer of `dst` (page size P', tables

@@ -85,16 +85,17 @@ struct Side {
   int32_t slot_bytes;       // stride between slots of a page plane
   int32_t gran_stride;      // stride between consecutive granules of a slot
   int32_t bt_stride;
-  int32_t packed;           // 1: packed buffer, address = piece index * VB
+  int32_t packed;           // 1: packed buffer (shard regions of Params::packed_cap bytes)
   FastDiv page;             // tokens per page
 };
 
 struct Params {
   Side src, dst;
-  int64_t packed_cap;       // bytes of the packed side (if any)
+  int64_t packed_cap;       // bytes of each shard region of the packed side (one region unsharded)
   FastDiv vpg;              // pieces per granule
   FastDiv gpt;              // granules per (token, plane)
   FastDiv ktp;              // pieces per (token, plane) = gpt * vpg
+  FastDiv gps;              // granules per shard (= gpt when unsharded)
   int32_t num_reqs;
   int32_t planes;
   int32_t window;
@@ -152,6 +153,20 @@ __device__ __forceinline__ bool pool_offset(const Side& s, int32_t r, uint32_t c
   *off = (int64_t)page * s.page_bytes + (int64_t)c * s.plane_bytes + (int64_t)slot * s.slot_bytes +
          s.head0_bytes + (int64_t)k * s.gran_stride + e_bytes;
   return true;
+}
+
+// Byte offset of piece (q2, k, e) on the packed side: granule k belongs to
+// shard k / gps, which holds its own (request, plane, token)-ordered granules
+// at shard * packed_cap.  Unsharded (gps = gpt) this is the piece index * VB.
+// False past the shard's capacity.
+template <int VB>
+__device__ __forceinline__ bool packed_offset(const Params& p, uint32_t q2, uint32_t k, uint32_t e,
+                                              int64_t* off) {
+  const uint32_t sh = fdiv(k, p.gps);
+  const uint32_t pos = k - sh * p.gps.d;
+  const int64_t in_shard = ((int64_t)q2 * p.gps.d + pos) * ((int64_t)p.vpg.d * VB) + (int64_t)e * VB;
+  *off = (int64_t)sh * p.packed_cap + in_shard;
+  return in_shard + VB <= p.packed_cap;
 }
 
 struct Loc {
@@ -250,13 +265,12 @@ __global__ __launch_bounds__(kThreads) void kv_reshard_kernel(Params p, const in
         at.r = __builtin_amdgcn_readfirstlane(at.r);
         at.c = __builtin_amdgcn_readfirstlane(at.c);
         at.t = __builtin_amdgcn_readfirstlane(at.t);
-        const uint32_t idx = wbase + lane;
-        int64_t soff = (int64_t)idx * VB, o = (int64_t)idx * VB;
+        int64_t soff = 0, o = 0;
         // both sides' table entries are in-bounds reads whatever the other side
         // holds, so both lookups issue before either is tested (bitwise &)
-        const bool s_ok = p.src.packed ? soff + VB <= p.packed_cap
+        const bool s_ok = p.src.packed ? packed_offset<VB>(p, q2, k, e, &soff)
                                        : pool_offset_wave(p.src, at, k, e * VB, src_pc, &soff);
-        const bool d_ok = p.dst.packed ? o + VB <= p.packed_cap
+        const bool d_ok = p.dst.packed ? packed_offset<VB>(p, q2, k, e, &o)
                                        : pool_offset_wave(p.dst, at, k, e * VB, dst_pc, &o);
         const bool good = s_ok & d_ok;
         ok[j] = good;
@@ -270,10 +284,10 @@ __global__ __launch_bounds__(kThreads) void kv_reshard_kernel(Params p, const in
         const uint32_t q2 = fdiv(q, p.gpt);
         const uint32_t k = q - q2 * p.gpt.d;
         const Loc at = locate(q2, tp, st, cnt, p.num_reqs);
-        int64_t soff = (int64_t)idx * VB, o = (int64_t)idx * VB;
-        const bool s_ok = p.src.packed ? soff + VB <= p.packed_cap
+        int64_t soff = 0, o = 0;
+        const bool s_ok = p.src.packed ? packed_offset<VB>(p, q2, k, e, &soff)
                                        : pool_offset(p.src, at.r, at.c, at.t, k, e * VB, &soff);
-        const bool d_ok = p.dst.packed ? o + VB <= p.packed_cap
+        const bool d_ok = p.dst.packed ? packed_offset<VB>(p, q2, k, e, &o)
                                        : pool_offset(p.dst, at.r, at.c, at.t, k, e * VB, &o);
         const bool good = s_ok & d_ok;
         ok[j] = good;
@@ -370,12 +384,15 @@ topkv_status_t move_layer(const topkv_view_t* src, const topkv_view_t* dst, int3
   const topkv_pool_t* geo = nullptr;     // geometry both pool sides share
   PoolInfo info[2] = {};
   int64_t packed_cap = 0;
+  int64_t shards = 1;
   int64_t max_tok = INT32_MAX;
   for (int i = 0; i < 2; ++i) {
     const topkv_view_t* v = sides[i];
     if (v->layout == TOPKV_LAYOUT_PACKED) {
-      if (v->bytes < 0 || (v->bytes > 0 && !v->data)) return TOPKV_ERR_INVALID_ARG;
+      if (v->bytes < 0 || (v->bytes > 0 && !v->data) || v->shards < 0) return TOPKV_ERR_INVALID_ARG;
       packed_cap = v->bytes;
+      shards = v->shards > 1 ? v->shards : 1;
+      if (head_count % shards != 0) return TOPKV_ERR_INVALID_ARG;
       continue;
     }
     const topkv_status_t st = pool_info(v, head_count, &info[i]);
@@ -395,7 +412,7 @@ topkv_status_t move_layer(const topkv_view_t* src, const topkv_view_t* dst, int3
   bool adjacent = true;
   for (int i = 0; i < 2; ++i)
     if (sides[i]->layout == TOPKV_LAYOUT_POOL_HEAD_MAJOR) adjacent = false;
-  const int64_t heads_per_gran = adjacent ? head_count : 1;
+  const int64_t heads_per_gran = adjacent ? head_count / shards : 1;
   const int64_t gran = heads_per_gran * head;
   // Piece width: every stride and base the pieces are addressed with.
   int vb = 16;
@@ -404,7 +421,7 @@ topkv_status_t move_layer(const topkv_view_t* src, const topkv_view_t* dst, int3
     for (int i = 0; i < 2 && fits; ++i) {
       const topkv_view_t* v = sides[i];
       if (v->layout == TOPKV_LAYOUT_PACKED) {
-        fits = reinterpret_cast<uintptr_t>(v->data) % vb == 0;
+        fits = reinterpret_cast<uintptr_t>(v->data) % vb == 0 && (shards == 1 || packed_cap % vb == 0);
       } else {
         const uintptr_t b = reinterpret_cast<uintptr_t>(v->pool.base);
         fits = b % vb == 0 && info[i].layer_bytes % vb == 0 && info[i].page_bytes % vb == 0 &&
@@ -445,6 +462,7 @@ topkv_status_t move_layer(const topkv_view_t* src, const topkv_view_t* dst, int3
   p.vpg = make_div((uint32_t)vpg);
   p.gpt = make_div((uint32_t)gpt);
   p.ktp = make_div((uint32_t)(gpt * vpg));
+  p.gps = make_div((uint32_t)(gpt / shards));
   p.num_reqs = num_reqs;
   p.planes = geo->planes;
   p.window = window;
@@ -475,11 +493,12 @@ topkv_view_t pool_view(int32_t layout, const topkv_pool_t* pool, int32_t layer, 
   return v;
 }
 
-topkv_view_t packed_view(const void* data, int64_t bytes) {
+topkv_view_t packed_view(const void* data, int64_t bytes, int32_t shards = 1) {
   topkv_view_t v = {};
   v.layout = TOPKV_LAYOUT_PACKED;
   v.data = const_cast<void*>(data);
   v.bytes = bytes;
+  v.shards = shards;
   return v;
 }
 
@@ -511,6 +530,26 @@ topkv_status_t topkv_unpack_layer_heads(const void* src, int64_t src_bytes, cons
                                         int32_t head_count, hipStream_t stream) {
   if (!dst) return TOPKV_ERR_INVALID_ARG;
   const topkv_view_t s = packed_view(src, src_bytes);
+  const topkv_view_t d = pool_view(TOPKV_LAYOUT_POOL, dst, layer, block_tables, bt_stride, head_begin);
+  return move_layer(&s, &d, num_reqs, seq_lens, head_count, 0, stream);
+}
+
+topkv_status_t topkv_pack_layer_shards(const topkv_pool_t* src, int32_t layer, int32_t num_reqs,
+                                      const int32_t* block_tables, int32_t bt_stride, const int32_t* seq_lens,
+                                      int32_t head_begin, int32_t head_count, int32_t shards, void* dst,
+                                      int64_t shard_bytes, hipStream_t stream) {
+  if (!src || shards < 1) return TOPKV_ERR_INVALID_ARG;
+  const topkv_view_t s = pool_view(TOPKV_LAYOUT_POOL, src, layer, block_tables, bt_stride, head_begin);
+  const topkv_view_t d = packed_view(dst, shard_bytes, shards);
+  return move_layer(&s, &d, num_reqs, seq_lens, head_count, 0, stream);
+}
+
+topkv_status_t topkv_unpack_layer_shards(const void* src, int64_t shard_bytes, int32_t shards,
+                                        const topkv_pool_t* dst, int32_t layer, int32_t num_reqs,
+                                        const int32_t* block_tables, int32_t bt_stride, const int32_t* seq_lens,
+                                        int32_t head_begin, int32_t head_count, hipStream_t stream) {
+  if (!dst || shards < 1) return TOPKV_ERR_INVALID_ARG;
+  const topkv_view_t s = packed_view(src, shard_bytes, shards);
   const topkv_view_t d = pool_view(TOPKV_LAYOUT_POOL, dst, layer, block_tables, bt_stride, head_begin);
   return move_layer(&s, &d, num_reqs, seq_lens, head_count, 0, stream);
 }

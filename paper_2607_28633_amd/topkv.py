@@ -44,7 +44,8 @@ EXPORTS = ["topkv_pack_layer", "topkv_unpack_layer", "topkv_pack_layer_batched",
            "topkv_kvcache1_pack_layer", "topkv_kvcache1_seal", "topkv_kvcache1_verify",
            "topkv_kvcache1_unpack_layer", "topkv_crc64", "topkv_crc64_workspace_bytes", "topkv_dma_create",
            "topkv_dma_submit", "topkv_dma_wait", "topkv_dma_destroy", "topkv_move_layer",
-           "topkv_pack_layer_heads", "topkv_unpack_layer_heads", "topkv_reblock_layer"]
+           "topkv_pack_layer_heads", "topkv_unpack_layer_heads", "topkv_reblock_layer",
+           "topkv_pack_layer_shards", "topkv_unpack_layer_shards"]
 
 TOPKV_LAYOUT_PACKED = 0
 TOPKV_LAYOUT_POOL = 1
@@ -61,7 +62,8 @@ class topkv_pool_t(ctypes.Structure):
 class topkv_view_t(ctypes.Structure):
     _fields_ = [("layout", ctypes.c_int32), ("layer", ctypes.c_int32), ("head_begin", ctypes.c_int32),
                 ("bt_stride", ctypes.c_int32), ("block_tables", ctypes.c_void_p), ("pool", topkv_pool_t),
-                ("data", ctypes.c_void_p), ("bytes", ctypes.c_int64)]
+                ("data", ctypes.c_void_p), ("bytes", ctypes.c_int64), ("shards", ctypes.c_int32),
+                ("reserved", ctypes.c_int32)]
 
 
 class topkv_launch_t(ctypes.Structure):
@@ -105,6 +107,8 @@ _SIGS = {
     "topkv_pack_layer_heads": (_I32, [_POOL, _I32, _I32, _P, _I32, _P, _I32, _I32, _P, _I64, _P]),
     "topkv_unpack_layer_heads": (_I32, [_P, _I64, _POOL, _I32, _I32, _P, _I32, _P, _I32, _I32, _P]),
     "topkv_reblock_layer": (_I32, [_POOL, _I32, _P, _I32, _POOL, _I32, _P, _I32, _I32, _P, _P]),
+    "topkv_pack_layer_shards": (_I32, [_POOL, _I32, _I32, _P, _I32, _P, _I32, _I32, _I32, _P, _I64, _P]),
+    "topkv_unpack_layer_shards": (_I32, [_P, _I64, _I32, _POOL, _I32, _I32, _P, _I32, _P, _I32, _I32, _P]),
     "topkv_dma_create": (_I32, [ctypes.POINTER(_P)]),
     "topkv_dma_submit": (_I32, [_P, _P, _P, _P, _I64, ctypes.POINTER(_I64)]),
     "topkv_dma_wait": (_I32, [_P, _I64]),
@@ -201,12 +205,17 @@ def pool_view(pool, layer, block_tables, bt_stride, head_begin=0, head_major=Fal
     else:
         desc = head_major_pool_from_tensor(pool) if head_major else pool_from_tensor(pool)
     layout = TOPKV_LAYOUT_POOL_HEAD_MAJOR if head_major else TOPKV_LAYOUT_POOL
-    return topkv_view_t(layout, int(layer), int(head_begin), int(bt_stride), _table_ptr(block_tables), desc, 0, 0)
+    return topkv_view_t(layout, int(layer), int(head_begin), int(bt_stride), _table_ptr(block_tables), desc, 0, 0,
+                        0, 0)
 
 
-def packed_view(buf, nbytes=None) -> topkv_view_t:
-    """A packed side of topkv_move_layer."""
-    return topkv_view_t(TOPKV_LAYOUT_PACKED, 0, 0, 0, 0, topkv_pool_t(), _ptr(buf), _nbytes(buf, nbytes))
+def packed_view(buf, nbytes=None, shards=1) -> topkv_view_t:
+    """A packed side of topkv_move_layer; with shards = S > 1, `nbytes` is each
+    shard region's capacity (default: the buffer split in S)."""
+    if nbytes is None and shards > 1:
+        nbytes = _nbytes(buf, None) // int(shards)
+    return topkv_view_t(TOPKV_LAYOUT_PACKED, 0, 0, 0, 0, topkv_pool_t(), _ptr(buf), _nbytes(buf, nbytes),
+                        int(shards), 0)
 
 
 def topkv_pack_layer(src, layer, block_table, seq_len, dst, stream=None) -> None:
@@ -441,6 +450,25 @@ def topkv_unpack_layer_heads(src, dst, layer, num_reqs, block_tables, bt_stride,
                                          _table_ptr(seq_lens), int(head_begin), int(head_count), _stream(stream)))
 
 
+def topkv_pack_layer_shards(src, layer, num_reqs, block_tables, bt_stride, seq_lens, head_begin, head_count, shards,
+                            dst, shard_bytes=None, stream=None) -> None:
+    if shard_bytes is None:
+        shard_bytes = _nbytes(dst, None) // int(shards)
+    _check(_lib.topkv_pack_layer_shards(ctypes.byref(_pool_arg(src)), int(layer), int(num_reqs),
+                                        _table_ptr(block_tables), int(bt_stride), _table_ptr(seq_lens),
+                                        int(head_begin), int(head_count), int(shards), _ptr(dst), int(shard_bytes),
+                                        _stream(stream)))
+
+
+def topkv_unpack_layer_shards(src, dst, layer, num_reqs, block_tables, bt_stride, seq_lens, head_begin, head_count,
+                              shards, shard_bytes=None, stream=None) -> None:
+    if shard_bytes is None:
+        shard_bytes = _nbytes(src, None) // int(shards)
+    _check(_lib.topkv_unpack_layer_shards(_ptr(src), int(shard_bytes), int(shards), ctypes.byref(_pool_arg(dst)),
+                                          int(layer), int(num_reqs), _table_ptr(block_tables), int(bt_stride),
+                                          _table_ptr(seq_lens), int(head_begin), int(head_count), _stream(stream)))
+
+
 def topkv_reblock_layer(src, src_layer, src_tables, src_stride, dst, dst_layer, dst_tables, dst_stride, num_reqs,
                         seq_lens, stream=None) -> None:
     _check(_lib.topkv_reblock_layer(ctypes.byref(_pool_arg(src)), int(src_layer), _table_ptr(src_tables),
@@ -547,3 +575,14 @@ def prepare_move_layer(src: topkv_view_t, dst: topkv_view_t, num_reqs, seq_lens,
     args = (ctypes.byref(src), ctypes.byref(dst), _I32(int(num_reqs)), _P(_table_ptr(seq_lens)),
             _I32(int(head_count)), _I32(int(window)), _P(_stream(stream)))
     return PreparedCall("topkv_move_layer", args, (src, dst))
+
+
+def prepare_pack_layer_shards(src, layer, num_reqs, block_tables, bt_stride, seq_lens, head_begin, head_count, shards,
+                              dst, shard_bytes=None, stream=None) -> PreparedCall:
+    pool = _pool_arg(src)
+    if shard_bytes is None:
+        shard_bytes = _nbytes(dst, None) // int(shards)
+    args = (ctypes.byref(pool), _I32(int(layer)), _I32(int(num_reqs)), _P(_table_ptr(block_tables)),
+            _I32(int(bt_stride)), _P(_table_ptr(seq_lens)), _I32(int(head_begin)), _I32(int(head_count)),
+            _I32(int(shards)), _P(_ptr(dst)), _I64(int(shard_bytes)), _P(_stream(stream)))
+    return PreparedCall("topkv_pack_layer_shards", args, (pool,))

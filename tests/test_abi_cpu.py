@@ -162,4 +162,8 @@ def test_move_layer_validation(tk):
     _expect(tk, INV, tk.topkv_unpack_layer_heads, buf, good, 1, 2, bt, 4, lens, -1, 2, src_bytes=1 << 20)
     _expect(tk, INV, tk.topkv_reblock_layer, good, 0, bt, 4, _pool(tk, base=0x900000, num_heads=4), 0, bt, 4,
             2, lens)
+    _expect(tk, INV, tk.topkv_move_layer, pv, tk.packed_view(buf, 1 << 20, shards=3), 2, lens, 8)  # 3 does not divide 8
+    _expect(tk, INV, tk.topkv_move_layer, pv, tk.packed_view(buf, 1 << 20, shards=-2), 2, lens, 8)
+    _expect(tk, INV, tk.topkv_pack_layer_shards, good, 1, 2, bt, 4, lens, 0, 8, 0, buf, shard_bytes=1 << 20)
+    _expect(tk, INV, tk.topkv_unpack_layer_shards, buf, good, 1, 2, bt, 4, lens, 0, 6, 4, shard_bytes=1 << 20)
     tk.topkv_move_layer(pv, pk, 0, 0, 8, stream=0)                             # no requests: nothing to launch

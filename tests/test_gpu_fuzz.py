@@ -1,7 +1,8 @@
 """Seeded random geometries through the C ABI vs the CPU oracle, bit for bit:
 planes 1-2, 1-9 heads, head_dim 1-40, 1/2/4/8-byte words, page sizes 1-40 on
 either side, up to 6 requests with empty and one-token ones, random windows
-and head slices, and every pair of views (packed, slot-major, head-major).
+and head slices, tensor-parallel shards of a packed side, and every pair of
+views (packed, slot-major, head-major).
 Each case is small; together they cover piece widths 1-16 bytes, ragged
 tiles and both grid modes."""
 import random
@@ -55,6 +56,8 @@ def _case(seed):
     c["kinds"] = rng.choice([("pool", "packed"), ("packed", "pool"), ("pool", "pool"), ("pool", "hm"),
                              ("hm", "packed"), ("packed", "hm"), ("hm", "hm"), ("hm", "pool")])
     c["layers"] = (rng.randint(0, c["L"] - 1), rng.randint(0, c["L"] - 1))
+    c["S"] = rng.choice([d for d in range(1, c["hc"] + 1) if c["hc"] % d == 0]) if "packed" in c["kinds"] else 1
+    c["slack"] = rng.choice([0, 0, 3])
     return c
 
 
@@ -93,9 +96,11 @@ def test_fuzz_layout_moves(tk, seed):
     c = _case(1000 + seed)
     sk, dk = c["kinds"]
     say(f"[fuzz] move seed {seed}: {sk}->{dk} C{c['C']} H{c['H']} D{c['D']} u{8 * c['eb']} P{c['P']}->{c['P2']} "
-        f"heads {c['h0s']}/{c['h0d']}+{c['hc']} lens {c['lens'].tolist()} W{c['W']}")
+        f"heads {c['h0s']}/{c['h0d']}+{c['hc']} shards {c['S']} lens {c['lens'].tolist()} W{c['W']}")
     npr = np.random.default_rng(1000 + seed)
-    n = rs.packed_heads_elems(c["C"], c["hc"], c["D"], c["lens"], c["W"])
+    S = c["S"]
+    cap = rs.packed_heads_elems(c["C"], c["hc"] // S, c["D"], c["lens"], c["W"]) + c["slack"]
+    n = S * cap
     if sk == "packed":
         s_h = npr.integers(0, 1 << 63, size=n, dtype=np.uint64).astype(WORDS[c["eb"]])
     else:
@@ -103,13 +108,14 @@ def test_fuzz_layout_moves(tk, seed):
     d_h = np.zeros(n, WORDS[c["eb"]]) if dk == "packed" else _pool(c, c["NP2"], c["P2"], dk == "hm", npr)
     lay = {"packed": rs.PACKED, "pool": rs.POOL, "hm": rs.POOL_HEAD_MAJOR}
     (ls, ld) = c["layers"]
-    want = rs.move_layer(rs.View(lay[sk], s_h, ls, c["bt1"], c["h0s"] if sk != "packed" else 0),
-                         rs.View(lay[dk], d_h.copy(), ld, c["bt2"], c["h0d"] if dk != "packed" else 0),
+    want = rs.move_layer(rs.View(lay[sk], s_h, ls, c["bt1"], c["h0s"] if sk != "packed" else 0, S, cap),
+                         rs.View(lay[dk], d_h.copy(), ld, c["bt2"], c["h0d"] if dk != "packed" else 0, S, cap),
                          c["lens"], c["hc"], c["W"])
     s_d, d_d = to_dev(s_h), to_dev(d_h)
     bt, bt2, lens = to_dev(c["bt1"]), to_dev(c["bt2"]), to_dev(c["lens"])
-    sv = tk.packed_view(s_d) if sk == "packed" else tk.pool_view(s_d, ls, bt, bt.shape[1], c["h0s"], sk == "hm")
-    dv = tk.packed_view(d_d) if dk == "packed" else tk.pool_view(d_d, ld, bt2, bt2.shape[1], c["h0d"], dk == "hm")
+    pk = dict(nbytes=cap * c["eb"], shards=S)
+    sv = tk.packed_view(s_d, **pk) if sk == "packed" else tk.pool_view(s_d, ls, bt, bt.shape[1], c["h0s"], sk == "hm")
+    dv = tk.packed_view(d_d, **pk) if dk == "packed" else tk.pool_view(d_d, ld, bt2, bt2.shape[1], c["h0d"], dk == "hm")
     tk.topkv_move_layer(sv, dv, len(c["lens"]), lens, c["hc"], c["W"])
     torch.cuda.synchronize()
     assert np.array_equal(to_host(d_d), want), f"seed {seed}: {sk} -> {dk} differs"

@@ -147,6 +147,38 @@ def test_head_major_parity(tk, case):
         assert np.array_equal(to_host(d_d), want), f"{case}: {sk} -> {dk} differs"
 
 
+@pytest.mark.parametrize("case", ["h8-d16", "h8-d128-p16-p64", "h4-d5-u8"])
+def test_shards_parity(tk, case):
+    """Packing for S tensor-parallel receivers in one launch (shard regions
+    with slack between them) and unpacking the shards back, vs the oracle."""
+    wl = WORKLOADS[case]()
+    C, H, D = _geom(wl)
+    src_h, dst_h = host_src_pool(wl), host_dst_prefill(wl)
+    src, dst = to_dev(src_h), to_dev(dst_h)
+    bt, bt2, lens = to_dev(wl.block_tables), to_dev(wl.dst_block_tables), to_dev(wl.seq_lens)
+    want_pool = dst_h.copy()
+    for S in sorted({s for s in (1, 2, 4, H) if H % s == 0}):
+        say(f"[reshard] shards {case}: S={S}")
+        per = rs.packed_heads_elems(C, H // S, D, wl.seq_lens)
+        cap = per + 16 // wl.elem_bytes                       # slack stays untouched
+        out = torch.full((S * cap,), SENTINEL, dtype=src.dtype, device="cuda")
+        tk.topkv_pack_layer_shards(src, 1, wl.num_reqs, bt, bt.shape[1], lens, 0, H, S, out,
+                                   shard_bytes=cap * wl.elem_bytes)
+        torch.cuda.synchronize()
+        want = rs.pack_layer_shards(src_h, 1, wl.block_tables, wl.seq_lens, 0, H, S, cap)
+        got = to_host(out)
+        for sh in range(S):
+            assert np.array_equal(got[sh * cap:sh * cap + per], want[sh * cap:sh * cap + per]), f"S={S} shard {sh}"
+            assert torch.equal(out[sh * cap + per:(sh + 1) * cap],
+                               torch.full_like(out[sh * cap + per:(sh + 1) * cap], SENTINEL)), f"S={S}: slack written"
+        tk.topkv_unpack_layer_shards(out, dst, 0, wl.num_reqs, bt2, bt2.shape[1], lens, 0, H, S,
+                                     shard_bytes=cap * wl.elem_bytes)
+        rs.move_layer(rs.View(rs.PACKED, want, shards=S, shard_elems=cap),
+                      rs.View(rs.POOL, want_pool, 0, wl.dst_block_tables), wl.seq_lens, H)
+    torch.cuda.synchronize()
+    assert np.array_equal(to_host(dst), want_pool), f"{case}: pool after sharded unpacks differs"
+
+
 def test_untrusted_tables_and_lengths(tk):
     """Out-of-range table entries are skipped, lengths are clamped to the
     table capacity and negative lengths count as zero; nothing else moves."""
@@ -201,6 +233,25 @@ def test_fullsize_70b_head_slices(tk):
         if layer in (0, 79):
             want = rs.pack_layer_heads(to_host(src[layer])[None], 0, wl.block_tables, wl.seq_lens, 4, 4)
             assert np.array_equal(to_host(halves[1]), want), f"layer {layer}: heads 4-7 vs oracle"
+    del src
+    torch.cuda.empty_cache()
+
+
+def test_fullsize_70b_shards_one_launch(tk):
+    """70B, 4096 tokens: both tensor-parallel halves in one launch equal the
+    two head-sliced launches, on every layer."""
+    wl = make_workload("llama3-70b-4k")
+    src = device_src_pool(wl)
+    bt, lens = to_dev(wl.block_tables), to_dev(wl.seq_lens)
+    n = int(wl.seq_lens[0])
+    half = 2 * n * 4 * 128
+    both = torch.empty(2 * half, dtype=torch.int16, device="cuda")
+    sep = torch.empty(2 * half, dtype=torch.int16, device="cuda")
+    for layer in range(wl.num_layers):
+        tk.topkv_pack_layer_shards(src, layer, 1, bt, bt.shape[1], lens, 0, 8, 2, both)
+        for i in range(2):
+            tk.topkv_pack_layer_heads(src, layer, 1, bt, bt.shape[1], lens, 4 * i, 4, sep[i * half:(i + 1) * half])
+        assert torch.equal(both, sep), f"layer {layer}: one-launch shards differ from per-shard launches"
     del src
     torch.cuda.empty_cache()
 
