@@ -40,6 +40,9 @@ namespace topkv_reshard {
 #ifndef TOPKV_RS_VPT
 #define TOPKV_RS_VPT 8            // pieces per lane per tile
 #endif
+#ifndef TOPKV_RS_SINGLE
+#define TOPKV_RS_SINGLE 1         // direct grid for one request without a window
+#endif
 #ifndef TOPKV_RS_WG_PER_CU
 #define TOPKV_RS_WG_PER_CU 16     // grid cap = CUs * this
 #endif
@@ -247,58 +250,127 @@ __global__ __launch_bounds__(kThreads) void kv_reshard_kernel(Params p, const in
 
   PageCache src_pc, dst_pc;
   for (uint32_t base = blockIdx.x * kTile; base < total; base += gridDim.x * kTile) {
-    V v[kVpt];
-    int64_t doff[kVpt];
+    // Three phases: every piece's addresses (searches, divisions, table
+    // lookups), then every load, then every store.  No loop or branch sits
+    // between the loads, so all kVpt of them are in flight at once; a skipped
+    // piece loads from the source base (always valid) and is not stored.
+    int64_t soff[kVpt], doff[kVpt];
     bool ok[kVpt];
 #pragma unroll
     for (int j = 0; j < kVpt; ++j) {
-      doff[j] = 0;
+      soff[j] = doff[j] = 0;
       ok[j] = false;
       if (kWave) {
         const uint32_t wbase = base + j * kThreads + wave_first;   // uniform
-        if (wbase >= total) continue;                               // the whole span is past the end
-        const uint32_t q2 = fdiv(wbase, p.ktp);
-        const uint32_t m = wbase - q2 * per_tp + lane;              // < per_tp
-        const uint32_t k = fdiv(m, p.vpg);
-        const uint32_t e = m - k * p.vpg.d;
-        Loc at = locate(q2, tp, st, cnt, p.num_reqs);
-        at.r = __builtin_amdgcn_readfirstlane(at.r);
-        at.c = __builtin_amdgcn_readfirstlane(at.c);
-        at.t = __builtin_amdgcn_readfirstlane(at.t);
-        int64_t soff = 0, o = 0;
-        // both sides' table entries are in-bounds reads whatever the other side
-        // holds, so both lookups issue before either is tested (bitwise &)
-        const bool s_ok = p.src.packed ? packed_offset<VB>(p, q2, k, e, &soff)
-                                       : pool_offset_wave(p.src, at, k, e * VB, src_pc, &soff);
-        const bool d_ok = p.dst.packed ? packed_offset<VB>(p, q2, k, e, &o)
-                                       : pool_offset_wave(p.dst, at, k, e * VB, dst_pc, &o);
-        const bool good = s_ok & d_ok;
-        ok[j] = good;
-        doff[j] = o;
-        if (good) v[j] = __builtin_nontemporal_load(reinterpret_cast<const V*>(p.src.base + soff));
+        if (wbase < total) {
+          const uint32_t q2 = fdiv(wbase, p.ktp);
+          const uint32_t m = wbase - q2 * per_tp + lane;            // < per_tp
+          const uint32_t k = fdiv(m, p.vpg);
+          const uint32_t e = m - k * p.vpg.d;
+          Loc at = locate(q2, tp, st, cnt, p.num_reqs);
+          at.r = __builtin_amdgcn_readfirstlane(at.r);
+          at.c = __builtin_amdgcn_readfirstlane(at.c);
+          at.t = __builtin_amdgcn_readfirstlane(at.t);
+          int64_t so = 0, o = 0;
+          // both sides' table entries are in-bounds reads whatever the other
+          // side holds, so both lookups issue before either is tested
+          const bool s_ok = p.src.packed ? packed_offset<VB>(p, q2, k, e, &so)
+                                         : pool_offset_wave(p.src, at, k, e * VB, src_pc, &so);
+          const bool d_ok = p.dst.packed ? packed_offset<VB>(p, q2, k, e, &o)
+                                         : pool_offset_wave(p.dst, at, k, e * VB, dst_pc, &o);
+          ok[j] = s_ok & d_ok;
+          soff[j] = ok[j] ? so : 0;
+          doff[j] = o;
+        }
       } else {
         const uint32_t idx = base + j * kThreads + threadIdx.x;
-        if (idx >= total) continue;
-        const uint32_t q = fdiv(idx, p.vpg);
-        const uint32_t e = idx - q * p.vpg.d;
-        const uint32_t q2 = fdiv(q, p.gpt);
-        const uint32_t k = q - q2 * p.gpt.d;
-        const Loc at = locate(q2, tp, st, cnt, p.num_reqs);
-        int64_t soff = 0, o = 0;
-        const bool s_ok = p.src.packed ? packed_offset<VB>(p, q2, k, e, &soff)
-                                       : pool_offset(p.src, at.r, at.c, at.t, k, e * VB, &soff);
-        const bool d_ok = p.dst.packed ? packed_offset<VB>(p, q2, k, e, &o)
-                                       : pool_offset(p.dst, at.r, at.c, at.t, k, e * VB, &o);
-        const bool good = s_ok & d_ok;
-        ok[j] = good;
-        doff[j] = o;
-        if (good) v[j] = __builtin_nontemporal_load(reinterpret_cast<const V*>(p.src.base + soff));
+        if (idx < total) {
+          const uint32_t q = fdiv(idx, p.vpg);
+          const uint32_t e = idx - q * p.vpg.d;
+          const uint32_t q2 = fdiv(q, p.gpt);
+          const uint32_t k = q - q2 * p.gpt.d;
+          const Loc at = locate(q2, tp, st, cnt, p.num_reqs);
+          int64_t so = 0, o = 0;
+          const bool s_ok = p.src.packed ? packed_offset<VB>(p, q2, k, e, &so)
+                                         : pool_offset(p.src, at.r, at.c, at.t, k, e * VB, &so);
+          const bool d_ok = p.dst.packed ? packed_offset<VB>(p, q2, k, e, &o)
+                                         : pool_offset(p.dst, at.r, at.c, at.t, k, e * VB, &o);
+          ok[j] = s_ok & d_ok;
+          soff[j] = ok[j] ? so : 0;
+          doff[j] = o;
+        }
       }
     }
+    V v[kVpt];
+#pragma unroll
+    for (int j = 0; j < kVpt; ++j) v[j] = __builtin_nontemporal_load(reinterpret_cast<const V*>(p.src.base + soff[j]));
 #pragma unroll
     for (int j = 0; j < kVpt; ++j)
       if (ok[j]) __builtin_nontemporal_store(v[j], reinterpret_cast<V*>(p.dst.base + doff[j]));
   }
+}
+
+// One request, no window, wave-uniform tokens (every 70B-class shape):
+// workgroup (x, y) copies tile x of plane y.  A token's page depends only on
+// the token, not on the request's length, so each wave's first page lookups
+// go out together with the length load; there is no prefix scan.  Pieces of
+// tokens at or past the (clamped) length are skipped.
+template <int VB>
+__global__ __launch_bounds__(kThreads) void kv_reshard_single_kernel(Params p,
+                                                                    const int32_t* __restrict__ seq_lens) {
+  typedef typename Vec<VB>::type V;
+  constexpr uint32_t kTile = (uint32_t)kThreads * kVpt;
+  const uint32_t per_tp = p.ktp.d;
+  const uint32_t lane = threadIdx.x & 63u;
+  const uint32_t wave_first = __builtin_amdgcn_readfirstlane(threadIdx.x & ~63u);
+  const uint32_t c = blockIdx.y;
+  const uint32_t base = blockIdx.x * kTile;
+  PageCache src_pc, dst_pc;
+  {
+    // the first span's token is known before the length: prime the page caches
+    const uint32_t t0 = fdiv(base + wave_first, p.ktp);
+    if (t0 < (uint32_t)p.max_tok) {
+      const Loc at0{0, c, t0};
+      int64_t unused;
+      if (!p.src.packed) pool_offset_wave(p.src, at0, 0, 0, src_pc, &unused);
+      if (!p.dst.packed) pool_offset_wave(p.dst, at0, 0, 0, dst_pc, &unused);
+    }
+  }
+  int32_t n = __builtin_amdgcn_readfirstlane(seq_lens[0]);
+  n = n < 0 ? 0 : (n > p.max_tok ? p.max_tok : n);
+  const uint32_t end = (uint32_t)n * per_tp;                  // pieces of this plane
+  // Each load issues as soon as its address is known (there is no loop here
+  // to hold it up); a skipped piece loads the source base and is not stored.
+  V v[kVpt];
+  int64_t doff[kVpt];
+  bool ok[kVpt];
+#pragma unroll
+  for (int j = 0; j < kVpt; ++j) {
+    int64_t soff = 0;
+    doff[j] = 0;
+    ok[j] = false;
+    const uint32_t wbase = base + j * kThreads + wave_first;    // uniform, within plane c
+    if (wbase < end) {
+      const uint32_t t = fdiv(wbase, p.ktp);
+      const uint32_t m = wbase - t * per_tp + lane;
+      const uint32_t k = fdiv(m, p.vpg);
+      const uint32_t e = m - k * p.vpg.d;
+      const Loc at{0, c, t};
+      const uint32_t q2 = c * (uint32_t)n + t;                  // global (plane, token) index
+      int64_t so = 0, o = 0;
+      const bool s_ok = p.src.packed ? packed_offset<VB>(p, q2, k, e, &so)
+                                     : pool_offset_wave(p.src, at, k, e * VB, src_pc, &so);
+      const bool d_ok = p.dst.packed ? packed_offset<VB>(p, q2, k, e, &o)
+                                     : pool_offset_wave(p.dst, at, k, e * VB, dst_pc, &o);
+      ok[j] = s_ok & d_ok;
+      soff = ok[j] ? so : 0;
+      doff[j] = o;
+    }
+    v[j] = __builtin_nontemporal_load(reinterpret_cast<const V*>(p.src.base + soff));
+  }
+#pragma unroll
+  for (int j = 0; j < kVpt; ++j)
+    if (ok[j]) __builtin_nontemporal_store(v[j], reinterpret_cast<V*>(p.dst.base + doff[j]));
 }
 
 // ---------------------------------------------------------------------------
@@ -373,6 +445,16 @@ KernelFn kernel_for_mode(int vb) {
 
 KernelFn kernel_for(int vb, bool wave) { return wave ? kernel_for_mode<true>(vb) : kernel_for_mode<false>(vb); }
 
+KernelFn single_kernel_for(int vb) {
+  switch (vb) {
+    case 16: return kv_reshard_single_kernel<16>;
+    case 8: return kv_reshard_single_kernel<8>;
+    case 4: return kv_reshard_single_kernel<4>;
+    case 2: return kv_reshard_single_kernel<2>;
+    default: return kv_reshard_single_kernel<1>;
+  }
+}
+
 topkv_status_t move_layer(const topkv_view_t* src, const topkv_view_t* dst, int32_t num_reqs,
                           const int32_t* seq_lens, int32_t head_count, int32_t window, hipStream_t stream) {
   if (!src || !dst || !valid_layout(src->layout) || !valid_layout(dst->layout)) return TOPKV_ERR_INVALID_ARG;
@@ -436,6 +518,9 @@ topkv_status_t move_layer(const topkv_view_t* src, const topkv_view_t* dst, int3
   const int64_t bound = (int64_t)num_reqs * max_tok * geo->planes * gpt * vpg;
   if (max_tok <= 0) return TOPKV_OK;
   if (bound >= ((int64_t)1 << 31) || vpg >= ((int64_t)1 << 31)) return TOPKV_ERR_UNSUPPORTED;
+  // Skipped pieces load from the source's base, so it must hold one piece; a
+  // packed source smaller than that holds nothing to move.
+  if (src->layout == TOPKV_LAYOUT_PACKED && packed_cap < vb) return TOPKV_OK;
 
   Params p = {};
   for (int i = 0; i < 2; ++i) {
@@ -477,7 +562,13 @@ topkv_status_t move_layer(const topkv_view_t* src, const topkv_view_t* dst, int3
   if (blocks < 1) blocks = 1;
   const size_t lds = sizeof(int32_t) * (kWaves + 3 * (size_t)num_reqs + 1);
   const bool wave = (gpt * vpg) % 64 == 0;
-  hipLaunchKernelGGL(kernel_for(vb, wave), dim3((unsigned)blocks), dim3(kThreads), lds, stream, p, seq_lens);
+  const int64_t plane_tiles = (max_tok * gpt * vpg + tile - 1) / tile;
+  if (TOPKV_RS_SINGLE && num_reqs == 1 && window == 0 && wave && plane_tiles <= INT32_MAX && geo->planes <= 65535) {
+    hipLaunchKernelGGL(single_kernel_for(vb), dim3((unsigned)plane_tiles, (unsigned)geo->planes), dim3(kThreads), 0,
+                       stream, p, seq_lens);
+  } else {
+    hipLaunchKernelGGL(kernel_for(vb, wave), dim3((unsigned)blocks), dim3(kThreads), lds, stream, p, seq_lens);
+  }
   return hipGetLastError() == hipSuccess ? TOPKV_OK : TOPKV_ERR_LAUNCH;
 }
 
