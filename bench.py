@@ -45,7 +45,16 @@ sys.path.insert(0, ROOT)
 
 HBM_PEAK_GBS = 8000.0          # MI355X HBM3E, AMD published peak
 PROFILES = os.path.join(ROOT, "profiles")
-KERNEL_SOURCE = os.path.join(ROOT, "paper_2607_28633_amd", "csrc", "topkv.hip")
+# the per-layer pack/unpack kernels: the fast kernels and the layout-move kernel
+# (whose one-request direct grid runs single-request layers)
+KERNEL_SOURCES = [os.path.join(ROOT, "paper_2607_28633_amd", "csrc", n) for n in ("topkv.hip", "reshard.hip")]
+
+
+def kernel_source_digest():
+    h = hashlib.sha256()
+    for path in KERNEL_SOURCES:
+        h.update(open(path, "rb").read())
+    return h.hexdigest()
 
 
 def log(msg):
@@ -94,6 +103,19 @@ def layer_bytes(wl, layer):
     return 2 * moved + 4 * pages + 4 * wl.num_reqs, 2 * moved + 4 * pages2 + 4 * wl.num_reqs
 
 
+def layer_kernel(wl, direction):
+    """The kernel a full-attention layer's launch runs: the library hands one
+    request with no window (a token's 16-byte pieces filling whole 64-lane
+    wave spans, the buffer holding the table's full bound) to the layout-move
+    kernel's direct grid, everything else to the fast kernels."""
+    row = wl.num_heads * wl.head_dim * wl.elem_bytes
+    tables, page = (wl.block_tables, wl.page_size) if direction == "pack" else (wl.dst_block_tables, wl.dst_page_size)
+    full_bound = wl.num_reqs == 1 and tables.shape[1] * page <= int(wl.seq_lens[0])   # packed slice = the lengths
+    if full_bound and not any(wl.window(l) for l in range(wl.num_layers)) and row % (64 * 16) == 0:
+        return "kv_reshard_single_kernel"
+    return f"kv_{direction}_kernel"
+
+
 def step_bytes(wl):
     """Algorithmic bytes of one pack and one unpack launch, averaged over layers."""
     per = [layer_bytes(wl, l) for l in range(wl.num_layers)]
@@ -111,8 +133,7 @@ def read_traffic(workload):
         if "=" in line and not line.lstrip().startswith("#"):
             k, v = line.split("=", 1)
             vals[k.strip()] = v.strip()
-    digest = hashlib.sha256(open(KERNEL_SOURCE, "rb").read()).hexdigest()
-    if vals.get("kernel_source_sha256") != digest:
+    if vals.get("kernel_source_sha256") != kernel_source_digest():
         return None
     return vals
 
@@ -281,7 +302,7 @@ def run(args):
     achieved = kern[dom]["gbs"]
     roofline = {"bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s",
                 "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": traffic,
-                "kernel": f"kv_{dom}_kernel", "bytes_per_launch": kern[dom]["bytes_per_launch"],
+                "kernel": f"{dom} launch: {layer_kernel(wl, dom)}", "bytes_per_launch": kern[dom]["bytes_per_launch"],
                 "avg_launch_us": kern[dom]["avg_us"]}
 
     # practical ceiling on this machine: a plain device copy of one layer's bytes

@@ -1,0 +1,23 @@
+// internal.h - calls between the library's own sources (not part of the C ABI).
+#ifndef TOPKV_INTERNAL_H_
+#define TOPKV_INTERNAL_H_
+
+#include "topkv.h"
+
+namespace topkv_internal {
+
+// A plain pack (pool -> packed, every head) or unpack (packed -> pool) of one
+// request with a device length and no window, run by the layout-move
+// kernel's one-request direct grid when that grid applies (a token's pieces
+// fill whole wave spans).  *launched tells whether it launched; when it did
+// not, nothing was queued and the caller launches its own kernel.  The caller
+// has validated the arguments; `launch` carries the stream and the optional
+// start/stop events.
+__attribute__((visibility("hidden")))
+topkv_status_t single_request_move(bool pack, const topkv_pool_t* pool, int32_t layer, void* packed,
+                                   int64_t packed_cap, const int32_t* tables, int32_t bt_stride,
+                                   const int32_t* seq_lens, const topkv_launch_t* launch, bool* launched);
+
+}  // namespace topkv_internal
+
+#endif  // TOPKV_INTERNAL_H_

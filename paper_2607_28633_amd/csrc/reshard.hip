@@ -29,10 +29,12 @@
 // tiles on a grid capped at a few workgroups per CU.  Table entries and
 // lengths are bounds-checked on the device before any access.
 #include <hip/hip_runtime.h>
+#include <hip/hip_ext.h>
 
 #include <atomic>
 #include <cstdint>
 
+#include "internal.h"
 #include "topkv.h"
 
 namespace topkv_reshard {
@@ -455,8 +457,12 @@ KernelFn single_kernel_for(int vb) {
   }
 }
 
-topkv_status_t move_layer(const topkv_view_t* src, const topkv_view_t* dst, int32_t num_reqs,
-                          const int32_t* seq_lens, int32_t head_count, int32_t window, hipStream_t stream) {
+// single_only: launch only the one-request direct grid (and report whether it
+// did through *launched); otherwise whichever grid applies.
+topkv_status_t move_layer_impl(const topkv_view_t* src, const topkv_view_t* dst, int32_t num_reqs,
+                               const int32_t* seq_lens, int32_t head_count, int32_t window,
+                               const topkv_launch_t& launch, bool single_only, bool* launched) {
+  *launched = false;
   if (!src || !dst || !valid_layout(src->layout) || !valid_layout(dst->layout)) return TOPKV_ERR_INVALID_ARG;
   if (src->layout == TOPKV_LAYOUT_PACKED && dst->layout == TOPKV_LAYOUT_PACKED) return TOPKV_ERR_INVALID_ARG;
   if (num_reqs < 0 || head_count <= 0 || window < 0 || (num_reqs > 0 && !seq_lens)) return TOPKV_ERR_INVALID_ARG;
@@ -563,13 +569,26 @@ topkv_status_t move_layer(const topkv_view_t* src, const topkv_view_t* dst, int3
   const size_t lds = sizeof(int32_t) * (kWaves + 3 * (size_t)num_reqs + 1);
   const bool wave = (gpt * vpg) % 64 == 0;
   const int64_t plane_tiles = (max_tok * gpt * vpg + tile - 1) / tile;
-  if (TOPKV_RS_SINGLE && num_reqs == 1 && window == 0 && wave && plane_tiles <= INT32_MAX && geo->planes <= 65535) {
-    hipLaunchKernelGGL(single_kernel_for(vb), dim3((unsigned)plane_tiles, (unsigned)geo->planes), dim3(kThreads), 0,
-                       stream, p, seq_lens);
-  } else {
-    hipLaunchKernelGGL(kernel_for(vb, wave), dim3((unsigned)blocks), dim3(kThreads), lds, stream, p, seq_lens);
-  }
-  return hipGetLastError() == hipSuccess ? TOPKV_OK : TOPKV_ERR_LAUNCH;
+  const bool single = TOPKV_RS_SINGLE && num_reqs == 1 && window == 0 && wave && plane_tiles <= INT32_MAX &&
+                      geo->planes <= 65535;
+  if (single_only && !single) return TOPKV_OK;
+  const dim3 grid = single ? dim3((unsigned)plane_tiles, (unsigned)geo->planes) : dim3((unsigned)blocks);
+  const KernelFn fn = single ? single_kernel_for(vb) : kernel_for(vb, wave);
+  const size_t shmem = single ? 0 : lds;
+  if (launch.start || launch.stop)
+    hipExtLaunchKernelGGL(fn, grid, dim3(kThreads), shmem, launch.stream, launch.start, launch.stop, 0, p, seq_lens);
+  else
+    hipLaunchKernelGGL(fn, grid, dim3(kThreads), shmem, launch.stream, p, seq_lens);
+  if (hipGetLastError() != hipSuccess) return TOPKV_ERR_LAUNCH;
+  *launched = true;
+  return TOPKV_OK;
+}
+
+topkv_status_t move_layer(const topkv_view_t* src, const topkv_view_t* dst, int32_t num_reqs,
+                          const int32_t* seq_lens, int32_t head_count, int32_t window, hipStream_t stream) {
+  topkv_launch_t launch = {stream, nullptr, nullptr};
+  bool launched = false;
+  return move_layer_impl(src, dst, num_reqs, seq_lens, head_count, window, launch, false, &launched);
 }
 
 topkv_view_t pool_view(int32_t layout, const topkv_pool_t* pool, int32_t layer, const int32_t* tables,
@@ -596,6 +615,26 @@ topkv_view_t packed_view(const void* data, int64_t bytes, int32_t shards = 1) {
 }  // namespace topkv_reshard
 
 using namespace topkv_reshard;
+
+namespace topkv_internal {
+
+topkv_status_t single_request_move(bool pack, const topkv_pool_t* pool, int32_t layer, void* packed,
+                                   int64_t packed_cap, const int32_t* tables, int32_t bt_stride,
+                                   const int32_t* seq_lens, const topkv_launch_t* launch, bool* launched) {
+  *launched = false;
+  const topkv_view_t pv = pool_view(TOPKV_LAYOUT_POOL, pool, layer, tables, bt_stride, 0);
+  const topkv_view_t kv = packed_view(packed, packed_cap, 1);
+  const topkv_status_t st = pack ? move_layer_impl(&pv, &kv, 1, seq_lens, pool->num_heads, 0, *launch, true, launched)
+                                 : move_layer_impl(&kv, &pv, 1, seq_lens, pool->num_heads, 0, *launch, true, launched);
+  // anything this path does not take (limits, shapes) goes back to the caller's kernel
+  if (st == TOPKV_ERR_INVALID_ARG || st == TOPKV_ERR_UNSUPPORTED || st == TOPKV_ERR_BOUNDS) {
+    *launched = false;
+    return TOPKV_OK;
+  }
+  return st;
+}
+
+}  // namespace topkv_internal
 
 extern "C" {
 

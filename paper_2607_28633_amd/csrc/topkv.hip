@@ -33,6 +33,7 @@
 #include <atomic>
 #include <cstdint>
 
+#include "internal.h"
 #include "topkv.h"
 
 #ifndef TOPKV_VPT
@@ -46,6 +47,9 @@
 #endif
 #ifndef TOPKV_NONTEMPORAL
 #define TOPKV_NONTEMPORAL 1   // streaming hint on the bulk loads and stores
+#endif
+#ifndef TOPKV_ROUTE_SINGLE
+#define TOPKV_ROUTE_SINGLE 1  // one whole-request move with a device length runs the layout-move direct grid
 #endif
 #ifndef TOPKV_THREADS
 #define TOPKV_THREADS 256     // threads per workgroup (a multiple of 64)
@@ -504,6 +508,19 @@ topkv_status_t launch_move(bool pack, const topkv_pool_t* pool, int32_t layer, v
   if (num_reqs > TOPKV_MAX_BATCH_REQS) return TOPKV_ERR_UNSUPPORTED;
   if (num_reqs == 0 || (!seq_lens && n_single == 0)) return TOPKV_OK;  // nothing to move
   if (!tables || !packed || bt_stride <= 0) return TOPKV_ERR_INVALID_ARG;
+
+  // One request with a device length, every token kept and the packed
+  // buffer large enough for the whole table: the layout-move kernel's
+  // one-request grid does the same copy with less index work per piece.
+  int64_t full_bound;
+  if (TOPKV_ROUTE_SINGLE && seq_lens && num_reqs == 1 && window == 0 && plane_stride == 0 &&
+      !__builtin_mul_overflow((int64_t)pool->planes * bt_stride * pool->page_size, g.row_bytes, &full_bound) &&
+      packed_cap >= full_bound) {
+    bool launched = false;
+    st = topkv_internal::single_request_move(pack, pool, layer, packed, packed_cap, tables, bt_stride, seq_lens,
+                                             launch, &launched);
+    if (st != TOPKV_OK || launched) return st;
+  }
 
   int vb = vector_bytes(reinterpret_cast<uintptr_t>(pool->base), reinterpret_cast<uintptr_t>(packed), g.row_bytes);
   while (plane_stride % vb) vb >>= 1;             // placed planes keep every run vector-aligned

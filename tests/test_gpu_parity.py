@@ -221,3 +221,57 @@ def test_untrusted_device_inputs(tk):
     oracle.unpack_layer(full, want_dst, 0, wl.dst_block_tables, lens)
     want_dst[0, wl.dst_block_tables[0, 1]] = keep
     assert np.array_equal(to_host(dst), want_dst)
+
+
+@pytest.mark.parametrize("n", [100, 10_000, -3, 0, 1, 127])
+def test_one_request_device_length(tk, n):
+    """One request with a device length and 1 KiB rows (4 heads x 128 x
+    2 bytes): with a packed buffer sized for the whole block table the move
+    runs the layout-move kernel's one-request grid, one vector short of that
+    the per-page kernel.  Both must skip out-of-range table entries, clamp
+    the length to the table (negative counts as zero) and leave a request
+    that overruns the buffer unmoved."""
+    P, W, NP, layer = 16, 8, 40, 1
+    wl = make_workload("tiny", seed=11, num_heads=4, head_dim=128, seq_lens=[100], num_pages=NP, dst_num_pages=NP)
+    C, H, D = wl.planes, wl.num_heads, wl.head_dim
+    row = C * H * D                                        # words per token over both planes
+    rng = np.random.default_rng(31)
+    good, good2 = (rng.permutation(NP)[:W].astype(np.int32) for _ in range(2))
+    spare = [p for p in range(NP) if p not in set(good2.tolist())][0]
+    bad, bad2 = good.copy(), good2.copy()
+    bad[2], bad[5] = -1, NP
+    bad2[3] = -7
+    clamp = min(max(n, 0), W * P)
+    src_h, dst_h = host_src_pool(wl), host_dst_prefill(wl)
+    src = to_dev(src_h)
+    lens = to_dev(np.array([n], dtype=np.int32))
+    packed_want = oracle.pack_layer(src_h, layer, good[None], np.array([clamp], np.int32))
+    full = W * P * row * 2                                 # bytes for the whole table
+    for cap in (full, full - 16):
+        say(f"[one_request] n={n} cap={cap}")
+        moved = clamp * row * 2 <= cap
+        sentinel = 0x2B2B
+        packed = torch.full((full // 2,), sentinel, dtype=torch.int16, device="cuda")
+        tk.topkv_pack_layer_batched(src, layer, 1, to_dev(bad), W, lens, packed, dst_bytes=cap)
+        torch.cuda.synchronize()
+        want = np.full(full // 2, sentinel, dtype=np.uint16)
+        if moved:
+            want[:packed_want.size] = packed_want
+            blk = want[:packed_want.size].reshape(C, clamp, H * D)
+            for i in (2, 5):
+                blk[:, i * P:(i + 1) * P] = sentinel
+        assert np.array_equal(to_host(packed).view(np.uint16), want), f"n={n} cap={cap}: pack differs"
+
+        dst = to_dev(dst_h)
+        src_packed = np.zeros(full // 2, dtype=np.uint16)
+        src_packed[:packed_want.size] = packed_want
+        tk.topkv_unpack_layer_batched(to_dev(src_packed), dst, layer, 1, to_dev(bad2), W, lens, src_bytes=cap)
+        torch.cuda.synchronize()
+        want_dst = dst_h.copy()
+        if moved:
+            tbl = good2.copy()
+            tbl[3] = spare
+            keep = want_dst[layer, spare].copy()
+            oracle.unpack_layer(packed_want, want_dst, layer, tbl[None], np.array([clamp], np.int32))
+            want_dst[layer, spare] = keep
+        assert np.array_equal(to_host(dst), want_dst), f"n={n} cap={cap}: unpack differs"
