@@ -46,13 +46,15 @@ sys.path.insert(0, ROOT)
 HBM_PEAK_GBS = 8000.0          # MI355X HBM3E, AMD published peak
 PROFILES = os.path.join(ROOT, "profiles")
 # the per-layer pack/unpack kernels: the fast kernels and the layout-move kernel
-# (whose one-request direct grid runs single-request layers)
+# (whose one-request direct grid runs single-request layers); models with
+# fixed-state layers add the state kernel
 KERNEL_SOURCES = [os.path.join(ROOT, "paper_2607_28633_amd", "csrc", n) for n in ("topkv.hip", "reshard.hip")]
+STATE_SOURCE = os.path.join(ROOT, "paper_2607_28633_amd", "csrc", "state.hip")
 
 
-def kernel_source_digest():
+def kernel_source_digest(with_state=False):
     h = hashlib.sha256()
-    for path in KERNEL_SOURCES:
+    for path in KERNEL_SOURCES + ([STATE_SOURCE] if with_state else []):
         h.update(open(path, "rb").read())
     return h.hexdigest()
 
@@ -89,7 +91,11 @@ def parse():
 def layer_bytes(wl, layer):
     """Algorithmic bytes of layer `layer`'s pack launch and unpack launch:
     read + write of the kept tokens' rows, 4 B per table entry covering them
-    (P of the pool being read or written), 4 B per length."""
+    (P of the pool being read or written), 4 B per length.  A fixed-state
+    layer: read + write of every request's state, 4 B per slot index."""
+    if wl.is_state(layer):
+        b = 2 * wl.num_reqs * wl.state_bytes + 4 * wl.num_reqs
+        return b, b
     row = wl.num_heads * wl.head_dim * wl.elem_bytes
     W = wl.window(layer)
     kept = moved = pages = pages2 = 0
@@ -107,7 +113,10 @@ def layer_kernel(wl, direction):
     """The kernel a full-attention layer's launch runs: the library hands one
     request with no window (a token's 16-byte pieces filling whole 64-lane
     wave spans, the buffer holding the table's full bound) to the layout-move
-    kernel's direct grid, everything else to the fast kernels."""
+    kernel's direct grid, everything else to the fast kernels.  Fixed-state
+    layers run the state kernel."""
+    if wl.layer_state:
+        return f"kv_{direction}_kernel (attention layers), kv_state_kernel (state layers)"
     row = wl.num_heads * wl.head_dim * wl.elem_bytes
     tables, page = (wl.block_tables, wl.page_size) if direction == "pack" else (wl.dst_block_tables, wl.dst_page_size)
     full_bound = wl.num_reqs == 1 and tables.shape[1] * page <= int(wl.seq_lens[0])   # packed slice = the lengths
@@ -133,7 +142,8 @@ def read_traffic(workload):
         if "=" in line and not line.lstrip().startswith("#"):
             k, v = line.split("=", 1)
             vals[k.strip()] = v.strip()
-    if vals.get("kernel_source_sha256") != kernel_source_digest():
+    from paper_2607_28633_amd.workloads import make_workload
+    if vals.get("kernel_source_sha256") != kernel_source_digest(bool(make_workload(workload).layer_state)):
         return None
     return vals
 
@@ -149,11 +159,12 @@ def calib_copy(args):
     print(json.dumps({"calib_copy_bytes": n, "launches": args.warmup + args.steps}), flush=True)
 
 
-def cpu_baseline(wl, src, dst, budget_s):
+def cpu_baseline(wl, src, dst, budget_s, states=None):
     """Time the oracle on host copies of a few layer slabs, cycling until the
     budget is spent.  Returns the cpu_baseline object."""
     import numpy as np
     import oracle
+    import oracle.state
     import torch
 
     def to_host_words(t):   # device bf16 slab -> host uint16 words, bit-exact
@@ -161,14 +172,21 @@ def cpu_baseline(wl, src, dst, budget_s):
 
     slabs = list(range(min(wl.phys_layers, 4)))
     host = {s: (to_host_words(src[s])[None], to_host_words(dst[s])[None]) for s in slabs}
+    if states is not None:
+        st_h = (to_host_words(states[0][0])[None], to_host_words(states[1][0])[None])
     done_bytes, spent, layers = 0, 0.0, 0
     while spent < budget_s and layers < 10_000:
         s = slabs[layers % len(slabs)]
         src_h, dst_h = host[s]
-        W = wl.window(layers % wl.num_layers)
+        lay = layers % wl.num_layers
+        W = wl.window(lay)
         t0 = time.perf_counter()
-        packed = oracle.pack_layer(src_h, 0, wl.block_tables, wl.seq_lens, window=W)
-        oracle.unpack_layer(packed, dst_h, 0, wl.dst_block_tables, wl.seq_lens, window=W)
+        if wl.is_state(lay):
+            packed = oracle.state.pack_state_layer(st_h[0], 0, wl.state_slots)
+            oracle.state.unpack_state_layer(packed, st_h[1], 0, wl.dst_state_slots)
+        else:
+            packed = oracle.pack_layer(src_h, 0, wl.block_tables, wl.seq_lens, window=W)
+            oracle.unpack_layer(packed, dst_h, 0, wl.dst_block_tables, wl.seq_lens, window=W)
         spent += time.perf_counter() - t0
         done_bytes += sum(layer_bytes(wl, layers % wl.num_layers))
         layers += 1
@@ -182,7 +200,8 @@ def cpu_baseline(wl, src, dst, budget_s):
         pass
     return {"value": round(done_bytes / spent / 1e9, 3), "unit": "GB/s", "cores": 1, "kind": "oracle",
             "sample": (f"{layers} layer pack+unpack passes of {wl.name} over host copies of "
-                       f"{len(slabs)} layer slab(s), numpy oracle, one thread, {spent:.1f} s"),
+                       f"{len(slabs)} layer slab(s){' and one state-cache layer' if states is not None else ''}, "
+                       f"numpy oracle, one thread, {spent:.1f} s"),
             "cpu_model": cpu, "host_threads_available": len(os.sched_getaffinity(0)),
             "ms_per_layer_pack_unpack": round(1e3 * spent / layers, 3)}
 
@@ -192,7 +211,8 @@ def run(args):
     import torch
 
     from paper_2607_28633_amd import topkv
-    from paper_2607_28633_amd.workloads import WORKLOADS, device_dst_prefill, device_src_pool, make_workload
+    from paper_2607_28633_amd.workloads import (WORKLOADS, device_dst_prefill, device_src_pool, device_state_cache,
+                                                make_workload)
 
     torch.cuda.set_device(0)
     wl = make_workload(args.workload)
@@ -204,8 +224,16 @@ def run(args):
     lens = torch.from_numpy(wl.seq_lens).cuda()
     nbytes = topkv.topkv_packed_layer_bytes(src, wl.seq_lens)
     L, R = wl.num_layers, wl.num_reqs
-    ring = min(L, max(2, (2 << 30) // max(nbytes, 1)))
-    packed = torch.empty((ring, nbytes // 2), dtype=torch.int16, device="cuda")
+    states = None
+    slot_bytes = 0
+    if wl.layer_state:      # fixed-state layers: state caches and slot indices on the device
+        states = (device_state_cache(wl), device_state_cache(wl, dst=True))
+        slots = torch.from_numpy(wl.state_slots).cuda()
+        slots2 = torch.from_numpy(wl.dst_state_slots).cuda()
+        slot_bytes = R * wl.state_bytes
+    slice_bytes = max(nbytes, slot_bytes)
+    ring = min(L, max(2, (2 << 30) // max(slice_bytes, 1)))
+    packed = torch.empty((ring, slice_bytes // 2), dtype=torch.int16, device="cuda")
     stream = torch.cuda.current_stream()
     log(f"[bench] pools src {tuple(src.shape)} dst {tuple(dst.shape)}, packed {nbytes} B/layer, ring {ring}")
 
@@ -215,13 +243,19 @@ def run(args):
         calls = []
         for l in range(L):
             e = evs[l] if evs else (None, None)
-            if direction == 0:
+            if wl.is_state(l) and direction == 0:
+                calls.append(topkv.prepare_pack_state_layer(
+                    states[0], wl.state_slab(l), R, slots, packed[l % ring], stream=on, start=e[0], stop=e[1]))
+            elif wl.is_state(l):
+                calls.append(topkv.prepare_unpack_state_layer(
+                    packed[l % ring], states[1], wl.state_slab(l), R, slots2, stream=on, start=e[0], stop=e[1]))
+            elif direction == 0:
                 calls.append(topkv.prepare_pack_layer_window(
-                    src, l % wl.phys_layers, R, bt, bt.shape[1], lens, wl.window(l), packed[l % ring],
+                    src, wl.kv_slab(l), R, bt, bt.shape[1], lens, wl.window(l), packed[l % ring],
                     stream=on, start=e[0], stop=e[1]))
             else:
                 calls.append(topkv.prepare_unpack_layer_window(
-                    packed[l % ring], dst, l % wl.phys_layers, R, bt2, bt2.shape[1], lens, wl.window(l),
+                    packed[l % ring], dst, wl.kv_slab(l), R, bt2, bt2.shape[1], lens, wl.window(l),
                     stream=on, start=e[0], stop=e[1]))
         return calls
 
@@ -329,6 +363,8 @@ def run(args):
                    "launch": args.launch,
                    "tokens": int(wl.seq_lens.astype(np.int64).sum()), "page_size": wl.page_size,
                    "dst_page_size": wl.dst_page_size, "packed_bytes_per_layer": nbytes,
+                   **({"state_layers": sum(wl.layer_state), "packed_state_bytes_per_layer": slot_bytes}
+                      if wl.layer_state else {}),
                    "step": "pack every layer (1 launch each), then unpack every layer",
                    "seed": wl.seed, "packed_ring": ring, "phys_layers": wl.phys_layers},
         "pct_of_peak": round(100 * bytes_step / (ms_per_step * 1e-3) / 1e9 / HBM_PEAK_GBS, 2),
@@ -339,7 +375,7 @@ def run(args):
     }
     if args.cpu_seconds > 0:
         log(f"[bench] CPU oracle sample (~{args.cpu_seconds} s)")
-        out["cpu_baseline"] = cpu_baseline(wl, src, dst, args.cpu_seconds)
+        out["cpu_baseline"] = cpu_baseline(wl, src, dst, args.cpu_seconds, states)
     else:
         out["cpu_baseline"] = None
     print(json.dumps(out), flush=True)
@@ -420,7 +456,7 @@ def run_reshard(args):
 
     torch.cuda.set_device(0)
     wl = make_workload(args.workload)
-    if any(wl.window(l) for l in range(wl.num_layers)):
+    if any(wl.window(l) for l in range(wl.num_layers)) or wl.layer_state:
         raise SystemExit("reshard mode measures full-attention layers")
     log(f"[bench] reshard {wl.describe()}")
     src, dst = device_src_pool(wl), device_dst_prefill(wl)
@@ -525,6 +561,8 @@ def run_pipeline(args, check=None):
 
     torch.cuda.set_device(0)
     wl = make_workload(args.workload)
+    if wl.layer_state or any(wl.window(l) for l in range(wl.num_layers)):
+        raise SystemExit("pipeline mode ships full-attention layers")
     src = device_src_pool(wl)
     L, R = wl.num_layers, wl.num_reqs
     bt = torch.from_numpy(wl.block_tables).cuda()

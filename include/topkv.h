@@ -406,6 +406,51 @@ topkv_status_t topkv_reblock_layer(const topkv_pool_t* src, int32_t src_layer, c
                                    const int32_t* dst_tables, int32_t dst_stride, int32_t num_reqs,
                                    const int32_t* seq_lens, hipStream_t stream);
 
+/* ---- Fixed-state layers (Section 2.2) ------------------------------------
+ * Section 2.2 extends Eq. 1 per layer kind: a linear-attention layer holds,
+ * per request, a state whose size does not depend on the sequence length.
+ * The state cache keeps one request's state of one layer in a slot:
+ *   [num_layers][num_slots][state_bytes] bytes at base (device memory).
+ * A packed state batch is the requests' states in request order: request r
+ * at bytes [r * state_bytes, (r + 1) * state_bytes).  Bytes are opaque. */
+typedef struct topkv_state_pool {
+  void*   base;         /* device memory, [num_layers][num_slots][state_bytes] */
+  int64_t num_slots;    /* slots per layer, > 0 */
+  int64_t state_bytes;  /* one request's state in one layer, > 0 */
+  int32_t num_layers;   /* > 0 */
+  int32_t reserved;     /* must be 0 */
+} topkv_state_pool_t;
+
+/* num_reqs * state_bytes, or -1 for a bad descriptor, num_reqs < 0 or
+ * overflow. */
+int64_t topkv_packed_state_bytes(const topkv_state_pool_t* pool, int32_t num_reqs);
+
+/* Pack one fixed-state layer of num_reqs requests in one launch.
+ *   src:       state cache (host struct describing device memory)
+ *   layer:     in [0, src->num_layers)
+ *   slots:     device int32[num_reqs], request r's slot; a slot outside
+ *              [0, num_slots) is skipped (its bytes of dst are not written)
+ *   dst:       device buffer of dst_bytes >= num_reqs * state_bytes bytes
+ *   launch:    stream and optional kernel-timestamp events (non-null)
+ * num_reqs == 0 launches nothing.  TOPKV_ERR_INVALID_ARG for a bad
+ * descriptor, layer, num_reqs < 0, null slots/dst, or dst_bytes too small;
+ * TOPKV_ERR_UNSUPPORTED when a state spans 2^31 or more tiles of 32 KiB;
+ * TOPKV_ERR_LAUNCH if the launch fails.  One kernel on the stream; 16-byte
+ * vectors when base, dst and state_bytes are 16-byte multiples, narrower
+ * ones otherwise. */
+topkv_status_t topkv_pack_state_layer(const topkv_state_pool_t* src, int32_t layer, int32_t num_reqs,
+                                      const int32_t* slots, void* dst, int64_t dst_bytes,
+                                      const topkv_launch_t* launch);
+
+/* Unpack: request r's state from src into slot slots[r] of layer `layer` of
+ * dst; every other slot keeps its contents, and a slot outside the cache is
+ * skipped.  Slots must be distinct (two requests naming one slot race).
+ * src_bytes >= num_reqs * state_bytes, else TOPKV_ERR_INVALID_ARG; other
+ * errors as for topkv_pack_state_layer. */
+topkv_status_t topkv_unpack_state_layer(const void* src, int64_t src_bytes, const topkv_state_pool_t* dst,
+                                        int32_t layer, int32_t num_reqs, const int32_t* slots,
+                                        const topkv_launch_t* launch);
+
 /* Layer shipper (Sec. 5.2: layer l's cache leaves while layers l+1 .. L still
  * compute).  Copies run on the GPU's DMA engines (ROCr asynchronous copies),
  * so they take no compute unit from the kernels still running; a worker

@@ -15,7 +15,8 @@ import sys
 
 PKG = os.path.dirname(os.path.abspath(__file__))
 ROOT = os.path.dirname(PKG)
-SOURCES = [os.path.join(PKG, "csrc", n) for n in ("topkv.hip", "check.hip", "kvcache1.hip", "dma.hip", "reshard.hip")]
+SOURCES = [os.path.join(PKG, "csrc", n) for n in ("topkv.hip", "check.hip", "kvcache1.hip", "dma.hip", "reshard.hip",
+                                                        "state.hip")]
 INCLUDE = os.path.join(ROOT, "include")
 LIBRARY = os.path.join(PKG, "libtopkv.so")
 ARCH = "gfx950"

@@ -45,7 +45,8 @@ EXPORTS = ["topkv_pack_layer", "topkv_unpack_layer", "topkv_pack_layer_batched",
            "topkv_kvcache1_unpack_layer", "topkv_crc64", "topkv_crc64_workspace_bytes", "topkv_dma_create",
            "topkv_dma_submit", "topkv_dma_wait", "topkv_dma_destroy", "topkv_move_layer",
            "topkv_pack_layer_heads", "topkv_unpack_layer_heads", "topkv_reblock_layer",
-           "topkv_pack_layer_shards", "topkv_unpack_layer_shards"]
+           "topkv_pack_layer_shards", "topkv_unpack_layer_shards", "topkv_packed_state_bytes",
+           "topkv_pack_state_layer", "topkv_unpack_state_layer"]
 
 TOPKV_LAYOUT_PACKED = 0
 TOPKV_LAYOUT_POOL = 1
@@ -64,6 +65,11 @@ class topkv_view_t(ctypes.Structure):
                 ("bt_stride", ctypes.c_int32), ("block_tables", ctypes.c_void_p), ("pool", topkv_pool_t),
                 ("data", ctypes.c_void_p), ("bytes", ctypes.c_int64), ("shards", ctypes.c_int32),
                 ("reserved", ctypes.c_int32)]
+
+
+class topkv_state_pool_t(ctypes.Structure):
+    _fields_ = [("base", ctypes.c_void_p), ("num_slots", ctypes.c_int64), ("state_bytes", ctypes.c_int64),
+                ("num_layers", ctypes.c_int32), ("reserved", ctypes.c_int32)]
 
 
 class topkv_launch_t(ctypes.Structure):
@@ -109,6 +115,11 @@ _SIGS = {
     "topkv_reblock_layer": (_I32, [_POOL, _I32, _P, _I32, _POOL, _I32, _P, _I32, _I32, _P, _P]),
     "topkv_pack_layer_shards": (_I32, [_POOL, _I32, _I32, _P, _I32, _P, _I32, _I32, _I32, _P, _I64, _P]),
     "topkv_unpack_layer_shards": (_I32, [_P, _I64, _I32, _POOL, _I32, _I32, _P, _I32, _P, _I32, _I32, _P]),
+    "topkv_packed_state_bytes": (_I64, [ctypes.POINTER(topkv_state_pool_t), _I32]),
+    "topkv_pack_state_layer": (_I32, [ctypes.POINTER(topkv_state_pool_t), _I32, _I32, _P, _P, _I64,
+                                      ctypes.POINTER(topkv_launch_t)]),
+    "topkv_unpack_state_layer": (_I32, [_P, _I64, ctypes.POINTER(topkv_state_pool_t), _I32, _I32, _P,
+                                        ctypes.POINTER(topkv_launch_t)]),
     "topkv_dma_create": (_I32, [ctypes.POINTER(_P)]),
     "topkv_dma_submit": (_I32, [_P, _P, _P, _P, _I64, ctypes.POINTER(_I64)]),
     "topkv_dma_wait": (_I32, [_P, _I64]),
@@ -183,6 +194,18 @@ def pool_from_tensor(t: torch.Tensor) -> topkv_pool_t:
     L, NP, C, P, H, D = t.shape
     return make_pool(t, num_pages=NP, num_layers=L, page_size=P, planes=C, num_heads=H,
                      head_dim=D, elem_bytes=t.element_size())
+
+
+def state_pool_from_tensor(t: torch.Tensor) -> topkv_state_pool_t:
+    """Descriptor of a state cache tensor [layers][slots][words of one state]."""
+    if t.dim() != 3:
+        raise ValueError("state cache tensor must be [layers][slots][words]")
+    L, NS, E = t.shape
+    return topkv_state_pool_t(_ptr(t), int(NS), int(E) * t.element_size(), int(L), 0)
+
+
+def _state_arg(pool) -> topkv_state_pool_t:
+    return pool if isinstance(pool, topkv_state_pool_t) else state_pool_from_tensor(pool)
 
 
 def _pool_arg(pool) -> topkv_pool_t:
@@ -586,3 +609,42 @@ def prepare_pack_layer_shards(src, layer, num_reqs, block_tables, bt_stride, seq
             _I32(int(bt_stride)), _P(_table_ptr(seq_lens)), _I32(int(head_begin)), _I32(int(head_count)),
             _I32(int(shards)), _P(_ptr(dst)), _I64(int(shard_bytes)), _P(_stream(stream)))
     return PreparedCall("topkv_pack_layer_shards", args, (pool,))
+
+
+# --- fixed-state layers ---------------------------------------------------------
+
+def topkv_packed_state_bytes(pool, num_reqs) -> int:
+    n = _lib.topkv_packed_state_bytes(ctypes.byref(_state_arg(pool)), int(num_reqs))
+    if n < 0:
+        raise TopkvError(TOPKV_ERR_INVALID_ARG)
+    return n
+
+
+def prepare_pack_state_layer(src, layer, num_reqs, slots, dst, dst_bytes=None, stream=None, start=None,
+                             stop=None) -> PreparedCall:
+    pool = _state_arg(src)
+    launch = topkv_launch_t(_stream(stream), _event(start), _event(stop))
+    args = (ctypes.byref(pool), _I32(int(layer)), _I32(int(num_reqs)), _P(_table_ptr(slots)), _P(_ptr(dst)),
+            _I64(_nbytes(dst, dst_bytes)), ctypes.byref(launch))
+    return PreparedCall("topkv_pack_state_layer", args, (pool, launch))
+
+
+def prepare_unpack_state_layer(src, dst, layer, num_reqs, slots, src_bytes=None, stream=None, start=None,
+                               stop=None) -> PreparedCall:
+    pool = _state_arg(dst)
+    launch = topkv_launch_t(_stream(stream), _event(start), _event(stop))
+    args = (_P(_ptr(src)), _I64(_nbytes(src, src_bytes)), ctypes.byref(pool), _I32(int(layer)),
+            _I32(int(num_reqs)), _P(_table_ptr(slots)), ctypes.byref(launch))
+    return PreparedCall("topkv_unpack_state_layer", args, (pool, launch))
+
+
+def topkv_pack_state_layer(src, layer, num_reqs, slots, dst, dst_bytes=None, stream=None, start=None,
+                           stop=None) -> None:
+    """Pack the fixed states of num_reqs requests (slot slots[r]) of one layer."""
+    prepare_pack_state_layer(src, layer, num_reqs, slots, dst, dst_bytes, stream, start, stop)()
+
+
+def topkv_unpack_state_layer(src, dst, layer, num_reqs, slots, src_bytes=None, stream=None, start=None,
+                             stop=None) -> None:
+    """Unpack num_reqs packed states into slots slots[r] of one layer."""
+    prepare_unpack_state_layer(src, dst, layer, num_reqs, slots, src_bytes, stream, start, stop)()

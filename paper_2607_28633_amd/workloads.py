@@ -65,9 +65,38 @@ class Workload:
     block_tables: np.ndarray       # int32 [R, max_pages_src]
     dst_block_tables: np.ndarray   # int32 [R, max_pages_dst]
     layer_windows: tuple = ()      # per logical layer: 0 = full attention, W > 0 = last-W-token window
+    # Fixed-state (linear-attention) layers, Section 2.2: per logical layer True = the layer holds a
+    # per-request state of state_bytes in a state cache [state_phys_layers][slots][state_bytes]
+    # instead of paged K/V; request r's state sits in slot state_slots[r] (dst_state_slots[r] on
+    # the receiving side).
+    layer_state: tuple = ()
+    state_bytes: int = 0
+    state_phys_layers: int = 0
+    num_state_slots: int = 0
+    dst_num_state_slots: int = 0
+    state_slots: Optional[np.ndarray] = None       # int32 [R]
+    dst_state_slots: Optional[np.ndarray] = None   # int32 [R]
 
     def window(self, layer: int) -> int:
         return int(self.layer_windows[layer]) if self.layer_windows else 0
+
+    def is_state(self, layer: int) -> bool:
+        return bool(self.layer_state[layer]) if self.layer_state else False
+
+    def kv_slab(self, layer: int) -> int:
+        """Physical K/V layer slab of logical layer `layer` (attention layers
+        are numbered among themselves when the model also has state layers)."""
+        if not self.layer_state:
+            return layer % self.phys_layers
+        return sum(1 for l in range(layer) if not self.layer_state[l]) % self.phys_layers
+
+    def state_slab(self, layer: int) -> int:
+        """State-cache layer of logical layer `layer` (a state layer)."""
+        return sum(1 for l in range(layer) if self.layer_state[l]) % self.state_phys_layers
+
+    def state_shape(self, dst: bool = False) -> tuple:
+        slots = self.dst_num_state_slots if dst else self.num_state_slots
+        return (self.state_phys_layers, slots, self.state_bytes // self.elem_bytes)
 
     @property
     def num_reqs(self) -> int:
@@ -95,6 +124,8 @@ class Workload:
             "dst_pool_pages": self.dst_num_pages, "requests": self.num_reqs,
             "tokens": int(self.seq_lens.astype(np.int64).sum()),
             "windowed_layers": sum(1 for w in self.layer_windows if w),
+            "state_layers": sum(1 for x in self.layer_state if x),
+            "state_bytes": self.state_bytes,
         }
 
 
@@ -135,10 +166,17 @@ WORKLOADS = {
     "reblock-70b": "80 layers, 8 KV heads, head_dim 128, page 16 -> 64, 100 requests lognormal(median 4096, sigma 1) in [256,32768], pools 1.25x pages, 8 physical layer slabs",
     "gpt-oss-120b": "36 layers alternating 128-token sliding window / full attention, 8 KV heads, head_dim 64, page 16, 32 requests lognormal(median 4096, sigma 1) in [512,16384], pools 1.25x pages",
     "llama3-70b-tp8": "one GPU's share of 70B at tensor parallelism 8: 80 layers, 1 KV head, head_dim 128, page 16, one 4096-token request, 4096-page pools",
+    "qwen3.5-397b-hybrid": "60 layers: every fourth full attention (2 KV heads, head_dim 256, page 16), the other 45 linear attention with a 2,170,880-byte state per request, 32 requests lognormal(median 4096, sigma 1) in [512,16384], pools and state slots 1.25x",
 }
 
+# Fixed state of one linear-attention layer of the hybrid shape, per request (bf16 words): the
+# recurrent state of 64 value heads x 128 x 128 plus a 3-step causal-convolution state over
+# 2 x 16 x 128 + 64 x 128 channels.
+HYBRID_STATE_BYTES = 2 * (64 * 128 * 128 + 3 * (2 * 16 * 128 + 64 * 128))
+
 DEFAULT_SEEDS = {"tiny": 0, "llama3-8b": 1, "llama3-70b-batch8": 2, "deepseek-v3-mla": 3,
-                 "reblock-70b": 4, "llama3-70b-4k": 5, "gpt-oss-120b": 6, "llama3-70b-tp8": 7}
+                 "reblock-70b": 4, "llama3-70b-4k": 5, "gpt-oss-120b": 6, "llama3-70b-tp8": 7,
+                 "qwen3.5-397b-hybrid": 8}
 
 
 def make_workload(name: str, seed: Optional[int] = None, *,
@@ -148,7 +186,7 @@ def make_workload(name: str, seed: Optional[int] = None, *,
                   num_pages: Optional[int] = None, dst_num_pages: Optional[int] = None,
                   num_heads: Optional[int] = None, head_dim: Optional[int] = None,
                   planes: Optional[int] = None, elem_bytes: int = 2,
-                  pool_slack: float = 1.25) -> Workload:
+                  pool_slack: float = 1.25, state_bytes: Optional[int] = None) -> Workload:
     """Build a named workload; keyword overrides shrink or reshape it for tests."""
     if name not in WORKLOADS:
         raise KeyError(f"unknown workload {name!r}; known: {sorted(WORKLOADS)}")
@@ -177,6 +215,10 @@ def make_workload(name: str, seed: Optional[int] = None, *,
         shape = dict(L=36, C=2, H=8, D=64, P=16, P2=16)
         lens = _lognormal_lengths(rng, 32, 4096, 1.0, 512, 16384)
         pools = None
+    elif name == "qwen3.5-397b-hybrid":
+        shape = dict(L=60, C=2, H=2, D=256, P=16, P2=16)
+        lens = _lognormal_lengths(rng, 32, 4096, 1.0, 512, 16384)
+        pools = None
     else:  # reblock-70b
         shape = dict(L=80, C=2, H=8, D=128, P=16, P2=64)
         lens = _lognormal_lengths(rng, 100, 4096, 1.0, 256, 32768)
@@ -201,16 +243,34 @@ def make_workload(name: str, seed: Optional[int] = None, *,
         np_src = int(num_pages)
     if dst_num_pages is not None:
         np_dst = int(dst_num_pages)
+    hybrid = name == "qwen3.5-397b-hybrid"
+    state = tuple(l % 4 != 3 for l in range(L)) if hybrid else ()
     if phys_layers is None:
-        phys_layers = min(L, 8) if name == "reblock-70b" else L
+        if name == "reblock-70b":
+            phys_layers = min(L, 8)
+        elif hybrid:
+            phys_layers = max(1, sum(1 for x in state if not x))
+        else:
+            phys_layers = L
 
     bt = _tables(rng, lens, P, np_src)
     bt2 = _tables(rng, lens, P2, np_dst)
     windows = tuple(128 if l % 2 == 0 else 0 for l in range(L)) if name == "gpt-oss-120b" else ()
+    extra = {}
+    if hybrid:
+        R = len(lens)
+        ns = max(1, math.ceil(pool_slack * R))
+        sb = HYBRID_STATE_BYTES if state_bytes is None else int(state_bytes)
+        if sb % int(elem_bytes):
+            raise ValueError("state_bytes must be a whole number of elements")
+        extra = dict(layer_state=state, state_bytes=sb, state_phys_layers=max(1, sum(state)),
+                     num_state_slots=ns, dst_num_state_slots=ns,
+                     state_slots=rng.permutation(ns)[:R].astype(np.int32),
+                     dst_state_slots=rng.permutation(ns)[:R].astype(np.int32))
     return Workload(name=name, seed=seed, num_layers=L, phys_layers=int(phys_layers),
                     planes=C, num_heads=H, head_dim=D, elem_bytes=int(elem_bytes),
                     page_size=P, num_pages=np_src, dst_page_size=P2, dst_num_pages=np_dst,
-                    seq_lens=lens, block_tables=bt, dst_block_tables=bt2, layer_windows=windows)
+                    seq_lens=lens, block_tables=bt, dst_block_tables=bt2, layer_windows=windows, **extra)
 
 
 def bf16_bits_from_f32(x: np.ndarray) -> np.ndarray:
@@ -273,3 +333,31 @@ def device_dst_prefill(wl: Workload, device="cuda"):
     for layer in range(t.shape[0]):
         t[layer].random_(-32768, 32768, generator=g)
     return t.view(torch.bfloat16)
+
+
+def host_state_cache(wl: Workload, dst: bool = False) -> np.ndarray:
+    """State cache contents on the host, shape ``wl.state_shape(dst)``: the
+    source holds bf16 ~ N(0, 1) (2-byte elements, else random words), the
+    destination a distinct pre-fill of arbitrary words."""
+    rng = np.random.default_rng([wl.seed, 4 if dst else 3])
+    shape = wl.state_shape(dst)
+    if wl.elem_bytes == 2 and not dst:
+        return bf16_bits_from_f32(rng.standard_normal(shape, dtype=np.float32))
+    return random_words(rng, shape, wl.elem_bytes)
+
+
+def device_state_cache(wl: Workload, dst: bool = False, device="cuda"):
+    """State cache generated on the device (bf16 ~ N(0, 1) for the source,
+    arbitrary 16-bit words for the destination pre-fill), one layer at a time."""
+    import torch
+    if wl.elem_bytes != 2:
+        raise ValueError("device generation is for bf16 caches")
+    g = torch.Generator(device=device)
+    g.manual_seed(wl.seed * 1000003 + (4 if dst else 3))
+    t = torch.empty(wl.state_shape(dst), device=device, dtype=torch.int16)
+    for layer in range(t.shape[0]):
+        if dst:
+            t[layer].random_(-32768, 32768, generator=g)
+        else:
+            t[layer].view(torch.bfloat16).normal_(generator=g)
+    return t

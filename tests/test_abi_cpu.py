@@ -167,3 +167,37 @@ def test_move_layer_validation(tk):
     _expect(tk, INV, tk.topkv_pack_layer_shards, good, 1, 2, bt, 4, lens, 0, 8, 0, buf, shard_bytes=1 << 20)
     _expect(tk, INV, tk.topkv_unpack_layer_shards, buf, good, 1, 2, bt, 4, lens, 0, 6, 4, shard_bytes=1 << 20)
     tk.topkv_move_layer(pv, pk, 0, 0, 8, stream=0)                             # no requests: nothing to launch
+
+
+def test_state_layer_validation(tk):
+    """Fixed-state layers: sizes on the host, bad descriptors and arguments
+    refused before any launch, an empty batch launches nothing."""
+    INV, UNS = tk.TOPKV_ERR_INVALID_ARG, tk.TOPKV_ERR_UNSUPPORTED
+    slots, buf = 0x20000, 0x40000
+
+    def st(**kw):
+        g = dict(base=0x10000, num_slots=5, state_bytes=1000, num_layers=3, reserved=0)
+        g.update(kw)
+        return tk.topkv_state_pool_t(g["base"], g["num_slots"], g["state_bytes"], g["num_layers"], g["reserved"])
+
+    lib = tk._lib
+    assert tk.topkv_packed_state_bytes(st(), 7) == 7000
+    assert tk.topkv_packed_state_bytes(st(), 0) == 0
+    for bad in (st(base=0), st(num_slots=0), st(state_bytes=0), st(num_layers=0), st(reserved=1),
+                st(num_slots=1 << 40, state_bytes=1 << 30)):
+        assert lib.topkv_packed_state_bytes(ctypes.byref(bad), 1) == -1
+    assert lib.topkv_packed_state_bytes(ctypes.byref(st()), -1) == -1
+    good = st()
+    _expect(tk, INV, tk.topkv_pack_state_layer, good, 3, 2, slots, buf, dst_bytes=1 << 20)     # layer >= L
+    _expect(tk, INV, tk.topkv_pack_state_layer, good, -1, 2, slots, buf, dst_bytes=1 << 20)
+    _expect(tk, INV, tk.topkv_pack_state_layer, good, 0, -1, slots, buf, dst_bytes=1 << 20)
+    _expect(tk, INV, tk.topkv_pack_state_layer, good, 0, 2, 0, buf, dst_bytes=1 << 20)         # null slots
+    _expect(tk, INV, tk.topkv_pack_state_layer, good, 0, 2, slots, 0, dst_bytes=1 << 20)       # null dst
+    _expect(tk, INV, tk.topkv_pack_state_layer, good, 0, 2, slots, buf, dst_bytes=1999)        # one byte short
+    _expect(tk, INV, tk.topkv_pack_state_layer, st(reserved=3), 0, 2, slots, buf, dst_bytes=1 << 20)
+    _expect(tk, INV, tk.topkv_unpack_state_layer, buf, good, 1, 3, slots, src_bytes=2999)
+    _expect(tk, INV, tk.topkv_unpack_state_layer, 0, good, 1, 3, slots, src_bytes=3000)
+    huge = st(num_slots=1, num_layers=1, state_bytes=1 << 50)
+    _expect(tk, UNS, tk.topkv_pack_state_layer, huge, 0, 1, slots, buf, dst_bytes=1 << 50)    # 2^35 tiles
+    tk.topkv_pack_state_layer(good, 2, 0, 0, 0, dst_bytes=0, stream=0)      # no requests: nothing to launch
+    tk.topkv_unpack_state_layer(0, good, 0, 0, 0, src_bytes=0, stream=0)

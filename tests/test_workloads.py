@@ -58,3 +58,28 @@ def test_bf16_rounding_and_values():
     pool = host_src_pool(make_workload("tiny"))
     f = (pool.astype(np.uint32) << 16).view(np.float32)
     assert abs(f.mean()) < 0.02 and 0.97 < f.std() < 1.03
+
+
+def test_hybrid_layer_kinds_and_slots():
+    """The hybrid workload: attention on every fourth layer, fixed-state layers
+    elsewhere, each kind numbered among itself for its slabs, distinct slots on
+    both sides, the state size of the stated shape, deterministic."""
+    from paper_2607_28633_amd.workloads import HYBRID_STATE_BYTES, host_state_cache
+    wl = make_workload("qwen3.5-397b-hybrid")
+    assert wl.num_layers == 60 and sum(wl.layer_state) == 45
+    assert [l for l in range(60) if not wl.is_state(l)] == list(range(3, 60, 4))
+    assert (wl.planes, wl.num_heads, wl.head_dim) == (2, 2, 256)
+    assert HYBRID_STATE_BYTES == 2 * (64 * 128 * 128 + 3 * (2 * 16 * 128 + 64 * 128)) == wl.state_bytes
+    assert [wl.kv_slab(l) for l in range(3, 60, 4)] == list(range(15)) and wl.phys_layers == 15
+    assert [wl.state_slab(l) for l in range(60) if wl.is_state(l)] == list(range(45))
+    for slots, NS in ((wl.state_slots, wl.num_state_slots), (wl.dst_state_slots, wl.dst_num_state_slots)):
+        assert slots.dtype == np.int32 and slots.size == wl.num_reqs == 32
+        assert len(set(slots.tolist())) == slots.size and slots.min() >= 0 and slots.max() < NS == 40
+    again = make_workload("qwen3.5-397b-hybrid")
+    assert np.array_equal(again.state_slots, wl.state_slots) and np.array_equal(again.seq_lens, wl.seq_lens)
+    small = make_workload("qwen3.5-397b-hybrid", num_layers=8, seq_lens=[5, 9], state_bytes=64)
+    a, b = host_state_cache(small), host_state_cache(small)
+    assert a.shape == (6, 3, 32) and np.array_equal(a, b)
+    assert not np.array_equal(host_state_cache(small, dst=True), a)
+    with pytest.raises(ValueError):
+        make_workload("qwen3.5-397b-hybrid", state_bytes=7)
