@@ -59,3 +59,57 @@ def test_fullsize(tk, name):
     torch.cuda.synchronize()
     del src, dst, packed, again
     torch.cuda.empty_cache()
+
+
+def test_fullsize_hybrid(tk):
+    """The hybrid model at full size (60 layers, 45 fixed-state, 32 requests):
+    every layer round-trips through the destination side with the call its
+    kind takes; the first and last layer of each kind is compared with the
+    oracle in full."""
+    import oracle.state as so
+    from paper_2607_28633_amd.workloads import device_state_cache
+    wl = make_workload("qwen3.5-397b-hybrid")
+    say(f"[fullsize] hybrid: {wl.describe()}")
+    src, dst = device_src_pool(wl), device_dst_prefill(wl)
+    st_src, st_dst = device_state_cache(wl), device_state_cache(wl, dst=True)
+    bt, bt2, lens = to_dev(wl.block_tables), to_dev(wl.dst_block_tables), to_dev(wl.seq_lens)
+    s1, s2 = to_dev(wl.state_slots), to_dev(wl.dst_state_slots)
+    R = wl.num_reqs
+    kv_bytes = tk.topkv_packed_layer_bytes(src, wl.seq_lens)
+    st_bytes = tk.topkv_packed_state_bytes(st_src, R)
+    packed = torch.empty(max(kv_bytes, st_bytes) // 2, dtype=torch.int16, device="cuda")
+    again = torch.empty_like(packed)
+    state_layers = [l for l in range(wl.num_layers) if wl.is_state(l)]
+    attn_layers = [l for l in range(wl.num_layers) if not wl.is_state(l)]
+    sample = {state_layers[0], state_layers[-1], attn_layers[0], attn_layers[-1]}
+    for layer in range(wl.num_layers):
+        if wl.is_state(layer):
+            slab, n, cache_s, cache_d = wl.state_slab(layer), st_bytes // 2, st_src, st_dst
+        else:
+            slab, n, cache_s, cache_d = wl.kv_slab(layer), kv_bytes // 2, src, dst
+        if layer in sample:
+            torch.cuda.synchronize()
+            src_h = to_host(cache_s[slab])[None]
+            dst_before = to_host(cache_d[slab])[None]
+        if wl.is_state(layer):
+            tk.topkv_pack_state_layer(st_src, slab, R, s1, packed, dst_bytes=st_bytes)
+            tk.topkv_unpack_state_layer(packed, st_dst, slab, R, s2, src_bytes=st_bytes)
+            tk.topkv_pack_state_layer(st_dst, slab, R, s2, again, dst_bytes=st_bytes)
+        else:
+            tk.topkv_pack_layer_batched(src, slab, R, bt, bt.shape[1], lens, packed, dst_bytes=kv_bytes)
+            tk.topkv_unpack_layer_batched(packed, dst, slab, R, bt2, bt2.shape[1], lens, src_bytes=kv_bytes)
+            tk.topkv_pack_layer_batched(dst, slab, R, bt2, bt2.shape[1], lens, again, dst_bytes=kv_bytes)
+        assert torch.equal(packed[:n], again[:n]), f"hybrid layer {layer}: round trip differs"
+        if layer in sample:
+            if wl.is_state(layer):
+                want = so.pack_state_layer(src_h, 0, wl.state_slots)
+                so.unpack_state_layer(want, dst_before, 0, wl.dst_state_slots)
+            else:
+                want = oracle.pack_layer(src_h, 0, wl.block_tables, wl.seq_lens)
+                oracle.unpack_layer(want, dst_before, 0, wl.dst_block_tables, wl.seq_lens)
+            assert np.array_equal(to_host(packed[:n]), want), f"hybrid layer {layer}: pack differs from oracle"
+            assert np.array_equal(to_host(cache_d[slab]), dst_before[0]), \
+                f"hybrid layer {layer}: unpacked slab differs from oracle"
+            say(f"  layer {layer} ({'state' if wl.is_state(layer) else 'attention'}, slab {slab}) bit-exact vs oracle")
+            del src_h, dst_before, want
+    torch.cuda.synchronize()
