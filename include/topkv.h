@@ -265,7 +265,8 @@ topkv_status_t topkv_kvcache1_unpack_layer(const void* blob, int64_t blob_bytes,
 
 /* CRC-64/XZ (as above) of nbytes of device memory at data (16-byte aligned,
  * any length), written to the device word *crc_out on the stream.
- * workspace: topkv_crc64_workspace_bytes(nbytes) bytes, caller-owned. */
+ * workspace: topkv_crc64_workspace_bytes(nbytes) bytes of device memory,
+ * 8-byte aligned, caller-owned. */
 topkv_status_t topkv_crc64(const void* data, int64_t nbytes, void* workspace,
                            int64_t workspace_bytes, uint64_t* crc_out, hipStream_t stream);
 int64_t topkv_crc64_workspace_bytes(int64_t nbytes);

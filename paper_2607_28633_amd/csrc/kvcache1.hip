@@ -14,19 +14,24 @@
 // register by x^8 mod P.  Hence, for the raw register R (preset 0, no final
 // complement), R(A || B) = R(A) * x^(8|B|) + R(B) over GF(2), leading zero
 // bytes leave R unchanged, and the CRC proper is
-// ~(~0 * x^(8N) + R(data)).  Work split:
-//   kernel 0: byte tables into the caller's workspace (slicing-by-8, and
-//     multiply-by-constant tables for the two fixed shifts below);
-//   kernel 1: each workgroup owns a 256 KiB chunk = 16 sub-chunks of 16 KiB;
-//     lane t takes bytes [64t, 64t + 64) of every sub-chunk (adjacent loads),
-//     runs them through the slicing tables (in LDS), advances its running
-//     register by one sub-chunk per step with a table multiply, and a tree
-//     of shift-and-add steps joins the lanes.  The data is front-padded with
-//     zero bytes to whole chunks (free, by the property above);
-//   kernel 2: one workgroup folds the chunk values (each lane a run of 2^q
-//     chunks, then a tree), appends the sub-16-byte tail and applies the
-//     preset and complement.
-// Shift constants x^(8 * 2^k) mod P are computed once on the host.
+// ~(~0 * x^(8N) + R(data)).  Multiplying a register by a fixed power of x is
+// linear, so it is the XOR of one lookup per register byte in a table of
+// that constant.  Work split:
+//   kernel 0: the tables, into the caller's workspace: slicing tables, the
+//     constant that advances a register by one sub-chunk, the join levels of
+//     the lanes inside a span and of the spans;
+//   kernel 1: the data, front-padded with zero bytes (free, by the property
+//     above), is cut into at most 256 equal spans of whole 64 KiB
+//     sub-chunks, one 1024-lane workgroup per span.  Lane t takes bytes
+//     [64t, 64t + 64) of every sub-chunk (adjacent loads, the next
+//     sub-chunk's in flight while this one is folded), runs them through
+//     slicing-by-4 tables held in LDS in 16 replicas (lane t reads replica
+//     t mod 16, which spreads a wave's random lookups over the LDS banks),
+//     and advances its running register by one sub-chunk per step; a tree of
+//     table multiplies joins the lanes at the end of the span;
+//   kernel 2: one workgroup joins the span registers the same way, appends
+//     the sub-16-byte tail and applies the preset and complement.
+// Shift constants x^(8n) mod P are computed on the host.
 #include <hip/hip_runtime.h>
 
 #include <cstdint>
@@ -37,18 +42,27 @@
 namespace {
 
 constexpr uint64_t kPolyReflected = 0xC96C5795D7870F42ull;   // ECMA-182, bit-reversed
-constexpr int kCrcThreads = 256;
+constexpr int kCrcThreads = 1024;                               // lanes per span workgroup
 constexpr int kPiece = 64;                                      // bytes per lane per sub-chunk
-constexpr int kSubLog2 = 14;                                    // 16 KiB sub-chunk = 256 lanes x 64 B
-constexpr int kSubs = 16;                                       // sub-chunks per workgroup
-constexpr int kChunkLog2 = 18;                                  // 256 KiB per workgroup
-constexpr int64_t kChunk = (int64_t)1 << kChunkLog2;
-constexpr int kTableWords = 8 * 256;                            // one set of 8 byte tables
-// workspace: [slicing tables][x^(8*16K) tables][x^(8*256K) tables][chunk registers...]
-constexpr int64_t kWsTables = 3 * kTableWords;
+constexpr int kLoads = kPiece / 16;                             // 16-byte loads per lane per sub-chunk
+constexpr int kSubLog2 = 16;                                    // 64 KiB sub-chunk = 1024 lanes x 64 B
+constexpr int64_t kSub = (int64_t)1 << kSubLog2;
+constexpr int kMaxSpans = 256;                                  // span workgroups per CRC at most
+constexpr int kLaneLevels = 10;                                 // log2(kCrcThreads)
+constexpr int kSpanLevels = 8;                                  // log2(kMaxSpans)
+constexpr int kTableWords = 8 * 256;                            // one set of 8 byte tables (16 KiB)
+constexpr int kCopies = 16;                                     // LDS replicas of the slicing tables
+// workspace table sets: 0 slicing, 1 sub-chunk advance, 2.. lane levels, then span levels
+constexpr int kSetSlice = 0, kSetSub = 1, kSetLane = 2, kSetSpan = kSetLane + kLaneLevels;
+constexpr int kSets = kSetSpan + kSpanLevels;
+constexpr int64_t kWsTables = (int64_t)kSets * kTableWords;     // then the span registers
 
 struct ShiftConsts {
   uint64_t x8pow2[64];    // x^(8 * 2^k) mod P, reflected
+};
+
+struct TableConsts {
+  uint64_t shift[kSets];  // the constant of each multiply set (unused for the slicing set)
 };
 
 __host__ __device__ inline uint64_t mul_x(uint64_t w) { return (w >> 1) ^ ((w & 1) ? kPolyReflected : 0); }
@@ -84,22 +98,18 @@ uint64_t x8n(const ShiftConsts& c, uint64_t n) {
   return r;
 }
 
-// Kernel 0: the byte tables every other kernel copies into LDS.
-//   [0, 2048):     slicing-by-8, t[k][b] = byte b followed by k zero bytes
-//   [2048, 4096):  b << 8k times x^(8 * 16 KiB)   (advance one sub-chunk)
-//   [4096, 6144):  b << 8k times x^(8 * 256 KiB)  (advance one chunk)
-// Multiplying a register by a constant is linear, so it is the XOR of one
-// lookup per register byte in such a table.
-__global__ __launch_bounds__(256) void crc64_tables_kernel(uint64_t* __restrict__ tables, uint64_t sub_shift,
-                                                           uint64_t chunk_shift) {
-  const int g = blockIdx.x * 256 + threadIdx.x;              // grid covers exactly 3 * 2048 entries
+// Kernel 0: table set g / 2048, table k, byte b:
+//   slicing set: byte b followed by k zero bytes;
+//   multiply sets: (b << 8k) times the set's constant.
+__global__ __launch_bounds__(256) void crc64_tables_kernel(uint64_t* __restrict__ tables, TableConsts tc) {
+  const int g = blockIdx.x * 256 + threadIdx.x;              // grid covers exactly kSets * 2048 entries
   const int set = g / kTableWords, k = (g / 256) % 8, b = g % 256;
   uint64_t v;
-  if (set == 0) {
+  if (set == kSetSlice) {
     v = (uint64_t)b;
     for (int i = 0; i < 8 * (k + 1); ++i) v = mul_x(v);
   } else {
-    v = mulmod((uint64_t)b << (8 * k), set == 1 ? sub_shift : chunk_shift);
+    v = mulmod((uint64_t)b << (8 * k), tc.shift[set]);
   }
   tables[g] = v;
 }
@@ -110,148 +120,173 @@ __device__ inline uint64_t lookup8(uint64_t v, const uint64_t* t) {   // t: 8 x 
          t[6 * 256 + ((v >> 48) & 0xff)] ^ t[7 * 256 + (v >> 56)];
 }
 
-// Eight bytes (little-endian word w) into the register: with the slicing
-// tables, byte 0 is followed by 7 more bytes, byte 7 by none.
-__device__ inline uint64_t crc_word(uint64_t reg, uint64_t w, const uint64_t* t) {
+// Four bytes (little-endian word w) into the register with slicing-by-4
+// tables in replicated layout: entry (k, b) of this lane's replica is
+// tc[(k * 256 + b) * kCopies]; byte 0 is followed by 3 more bytes, byte 3 by
+// none.
+__device__ inline uint64_t crc_word4(uint64_t reg, uint32_t w, const uint64_t* tc) {
   reg ^= w;
-  return t[7 * 256 + (reg & 0xff)] ^ t[6 * 256 + ((reg >> 8) & 0xff)] ^ t[5 * 256 + ((reg >> 16) & 0xff)] ^
-         t[4 * 256 + ((reg >> 24) & 0xff)] ^ t[3 * 256 + ((reg >> 32) & 0xff)] ^
-         t[2 * 256 + ((reg >> 40) & 0xff)] ^ t[1 * 256 + ((reg >> 48) & 0xff)] ^ t[0 * 256 + (reg >> 56)];
-}
-
-__device__ inline void copy_words(uint64_t* lds, const uint64_t* __restrict__ src, int words) {
-  for (int i = threadIdx.x; i < words; i += blockDim.x) lds[i] = src[i];
+  return tc[(3 * 256 + (reg & 0xff)) * kCopies] ^ tc[(2 * 256 + ((reg >> 8) & 0xff)) * kCopies] ^
+         tc[(1 * 256 + ((reg >> 16) & 0xff)) * kCopies] ^ tc[((reg >> 24) & 0xff) * kCopies] ^ (reg >> 32);
 }
 
 typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
 
-// Kernel 1: raw register of each 256 KiB chunk of the front-padded stream.
-// data: 16-byte aligned, `head` bytes (a multiple of 16); `pad` leading zero
-// bytes (a multiple of 16) make head + pad a whole number of chunks.  Lane t
-// owns bytes [t*64, t*64 + 64) of each 16 KiB sub-chunk (four adjacent
-// 16-byte loads, so every line is used at once), folds its pieces across the
-// 16 sub-chunks (advance by 16 KiB = one table multiply), and a tree of
-// shift-and-add steps joins the 256 lanes.
-__global__ __launch_bounds__(kCrcThreads) void crc64_chunks_kernel(const u32x4* __restrict__ data, int64_t head,
-                                                                   int64_t pad, const uint64_t* __restrict__ tables,
-                                                                   uint64_t* __restrict__ partial, ShiftConsts sc) {
-  __shared__ uint64_t t_slice[kTableWords];
+// Copy `words` words (a multiple of nthreads * kBatch) from global memory
+// into LDS with kBatch loads in flight per thread before their stores.
+template <int kBatch>
+__device__ inline void stage(uint64_t* lds, const uint64_t* __restrict__ src, int words, int nthreads) {
+  for (int base = 0; base < words; base += nthreads * kBatch) {
+    uint64_t v[kBatch];
+#pragma unroll
+    for (int j = 0; j < kBatch; ++j) v[j] = src[base + j * nthreads + threadIdx.x];
+#pragma unroll
+    for (int j = 0; j < kBatch; ++j) lds[base + j * nthreads + threadIdx.x] = v[j];
+  }
+}
+
+// Kernel 1: raw register of each span of the front-padded stream.  data:
+// 16-byte aligned, `head` bytes (a multiple of 16); `pad` leading zero bytes
+// (a multiple of 16) make head + pad = gridDim.x spans of span_subs
+// sub-chunks.
+__global__ __launch_bounds__(kCrcThreads) void crc64_span_kernel(const u32x4* __restrict__ data, int64_t pad,
+                                                                 int64_t span_subs,
+                                                                 const uint64_t* __restrict__ tables,
+                                                                 uint64_t* __restrict__ partial) {
+  __shared__ uint64_t t_slice[4 * 256 * kCopies];   // tables 0..3, kCopies replicas (128 KiB)
   __shared__ uint64_t t_sub[kTableWords];
   __shared__ uint64_t acc[kCrcThreads];
-  copy_words(t_slice, tables, kTableWords);
-  copy_words(t_sub, tables + kTableWords, kTableWords);
-  __syncthreads();
-  const int64_t base = (int64_t)blockIdx.x * kChunk + (int64_t)threadIdx.x * kPiece - pad;   // data offset
-  u32x4 cur[4], nxt[4];
-  auto load = [&](u32x4 (&v)[4], int sub) {
+  {
+    // thread e writes entry e = (k, b) of tables 0..3 into all kCopies replicas
+    static_assert(4 * 256 == kCrcThreads, "one slicing entry per thread");
+    const uint64_t v = tables[kSetSlice * kTableWords + threadIdx.x];
 #pragma unroll
-    for (int j = 0; j < 4; ++j) {
-      const int64_t off = base + ((int64_t)sub << kSubLog2) + 16 * j;
+    for (int c = 0; c < kCopies; ++c) t_slice[threadIdx.x * kCopies + c] = v;
+    stage<2>(t_sub, tables + kSetSub * kTableWords, kTableWords, kCrcThreads);
+  }
+  __syncthreads();
+  const uint64_t* tc = t_slice + (threadIdx.x % kCopies);
+  const int64_t base = (int64_t)blockIdx.x * span_subs * kSub + (int64_t)threadIdx.x * kPiece - pad;  // data offset
+  u32x4 cur[kLoads], nxt[kLoads];
+  auto load = [&](u32x4 (&v)[kLoads], int64_t sub) {
+#pragma unroll
+    for (int j = 0; j < kLoads; ++j) {
+      const int64_t off = base + (sub << kSubLog2) + 16 * j;
       v[j] = off >= 0 ? __builtin_nontemporal_load(data + off / 16) : u32x4{0u, 0u, 0u, 0u};   // off < head
     }
   };
   load(cur, 0);
   uint64_t fold = 0;
-#pragma unroll 2
-  for (int sub = 0; sub < kSubs; ++sub) {
-    if (sub + 1 < kSubs) load(nxt, sub + 1);
+  for (int64_t sub = 0; sub < span_subs; ++sub) {
+    if (sub + 1 < span_subs) load(nxt, sub + 1);
     uint64_t reg = 0;
 #pragma unroll
-    for (int j = 0; j < 4; ++j) {
-      reg = crc_word(reg, ((uint64_t)cur[j].y << 32) | cur[j].x, t_slice);
-      reg = crc_word(reg, ((uint64_t)cur[j].w << 32) | cur[j].z, t_slice);
+    for (int j = 0; j < kLoads; ++j) {
+      reg = crc_word4(reg, cur[j].x, tc);
+      reg = crc_word4(reg, cur[j].y, tc);
+      reg = crc_word4(reg, cur[j].z, tc);
+      reg = crc_word4(reg, cur[j].w, tc);
     }
     fold = lookup8(fold, t_sub) ^ reg;
 #pragma unroll
-    for (int j = 0; j < 4; ++j) cur[j] = nxt[j];
+    for (int j = 0; j < kLoads; ++j) cur[j] = nxt[j];
   }
   acc[threadIdx.x] = fold;
+  __syncthreads();   // every lane is done with the slicing tables: their LDS holds the join levels now
+  uint64_t* lvl_tab = t_slice;                                   // levels 0..7 (8 x 16 KiB)
+  stage<16>(lvl_tab, tables + kSetLane * kTableWords, 8 * kTableWords, kCrcThreads);
+  stage<2>(t_sub, tables + (kSetLane + 8) * kTableWords, kTableWords, kCrcThreads);   // level 8
   __syncthreads();
-  // join lanes t and t + s: the later group holds s lanes x 64 bytes of every sub-chunk
-  for (int lvl = 0; lvl < 8; ++lvl) {
+  // join lanes t and t + s: the later group holds s lanes x kPiece bytes of every sub-chunk
+  for (int lvl = 0; lvl < kLaneLevels; ++lvl) {
     const int s = 1 << lvl;
     const int t = threadIdx.x;
-    if ((t & (2 * s - 1)) == 0) acc[t] = mulmod(sc.x8pow2[6 + lvl], acc[t]) ^ acc[t + s];
+    if ((t & (2 * s - 1)) == 0) {
+      const uint64_t* tab = lvl < 8 ? lvl_tab + lvl * kTableWords
+                                    : lvl == 8 ? t_sub : tables + (kSetLane + lvl) * kTableWords;
+      acc[t] = lookup8(acc[t], tab) ^ acc[t + s];
+    }
     __syncthreads();
   }
   if (threadIdx.x == 0) partial[blockIdx.x] = acc[0];
 }
 
-// Kernel 2 (one workgroup): fold `chunks` chunk registers, each lane a run of
-// 2^run_log2 of them (front-padded with zero registers; advancing one chunk is
-// one table multiply), join the lanes, append the tail bytes and finish:
-// out = ~(preset_shift + R).
-__global__ __launch_bounds__(kCrcThreads) void crc64_finish_kernel(const uint64_t* __restrict__ tables,
-                                                                   const uint64_t* __restrict__ partial,
-                                                                   int64_t chunks, int run_log2,
-                                                                   const unsigned char* __restrict__ tail,
-                                                                   int tail_len, uint64_t preset_shift,
-                                                                   uint64_t* __restrict__ out, ShiftConsts sc) {
-  __shared__ uint64_t t_chunk[kTableWords];
-  __shared__ uint64_t acc[kCrcThreads];
-  copy_words(t_chunk, tables + 2 * kTableWords, kTableWords);
+// Kernel 2 (one workgroup of kMaxSpans lanes): lane t holds span register
+// t - lead (the first `lead` lanes hold zero spans, i.e. more leading zero
+// bytes), a tree of table multiplies joins them, then the tail bytes are
+// appended and the CRC finished: out = ~(preset_shift + R).
+__global__ __launch_bounds__(kMaxSpans) void crc64_finish_kernel(const uint64_t* __restrict__ tables,
+                                                                 const uint64_t* __restrict__ partial, int spans,
+                                                                 const unsigned char* __restrict__ tail,
+                                                                 int tail_len, uint64_t preset_shift,
+                                                                 uint64_t* __restrict__ out) {
+  __shared__ uint64_t lvl_tab[kSpanLevels * kTableWords];       // 128 KiB
+  __shared__ uint64_t t0[256];
+  __shared__ uint64_t acc[kMaxSpans];
+  const int lead = kMaxSpans - spans;
+  acc[threadIdx.x] = (int)threadIdx.x >= lead ? partial[threadIdx.x - lead] : 0ull;
+  t0[threadIdx.x] = tables[kSetSlice * kTableWords + threadIdx.x];   // slicing table 0 (kMaxSpans == 256)
+  stage<16>(lvl_tab, tables + kSetSpan * kTableWords, kSpanLevels * kTableWords, kMaxSpans);
   __syncthreads();
-  const int64_t run = (int64_t)1 << run_log2;
-  const int64_t lead = (int64_t)kCrcThreads * run - chunks;    // leading zero chunks
-  uint64_t reg = 0;
-  for (int64_t j0 = 0; j0 < run; j0 += 8) {
-    uint64_t vals[8];   // issue the loads of eight chunk registers, then fold them
-#pragma unroll
-    for (int j = 0; j < 8; ++j) {
-      const int64_t v = (int64_t)threadIdx.x * run + j0 + j - lead;
-      vals[j] = (j0 + j < run && v >= 0) ? partial[v] : 0ull;
-    }
-#pragma unroll
-    for (int j = 0; j < 8; ++j)
-      if (j0 + j < run) reg = lookup8(reg, t_chunk) ^ vals[j];
-  }
-  acc[threadIdx.x] = reg;
-  __syncthreads();
-  for (int lvl = 0; lvl < 8; ++lvl) {
+  for (int lvl = 0; lvl < kSpanLevels; ++lvl) {
     const int s = 1 << lvl;
     const int t = threadIdx.x;
-    if ((t & (2 * s - 1)) == 0) acc[t] = mulmod(sc.x8pow2[kChunkLog2 + run_log2 + lvl], acc[t]) ^ acc[t + s];
+    if ((t & (2 * s - 1)) == 0) acc[t] = lookup8(acc[t], lvl_tab + lvl * kTableWords) ^ acc[t + s];
     __syncthreads();
   }
   if (threadIdx.x == 0) {
     uint64_t r = acc[0];
-    for (int b = 0; b < tail_len; ++b) r = tables[(r ^ tail[b]) & 0xff] ^ (r >> 8);   // slicing table 0
+    for (int b = 0; b < tail_len; ++b) r = t0[(r ^ tail[b]) & 0xff] ^ (r >> 8);
     out[0] = ~(preset_shift ^ r);
   }
 }
 
-int64_t crc_chunks(int64_t head) { return (head + kChunk - 1) / kChunk; }
+// Workspace words one CRC needs: tables + span registers.
+int64_t crc_words(int64_t) { return kWsTables + kMaxSpans; }
 
-// Workspace words one CRC of n bytes needs: tables + chunk registers.
-int64_t crc_words(int64_t n) { return kWsTables + crc_chunks(n - n % 16) + 1; }
+// Span geometry of a CRC over n bytes: the 16-byte-aligned head is cut into
+// `spans` spans of `span_subs` sub-chunks each (spans <= kMaxSpans).
+struct Spans {
+  int64_t head, span_subs, span, spans;
+};
 
-// Queue the byte tables into ws (first kWsTables words).
-topkv_status_t crc64_tables(uint64_t* ws, hipStream_t stream) {
+Spans span_geometry(int64_t n) {
+  Spans g;
+  g.head = n - n % 16;
+  const int64_t subs = (g.head + kSub - 1) / kSub;
+  g.span_subs = subs > 0 ? (subs + kMaxSpans - 1) / kMaxSpans : 1;
+  g.span = g.span_subs * kSub;
+  g.spans = (g.head + g.span - 1) / g.span;
+  return g;
+}
+
+// Queue the tables for CRCs whose spans have `span` bytes into ws (first
+// kWsTables words).
+topkv_status_t crc64_tables(uint64_t* ws, int64_t span, hipStream_t stream) {
   const ShiftConsts& sc = shift_consts();
-  hipLaunchKernelGGL(crc64_tables_kernel, dim3((unsigned)(kWsTables / 256)), dim3(256), 0, stream, ws,
-                     sc.x8pow2[kSubLog2], sc.x8pow2[kChunkLog2]);
+  TableConsts tc;
+  tc.shift[kSetSlice] = 0;
+  tc.shift[kSetSub] = sc.x8pow2[kSubLog2];                                     // x^(8 * sub-chunk)
+  for (int l = 0; l < kLaneLevels; ++l) tc.shift[kSetLane + l] = x8n(sc, (uint64_t)kPiece << l);
+  for (int l = 0; l < kSpanLevels; ++l) tc.shift[kSetSpan + l] = x8n(sc, (uint64_t)span << l);
+  hipLaunchKernelGGL(crc64_tables_kernel, dim3((unsigned)(kWsTables / 256)), dim3(256), 0, stream, ws, tc);
   return hipGetLastError() == hipSuccess ? TOPKV_OK : TOPKV_ERR_LAUNCH;
 }
 
 // Queue the CRC-64/XZ of data[0, n) into out (device).  data 16-byte aligned;
-// ws holds the tables (crc64_tables) followed by room for the chunk registers.
+// `tables` were queued by crc64_tables for this n's span; partial has room
+// for kMaxSpans words.
 topkv_status_t crc64_launch(const unsigned char* data, int64_t n, const uint64_t* tables, uint64_t* partial,
                             uint64_t* out, hipStream_t stream) {
   const ShiftConsts& sc = shift_consts();
-  const int64_t head = n - n % 16;
-  const int64_t chunks = crc_chunks(head);
-  const int64_t pad = chunks * kChunk - head;
-  if (chunks > 0) {
-    if (chunks > INT32_MAX) return TOPKV_ERR_UNSUPPORTED;
-    hipLaunchKernelGGL(crc64_chunks_kernel, dim3((unsigned)chunks), dim3(kCrcThreads), 0, stream,
-                       reinterpret_cast<const u32x4*>(data), head, pad, tables, partial, sc);
+  const Spans g = span_geometry(n);
+  if (g.spans > 0) {
+    hipLaunchKernelGGL(crc64_span_kernel, dim3((unsigned)g.spans), dim3(kCrcThreads), 0, stream,
+                       reinterpret_cast<const u32x4*>(data), g.spans * g.span - g.head, g.span_subs, tables, partial);
     if (hipGetLastError() != hipSuccess) return TOPKV_ERR_LAUNCH;
   }
-  int run_log2 = 0;
-  while (((int64_t)kCrcThreads << run_log2) < chunks) ++run_log2;
-  if (kChunkLog2 + run_log2 + 8 > 63) return TOPKV_ERR_UNSUPPORTED;
-  hipLaunchKernelGGL(crc64_finish_kernel, dim3(1), dim3(kCrcThreads), 0, stream, tables, partial, chunks, run_log2,
-                     data + head, (int)(n - head), mulmod(x8n(sc, (uint64_t)n), ~0ull), out, sc);
+  hipLaunchKernelGGL(crc64_finish_kernel, dim3(1), dim3(kMaxSpans), 0, stream, tables, partial, (int)g.spans,
+                     data + g.head, (int)(n - g.head), mulmod(x8n(sc, (uint64_t)n), ~0ull), out);
   return hipGetLastError() == hipSuccess ? TOPKV_OK : TOPKV_ERR_LAUNCH;
 }
 
@@ -347,16 +382,21 @@ HeaderFields fields(const topkv_pool_t* g, int32_t seq_len, uint64_t request_id,
   return f;
 }
 
-// Both checksums of a blob body into ws[0..1]; then the byte tables, then
-// the chunk registers of K and of V.
+// Both checksums of a blob body into ws[0..1]; then the tables, then the
+// span registers of K and of V.
 topkv_status_t blob_crcs(const unsigned char* blob, const Blob& b, uint64_t* ws, hipStream_t stream) {
   uint64_t* tables = ws + 2;
   uint64_t* partial_k = tables + kWsTables;
   uint64_t* partial_v = partial_k + crc_words(b.k_bytes) - kWsTables;
-  topkv_status_t st = crc64_tables(tables, stream);
+  const int64_t span_k = span_geometry(b.k_bytes).span, span_v = span_geometry(b.v_bytes).span;
+  topkv_status_t st = crc64_tables(tables, span_k, stream);
   if (st != TOPKV_OK) return st;
   st = crc64_launch(blob + kHeaderBytes, b.k_bytes, tables, partial_k, ws, stream);
   if (st != TOPKV_OK) return st;
+  if (span_v != span_k) {   // stream order: K's kernels are done with the tables before they change
+    st = crc64_tables(tables, span_v, stream);
+    if (st != TOPKV_OK) return st;
+  }
   return crc64_launch(blob + kHeaderBytes + b.k_bytes, b.v_bytes, tables, partial_v, ws + 1, stream);
 }
 
@@ -381,7 +421,7 @@ topkv_status_t topkv_crc64(const void* data, int64_t nbytes, void* workspace, in
   if (workspace_bytes < topkv_crc64_workspace_bytes(nbytes)) return TOPKV_ERR_INVALID_ARG;
   if (nbytes > 0 && !aligned16(data)) return TOPKV_ERR_UNSUPPORTED;
   uint64_t* ws = static_cast<uint64_t*>(workspace);
-  const topkv_status_t st = crc64_tables(ws, stream);
+  const topkv_status_t st = crc64_tables(ws, span_geometry(nbytes).span, stream);
   if (st != TOPKV_OK) return st;
   return crc64_launch(static_cast<const unsigned char*>(data), nbytes, ws, ws + kWsTables, crc_out, stream);
 }
