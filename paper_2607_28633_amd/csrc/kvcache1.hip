@@ -23,10 +23,12 @@
 //   kernel 1: the data, front-padded with zero bytes (free, by the property
 //     above), is cut into at most 256 equal spans of whole 64 KiB
 //     sub-chunks, one 1024-lane workgroup per span.  Lane t takes bytes
-//     [64t, 64t + 64) of every sub-chunk (adjacent loads, the next
-//     sub-chunk's in flight while this one is folded), runs them through
-//     slicing-by-4 tables held in LDS in 16 replicas (lane t reads replica
-//     t mod 16, which spreads a wave's random lookups over the LDS banks),
+//     [64t, 64t + 64) of every sub-chunk: a wave loads its 4 KiB slice with
+//     fully coalesced 16-byte loads (the next sub-chunk's in flight while
+//     this one is folded) and hands each lane its 64 bytes through an LDS
+//     staging area; lanes run them through slicing-by-4 tables held in LDS
+//     in 8 replicas (lane t reads replica t mod 8, which spreads a wave's
+//     random lookups over the LDS banks),
 //     and advances its running register by one sub-chunk per step; a tree of
 //     table multiplies joins the lanes at the end of the span;
 //   kernel 2: one workgroup joins the span registers the same way, appends
@@ -51,7 +53,9 @@ constexpr int kMaxSpans = 256;                                  // span workgrou
 constexpr int kLaneLevels = 10;                                 // log2(kCrcThreads)
 constexpr int kSpanLevels = 8;                                  // log2(kMaxSpans)
 constexpr int kTableWords = 8 * 256;                            // one set of 8 byte tables (16 KiB)
-constexpr int kCopies = 16;                                     // LDS replicas of the slicing tables
+constexpr int kCopies = 8;                                      // LDS replicas of the slicing tables
+constexpr int kWaves = kCrcThreads / 64;
+constexpr int kStageWords = kWaves * 64 * kPiece / 8;           // per-wave staging of one sub-chunk slice
 // workspace table sets: 0 slicing, 1 sub-chunk advance, 2.. lane levels, then span levels
 constexpr int kSetSlice = 0, kSetSub = 1, kSetLane = 2, kSetSpan = kSetLane + kLaneLevels;
 constexpr int kSets = kSetSpan + kSpanLevels;
@@ -153,9 +157,13 @@ __global__ __launch_bounds__(kCrcThreads) void crc64_span_kernel(const u32x4* __
                                                                  int64_t span_subs,
                                                                  const uint64_t* __restrict__ tables,
                                                                  uint64_t* __restrict__ partial) {
-  __shared__ uint64_t t_slice[4 * 256 * kCopies];   // tables 0..3, kCopies replicas (128 KiB)
+  // [0, 8192): slicing tables 0..3 in kCopies replicas (64 KiB); [8192, 16384): per-wave staging
+  // (64 KiB); after the span, all 128 KiB hold join levels 0..7
+  __shared__ __attribute__((aligned(16))) uint64_t big[4 * 256 * kCopies + kStageWords];
   __shared__ uint64_t t_sub[kTableWords];
   __shared__ uint64_t acc[kCrcThreads];
+  static_assert(4 * 256 * kCopies + kStageWords == 8 * kTableWords, "join levels 0..7 fill the region");
+  uint64_t* t_slice = big;
   {
     // thread e writes entry e = (k, b) of tables 0..3 into all kCopies replicas
     static_assert(4 * 256 == kCrcThreads, "one slicing entry per thread");
@@ -166,26 +174,44 @@ __global__ __launch_bounds__(kCrcThreads) void crc64_span_kernel(const u32x4* __
   }
   __syncthreads();
   const uint64_t* tc = t_slice + (threadIdx.x % kCopies);
-  const int64_t base = (int64_t)blockIdx.x * span_subs * kSub + (int64_t)threadIdx.x * kPiece - pad;  // data offset
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  // this wave's 4 KiB staging area: 4 rows of 64 16-byte slots; slot (row j, lane l) holds the
+  // wave's bytes [1024 j + 16 l, +16) at position l ^ ((l >> 4) & 3), which keeps both the
+  // row-wise writes and the lane-piece reads free of bank conflicts
+  u32x4* stage_area = reinterpret_cast<u32x4*>(big + 4 * 256 * kCopies) + wave * 4 * 64;
+  // data offset of this wave's slice of sub-chunk 0 plus this lane's 16-byte column
+  const int64_t base = (int64_t)blockIdx.x * span_subs * kSub + (int64_t)wave * 64 * kPiece + 16 * lane - pad;
   u32x4 cur[kLoads], nxt[kLoads];
   auto load = [&](u32x4 (&v)[kLoads], int64_t sub) {
 #pragma unroll
     for (int j = 0; j < kLoads; ++j) {
-      const int64_t off = base + (sub << kSubLog2) + 16 * j;
+      const int64_t off = base + (sub << kSubLog2) + 1024 * j;
       v[j] = off >= 0 ? __builtin_nontemporal_load(data + off / 16) : u32x4{0u, 0u, 0u, 0u};   // off < head
     }
   };
+  const int wr = lane ^ ((lane >> 4) & 3);                        // write slot of this lane in each row
+  const int rrow = lane >> 4, rcol = 4 * (lane & 15);             // this lane's piece: row, first column
   load(cur, 0);
   uint64_t fold = 0;
   for (int64_t sub = 0; sub < span_subs; ++sub) {
     if (sub + 1 < span_subs) load(nxt, sub + 1);
+#pragma unroll
+    for (int j = 0; j < kLoads; ++j) stage_area[j * 64 + wr] = cur[j];
+    __builtin_amdgcn_wave_barrier();
+    u32x4 piece[kLoads];
+#pragma unroll
+    for (int m = 0; m < kLoads; ++m) {
+      const int l = rcol + m;
+      piece[m] = stage_area[rrow * 64 + (l ^ ((l >> 4) & 3))];
+    }
+    __builtin_amdgcn_wave_barrier();   // reads done before the next sub-chunk's writes
     uint64_t reg = 0;
 #pragma unroll
     for (int j = 0; j < kLoads; ++j) {
-      reg = crc_word4(reg, cur[j].x, tc);
-      reg = crc_word4(reg, cur[j].y, tc);
-      reg = crc_word4(reg, cur[j].z, tc);
-      reg = crc_word4(reg, cur[j].w, tc);
+      reg = crc_word4(reg, piece[j].x, tc);
+      reg = crc_word4(reg, piece[j].y, tc);
+      reg = crc_word4(reg, piece[j].z, tc);
+      reg = crc_word4(reg, piece[j].w, tc);
     }
     fold = lookup8(fold, t_sub) ^ reg;
 #pragma unroll
@@ -193,7 +219,7 @@ __global__ __launch_bounds__(kCrcThreads) void crc64_span_kernel(const u32x4* __
   }
   acc[threadIdx.x] = fold;
   __syncthreads();   // every lane is done with the slicing tables: their LDS holds the join levels now
-  uint64_t* lvl_tab = t_slice;                                   // levels 0..7 (8 x 16 KiB)
+  uint64_t* lvl_tab = big;                                       // levels 0..7 (8 x 16 KiB)
   stage<16>(lvl_tab, tables + kSetLane * kTableWords, 8 * kTableWords, kCrcThreads);
   stage<2>(t_sub, tables + (kSetLane + 8) * kTableWords, kTableWords, kCrcThreads);   // level 8
   __syncthreads();
