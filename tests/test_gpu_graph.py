@@ -111,3 +111,68 @@ def test_layout_moves_in_a_graph(tk):
     import oracle.reshard as rs
     want = rs.pack_layer_heads(to_host(src[2])[None], 0, wl.block_tables, wl.seq_lens, 4, 4)
     assert np.array_equal(to_host(packed_g[2, 1]), want), "last layer's second head half vs the oracle"
+
+
+def test_hybrid_sweep_in_a_graph(tk):
+    """A reduced hybrid model's sweep (state layers through the state calls,
+    attention layers through the batched calls, both directions) captured
+    once and replayed with eager work in between, equal to eager launches;
+    also a CRC-64 and a one-request pack in the same graph."""
+    from paper_2607_28633_amd.workloads import device_state_cache
+    wl = make_workload("qwen3.5-397b-hybrid", num_layers=8, seq_lens=[300, 17, 4096, 1], state_bytes=65536)
+    say(f"[graph] hybrid sweep: {wl.describe()}")
+    src, dst0 = device_src_pool(wl), device_dst_prefill(wl)
+    st_src, st_dst0 = device_state_cache(wl), device_state_cache(wl, dst=True)
+    bt = torch.from_numpy(wl.block_tables).cuda()
+    bt2 = torch.from_numpy(wl.dst_block_tables).cuda()
+    lens = torch.from_numpy(wl.seq_lens).cuda()
+    s1, s2 = torch.from_numpy(wl.state_slots).cuda(), torch.from_numpy(wl.dst_state_slots).cuda()
+    L, R = wl.num_layers, wl.num_reqs
+    kv = tk.topkv_packed_layer_bytes(src, wl.seq_lens)
+    stb = tk.topkv_packed_state_bytes(st_src, R)
+    width = max(kv, stb) // 2
+    one = tk.topkv_packed_layer_bytes(src, wl.seq_lens[2:3]) // 2
+    ws = torch.empty(tk.topkv_crc64_workspace_bytes(kv) // 8, dtype=torch.int64, device="cuda")
+
+    def sweep(packed, dst, st_dst, crc, single):
+        for l in range(L):
+            if wl.is_state(l):
+                tk.topkv_pack_state_layer(st_src, wl.state_slab(l), R, s1, packed[l], dst_bytes=stb)
+            else:
+                tk.topkv_pack_layer_batched(src, wl.kv_slab(l), R, bt, bt.shape[1], lens, packed[l], dst_bytes=kv)
+        for l in range(L):
+            if wl.is_state(l):
+                tk.topkv_unpack_state_layer(packed[l], st_dst, wl.state_slab(l), R, s2, src_bytes=stb)
+            else:
+                tk.topkv_unpack_layer_batched(packed[l], dst, wl.kv_slab(l), R, bt2, bt2.shape[1], lens,
+                                              src_bytes=kv)
+        tk.topkv_crc64(packed[L - 1], kv, ws, crc)
+        tk.topkv_pack_layer_batched(src, 0, 1, bt[2:3], bt.shape[1], lens[2:3], single, dst_bytes=2 * one)
+
+    def outputs():
+        return (torch.zeros((L, width), dtype=torch.int16, device="cuda"), dst0.clone(), st_dst0.clone(),
+                torch.zeros(1, dtype=torch.int64, device="cuda"), torch.zeros(one, dtype=torch.int16, device="cuda"))
+
+    out_g = outputs()
+    torch.cuda.synchronize()
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g):
+        sweep(*out_g)
+    torch.cuda.synchronize()
+    for replay in range(3):
+        src.view(torch.int16).add_(replay + 1)
+        st_src.add_(replay + 3)
+        fresh = outputs()
+        for a, b in zip(out_g, fresh):
+            a.copy_(b)
+        out_e = outputs()
+        sweep(*out_e)
+        torch.cuda.synchronize()
+        g.replay()
+        torch.cuda.synchronize()
+        for i, (a, b) in enumerate(zip(out_g, out_e)):
+            assert torch.equal(a.view(torch.int16), b.view(torch.int16)), f"replay {replay}: output {i} differs"
+    import oracle.state as so
+    lay = max(l for l in range(L) if wl.is_state(l))
+    want = so.pack_state_layer(to_host(st_src[wl.state_slab(lay)])[None], 0, wl.state_slots)
+    assert np.array_equal(to_host(out_g[0][lay])[:stb // 2], want), "last state layer vs the oracle"
