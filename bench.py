@@ -537,14 +537,16 @@ def run_pipeline(args, check=None):
     """Section 5.2 on one GPU.  A prefill stream computes layer after layer
     (one bf16 GEMM per layer, sized to --layer-ms); as each layer finishes its
     KV is packed (one launch) and shipped over PCIe into pinned host memory.
-    Three placements of that transfer are timed against the same prefill:
+    Four placements of that transfer are timed against the same prefill:
       side  - pack + HIP device-to-host copy on a second stream (the copy is
               a kernel on the compute units);
       fused - the pack kernel, on a second stream, writes the packed layer
               straight into mapped pinned host memory (no staging, no copy);
       dma   - the pack runs on the prefill stream right after its layer and
               the library's shipper copies it on a DMA engine once the
-              layer's event has completed (no compute unit used).
+              layer's event has completed (no compute unit used);
+      dma_side_pack - as dma, with the pack on a second stream after the
+              layer's compute, so it can overlap the next layer's compute.
     Measured: compute alone, transfer alone (side placement), both back to
     back (serial), and each placement alone and overlapped.
     hidden = 1 - exposed / transfer with exposed = pipelined - compute, beside
@@ -628,14 +630,25 @@ def run_pipeline(args, check=None):
                 xfer(l)
         return body
 
-    def dma_body(with_compute):
+    computed = [torch.cuda.Event() for _ in range(L)]
+
+    def dma_body(with_compute, pack_on_side=False):
+        """Pack each layer after its compute (on the prefill stream, or on a
+        side stream so the pack can overlap the next layer's compute), then
+        hand its copy to the shipper."""
         def body():
             last = 0
             for l in range(L):
                 if with_compute:
                     compute(l)
-                main_pack[l]()
-                ready[l].record(main)
+                if pack_on_side:
+                    computed[l].record(main)
+                    side.wait_event(computed[l])
+                    side_pack[l]()
+                    ready[l].record(side)
+                else:
+                    main_pack[l]()
+                    ready[l].record(main)
                 last = topkv.topkv_dma_submit(dma, ready[l], host[l], packed[l], nbytes)
             topkv.topkv_dma_wait(dma, last)
         return body
@@ -672,7 +685,8 @@ def run_pipeline(args, check=None):
     runs = {"compute": best(each(compute)), "transfer": best(each(side_xfer)), "serial": best(serial)}
     plans = {"side": (each(side_xfer), over_side(side_xfer)),
              "fused": (each(fused_xfer), over_side(fused_xfer)),
-             "dma": (dma_body(False), dma_body(True))}
+             "dma": (dma_body(False), dma_body(True)),
+             "dma_side_pack": (dma_body(False, True), dma_body(True, True))}
     variants = {}
     for name, (alone, overlapped) in plans.items():
         v = {"transfer_ms": best(alone), "pipelined_ms": best(overlapped)}

@@ -1,5 +1,6 @@
 """Pipelined layer-by-layer transfer (Section 5.2) on one GPU: in every
-placement (side stream, pack straight into mapped host memory, DMA shipper)
+placement (side stream, pack straight into mapped host memory, DMA shipper
+with the pack on the prefill stream or on a second stream)
 the layers shipped while the synthetic prefill runs arrive bit-exact in
 pinned host memory; the staging and host buffers are poisoned before every
 run, so a copy that read stale data would fail."""
@@ -32,10 +33,10 @@ def test_pipelined_layers_arrive_intact():
         seen.append(variant)
 
     args = types.SimpleNamespace(workload="llama3-8b", steps=1, layer_ms=0.2)
-    say("[pipeline] llama3-8b, 32 layers, 3 placements")
+    say("[pipeline] llama3-8b, 32 layers, 4 placements")
     out = bench.run_pipeline(args, check=check)
     say(f"  {out['ms']} {out['placements']}")
-    assert seen == ["side", "fused", "dma"]
+    assert seen == ["side", "fused", "dma", "dma_side_pack"]
     assert out["ms"]["serial"] >= out["ms"]["compute"]
 
 
