@@ -435,7 +435,7 @@ int64_t topkv_packed_state_bytes(const topkv_state_pool_t* pool, int32_t num_req
  *   launch:    stream and optional kernel-timestamp events (non-null)
  * num_reqs == 0 launches nothing.  TOPKV_ERR_INVALID_ARG for a bad
  * descriptor, layer, num_reqs < 0, null slots/dst, or dst_bytes too small;
- * TOPKV_ERR_UNSUPPORTED when a state spans 2^31 or more tiles of 32 KiB;
+ * TOPKV_ERR_UNSUPPORTED when a state spans 2^31 or more tiles;
  * TOPKV_ERR_LAUNCH if the launch fails.  One kernel on the stream; 16-byte
  * vectors when base, dst and state_bytes are 16-byte multiples, narrower
  * ones otherwise. */
@@ -451,6 +451,30 @@ topkv_status_t topkv_pack_state_layer(const topkv_state_pool_t* src, int32_t lay
 topkv_status_t topkv_unpack_state_layer(const void* src, int64_t src_bytes, const topkv_state_pool_t* dst,
                                         int32_t layer, int32_t num_reqs, const int32_t* slots,
                                         const topkv_launch_t* launch);
+
+/* Checked path for fixed-state layers: report the slot indices that
+ * topkv_pack_state_layer / topkv_unpack_state_layer would skip, and (with
+ * check_duplicates != 0) slots named twice in the batch, which an unpack
+ * destination must not have (two writers of one slot race).
+ *   pool:      geometry only (num_slots); base is not accessed
+ *   slots:     device int32[num_reqs]
+ *   workspace: device memory of topkv_check_state_workspace_bytes(pool)
+ *              bytes (a slot bitmap), cleared by this call; may be null when
+ *              check_duplicates == 0
+ *   result:    device int32[4], written on the stream: [0] TOPKV_OK or
+ *              TOPKV_ERR_BOUNDS, [1] slots out of range, [2] repeated slots,
+ *              [3] 0.  Read it after the stream has synchronised.
+ * TOPKV_ERR_INVALID_ARG for a bad descriptor, num_reqs < 0, null slots
+ * (num_reqs > 0) or result, or a missing or short workspace.  Launches small
+ * kernels without synchronising; calls sharing a workspace on overlapping
+ * streams race. */
+topkv_status_t topkv_check_state_slots(const topkv_state_pool_t* pool, int32_t num_reqs, const int32_t* slots,
+                                       int32_t check_duplicates, void* workspace, int64_t workspace_bytes,
+                                       int32_t* result, hipStream_t stream);
+
+/* Workspace bytes topkv_check_state_slots needs (num_slots bits in 4-byte
+ * words); -1 for a null pool or num_slots <= 0. */
+int64_t topkv_check_state_workspace_bytes(const topkv_state_pool_t* pool);
 
 /* Layer shipper (Sec. 5.2: layer l's cache leaves while layers l+1 .. L still
  * compute).  Copies run on the GPU's DMA engines (ROCr asynchronous copies),

@@ -1,7 +1,8 @@
 // check.hip - checked path of libtopkv.so: device-side validation of block
-// tables and lengths (declared in include/topkv.h).  The movement kernels in
-// topkv.hip never depend on it; they bounds-check what they read and skip
-// bad entries silently, and this call reports them.
+// tables and lengths, and of fixed-state slot indices (declared in
+// include/topkv.h).  The movement kernels never depend on it; they
+// bounds-check what they read and skip bad entries silently, and these calls
+// report them.
 #include <hip/hip_runtime.h>
 
 #include <cstdint>
@@ -50,6 +51,26 @@ __global__ __launch_bounds__(256) void kv_check_tables_kernel(const int32_t* __r
   }
 }
 
+// One thread per request of a fixed-state layer batch: its slot must lie in
+// [0, num_slots) and, with check_duplicates, no slot may be named twice.
+__global__ __launch_bounds__(256) void kv_check_slots_kernel(const int32_t* __restrict__ slots, int32_t num_reqs,
+                                                             int64_t num_slots, int32_t check_duplicates,
+                                                             uint32_t* __restrict__ bitmap,
+                                                             int32_t* __restrict__ result) {
+  const int32_t r = (int32_t)(blockIdx.x * blockDim.x + threadIdx.x);
+  if (r >= num_reqs) return;
+  const int32_t e = slots[r];
+  if (e < 0 || (int64_t)e >= num_slots) {
+    atomicAdd(&result[1], 1);
+    return;
+  }
+  if (check_duplicates) {
+    const uint32_t bit = 1u << (e & 31);
+    const uint32_t old = atomicOr(&bitmap[e >> 5], bit);
+    if (old & bit) atomicAdd(&result[2], 1);
+  }
+}
+
 __global__ void kv_check_finish_kernel(int32_t* __restrict__ result) {
   if (threadIdx.x == 0)
     result[0] = (result[1] | result[2] | result[3]) ? (int32_t)TOPKV_ERR_BOUNDS : (int32_t)TOPKV_OK;
@@ -86,6 +107,34 @@ topkv_status_t topkv_check_tables(const topkv_pool_t* pool, int32_t num_reqs, co
     hipLaunchKernelGGL(kv_check_tables_kernel, dim3((unsigned)((slots + 255) / 256)), dim3(256), 0, stream,
                        block_tables, seq_lens, num_reqs, bt_stride, pool->page_size, pool->num_pages,
                        (int32_t)dup, bitmap, result);
+    if (hipGetLastError() != hipSuccess) return TOPKV_ERR_LAUNCH;
+  }
+  hipLaunchKernelGGL(kv_check_finish_kernel, dim3(1), dim3(64), 0, stream, result);
+  return hipGetLastError() == hipSuccess ? TOPKV_OK : TOPKV_ERR_LAUNCH;
+}
+
+int64_t topkv_check_state_workspace_bytes(const topkv_state_pool_t* pool) {
+  if (!pool || pool->num_slots <= 0) return -1;
+  return ((pool->num_slots + 31) / 32) * (int64_t)sizeof(uint32_t);
+}
+
+topkv_status_t topkv_check_state_slots(const topkv_state_pool_t* pool, int32_t num_reqs, const int32_t* slots,
+                                       int32_t check_duplicates, void* workspace, int64_t workspace_bytes,
+                                       int32_t* result, hipStream_t stream) {
+  if (!pool || pool->num_slots <= 0 || num_reqs < 0 || !result || (num_reqs > 0 && !slots))
+    return TOPKV_ERR_INVALID_ARG;
+  const int64_t words = (pool->num_slots + 31) / 32;
+  const bool dup = check_duplicates != 0;
+  if (dup && (!workspace || workspace_bytes < words * (int64_t)sizeof(uint32_t))) return TOPKV_ERR_INVALID_ARG;
+  uint32_t* bitmap = dup ? static_cast<uint32_t*>(workspace) : nullptr;
+  const int64_t clear_words = dup ? words : 0;
+  const unsigned clear_grid = (unsigned)(clear_words / 256 + 1 < 1024 ? clear_words / 256 + 1 : 1024);
+  hipLaunchKernelGGL(kv_check_clear_kernel, dim3(clear_grid), dim3(256), 0, stream, bitmap, clear_words,
+                     result);
+  if (hipGetLastError() != hipSuccess) return TOPKV_ERR_LAUNCH;
+  if (num_reqs > 0) {
+    hipLaunchKernelGGL(kv_check_slots_kernel, dim3((unsigned)((num_reqs + 255) / 256)), dim3(256), 0, stream,
+                       slots, num_reqs, pool->num_slots, (int32_t)dup, bitmap, result);
     if (hipGetLastError() != hipSuccess) return TOPKV_ERR_LAUNCH;
   }
   hipLaunchKernelGGL(kv_check_finish_kernel, dim3(1), dim3(64), 0, stream, result);

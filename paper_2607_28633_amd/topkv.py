@@ -46,7 +46,8 @@ EXPORTS = ["topkv_pack_layer", "topkv_unpack_layer", "topkv_pack_layer_batched",
            "topkv_dma_submit", "topkv_dma_wait", "topkv_dma_destroy", "topkv_move_layer",
            "topkv_pack_layer_heads", "topkv_unpack_layer_heads", "topkv_reblock_layer",
            "topkv_pack_layer_shards", "topkv_unpack_layer_shards", "topkv_packed_state_bytes",
-           "topkv_pack_state_layer", "topkv_unpack_state_layer"]
+           "topkv_pack_state_layer", "topkv_unpack_state_layer", "topkv_check_state_slots",
+           "topkv_check_state_workspace_bytes"]
 
 TOPKV_LAYOUT_PACKED = 0
 TOPKV_LAYOUT_POOL = 1
@@ -120,6 +121,8 @@ _SIGS = {
                                       ctypes.POINTER(topkv_launch_t)]),
     "topkv_unpack_state_layer": (_I32, [_P, _I64, ctypes.POINTER(topkv_state_pool_t), _I32, _I32, _P,
                                         ctypes.POINTER(topkv_launch_t)]),
+    "topkv_check_state_slots": (_I32, [ctypes.POINTER(topkv_state_pool_t), _I32, _P, _I32, _P, _I64, _P, _P]),
+    "topkv_check_state_workspace_bytes": (_I64, [ctypes.POINTER(topkv_state_pool_t)]),
     "topkv_dma_create": (_I32, [ctypes.POINTER(_P)]),
     "topkv_dma_submit": (_I32, [_P, _P, _P, _P, _I64, ctypes.POINTER(_I64)]),
     "topkv_dma_wait": (_I32, [_P, _I64]),
@@ -648,3 +651,17 @@ def topkv_unpack_state_layer(src, dst, layer, num_reqs, slots, src_bytes=None, s
                              stop=None) -> None:
     """Unpack num_reqs packed states into slots slots[r] of one layer."""
     prepare_unpack_state_layer(src, dst, layer, num_reqs, slots, src_bytes, stream, start, stop)()
+
+
+def topkv_check_state_workspace_bytes(pool) -> int:
+    return int(_lib.topkv_check_state_workspace_bytes(ctypes.byref(_state_arg(pool))))
+
+
+def topkv_check_state_slots(pool, num_reqs, slots, result, check_duplicates=True, workspace=None,
+                            workspace_bytes=None, stream=None) -> None:
+    """Queue the slot check; result (device int32[4]) holds [status, out of
+    range, repeated, 0] once the stream has synchronised."""
+    wsb = 0 if workspace is None else _nbytes(workspace, workspace_bytes)
+    _check(_lib.topkv_check_state_slots(ctypes.byref(_state_arg(pool)), int(num_reqs), _table_ptr(slots),
+                                        int(bool(check_duplicates)), _ptr(workspace), wsb, _ptr(result),
+                                        _stream(stream)))

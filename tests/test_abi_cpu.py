@@ -199,5 +199,15 @@ def test_state_layer_validation(tk):
     _expect(tk, INV, tk.topkv_unpack_state_layer, 0, good, 1, 3, slots, src_bytes=3000)
     huge = st(num_slots=1, num_layers=1, state_bytes=1 << 50)
     _expect(tk, UNS, tk.topkv_pack_state_layer, huge, 0, 1, slots, buf, dst_bytes=1 << 50)    # 2^35 tiles
+    res, ws = 0x50000, 0x60000
+    assert tk.topkv_check_state_workspace_bytes(good) == 4
+    assert tk.topkv_check_state_workspace_bytes(st(num_slots=33)) == 8
+    assert tk.topkv_check_state_workspace_bytes(st(num_slots=0)) == -1
+    _expect(tk, INV, tk.topkv_check_state_slots, good, 2, slots, 0)                       # null result
+    _expect(tk, INV, tk.topkv_check_state_slots, good, 2, 0, res)                         # null slots
+    _expect(tk, INV, tk.topkv_check_state_slots, good, -1, slots, res)
+    _expect(tk, INV, tk.topkv_check_state_slots, good, 2, slots, res)                     # duplicates need a workspace
+    _expect(tk, INV, tk.topkv_check_state_slots, good, 2, slots, res, workspace=ws, workspace_bytes=3)
+    _expect(tk, INV, tk.topkv_check_state_slots, st(num_slots=0), 2, slots, res, check_duplicates=False)
     tk.topkv_pack_state_layer(good, 2, 0, 0, 0, dst_bytes=0, stream=0)      # no requests: nothing to launch
     tk.topkv_unpack_state_layer(0, good, 0, 0, 0, src_bytes=0, stream=0)

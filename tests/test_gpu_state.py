@@ -159,3 +159,28 @@ def test_hybrid_model_sweep(tk):
         assert np.array_equal(to_host(bufs[l])[:n], want), f"layer {l} pack differs"
     assert np.array_equal(to_host(kv_dst), kv_dst_h), "attention pools differ after the sweep"
     assert np.array_equal(to_host(st_dst), st_dst_h), "state caches differ after the sweep"
+
+
+def test_check_state_slots(tk):
+    """The checked path counts slots outside the cache and, when asked,
+    slots named twice; a clean batch reports TOPKV_OK."""
+    L, NS, E = 2, 40, 64
+    cache = to_dev(_cache(7, L, NS, E))
+    res = torch.full((4,), -9, dtype=torch.int32, device="cuda")
+    ws = torch.empty(tk.topkv_check_state_workspace_bytes(cache) // 4, dtype=torch.int32, device="cuda")
+    cases = [
+        (np.arange(NS, dtype=np.int32)[::-1].copy(), True, [0, 0, 0]),
+        (np.array([3, -1, 3, NS, 39, 3, 1 << 30, 0], dtype=np.int32), True, [3, 2, 0]),
+        (np.array([3, -1, 3, NS, 39, 3, 1 << 30, 0], dtype=np.int32), False, [3, 0, 0]),
+        (np.array([5, 5], dtype=np.int32), True, [0, 1, 0]),
+        (np.zeros(0, dtype=np.int32), True, [0, 0, 0]),
+    ]
+    for slots, dup, want in cases:
+        say(f"[state] check slots {slots.tolist()[:8]} duplicates={dup}")
+        ws.fill_(-1)                      # the call must clear its own bitmap
+        tk.topkv_check_state_slots(cache, slots.size, to_dev(slots) if slots.size else None, res,
+                                   check_duplicates=dup, workspace=ws if dup else None)
+        torch.cuda.synchronize()
+        got = res.cpu().tolist()
+        status = tk.TOPKV_OK if not any(want) else tk.TOPKV_ERR_BOUNDS
+        assert got == [status] + want, f"{slots.tolist()} dup={dup}: {got}"
