@@ -2,7 +2,10 @@
  * paged pool is packed (gather into the wire order [plane][token][head][dim]),
  * unpacked into a pool with another page size, packed again and compared; the
  * destination pool is then re-blocked back pool-to-pool and two head halves
- * are packed and checked against the full-head packed layer.
+ * are packed and checked against the full-head packed layer.  Then a
+ * fixed-state layer: two requests' states are packed from a state cache and
+ * unpacked into other slots of a second cache; and the device CRC-64 of
+ * "123456789" is checked against the published CRC-64/XZ check value.
  *
  * Build:  gcc -std=c11 -D__HIP_PLATFORM_AMD__ -I/opt/rocm/include -Iinclude \
  *             paper_2607_28633_amd/examples/roundtrip.c \
@@ -117,9 +120,58 @@ int main(void) {
             }
     }
 
+    /* fixed-state layer: states of slots {3, 1} of layer 1, unpacked into slots {0, 2} of a second cache */
+    enum { SLOTS = 4, STATE = 1000 };
+    const size_t cache_bytes = (size_t)LAYERS * SLOTS * STATE;
+    unsigned char* hc = malloc(cache_bytes);
+    unsigned char* hs = malloc(cache_bytes);
+    if (!hc || !hs) return 1;
+    for (size_t i = 0; i < cache_bytes; ++i) hc[i] = (unsigned char)(i * 131u + 7u);
+    void *d_cache, *d_cache2, *d_states, *d_slots, *d_slots2;
+    HIP_OK(hipMalloc(&d_cache, cache_bytes));
+    HIP_OK(hipMalloc(&d_cache2, cache_bytes));
+    HIP_OK(hipMalloc(&d_states, 2 * STATE));
+    HIP_OK(hipMalloc(&d_slots, 2 * sizeof(int32_t)));
+    HIP_OK(hipMalloc(&d_slots2, 2 * sizeof(int32_t)));
+    const int32_t slots[2] = {3, 1}, slots2[2] = {0, 2};
+    HIP_OK(hipMemcpy(d_cache, hc, cache_bytes, hipMemcpyHostToDevice));
+    HIP_OK(hipMemset(d_cache2, 0, cache_bytes));
+    HIP_OK(hipMemcpy(d_slots, slots, sizeof slots, hipMemcpyHostToDevice));
+    HIP_OK(hipMemcpy(d_slots2, slots2, sizeof slots2, hipMemcpyHostToDevice));
+    topkv_state_pool_t cache = {d_cache, SLOTS, STATE, LAYERS, 0};
+    topkv_state_pool_t cache2 = {d_cache2, SLOTS, STATE, LAYERS, 0};
+    topkv_launch_t on_null = {0, 0, 0};
+    if (topkv_packed_state_bytes(&cache, 2) != 2 * STATE) { fprintf(stderr, "packed state bytes\n"); return 1; }
+    TOPKV_OK_OR_FAIL(topkv_pack_state_layer(&cache, layer, 2, d_slots, d_states, 2 * STATE, &on_null));
+    TOPKV_OK_OR_FAIL(topkv_unpack_state_layer(d_states, 2 * STATE, &cache2, layer, 2, d_slots2, &on_null));
+    HIP_OK(hipDeviceSynchronize());
+    HIP_OK(hipMemcpy(hs, d_cache2, cache_bytes, hipMemcpyDeviceToHost));
+    for (size_t i = 0; i < cache_bytes; ++i) {
+        const size_t l = i / ((size_t)SLOTS * STATE), sl = i / STATE % SLOTS, e = i % STATE;
+        unsigned char want = 0;
+        if (l == (size_t)layer && (sl == 0 || sl == 2))
+            want = hc[((size_t)layer * SLOTS + (size_t)slots[sl / 2]) * STATE + e];
+        if (hs[i] != want) { fprintf(stderr, "state cache byte %zu differs\n", i); return 1; }
+    }
+
+    /* CRC-64/XZ of "123456789" on the device: the published check value */
+    const char msg[] = "123456789";
+    void *d_msg, *d_ws, *d_crc;
+    const int64_t ws_bytes = topkv_crc64_workspace_bytes(9);
+    HIP_OK(hipMalloc(&d_msg, 16));
+    HIP_OK(hipMalloc(&d_ws, (size_t)ws_bytes));
+    HIP_OK(hipMalloc(&d_crc, sizeof(uint64_t)));
+    HIP_OK(hipMemcpy(d_msg, msg, 9, hipMemcpyHostToDevice));
+    TOPKV_OK_OR_FAIL(topkv_crc64(d_msg, 9, d_ws, ws_bytes, (uint64_t*)d_crc, 0));
+    uint64_t crc = 0;
+    HIP_OK(hipMemcpy(&crc, d_crc, sizeof crc, hipMemcpyDeviceToHost));
+    if (crc != 0x995DC9BBDF1939FAull) { fprintf(stderr, "crc64 %016llx\n", (unsigned long long)crc); return 1; }
+
     hipFree(d_pool); hipFree(d_dst); hipFree(d_back); hipFree(d_a); hipFree(d_b); hipFree(d_half);
     hipFree(d_bt_src); hipFree(d_bt_dst); hipFree(d_len);
-    free(host_pool); free(a); free(b);
+    hipFree(d_cache); hipFree(d_cache2); hipFree(d_states); hipFree(d_slots); hipFree(d_slots2);
+    hipFree(d_msg); hipFree(d_ws); hipFree(d_crc);
+    free(host_pool); free(a); free(b); free(hc); free(hs);
     printf("roundtrip ok\n");
     return 0;
 }
