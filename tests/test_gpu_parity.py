@@ -275,3 +275,32 @@ def test_one_request_device_length(tk, n):
             oracle.unpack_layer(packed_want, want_dst, layer, tbl[None], np.array([clamp], np.int32))
             want_dst[layer, spare] = keep
         assert np.array_equal(to_host(dst), want_dst), f"n={n} cap={cap}: unpack differs"
+
+
+@pytest.mark.parametrize("offset", [2, 8])
+def test_one_request_misaligned_packed(tk, offset):
+    """The one-request grid with a packed buffer `offset` bytes off 16-byte
+    alignment (2- and 8-byte pieces): pack and unpack equal the oracle, and
+    nothing outside the batch is written."""
+    P, W, NP, layer, n = 16, 8, 40, 0, 117
+    wl = make_workload("tiny", seed=12, num_heads=4, head_dim=128, seq_lens=[n], num_pages=NP, dst_num_pages=NP)
+    row = wl.planes * wl.num_heads * wl.head_dim              # words per token over both planes
+    rng = np.random.default_rng(offset)
+    bt, bt2 = (rng.permutation(NP)[:W].astype(np.int32)[None] for _ in range(2))
+    src_h, dst_h = host_src_pool(wl), host_dst_prefill(wl)
+    src, dst = to_dev(src_h), to_dev(dst_h)
+    lens = to_dev(np.array([n], dtype=np.int32))
+    full = W * P * row * 2                                     # bytes for the whole table: the routed grid
+    say(f"[one_request_misaligned] offset {offset}")
+    raw = torch.zeros(full + 64, dtype=torch.uint8, device="cuda")
+    base = raw.data_ptr() + offset
+    tk.topkv_pack_layer_batched(src, layer, 1, to_dev(bt), W, lens, base, dst_bytes=full)
+    torch.cuda.synchronize()
+    want = oracle.pack_layer(src_h, layer, bt, np.array([n], np.int32))
+    got = raw.cpu().numpy()
+    assert np.array_equal(got[offset:offset + want.nbytes].view(np.uint16), want)
+    assert (got[:offset] == 0).all() and (got[offset + want.nbytes:] == 0).all()
+    tk.topkv_unpack_layer_batched(base, dst, layer, 1, to_dev(bt2), W, lens, src_bytes=full)
+    torch.cuda.synchronize()
+    oracle.unpack_layer(want, dst_h, layer, bt2, np.array([n], np.int32))
+    assert np.array_equal(to_host(dst), dst_h)
