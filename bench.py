@@ -383,8 +383,11 @@ def run(args):
 
 def run_kvcache1(args):
     """Whole-request serialization of request 0 (Section 3.5 KVCACHE1 format):
-    per step, pack every layer into the blob, seal (CRC-64 of K and V + header),
-    verify on the receiving side, unpack every layer into the decode pool."""
+    per step, pack every layer into the blob (one launch for the whole
+    request), seal (CRC-64 of K and V + header), verify on the receiving
+    side, unpack every layer into the decode pool (one launch).  The
+    layer-by-layer calls a pipelined sender uses (one launch per layer) are
+    timed beside them."""
     import torch
 
     from paper_2607_28633_amd import topkv
@@ -406,11 +409,16 @@ def run_kvcache1(args):
     stream = torch.cuda.current_stream()
     L = wl.num_layers
     phases = {
-        "pack_layers": lambda: [topkv.topkv_kvcache1_pack_layer(src, l, bt, n, blob, stream=stream) for l in range(L)],
+        "pack_layers": lambda: topkv.topkv_kvcache1_pack_layers(src, 0, L, bt, n, blob, stream=stream),
         "seal": lambda: topkv.topkv_kvcache1_seal(geo, n, 1, 2, blob, ws, stream=stream),
         "verify": lambda: topkv.topkv_kvcache1_verify(geo, n, 1, 2, blob, ws, res, stream=stream),
-        "unpack_layers": lambda: [topkv.topkv_kvcache1_unpack_layer(blob, dst, l, bt2, n, stream=stream)
-                                  for l in range(L)],
+        "unpack_layers": lambda: topkv.topkv_kvcache1_unpack_layers(blob, dst, 0, L, bt2, n, stream=stream),
+    }
+    per_layer = {
+        "pack_per_layer": lambda: [topkv.topkv_kvcache1_pack_layer(src, l, bt, n, blob, stream=stream)
+                                   for l in range(L)],
+        "unpack_per_layer": lambda: [topkv.topkv_kvcache1_unpack_layer(blob, dst, l, bt2, n, stream=stream)
+                                     for l in range(L)],
     }
     for _ in range(args.warmup):
         for f in phases.values():
@@ -431,13 +439,24 @@ def run_kvcache1(args):
         us = 1e3 * sum(marks[k][j].elapsed_ms(marks[k][j + 1]) for k in range(args.steps)) / args.steps
         out_ph[name] = {"us": round(us, 2), "bytes": moved[name], "gbs": round(moved[name] / us / 1e3, 1)}
     total_us = 1e3 * marks[0][0].elapsed_ms(marks[-1][-1]) / args.steps
+    side = {}
+    for name, f in per_layer.items():
+        f()
+        e0, e1 = topkv.HipEvent(), topkv.HipEvent()
+        e0.record(stream)
+        for _ in range(args.steps):
+            f()
+        e1.record(stream)
+        e1.synchronize()
+        us = 1e3 * e0.elapsed_ms(e1) / args.steps
+        side[name] = {"us": round(us, 2), "launches": L, "gbs": round(2 * body / us / 1e3, 1)}
     print(json.dumps({
         "metric": "KVCACHE1 whole-request serialize + verify + deserialize GB/s", "mode": "kvcache1",
         "value": round(sum(moved.values()) / total_us / 1e3, 1), "unit": "GB/s", "n_gpus": 1,
         "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(total_us / 1e3, 4),
         "higher_is_better": True, "dtype": "bf16", "data": "synthetic", "verified": ok,
         "config": {"workload": f"{wl.name}: {WORKLOADS[wl.name]}", "request_tokens": n, "blob_bytes": nbytes},
-        "phases": out_ph}), flush=True)
+        "phases": out_ph, "layer_by_layer": side}), flush=True)
 
 
 def run_reshard(args):

@@ -18,6 +18,17 @@ topkv_status_t single_request_move(bool pack, const topkv_pool_t* pool, int32_t 
                                    int64_t packed_cap, const int32_t* tables, int32_t bt_stride,
                                    const int32_t* seq_lens, const topkv_launch_t* launch, bool* launched);
 
+// One request with caller-placed planes, layers [first_layer, first_layer +
+// layers) in one launch: plane c of layer first_layer + z is at packed +
+// z * layer_stride + c * plane_stride, and the last byte moved must lie
+// within packed_cap.  TOPKV_ERR_UNSUPPORTED (nothing queued) when one
+// layer's work is too large for the direct grid that carries the layer
+// dimension; the caller then moves the layers one launch each.
+__attribute__((visibility("hidden")))
+topkv_status_t placed_layers_move(bool pack, const topkv_pool_t* pool, int32_t first_layer, int32_t layers,
+                                  void* packed, int64_t packed_cap, int64_t plane_stride, int64_t layer_stride,
+                                  const int32_t* block_table, int32_t seq_len, hipStream_t stream);
+
 }  // namespace topkv_internal
 
 #endif  // TOPKV_INTERNAL_H_

@@ -39,6 +39,7 @@
 #include <cstdint>
 #include <cstring>
 
+#include "internal.h"
 #include "topkv.h"
 
 namespace {
@@ -432,6 +433,34 @@ int64_t blob_ws_bytes(const Blob& b) {
 
 bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15) == 0; }
 
+// Layers [first_layer, first_layer + num_layers) of one request into (pack) or
+// out of (unpack) their rows of the blob's K and V tensors: one launch when
+// the layer dimension fits the direct grid, else one launch per layer.
+topkv_status_t kv1_move_layers(bool pack, const topkv_pool_t* pool, int32_t first_layer, int32_t num_layers,
+                                      const int32_t* block_table, int32_t seq_len, void* blob, int64_t blob_bytes,
+                                      hipStream_t stream) {
+  Blob b;
+  topkv_status_t st = blob_geometry(pool, seq_len, &b);
+  if (st != TOPKV_OK) return st;
+  if (!blob || blob_bytes < b.total || first_layer < 0 || num_layers < 0 ||
+      (int64_t)first_layer + num_layers > pool->num_layers)
+    return TOPKV_ERR_INVALID_ARG;
+  if (!aligned16(blob)) return TOPKV_ERR_UNSUPPORTED;
+  if (seq_len == 0 || num_layers == 0) return TOPKV_OK;
+  const int64_t layer_rows = (int64_t)seq_len * b.row;                 // one layer's rows in one tensor
+  unsigned char* k = static_cast<unsigned char*>(blob) + kHeaderBytes + first_layer * layer_rows;
+  const int64_t cap = blob_bytes - (kHeaderBytes + first_layer * layer_rows);
+  st = topkv_internal::placed_layers_move(pack, pool, first_layer, num_layers, k, cap, b.k_bytes, layer_rows,
+                                          block_table, seq_len, stream);
+  if (st != TOPKV_ERR_UNSUPPORTED) return st;
+  for (int32_t l = 0; l < num_layers; ++l) {                            // too large for one grid
+    st = topkv_internal::placed_layers_move(pack, pool, first_layer + l, 1, k + l * layer_rows, cap - l * layer_rows,
+                                            b.k_bytes, 0, block_table, seq_len, stream);
+    if (st != TOPKV_OK) return st;
+  }
+  return TOPKV_OK;
+}
+
 }  // namespace
 
 extern "C" {
@@ -522,6 +551,19 @@ topkv_status_t topkv_kvcache1_unpack_layer(const void* blob, int64_t blob_bytes,
   const unsigned char* k = static_cast<const unsigned char*>(blob) + kHeaderBytes + (int64_t)layer * seq_len * b.row;
   return topkv_unpack_layer_planes(k, b.k_bytes, blob_bytes - (kHeaderBytes + (int64_t)layer * seq_len * b.row),
                                    dst, layer, block_table, seq_len, stream);
+}
+
+topkv_status_t topkv_kvcache1_pack_layers(const topkv_pool_t* src, int32_t first_layer, int32_t num_layers,
+                                          const int32_t* block_table, int32_t seq_len, void* blob,
+                                          int64_t blob_bytes, hipStream_t stream) {
+  return kv1_move_layers(true, src, first_layer, num_layers, block_table, seq_len, blob, blob_bytes, stream);
+}
+
+topkv_status_t topkv_kvcache1_unpack_layers(const void* blob, int64_t blob_bytes, const topkv_pool_t* dst,
+                                            int32_t first_layer, int32_t num_layers, const int32_t* block_table,
+                                            int32_t seq_len, hipStream_t stream) {
+  return kv1_move_layers(false, dst, first_layer, num_layers, block_table, seq_len, const_cast<void*>(blob),
+                         blob_bytes, stream);
 }
 
 }  // extern "C"

@@ -87,6 +87,8 @@ struct MoveParams {
   int32_t window;             // > 0: only the last `window` tokens of each request move
   int32_t pad_;
   int64_t plane_stride;       // single request only: > 0 places plane c at packed + c * plane_stride
+  int64_t layer_bytes;        // single request, several layers: pool bytes per layer
+  int64_t layer_stride;       // single request, several layers: packed bytes between consecutive layers
 };
 
 // First token a windowed layer keeps (window 0 keeps all): the last
@@ -247,8 +249,10 @@ __device__ __forceinline__ void move_direct(char* __restrict__ pool, char* __res
                                             const int32_t* __restrict__ tables,
                                             const int32_t* __restrict__ seq_lens, const MoveParams& p) {
   constexpr int32_t kTile = kThreads * VPT * VB;
-  // grid: z = request, y = table entry, x = plane * tiles_per_plane + tile
-  const int32_t r = blockIdx.z;
+  // grid: z = request (single request: z = layer after the first), y = table
+  // entry, x = plane * tiles_per_plane + tile
+  const int32_t r = kBatched ? (int32_t)blockIdx.z : 0;
+  const int64_t lz = kBatched ? 0 : (int64_t)blockIdx.z;
   const int32_t i = blockIdx.y;
   const int32_t c = (int32_t)(blockIdx.x / (uint32_t)p.tiles_per_plane);
   const int32_t k = (int32_t)(blockIdx.x - (uint32_t)c * p.tiles_per_plane);
@@ -274,7 +278,7 @@ __device__ __forceinline__ void move_direct(char* __restrict__ pool, char* __res
   const bool live = (hi > lo) & (tstart < run) & (page >= 0) & ((int64_t)page < p.num_pages);
   if (!live) return;
   const int32_t nv = (int32_t)((run - tstart < kTile ? run - tstart : kTile) / VB);
-  char* pool_ptr = pool + (int64_t)page * p.page_bytes + (int64_t)c * p.plane_bytes +
+  char* pool_ptr = pool + lz * p.layer_bytes + (int64_t)page * p.page_bytes + (int64_t)c * p.plane_bytes +
                    (int64_t)(lo - first) * p.row_bytes + tstart;
   typename Vec<VB>::type v[VPT];
   // Pack: the pool loads go out before the token offset is known (their
@@ -289,8 +293,8 @@ __device__ __forceinline__ void move_direct(char* __restrict__ pool, char* __res
     plane_off = ((int64_t)tok0 * p.planes + (int64_t)c * cnt) * p.row_bytes;
     end = ((int64_t)tok0 + cnt) * p.planes * p.row_bytes;
   }
-  if (end > p.packed_cap) return;
-  char* packed_ptr = packed + plane_off + (int64_t)(lo - start) * p.row_bytes + tstart;
+  if (end + lz * p.layer_stride > p.packed_cap) return;
+  char* packed_ptr = packed + lz * p.layer_stride + plane_off + (int64_t)(lo - start) * p.row_bytes + tstart;
   if (kPack) {
     store_tile<VB, VPT>(packed_ptr, v, nv);
   } else {
@@ -498,13 +502,17 @@ int vectors_per_lane(int vb, int64_t plane_bytes) {
 topkv_status_t launch_move(bool pack, const topkv_pool_t* pool, int32_t layer, void* packed,
                            int64_t packed_cap, int32_t num_reqs, const int32_t* tables,
                            int32_t bt_stride, const int32_t* seq_lens, int32_t n_single, int32_t window,
-                           int64_t plane_stride, const topkv_launch_t* launch) {
+                           int64_t plane_stride, const topkv_launch_t* launch, int32_t layers = 1,
+                           int64_t layer_stride = 0) {
   Geometry g;
   topkv_status_t st = pool_geometry(pool, layer, &g);
   if (st != TOPKV_OK) return st;
   if (!launch) return TOPKV_ERR_INVALID_ARG;
   if (num_reqs < 0 || n_single < 0 || packed_cap < 0 || window < 0 || plane_stride < 0) return TOPKV_ERR_INVALID_ARG;
   if (plane_stride > 0 && seq_lens) return TOPKV_ERR_INVALID_ARG;   // placed planes: one request only
+  // several layers in one launch: one request with placed planes, layers [layer, layer + layers)
+  if (layers < 1 || layer_stride < 0 || (int64_t)layer + layers > pool->num_layers) return TOPKV_ERR_INVALID_ARG;
+  if (layers > 1 && (seq_lens || plane_stride <= 0 || layers > 65535)) return TOPKV_ERR_INVALID_ARG;
   if (num_reqs > TOPKV_MAX_BATCH_REQS) return TOPKV_ERR_UNSUPPORTED;
   if (num_reqs == 0 || (!seq_lens && n_single == 0)) return TOPKV_OK;  // nothing to move
   if (!tables || !packed || bt_stride <= 0) return TOPKV_ERR_INVALID_ARG;
@@ -523,7 +531,7 @@ topkv_status_t launch_move(bool pack, const topkv_pool_t* pool, int32_t layer, v
   }
 
   int vb = vector_bytes(reinterpret_cast<uintptr_t>(pool->base), reinterpret_cast<uintptr_t>(packed), g.row_bytes);
-  while (plane_stride % vb) vb >>= 1;             // placed planes keep every run vector-aligned
+  while (plane_stride % vb || layer_stride % vb) vb >>= 1;   // placed planes keep every run vector-aligned
   const int vpt = vectors_per_lane(vb, g.plane_bytes);
   const int64_t tile = (int64_t)kThreads * vpt * vb;
   const int64_t tpp = (g.plane_bytes + tile - 1) / tile;
@@ -547,8 +555,9 @@ topkv_status_t launch_move(bool pack, const topkv_pool_t* pool, int32_t layer, v
   const bool direct = slots <= TOPKV_DIRECT_MAX && bt_stride <= 65535 && reqs <= 65535;
   dim3 grid3;
   unsigned grid = 0;
+  if (layers > 1 && !direct) return TOPKV_ERR_UNSUPPORTED;   // the caller moves one layer per launch instead
   if (direct) {
-    grid3 = dim3((unsigned)per_page, (unsigned)bt_stride, (unsigned)reqs);
+    grid3 = dim3((unsigned)per_page, (unsigned)bt_stride, (unsigned)(seq_lens ? reqs : layers));
     grid = (unsigned)slots;
   } else {
     int cus = 0;
@@ -578,6 +587,8 @@ topkv_status_t launch_move(bool pack, const topkv_pool_t* pool, int32_t layer, v
   p.window = window;
   p.pad_ = 0;
   p.plane_stride = plane_stride;
+  p.layer_bytes = g.layer_bytes;
+  p.layer_stride = layer_stride;
 
   const size_t lds = (seq_lens && !direct) ? sizeof(uint64_t) * kWaves + sizeof(int32_t) * 3 * ((size_t)num_reqs + 1)
                                            : 0;
@@ -601,6 +612,22 @@ int64_t single_bytes(const topkv_pool_t* pool, int32_t n) {
 }
 
 }  // namespace topkv
+
+namespace topkv_internal {
+
+topkv_status_t placed_layers_move(bool pack, const topkv_pool_t* pool, int32_t first_layer, int32_t layers,
+                                  void* packed, int64_t packed_cap, int64_t plane_stride, int64_t layer_stride,
+                                  const int32_t* block_table, int32_t seq_len, hipStream_t stream) {
+  if (!pool || seq_len < 0 || plane_stride <= 0) return TOPKV_ERR_INVALID_ARG;
+  const topkv_launch_t l = {stream, nullptr, nullptr};
+  const int64_t pages = pool->page_size > 0 ? ((int64_t)seq_len + pool->page_size - 1) / pool->page_size : 0;
+  if (pages > INT32_MAX) return TOPKV_ERR_UNSUPPORTED;
+  return topkv::launch_move(pack, pool, first_layer, packed, packed_cap, 1, block_table,
+                            (int32_t)(pages > 0 ? pages : 1), nullptr, seq_len, 0, plane_stride, &l, layers,
+                            layer_stride);
+}
+
+}  // namespace topkv_internal
 
 // ---------------------------------------------------------------------------
 // C ABI

@@ -47,7 +47,7 @@ EXPORTS = ["topkv_pack_layer", "topkv_unpack_layer", "topkv_pack_layer_batched",
            "topkv_pack_layer_heads", "topkv_unpack_layer_heads", "topkv_reblock_layer",
            "topkv_pack_layer_shards", "topkv_unpack_layer_shards", "topkv_packed_state_bytes",
            "topkv_pack_state_layer", "topkv_unpack_state_layer", "topkv_check_state_slots",
-           "topkv_check_state_workspace_bytes"]
+           "topkv_check_state_workspace_bytes", "topkv_kvcache1_pack_layers", "topkv_kvcache1_unpack_layers"]
 
 TOPKV_LAYOUT_PACKED = 0
 TOPKV_LAYOUT_POOL = 1
@@ -107,6 +107,8 @@ _SIGS = {
     "topkv_kvcache1_seal": (_I32, [_POOL, _I32, ctypes.c_uint64, ctypes.c_uint64, _P, _I64, _P, _I64, _P]),
     "topkv_kvcache1_verify": (_I32, [_POOL, _I32, ctypes.c_uint64, ctypes.c_uint64, _P, _I64, _P, _I64, _P, _P]),
     "topkv_kvcache1_unpack_layer": (_I32, [_P, _I64, _POOL, _I32, _P, _I32, _P]),
+    "topkv_kvcache1_pack_layers": (_I32, [_POOL, _I32, _I32, _P, _I32, _P, _I64, _P]),
+    "topkv_kvcache1_unpack_layers": (_I32, [_P, _I64, _POOL, _I32, _I32, _P, _I32, _P]),
     "topkv_crc64": (_I32, [_P, _I64, _P, _I64, _P, _P]),
     "topkv_crc64_workspace_bytes": (_I64, [_I64]),
     "topkv_move_layer": (_I32, [ctypes.POINTER(topkv_view_t), ctypes.POINTER(topkv_view_t), _I32, _P, _I32,
@@ -351,6 +353,20 @@ def topkv_kvcache1_verify(geometry, seq_len, request_id, model_id, blob, workspa
 def topkv_kvcache1_unpack_layer(blob, dst, layer, block_table, seq_len, blob_bytes=None, stream=None) -> None:
     _check(_lib.topkv_kvcache1_unpack_layer(_ptr(blob), _nbytes(blob, blob_bytes), ctypes.byref(_pool_arg(dst)),
                                             int(layer), _table_ptr(block_table), int(seq_len), _stream(stream)))
+
+
+def topkv_kvcache1_pack_layers(src, first_layer, num_layers, block_table, seq_len, blob, blob_bytes=None,
+                               stream=None) -> None:
+    _check(_lib.topkv_kvcache1_pack_layers(ctypes.byref(_pool_arg(src)), int(first_layer), int(num_layers),
+                                           _table_ptr(block_table), int(seq_len), _ptr(blob),
+                                           _nbytes(blob, blob_bytes), _stream(stream)))
+
+
+def topkv_kvcache1_unpack_layers(blob, dst, first_layer, num_layers, block_table, seq_len, blob_bytes=None,
+                                 stream=None) -> None:
+    _check(_lib.topkv_kvcache1_unpack_layers(_ptr(blob), _nbytes(blob, blob_bytes), ctypes.byref(_pool_arg(dst)),
+                                             int(first_layer), int(num_layers), _table_ptr(block_table),
+                                             int(seq_len), _stream(stream)))
 
 
 def topkv_crc64(data, nbytes, workspace, crc_out, workspace_bytes=None, stream=None) -> None:

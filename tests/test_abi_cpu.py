@@ -211,3 +211,17 @@ def test_state_layer_validation(tk):
     _expect(tk, INV, tk.topkv_check_state_slots, st(num_slots=0), 2, slots, res, check_duplicates=False)
     tk.topkv_pack_state_layer(good, 2, 0, 0, 0, dst_bytes=0, stream=0)      # no requests: nothing to launch
     tk.topkv_unpack_state_layer(0, good, 0, 0, 0, src_bytes=0, stream=0)
+
+
+def test_kvcache1_layer_range_validation(tk):
+    """Whole-request KVCACHE1 calls refuse layer ranges outside the pool
+    before any launch; an empty range queues nothing."""
+    INV = tk.TOPKV_ERR_INVALID_ARG
+    good = _pool(tk)                     # 2 layers
+    bt, blob = 0x20000, 0x40000
+    nbytes = tk.topkv_kvcache1_bytes(good, 16)
+    for first, count in ((-1, 1), (0, 3), (1, 2), (2, 1), (0, -1)):
+        _expect(tk, INV, tk.topkv_kvcache1_pack_layers, good, first, count, bt, 16, blob, blob_bytes=nbytes)
+        _expect(tk, INV, tk.topkv_kvcache1_unpack_layers, blob, good, first, count, bt, 16, blob_bytes=nbytes)
+    _expect(tk, INV, tk.topkv_kvcache1_pack_layers, good, 0, 2, bt, 16, blob, blob_bytes=nbytes - 1)
+    tk.topkv_kvcache1_pack_layers(good, 1, 0, bt, 16, blob, blob_bytes=nbytes, stream=0)

@@ -43,22 +43,29 @@ def test_device_crc64(tk, n):
         assert got == 0x995DC9BBDF1939FA
 
 
-def _blob_run(tk, wl, src, dst, r, rid=0x1234, mid=0x77):
-    """Serialize request r from src, verify, unpack into dst; returns the blob."""
+def _blob_run(tk, wl, src, dst, r, rid=0x1234, mid=0x77, whole=False):
+    """Serialize request r from src, verify, unpack into dst; returns the blob.
+    whole: every layer in one call (topkv_kvcache1_pack_layers / unpack_layers)."""
     n = int(wl.seq_lens[r])
     geo = tk.pool_from_tensor(src)
     nbytes = tk.topkv_kvcache1_bytes(geo, n)
     blob = torch.full((nbytes,), 0xAB, dtype=torch.uint8, device="cuda")
     ws = torch.empty(tk.topkv_kvcache1_workspace_bytes(geo, n) // 8, dtype=torch.int64, device="cuda")
     bt = to_dev(wl.block_tables[r])
-    for layer in range(wl.num_layers):
-        tk.topkv_kvcache1_pack_layer(src, layer, bt, n, blob)
+    if whole:
+        tk.topkv_kvcache1_pack_layers(src, 0, wl.num_layers, bt, n, blob)
+    else:
+        for layer in range(wl.num_layers):
+            tk.topkv_kvcache1_pack_layer(src, layer, bt, n, blob)
     tk.topkv_kvcache1_seal(geo, n, rid, mid, blob, ws)
     res = torch.full((4,), 99, dtype=torch.int32, device="cuda")
     tk.topkv_kvcache1_verify(geo, n, rid, mid, blob, ws, res)
     bt2 = to_dev(wl.dst_block_tables[r])
-    for layer in range(wl.num_layers):
-        tk.topkv_kvcache1_unpack_layer(blob, dst, layer, bt2, n)
+    if whole:
+        tk.topkv_kvcache1_unpack_layers(blob, dst, 0, wl.num_layers, bt2, n)
+    else:
+        for layer in range(wl.num_layers):
+            tk.topkv_kvcache1_unpack_layer(blob, dst, layer, bt2, n)
     torch.cuda.synchronize()
     assert res.cpu().tolist() == [tk.TOPKV_OK, 0, 0, 0]
     return blob, ws
@@ -117,7 +124,7 @@ def test_kvcache1_fullsize_70b(tk):
     say(f"[kvcache1] full size: {wl.describe()}")
     src, dst = device_src_pool(wl), device_dst_prefill(wl)
     n = int(wl.seq_lens[0])
-    blob, ws = _blob_run(tk, wl, src, dst, 0, rid=42, mid=70)
+    blob, ws = _blob_run(tk, wl, src, dst, 0, rid=42, mid=70, whole=True)   # all 80 layers in one launch
     assert blob.numel() == 128 + 1_342_177_280
     hdr = okv.parse_header(blob[:128].cpu().numpy().tobytes())
     body = blob[128:].cpu().numpy()
@@ -134,3 +141,43 @@ def test_kvcache1_fullsize_70b(tk):
         assert np.array_equal(again, want), f"layer {layer}: unpacked pool does not hold the request"
     del src, dst, blob
     torch.cuda.empty_cache()
+
+
+@pytest.mark.parametrize("case", ["tiny", "mla", "reblock"])
+def test_kvcache1_layer_ranges(tk, case):
+    """Several layers per call (the whole request, or split ranges) give the
+    same blob and the same destination pool as one call per layer."""
+    if case == "tiny":
+        wl = make_workload("tiny", dst_page_size=48)
+    elif case == "mla":
+        wl = make_workload("deepseek-v3-mla", num_layers=3, seq_lens=[700, 1, 64, 129])
+    else:
+        wl = make_workload("reblock-70b", num_layers=3, phys_layers=3, seq_lens=[300, 17, 4096])
+    say(f"[kvcache1] layer ranges {case}")
+    src = to_dev(host_src_pool(wl))
+    dst0 = to_dev(host_dst_prefill(wl))
+    geo = tk.pool_from_tensor(src)
+    L = wl.num_layers
+    for r in range(wl.num_reqs):
+        n = int(wl.seq_lens[r])
+        nbytes = tk.topkv_kvcache1_bytes(geo, n)
+        bt, bt2 = to_dev(wl.block_tables[r]), to_dev(wl.dst_block_tables[r])
+        ref = torch.full((nbytes,), 0xAB, dtype=torch.uint8, device="cuda")
+        for layer in range(L):
+            tk.topkv_kvcache1_pack_layer(src, layer, bt, n, ref)
+        ref_dst = dst0.clone()
+        for layer in range(L):
+            tk.topkv_kvcache1_unpack_layer(ref, ref_dst, layer, bt2, n)
+        for ranges in ([(0, L)], [(0, 1), (1, L - 1)], [(L - 1, 1), (0, L - 1)], [(0, 0), (0, L)]):
+            blob = torch.full((nbytes,), 0xAB, dtype=torch.uint8, device="cuda")
+            for first, count in ranges:
+                tk.topkv_kvcache1_pack_layers(src, first, count, bt, n, blob)
+            got_dst = dst0.clone()
+            for first, count in ranges:
+                tk.topkv_kvcache1_unpack_layers(ref, got_dst, first, count, bt2, n)
+            torch.cuda.synchronize()
+            assert torch.equal(blob, ref), f"{case} request {r} ranges {ranges}: blob differs"
+            assert torch.equal(got_dst.view(torch.int16), ref_dst.view(torch.int16)), \
+                f"{case} request {r} ranges {ranges}: pool differs"
+    with pytest.raises(tk.TopkvError):
+        tk.topkv_kvcache1_pack_layers(src, 1, L, to_dev(wl.block_tables[0]), int(wl.seq_lens[0]), blob)
