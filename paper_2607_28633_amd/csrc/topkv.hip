@@ -43,7 +43,10 @@
 #define TOPKV_WG_PER_CU 8     // persistent grid cap = CUs * this
 #endif
 #ifndef TOPKV_DIRECT_MAX
-#define TOPKV_DIRECT_MAX 65536  // largest one-shot direct-mapped grid (slots)
+#define TOPKV_DIRECT_MAX (1 << 20)  // largest one-shot direct-mapped grid (slots)
+#endif
+#ifndef TOPKV_DIRECT_MAX_REQS
+#define TOPKV_DIRECT_MAX_REQS 1024  // direct grid: each slot sums the lengths of the requests before its own
 #endif
 #ifndef TOPKV_NONTEMPORAL
 #define TOPKV_NONTEMPORAL 1   // streaming hint on the bulk loads and stores
@@ -552,7 +555,7 @@ topkv_status_t launch_move(bool pack, const topkv_pool_t* pool, int32_t layer, v
   // get its own workgroup; otherwise a persistent grid over the live items.
   const int64_t reqs = seq_lens ? (int64_t)num_reqs : 1;
   const int64_t slots = reqs * bt_stride * per_page;
-  const bool direct = slots <= TOPKV_DIRECT_MAX && bt_stride <= 65535 && reqs <= 65535;
+  const bool direct = slots <= TOPKV_DIRECT_MAX && bt_stride <= 65535 && reqs <= TOPKV_DIRECT_MAX_REQS;
   dim3 grid3;
   unsigned grid = 0;
   if (layers > 1 && !direct) return TOPKV_ERR_UNSUPPORTED;   // the caller moves one layer per launch instead

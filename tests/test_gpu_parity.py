@@ -304,3 +304,36 @@ def test_one_request_misaligned_packed(tk, offset):
     torch.cuda.synchronize()
     oracle.unpack_layer(want, dst_h, layer, bt2, np.array([n], np.int32))
     assert np.array_equal(to_host(dst), dst_h)
+
+
+def _persistent_case(kind):
+    rng = np.random.default_rng(21 if kind == "many-requests" else 22)
+    if kind == "many-requests":             # more requests than one direct grid takes
+        lens = rng.integers(0, 41, size=1100)
+    else:                                   # more than 2^20 (request, entry, plane) slots: 600 x 1000 x 2
+        lens = np.concatenate([[16000], rng.integers(0, 21, size=599)])
+    return make_workload("tiny", num_layers=1, seq_lens=lens.astype(np.int32))
+
+
+@pytest.mark.parametrize("kind", ["many-requests", "many-slots"])
+@pytest.mark.parametrize("window", [0, 7])
+def test_persistent_grid(tk, kind, window):
+    """Batches beyond the direct grid's limits run the persistent grid (length
+    scan, request search); pack and unpack, with and without a window, equal
+    the oracle."""
+    wl = _persistent_case(kind)
+    say(f"[persistent] {kind}: {wl.num_reqs} requests, table width {wl.block_tables.shape[1]}, window {window}")
+    src_h, dst_h = host_src_pool(wl), host_dst_prefill(wl)
+    src, dst = to_dev(src_h), to_dev(dst_h)
+    bt, bt2, lens = to_dev(wl.block_tables), to_dev(wl.dst_block_tables), to_dev(wl.seq_lens)
+    n = oracle.packed_layer_elems(wl.planes, wl.num_heads, wl.head_dim, wl.seq_lens, window)
+    packed = torch.full((n + 64,), 0x1357, dtype=torch.int16, device="cuda")
+    tk.topkv_pack_layer_window(src, 0, wl.num_reqs, bt, bt.shape[1], lens, window, packed, dst_bytes=2 * n)
+    tk.topkv_unpack_layer_window(packed, dst, 0, wl.num_reqs, bt2, bt2.shape[1], lens, window, src_bytes=2 * n)
+    torch.cuda.synchronize()
+    want = oracle.pack_layer(src_h, 0, wl.block_tables, wl.seq_lens, window=window)
+    got = to_host(packed)
+    assert np.array_equal(got[:n], want), f"{kind} window {window}: pack differs"
+    assert (got[n:] == 0x1357).all(), "write past the batch"
+    oracle.unpack_layer(want, dst_h, 0, wl.dst_block_tables, wl.seq_lens, window=window)
+    assert np.array_equal(to_host(dst), dst_h), f"{kind} window {window}: unpack differs"
