@@ -45,6 +45,9 @@ namespace topkv_reshard {
 #ifndef TOPKV_RS_SINGLE
 #define TOPKV_RS_SINGLE 1         // direct grid for one request without a window
 #endif
+#ifndef TOPKV_RS_DIRECT
+#define TOPKV_RS_DIRECT 1          // batches without a window take the direct grid when it fits
+#endif
 #ifndef TOPKV_RS_WG_PER_CU
 #define TOPKV_RS_WG_PER_CU 16     // grid cap = CUs * this
 #endif
@@ -312,35 +315,55 @@ __global__ __launch_bounds__(kThreads) void kv_reshard_kernel(Params p, const in
   }
 }
 
-// One request, no window, wave-uniform tokens (every 70B-class shape):
-// workgroup (x, y) copies tile x of plane y.  A token's page depends only on
-// the token, not on the request's length, so each wave's first page lookups
-// go out together with the length load; there is no prefix scan.  Pieces of
-// tokens at or past the (clamped) length are skipped.
-template <int VB>
-__global__ __launch_bounds__(kThreads) void kv_reshard_single_kernel(Params p,
-                                                                    const int32_t* __restrict__ seq_lens) {
+// Kept tokens (window 0) of requests [0, r): the (plane, token) offset of
+// request r in the packed order is planes times this.  Each wave sums the
+// lengths on its own (lanes stride over them, then a butterfly), so no LDS and
+// no barrier are involved.
+__device__ __forceinline__ int32_t kept_before(const int32_t* __restrict__ seq_lens, int32_t r, int32_t max_tok) {
+  int32_t s = 0;
+  for (int j = threadIdx.x & 63; j < r; j += 64) {
+    int32_t n = seq_lens[j];
+    s += n < 0 ? 0 : (n > max_tok ? max_tok : n);
+  }
+#pragma unroll
+  for (int off = 32; off > 0; off >>= 1) s += __shfl_xor(s, off, 64);
+  return __builtin_amdgcn_readfirstlane(s);
+}
+
+// Direct grid without a window, wave-uniform tokens (every 70B-class shape):
+// workgroup (x, y[, z]) copies tile x of plane y [of request z], in packed
+// order.  A token's page depends only on the token, not on the request's
+// length, so each wave's first page lookups go out together with the length
+// load; there is no prefix scan.  Pieces of tokens at or past the (clamped)
+// length are skipped.  kBatch: requests on grid z, each at the (plane, token)
+// offset of the lengths before it, and tiles past a request's length exit at
+// once; otherwise one request.
+template <int VB, bool kBatch>
+__device__ __forceinline__ void direct_move(const Params& p, const int32_t* __restrict__ seq_lens) {
   typedef typename Vec<VB>::type V;
   constexpr uint32_t kTile = (uint32_t)kThreads * kVpt;
   const uint32_t per_tp = p.ktp.d;
   const uint32_t lane = threadIdx.x & 63u;
   const uint32_t wave_first = __builtin_amdgcn_readfirstlane(threadIdx.x & ~63u);
   const uint32_t c = blockIdx.y;
+  const int32_t r = kBatch ? (int32_t)blockIdx.z : 0;
   const uint32_t base = blockIdx.x * kTile;
   PageCache src_pc, dst_pc;
   {
     // the first span's token is known before the length: prime the page caches
     const uint32_t t0 = fdiv(base + wave_first, p.ktp);
     if (t0 < (uint32_t)p.max_tok) {
-      const Loc at0{0, c, t0};
+      const Loc at0{r, c, t0};
       int64_t unused;
       if (!p.src.packed) pool_offset_wave(p.src, at0, 0, 0, src_pc, &unused);
       if (!p.dst.packed) pool_offset_wave(p.dst, at0, 0, 0, dst_pc, &unused);
     }
   }
-  int32_t n = __builtin_amdgcn_readfirstlane(seq_lens[0]);
+  int32_t n = __builtin_amdgcn_readfirstlane(seq_lens[r]);
   n = n < 0 ? 0 : (n > p.max_tok ? p.max_tok : n);
   const uint32_t end = (uint32_t)n * per_tp;                  // pieces of this plane
+  if (kBatch && base >= end) return;                          // past this request's tokens
+  const uint32_t q0 = (kBatch && r > 0) ? (uint32_t)(p.planes * kept_before(seq_lens, r, p.max_tok)) : 0u;
   // Each load issues as soon as its address is known (there is no loop here
   // to hold it up); a skipped piece loads the source base and is not stored.
   V v[kVpt];
@@ -357,8 +380,8 @@ __global__ __launch_bounds__(kThreads) void kv_reshard_single_kernel(Params p,
       const uint32_t m = wbase - t * per_tp + lane;
       const uint32_t k = fdiv(m, p.vpg);
       const uint32_t e = m - k * p.vpg.d;
-      const Loc at{0, c, t};
-      const uint32_t q2 = c * (uint32_t)n + t;                  // global (plane, token) index
+      const Loc at{r, c, t};
+      const uint32_t q2 = q0 + c * (uint32_t)n + t;             // global (request, plane, token) index
       int64_t so = 0, o = 0;
       const bool s_ok = p.src.packed ? packed_offset<VB>(p, q2, k, e, &so)
                                      : pool_offset_wave(p.src, at, k, e * VB, src_pc, &so);
@@ -373,6 +396,18 @@ __global__ __launch_bounds__(kThreads) void kv_reshard_single_kernel(Params p,
 #pragma unroll
   for (int j = 0; j < kVpt; ++j)
     if (ok[j]) __builtin_nontemporal_store(v[j], reinterpret_cast<V*>(p.dst.base + doff[j]));
+}
+
+template <int VB>
+__global__ __launch_bounds__(kThreads) void kv_reshard_single_kernel(Params p,
+                                                                    const int32_t* __restrict__ seq_lens) {
+  direct_move<VB, false>(p, seq_lens);
+}
+
+template <int VB>
+__global__ __launch_bounds__(kThreads) void kv_reshard_direct_kernel(Params p,
+                                                                    const int32_t* __restrict__ seq_lens) {
+  direct_move<VB, true>(p, seq_lens);
 }
 
 // ---------------------------------------------------------------------------
@@ -454,6 +489,16 @@ KernelFn single_kernel_for(int vb) {
     case 4: return kv_reshard_single_kernel<4>;
     case 2: return kv_reshard_single_kernel<2>;
     default: return kv_reshard_single_kernel<1>;
+  }
+}
+
+KernelFn direct_kernel_for(int vb) {
+  switch (vb) {
+    case 16: return kv_reshard_direct_kernel<16>;
+    case 8: return kv_reshard_direct_kernel<8>;
+    case 4: return kv_reshard_direct_kernel<4>;
+    case 2: return kv_reshard_direct_kernel<2>;
+    default: return kv_reshard_direct_kernel<1>;
   }
 }
 
@@ -571,10 +616,16 @@ topkv_status_t move_layer_impl(const topkv_view_t* src, const topkv_view_t* dst,
   const int64_t plane_tiles = (max_tok * gpt * vpg + tile - 1) / tile;
   const bool single = TOPKV_RS_SINGLE && num_reqs == 1 && window == 0 && wave && plane_tiles <= INT32_MAX &&
                       geo->planes <= 65535;
+  // a batch without a window: the same direct grid with requests on z, while it stays within
+  // 2^20 workgroups and 1024 requests (each workgroup sums the lengths before its request)
+  const bool direct = !single && TOPKV_RS_DIRECT && num_reqs > 1 && num_reqs <= 1024 && window == 0 && wave &&
+                      geo->planes <= 65535 && plane_tiles * geo->planes * num_reqs <= ((int64_t)1 << 20);
   if (single_only && !single) return TOPKV_OK;
-  const dim3 grid = single ? dim3((unsigned)plane_tiles, (unsigned)geo->planes) : dim3((unsigned)blocks);
-  const KernelFn fn = single ? single_kernel_for(vb) : kernel_for(vb, wave);
-  const size_t shmem = single ? 0 : lds;
+  const dim3 grid = single   ? dim3((unsigned)plane_tiles, (unsigned)geo->planes)
+                    : direct ? dim3((unsigned)plane_tiles, (unsigned)geo->planes, (unsigned)num_reqs)
+                             : dim3((unsigned)blocks);
+  const KernelFn fn = single ? single_kernel_for(vb) : direct ? direct_kernel_for(vb) : kernel_for(vb, wave);
+  const size_t shmem = (single || direct) ? 0 : lds;
   if (launch.start || launch.stop)
     hipExtLaunchKernelGGL(fn, grid, dim3(kThreads), shmem, launch.stream, launch.start, launch.stop, 0, p, seq_lens);
   else
