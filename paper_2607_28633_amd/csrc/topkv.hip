@@ -45,6 +45,9 @@
 #ifndef TOPKV_DIRECT_MAX
 #define TOPKV_DIRECT_MAX (1 << 20)  // largest one-shot direct-mapped grid (slots)
 #endif
+#ifndef TOPKV_WINDOW_PERSISTENT
+#define TOPKV_WINDOW_PERSISTENT 1   // windows that keep a small share of the table take the persistent grid
+#endif
 #ifndef TOPKV_DIRECT_MAX_REQS
 #define TOPKV_DIRECT_MAX_REQS 1024  // direct grid: each slot sums the lengths of the requests before its own
 #endif
@@ -555,7 +558,12 @@ topkv_status_t launch_move(bool pack, const topkv_pool_t* pool, int32_t layer, v
   // get its own workgroup; otherwise a persistent grid over the live items.
   const int64_t reqs = seq_lens ? (int64_t)num_reqs : 1;
   const int64_t slots = reqs * bt_stride * per_page;
-  const bool direct = slots <= TOPKV_DIRECT_MAX && bt_stride <= 65535 && reqs <= TOPKV_DIRECT_MAX_REQS;
+  // A window keeps at most ceil(window / P) + 1 pages of each request; when that is a small share of
+  // the table, a direct grid would be mostly slots that exit at once, so the persistent grid (which
+  // visits live items only) takes the launch.
+  const int64_t win_pages = window > 0 ? ((int64_t)window + pool->page_size - 1) / pool->page_size + 1 : bt_stride;
+  const bool sparse = TOPKV_WINDOW_PERSISTENT && seq_lens && win_pages * 4 <= bt_stride;
+  const bool direct = !sparse && slots <= TOPKV_DIRECT_MAX && bt_stride <= 65535 && reqs <= TOPKV_DIRECT_MAX_REQS;
   dim3 grid3;
   unsigned grid = 0;
   if (layers > 1 && !direct) return TOPKV_ERR_UNSUPPORTED;   // the caller moves one layer per launch instead
