@@ -7,16 +7,18 @@
 namespace topkv_internal {
 
 // A plain pack (pool -> packed, every head) or unpack (packed -> pool) of one
-// request with a device length and no window, run by the layout-move
-// kernel's one-request direct grid when that grid applies (a token's pieces
-// fill whole wave spans).  *launched tells whether it launched; when it did
-// not, nothing was queued and the caller launches its own kernel.  The caller
-// has validated the arguments; `launch` carries the stream and the optional
-// start/stop events.
+// request with no window, run by the layout-move kernel's one-request direct
+// grid when that grid applies (a token's pieces fill whole wave spans).  The
+// length is the device value seq_lens[0], or seq_len (>= 0) when seq_lens is
+// null.  *launched tells whether it launched; when it did not, nothing was
+// queued and the caller launches its own kernel.  The caller has validated
+// the arguments; `launch` carries the stream and the optional start/stop
+// events.
 __attribute__((visibility("hidden")))
 topkv_status_t single_request_move(bool pack, const topkv_pool_t* pool, int32_t layer, void* packed,
                                    int64_t packed_cap, const int32_t* tables, int32_t bt_stride,
-                                   const int32_t* seq_lens, const topkv_launch_t* launch, bool* launched);
+                                   const int32_t* seq_lens, int32_t seq_len, const topkv_launch_t* launch,
+                                   bool* launched);
 
 // One request with caller-placed planes, layers [first_layer, first_layer +
 // layers) in one launch: plane c of layer first_layer + z is at packed +

@@ -108,6 +108,8 @@ struct Params {
   int32_t planes;
   int32_t window;
   int32_t max_tok;          // lengths are clamped to [0, max_tok]
+  int32_t n_host;           // one request with a host-side length: its tokens (else unused)
+  int32_t pad_;
 };
 
 // Per-request kept-token counts and first kept tokens, and the exclusive
@@ -337,8 +339,9 @@ __device__ __forceinline__ int32_t kept_before(const int32_t* __restrict__ seq_l
 // load; there is no prefix scan.  Pieces of tokens at or past the (clamped)
 // length are skipped.  kBatch: requests on grid z, each at the (plane, token)
 // offset of the lengths before it, and tiles past a request's length exit at
-// once; otherwise one request.
-template <int VB, bool kBatch>
+// once; otherwise one request.  kHostLen: the one request's length is the
+// launch constant n_host instead of a device value.
+template <int VB, bool kBatch, bool kHostLen = false>
 __device__ __forceinline__ void direct_move(const Params& p, const int32_t* __restrict__ seq_lens) {
   typedef typename Vec<VB>::type V;
   constexpr uint32_t kTile = (uint32_t)kThreads * kVpt;
@@ -359,7 +362,7 @@ __device__ __forceinline__ void direct_move(const Params& p, const int32_t* __re
       if (!p.dst.packed) pool_offset_wave(p.dst, at0, 0, 0, dst_pc, &unused);
     }
   }
-  int32_t n = __builtin_amdgcn_readfirstlane(seq_lens[r]);
+  int32_t n = kHostLen ? p.n_host : __builtin_amdgcn_readfirstlane(seq_lens[r]);
   n = n < 0 ? 0 : (n > p.max_tok ? p.max_tok : n);
   const uint32_t end = (uint32_t)n * per_tp;                  // pieces of this plane
   if (kBatch && base >= end) return;                          // past this request's tokens
@@ -398,10 +401,10 @@ __device__ __forceinline__ void direct_move(const Params& p, const int32_t* __re
     if (ok[j]) __builtin_nontemporal_store(v[j], reinterpret_cast<V*>(p.dst.base + doff[j]));
 }
 
-template <int VB>
+template <int VB, bool kHostLen>
 __global__ __launch_bounds__(kThreads) void kv_reshard_single_kernel(Params p,
                                                                     const int32_t* __restrict__ seq_lens) {
-  direct_move<VB, false>(p, seq_lens);
+  direct_move<VB, false, kHostLen>(p, seq_lens);
 }
 
 template <int VB>
@@ -482,13 +485,14 @@ KernelFn kernel_for_mode(int vb) {
 
 KernelFn kernel_for(int vb, bool wave) { return wave ? kernel_for_mode<true>(vb) : kernel_for_mode<false>(vb); }
 
+template <bool kHostLen>
 KernelFn single_kernel_for(int vb) {
   switch (vb) {
-    case 16: return kv_reshard_single_kernel<16>;
-    case 8: return kv_reshard_single_kernel<8>;
-    case 4: return kv_reshard_single_kernel<4>;
-    case 2: return kv_reshard_single_kernel<2>;
-    default: return kv_reshard_single_kernel<1>;
+    case 16: return kv_reshard_single_kernel<16, kHostLen>;
+    case 8: return kv_reshard_single_kernel<8, kHostLen>;
+    case 4: return kv_reshard_single_kernel<4, kHostLen>;
+    case 2: return kv_reshard_single_kernel<2, kHostLen>;
+    default: return kv_reshard_single_kernel<1, kHostLen>;
   }
 }
 
@@ -506,11 +510,16 @@ KernelFn direct_kernel_for(int vb) {
 // did through *launched); otherwise whichever grid applies.
 topkv_status_t move_layer_impl(const topkv_view_t* src, const topkv_view_t* dst, int32_t num_reqs,
                                const int32_t* seq_lens, int32_t head_count, int32_t window,
-                               const topkv_launch_t& launch, bool single_only, bool* launched) {
+                               const topkv_launch_t& launch, bool single_only, bool* launched,
+                               int32_t n_host = -1) {
   *launched = false;
   if (!src || !dst || !valid_layout(src->layout) || !valid_layout(dst->layout)) return TOPKV_ERR_INVALID_ARG;
   if (src->layout == TOPKV_LAYOUT_PACKED && dst->layout == TOPKV_LAYOUT_PACKED) return TOPKV_ERR_INVALID_ARG;
-  if (num_reqs < 0 || head_count <= 0 || window < 0 || (num_reqs > 0 && !seq_lens)) return TOPKV_ERR_INVALID_ARG;
+  // a host-side length (n_host >= 0) stands for seq_lens: one request, one-request grid only
+  const bool host_len = n_host >= 0;
+  if (host_len && (num_reqs != 1 || !single_only || seq_lens)) return TOPKV_ERR_INVALID_ARG;
+  if (num_reqs < 0 || head_count <= 0 || window < 0 || (num_reqs > 0 && !seq_lens && !host_len))
+    return TOPKV_ERR_INVALID_ARG;
   if (num_reqs > TOPKV_MAX_BATCH_REQS) return TOPKV_ERR_UNSUPPORTED;
 
   const topkv_view_t* sides[2] = {src, dst};
@@ -603,6 +612,7 @@ topkv_status_t move_layer_impl(const topkv_view_t* src, const topkv_view_t* dst,
   p.planes = geo->planes;
   p.window = window;
   p.max_tok = (int32_t)max_tok;
+  p.n_host = host_len ? (n_host < max_tok ? n_host : (int32_t)max_tok) : 0;
 
   int cus = 0;
   const topkv_status_t st = cu_count(&cus);
@@ -613,7 +623,9 @@ topkv_status_t move_layer_impl(const topkv_view_t* src, const topkv_view_t* dst,
   if (blocks < 1) blocks = 1;
   const size_t lds = sizeof(int32_t) * (kWaves + 3 * (size_t)num_reqs + 1);
   const bool wave = (gpt * vpg) % 64 == 0;
-  const int64_t plane_tiles = (max_tok * gpt * vpg + tile - 1) / tile;
+  // a host-side length sizes the grid exactly; a device one by the table's capacity
+  const int64_t grid_tok = host_len ? p.n_host : max_tok;
+  const int64_t plane_tiles = (grid_tok * gpt * vpg + tile - 1) / tile;
   const bool single = TOPKV_RS_SINGLE && num_reqs == 1 && window == 0 && wave && plane_tiles <= INT32_MAX &&
                       geo->planes <= 65535;
   // a batch without a window: the same direct grid with requests on z, while it stays within
@@ -624,7 +636,10 @@ topkv_status_t move_layer_impl(const topkv_view_t* src, const topkv_view_t* dst,
   const dim3 grid = single   ? dim3((unsigned)plane_tiles, (unsigned)geo->planes)
                     : direct ? dim3((unsigned)plane_tiles, (unsigned)geo->planes, (unsigned)num_reqs)
                              : dim3((unsigned)blocks);
-  const KernelFn fn = single ? single_kernel_for(vb) : direct ? direct_kernel_for(vb) : kernel_for(vb, wave);
+  if (plane_tiles == 0) return TOPKV_OK;   // a host-side length of 0: nothing to move
+  const KernelFn fn = single   ? (host_len ? single_kernel_for<true>(vb) : single_kernel_for<false>(vb))
+                      : direct ? direct_kernel_for(vb)
+                               : kernel_for(vb, wave);
   const size_t shmem = (single || direct) ? 0 : lds;
   if (launch.start || launch.stop)
     hipExtLaunchKernelGGL(fn, grid, dim3(kThreads), shmem, launch.stream, launch.start, launch.stop, 0, p, seq_lens);
@@ -671,12 +686,15 @@ namespace topkv_internal {
 
 topkv_status_t single_request_move(bool pack, const topkv_pool_t* pool, int32_t layer, void* packed,
                                    int64_t packed_cap, const int32_t* tables, int32_t bt_stride,
-                                   const int32_t* seq_lens, const topkv_launch_t* launch, bool* launched) {
+                                   const int32_t* seq_lens, int32_t seq_len, const topkv_launch_t* launch,
+                                   bool* launched) {
   *launched = false;
   const topkv_view_t pv = pool_view(TOPKV_LAYOUT_POOL, pool, layer, tables, bt_stride, 0);
   const topkv_view_t kv = packed_view(packed, packed_cap, 1);
-  const topkv_status_t st = pack ? move_layer_impl(&pv, &kv, 1, seq_lens, pool->num_heads, 0, *launch, true, launched)
-                                 : move_layer_impl(&kv, &pv, 1, seq_lens, pool->num_heads, 0, *launch, true, launched);
+  const int32_t n_host = seq_lens ? -1 : seq_len;
+  const topkv_status_t st =
+      pack ? move_layer_impl(&pv, &kv, 1, seq_lens, pool->num_heads, 0, *launch, true, launched, n_host)
+           : move_layer_impl(&kv, &pv, 1, seq_lens, pool->num_heads, 0, *launch, true, launched, n_host);
   // anything this path does not take (limits, shapes) goes back to the caller's kernel
   if (st == TOPKV_ERR_INVALID_ARG || st == TOPKV_ERR_UNSUPPORTED || st == TOPKV_ERR_BOUNDS) {
     *launched = false;

@@ -523,16 +523,21 @@ topkv_status_t launch_move(bool pack, const topkv_pool_t* pool, int32_t layer, v
   if (num_reqs == 0 || (!seq_lens && n_single == 0)) return TOPKV_OK;  // nothing to move
   if (!tables || !packed || bt_stride <= 0) return TOPKV_ERR_INVALID_ARG;
 
-  // One request with a device length, every token kept and the packed
-  // buffer large enough for the whole table: the layout-move kernel's
-  // one-request grid does the same copy with less index work per piece.
-  int64_t full_bound;
-  if (TOPKV_ROUTE_SINGLE && seq_lens && num_reqs == 1 && window == 0 && plane_stride == 0 &&
-      !__builtin_mul_overflow((int64_t)pool->planes * bt_stride * pool->page_size, g.row_bytes, &full_bound) &&
-      packed_cap >= full_bound) {
+  // One request, every token kept, planes in the packed order: the
+  // layout-move kernel's one-request grid does the same copy with less index
+  // work per piece.  A device length needs a packed buffer large enough for
+  // the whole table (that grid skips pieces past the buffer's end, where this
+  // kernel leaves an overrunning request unmoved); a host length is checked
+  // against the buffer here.
+  const int64_t route_tok = seq_lens ? (int64_t)bt_stride * pool->page_size : n_single;
+  int64_t route_rows, route_bytes;
+  const bool fits = !__builtin_mul_overflow((int64_t)pool->planes, route_tok, &route_rows) &&
+                    !__builtin_mul_overflow(route_rows, g.row_bytes, &route_bytes) && route_bytes <= packed_cap &&
+                    route_tok <= (int64_t)bt_stride * pool->page_size;
+  if (TOPKV_ROUTE_SINGLE && num_reqs == 1 && window == 0 && plane_stride == 0 && layers == 1 && fits) {
     bool launched = false;
     st = topkv_internal::single_request_move(pack, pool, layer, packed, packed_cap, tables, bt_stride, seq_lens,
-                                             launch, &launched);
+                                             n_single, launch, &launched);
     if (st != TOPKV_OK || launched) return st;
   }
 

@@ -61,6 +61,45 @@ def test_fullsize(tk, name):
     torch.cuda.empty_cache()
 
 
+@pytest.mark.parametrize("name", ["llama3-70b-4k", "llama3-8b"])
+def test_fullsize_host_length(tk, name):
+    """The one-request workloads through topkv_pack_layer / topkv_unpack_layer
+    (host-side length, tables cut to the request's pages): every layer round
+    trips through the destination pool, sampled layers equal the oracle."""
+    wl = make_workload(name)
+    say(f"[fullsize_host] {name}: {wl.describe()}")
+    src = device_src_pool(wl)
+    dst = device_dst_prefill(wl)
+    n = int(wl.seq_lens[0])
+    k, k2 = -(-n // wl.page_size), -(-n // wl.dst_page_size)
+    bt, bt2 = to_dev(wl.block_tables[0, :k]), to_dev(wl.dst_block_tables[0, :k2])
+    nbytes = tk.topkv_packed_layer_bytes(src, [n])
+    packed = torch.empty(nbytes // 2, dtype=torch.int16, device="cuda")
+    again = torch.empty_like(packed)
+    sample = {0, wl.num_layers - 1}
+    for layer in range(wl.num_layers):
+        slab = layer % wl.phys_layers
+        if layer in sample:
+            torch.cuda.synchronize()
+            src_h = to_host(src[slab])[None]
+            dst_before = to_host(dst[slab])[None]
+        tk.topkv_pack_layer(src, slab, bt, n, packed)
+        tk.topkv_unpack_layer(packed, dst, slab, bt2, n)
+        tk.topkv_pack_layer(dst, slab, bt2, n, again)
+        assert torch.equal(packed, again), f"{name} layer {layer}: round trip through the destination differs"
+        if layer in sample:
+            want = oracle.pack_layer(src_h, 0, wl.block_tables, wl.seq_lens)
+            assert np.array_equal(to_host(packed), want), f"{name} layer {layer}: pack differs from oracle"
+            oracle.unpack_layer(want, dst_before, 0, wl.dst_block_tables, wl.seq_lens)
+            assert np.array_equal(to_host(dst[slab]), dst_before[0]), \
+                f"{name} layer {layer}: unpacked slab differs from oracle"
+            say(f"  layer {layer} (slab {slab}) bit-exact vs oracle, {nbytes} B")
+            del src_h, dst_before, want
+    torch.cuda.synchronize()
+    del src, dst, packed, again
+    torch.cuda.empty_cache()
+
+
 def test_fullsize_hybrid(tk):
     """The hybrid model at full size (60 layers, 45 fixed-state, 32 requests):
     every layer round-trips through the destination side with the call its

@@ -277,6 +277,49 @@ def test_one_request_device_length(tk, n):
         assert np.array_equal(to_host(dst), want_dst), f"n={n} cap={cap}: unpack differs"
 
 
+@pytest.mark.parametrize("n,P2", [(117, 16), (117, 64), (128, 16), (1, 16)])
+def test_one_request_host_length_hostile(tk, n, P2):
+    """topkv_pack_layer / topkv_unpack_layer (host length) through tables with
+    out-of-range entries: pack leaves those pages' rows of the packed buffer
+    alone, unpack reads the packed rows but writes nothing for a bad
+    destination page; every other row moves."""
+    P, NP, layer = 16, 40, 1
+    wl = make_workload("tiny", seed=13, num_heads=4, head_dim=128, seq_lens=[n], num_pages=NP,
+                       dst_page_size=P2, dst_num_pages=NP)
+    C, H, D = wl.planes, wl.num_heads, wl.head_dim
+    k, k2 = -(-n // P), -(-n // P2)
+    rng = np.random.default_rng(n + P2)
+    good, good2 = rng.permutation(NP)[:k].astype(np.int32), rng.permutation(NP)[:k2].astype(np.int32)
+    bad, bad2 = good.copy(), good2.copy()
+    bad[k // 2] = -1 if k > 1 else NP
+    bad2[-1] = NP + 3
+    src_h, dst_h = host_src_pool(wl), host_dst_prefill(wl)
+    src, dst = to_dev(src_h), to_dev(dst_h)
+    say(f"[one_request_host] n={n} P'={P2}")
+    sentinel = 0x4D4D
+    nwords = C * n * H * D
+    packed = torch.full((nwords,), sentinel, dtype=torch.int16, device="cuda")
+    tk.topkv_pack_layer(src, layer, to_dev(bad), n, packed)
+    torch.cuda.synchronize()
+    want = oracle.pack_layer(src_h, layer, good[None], np.array([n], np.int32)).copy()
+    blk = want.reshape(C, n, H * D)
+    i = k // 2
+    blk[:, i * P:min(n, (i + 1) * P)] = sentinel
+    assert np.array_equal(to_host(packed).view(np.uint16), want), f"n={n}: pack differs"
+
+    full = oracle.pack_layer(src_h, layer, good[None], np.array([n], np.int32))
+    tk.topkv_unpack_layer(to_dev(full), dst, layer, to_dev(bad2), n)
+    torch.cuda.synchronize()
+    want_dst = dst_h.copy()
+    spare = [p for p in range(NP) if p not in set(good2.tolist())][0]
+    tbl = good2.copy()
+    tbl[-1] = spare
+    keep = want_dst[layer, spare].copy()
+    oracle.unpack_layer(full, want_dst, layer, tbl[None], np.array([n], np.int32))
+    want_dst[layer, spare] = keep
+    assert np.array_equal(to_host(dst), want_dst), f"n={n} P'={P2}: unpack differs"
+
+
 @pytest.mark.parametrize("offset", [2, 8])
 def test_one_request_misaligned_packed(tk, offset):
     """The one-request grid with a packed buffer `offset` bytes off 16-byte
