@@ -48,6 +48,12 @@ namespace topkv_reshard {
 #ifndef TOPKV_RS_DIRECT
 #define TOPKV_RS_DIRECT 1          // batches without a window take the direct grid when it fits
 #endif
+#ifndef TOPKV_XCD_REMAP
+#define TOPKV_XCD_REMAP 0         // 1: each XCD takes a contiguous eighth of a direct grid (measured slower)
+#endif
+#ifndef TOPKV_EARLY_LENS
+#define TOPKV_EARLY_LENS 1        // direct batches: earlier requests' lengths load with the request's own
+#endif
 #ifndef TOPKV_RS_WG_PER_CU
 #define TOPKV_RS_WG_PER_CU 16     // grid cap = CUs * this
 #endif
@@ -321,10 +327,13 @@ __global__ __launch_bounds__(kThreads) void kv_reshard_kernel(Params p, const in
 // request r in the packed order is planes times this.  Each wave sums the
 // lengths on its own (lanes stride over them, then a butterfly), so no LDS and
 // no barrier are involved.
-__device__ __forceinline__ int32_t kept_before(const int32_t* __restrict__ seq_lens, int32_t r, int32_t max_tok) {
+// `mine` is seq_lens[lane] for lanes below r, already loaded by the caller.
+__device__ __forceinline__ int32_t kept_before(const int32_t* __restrict__ seq_lens, int32_t r, int32_t max_tok,
+                                               int32_t mine) {
+  const int lane = threadIdx.x & 63;
   int32_t s = 0;
-  for (int j = threadIdx.x & 63; j < r; j += 64) {
-    int32_t n = seq_lens[j];
+  for (int j = lane; j < r; j += 64) {
+    int32_t n = j == lane ? mine : seq_lens[j];
     s += n < 0 ? 0 : (n > max_tok ? max_tok : n);
   }
 #pragma unroll
@@ -341,6 +350,23 @@ __device__ __forceinline__ int32_t kept_before(const int32_t* __restrict__ seq_l
 // offset of the lengths before it, and tiles past a request's length exit at
 // once; otherwise one request.  kHostLen: the one request's length is the
 // launch constant n_host instead of a device value.
+// Workgroup coordinates of a direct grid.  The dispatcher hands linear
+// workgroup ids to the 8 XCDs round-robin; with TOPKV_XCD_REMAP the ids are
+// permuted so XCD k runs the k-th contiguous eighth of the grid (a bijection
+// when the workgroup count is a multiple of 8, else the identity).
+__device__ __forceinline__ uint3 grid_block() {
+#if TOPKV_XCD_REMAP
+  const uint32_t gx = gridDim.x, gy = gridDim.y;
+  const uint32_t g = gx * gy * gridDim.z;
+  uint32_t l = blockIdx.x + gx * (blockIdx.y + gy * blockIdx.z);
+  if ((g & 7u) == 0) l = (l & 7u) * (g >> 3) + (l >> 3);
+  const uint32_t xy = l % (gx * gy);
+  return make_uint3(xy % gx, xy / gx, l / (gx * gy));
+#else
+  return make_uint3(blockIdx.x, blockIdx.y, blockIdx.z);
+#endif
+}
+
 template <int VB, bool kBatch, bool kHostLen = false>
 __device__ __forceinline__ void direct_move(const Params& p, const int32_t* __restrict__ seq_lens) {
   typedef typename Vec<VB>::type V;
@@ -348,9 +374,10 @@ __device__ __forceinline__ void direct_move(const Params& p, const int32_t* __re
   const uint32_t per_tp = p.ktp.d;
   const uint32_t lane = threadIdx.x & 63u;
   const uint32_t wave_first = __builtin_amdgcn_readfirstlane(threadIdx.x & ~63u);
-  const uint32_t c = blockIdx.y;
-  const int32_t r = kBatch ? (int32_t)blockIdx.z : 0;
-  const uint32_t base = blockIdx.x * kTile;
+  const uint3 b = grid_block();
+  const uint32_t c = b.y;
+  const int32_t r = kBatch ? (int32_t)b.z : 0;
+  const uint32_t base = b.x * kTile;
   PageCache src_pc, dst_pc;
   {
     // the first span's token is known before the length: prime the page caches
@@ -362,11 +389,22 @@ __device__ __forceinline__ void direct_move(const Params& p, const int32_t* __re
       if (!p.dst.packed) pool_offset_wave(p.dst, at0, 0, 0, dst_pc, &unused);
     }
   }
+  // with a batch, each lane below r also loads one earlier request's length
+  // (for the request's packed offset) next to this request's own
+  int32_t mine = 0;
+#if TOPKV_EARLY_LENS
+  if (kBatch && (int32_t)lane < r) mine = __builtin_nontemporal_load(seq_lens + lane);
+#endif
   int32_t n = kHostLen ? p.n_host : __builtin_amdgcn_readfirstlane(seq_lens[r]);
+#if TOPKV_EARLY_LENS
+  if (kBatch) asm volatile("" ::"v"(mine));   // keep the load here: not sunk past the exit test below
+#else
+  if (kBatch && (int32_t)lane < r) mine = seq_lens[lane];
+#endif
   n = n < 0 ? 0 : (n > p.max_tok ? p.max_tok : n);
   const uint32_t end = (uint32_t)n * per_tp;                  // pieces of this plane
   if (kBatch && base >= end) return;                          // past this request's tokens
-  const uint32_t q0 = (kBatch && r > 0) ? (uint32_t)(p.planes * kept_before(seq_lens, r, p.max_tok)) : 0u;
+  const uint32_t q0 = (kBatch && r > 0) ? (uint32_t)(p.planes * kept_before(seq_lens, r, p.max_tok, mine)) : 0u;
   // Each load issues as soon as its address is known (there is no loop here
   // to hold it up); a skipped piece loads the source base and is not stored.
   V v[kVpt];

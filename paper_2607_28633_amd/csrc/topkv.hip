@@ -57,6 +57,12 @@
 #ifndef TOPKV_ROUTE_SINGLE
 #define TOPKV_ROUTE_SINGLE 1  // one whole-request move with a device length runs the layout-move direct grid
 #endif
+#ifndef TOPKV_XCD_REMAP
+#define TOPKV_XCD_REMAP 0     // 1: each XCD takes a contiguous eighth of the direct grid (measured slower)
+#endif
+#ifndef TOPKV_EARLY_LENS
+#define TOPKV_EARLY_LENS 1    // direct grid: earlier requests' lengths load with the slot's own words
+#endif
 #ifndef TOPKV_THREADS
 #define TOPKV_THREADS 256     // threads per workgroup (a multiple of 64)
 #endif
@@ -231,11 +237,13 @@ __device__ __forceinline__ void copy_tile(char* __restrict__ dst, const char* __
 // stride over the lengths, then a butterfly of 32-bit shuffles), so no LDS
 // and no barrier are involved.  The host keeps one launch's token capacity
 // (num_reqs * bt_stride * page_size) below 2^31, so 32 bits suffice.
+// `mine` is seq_lens[lane] for lanes below r, already loaded by the caller.
 __device__ __forceinline__ int32_t tokens_before(const int32_t* __restrict__ seq_lens, int32_t r,
-                                                 int32_t max_tok, int32_t window) {
+                                                 int32_t max_tok, int32_t window, int32_t mine) {
+  const int lane = threadIdx.x & 63;
   int32_t s = 0;
-  for (int j = threadIdx.x & 63; j < r; j += 64) {
-    int32_t n = seq_lens[j];
+  for (int j = lane; j < r; j += 64) {
+    int32_t n = j == lane ? mine : seq_lens[j];
     n = n < 0 ? 0 : (n > max_tok ? max_tok : n);
     s += (window > 0 && n > window) ? window : n;
   }
@@ -250,6 +258,23 @@ __device__ __forceinline__ int32_t tokens_before(const int32_t* __restrict__ seq
 // next to the loads of the earlier lengths that give the request's token
 // offset; slots past a request's last page exit.  Used when the slot count is
 // small enough for a one-shot grid.
+// Workgroup coordinates of the direct grid.  The dispatcher hands linear
+// workgroup ids to the 8 XCDs round-robin; with TOPKV_XCD_REMAP the ids are
+// permuted so XCD k runs the k-th contiguous eighth of the grid (a bijection
+// when the workgroup count is a multiple of 8, else the identity).
+__device__ __forceinline__ uint3 grid_block() {
+#if TOPKV_XCD_REMAP
+  const uint32_t gx = gridDim.x, gy = gridDim.y;
+  const uint32_t g = gx * gy * gridDim.z;
+  uint32_t l = blockIdx.x + gx * (blockIdx.y + gy * blockIdx.z);
+  if ((g & 7u) == 0) l = (l & 7u) * (g >> 3) + (l >> 3);
+  const uint32_t xy = l % (gx * gy);
+  return make_uint3(xy % gx, xy / gx, l / (gx * gy));
+#else
+  return make_uint3(blockIdx.x, blockIdx.y, blockIdx.z);
+#endif
+}
+
 template <int VB, int VPT, bool kPack, bool kBatched>
 __device__ __forceinline__ void move_direct(char* __restrict__ pool, char* __restrict__ packed,
                                             const int32_t* __restrict__ tables,
@@ -257,17 +282,28 @@ __device__ __forceinline__ void move_direct(char* __restrict__ pool, char* __res
   constexpr int32_t kTile = kThreads * VPT * VB;
   // grid: z = request (single request: z = layer after the first), y = table
   // entry, x = plane * tiles_per_plane + tile
-  const int32_t r = kBatched ? (int32_t)blockIdx.z : 0;
-  const int64_t lz = kBatched ? 0 : (int64_t)blockIdx.z;
-  const int32_t i = blockIdx.y;
-  const int32_t c = (int32_t)(blockIdx.x / (uint32_t)p.tiles_per_plane);
-  const int32_t k = (int32_t)(blockIdx.x - (uint32_t)c * p.tiles_per_plane);
+  const uint3 b = grid_block();
+  const int32_t r = kBatched ? (int32_t)b.z : 0;
+  const int64_t lz = kBatched ? 0 : (int64_t)b.z;
+  const int32_t i = b.y;
+  const int32_t c = (int32_t)(b.x / (uint32_t)p.tiles_per_plane);
+  const int32_t k = (int32_t)(b.x - (uint32_t)c * p.tiles_per_plane);
   const int32_t max_tok = p.bt_stride * p.page_size;   // < 2^31 (host check)
 
-  // This slot's table entry and length, loaded together.
-  int32_t page, n;
+  // This slot's table entry and length, loaded together; with them each lane
+  // below r loads one earlier request's length (the request's token offset
+  // needs them), so the offset costs no further memory latency.
+  int32_t page, n, mine = 0;
   if (kBatched) {
+#if TOPKV_EARLY_LENS
+    if ((int32_t)(threadIdx.x & 63) < r) mine = __builtin_nontemporal_load(seq_lens + (threadIdx.x & 63));
+#endif
     load_pair(tables + (int64_t)r * p.bt_stride + i, seq_lens + r, &page, &n);
+#if TOPKV_EARLY_LENS
+    asm volatile("" ::"v"(mine));   // keep the load here: not sunk past the exit test below
+#else
+    if ((int32_t)(threadIdx.x & 63) < r) mine = seq_lens[threadIdx.x & 63];
+#endif
   } else {
     page = tables[(int64_t)r * p.bt_stride + i];
     n = p.n_single;
@@ -290,7 +326,7 @@ __device__ __forceinline__ void move_direct(char* __restrict__ pool, char* __res
   // Pack: the pool loads go out before the token offset is known (their
   // addresses do not depend on it), so the offset sum overlaps them.
   if (kPack) load_tile<VB, VPT>(v, pool_ptr, nv);
-  const int32_t tok0 = (kBatched && r > 0) ? tokens_before(seq_lens, r, max_tok, p.window) : 0;
+  const int32_t tok0 = (kBatched && r > 0) ? tokens_before(seq_lens, r, max_tok, p.window, mine) : 0;
   int64_t plane_off, end;
   if (!kBatched && p.plane_stride > 0) {          // caller-placed planes (one request)
     plane_off = (int64_t)c * p.plane_stride;
