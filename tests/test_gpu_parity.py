@@ -380,3 +380,88 @@ def test_persistent_grid(tk, kind, window):
     assert (got[n:] == 0x1357).all(), "write past the batch"
     oracle.unpack_layer(want, dst_h, 0, wl.dst_block_tables, wl.seq_lens, window=window)
     assert np.array_equal(to_host(dst), dst_h), f"{kind} window {window}: unpack differs"
+
+
+@pytest.mark.parametrize("window", [0, 7])
+def test_max_batch(tk, window):
+    """Exactly TOPKV_MAX_BATCH_REQS requests in one launch (the largest batch
+    the header accepts; its per-request prefix sums fill the most LDS): the
+    fast pack/unpack and the layout move (a head slice, packed and unpacked)
+    equal the oracles; one request more is refused before any launch."""
+    import oracle.reshard as rs
+    R = tk.TOPKV_MAX_BATCH_REQS
+    rng = np.random.default_rng(31)
+    lens = rng.integers(0, 41, size=R).astype(np.int32)
+    lens[rng.integers(0, R, size=64)] = 0            # empty requests scattered through the batch
+    wl = make_workload("tiny", num_layers=1, num_heads=4, seq_lens=lens)
+    say(f"[max batch] {wl.num_reqs} requests, {int(lens.sum())} tokens, window {window}")
+    src_h, dst_h = host_src_pool(wl), host_dst_prefill(wl)
+    src, dst = to_dev(src_h), to_dev(dst_h)
+    bt, bt2, dlens = to_dev(wl.block_tables), to_dev(wl.dst_block_tables), to_dev(wl.seq_lens)
+    n = oracle.packed_layer_elems(wl.planes, wl.num_heads, wl.head_dim, wl.seq_lens, window)
+    packed = torch.full((n + 64,), 0x2468, dtype=torch.int16, device="cuda")
+    tk.topkv_pack_layer_window(src, 0, R, bt, bt.shape[1], dlens, window, packed, dst_bytes=2 * n)
+    tk.topkv_unpack_layer_window(packed, dst, 0, R, bt2, bt2.shape[1], dlens, window, src_bytes=2 * n)
+    torch.cuda.synchronize()
+    want = oracle.pack_layer(src_h, 0, wl.block_tables, wl.seq_lens, window=window)
+    got = to_host(packed)
+    assert np.array_equal(got[:n], want), "pack differs"
+    assert (got[n:] == 0x2468).all(), "write past the batch"
+    want_dst = dst_h.copy()
+    oracle.unpack_layer(want, want_dst, 0, wl.dst_block_tables, wl.seq_lens, window=window)
+    assert np.array_equal(to_host(dst), want_dst), "unpack differs"
+
+    h0, hc = 1, 2
+    nh = rs.packed_heads_elems(wl.planes, hc, wl.head_dim, wl.seq_lens, window)
+    half = torch.full((nh + 64,), 0x2468, dtype=torch.int16, device="cuda")
+    tk.topkv_move_layer(tk.pool_view(src, 0, bt, bt.shape[1], head_begin=h0), tk.packed_view(half, 2 * nh),
+                        R, dlens, hc, window)
+    tk.topkv_move_layer(tk.packed_view(half, 2 * nh), tk.pool_view(dst, 0, bt2, bt2.shape[1], head_begin=h0),
+                        R, dlens, hc, window)
+    torch.cuda.synchronize()
+    want_h = rs.pack_layer_heads(src_h, 0, wl.block_tables, wl.seq_lens, h0, hc, window)
+    got_h = to_host(half)
+    assert np.array_equal(got_h[:nh], want_h), "head-slice pack differs"
+    assert (got_h[nh:] == 0x2468).all(), "head-slice write past the batch"
+    rs.unpack_layer_heads(want_h, want_dst, 0, wl.dst_block_tables, wl.seq_lens, h0, hc, window)
+    assert np.array_equal(to_host(dst), want_dst), "head-slice unpack differs"
+
+    with pytest.raises(tk.TopkvError) as ei:
+        tk.topkv_pack_layer_window(src, 0, R + 1, bt, bt.shape[1], dlens, window, packed, dst_bytes=2 * n)
+    assert ei.value.status == tk.TOPKV_ERR_UNSUPPORTED
+
+
+def test_widest_table(tk):
+    """One request through a block table of 2^27 - 1 entries at page size 16:
+    the launch's token capacity (table width x page size) is 2^31 - 16, the
+    largest a launch accepts.  Only the request's own pages are read; pack and
+    unpack equal the oracle.  A table one entry wider is refused before any
+    launch."""
+    wl = make_workload("tiny", num_layers=1, seq_lens=[100, 37])
+    width = (1 << 27) - 1
+    src_h, dst_h = host_src_pool(wl), host_dst_prefill(wl)
+    src, dst = to_dev(src_h), to_dev(dst_h)
+    say(f"[widest table] {wl.num_reqs} requests, table width {width} (int32, {4 * width * wl.num_reqs >> 20} MiB)")
+    bt = torch.full((wl.num_reqs, width), -1, dtype=torch.int32, device="cuda")
+    bt2 = torch.full((wl.num_reqs, width), -1, dtype=torch.int32, device="cuda")
+    k = wl.block_tables.shape[1]
+    bt[:, :k] = to_dev(wl.block_tables)
+    bt2[:, :wl.dst_block_tables.shape[1]] = to_dev(wl.dst_block_tables)
+    lens = to_dev(wl.seq_lens)
+    want = oracle.pack_layer(src_h, 0, wl.block_tables, wl.seq_lens)
+    want_dst = dst_h.copy()
+    oracle.unpack_layer(want, want_dst, 0, wl.dst_block_tables, wl.seq_lens)
+    for r in range(wl.num_reqs):            # one request per launch keeps the capacity at 2^31 - 16
+        size = int(wl.seq_lens[r]) * wl.planes * wl.num_heads * wl.head_dim       # elements of request r
+        off = int(wl.seq_lens[:r].sum()) * wl.planes * wl.num_heads * wl.head_dim
+        packed = torch.full((size + 64,), 0x1111, dtype=torch.int16, device="cuda")
+        tk.topkv_pack_layer_batched(src, 0, 1, bt[r], width, lens[r:r + 1], packed, dst_bytes=2 * size)
+        tk.topkv_unpack_layer_batched(packed, dst, 0, 1, bt2[r], width, lens[r:r + 1], src_bytes=2 * size)
+        torch.cuda.synchronize()
+        got = to_host(packed)
+        assert np.array_equal(got[:size], want[off:off + size]), f"request {r}: pack differs"
+        assert (got[size:] == 0x1111).all(), f"request {r}: write past the request"
+    assert np.array_equal(to_host(dst), want_dst), "unpack differs"
+    with pytest.raises(tk.TopkvError) as ei:
+        tk.topkv_pack_layer_batched(src, 0, 1, bt[0], width + 1, lens[0:1], packed, dst_bytes=2 * size)
+    assert ei.value.status == tk.TOPKV_ERR_UNSUPPORTED
