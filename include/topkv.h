@@ -4,7 +4,9 @@
  * C ABI of libtopkv.so.  Every entry point takes plain device pointers and
  * sizes, launches hand-written HIP kernels on the caller's stream and returns
  * without synchronising.  The library never allocates, frees or keeps
- * per-call state; it caches only each device's compute-unit count.
+ * per-call state; it caches only each device's compute-unit count.  (Checked
+ * mode, below, is the one exception: a debugging aid that allocates and
+ * synchronises.)
  *
  * What is computed (arxiv 2607.28633, "Topology-Aware Data Movement for
  * Disaggregated GPU Inference"):
@@ -51,8 +53,24 @@
  * kernel skip that page (nothing read or written for it); a device seq_len
  * below 0 counts as 0 and one above bt_stride * P as bt_stride * P; a batched
  * request whose packed block would cross the end of the packed buffer is not
- * moved.  Such skips are silent; topkv_check_tables reports them.
- * Overlapping source and destination ranges are undefined behaviour.
+ * moved.  Such skips are silent; topkv_check_tables reports bad entries and
+ * lengths (and pages an unpack would write twice), and checked mode reports
+ * all of them.  Overlapping source and destination ranges are undefined
+ * behaviour.
+ *
+ * Checked mode: with TOPKV_CHECKED=1 in the environment (read on every
+ * call), each pack / unpack call (every topkv_pack_layer* and
+ * topkv_unpack_layer* call, and the KVCACHE1 layer calls) and each
+ * fixed-state call first validates its device-side inputs on its stream,
+ * synchronises that stream, and returns TOPKV_ERR_BOUNDS without moving
+ * anything if a table entry the move would read lies outside [0, num_pages)
+ * (with a window only the window's pages count), a length lies outside
+ * [0, bt_stride * page_size], an unpack names a destination page twice, the
+ * packed buffer cannot hold every kept token, or (fixed-state calls) a slot
+ * lies outside the cache or an unpack names it twice.  A stream under
+ * capture gets TOPKV_ERR_UNSUPPORTED (checked mode synchronises).  The
+ * library allocates a small per-device buffer (16 bytes plus one bit per
+ * pool page or state slot) on first use and keeps it until the process ends.
  *
  * Build: hipcc --offload-arch=gfx950 (see the package's build script).  C
  * callers compile with -D__HIP_PLATFORM_AMD__ -I/opt/rocm/include.
@@ -72,7 +90,7 @@ typedef enum topkv_status {
   TOPKV_ERR_INVALID_ARG = 1,  /* null pointer, bad layer index, non-positive dimension */
   TOPKV_ERR_UNSUPPORTED = 2,  /* valid but beyond the library's limits (see each call) */
   TOPKV_ERR_LAUNCH = 3,       /* the HIP runtime refused the launch */
-  TOPKV_ERR_BOUNDS = 4,       /* topkv_check_tables found an invalid table or length */
+  TOPKV_ERR_BOUNDS = 4,       /* invalid device-side table, length, slot or capacity (checked path) */
   TOPKV_ERR_DEVICE = 5,       /* a HIP runtime query failed */
   TOPKV_ERR_CHECKSUM = 6      /* topkv_kvcache1_verify: header or checksum mismatch */
 } topkv_status_t;

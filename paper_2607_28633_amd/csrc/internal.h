@@ -31,6 +31,32 @@ topkv_status_t placed_layers_move(bool pack, const topkv_pool_t* pool, int32_t f
                                   void* packed, int64_t packed_cap, int64_t plane_stride, int64_t layer_stride,
                                   const int32_t* block_table, int32_t seq_len, hipStream_t stream);
 
+// Checked mode: true when the environment holds TOPKV_CHECKED=1 (read on
+// every call, so it can be switched at run time).
+__attribute__((visibility("hidden")))
+bool checked_mode();
+
+// Checked mode's validation of a pack/unpack call, run on `stream` before its
+// launch, then synchronised: table entries of every page the move reads
+// (within the window, when window > 0) in [0, num_pages), lengths in
+// [0, bt_stride * page_size], with `duplicates` no destination page named
+// twice, and the packed buffer large enough: fixed_bytes + per_token * (kept
+// tokens of the batch) <= packed_cap.  The length is the device seq_lens[r],
+// or seq_len for one request when seq_lens is null.  TOPKV_ERR_BOUNDS when
+// anything fails (nothing is moved), TOPKV_ERR_UNSUPPORTED under stream
+// capture.  Uses a per-device buffer the library allocates on first use.
+__attribute__((visibility("hidden")))
+topkv_status_t checked_tables(const topkv_pool_t* pool, int32_t num_reqs, const int32_t* block_tables,
+                              int32_t bt_stride, const int32_t* seq_lens, int32_t seq_len, int32_t window,
+                              bool duplicates, int64_t per_token, int64_t fixed_bytes, int64_t packed_cap,
+                              hipStream_t stream);
+
+// The same for a fixed-state layer: every slot in [0, num_slots), and with
+// `duplicates` no slot named twice.
+__attribute__((visibility("hidden")))
+topkv_status_t checked_slots(const topkv_state_pool_t* pool, int32_t num_reqs, const int32_t* slots,
+                             bool duplicates, hipStream_t stream);
+
 }  // namespace topkv_internal
 
 #endif  // TOPKV_INTERNAL_H_

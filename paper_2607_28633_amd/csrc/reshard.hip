@@ -587,6 +587,25 @@ topkv_status_t move_layer_impl(const topkv_view_t* src, const topkv_view_t* dst,
   }
   if (num_reqs == 0) return TOPKV_OK;
 
+  // Checked mode: validate each pool side's tables (an unpack destination for
+  // pages named twice), and the packed side's room for every kept token.  The
+  // one-request route from a pack/unpack call was checked by its caller.
+  if (!single_only && topkv_internal::checked_mode()) {
+    const bool has_packed = src->layout == TOPKV_LAYOUT_PACKED || dst->layout == TOPKV_LAYOUT_PACKED;
+    const int64_t per_token = (int64_t)geo->planes * (head_count / shards) * geo->head_dim * geo->elem_bytes;
+    bool cap_checked = false;
+    for (int i = 0; i < 2; ++i) {
+      const topkv_view_t* v = sides[i];
+      if (v->layout == TOPKV_LAYOUT_PACKED) continue;
+      const bool with_cap = has_packed && !cap_checked;
+      const topkv_status_t cs = topkv_internal::checked_tables(
+          &v->pool, num_reqs, v->block_tables, v->bt_stride, seq_lens, 0, window, i == 1, with_cap ? per_token : 0,
+          0, with_cap ? packed_cap : INT64_MAX, launch.stream);
+      if (cs != TOPKV_OK) return cs;
+      cap_checked = cap_checked || with_cap;
+    }
+  }
+
   // Heads ride together in one granule when both sides keep them adjacent.
   const int64_t head = (int64_t)geo->head_dim * geo->elem_bytes;
   bool adjacent = true;

@@ -17,6 +17,7 @@
 
 #include <cstdint>
 
+#include "internal.h"
 #include "topkv.h"
 
 namespace topkv_state {
@@ -135,6 +136,10 @@ topkv_status_t launch_state(bool pack, const topkv_state_pool_t* pool, int32_t l
   int64_t need;
   if (__builtin_mul_overflow((int64_t)num_reqs, pool->state_bytes, &need)) return TOPKV_ERR_UNSUPPORTED;
   if (packed_bytes < need) return TOPKV_ERR_INVALID_ARG;   // the batch must fit the packed buffer
+  if (topkv_internal::checked_mode()) {
+    const topkv_status_t st = topkv_internal::checked_slots(pool, num_reqs, slots, !pack, launch->stream);
+    if (st != TOPKV_OK) return st;
+  }
 
   char* base = static_cast<char*>(pool->base) + (int64_t)layer * lay;
   int vb = 16;

@@ -558,6 +558,21 @@ topkv_status_t launch_move(bool pack, const topkv_pool_t* pool, int32_t layer, v
   if (num_reqs > TOPKV_MAX_BATCH_REQS) return TOPKV_ERR_UNSUPPORTED;
   if (num_reqs == 0 || (!seq_lens && n_single == 0)) return TOPKV_OK;  // nothing to move
   if (!tables || !packed || bt_stride <= 0) return TOPKV_ERR_INVALID_ARG;
+  // a host-side length must fit its table
+  if (!seq_lens && ((int64_t)n_single + pool->page_size - 1) / pool->page_size > bt_stride)
+    return TOPKV_ERR_INVALID_ARG;
+
+  if (topkv_internal::checked_mode()) {
+    // packed bytes per kept token, and (placed planes) the bytes before the last plane's rows
+    const int64_t per_token = plane_stride > 0 ? g.row_bytes : (int64_t)pool->planes * g.row_bytes;
+    int64_t fixed = 0;
+    if (plane_stride > 0 && (__builtin_mul_overflow((int64_t)(layers - 1), layer_stride, &fixed) ||
+                             __builtin_add_overflow(fixed, (int64_t)(pool->planes - 1) * plane_stride, &fixed)))
+      return TOPKV_ERR_UNSUPPORTED;
+    st = topkv_internal::checked_tables(pool, seq_lens ? num_reqs : 1, tables, bt_stride, seq_lens, n_single,
+                                        window, !pack, per_token, fixed, packed_cap, launch->stream);
+    if (st != TOPKV_OK) return st;
+  }
 
   // One request, every token kept, planes in the packed order: the
   // layout-move kernel's one-request grid does the same copy with less index
@@ -586,8 +601,7 @@ topkv_status_t launch_move(bool pack, const topkv_pool_t* pool, int32_t layer, v
   if (seq_lens) {
     max_pages = (int64_t)num_reqs * bt_stride;
   } else {
-    max_pages = ((int64_t)n_single + pool->page_size - 1) / pool->page_size;
-    if (max_pages > bt_stride) return TOPKV_ERR_INVALID_ARG;
+    max_pages = ((int64_t)n_single + pool->page_size - 1) / pool->page_size;   // <= bt_stride (checked above)
   }
   // one launch's token capacity (requests x table width x page size) must stay below 2^31
   const int64_t tok_cap = (seq_lens ? (int64_t)num_reqs : 1) * bt_stride * (int64_t)pool->page_size;
@@ -809,7 +823,7 @@ const char* topkv_status_string(topkv_status_t status) {
     case TOPKV_ERR_INVALID_ARG: return "TOPKV_ERR_INVALID_ARG: null pointer, bad layer or non-positive size";
     case TOPKV_ERR_UNSUPPORTED: return "TOPKV_ERR_UNSUPPORTED: size beyond the library's limits";
     case TOPKV_ERR_LAUNCH: return "TOPKV_ERR_LAUNCH: the HIP runtime refused the kernel launch";
-    case TOPKV_ERR_BOUNDS: return "TOPKV_ERR_BOUNDS: block table or length out of range";
+    case TOPKV_ERR_BOUNDS: return "TOPKV_ERR_BOUNDS: block table entry, length, slot or packed capacity out of range";
     case TOPKV_ERR_DEVICE: return "TOPKV_ERR_DEVICE: HIP device query failed";
     case TOPKV_ERR_CHECKSUM: return "TOPKV_ERR_CHECKSUM: serialized header or checksum mismatch";
   }

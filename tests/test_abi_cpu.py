@@ -225,3 +225,20 @@ def test_kvcache1_layer_range_validation(tk):
         _expect(tk, INV, tk.topkv_kvcache1_unpack_layers, blob, good, first, count, bt, 16, blob_bytes=nbytes)
     _expect(tk, INV, tk.topkv_kvcache1_pack_layers, good, 0, 2, bt, 16, blob, blob_bytes=nbytes - 1)
     tk.topkv_kvcache1_pack_layers(good, 1, 0, bt, 16, blob, blob_bytes=nbytes, stream=0)
+
+
+def test_checked_mode_validates_arguments_first(tk, monkeypatch):
+    """With TOPKV_CHECKED=1 the host-side argument checks still come first:
+    a call with bad arguments is refused before checked mode touches the
+    runtime (no GPU is needed to see it)."""
+    monkeypatch.setenv("TOPKV_CHECKED", "1")
+    INV, UNS = tk.TOPKV_ERR_INVALID_ARG, tk.TOPKV_ERR_UNSUPPORTED
+    bt, lens, buf = 0x20000, 0x30000, 0x40000
+    good = _pool(tk)
+    _expect(tk, INV, tk.topkv_pack_layer, _pool(tk, base=0), 0, bt, 16, buf)
+    _expect(tk, INV, tk.topkv_pack_layer, good, 0, bt, -1, buf)
+    _expect(tk, INV, tk.topkv_pack_layer_batched, good, 0, 3, bt, 0, lens, buf, dst_bytes=1 << 20)
+    _expect(tk, INV, tk.topkv_unpack_layer_batched, buf, good, 0, 3, bt, 4, lens, src_bytes=-1)
+    _expect(tk, UNS, tk.topkv_pack_layer_batched, good, 0, tk.TOPKV_MAX_BATCH_REQS + 1, bt, 4, lens,
+            buf, dst_bytes=1 << 20)
+    tk.topkv_pack_layer(good, 0, 0, 0, 0, stream=0)            # zero tokens: still nothing to do
