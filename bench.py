@@ -37,6 +37,7 @@ import hashlib
 import json
 import math
 import os
+import struct
 import sys
 import time
 
@@ -45,17 +46,50 @@ sys.path.insert(0, ROOT)
 
 HBM_PEAK_GBS = 8000.0          # MI355X HBM3E, AMD published peak
 PROFILES = os.path.join(ROOT, "profiles")
-# the per-layer pack/unpack kernels: the fast kernels and the layout-move kernel
-# (whose one-request direct grid runs single-request layers); models with
-# fixed-state layers add the state kernel
-KERNEL_SOURCES = [os.path.join(ROOT, "paper_2607_28633_amd", "csrc", n) for n in ("topkv.hip", "reshard.hip")]
-STATE_SOURCE = os.path.join(ROOT, "paper_2607_28633_amd", "csrc", "state.hip")
+# The committed PMC summaries are pinned to the compiled gfx950 code of the
+# translation units holding the per-layer pack/unpack kernels (the fast
+# kernels and the layout-move kernel, whose one-request grid runs
+# single-request layers; models with fixed-state layers add the state
+# kernel): host-only changes keep them valid, any change to those kernels'
+# machine code or descriptors makes them stale.
+LIBRARY = os.path.join(ROOT, "paper_2607_28633_amd", "libtopkv.so")
+KERNEL_TAGS = (b"kv_pack_kernel", b"kv_reshard_")
+STATE_TAG = b"kv_state_kernel"
 
 
-def kernel_source_digest(with_state=False):
+def _elf_sections(b):
+    """{name: bytes} of a 64-bit little-endian ELF image."""
+    shoff = struct.unpack_from("<Q", b, 0x28)[0]
+    shentsize, shnum, shstrndx = struct.unpack_from("<HHH", b, 0x3A)
+    hdr = [struct.unpack_from("<IIQQQQ", b, shoff + i * shentsize) for i in range(shnum)]
+    names = hdr[shstrndx][4]
+    return {b[names + h[0]:b.index(b"\0", names + h[0])].decode(): b[h[4]:h[4] + h[5]] for h in hdr}
+
+
+def kernel_code_digest(with_state=False, library=LIBRARY):
+    """SHA-256 over the machine code (.text) and kernel descriptors (.rodata)
+    of the gfx950 code objects in the library's offload bundles that hold
+    the pack/unpack kernels (symbol tables are left out: their order varies
+    from build to build)."""
+    magic = b"__CLANG_OFFLOAD_BUNDLE__"
+    fat = _elf_sections(open(library, "rb").read())[".hip_fatbin"]
+    objs = []
+    pos = fat.find(magic)
+    while pos >= 0:
+        q = pos + 32
+        for _ in range(struct.unpack_from("<Q", fat, pos + 24)[0]):
+            off, size, tlen = struct.unpack_from("<QQQ", fat, q)
+            if b"gfx950" in fat[q + 24:q + 24 + tlen]:
+                objs.append(fat[pos + off:pos + off + size])
+            q += 24 + tlen
+        pos = fat.find(magic, pos + 1)
+    tags = KERNEL_TAGS + ((STATE_TAG,) if with_state else ())
     h = hashlib.sha256()
-    for path in KERNEL_SOURCES + ([STATE_SOURCE] if with_state else []):
-        h.update(open(path, "rb").read())
+    for tag in tags:
+        for co in objs:
+            if tag in co:
+                sec = _elf_sections(co)
+                h.update(tag + sec[".text"] + sec[".rodata"])
     return h.hexdigest()
 
 
@@ -133,7 +167,7 @@ def step_bytes(wl):
 
 def read_traffic(workload):
     """HBM traffic per launch from the committed rocprofv3 --pmc summary, or
-    None when the kernel source has changed since the counters were taken."""
+    None when the kernels' code has changed since the counters were taken."""
     path = os.path.join(PROFILES, f"kv_pack_unpack_{workload}_pmc.txt")
     if not os.path.exists(path):
         return None
@@ -143,7 +177,7 @@ def read_traffic(workload):
             k, v = line.split("=", 1)
             vals[k.strip()] = v.strip()
     from paper_2607_28633_amd.workloads import make_workload
-    if vals.get("kernel_source_sha256") != kernel_source_digest(bool(make_workload(workload).layer_state)):
+    if vals.get("kernel_code_sha256") != kernel_code_digest(bool(make_workload(workload).layer_state)):
         return None
     return vals
 

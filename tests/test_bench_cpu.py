@@ -34,3 +34,17 @@ def test_more_than_one_gpu_is_refused():
     r = subprocess.run([sys.executable, os.path.join(ROOT, "bench.py"), "--gpus", "2"],
                        capture_output=True, text=True, cwd=ROOT, timeout=120)
     assert r.returncode == 2 and "one GPU" in r.stderr
+
+
+def test_kernel_code_digest():
+    """The PMC summaries' staleness pin reads the built library's gfx950 code
+    objects: every tagged translation unit is found, the digest is stable, and
+    adding the state kernel changes it."""
+    import bench
+    from paper_2607_28633_amd.build import LIBRARY
+    fat = bench._elf_sections(open(LIBRARY, "rb").read())[".hip_fatbin"]
+    for tag in bench.KERNEL_TAGS + (bench.STATE_TAG,):
+        assert tag in fat, tag
+    a, b = bench.kernel_code_digest(), bench.kernel_code_digest()
+    assert a == b and len(a) == 64
+    assert bench.kernel_code_digest(True) != a
