@@ -193,12 +193,10 @@ def calib_copy(args):
     print(json.dumps({"calib_copy_bytes": n, "launches": args.warmup + args.steps}), flush=True)
 
 
-def cpu_baseline(wl, src, dst, budget_s, states=None):
-    """Time the oracle on host copies of a few layer slabs, cycling until the
-    budget is spent.  Returns the cpu_baseline object."""
+def host_slabs(wl, src, dst, states=None):
+    """Host copies (uint16 words, bit-exact) of the first few device layer
+    slabs of both pools, and of one layer of each state cache."""
     import numpy as np
-    import oracle
-    import oracle.state
     import torch
 
     def to_host_words(t):   # device bf16 slab -> host uint16 words, bit-exact
@@ -206,8 +204,29 @@ def cpu_baseline(wl, src, dst, budget_s, states=None):
 
     slabs = list(range(min(wl.phys_layers, 4)))
     host = {s: (to_host_words(src[s])[None], to_host_words(dst[s])[None]) for s in slabs}
+    st_h = None
     if states is not None:
         st_h = (to_host_words(states[0][0])[None], to_host_words(states[1][0])[None])
+    return slabs, host, st_h
+
+
+def cpu_model():
+    try:
+        for line in open("/proc/cpuinfo"):
+            if line.startswith("model name"):
+                return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown"
+
+
+def cpu_baseline(wl, hs, budget_s):
+    """Time the oracle on host copies of a few layer slabs, cycling until the
+    budget is spent.  Returns the cpu_baseline object."""
+    import oracle
+    import oracle.state
+
+    slabs, host, st_h = hs
     done_bytes, spent, layers = 0, 0.0, 0
     while spent < budget_s and layers < 10_000:
         s = slabs[layers % len(slabs)]
@@ -224,19 +243,150 @@ def cpu_baseline(wl, src, dst, budget_s, states=None):
         spent += time.perf_counter() - t0
         done_bytes += sum(layer_bytes(wl, layers % wl.num_layers))
         layers += 1
-    cpu = "unknown"
-    try:
-        for line in open("/proc/cpuinfo"):
-            if line.startswith("model name"):
-                cpu = line.split(":", 1)[1].strip()
-                break
-    except OSError:
-        pass
     return {"value": round(done_bytes / spent / 1e9, 3), "unit": "GB/s", "cores": 1, "kind": "oracle",
             "sample": (f"{layers} layer pack+unpack passes of {wl.name} over host copies of "
-                       f"{len(slabs)} layer slab(s){' and one state-cache layer' if states is not None else ''}, "
+                       f"{len(slabs)} layer slab(s){' and one state-cache layer' if st_h is not None else ''}, "
                        f"numpy oracle, one thread, {spent:.1f} s"),
-            "cpu_model": cpu, "host_threads_available": len(os.sched_getaffinity(0)),
+            "cpu_model": cpu_model(), "host_threads_available": len(os.sched_getaffinity(0)),
+            "ms_per_layer_pack_unpack": round(1e3 * spent / layers, 3)}
+
+
+def host_ops(wl, layer, pool, packed, direction, group):
+    """One layer's pack (direction 0: pool -> packed) or unpack (1: packed ->
+    pool) on the host as bulk operations: ("pages", pool, page ids, plane
+    views) moves `group` whole pages of one request at once (one gather or
+    scatter of the pages, one copy per plane), ("copy", dst, src) moves one
+    partial page run or one fixed state.  pool: the layer's words,
+    [pages][planes][slots][heads][dim] (a state cache layer: [slots][words]);
+    packed: flat words."""
+    if wl.is_state(layer):
+        E = pool.shape[1]
+        slots = wl.state_slots if direction == 0 else wl.dst_state_slots
+        return [("copy", packed[r * E:(r + 1) * E], pool[s]) if direction == 0
+                else ("copy", pool[s], packed[r * E:(r + 1) * E]) for r, s in enumerate(int(x) for x in slots)]
+    P = wl.page_size if direction == 0 else wl.dst_page_size
+    bt = wl.block_tables if direction == 0 else wl.dst_block_tables
+    W = wl.window(layer)
+    C, row = wl.planes, wl.num_heads * wl.head_dim
+    ops, off = [], 0
+    for r, n in enumerate(int(x) for x in wl.seq_lens):
+        s = n - W if 0 < W < n else 0
+        cnt = n - s
+        region = packed[off:off + C * cnt * row].reshape(C, cnt, row)
+        full_lo, full_hi = -(-s // P), n // P            # pages whose P slots are all kept
+        for i in range(s // P, -(-n // P)):
+            if full_lo <= i < full_hi:
+                continue
+            lo, hi = max(i * P, s), min(i * P + P, n)
+            for c in range(C):
+                k = region[c, lo - s:hi - s].reshape(-1)
+                p = pool[bt[r, i], c, lo - i * P:hi - i * P].reshape(-1)
+                ops.append(("copy", k, p) if direction == 0 else ("copy", p, k))
+        for i0 in range(full_lo, full_hi, group):
+            i1 = min(i0 + group, full_hi)
+            views = region[:, i0 * P - s:i1 * P - s].reshape(C, i1 - i0, P, row)
+            ops.append(("pages", pool, bt[r, i0:i1], views))
+        off += C * cnt * row
+    return ops
+
+
+def op_bytes(op):
+    return op[1].nbytes if op[0] == "copy" else op[3].nbytes
+
+
+def run_ops(ops, direction):
+    import numpy as np
+    for op in ops:
+        if op[0] == "copy":
+            np.copyto(op[1], op[2])
+            continue
+        _, pool, idx, views = op
+        k = len(idx)
+        if direction == 0:
+            pages = pool[idx]                               # gather the group's pages
+            for c in range(views.shape[0]):
+                np.copyto(views[c], pages[:, c].reshape(views.shape[1:]))
+        else:
+            pages = np.empty((k,) + pool.shape[1:], dtype=pool.dtype)
+            for c in range(views.shape[0]):
+                np.copyto(pages[:, c].reshape(views.shape[1:]), views[c])
+            pool[idx] = pages                               # scatter them
+
+
+def split_ops(ops, parts):
+    """Consecutive chunks of about equal bytes, one per thread."""
+    total = sum(op_bytes(op) for op in ops)
+    chunks, cur, acc = [], [], 0
+    for op in ops:
+        cur.append(op)
+        acc += op_bytes(op)
+        if acc >= total * (len(chunks) + 1) / parts and len(chunks) < parts - 1:
+            chunks.append(cur)
+            cur = []
+    chunks.append(cur)
+    return chunks
+
+
+def cpu_threaded(wl, hs, budget_s, threads=None):
+    """The same layers on the host over a thread pool (by default one thread
+    per 4 MiB moved per direction, up to the cores the process may use): each
+    layer's whole pages move in groups (one numpy gather or scatter per group,
+    which runs without the interpreter lock), partial pages and fixed states
+    one copy each, split into one chunk per thread.  Each layer kind is
+    checked against the oracle on layer slab 0 before anything is timed.  A
+    faster host baseline than the oracle; not part of the GPU path."""
+    from concurrent.futures import ThreadPoolExecutor
+
+    import numpy as np
+    import oracle
+    import oracle.state
+
+    slabs, host, st_h = hs
+    if not threads:
+        # one thread per 4 MiB moved per direction, up to the cores available: on a 16.8 MB layer
+        # (the 70B headline) 4 threads moved 102 GB/s on the GPU machine's host, 16 threads 36 GB/s
+        per_dir = max(layer_bytes(wl, l)[0] for l in range(wl.num_layers)) // 2
+        threads = max(1, min(len(os.sched_getaffinity(0)), per_dir // (4 << 20)))
+    kinds = sorted({(wl.is_state(l), wl.window(l)) for l in range(wl.num_layers)})
+    rep = {k: next(l for l in range(wl.num_layers) if (wl.is_state(l), wl.window(l)) == k) for k in kinds}
+    packed = np.empty(max(layer_bytes(wl, l)[0] for l in range(wl.num_layers)) // 4 + 8, dtype=np.uint16)
+    pages = sum(-(-int(n) // wl.page_size) for n in wl.seq_lens)
+    group = max(1, -(-pages // threads))                # one group of whole pages per thread
+    plans = {}
+    for s_ in slabs:
+        for k, l in rep.items():
+            src_l, dst_l = (st_h[0][0], st_h[1][0]) if k[0] else (host[s_][0][0], host[s_][1][0])
+            plans[(s_, k)] = [split_ops(host_ops(wl, l, src_l, packed, 0, group), threads),
+                              split_ops(host_ops(wl, l, dst_l, packed, 1, group), threads)]
+    with ThreadPoolExecutor(threads) as ex:
+        def layer_pass(s_, k):
+            for d in (0, 1):
+                list(ex.map(lambda ch: run_ops(ch, d), plans[(s_, k)][d]))
+        for k, l in rep.items():       # check each layer kind on slab 0 against the oracle
+            src_l, dst_l = (st_h[0], st_h[1]) if k[0] else host[slabs[0]]
+            want_dst = dst_l.copy()
+            if k[0]:
+                want = oracle.state.pack_state_layer(src_l, 0, wl.state_slots)
+                oracle.state.unpack_state_layer(want, want_dst, 0, wl.dst_state_slots)
+            else:
+                want = oracle.pack_layer(src_l, 0, wl.block_tables, wl.seq_lens, window=k[1])
+                oracle.unpack_layer(want, want_dst, 0, wl.dst_block_tables, wl.seq_lens, window=k[1])
+            layer_pass(slabs[0], k)
+            if not (np.array_equal(packed[:want.size], want) and np.array_equal(dst_l, want_dst)):
+                raise AssertionError(f"threaded host pack/unpack differs from the oracle (layer kind {k})")
+        done_bytes, spent, layers = 0, 0.0, 0
+        while spent < budget_s and layers < 100_000:
+            lay = layers % wl.num_layers
+            k = (wl.is_state(lay), wl.window(lay))
+            t0 = time.perf_counter()
+            layer_pass(slabs[layers % len(slabs)], k)
+            spent += time.perf_counter() - t0
+            done_bytes += sum(layer_bytes(wl, lay))
+            layers += 1
+    return {"value": round(done_bytes / spent / 1e9, 3), "unit": "GB/s", "threads": threads,
+            "host_threads_available": len(os.sched_getaffinity(0)),
+            "kind": "host pack+unpack: numpy page gathers/scatters over a thread pool (checked against the oracle)",
+            "sample": f"{layers} layer pack+unpack passes of {wl.name}, {spent:.1f} s",
             "ms_per_layer_pack_unpack": round(1e3 * spent / layers, 3)}
 
 
@@ -409,9 +559,13 @@ def run(args):
     }
     if args.cpu_seconds > 0:
         log(f"[bench] CPU oracle sample (~{args.cpu_seconds} s)")
-        out["cpu_baseline"] = cpu_baseline(wl, src, dst, args.cpu_seconds, states)
+        hs = host_slabs(wl, src, dst, states)
+        out["cpu_baseline"] = cpu_baseline(wl, hs, args.cpu_seconds)
+        log(f"[bench] threaded host pack/unpack (~{min(5.0, args.cpu_seconds / 2):.0f} s)")
+        out["cpu_threaded"] = cpu_threaded(wl, hs, min(5.0, args.cpu_seconds / 2))
     else:
         out["cpu_baseline"] = None
+        out["cpu_threaded"] = None
     print(json.dumps(out), flush=True)
 
 

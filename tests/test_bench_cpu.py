@@ -48,3 +48,29 @@ def test_kernel_code_digest():
     a, b = bench.kernel_code_digest(), bench.kernel_code_digest()
     assert a == b and len(a) == 64
     assert bench.kernel_code_digest(True) != a
+
+
+def _host_slabs(wl):
+    from paper_2607_28633_amd.workloads import host_dst_prefill, host_src_pool, host_state_cache
+    src, dst = host_src_pool(wl), host_dst_prefill(wl)
+    slabs = list(range(min(wl.phys_layers, 2)))
+    host = {s: (src[s][None].copy(), dst[s][None].copy()) for s in slabs}
+    st = None
+    if wl.layer_state:
+        st = (host_state_cache(wl)[0][None].copy(), host_state_cache(wl, dst=True)[0][None].copy())
+    return slabs, host, st
+
+
+def test_threaded_host_baseline_matches_oracle():
+    """The bench's threaded host pack/unpack equals the oracle (it checks each
+    layer kind itself before timing) on full, re-blocked, windowed and
+    fixed-state layers."""
+    import bench
+    from paper_2607_28633_amd.workloads import make_workload
+    cases = [make_workload("tiny"),
+             make_workload("tiny", dst_page_size=48, seq_lens=[100, 0, 37, 16]),
+             make_workload("gpt-oss-120b", num_layers=2, seq_lens=[300, 17, 129, 128]),
+             make_workload("qwen3.5-397b-hybrid", num_layers=4, seq_lens=[40, 3, 77], state_bytes=1000)]
+    for wl in cases:
+        res = bench.cpu_threaded(wl, _host_slabs(wl), 0.05, threads=3)
+        assert res["value"] > 0 and res["threads"] == 3, wl.name
