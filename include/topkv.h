@@ -298,6 +298,35 @@ topkv_status_t topkv_kvcache1_unpack_layers(const void* blob, int64_t blob_bytes
                                             int32_t first_layer, int32_t num_layers, const int32_t* block_table,
                                             int32_t seq_len, hipStream_t stream);
 
+/* Whole-request serialization in one pass (Section 3.5): every layer's K and
+ * V rows move from the pool into the blob inside the CRC kernels that
+ * checksum them, then the header is written.  The blob (header included) is
+ * byte for byte what topkv_kvcache1_pack_layers(all layers) followed by
+ * topkv_kvcache1_seal writes, including where a table entry lies outside the
+ * pool (those rows keep the blob's bytes and are checksummed as they are);
+ * the pool is read once and the blob written once instead of being written
+ * and read back.  Same arguments and workspace as those two calls;
+ * block_table: device int32[ceil(seq_len / page_size)].  Requests beyond the
+ * one-pass limits (layers * seq_len >= 2^31, rows of 2^31 - 2^17 bytes or
+ * more, a pool base off 16-byte alignment) take the two calls internally. */
+topkv_status_t topkv_kvcache1_pack_seal(const topkv_pool_t* src, const int32_t* block_table,
+                                        int32_t seq_len, uint64_t request_id, uint64_t model_id,
+                                        void* blob, int64_t blob_bytes, void* workspace,
+                                        int64_t workspace_bytes, hipStream_t stream);
+
+/* Receiver in one pass: the blob's K and V tensors are checksummed and, in the
+ * same kernels, scattered into every layer of the pool (any page size), and
+ * the header is compared as topkv_kvcache1_verify does (same result words).
+ * The pool pages named by block_table are written whatever the verdict: a
+ * caller that sees result[0] != TOPKV_OK must treat them as garbage (and
+ * retry the transfer).  Rows whose table entry lies outside the pool are not
+ * written.  Same fallback limits as topkv_kvcache1_pack_seal. */
+topkv_status_t topkv_kvcache1_verify_unpack(const void* blob, int64_t blob_bytes,
+                                            const topkv_pool_t* dst, const int32_t* block_table,
+                                            int32_t seq_len, uint64_t request_id, uint64_t model_id,
+                                            void* workspace, int64_t workspace_bytes, int32_t* result,
+                                            hipStream_t stream);
+
 /* CRC-64/XZ (as above) of nbytes of device memory at data (16-byte aligned,
  * any length), written to the device word *crc_out on the stream.
  * workspace: topkv_crc64_workspace_bytes(nbytes) bytes of device memory,

@@ -150,14 +150,51 @@ __device__ inline void stage(uint64_t* lds, const uint64_t* __restrict__ src, in
   }
 }
 
-// Kernel 1: raw register of each span of the front-padded stream.  data:
-// 16-byte aligned, `head` bytes (a multiple of 16); `pad` leading zero bytes
-// (a multiple of 16) make head + pad = gridDim.x spans of span_subs
+// n / d for 0 <= n < 2^31 by a multiply-high (Granlund and Montgomery,
+// 1994): s = ceil(log2 d), m = floor(2^32 (2^s - d) / d) + 1, and the
+// quotient is (mulhi(n, m) + n) >> s.
+struct Div32 {
+  uint32_t d, m, s;
+};
+
+Div32 make_div32(uint32_t d) {
+  uint32_t s = 0;
+  while ((1ull << s) < d) ++s;
+  return Div32{d, (uint32_t)((((1ull << 32) * ((1ull << s) - d)) / d) + 1), s};
+}
+
+__device__ __forceinline__ uint32_t div32(uint32_t n, const Div32& f) { return (__umulhi(n, f.m) + n) >> f.s; }
+
+// Where a span kernel's 16-byte pieces come from and go to.  kStream: the
+// CRC input is `data`.  kGather: the input is one KVCACHE1 tensor gathered
+// from the pool (byte `off` of the tensor is layer first + l, token t, byte b
+// of plane `plane_off`'s row), and each piece is also stored to the blob
+// tensor; a piece whose page entry is out of range keeps the blob's bytes
+// (they are read and folded instead, nothing is written).  kScatter: the
+// input is the blob tensor and each piece is also stored to its pool slot
+// (pieces of out-of-range pages are not stored).
+enum { kStream = 0, kGather = 1, kScatter = 2 };
+
+struct PoolSide {
+  char* pool;             // pool base (layer 0)
+  u32x4* blob;            // the tensor's first byte in the blob
+  const int32_t* table;   // the request's block table
+  int64_t layer_bytes, page_bytes, plane_off, num_pages;
+  int64_t step_q;         // kSub / row_bytes
+  int32_t step_r;         // kSub mod row_bytes
+  int32_t row_bytes, seq_len, page_size, first_layer;
+  Div32 d_row, d_seq, d_page;
+};
+
+// Kernel 1: raw register of each span of the front-padded stream.  The
+// tensor (or data) has `head` bytes (a multiple of 16); `pad` leading zero
+// bytes (a multiple of 16) make head + pad = gridDim.x spans of span_subs
 // sub-chunks.
+template <int kMode>
 __global__ __launch_bounds__(kCrcThreads) void crc64_span_kernel(const u32x4* __restrict__ data, int64_t pad,
                                                                  int64_t span_subs,
                                                                  const uint64_t* __restrict__ tables,
-                                                                 uint64_t* __restrict__ partial) {
+                                                                 uint64_t* __restrict__ partial, PoolSide ps) {
   // [0, 8192): slicing tables 0..3 in kCopies replicas (64 KiB); [8192, 16384): per-wave staging
   // (64 KiB); after the span, all 128 KiB hold join levels 0..7
   __shared__ __attribute__((aligned(16))) uint64_t big[4 * 256 * kCopies + kStageWords];
@@ -180,22 +217,138 @@ __global__ __launch_bounds__(kCrcThreads) void crc64_span_kernel(const u32x4* __
   // wave's bytes [1024 j + 16 l, +16) at position l ^ ((l >> 4) & 3), which keeps both the
   // row-wise writes and the lane-piece reads free of bank conflicts
   u32x4* stage_area = reinterpret_cast<u32x4*>(big + 4 * 256 * kCopies) + wave * 4 * 64;
-  // data offset of this wave's slice of sub-chunk 0 plus this lane's 16-byte column
-  const int64_t base = (int64_t)blockIdx.x * span_subs * kSub + (int64_t)wave * 64 * kPiece + 16 * lane - pad;
+  // this lane's 16-byte column within a sub-chunk, and the first sub-chunk's data offset
+  const int32_t local = wave * 64 * kPiece + 16 * lane;
+  const int64_t span0 = (int64_t)blockIdx.x * span_subs * kSub - pad;
+  const int64_t base = span0 + local;
+
+  // Pool side.  A sub-chunk's first tensor byte sb is tracked as the floor
+  // quotient and remainder (r0, in0) of sb / row_bytes (sb < 0 in the front
+  // padding gives r0 < 0): one step of kSub bytes adds (step_q, step_r) with a
+  // carry.  A piece at x = in0 + its offset inside the sub-chunk then lies in
+  // row r0 + x / row_bytes (rows < 0: padding) at byte x mod row_bytes.
+  struct RowPos {
+    int64_t r0;
+    int32_t in0;
+  };
+  auto advance = [&](RowPos p) {
+    p.in0 += ps.step_r;
+    p.r0 += ps.step_q;
+    if (p.in0 >= ps.row_bytes) {
+      p.in0 -= ps.row_bytes;
+      ++p.r0;
+    }
+    return p;
+  };
+  RowPos pos0;
+  if (kMode != kStream) {
+    const int64_t q = span0 >= 0 ? span0 / ps.row_bytes : -((-span0 + ps.row_bytes - 1) / ps.row_bytes);
+    pos0 = RowPos{q, (int32_t)(span0 - q * ps.row_bytes)};
+  }
+  // the piece's (layer-major) row and its byte in the row; false in the padding
+  auto row_of = [&](const RowPos& p, int j, uint32_t* row, uint32_t* inrow) -> bool {
+    const uint32_t x = (uint32_t)(p.in0 + local + 1024 * j);
+    const uint32_t q = div32(x, ps.d_row);
+    const int64_t r = p.r0 + q;
+    if (r < 0) return false;
+    *row = (uint32_t)r;
+    *inrow = x - q * (uint32_t)ps.row_bytes;
+    return true;
+  };
+  auto lookup = [&](int32_t (&pg)[kLoads], const RowPos& p) {
+#pragma unroll
+    for (int j = 0; j < kLoads; ++j) {
+      uint32_t row, inrow;
+      pg[j] = -1;
+      if (row_of(p, j, &row, &inrow)) {
+        const uint32_t l = div32(row, ps.d_seq);
+        pg[j] = ps.table[div32(row - l * (uint32_t)ps.seq_len, ps.d_page)];
+      }
+    }
+  };
+  // pool byte of the piece: -1 in the padding, -2 when its page entry is out of range
+  auto locate = [&](const RowPos& p, int j, int32_t page) -> int64_t {
+    uint32_t row, inrow;
+    if (!row_of(p, j, &row, &inrow)) return -1;
+    if (page < 0 || (int64_t)page >= ps.num_pages) return -2;
+    const uint32_t l = div32(row, ps.d_seq);
+    const uint32_t t = row - l * (uint32_t)ps.seq_len;
+    const uint32_t i = div32(t, ps.d_page);
+    return ((int64_t)ps.first_layer + l) * ps.layer_bytes + (int64_t)page * ps.page_bytes + ps.plane_off +
+           (int64_t)(t - i * (uint32_t)ps.page_size) * ps.row_bytes + inrow;
+  };
+  const u32x4 zero = {0u, 0u, 0u, 0u};
+  const u32x4* in = kMode == kScatter ? ps.blob : data;
+
   u32x4 cur[kLoads], nxt[kLoads];
+  int32_t pg_a[kLoads] = {}, pg_b[kLoads] = {};
+  // kStream / kScatter: contiguous input (the data, or the blob tensor)
   auto load = [&](u32x4 (&v)[kLoads], int64_t sub) {
 #pragma unroll
     for (int j = 0; j < kLoads; ++j) {
       const int64_t off = base + (sub << kSubLog2) + 1024 * j;
-      v[j] = off >= 0 ? __builtin_nontemporal_load(data + off / 16) : u32x4{0u, 0u, 0u, 0u};   // off < head
+      v[j] = off >= 0 ? __builtin_nontemporal_load(in + off / 16) : zero;   // off < head
     }
   };
+  // kGather: pool pieces (page entries pg loaded an iteration earlier); bad pages read the blob
+  auto gather = [&](u32x4 (&v)[kLoads], int64_t sub, const RowPos& p, const int32_t (&pg)[kLoads]) {
+#pragma unroll
+    for (int j = 0; j < kLoads; ++j) {
+      const int64_t po = locate(p, j, pg[j]);
+      const int64_t off = base + (sub << kSubLog2) + 1024 * j;
+      v[j] = po >= 0    ? __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(ps.pool + po))
+             : po == -2 ? ps.blob[off / 16]
+                        : zero;
+    }
+  };
+  auto put = [&](const u32x4 (&v)[kLoads], int64_t sub, const RowPos& p, const int32_t (&pg)[kLoads]) {
+#pragma unroll
+    for (int j = 0; j < kLoads; ++j) {
+      const int64_t po = locate(p, j, pg[j]);
+      if (po < 0) continue;
+      if (kMode == kGather) {
+        const int64_t off = base + (sub << kSubLog2) + 1024 * j;
+        __builtin_nontemporal_store(v[j], ps.blob + off / 16);
+      } else {
+        __builtin_nontemporal_store(v[j], reinterpret_cast<u32x4*>(ps.pool + po));
+      }
+    }
+  };
+
+  RowPos pos = pos0;   // this sub-chunk's row position (pool modes)
+  if (kMode == kGather) {
+    lookup(pg_a, pos);
+    gather(cur, 0, pos, pg_a);
+    if (span_subs > 1) lookup(pg_b, advance(pos));
+  } else {
+    load(cur, 0);
+    if (kMode == kScatter) lookup(pg_a, pos);
+  }
   const int wr = lane ^ ((lane >> 4) & 3);                        // write slot of this lane in each row
   const int rrow = lane >> 4, rcol = 4 * (lane & 15);             // this lane's piece: row, first column
-  load(cur, 0);
   uint64_t fold = 0;
   for (int64_t sub = 0; sub < span_subs; ++sub) {
-    if (sub + 1 < span_subs) load(nxt, sub + 1);
+    if (kMode == kGather) {
+      // pg_a: this sub-chunk's entries, pg_b: the next one's (loaded a sub-chunk ago)
+      const RowPos p1 = advance(pos);
+      if (sub + 1 < span_subs) gather(nxt, sub + 1, p1, pg_b);
+      put(cur, sub, pos, pg_a);
+#pragma unroll
+      for (int j = 0; j < kLoads; ++j) pg_a[j] = pg_b[j];
+      if (sub + 2 < span_subs) lookup(pg_b, advance(p1));
+      pos = p1;
+    } else {
+      if (sub + 1 < span_subs) {
+        load(nxt, sub + 1);
+        if (kMode == kScatter) lookup(pg_b, advance(pos));
+      }
+      if (kMode == kScatter) {
+        put(cur, sub, pos, pg_a);
+#pragma unroll
+        for (int j = 0; j < kLoads; ++j) pg_a[j] = pg_b[j];
+        pos = advance(pos);
+      }
+    }
 #pragma unroll
     for (int j = 0; j < kLoads; ++j) stage_area[j * 64 + wr] = cur[j];
     __builtin_amdgcn_wave_barrier();
@@ -308,8 +461,9 @@ topkv_status_t crc64_launch(const unsigned char* data, int64_t n, const uint64_t
   const ShiftConsts& sc = shift_consts();
   const Spans g = span_geometry(n);
   if (g.spans > 0) {
-    hipLaunchKernelGGL(crc64_span_kernel, dim3((unsigned)g.spans), dim3(kCrcThreads), 0, stream,
-                       reinterpret_cast<const u32x4*>(data), g.spans * g.span - g.head, g.span_subs, tables, partial);
+    hipLaunchKernelGGL(crc64_span_kernel<kStream>, dim3((unsigned)g.spans), dim3(kCrcThreads), 0, stream,
+                       reinterpret_cast<const u32x4*>(data), g.spans * g.span - g.head, g.span_subs, tables, partial,
+                       PoolSide{});
     if (hipGetLastError() != hipSuccess) return TOPKV_ERR_LAUNCH;
   }
   hipLaunchKernelGGL(crc64_finish_kernel, dim3(1), dim3(kMaxSpans), 0, stream, tables, partial, (int)g.spans,
@@ -433,6 +587,59 @@ int64_t blob_ws_bytes(const Blob& b) {
 
 bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15) == 0; }
 
+// Whether the span kernels can move a whole request's tensors between the pool
+// and the blob themselves (32-bit row and token arithmetic, 16-byte pieces).
+bool fused_fits(const topkv_pool_t* pool, int32_t seq_len, const Blob& b) {
+  return seq_len > 0 && (int64_t)pool->num_layers * seq_len < INT32_MAX && b.row < INT32_MAX - 2 * kSub &&
+         aligned16(pool->base);
+}
+
+// Both checksums of the blob body into ws[0..1] while the K and V tensors of
+// every layer move between the pool and the blob inside the span kernels
+// (kGather: pool -> blob, kScatter: blob -> pool).
+template <int kMode>
+topkv_status_t fused_blob_crcs(const topkv_pool_t* pool, const int32_t* table, int32_t seq_len, unsigned char* blob,
+                               const Blob& b, uint64_t* ws, hipStream_t stream) {
+  uint64_t* tables = ws + 2;
+  uint64_t* partial[2] = {tables + kWsTables, tables + kWsTables + kMaxSpans};
+  const ShiftConsts& sc = shift_consts();
+  PoolSide ps{};
+  ps.pool = static_cast<char*>(pool->base);
+  ps.table = table;
+  ps.row_bytes = (int32_t)b.row;
+  ps.page_size = pool->page_size;
+  ps.page_bytes = (int64_t)pool->planes * pool->page_size * b.row;
+  ps.layer_bytes = pool->num_pages * ps.page_bytes;
+  ps.num_pages = pool->num_pages;
+  ps.seq_len = seq_len;
+  ps.first_layer = 0;
+  ps.step_q = kSub / b.row;
+  ps.step_r = (int32_t)(kSub % b.row);
+  ps.d_row = make_div32((uint32_t)b.row);
+  ps.d_seq = make_div32((uint32_t)seq_len);
+  ps.d_page = make_div32((uint32_t)pool->page_size);
+  const Spans g = span_geometry(b.k_bytes);                 // K and V tensors have the same size
+  topkv_status_t st = crc64_tables(tables, g.span, stream);
+  if (st != TOPKV_OK) return st;
+  for (int c = 0; c < pool->planes; ++c) {
+    ps.plane_off = (int64_t)c * pool->page_size * b.row;
+    ps.blob = reinterpret_cast<u32x4*>(blob + kHeaderBytes + c * b.k_bytes);
+    hipLaunchKernelGGL(crc64_span_kernel<kMode>, dim3((unsigned)g.spans), dim3(kCrcThreads), 0, stream, ps.blob,
+                       g.spans * g.span - g.head, g.span_subs, tables, partial[c], ps);
+    if (hipGetLastError() != hipSuccess) return TOPKV_ERR_LAUNCH;
+    hipLaunchKernelGGL(crc64_finish_kernel, dim3(1), dim3(kMaxSpans), 0, stream, tables, partial[c], (int)g.spans,
+                       reinterpret_cast<const unsigned char*>(ps.blob) + g.head, 0,
+                       mulmod(x8n(sc, (uint64_t)b.k_bytes), ~0ull), ws + c);
+    if (hipGetLastError() != hipSuccess) return TOPKV_ERR_LAUNCH;
+  }
+  if (pool->planes == 1) {     // an MLA cache has no V tensor: its checksum is that of no bytes
+    hipLaunchKernelGGL(crc64_finish_kernel, dim3(1), dim3(kMaxSpans), 0, stream, tables, partial[1], 0,
+                       blob + kHeaderBytes + b.k_bytes, 0, mulmod(x8n(sc, 0), ~0ull), ws + 1);
+    if (hipGetLastError() != hipSuccess) return TOPKV_ERR_LAUNCH;
+  }
+  return TOPKV_OK;
+}
+
 // Layers [first_layer, first_layer + num_layers) of one request into (pack) or
 // out of (unpack) their rows of the blob's K and V tensors: one launch when
 // the layer dimension fits the direct grid, else one launch per layer.
@@ -551,6 +758,66 @@ topkv_status_t topkv_kvcache1_unpack_layer(const void* blob, int64_t blob_bytes,
   const unsigned char* k = static_cast<const unsigned char*>(blob) + kHeaderBytes + (int64_t)layer * seq_len * b.row;
   return topkv_unpack_layer_planes(k, b.k_bytes, blob_bytes - (kHeaderBytes + (int64_t)layer * seq_len * b.row),
                                    dst, layer, block_table, seq_len, stream);
+}
+
+topkv_status_t topkv_kvcache1_pack_seal(const topkv_pool_t* src, const int32_t* block_table, int32_t seq_len,
+                                        uint64_t request_id, uint64_t model_id, void* blob, int64_t blob_bytes,
+                                        void* workspace, int64_t workspace_bytes, hipStream_t stream) {
+  Blob b;
+  topkv_status_t st = blob_geometry(src, seq_len, &b);
+  if (st != TOPKV_OK) return st;
+  if (!src->base || !blob || blob_bytes < b.total || !workspace || workspace_bytes < blob_ws_bytes(b) ||
+      (seq_len > 0 && !block_table) || src->page_size <= 0 || src->num_pages <= 0)
+    return TOPKV_ERR_INVALID_ARG;
+  if (!aligned16(blob)) return TOPKV_ERR_UNSUPPORTED;
+  if (!fused_fits(src, seq_len, b)) {          // the two-step path: move every layer, then checksum
+    st = kv1_move_layers(true, src, 0, src->num_layers, block_table, seq_len, blob, blob_bytes, stream);
+    return st != TOPKV_OK ? st : topkv_kvcache1_seal(src, seq_len, request_id, model_id, blob, blob_bytes,
+                                                      workspace, workspace_bytes, stream);
+  }
+  if (topkv_internal::checked_mode()) {
+    st = topkv_internal::checked_tables(src, 1, block_table, (seq_len + src->page_size - 1) / src->page_size,
+                                        nullptr, seq_len, 0, false, 0, 0, INT64_MAX, stream);
+    if (st != TOPKV_OK) return st;
+  }
+  uint64_t* ws = static_cast<uint64_t*>(workspace);
+  unsigned char* bytes = static_cast<unsigned char*>(blob);
+  st = fused_blob_crcs<kGather>(src, block_table, seq_len, bytes, b, ws, stream);
+  if (st != TOPKV_OK) return st;
+  hipLaunchKernelGGL(kv1_header_kernel, dim3(1), dim3(64), 0, stream, bytes,
+                     fields(src, seq_len, request_id, model_id, b), (const uint64_t*)ws);
+  return hipGetLastError() == hipSuccess ? TOPKV_OK : TOPKV_ERR_LAUNCH;
+}
+
+topkv_status_t topkv_kvcache1_verify_unpack(const void* blob, int64_t blob_bytes, const topkv_pool_t* dst,
+                                            const int32_t* block_table, int32_t seq_len, uint64_t request_id,
+                                            uint64_t model_id, void* workspace, int64_t workspace_bytes,
+                                            int32_t* result, hipStream_t stream) {
+  Blob b;
+  topkv_status_t st = blob_geometry(dst, seq_len, &b);
+  if (st != TOPKV_OK) return st;
+  if (!dst->base || !blob || blob_bytes < b.total || !workspace || workspace_bytes < blob_ws_bytes(b) || !result ||
+      (seq_len > 0 && !block_table) || dst->page_size <= 0 || dst->num_pages <= 0)
+    return TOPKV_ERR_INVALID_ARG;
+  if (!aligned16(blob)) return TOPKV_ERR_UNSUPPORTED;
+  if (!fused_fits(dst, seq_len, b)) {          // the two-step path: checksum, then move every layer
+    st = topkv_kvcache1_verify(dst, seq_len, request_id, model_id, blob, blob_bytes, workspace, workspace_bytes,
+                               result, stream);
+    return st != TOPKV_OK ? st : kv1_move_layers(false, dst, 0, dst->num_layers, block_table, seq_len,
+                                                 const_cast<void*>(blob), blob_bytes, stream);
+  }
+  if (topkv_internal::checked_mode()) {
+    st = topkv_internal::checked_tables(dst, 1, block_table, (seq_len + dst->page_size - 1) / dst->page_size,
+                                        nullptr, seq_len, 0, true, 0, 0, INT64_MAX, stream);
+    if (st != TOPKV_OK) return st;
+  }
+  uint64_t* ws = static_cast<uint64_t*>(workspace);
+  unsigned char* bytes = static_cast<unsigned char*>(const_cast<void*>(blob));
+  st = fused_blob_crcs<kScatter>(dst, block_table, seq_len, bytes, b, ws, stream);
+  if (st != TOPKV_OK) return st;
+  hipLaunchKernelGGL(kv1_verify_kernel, dim3(1), dim3(64), 0, stream, bytes,
+                     fields(dst, seq_len, request_id, model_id, b), (const uint64_t*)ws, result);
+  return hipGetLastError() == hipSuccess ? TOPKV_OK : TOPKV_ERR_LAUNCH;
 }
 
 topkv_status_t topkv_kvcache1_pack_layers(const topkv_pool_t* src, int32_t first_layer, int32_t num_layers,

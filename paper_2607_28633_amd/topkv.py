@@ -47,7 +47,8 @@ EXPORTS = ["topkv_pack_layer", "topkv_unpack_layer", "topkv_pack_layer_batched",
            "topkv_pack_layer_heads", "topkv_unpack_layer_heads", "topkv_reblock_layer",
            "topkv_pack_layer_shards", "topkv_unpack_layer_shards", "topkv_packed_state_bytes",
            "topkv_pack_state_layer", "topkv_unpack_state_layer", "topkv_check_state_slots",
-           "topkv_check_state_workspace_bytes", "topkv_kvcache1_pack_layers", "topkv_kvcache1_unpack_layers"]
+           "topkv_check_state_workspace_bytes", "topkv_kvcache1_pack_layers", "topkv_kvcache1_unpack_layers",
+           "topkv_kvcache1_pack_seal", "topkv_kvcache1_verify_unpack"]
 
 TOPKV_LAYOUT_PACKED = 0
 TOPKV_LAYOUT_POOL = 1
@@ -109,6 +110,9 @@ _SIGS = {
     "topkv_kvcache1_unpack_layer": (_I32, [_P, _I64, _POOL, _I32, _P, _I32, _P]),
     "topkv_kvcache1_pack_layers": (_I32, [_POOL, _I32, _I32, _P, _I32, _P, _I64, _P]),
     "topkv_kvcache1_unpack_layers": (_I32, [_P, _I64, _POOL, _I32, _I32, _P, _I32, _P]),
+    "topkv_kvcache1_pack_seal": (_I32, [_POOL, _P, _I32, ctypes.c_uint64, ctypes.c_uint64, _P, _I64, _P, _I64, _P]),
+    "topkv_kvcache1_verify_unpack": (_I32, [_P, _I64, _POOL, _P, _I32, ctypes.c_uint64, ctypes.c_uint64, _P, _I64,
+                                            _P, _P]),
     "topkv_crc64": (_I32, [_P, _I64, _P, _I64, _P, _P]),
     "topkv_crc64_workspace_bytes": (_I64, [_I64]),
     "topkv_move_layer": (_I32, [ctypes.POINTER(topkv_view_t), ctypes.POINTER(topkv_view_t), _I32, _P, _I32,
@@ -348,6 +352,21 @@ def topkv_kvcache1_verify(geometry, seq_len, request_id, model_id, blob, workspa
     _check(_lib.topkv_kvcache1_verify(ctypes.byref(_pool_arg(geometry)), int(seq_len), int(request_id),
                                       int(model_id), _ptr(blob), _nbytes(blob, blob_bytes), _ptr(workspace),
                                       _nbytes(workspace, workspace_bytes), _table_ptr(result), _stream(stream)))
+
+
+def topkv_kvcache1_pack_seal(src, block_table, seq_len, request_id, model_id, blob, workspace, blob_bytes=None,
+                             workspace_bytes=None, stream=None) -> None:
+    _check(_lib.topkv_kvcache1_pack_seal(ctypes.byref(_pool_arg(src)), _table_ptr(block_table), int(seq_len),
+                                         int(request_id), int(model_id), _ptr(blob), _nbytes(blob, blob_bytes),
+                                         _ptr(workspace), _nbytes(workspace, workspace_bytes), _stream(stream)))
+
+
+def topkv_kvcache1_verify_unpack(blob, dst, block_table, seq_len, request_id, model_id, workspace, result,
+                                 blob_bytes=None, workspace_bytes=None, stream=None) -> None:
+    _check(_lib.topkv_kvcache1_verify_unpack(_ptr(blob), _nbytes(blob, blob_bytes), ctypes.byref(_pool_arg(dst)),
+                                             _table_ptr(block_table), int(seq_len), int(request_id), int(model_id),
+                                             _ptr(workspace), _nbytes(workspace, workspace_bytes),
+                                             _table_ptr(result), _stream(stream)))
 
 
 def topkv_kvcache1_unpack_layer(blob, dst, layer, block_table, seq_len, blob_bytes=None, stream=None) -> None:

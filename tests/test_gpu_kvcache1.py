@@ -181,3 +181,117 @@ def test_kvcache1_layer_ranges(tk, case):
                 f"{case} request {r} ranges {ranges}: pool differs"
     with pytest.raises(tk.TopkvError):
         tk.topkv_kvcache1_pack_layers(src, 1, L, to_dev(wl.block_tables[0]), int(wl.seq_lens[0]), blob)
+
+
+# ---------------------------------------------------------------------------
+# One-pass whole-request calls: topkv_kvcache1_pack_seal / verify_unpack
+# ---------------------------------------------------------------------------
+
+def _fused_case(case):
+    if case == "tiny":
+        return make_workload("tiny", dst_page_size=48)
+    if case == "mla":
+        return make_workload("deepseek-v3-mla", num_layers=3, seq_lens=[700, 1, 64, 129])
+    if case == "reblock":
+        return make_workload("reblock-70b", num_layers=2, phys_layers=2, seq_lens=[300, 17, 4096])
+    # 16-byte rows and 7-token pages: many rows and page changes inside every 16-byte piece's sub-chunk
+    return make_workload("tiny", num_heads=1, head_dim=8, page_size=7, dst_page_size=5, seq_lens=[333, 0, 2, 70])
+
+
+@pytest.mark.parametrize("case", ["tiny", "mla", "reblock", "row16-p7"])
+def test_kvcache1_pack_seal_verify_unpack(tk, case):
+    """The one-pass sender writes the oracle's blob byte for byte (header and
+    checksums included); the one-pass receiver reports no mismatch and leaves
+    the pool the oracle's unpack gives."""
+    wl = _fused_case(case)
+    say(f"[kvcache1 one-pass] {case}: {wl.describe()}")
+    src_h, dst_h = host_src_pool(wl), host_dst_prefill(wl)
+    src, dst = to_dev(src_h), to_dev(dst_h)
+    geo = tk.pool_from_tensor(src)
+    want_dst = dst_h.copy()
+    res = torch.full((4,), 99, dtype=torch.int32, device="cuda")
+    for r in range(wl.num_reqs):
+        n = int(wl.seq_lens[r])
+        nbytes = tk.topkv_kvcache1_bytes(geo, n)
+        blob = torch.full((nbytes,), 0xAB, dtype=torch.uint8, device="cuda")
+        ws = torch.empty(tk.topkv_kvcache1_workspace_bytes(geo, n) // 8, dtype=torch.int64, device="cuda")
+        tk.topkv_kvcache1_pack_seal(src, to_dev(wl.block_tables[r]), n, r + 1, 9, blob, ws)
+        torch.cuda.synchronize()
+        want = okv.serialize(src_h, wl.block_tables[r], n, r + 1, 9)
+        assert blob.cpu().numpy().tobytes() == want, f"{case} request {r}: blob differs from the oracle"
+        tk.topkv_kvcache1_verify_unpack(blob, dst, to_dev(wl.dst_block_tables[r]), n, r + 1, 9, ws, res)
+        torch.cuda.synchronize()
+        assert res.cpu().tolist() == [tk.TOPKV_OK, 0, 0, 0], f"{case} request {r}"
+        for layer in range(wl.num_layers):
+            okv.unpack_layer(want, want_dst, layer, wl.dst_block_tables[r])
+    assert np.array_equal(to_host(dst), want_dst), f"{case}: unpacked pool differs"
+
+
+def test_kvcache1_one_pass_hostile_and_corrupt(tk):
+    """Table entries outside the pool: the one-pass sender leaves those rows'
+    blob bytes as they were and checksums them, exactly like the two calls it
+    replaces; the receiver skips them like topkv_kvcache1_unpack_layers.
+    Corrupted K or V bytes are reported (and the pool is still written)."""
+    wl = make_workload("tiny", dst_page_size=16)
+    say("[kvcache1 one-pass] hostile tables, corruption")
+    src, dst0 = to_dev(host_src_pool(wl)), to_dev(host_dst_prefill(wl))
+    geo = tk.pool_from_tensor(src)
+    n = int(wl.seq_lens[0])                                  # 64 tokens, 4 pages
+    bt = wl.block_tables[0].copy()
+    bt[1], bt[3] = wl.num_pages, -2
+    nbytes = tk.topkv_kvcache1_bytes(geo, n)
+    ws = torch.empty(tk.topkv_kvcache1_workspace_bytes(geo, n) // 8, dtype=torch.int64, device="cuda")
+    two = torch.full((nbytes,), 0x5C, dtype=torch.uint8, device="cuda")
+    tk.topkv_kvcache1_pack_layers(src, 0, wl.num_layers, to_dev(bt), n, two)
+    tk.topkv_kvcache1_seal(geo, n, 3, 4, two, ws)
+    one = torch.full((nbytes,), 0x5C, dtype=torch.uint8, device="cuda")
+    tk.topkv_kvcache1_pack_seal(src, to_dev(bt), n, 3, 4, one, ws)
+    torch.cuda.synchronize()
+    assert torch.equal(one, two), "one-pass blob differs from pack_layers + seal on a hostile table"
+    bt2 = wl.dst_block_tables[0].copy()
+    bt2[2] = 10 ** 6
+    want_dst, got_dst = dst0.clone(), dst0.clone()
+    tk.topkv_kvcache1_unpack_layers(two, want_dst, 0, wl.num_layers, to_dev(bt2), n)
+    res = torch.zeros(4, dtype=torch.int32, device="cuda")
+    tk.topkv_kvcache1_verify_unpack(two, got_dst, to_dev(bt2), n, 3, 4, ws, res)
+    torch.cuda.synchronize()
+    assert res.cpu().tolist() == [tk.TOPKV_OK, 0, 0, 0]
+    assert torch.equal(got_dst, want_dst), "one-pass receiver differs from unpack_layers on a hostile table"
+    k_bytes = wl.num_layers * n * wl.num_heads * wl.head_dim * 2
+    for pos, want in ((128 + 5, [tk.TOPKV_ERR_CHECKSUM, 0, 1, 0]), (128 + k_bytes + 11, [tk.TOPKV_ERR_CHECKSUM, 0, 0, 1])):
+        bad = two.clone()
+        bad[pos] ^= 0x01
+        got = dst0.clone()
+        tk.topkv_kvcache1_verify_unpack(bad, got, to_dev(bt2), n, 3, 4, ws, res)
+        torch.cuda.synchronize()
+        assert res.cpu().tolist() == want, f"corruption at byte {pos}"
+        assert not torch.equal(got, dst0), "the receiver writes the pool whatever the verdict"
+
+
+def test_kvcache1_one_pass_fullsize_70b(tk):
+    """The 80-layer 70B request (1.34 GB blob): the one-pass sender's blob and
+    the one-pass receiver's pool equal those of the two-step calls."""
+    wl = make_workload("llama3-70b-4k")
+    say(f"[kvcache1 one-pass] full size: {wl.describe()}")
+    src, dst = device_src_pool(wl), device_dst_prefill(wl)
+    geo = tk.pool_from_tensor(src)
+    n = int(wl.seq_lens[0])
+    bt, bt2 = to_dev(wl.block_tables[0]), to_dev(wl.dst_block_tables[0])
+    nbytes = tk.topkv_kvcache1_bytes(geo, n)
+    ws = torch.empty(tk.topkv_kvcache1_workspace_bytes(geo, n) // 8, dtype=torch.int64, device="cuda")
+    one = torch.empty(nbytes, dtype=torch.uint8, device="cuda")
+    tk.topkv_kvcache1_pack_seal(src, bt, n, 42, 70, one, ws)
+    two = torch.empty(nbytes, dtype=torch.uint8, device="cuda")
+    tk.topkv_kvcache1_pack_layers(src, 0, wl.num_layers, bt, n, two)
+    tk.topkv_kvcache1_seal(geo, n, 42, 70, two, ws)
+    torch.cuda.synchronize()
+    assert torch.equal(one, two), "one-pass blob differs at full size"
+    res = torch.zeros(4, dtype=torch.int32, device="cuda")
+    tk.topkv_kvcache1_verify_unpack(one, dst, bt2, n, 42, 70, ws, res)
+    torch.cuda.synchronize()
+    assert res.cpu().tolist() == [tk.TOPKV_OK, 0, 0, 0]
+    for layer in (0, 37, 79):
+        assert np.array_equal(oracle.pack_request(to_host(dst[layer])[None], 0, wl.dst_block_tables[0], n),
+                              oracle.pack_request(to_host(src[layer])[None], 0, wl.block_tables[0], n)), layer
+    del src, dst, one, two
+    torch.cuda.empty_cache()
