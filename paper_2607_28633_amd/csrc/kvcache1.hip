@@ -34,6 +34,17 @@
 //   kernel 2: one workgroup joins the span registers the same way, appends
 //     the sub-16-byte tail and applies the preset and complement.
 // Shift constants x^(8n) mod P are computed on the host.
+//
+// One-pass serialization: kernel 1 also runs with the pool as its source
+// (kGather: each 16-byte piece of a tensor is loaded from its pool slot
+// through the block table, stored to the blob and folded) or its sink
+// (kScatter: loaded from the blob, folded and stored to its pool slot), so a
+// whole request is serialized or received with the pool and the blob each
+// touched once.  A piece's pool slot follows from its tensor offset: the
+// sub-chunk's (row, byte) position is carried across sub-chunks as a floor
+// quotient and remainder, pieces add their offset with multiply-high
+// divisions, and the page entries of the next sub-chunk are loaded while the
+// current one is folded.
 #include <hip/hip_runtime.h>
 
 #include <cstdint>
@@ -290,8 +301,11 @@ __global__ __launch_bounds__(kCrcThreads) void crc64_span_kernel(const u32x4* __
       v[j] = off >= 0 ? __builtin_nontemporal_load(in + off / 16) : zero;   // off < head
     }
   };
-  // kGather: pool pieces (page entries pg loaded an iteration earlier); bad pages read the blob
-  auto gather = [&](u32x4 (&v)[kLoads], int64_t sub, const RowPos& p, const int32_t (&pg)[kLoads]) {
+  // kGather: pool pieces (page entries pg loaded an iteration earlier); bad pages read the blob.
+  // Bit j of *moved: piece j came from the pool (so the blob store writes it).
+  auto gather = [&](u32x4 (&v)[kLoads], int64_t sub, const RowPos& p, const int32_t (&pg)[kLoads],
+                    uint32_t* moved) {
+    *moved = 0;
 #pragma unroll
     for (int j = 0; j < kLoads; ++j) {
       const int64_t po = locate(p, j, pg[j]);
@@ -299,42 +313,42 @@ __global__ __launch_bounds__(kCrcThreads) void crc64_span_kernel(const u32x4* __
       v[j] = po >= 0    ? __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(ps.pool + po))
              : po == -2 ? ps.blob[off / 16]
                         : zero;
+      *moved |= (po >= 0 ? 1u : 0u) << j;
     }
   };
-  auto put = [&](const u32x4 (&v)[kLoads], int64_t sub, const RowPos& p, const int32_t (&pg)[kLoads]) {
+  auto put_blob = [&](const u32x4 (&v)[kLoads], int64_t sub, uint32_t moved) {
+#pragma unroll
+    for (int j = 0; j < kLoads; ++j)
+      if (moved >> j & 1) __builtin_nontemporal_store(v[j], ps.blob + (base + (sub << kSubLog2) + 1024 * j) / 16);
+  };
+  auto put_pool = [&](const u32x4 (&v)[kLoads], const RowPos& p, const int32_t (&pg)[kLoads]) {
 #pragma unroll
     for (int j = 0; j < kLoads; ++j) {
       const int64_t po = locate(p, j, pg[j]);
-      if (po < 0) continue;
-      if (kMode == kGather) {
-        const int64_t off = base + (sub << kSubLog2) + 1024 * j;
-        __builtin_nontemporal_store(v[j], ps.blob + off / 16);
-      } else {
-        __builtin_nontemporal_store(v[j], reinterpret_cast<u32x4*>(ps.pool + po));
-      }
+      if (po >= 0) __builtin_nontemporal_store(v[j], reinterpret_cast<u32x4*>(ps.pool + po));
     }
   };
+  uint32_t moved_cur = 0, moved_nxt = 0;
 
   RowPos pos = pos0;   // this sub-chunk's row position (pool modes)
+  const int wr = lane ^ ((lane >> 4) & 3);                        // write slot of this lane in each row
+  const int rrow = lane >> 4, rcol = 4 * (lane & 15);             // this lane's piece: row, first column
+  uint64_t fold = 0;
   if (kMode == kGather) {
     lookup(pg_a, pos);
-    gather(cur, 0, pos, pg_a);
+    gather(cur, 0, pos, pg_a, &moved_cur);
     if (span_subs > 1) lookup(pg_b, advance(pos));
   } else {
     load(cur, 0);
     if (kMode == kScatter) lookup(pg_a, pos);
   }
-  const int wr = lane ^ ((lane >> 4) & 3);                        // write slot of this lane in each row
-  const int rrow = lane >> 4, rcol = 4 * (lane & 15);             // this lane's piece: row, first column
-  uint64_t fold = 0;
   for (int64_t sub = 0; sub < span_subs; ++sub) {
     if (kMode == kGather) {
       // pg_a: this sub-chunk's entries, pg_b: the next one's (loaded a sub-chunk ago)
       const RowPos p1 = advance(pos);
-      if (sub + 1 < span_subs) gather(nxt, sub + 1, p1, pg_b);
-      put(cur, sub, pos, pg_a);
-#pragma unroll
-      for (int j = 0; j < kLoads; ++j) pg_a[j] = pg_b[j];
+      if (sub + 1 < span_subs) gather(nxt, sub + 1, p1, pg_b, &moved_nxt);
+      put_blob(cur, sub, moved_cur);
+      moved_cur = moved_nxt;
       if (sub + 2 < span_subs) lookup(pg_b, advance(p1));
       pos = p1;
     } else {
@@ -343,7 +357,7 @@ __global__ __launch_bounds__(kCrcThreads) void crc64_span_kernel(const u32x4* __
         if (kMode == kScatter) lookup(pg_b, advance(pos));
       }
       if (kMode == kScatter) {
-        put(cur, sub, pos, pg_a);
+        put_pool(cur, pos, pg_a);
 #pragma unroll
         for (int j = 0; j < kLoads; ++j) pg_a[j] = pg_b[j];
         pos = advance(pos);
