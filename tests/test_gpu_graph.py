@@ -176,3 +176,47 @@ def test_hybrid_sweep_in_a_graph(tk):
     lay = max(l for l in range(L) if wl.is_state(l))
     want = so.pack_state_layer(to_host(st_src[wl.state_slab(lay)])[None], 0, wl.state_slots)
     assert np.array_equal(to_host(out_g[0][lay])[:stb // 2], want), "last state layer vs the oracle"
+
+
+def test_graph_kvcache1_one_pass(tk):
+    """The one-pass KVCACHE1 sender and receiver captured in one graph: every
+    replay (new pool contents, cleared outputs and eager work in between)
+    leaves the blob, the verdict and the decode pool the eager calls give."""
+    from gpu_util import to_dev
+    wl = make_workload("llama3-70b-4k", num_layers=3, num_pages=600, dst_num_pages=700, seq_lens=[1000])
+    say(f"[graph] one-pass KVCACHE1: {wl.describe()}")
+    src, dst0 = device_src_pool(wl), device_dst_prefill(wl)
+    geo = tk.pool_from_tensor(src)
+    n = int(wl.seq_lens[0])
+    bt, bt2 = to_dev(wl.block_tables[0]), to_dev(wl.dst_block_tables[0])
+    nbytes = tk.topkv_kvcache1_bytes(geo, n)
+    ws_bytes = tk.topkv_kvcache1_workspace_bytes(geo, n)
+
+    def run(blob, dst, ws, res):
+        tk.topkv_kvcache1_pack_seal(src, bt, n, 11, 22, blob, ws)
+        tk.topkv_kvcache1_verify_unpack(blob, dst, bt2, n, 11, 22, ws, res)
+
+    blob_g = torch.zeros(nbytes, dtype=torch.uint8, device="cuda")
+    dst_g = dst0.clone()
+    ws_g = torch.zeros(ws_bytes // 8, dtype=torch.int64, device="cuda")
+    res_g = torch.full((4,), 7, dtype=torch.int32, device="cuda")
+    torch.cuda.synchronize()
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g):
+        run(blob_g, dst_g, ws_g, res_g)
+    torch.cuda.synchronize()
+    for replay in range(3):
+        src.view(torch.int16).add_(replay + 1)
+        blob_g.zero_()
+        dst_g.copy_(dst0)
+        res_g.fill_(7)
+        blob_e, dst_e = torch.zeros_like(blob_g), dst0.clone()
+        ws_e = torch.zeros_like(ws_g)
+        res_e = torch.full((4,), 7, dtype=torch.int32, device="cuda")
+        run(blob_e, dst_e, ws_e, res_e)
+        torch.cuda.synchronize()
+        g.replay()
+        torch.cuda.synchronize()
+        assert res_e.tolist() == [tk.TOPKV_OK, 0, 0, 0] and res_g.tolist() == res_e.tolist(), f"replay {replay}"
+        assert torch.equal(blob_g, blob_e), f"replay {replay}: blob differs"
+        assert torch.equal(dst_g.view(torch.int16), dst_e.view(torch.int16)), f"replay {replay}: pool differs"
