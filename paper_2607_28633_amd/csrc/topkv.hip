@@ -63,6 +63,9 @@
 #ifndef TOPKV_EARLY_LENS
 #define TOPKV_EARLY_LENS 1    // direct grid: earlier requests' lengths load with the slot's own words
 #endif
+#ifndef TOPKV_DIRECT_LDS_PAD
+#define TOPKV_DIRECT_LDS_PAD 0      // dynamic LDS bytes per direct-grid workgroup (caps workgroups per CU)
+#endif
 #ifndef TOPKV_THREADS
 #define TOPKV_THREADS 256     // threads per workgroup (a multiple of 64)
 #endif
@@ -657,7 +660,7 @@ topkv_status_t launch_move(bool pack, const topkv_pool_t* pool, int32_t layer, v
   p.layer_stride = layer_stride;
 
   const size_t lds = (seq_lens && !direct) ? sizeof(uint64_t) * kWaves + sizeof(int32_t) * 3 * ((size_t)num_reqs + 1)
-                                           : 0;
+                                           : (direct ? (size_t)TOPKV_DIRECT_LDS_PAD : 0);
   void* args[] = {&pool_ptr, &packed_ptr, &tables, &seq_lens, &p};
   const void* fn = reinterpret_cast<const void*>(pick_kernel(pack, vb, vpt, direct, seq_lens != nullptr));
   hipError_t e;
