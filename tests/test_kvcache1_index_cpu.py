@@ -99,6 +99,6 @@ def _check(L, NP, C, P, H, D, eb, s, seed=0):
 def test_one_pass_addressing():
     _check(2, 20, 2, 16, 2, 64, 2, 100)          # 256-byte rows, ragged last page, front padding
     _check(3, 40, 2, 16, 1, 8, 2, 33)            # 16-byte rows: many rows per sub-chunk
-    _check(2, 30, 1, 64, 1, 576, 2, 129)         # MLA latent rows (1152 B), 64-token pages
+    _check(8, 40, 1, 64, 1, 576, 2, 2000)        # MLA rows (1152 B, not dividing 64 KiB), 18 MB: carried remainder
     _check(4, 70, 2, 7, 3, 40, 2, 150)           # 240-byte rows, 7-token pages
-    _check(20, 700, 2, 16, 8, 128, 2, 512)       # 2 KiB rows, 21 MB: two sub-chunks per span
+    _check(2, 30, 2, 16, 8, 128, 2, 300)         # 2 KiB rows
