@@ -54,6 +54,12 @@
 #ifndef TOPKV_NONTEMPORAL
 #define TOPKV_NONTEMPORAL 1   // streaming hint on the bulk loads and stores
 #endif
+#ifndef TOPKV_NT_LOADS
+#define TOPKV_NT_LOADS TOPKV_NONTEMPORAL
+#endif
+#ifndef TOPKV_NT_STORES
+#define TOPKV_NT_STORES TOPKV_NONTEMPORAL
+#endif
 #ifndef TOPKV_ROUTE_SINGLE
 #define TOPKV_ROUTE_SINGLE 1  // one whole-request move with a device length runs the layout-move direct grid
 #endif
@@ -187,7 +193,7 @@ __device__ __forceinline__ void load_tile(typename Vec<VB>::type (&v)[VPT], cons
   if (nv == kThreads * VPT) {
 #pragma unroll
     for (int j = 0; j < VPT; ++j) {
-#if TOPKV_NONTEMPORAL
+#if TOPKV_NT_LOADS
       v[j] = __builtin_nontemporal_load(s + j * kThreads + threadIdx.x);
 #else
       v[j] = s[j * kThreads + threadIdx.x];
@@ -213,7 +219,7 @@ __device__ __forceinline__ void store_tile(char* __restrict__ dst, const typenam
   if (nv == kThreads * VPT) {
 #pragma unroll
     for (int j = 0; j < VPT; ++j) {
-#if TOPKV_NONTEMPORAL
+#if TOPKV_NT_STORES
       __builtin_nontemporal_store(v[j], d + j * kThreads + threadIdx.x);
 #else
       d[j * kThreads + threadIdx.x] = v[j];
