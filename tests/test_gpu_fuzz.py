@@ -4,7 +4,8 @@ either side, up to 6 requests with empty and one-token ones, random windows
 and head slices, tensor-parallel shards of a packed side, and every pair of
 views (packed, slot-major, head-major).
 Each case is small; together they cover piece widths 1-16 bytes, ragged
-tiles and both grid modes."""
+tiles and both grid modes.  A third set sends random KVCACHE1 geometries
+through the one-pass sender and receiver."""
 import random
 
 import numpy as np
@@ -119,3 +120,48 @@ def test_fuzz_layout_moves(tk, seed):
     tk.topkv_move_layer(sv, dv, len(c["lens"]), lens, c["hc"], c["W"])
     torch.cuda.synchronize()
     assert np.array_equal(to_host(d_d), want), f"seed {seed}: {sk} -> {dk} differs"
+
+
+def _kv1_case(seed):
+    rng = random.Random(seed)
+    eb = rng.choice([1, 2, 4, 8])
+    c = dict(C=rng.choice([1, 2]), H=rng.randint(1, 4), eb=eb, P=rng.randint(1, 40), P2=rng.randint(1, 40),
+             L=rng.randint(1, 4))
+    c["D"] = (16 // eb) * rng.randint(1, 6)                  # rows are whole 16-byte pieces (KVCACHE1 layout)
+    c["n"] = rng.choice([0, 1, rng.randint(1, 700), rng.randint(1, 700)])
+    for side, P in (("1", c["P"]), ("2", c["P2"])):
+        k = _pages(c["n"], P)
+        NP = k + rng.randint(1, 6)
+        perm = list(range(NP))
+        rng.shuffle(perm)
+        c["NP" + side], c["bt" + side] = NP, np.array(perm[:max(k, 1)], dtype=np.int32)
+    return c
+
+
+@pytest.mark.parametrize("seed", range(40))
+def test_fuzz_kvcache1_one_pass(tk, seed):
+    """The one-pass KVCACHE1 sender and receiver on a random geometry: the blob
+    is the oracle's serialization byte for byte and the receiver rebuilds the
+    oracle's pool (every layer, the destination at another page size)."""
+    import oracle.kvcache1 as okv
+    c = _kv1_case(5000 + seed)
+    say(f"[fuzz] kvcache1 seed {seed}: L{c['L']} C{c['C']} H{c['H']} D{c['D']} u{8 * c['eb']} "
+        f"P{c['P']}->{c['P2']} n {c['n']}")
+    npr = np.random.default_rng(5000 + seed)
+    src_h, dst_h = _pool(c, c["NP1"], c["P"], False, npr), _pool(c, c["NP2"], c["P2"], False, npr)
+    src, dst = to_dev(src_h), to_dev(dst_h)
+    geo = tk.pool_from_tensor(src)
+    n = c["n"]
+    nbytes = tk.topkv_kvcache1_bytes(geo, n)
+    blob = torch.full((nbytes,), 0x3B, dtype=torch.uint8, device="cuda")
+    ws = torch.empty(tk.topkv_kvcache1_workspace_bytes(geo, n) // 8, dtype=torch.int64, device="cuda")
+    res = torch.full((4,), 9, dtype=torch.int32, device="cuda")
+    tk.topkv_kvcache1_pack_seal(src, to_dev(c["bt1"]), n, seed, 77, blob, ws)
+    tk.topkv_kvcache1_verify_unpack(blob, dst, to_dev(c["bt2"]), n, seed, 77, ws, res)
+    torch.cuda.synchronize()
+    want = okv.serialize(src_h, c["bt1"], n, seed, 77)
+    assert blob.cpu().numpy().tobytes() == want, f"seed {seed}: blob differs"
+    assert res.cpu().tolist() == [tk.TOPKV_OK, 0, 0, 0], f"seed {seed}"
+    for layer in range(c["L"]):
+        okv.unpack_layer(want, dst_h, layer, c["bt2"])
+    assert np.array_equal(to_host(dst), dst_h), f"seed {seed}: unpacked pool differs"
