@@ -266,33 +266,38 @@ __global__ __launch_bounds__(kCrcThreads) void crc64_span_kernel(const u32x4* __
     *inrow = x - q * (uint32_t)ps.row_bytes;
     return true;
   };
-  auto lookup = [&](int32_t (&pg)[kLoads], const RowPos& p) {
+  // A piece's pool offset splits into a page-independent part pb (layer,
+  // plane, slot and byte; -1 in the padding), worked out once per piece
+  // together with its table index, and the page entry pg loaded from the
+  // table: offset = pb + pg * page_bytes (one 32 x 32 -> 64-bit multiply-add).
+  auto lookup = [&](int64_t (&pb)[kLoads], int32_t (&pg)[kLoads], const RowPos& p) {
 #pragma unroll
     for (int j = 0; j < kLoads; ++j) {
       uint32_t row, inrow;
+      pb[j] = -1;
       pg[j] = -1;
       if (row_of(p, j, &row, &inrow)) {
         const uint32_t l = div32(row, ps.d_seq);
-        pg[j] = ps.table[div32(row - l * (uint32_t)ps.seq_len, ps.d_page)];
+        const uint32_t t = row - l * (uint32_t)ps.seq_len;
+        const uint32_t i = div32(t, ps.d_page);
+        pg[j] = ps.table[i];
+        pb[j] = (int64_t)(ps.first_layer + (int32_t)l) * ps.layer_bytes + ps.plane_off +
+                (int64_t)((uint64_t)(t - i * (uint32_t)ps.page_size) * (uint32_t)ps.row_bytes) + inrow;
       }
     }
   };
-  // pool byte of the piece: -1 in the padding, -2 when its page entry is out of range
-  auto locate = [&](const RowPos& p, int j, int32_t page) -> int64_t {
-    uint32_t row, inrow;
-    if (!row_of(p, j, &row, &inrow)) return -1;
+  // pool byte of a piece: -1 in the padding, -2 when its page entry is out of range
+  auto slot_of = [&](int64_t pb, int32_t page) -> int64_t {
+    if (pb < 0) return -1;
     if (page < 0 || (int64_t)page >= ps.num_pages) return -2;
-    const uint32_t l = div32(row, ps.d_seq);
-    const uint32_t t = row - l * (uint32_t)ps.seq_len;
-    const uint32_t i = div32(t, ps.d_page);
-    return ((int64_t)ps.first_layer + l) * ps.layer_bytes + (int64_t)page * ps.page_bytes + ps.plane_off +
-           (int64_t)(t - i * (uint32_t)ps.page_size) * ps.row_bytes + inrow;
+    return pb + (int64_t)((uint64_t)(uint32_t)page * (uint32_t)ps.page_bytes);
   };
   const u32x4 zero = {0u, 0u, 0u, 0u};
   const u32x4* in = kMode == kScatter ? ps.blob : data;
 
   u32x4 cur[kLoads], nxt[kLoads];
   int32_t pg_a[kLoads] = {}, pg_b[kLoads] = {};
+  int64_t pb_a[kLoads] = {}, pb_b[kLoads] = {};
   // kStream / kScatter: contiguous input (the data, or the blob tensor)
   auto load = [&](u32x4 (&v)[kLoads], int64_t sub) {
 #pragma unroll
@@ -303,12 +308,12 @@ __global__ __launch_bounds__(kCrcThreads) void crc64_span_kernel(const u32x4* __
   };
   // kGather: pool pieces (page entries pg loaded an iteration earlier); bad pages read the blob.
   // Bit j of *moved: piece j came from the pool (so the blob store writes it).
-  auto gather = [&](u32x4 (&v)[kLoads], int64_t sub, const RowPos& p, const int32_t (&pg)[kLoads],
+  auto gather = [&](u32x4 (&v)[kLoads], int64_t sub, const int64_t (&pb)[kLoads], const int32_t (&pg)[kLoads],
                     uint32_t* moved) {
     *moved = 0;
 #pragma unroll
     for (int j = 0; j < kLoads; ++j) {
-      const int64_t po = locate(p, j, pg[j]);
+      const int64_t po = slot_of(pb[j], pg[j]);
       const int64_t off = base + (sub << kSubLog2) + 1024 * j;
       v[j] = po >= 0    ? __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(ps.pool + po))
              : po == -2 ? ps.blob[off / 16]
@@ -321,10 +326,10 @@ __global__ __launch_bounds__(kCrcThreads) void crc64_span_kernel(const u32x4* __
     for (int j = 0; j < kLoads; ++j)
       if (moved >> j & 1) __builtin_nontemporal_store(v[j], ps.blob + (base + (sub << kSubLog2) + 1024 * j) / 16);
   };
-  auto put_pool = [&](const u32x4 (&v)[kLoads], const RowPos& p, const int32_t (&pg)[kLoads]) {
+  auto put_pool = [&](const u32x4 (&v)[kLoads], const int64_t (&pb)[kLoads], const int32_t (&pg)[kLoads]) {
 #pragma unroll
     for (int j = 0; j < kLoads; ++j) {
-      const int64_t po = locate(p, j, pg[j]);
+      const int64_t po = slot_of(pb[j], pg[j]);
       if (po >= 0) __builtin_nontemporal_store(v[j], reinterpret_cast<u32x4*>(ps.pool + po));
     }
   };
@@ -335,31 +340,34 @@ __global__ __launch_bounds__(kCrcThreads) void crc64_span_kernel(const u32x4* __
   const int rrow = lane >> 4, rcol = 4 * (lane & 15);             // this lane's piece: row, first column
   uint64_t fold = 0;
   if (kMode == kGather) {
-    lookup(pg_a, pos);
-    gather(cur, 0, pos, pg_a, &moved_cur);
-    if (span_subs > 1) lookup(pg_b, advance(pos));
+    lookup(pb_a, pg_a, pos);
+    gather(cur, 0, pb_a, pg_a, &moved_cur);
+    if (span_subs > 1) lookup(pb_b, pg_b, advance(pos));
   } else {
     load(cur, 0);
-    if (kMode == kScatter) lookup(pg_a, pos);
+    if (kMode == kScatter) lookup(pb_a, pg_a, pos);
   }
   for (int64_t sub = 0; sub < span_subs; ++sub) {
     if (kMode == kGather) {
       // pg_a: this sub-chunk's entries, pg_b: the next one's (loaded a sub-chunk ago)
       const RowPos p1 = advance(pos);
-      if (sub + 1 < span_subs) gather(nxt, sub + 1, p1, pg_b, &moved_nxt);
+      if (sub + 1 < span_subs) gather(nxt, sub + 1, pb_b, pg_b, &moved_nxt);
       put_blob(cur, sub, moved_cur);
       moved_cur = moved_nxt;
-      if (sub + 2 < span_subs) lookup(pg_b, advance(p1));
+      if (sub + 2 < span_subs) lookup(pb_b, pg_b, advance(p1));
       pos = p1;
     } else {
       if (sub + 1 < span_subs) {
         load(nxt, sub + 1);
-        if (kMode == kScatter) lookup(pg_b, advance(pos));
+        if (kMode == kScatter) lookup(pb_b, pg_b, advance(pos));
       }
       if (kMode == kScatter) {
-        put_pool(cur, pos, pg_a);
+        put_pool(cur, pb_a, pg_a);
 #pragma unroll
-        for (int j = 0; j < kLoads; ++j) pg_a[j] = pg_b[j];
+        for (int j = 0; j < kLoads; ++j) {
+          pg_a[j] = pg_b[j];
+          pb_a[j] = pb_b[j];
+        }
         pos = advance(pos);
       }
     }
@@ -605,7 +613,7 @@ bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15) == 
 // and the blob themselves (32-bit row and token arithmetic, 16-byte pieces).
 bool fused_fits(const topkv_pool_t* pool, int32_t seq_len, const Blob& b) {
   return seq_len > 0 && (int64_t)pool->num_layers * seq_len < INT32_MAX && b.row < INT32_MAX - 2 * kSub &&
-         aligned16(pool->base);
+         (int64_t)pool->planes * pool->page_size * b.row <= UINT32_MAX && aligned16(pool->base);
 }
 
 // Both checksums of the blob body into ws[0..1] while the K and V tensors of
