@@ -175,17 +175,20 @@ topkv_status_t checked_tables(const topkv_pool_t* pool, int32_t num_reqs, const 
       return TOPKV_ERR_DEVICE;
     lens = staged;
   }
-  st = launch_table_check(pool, num_reqs, block_tables, bt_stride, lens, window, duplicates,
-                          reinterpret_cast<uint32_t*>(b.ptr + kBitmapOffset), result, stream);
-  if (st != TOPKV_OK) return st;
   int32_t res[4] = {0, 0, 0, 0};
   std::vector<int32_t> host(seq_lens ? (size_t)num_reqs : 1, seq_len);
-  if (hipMemcpyAsync(res, result, sizeof(res), hipMemcpyDeviceToHost, stream) != hipSuccess)
-    return TOPKV_ERR_DEVICE;
-  if (seq_lens && hipMemcpyAsync(host.data(), seq_lens, sizeof(int32_t) * (size_t)num_reqs, hipMemcpyDeviceToHost,
-                                 stream) != hipSuccess)
-    return TOPKV_ERR_DEVICE;
-  if (hipStreamSynchronize(stream) != hipSuccess) return TOPKV_ERR_DEVICE;
+  st = launch_table_check(pool, num_reqs, block_tables, bt_stride, lens, window, duplicates,
+                          reinterpret_cast<uint32_t*>(b.ptr + kBitmapOffset), result, stream);
+  if (st == TOPKV_OK && hipMemcpyAsync(res, result, sizeof(res), hipMemcpyDeviceToHost, stream) != hipSuccess)
+    st = TOPKV_ERR_DEVICE;
+  if (st == TOPKV_OK && seq_lens &&
+      hipMemcpyAsync(host.data(), seq_lens, sizeof(int32_t) * (size_t)num_reqs, hipMemcpyDeviceToHost, stream) !=
+          hipSuccess)
+    st = TOPKV_ERR_DEVICE;
+  // Whatever was queued (the staged length's copy included) completes before
+  // this frame and the buffer's lock go away, also on the failure paths.
+  if (hipStreamSynchronize(stream) != hipSuccess && st == TOPKV_OK) st = TOPKV_ERR_DEVICE;
+  if (st != TOPKV_OK) return st;
   if (res[0] != TOPKV_OK) return TOPKV_ERR_BOUNDS;
   // The packed buffer must hold every kept token (a batched request that
   // would cross its end is otherwise left unmoved); lengths are in range here.
@@ -210,13 +213,13 @@ topkv_status_t checked_slots(const topkv_state_pool_t* pool, int32_t num_reqs, c
   st = grow(b, kBitmapOffset + 4 * words);
   if (st != TOPKV_OK) return st;
   int32_t* result = reinterpret_cast<int32_t*>(b.ptr);
+  int32_t res[4] = {0, 0, 0, 0};
   st = topkv_check_state_slots(pool, num_reqs, slots, duplicates ? 1 : 0, b.ptr + kBitmapOffset, 4 * words, result,
                                stream);
+  if (st == TOPKV_OK && hipMemcpyAsync(res, result, sizeof(res), hipMemcpyDeviceToHost, stream) != hipSuccess)
+    st = TOPKV_ERR_DEVICE;
+  if (hipStreamSynchronize(stream) != hipSuccess && st == TOPKV_OK) st = TOPKV_ERR_DEVICE;
   if (st != TOPKV_OK) return st;
-  int32_t res[4] = {0, 0, 0, 0};
-  if (hipMemcpyAsync(res, result, sizeof(res), hipMemcpyDeviceToHost, stream) != hipSuccess)
-    return TOPKV_ERR_DEVICE;
-  if (hipStreamSynchronize(stream) != hipSuccess) return TOPKV_ERR_DEVICE;
   return res[0] == TOPKV_OK ? TOPKV_OK : TOPKV_ERR_BOUNDS;
 }
 
@@ -263,7 +266,7 @@ topkv_status_t topkv_check_state_slots(const topkv_state_pool_t* pool, int32_t n
                      result);
   if (hipGetLastError() != hipSuccess) return TOPKV_ERR_LAUNCH;
   if (num_reqs > 0) {
-    hipLaunchKernelGGL(kv_check_slots_kernel, dim3((unsigned)((num_reqs + 255) / 256)), dim3(256), 0, stream,
+    hipLaunchKernelGGL(kv_check_slots_kernel, dim3((unsigned)(((int64_t)num_reqs + 255) / 256)), dim3(256), 0, stream,
                        slots, num_reqs, pool->num_slots, (int32_t)dup, bitmap, result);
     if (hipGetLastError() != hipSuccess) return TOPKV_ERR_LAUNCH;
   }

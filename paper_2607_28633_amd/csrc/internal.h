@@ -31,6 +31,12 @@ topkv_status_t placed_layers_move(bool pack, const topkv_pool_t* pool, int32_t f
                                   void* packed, int64_t packed_cap, int64_t plane_stride, int64_t layer_stride,
                                   const int32_t* block_table, int32_t seq_len, hipStream_t stream);
 
+// The pool descriptor checks every pack/unpack applies (positive sizes,
+// element size 1/2/4/8, no overflow of the pool's byte size, row and page
+// count within 32 bits): TOPKV_OK, or the status such a call would return.
+__attribute__((visibility("hidden")))
+topkv_status_t pool_ok(const topkv_pool_t* pool);
+
 // Checked mode: true when the environment holds TOPKV_CHECKED=1 (read on
 // every call, so it can be switched at run time).
 __attribute__((visibility("hidden")))

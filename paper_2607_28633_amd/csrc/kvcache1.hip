@@ -509,7 +509,8 @@ topkv_status_t blob_geometry(const topkv_pool_t* g, int32_t seq_len, Blob* b) {
     return TOPKV_ERR_INVALID_ARG;
   int64_t row, tensor;
   if (__builtin_mul_overflow((int64_t)g->num_heads * g->head_dim, (int64_t)g->elem_bytes, &row) ||
-      __builtin_mul_overflow(row * seq_len, (int64_t)g->num_layers, &tensor))
+      __builtin_mul_overflow(row, (int64_t)seq_len, &tensor) ||
+      __builtin_mul_overflow(tensor, (int64_t)g->num_layers, &tensor) || tensor > INT64_MAX / 2 - kHeaderBytes)
     return TOPKV_ERR_UNSUPPORTED;
   if (row % 16) return TOPKV_ERR_UNSUPPORTED;   // tensors must stay 16-byte aligned inside the blob
   b->row = row;
@@ -791,6 +792,8 @@ topkv_status_t topkv_kvcache1_pack_seal(const topkv_pool_t* src, const int32_t* 
   if (!src->base || !blob || blob_bytes < b.total || !workspace || workspace_bytes < blob_ws_bytes(b) ||
       (seq_len > 0 && !block_table) || src->page_size <= 0 || src->num_pages <= 0)
     return TOPKV_ERR_INVALID_ARG;
+  st = topkv_internal::pool_ok(src);      // the descriptor checks of every pack/unpack, on either path
+  if (st != TOPKV_OK) return st;
   if (!aligned16(blob)) return TOPKV_ERR_UNSUPPORTED;
   if (!fused_fits(src, seq_len, b)) {          // the two-step path: move every layer, then checksum
     st = kv1_move_layers(true, src, 0, src->num_layers, block_table, seq_len, blob, blob_bytes, stream);
@@ -821,6 +824,8 @@ topkv_status_t topkv_kvcache1_verify_unpack(const void* blob, int64_t blob_bytes
   if (!dst->base || !blob || blob_bytes < b.total || !workspace || workspace_bytes < blob_ws_bytes(b) || !result ||
       (seq_len > 0 && !block_table) || dst->page_size <= 0 || dst->num_pages <= 0)
     return TOPKV_ERR_INVALID_ARG;
+  st = topkv_internal::pool_ok(dst);      // the descriptor checks of every pack/unpack, on either path
+  if (st != TOPKV_OK) return st;
   if (!aligned16(blob)) return TOPKV_ERR_UNSUPPORTED;
   if (!fused_fits(dst, seq_len, b)) {          // the two-step path: checksum, then move every layer
     st = topkv_kvcache1_verify(dst, seq_len, request_id, model_id, blob, blob_bytes, workspace, workspace_bytes,

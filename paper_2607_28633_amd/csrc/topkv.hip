@@ -574,9 +574,10 @@ topkv_status_t launch_move(bool pack, const topkv_pool_t* pool, int32_t layer, v
   if (topkv_internal::checked_mode()) {
     // packed bytes per kept token, and (placed planes) the bytes before the last plane's rows
     const int64_t per_token = plane_stride > 0 ? g.row_bytes : (int64_t)pool->planes * g.row_bytes;
-    int64_t fixed = 0;
+    int64_t fixed = 0, planes_before = 0;
     if (plane_stride > 0 && (__builtin_mul_overflow((int64_t)(layers - 1), layer_stride, &fixed) ||
-                             __builtin_add_overflow(fixed, (int64_t)(pool->planes - 1) * plane_stride, &fixed)))
+                             __builtin_mul_overflow((int64_t)(pool->planes - 1), plane_stride, &planes_before) ||
+                             __builtin_add_overflow(fixed, planes_before, &fixed)))
       return TOPKV_ERR_UNSUPPORTED;
     st = topkv_internal::checked_tables(pool, seq_lens ? num_reqs : 1, tables, bt_stride, seq_lens, n_single,
                                         window, !pack, per_token, fixed, packed_cap, launch->stream);
@@ -680,8 +681,9 @@ topkv_status_t launch_move(bool pack, const topkv_pool_t* pool, int32_t layer, v
 
 int64_t single_bytes(const topkv_pool_t* pool, int32_t n) {
   int64_t b;
-  if (__builtin_mul_overflow((int64_t)pool->num_heads * pool->head_dim * pool->elem_bytes,
-                             (int64_t)pool->planes * n, &b))
+  if (__builtin_mul_overflow((int64_t)pool->num_heads, (int64_t)pool->head_dim, &b) ||
+      __builtin_mul_overflow(b, (int64_t)pool->elem_bytes, &b) ||
+      __builtin_mul_overflow(b, (int64_t)pool->planes * n, &b))
     return -1;
   return b;
 }
@@ -689,6 +691,11 @@ int64_t single_bytes(const topkv_pool_t* pool, int32_t n) {
 }  // namespace topkv
 
 namespace topkv_internal {
+
+topkv_status_t pool_ok(const topkv_pool_t* pool) {
+  topkv::Geometry g;
+  return topkv::pool_geometry(pool, 0, &g);
+}
 
 topkv_status_t placed_layers_move(bool pack, const topkv_pool_t* pool, int32_t first_layer, int32_t layers,
                                   void* packed, int64_t packed_cap, int64_t plane_stride, int64_t layer_stride,

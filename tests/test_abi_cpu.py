@@ -227,6 +227,26 @@ def test_kvcache1_layer_range_validation(tk):
     tk.topkv_kvcache1_pack_layers(good, 1, 0, bt, 16, blob, blob_bytes=nbytes, stream=0)
 
 
+def test_kvcache1_one_pass_refuses_bad_pool_descriptors(tk):
+    """The one-pass serializer and receiver apply the pool checks of every
+    pack/unpack before choosing a path (element size 1/2/4/8, page count
+    within 32 bits), and a blob size that overflows is refused."""
+    INV, UNS = tk.TOPKV_ERR_INVALID_ARG, tk.TOPKV_ERR_UNSUPPORTED
+    bt, blob, ws, res = 0x20000, 0x40000, 0x60000, 0x70000
+    big = 1 << 40
+    for pool, code in ((_pool(tk, num_heads=1, head_dim=16, elem_bytes=3), INV),   # 48-byte rows
+                       (_pool(tk, num_pages=1 << 33), UNS)):
+        nbytes = tk.topkv_kvcache1_bytes(pool, 16)
+        assert nbytes > 0
+        _expect(tk, code, tk.topkv_kvcache1_pack_seal, pool, bt, 16, 1, 2, blob, ws, blob_bytes=nbytes,
+                workspace_bytes=big)
+        _expect(tk, code, tk.topkv_kvcache1_verify_unpack, blob, pool, bt, 16, 1, 2, ws, res, blob_bytes=nbytes,
+                workspace_bytes=big)
+    huge = _pool(tk, num_heads=1 << 20, head_dim=1 << 20, num_layers=1 << 20)
+    assert tk.topkv_kvcache1_bytes(huge, 1 << 20) == -1
+    assert tk.topkv_kvcache1_workspace_bytes(huge, 1 << 20) == -1
+
+
 def test_checked_mode_validates_arguments_first(tk, monkeypatch):
     """With TOPKV_CHECKED=1 the host-side argument checks still come first:
     a call with bad arguments is refused before checked mode touches the
