@@ -632,9 +632,11 @@ topkv_status_t move_layer_impl(const topkv_view_t* src, const topkv_view_t* dst,
   const int64_t vpg = gran / vb;
   const int64_t gpt = head_count / heads_per_gran;
   // Upper bound of pieces in the launch; indices are 32-bit in the kernel.
-  const int64_t bound = (int64_t)num_reqs * max_tok * geo->planes * gpt * vpg;
   if (max_tok <= 0) return TOPKV_OK;
-  if (bound >= ((int64_t)1 << 31) || vpg >= ((int64_t)1 << 31)) return TOPKV_ERR_UNSUPPORTED;
+  int64_t bound;
+  if (__builtin_mul_overflow((int64_t)num_reqs * max_tok, (int64_t)geo->planes, &bound) ||
+      __builtin_mul_overflow(bound, gpt * vpg, &bound) || bound >= ((int64_t)1 << 31) || vpg >= ((int64_t)1 << 31))
+    return TOPKV_ERR_UNSUPPORTED;
   // Skipped pieces load from the source's base, so it must hold one piece; a
   // packed source smaller than that holds nothing to move.
   if (src->layout == TOPKV_LAYOUT_PACKED && packed_cap < vb) return TOPKV_OK;
