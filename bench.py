@@ -777,7 +777,10 @@ def run_pipeline(args, check=None):
       dma_side_pack - as dma, with the pack on a second stream after the
               layer's compute, so it can overlap the next layer's compute.
     Measured: compute alone, transfer alone (side placement), both back to
-    back (serial), and each placement alone and overlapped.
+    back (serial), and each placement alone and overlapped.  The receive side
+    is timed after them: every layer copied host -> device by the shipper
+    (copy_in), every layer unpacked into a decode pool (unpack), and both with
+    each layer unpacked as soon as its copy is in (receive).
     hidden = 1 - exposed / transfer with exposed = pipelined - compute, beside
     the paper's model T_eff = max(T_last, T_xfer - T_rem) (T_last: the final
     layer's prefill compute; T_rem: the compute after the first layer).  With `check(placement, host)`, the
@@ -788,7 +791,7 @@ def run_pipeline(args, check=None):
     import torch
 
     from paper_2607_28633_amd import topkv
-    from paper_2607_28633_amd.workloads import WORKLOADS, device_src_pool, make_workload
+    from paper_2607_28633_amd.workloads import WORKLOADS, device_dst_prefill, device_src_pool, make_workload
 
     torch.cuda.set_device(0)
     wl = make_workload(args.workload)
@@ -924,6 +927,45 @@ def run_pipeline(args, check=None):
         variants[name] = {key: round(x, 4) for key, x in v.items()}
         if check is not None:
             check(name, host)
+
+    # Receive side: the decode GPU takes each layer from pinned host memory on
+    # a DMA engine and unpacks it into its own pool (its own page order) as
+    # soon as that layer's copy is in, while later layers' copies continue.
+    # The host buffer holds the wire bytes of the last placement run above.
+    dst = device_dst_prefill(wl)
+    bt2 = torch.from_numpy(wl.dst_block_tables).cuda()
+    unpack = [topkv.prepare_unpack_layer_batched_ex(packed[l], dst, l % wl.phys_layers, R, bt2, bt2.shape[1], lens,
+                                                    src_bytes=nbytes, stream=main) for l in range(L)]
+
+    def copy_in():
+        last = 0
+        for l in range(L):
+            last = topkv.topkv_dma_submit(dma, None, packed[l], host[l], nbytes)
+        topkv.topkv_dma_wait(dma, last)
+
+    def receive():
+        tickets = [topkv.topkv_dma_submit(dma, None, packed[l], host[l], nbytes) for l in range(L)]
+        for l in range(L):
+            topkv.topkv_dma_wait(dma, tickets[l])
+            unpack[l]()
+
+    def clocked(body):
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        body()
+        torch.cuda.synchronize()
+        return (time.perf_counter() - t0) * 1e3
+
+    def least(body):
+        clocked(body)
+        return min(clocked(body) for _ in range(max(1, args.steps)))
+
+    recv = {"copy_in_ms": least(copy_in), "unpack_ms": least(lambda: [u() for u in unpack]),
+            "receive_ms": least(receive)}
+    recv["exposed_unpack_ms"] = max(0.0, recv["receive_ms"] - recv["copy_in_ms"])
+    recv["hidden_unpack"] = 1 - recv["exposed_unpack_ms"] / recv["unpack_ms"]
+    recv = {key: round(x, 4) for key, x in recv.items()}
+    recv["link_gbs"] = round(L * nbytes / (recv["copy_in_ms"] * 1e-3) / 1e9, 1)
     topkv.topkv_dma_destroy(dma)
 
     top = max(variants, key=lambda n: variants[n]["hidden"])
@@ -940,6 +982,7 @@ def run_pipeline(args, check=None):
                    "prefill": f"bf16 GEMM [{M}x{N}]x[{N}x{N}] per layer", "best_placement": top},
         "ms": {key: round(x, 3) for key, x in runs.items()},
         "placements": variants,
+        "receive": recv,
         "per_layer_ms": {"prefill": round(layer_ms, 4), "transfer": round(t_xfer / L, 4)},
         "link_gbs": round(L * nbytes / (t_xfer * 1e-3) / 1e9, 1),
         "model": {"T_xfer_ms": round(t_xfer, 3), "T_rem_ms": round(t_rem, 3), "T_eff_ms": round(t_eff, 3),

@@ -74,3 +74,49 @@ def test_dma_shipper_copies_in_order():
         assert e.value.status == topkv.TOPKV_ERR_BOUNDS
     finally:
         topkv.topkv_dma_destroy(dma)
+
+
+def test_receive_side_ships_into_the_decode_pool():
+    """The decode half of the pipeline (Section 5.2): each packed layer arrives
+    in pinned host memory, the shipper copies it host -> device on a DMA
+    engine, and the layer is unpacked into the decode pool (its own page
+    order) as soon as its copy is done, while later layers' copies are still
+    in flight.  The device staging buffer is poisoned first; every layer of
+    the decode pool must match the oracle's unpack of the oracle's pack, and
+    nothing outside the requests' slots may change."""
+    import torch
+
+    from paper_2607_28633_amd import topkv
+    from paper_2607_28633_amd.workloads import host_dst_prefill, host_src_pool
+    from gpu_util import to_dev
+
+    wl = make_workload("llama3-8b", num_layers=4, num_pages=600, dst_num_pages=700, seq_lens=[4096, 1000, 17])
+    say(f"[receive] llama3-8b shape, {wl.num_layers} layers, lengths {wl.seq_lens.tolist()}")
+    src_h, dst_h = host_src_pool(wl), host_dst_prefill(wl)
+    L = wl.num_layers
+    wire = [oracle.pack_layer(src_h, l, wl.block_tables, wl.seq_lens) for l in range(L)]   # the sender's bytes
+    nbytes = wire[0].size * 2
+    host = torch.empty((L, nbytes // 2), dtype=torch.int16, pin_memory=True)
+    for l in range(L):
+        host[l].copy_(torch.from_numpy(wire[l].view(np.int16)))
+    staging = torch.full((L, nbytes // 2), -1, dtype=torch.int16, device="cuda")
+    dst = to_dev(dst_h)
+    bt2, lens = to_dev(wl.dst_block_tables), to_dev(wl.seq_lens)
+    torch.cuda.synchronize()
+    dma = topkv.topkv_dma_create()
+    try:
+        tickets = [topkv.topkv_dma_submit(dma, None, staging[l], host[l], nbytes) for l in range(L)]
+        for l in range(L):
+            topkv.topkv_dma_wait(dma, tickets[l])      # layer l is in HBM: unpack it, later copies continue
+            topkv.topkv_unpack_layer_batched(staging[l], dst, l, wl.num_reqs, bt2, bt2.shape[1], lens,
+                                             src_bytes=nbytes)
+        torch.cuda.synchronize()
+    finally:
+        topkv.topkv_dma_destroy(dma)
+    want = dst_h.copy()
+    for l in range(L):
+        oracle.unpack_layer(wire[l], want, l, wl.dst_block_tables, wl.seq_lens)
+    got = to_host(dst)
+    for l in range(L):
+        assert np.array_equal(got[l], want[l]), \
+            f"receive layer {l}: {int((got[l] != want[l]).sum())} elements differ"
