@@ -543,7 +543,10 @@ int64_t topkv_check_state_workspace_bytes(const topkv_state_pool_t* pool);
 /* Layer shipper (Sec. 5.2: layer l's cache leaves while layers l+1 .. L still
  * compute).  Copies run on the GPU's DMA engines (ROCr asynchronous copies),
  * so they take no compute unit from the kernels still running; a worker
- * thread starts each copy once its `ready` event has completed.
+ * thread starts each copy once its `ready` event has completed.  Either
+ * direction works: the sender ships packed layers device -> pinned host, the
+ * receiver copies them pinned host -> device and unpacks each layer once
+ * topkv_dma_wait has returned for its ticket.
  *
  * topkv_dma_create: a shipper for the current HIP device, returned in *out
  *   (owned by the caller; free it with topkv_dma_destroy).  TOPKV_ERR_DEVICE

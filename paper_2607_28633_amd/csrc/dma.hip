@@ -9,7 +9,9 @@
 // hsa_amd_memory_async_copy drives the GPU's DMA engines instead and uses no
 // compute unit.  A host worker thread turns "event completed" into "start the
 // copy" (HIP events are not HSA signals), keeping up to kInFlight copies
-// outstanding; tickets complete in submission order.
+// outstanding; tickets complete in submission order.  The receiving side
+// uses the same path the other way round: pinned host memory into device
+// memory, each layer unpacked once its ticket has completed.
 #include <hip/hip_runtime.h>
 #include <hsa/hsa.h>
 #include <hsa/hsa_ext_amd.h>
