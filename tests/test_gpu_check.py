@@ -265,3 +265,44 @@ def test_checked_mode_layout_moves(tk):
         tk.topkv_pack_layer_heads(c.src, 1, wl.num_reqs, to_dev(bt), bt.shape[1], lens, 1, 1, half, dst_bytes=2 * nh)
         torch.cuda.synchronize()
         assert np.array_equal(to_host(half)[:nh], rs.pack_layer_heads(c.src_h, 1, bt, wl.seq_lens, 1, 1))
+
+
+def test_checked_mode_one_pass_kvcache1(tk):
+    """The one-pass KVCACHE1 calls under checked mode: a table entry outside
+    the pool is refused on both sides and a page named twice by the receiver's
+    table is refused, writing neither blob, pool nor result; a sender may
+    repeat a page, and valid calls give the two-step calls' blob and pool."""
+    say("[checked] one-pass KVCACHE1")
+    c = _Case(tk)
+    wl = c.wl
+    geo = tk.pool_from_tensor(c.src)
+    n = int(wl.seq_lens[0])                                  # 64 tokens, 4 pages
+    bt, bt2 = wl.block_tables[0].copy(), wl.dst_block_tables[0].copy()
+    nbytes = tk.topkv_kvcache1_bytes(geo, n)
+    ws = torch.empty(tk.topkv_kvcache1_workspace_bytes(geo, n) // 8, dtype=torch.int64, device="cuda")
+    blob = torch.full((nbytes,), 0x5C, dtype=torch.uint8, device="cuda")
+    res = torch.full((4,), 77, dtype=torch.int32, device="cuda")
+    with checked():
+        bad = bt.copy()
+        bad[2] = wl.num_pages
+        _bounds(tk, tk.topkv_kvcache1_pack_seal, c.src, to_dev(bad), n, 1, 2, blob, ws)
+        torch.cuda.synchronize()
+        assert (blob == 0x5C).all().item(), "a refused sender wrote its blob"
+        tk.topkv_kvcache1_pack_seal(c.src, to_dev(bt), n, 1, 2, blob, ws)
+        two = torch.empty_like(blob)
+        tk.topkv_kvcache1_pack_layers(c.src, 0, wl.num_layers, to_dev(bt), n, two)
+        tk.topkv_kvcache1_seal(geo, n, 1, 2, two, ws)
+        torch.cuda.synchronize()
+        assert torch.equal(blob, two), "checked one-pass blob differs from the two-step blob"
+        for table in (np.array([bt2[0], bt2[1], bt2[0], bt2[3]], dtype=np.int32),       # a page named twice
+                      np.array([bt2[0], -1, bt2[2], bt2[3]], dtype=np.int32)):         # an entry outside
+            _bounds(tk, tk.topkv_kvcache1_verify_unpack, blob, c.dst, to_dev(table), n, 1, 2, ws, res)
+        torch.cuda.synchronize()
+        assert np.array_equal(to_host(c.dst), c.dst_h), "a refused receiver wrote its pool"
+        assert res.cpu().tolist() == [77] * 4, "a refused receiver wrote its result"
+        rep = bt.copy()
+        rep[3] = rep[0]                                      # a sender may read one page twice
+        tk.topkv_kvcache1_pack_seal(c.src, to_dev(rep), n, 1, 2, blob, ws)
+        tk.topkv_kvcache1_verify_unpack(blob, c.dst, to_dev(bt2), n, 1, 2, ws, res)
+        torch.cuda.synchronize()
+        assert res.cpu().tolist() == [tk.TOPKV_OK, 0, 0, 0]
