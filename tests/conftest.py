@@ -13,3 +13,12 @@ if HERE not in sys.path:
 
 def pytest_configure(config):
     config.addinivalue_line("markers", "gpu: needs an MI355X (gfx950) GPU and the built HIP library")
+
+
+@pytest.fixture(autouse=True)
+def _unchecked_library(monkeypatch):
+    """Every test starts with the library's checked mode off, whatever the
+    environment says: several tests feed the fast path hostile tables on
+    purpose to see its silent skips, which checked mode would refuse.  Tests
+    of checked mode switch it on themselves."""
+    monkeypatch.delenv("TOPKV_CHECKED", raising=False)
