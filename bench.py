@@ -220,9 +220,19 @@ def cpu_model():
     return "unknown"
 
 
-def cpu_baseline(wl, hs, budget_s):
+def layer_kinds(wl):
+    """The workload's kinds of layer, (fixed state?, window), each with the
+    first layer of that kind."""
+    kinds = sorted({(wl.is_state(l), wl.window(l)) for l in range(wl.num_layers)})
+    return {k: next(l for l in range(wl.num_layers) if (wl.is_state(l), wl.window(l)) == k) for k in kinds}
+
+
+def cpu_baseline(wl, hs, budget_s, refs=None):
     """Time the oracle on host copies of a few layer slabs, cycling until the
-    budget is spent.  Returns the cpu_baseline object."""
+    budget is spent.  Returns the cpu_baseline object.  With a dict `refs`,
+    also stores there, untimed, the oracle's result for each layer kind on
+    the first slab as it stands afterwards: refs[kind] = (packed words, the
+    destination after the unpack), which cpu_threaded checks itself against."""
     import oracle
     import oracle.state
 
@@ -243,6 +253,20 @@ def cpu_baseline(wl, hs, budget_s):
         spent += time.perf_counter() - t0
         done_bytes += sum(layer_bytes(wl, layers % wl.num_layers))
         layers += 1
+    if refs is not None:
+        # kinds in the order cpu_threaded checks them, each unpacked on top of the one before
+        # (kinds that are not fixed-state share the slab's destination layer)
+        cur = {False: host[slabs[0]][1].copy(), True: st_h[1].copy() if st_h is not None else None}
+        for k in layer_kinds(wl):
+            src_l = st_h[0] if k[0] else host[slabs[0]][0]
+            want_dst = cur[k[0]]
+            if k[0]:
+                want = oracle.state.pack_state_layer(src_l, 0, wl.state_slots)
+                oracle.state.unpack_state_layer(want, want_dst, 0, wl.dst_state_slots)
+            else:
+                want = oracle.pack_layer(src_l, 0, wl.block_tables, wl.seq_lens, window=k[1])
+                oracle.unpack_layer(want, want_dst, 0, wl.dst_block_tables, wl.seq_lens, window=k[1])
+            refs[k] = (want, want_dst.copy())
     return {"value": round(done_bytes / spent / 1e9, 3), "unit": "GB/s", "cores": 1, "kind": "oracle",
             "sample": (f"{layers} layer pack+unpack passes of {wl.name} over host copies of "
                        f"{len(slabs)} layer slab(s){' and one state-cache layer' if st_h is not None else ''}, "
@@ -327,19 +351,18 @@ def split_ops(ops, parts):
     return chunks
 
 
-def cpu_threaded(wl, hs, budget_s, threads=None):
+def cpu_threaded(wl, hs, budget_s, refs, threads=None):
     """The same layers on the host over a thread pool (by default one thread
     per 4 MiB moved per direction, up to the cores the process may use): each
     layer's whole pages move in groups (one numpy gather or scatter per group,
     which runs without the interpreter lock), partial pages and fixed states
     one copy each, split into one chunk per thread.  Each layer kind is
-    checked against the oracle on layer slab 0 before anything is timed.  A
-    faster host baseline than the oracle; not part of the GPU path."""
+    checked on layer slab 0, before anything is timed, against the oracle's
+    result that cpu_baseline stored in `refs`.  A faster host baseline than
+    the oracle; not part of the GPU path."""
     from concurrent.futures import ThreadPoolExecutor
 
     import numpy as np
-    import oracle
-    import oracle.state
 
     slabs, host, st_h = hs
     if not threads:
@@ -347,8 +370,7 @@ def cpu_threaded(wl, hs, budget_s, threads=None):
         # (the 70B headline) 4 threads moved 102 GB/s on the GPU machine's host, 16 threads 36 GB/s
         per_dir = max(layer_bytes(wl, l)[0] for l in range(wl.num_layers)) // 2
         threads = max(1, min(len(os.sched_getaffinity(0)), per_dir // (4 << 20)))
-    kinds = sorted({(wl.is_state(l), wl.window(l)) for l in range(wl.num_layers)})
-    rep = {k: next(l for l in range(wl.num_layers) if (wl.is_state(l), wl.window(l)) == k) for k in kinds}
+    rep = layer_kinds(wl)
     packed = np.empty(max(layer_bytes(wl, l)[0] for l in range(wl.num_layers)) // 4 + 8, dtype=np.uint16)
     pages = sum(-(-int(n) // wl.page_size) for n in wl.seq_lens)
     group = max(1, -(-pages // threads))                # one group of whole pages per thread
@@ -362,15 +384,9 @@ def cpu_threaded(wl, hs, budget_s, threads=None):
         def layer_pass(s_, k):
             for d in (0, 1):
                 list(ex.map(lambda ch: run_ops(ch, d), plans[(s_, k)][d]))
-        for k, l in rep.items():       # check each layer kind on slab 0 against the oracle
-            src_l, dst_l = (st_h[0], st_h[1]) if k[0] else host[slabs[0]]
-            want_dst = dst_l.copy()
-            if k[0]:
-                want = oracle.state.pack_state_layer(src_l, 0, wl.state_slots)
-                oracle.state.unpack_state_layer(want, want_dst, 0, wl.dst_state_slots)
-            else:
-                want = oracle.pack_layer(src_l, 0, wl.block_tables, wl.seq_lens, window=k[1])
-                oracle.unpack_layer(want, want_dst, 0, wl.dst_block_tables, wl.seq_lens, window=k[1])
+        for k, l in rep.items():       # check each layer kind on slab 0 against the oracle's result
+            dst_l = st_h[1] if k[0] else host[slabs[0]][1]
+            want, want_dst = refs[k]
             layer_pass(slabs[0], k)
             if not (np.array_equal(packed[:want.size], want) and np.array_equal(dst_l, want_dst)):
                 raise AssertionError(f"threaded host pack/unpack differs from the oracle (layer kind {k})")
@@ -385,7 +401,7 @@ def cpu_threaded(wl, hs, budget_s, threads=None):
             layers += 1
     return {"value": round(done_bytes / spent / 1e9, 3), "unit": "GB/s", "threads": threads,
             "host_threads_available": len(os.sched_getaffinity(0)),
-            "kind": "host pack+unpack: numpy page gathers/scatters over a thread pool (checked against the oracle)",
+            "kind": "host pack+unpack: numpy page gathers/scatters over a thread pool (checked against the oracle leg's results)",
             "sample": f"{layers} layer pack+unpack passes of {wl.name}, {spent:.1f} s",
             "ms_per_layer_pack_unpack": round(1e3 * spent / layers, 3)}
 
@@ -560,9 +576,10 @@ def run(args):
     if args.cpu_seconds > 0:
         log(f"[bench] CPU oracle sample (~{args.cpu_seconds} s)")
         hs = host_slabs(wl, src, dst, states)
-        out["cpu_baseline"] = cpu_baseline(wl, hs, args.cpu_seconds)
+        refs = {}
+        out["cpu_baseline"] = cpu_baseline(wl, hs, args.cpu_seconds, refs)
         log(f"[bench] threaded host pack/unpack (~{min(5.0, args.cpu_seconds / 2):.0f} s)")
-        out["cpu_threaded"] = cpu_threaded(wl, hs, min(5.0, args.cpu_seconds / 2))
+        out["cpu_threaded"] = cpu_threaded(wl, hs, min(5.0, args.cpu_seconds / 2), refs)
     else:
         out["cpu_baseline"] = None
         out["cpu_threaded"] = None

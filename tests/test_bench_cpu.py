@@ -72,5 +72,7 @@ def test_threaded_host_baseline_matches_oracle():
              make_workload("gpt-oss-120b", num_layers=2, seq_lens=[300, 17, 129, 128]),
              make_workload("qwen3.5-397b-hybrid", num_layers=4, seq_lens=[40, 3, 77], state_bytes=1000)]
     for wl in cases:
-        res = bench.cpu_threaded(wl, _host_slabs(wl), 0.05, threads=3)
+        hs, refs = _host_slabs(wl), {}
+        bench.cpu_baseline(wl, hs, 0.05, refs)          # the oracle's results the threaded leg checks against
+        res = bench.cpu_threaded(wl, hs, 0.05, refs, threads=3)
         assert res["value"] > 0 and res["threads"] == 3, wl.name
