@@ -1,5 +1,6 @@
-"""bench.py on the CPU: its byte accounting follows Eq. 1 and the SURVEY's
-per-launch definition, and it refuses more than one GPU before touching one."""
+"""bench.py on the CPU: its byte accounting follows Eq. 1 (bytes read plus
+bytes written per launch), and it refuses more than one GPU before touching
+one."""
 import os
 import subprocess
 import sys
