@@ -1,5 +1,5 @@
-"""bench.py on the CPU: its byte accounting follows Eq. 1 (bytes read plus
-bytes written per launch), and it refuses more than one GPU before touching
+"""bench.py on the CPU: its byte accounting follows Eq. 1 (per launch: the
+layer's bytes read and written, plus the table entries and lengths read), and it refuses more than one GPU before touching
 one."""
 import os
 import subprocess
