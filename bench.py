@@ -1,35 +1,53 @@
 #!/usr/bin/env python3
 """Per-layer paged KV-cache pack + unpack throughput on one MI355X.
 
-One step = pack every layer of the workload (one batched launch per layer,
-pool -> contiguous send buffer), then unpack every layer (one launch per
-layer, send buffer -> destination pool), i.e. the per-layer transfer unit of
-the paper's pipelined layer-by-layer KV transfer (Section 5.2) for both ends.
+One step = pack every layer of the workload (pool -> contiguous send
+buffer), then unpack every layer (send buffer -> destination pool): the
+per-layer transfer unit of the paper's pipelined layer-by-layer KV transfer
+(Section 5.2) at both ends.  Two ways of issuing a sweep are timed:
+  engine   - the layer engine (topkv_engine_pack_layers / _unpack_layers):
+             one persistent launch per direction over each run of
+             full-attention layers, each layer moved as one batched launch
+             would move it, every layer ready at launch (windowed and
+             fixed-state layers keep one launch each);
+  launches - one batched launch per layer.
+--issue picks the one that gives `value` (engine by default); the other is
+reported beside it.  Each sweep is replayed from a captured HIP graph
+(--launch graph, default) or issued from the host (--launch eager).
 
 value      = algorithmic bytes of the whole step / wall time of the step (GB/s,
              10^9), inputs resident in HBM, timed with HIP events on the launch
              stream over exactly --steps steps after --warmup untimed ones.
-             Each sweep (L launches of one direction) is replayed from a
-             captured HIP graph (--launch graph, default) or issued from the
-             host (--launch eager).
 roofline   = the dominant kernel's algorithmic bytes per launch / its average
              launch duration, i.e. the time between HIP events at that
              direction's sweep boundaries over the timed region divided by
-             the launches in it (includes the sub-microsecond gaps between
-             graph-launched kernels).  --kernel-events adds per-launch
-             kernel-timestamp events as a diagnostic.
+             the launches in it.
+verified   = the packed slot and destination slab of three layers after the
+             timed steps (both overwritten before them) against the oracle
+             results computed by the cpu_baseline leg; exit status 1 when
+             they differ.
+ceiling    = the same box's practical ceiling and floor, measured the same
+             way: an empty launch, the per-layer grid with every length 0, a
+             hand-written streaming copy of one layer's bytes per launch and
+             of 64 MiB / 256 MiB / 1 GiB, the layer engine's schedule without
+             tables, and a per-workgroup wall-clock timeline of one layer's
+             copy (libtopkv_ceiling.so).  copy_ceiling_gbs is the per-layer
+             copy.
+configs    = (default workload) the 70B batch of 8, DeepSeek-V3 MLA and 70B
+             re-blocking workloads, a few steps under both issue modes.
 cpu_baseline = the CPU oracle (numpy, one thread) on a bounded sample of the
              same workload, on this host, same byte definition.
 
 Algorithmic bytes per layer and direction: read + write of
 planes * sum(n) * row_bytes each, plus 4 B per block-table entry read
 (ceil(n/P) per request, P of the pool being read or written) and 4 B per
-seq_len.  Cache defeat: every layer packs into its own buffer slice while the
-packed volume fits 2 GiB (ring otherwise), and the whole pack sweep runs
-before the unpack sweep, so no kernel reads data another just wrote (the
-MI355X last-level cache holds 256 MB).
+seq_len.  Cache defeat: every layer packs into its own buffer slot while the
+packed volume fits 24 GiB (a ring of slots otherwise), and the whole pack
+sweep runs before the unpack sweep, so no kernel reads data another just
+wrote (the MI355X last-level cache holds 256 MB).
 
-    python bench.py [--steps K] [--warmup W] [--workload NAME]
+    python bench.py [--steps K] [--warmup W] [--workload NAME] [--issue engine|launches]
+    python bench.py --mode ceiling     # ceiling and floor beside both issue modes
     python bench.py --calib-copy-bytes N   # plain copy kernel, for PMC scaling
 """
 import argparse
@@ -107,14 +125,22 @@ def parse():
     ap.add_argument("--cpu-seconds", type=float, default=10.0,
                     help="budget of the CPU-oracle sample (0 disables it)")
     ap.add_argument("--launch", choices=["eager", "graph"], default="graph",
-                    help="issue each sweep as L host launches, or replay it as a captured HIP graph")
+                    help="issue each sweep from the host, or replay it as a captured HIP graph")
+    ap.add_argument("--issue", choices=["engine", "launches"], default="engine",
+                    help="engine: one layer-engine launch per direction over each run of full-attention layers "
+                         "(value); launches: one launch per layer.  The other mode is timed beside it")
+    ap.add_argument("--no-configs", dest="configs", action="store_false",
+                    help="skip the batched configurations (batch of 8, MLA, re-blocking) of the default run")
+    ap.add_argument("--threads", type=int, default=0,
+                    help="threaded host baseline: thread count (0: sweep powers of two up to the cores)")
     ap.add_argument("--kernel-events", action="store_true",
                     help="also time every launch with its own kernel-timestamp events (diagnostic)")
-    ap.add_argument("--mode", choices=["layers", "kvcache1", "pipeline", "reshard"], default="layers",
+    ap.add_argument("--mode", choices=["layers", "kvcache1", "pipeline", "reshard", "ceiling"], default="layers",
                     help="layers: per-layer pack/unpack sweep (the headline); kvcache1: whole-request "
                          "serialization (pack every layer into a KVCACHE1 blob, seal, verify, unpack); "
                          "pipeline: layer-by-layer transfer overlapped with a synthetic prefill; "
-                         "reshard: head-sliced pack, head-major unpack, pool-to-pool re-blocking")
+                         "reshard: head-sliced pack, head-major unpack, pool-to-pool re-blocking; "
+                         "ceiling: plain copies and empty launches beside the workload's per-layer sweeps")
     ap.add_argument("--layer-ms", type=float, default=0.5,
                     help="pipeline mode: synthetic prefill time per layer (the paper's 0.5 ms for 70B)")
     ap.add_argument("--calib-copy-bytes", type=int, default=0,
@@ -183,12 +209,16 @@ def read_traffic(workload):
 
 
 def calib_copy(args):
+    """A plain copy of known size with the hand-written streaming copy kernel
+    (the scale of the PMC traffic counters)."""
     import torch
+
+    from paper_2607_28633_amd import ceiling as cl
     n = int(args.calib_copy_bytes)
     a = torch.empty(n, dtype=torch.uint8, device="cuda").fill_(1)
     b = torch.empty_like(a)
     for _ in range(args.warmup + args.steps):
-        b.copy_(a)
+        cl.topkv_ceiling_copy(a, b, n)
     torch.cuda.synchronize()
     print(json.dumps({"calib_copy_bytes": n, "launches": args.warmup + args.steps}), flush=True)
 
@@ -227,12 +257,15 @@ def layer_kinds(wl):
     return {k: next(l for l in range(wl.num_layers) if (wl.is_state(l), wl.window(l)) == k) for k in kinds}
 
 
-def cpu_baseline(wl, hs, budget_s, refs=None):
+def cpu_baseline(wl, hs, budget_s, refs=None, verify=None):
     """Time the oracle on host copies of a few layer slabs, cycling until the
     budget is spent.  Returns the cpu_baseline object.  With a dict `refs`,
     also stores there, untimed, the oracle's result for each layer kind on
     the first slab as it stands afterwards: refs[kind] = (packed words, the
-    destination after the unpack), which cpu_threaded checks itself against."""
+    destination after the unpack), which cpu_threaded checks itself against.
+    verify = (layers, source slabs, destination slabs as generated): refs[
+    ("verify", l)] = the oracle's packed words of layer l and its destination
+    slab after the unpack, against which the benchmark checks its timed run."""
     import oracle
     import oracle.state
 
@@ -267,6 +300,13 @@ def cpu_baseline(wl, hs, budget_s, refs=None):
                 want = oracle.pack_layer(src_l, 0, wl.block_tables, wl.seq_lens, window=k[1])
                 oracle.unpack_layer(want, want_dst, 0, wl.dst_block_tables, wl.seq_lens, window=k[1])
             refs[k] = (want, want_dst.copy())
+    if refs is not None and verify is not None:
+        for l in verify[0]:
+            W = wl.window(l)
+            want = oracle.pack_layer(verify[1][l][None], 0, wl.block_tables, wl.seq_lens, window=W)
+            want_dst = verify[2][wl.kv_slab(l)][None].copy()
+            oracle.unpack_layer(want, want_dst, 0, wl.dst_block_tables, wl.seq_lens, window=W)
+            refs[("verify", l)] = (want, want_dst[0])
     return {"value": round(done_bytes / spent / 1e9, 3), "unit": "GB/s", "cores": 1, "kind": "oracle",
             "sample": (f"{layers} layer pack+unpack passes of {wl.name} over host copies of "
                        f"{len(slabs)} layer slab(s){' and one state-cache layer' if st_h is not None else ''}, "
@@ -352,8 +392,9 @@ def split_ops(ops, parts):
 
 
 def cpu_threaded(wl, hs, budget_s, refs, threads=None):
-    """The same layers on the host over a thread pool (by default one thread
-    per 4 MiB moved per direction, up to the cores the process may use): each
+    """The same layers on the host over a thread pool of `threads` threads
+    (by default each power of two up to the cores the process may use, and
+    that count, is timed and the best kept, with every count's GB/s): each
     layer's whole pages move in groups (one numpy gather or scatter per group,
     which runs without the interpreter lock), partial pages and fixed states
     one copy each, split into one chunk per thread.  Each layer kind is
@@ -365,11 +406,15 @@ def cpu_threaded(wl, hs, budget_s, refs, threads=None):
     import numpy as np
 
     slabs, host, st_h = hs
+    cores = len(os.sched_getaffinity(0))
     if not threads:
-        # one thread per 4 MiB moved per direction, up to the cores available: on a 16.8 MB layer
-        # (the 70B headline) 4 threads moved 102 GB/s on the GPU machine's host, 16 threads 36 GB/s
-        per_dir = max(layer_bytes(wl, l)[0] for l in range(wl.num_layers)) // 2
-        threads = max(1, min(len(os.sched_getaffinity(0)), per_dir // (4 << 20)))
+        # every power of two up to the cores the process may use, and that count itself, each for
+        # an equal share of the budget; the best is the baseline
+        counts = sorted({1 << i for i in range(cores.bit_length()) if 1 << i <= cores} | {cores})
+        sweep = [cpu_threaded(wl, hs, budget_s / len(counts), refs, threads=t) for t in counts]
+        best = max(sweep, key=lambda r: r["value"])
+        best["thread_sweep"] = {str(r["threads"]): r["value"] for r in sweep}
+        return best
     rep = layer_kinds(wl)
     packed = np.empty(max(layer_bytes(wl, l)[0] for l in range(wl.num_layers)) // 4 + 8, dtype=np.uint16)
     pages = sum(-(-int(n) // wl.page_size) for n in wl.seq_lens)
@@ -406,184 +451,475 @@ def cpu_threaded(wl, hs, budget_s, refs, threads=None):
             "ms_per_layer_pack_unpack": round(1e3 * spent / layers, 3)}
 
 
-def run(args):
-    import numpy as np
-    import torch
+def ring_slots(wl, slice_bytes):
+    """Packed slots of the sweep: every layer its own slot while the packed
+    volume fits 24 GiB; otherwise a ring of at least two slots, a whole
+    number of pool-slab cycles when the pool has fewer slabs than layers (so
+    consecutive layers keep consecutive slots and slabs).  Either way far more
+    than the 256 MB last-level cache."""
+    L = wl.num_layers
+    ring = min(L, max(2, (24 << 30) // max(slice_bytes, 1)))
+    if ring < L and wl.phys_layers < L and ring >= wl.phys_layers:
+        ring -= ring % wl.phys_layers
+    return ring
 
-    from paper_2607_28633_amd import topkv
-    from paper_2607_28633_amd.workloads import (WORKLOADS, device_dst_prefill, device_src_pool, device_state_cache,
-                                                make_workload)
 
-    torch.cuda.set_device(0)
-    wl = make_workload(args.workload)
-    log(f"[bench] workload {wl.describe()}")
-    src = device_src_pool(wl)
-    dst = device_dst_prefill(wl)
-    bt = torch.from_numpy(wl.block_tables).cuda()
-    bt2 = torch.from_numpy(wl.dst_block_tables).cuda()
-    lens = torch.from_numpy(wl.seq_lens).cuda()
-    nbytes = topkv.topkv_packed_layer_bytes(src, wl.seq_lens)
-    L, R = wl.num_layers, wl.num_reqs
-    states = None
-    slot_bytes = 0
-    if wl.layer_state:      # fixed-state layers: state caches and slot indices on the device
-        states = (device_state_cache(wl), device_state_cache(wl, dst=True))
-        slots = torch.from_numpy(wl.state_slots).cuda()
-        slots2 = torch.from_numpy(wl.dst_state_slots).cuda()
-        slot_bytes = R * wl.state_bytes
-    slice_bytes = max(nbytes, slot_bytes)
-    ring = min(L, max(2, (2 << 30) // max(slice_bytes, 1)))
-    packed = torch.empty((ring, slice_bytes // 2), dtype=torch.int16, device="cuda")
-    stream = torch.cuda.current_stream()
-    log(f"[bench] pools src {tuple(src.shape)} dst {tuple(dst.shape)}, packed {nbytes} B/layer, ring {ring}")
+def engine_chunks(wl, ring):
+    """The sweep's launches under the layer engine: maximal runs of
+    consecutive full-attention layers (no window, no fixed state) whose pool
+    slabs and packed slots are both consecutive, one engine launch each
+    ("engine", first layer, count); every other layer keeps its own call
+    ("layer", l, 1)."""
+    L, out, l = wl.num_layers, [], 0
+    plain = lambda x: not wl.is_state(x) and not wl.window(x)
+    while l < L:
+        if not plain(l):
+            out.append(("layer", l, 1))
+            l += 1
+            continue
+        n = 1
+        while (l + n < L and plain(l + n) and wl.kv_slab(l + n) == wl.kv_slab(l) + n
+               and (l + n) % ring == l % ring + n):
+            n += 1
+        out.append(("engine", l, n))
+        l += n
+    return out
 
-    def sweep(direction, evs=None, on=stream):
-        """One direction's launches (every layer), arguments marshalled up front,
-        bound to stream `on` (None: the stream current when called)."""
+
+class Setup:
+    """Device pools, tables and the packed ring of one workload."""
+
+    def __init__(self, wl, topkv):
+        import torch
+        from paper_2607_28633_amd.workloads import device_dst_prefill, device_src_pool, device_state_cache
+        self.wl, self.tk = wl, topkv
+        self.src, self.dst = device_src_pool(wl), device_dst_prefill(wl)
+        self.bt = torch.from_numpy(wl.block_tables).cuda()
+        self.bt2 = torch.from_numpy(wl.dst_block_tables).cuda()
+        self.lens = torch.from_numpy(wl.seq_lens).cuda()
+        self.nbytes = topkv.topkv_packed_layer_bytes(self.src, wl.seq_lens)
+        self.states, self.slot_bytes = None, 0
+        if wl.layer_state:      # fixed-state layers: state caches and slot indices on the device
+            self.states = (device_state_cache(wl), device_state_cache(wl, dst=True))
+            self.slots = torch.from_numpy(wl.state_slots).cuda()
+            self.slots2 = torch.from_numpy(wl.dst_state_slots).cuda()
+            self.slot_bytes = wl.num_reqs * wl.state_bytes
+        self.slice = max(self.nbytes, self.slot_bytes)
+        self.ring = ring_slots(wl, self.slice)
+        self.packed = torch.empty((self.ring, self.slice // 2), dtype=torch.int16, device="cuda")
+        self.chunks = engine_chunks(wl, self.ring)
+
+    def sweep(self, direction, issue, evs=None, on=None):
+        """One direction's launches over every layer (prepared calls bound to
+        stream `on`; None: the stream current when called).  issue "engine":
+        the layer engine over each run of engine_chunks; "launches": one
+        batched launch per layer.  evs: per-launch kernel-timestamp events
+        (per-layer launches only)."""
+        tk, wl, R = self.tk, self.wl, self.wl.num_reqs
         calls = []
-        for l in range(L):
-            e = evs[l] if evs else (None, None)
+
+        def one(l, e=(None, None)):
+            slot = self.packed[l % self.ring]
             if wl.is_state(l) and direction == 0:
-                calls.append(topkv.prepare_pack_state_layer(
-                    states[0], wl.state_slab(l), R, slots, packed[l % ring], stream=on, start=e[0], stop=e[1]))
-            elif wl.is_state(l):
-                calls.append(topkv.prepare_unpack_state_layer(
-                    packed[l % ring], states[1], wl.state_slab(l), R, slots2, stream=on, start=e[0], stop=e[1]))
-            elif direction == 0:
-                calls.append(topkv.prepare_pack_layer_window(
-                    src, wl.kv_slab(l), R, bt, bt.shape[1], lens, wl.window(l), packed[l % ring],
-                    stream=on, start=e[0], stop=e[1]))
+                return tk.prepare_pack_state_layer(self.states[0], wl.state_slab(l), R, self.slots, slot, stream=on,
+                                                   start=e[0], stop=e[1])
+            if wl.is_state(l):
+                return tk.prepare_unpack_state_layer(slot, self.states[1], wl.state_slab(l), R, self.slots2,
+                                                     stream=on, start=e[0], stop=e[1])
+            if direction == 0:
+                return tk.prepare_pack_layer_window(self.src, wl.kv_slab(l), R, self.bt, self.bt.shape[1], self.lens,
+                                                   wl.window(l), slot, stream=on, start=e[0], stop=e[1])
+            return tk.prepare_unpack_layer_window(slot, self.dst, wl.kv_slab(l), R, self.bt2, self.bt2.shape[1],
+                                                  self.lens, wl.window(l), stream=on, start=e[0], stop=e[1])
+
+        if issue == "launches":
+            return [one(l, evs[l] if evs else (None, None)) for l in range(wl.num_layers)]
+        for kind, l, n in self.chunks:
+            if kind == "layer":
+                calls.append(one(l))
+                continue
+            block = self.packed[l % self.ring:l % self.ring + n]
+            if direction == 0:
+                calls.append(tk.prepare_engine_pack_layers(self.src, wl.kv_slab(l), n, R, self.bt, self.bt.shape[1],
+                                                           self.lens, block, self.slice, stream=on))
             else:
-                calls.append(topkv.prepare_unpack_layer_window(
-                    packed[l % ring], dst, wl.kv_slab(l), R, bt2, bt2.shape[1], lens, wl.window(l),
-                    stream=on, start=e[0], stop=e[1]))
+                calls.append(tk.prepare_engine_unpack_layers(block, self.slice, self.dst, wl.kv_slab(l), n, R,
+                                                             self.bt2, self.bt2.shape[1], self.lens, stream=on))
         return calls
+
+
+def time_sweeps(setup, issue, steps, warmup, launch="graph", before_timed=None):
+    """Warm up, then time `steps` steps (pack sweep, then unpack sweep) with
+    HIP events on the launch stream at the sweep boundaries.  Returns
+    (ms per step, [pack sweep us, unpack sweep us] summed over the steps,
+    launches per sweep)."""
+    import torch
+    tk = setup.tk
+    stream = torch.cuda.current_stream()
+    sweeps = [setup.sweep(0, issue, on=stream), setup.sweep(1, issue, on=stream)]
 
     def run_calls(calls):
         for c in calls:
             c()
 
-    sweeps = [sweep(0), sweep(1)]
-    for _ in range(args.warmup):
+    for _ in range(warmup):
         run_calls(sweeps[0])
         run_calls(sweeps[1])
     torch.cuda.synchronize()
-    if args.launch == "graph":
-        # each direction's sweep captured once; replays launch the L kernels from the GPU side
+    if launch == "graph":
+        # each direction's sweep captured once; replays launch its kernels from the GPU side
         graphs = []
         for d in (0, 1):
             g = torch.cuda.CUDAGraph()
             with torch.cuda.graph(g):
-                run_calls(sweep(d, on=None))   # bound to the capture stream
+                run_calls(setup.sweep(d, issue, on=None))   # bound to the capture stream
             graphs.append(g)
-        for _ in range(max(1, args.warmup)):
+        for _ in range(max(1, warmup)):
             graphs[0].replay()
             graphs[1].replay()
         torch.cuda.synchronize()
-        issue = [graphs[0].replay, graphs[1].replay]
+        issue_fns = [graphs[0].replay, graphs[1].replay]
     else:
-        issue = [lambda: run_calls(sweeps[0]), lambda: run_calls(sweeps[1])]
-    log(f"[bench] {args.warmup} warmup steps done ({args.launch} launches)")
-
-    # timed region: events on the launch stream at the sweep boundaries
-    marks = [[topkv.HipEvent() for _ in range(3)] for _ in range(args.steps)]
-    torch.cuda.synchronize()
-    h0 = time.perf_counter()
-    for k in range(args.steps):
+        issue_fns = [lambda: run_calls(sweeps[0]), lambda: run_calls(sweeps[1])]
+    if before_timed is not None:
+        before_timed()
+        torch.cuda.synchronize()
+    marks = [[tk.HipEvent() for _ in range(3)] for _ in range(steps)]
+    for k in range(steps):
         marks[k][0].record(stream)
-        issue[0]()
+        issue_fns[0]()
         marks[k][1].record(stream)
-        issue[1]()
+        issue_fns[1]()
         marks[k][2].record(stream)
     marks[-1][2].synchronize()
     torch.cuda.synchronize()
-    host_s = time.perf_counter() - h0
     wall_ms = marks[0][0].elapsed_ms(marks[-1][2])
-    ms_per_step = wall_ms / args.steps
-    sweep_us = [1e3 * sum(marks[k][d].elapsed_ms(marks[k][d + 1]) for k in range(args.steps)) for d in (0, 1)]
-    log(f"[bench] {args.steps} timed steps: {wall_ms:.3f} ms on the GPU clock, {host_s * 1e3:.3f} ms host")
+    sweep_us = [1e3 * sum(marks[k][d].elapsed_ms(marks[k][d + 1]) for k in range(steps)) for d in (0, 1)]
+    return wall_ms / steps, sweep_us, len(sweeps[0])
 
-    per_layer = [layer_bytes(wl, l) for l in range(L)]
-    dir_bytes = [sum(b[d] for b in per_layer) for d in (0, 1)]     # one sweep
-    bytes_step = dir_bytes[0] + dir_bytes[1]
-    kern = {}
+
+def kernel_figures(wl, sweep_us, steps, launches):
+    """Per-launch figures of each direction: algorithmic bytes per launch,
+    average launch duration (sweep time / launches, so it includes the
+    sub-microsecond gaps between launches), GB/s."""
+    per_layer = [layer_bytes(wl, l) for l in range(wl.num_layers)]
+    out = {}
     for d, name in ((0, "pack"), (1, "unpack")):
-        us = sweep_us[d] / (args.steps * L)
-        b = dir_bytes[d] / L
-        kern[name] = {"bytes_per_launch": int(round(b)), "avg_us": round(us, 3), "gbs": round(b / us / 1e3, 1),
-                      "launches": args.steps * L}
+        b = sum(x[d] for x in per_layer) / launches
+        us = sweep_us[d] / (steps * launches)
+        out[name] = {"bytes_per_launch": int(round(b)), "avg_us": round(us, 3), "gbs": round(b / us / 1e3, 1),
+                     "launches": steps * launches,
+                     "us_per_layer": round(sweep_us[d] / (steps * wl.num_layers), 3)}
+    return out
+
+
+def step_gbs(wl, ms_per_step):
+    per_layer = [layer_bytes(wl, l) for l in range(wl.num_layers)]
+    return sum(p + u for p, u in per_layer) / (ms_per_step * 1e-3) / 1e9
+
+
+def verify_layers(wl, ring):
+    """Logical layers whose packed slot and destination slab the timed run
+    leaves for checking: the last writer of each slot among the final `ring`
+    layers, full-attention or windowed (not fixed-state), first / middle /
+    last of them."""
+    cand = [l for l in range(wl.num_layers - ring, wl.num_layers) if not wl.is_state(l)]
+    if not cand:
+        return []
+    return sorted({cand[0], cand[len(cand) // 2], cand[-1]})
+
+
+def ceiling(setup, steps):
+    """The practical ceiling and floor on this machine, measured like the
+    headline (graph replays of L launches, or one launch per direction, with
+    the same cache defeat): the empty kernel, the per-layer pack grid with
+    every length 0, the hand-written streaming copy of one layer's packed
+    bytes per launch into each layer's own slot, that copy at 64 MiB, 256 MiB
+    and 1 GiB, and the layer engine's schedule without tables
+    (topkv_ceiling_copy_layers: pool slab prefixes -> packed slots -> a
+    second pool's slab prefixes, one launch per direction)."""
+    import numpy as np
+    import torch
+
+    from paper_2607_28633_amd import ceiling as cl
+    tk, wl = setup.tk, setup.wl
+    stream = torch.cuda.current_stream()
+    L, n = wl.num_layers, setup.nbytes
+    reps = max(3, steps)
+
+    def graph_us(make_calls, per):
+        g = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(g):
+            for c in make_calls():
+                c()
+        for _ in range(2):
+            g.replay()
+        torch.cuda.synchronize()
+        e0, e1 = tk.HipEvent(), tk.HipEvent()
+        e0.record(stream)
+        for _ in range(reps):
+            g.replay()
+        e1.record(stream)
+        e1.synchronize()
+        return 1e3 * e0.elapsed_ms(e1) / (reps * per)
+
+    out = {}
+    out["empty_kernel_us_per_launch"] = round(graph_us(lambda: [lambda: cl.topkv_ceiling_empty(None)] * L, L), 3)
+    zero = torch.zeros_like(setup.lens)
+    R = wl.num_reqs
+    out["zero_length_pack_us_per_launch"] = round(graph_us(lambda: [tk.prepare_pack_layer_window(
+        setup.src, wl.kv_slab(l), R, setup.bt, setup.bt.shape[1], zero, 0, setup.packed[l % setup.ring])
+        for l in range(L)], L), 3)
+    out["zero_length_unpack_us_per_launch"] = round(graph_us(lambda: [tk.prepare_unpack_layer_window(
+        setup.packed[l % setup.ring], setup.dst, wl.kv_slab(l), R, setup.bt2, setup.bt2.shape[1], zero, 0)
+        for l in range(L)], L), 3)
+    flat = setup.src.view(-1).view(torch.uint8)
+    slab = flat.numel() // setup.src.shape[0]
+    copies = {}
+    for size, count in ((n, max(2, min(L, (2 << 30) // n))), (64 << 20, 20), (256 << 20, 6), (1 << 30, 2)):
+        if size > flat.numel() // 2:
+            continue
+        dst = torch.empty(count * size, dtype=torch.uint8, device="cuda")
+        # sources spread over the pool, each copy to its own destination
+        offs = [((l * 7919 * size) % max(1, flat.numel() - size)) // 4096 * 4096 for l in range(count)]
+
+        def make(size=size, count=count, dst=dst, offs=offs):
+            return [(lambda s=flat[o:o + size], d=dst[l * size:(l + 1) * size]: cl.topkv_ceiling_copy(s, d, size, None))
+                    for l, o in enumerate(offs)]
+
+        us = graph_us(make, count)
+        copies[f"{size >> 20}MiB" if size != n else "layer"] = {"bytes": size, "us_per_launch": round(us, 3),
+                                                               "gbs": round(2 * size / us / 1e3, 1)}
+        del dst
+    out["copy_per_launch"] = copies
+    # the engine's schedule without tables: read each slab's first n bytes into the packed slots, then
+    # write them to the second pool's slabs, one launch per direction, alternating as the step does
+    lay = min(L, setup.ring, setup.src.shape[0], setup.dst.shape[0])
+    pk = lambda: cl.topkv_ceiling_copy_layers(setup.src, slab, setup.packed, setup.slice, n, lay, 0, None)
+    dslab = setup.dst.view(-1).numel() * 2 // setup.dst.shape[0]
+    up = lambda: cl.topkv_ceiling_copy_layers(setup.packed, setup.slice, setup.dst, dslab, n, lay, 0, None)
+    for _ in range(2):
+        pk()
+        up()
+    torch.cuda.synchronize()
+    m = [[tk.HipEvent() for _ in range(3)] for _ in range(reps)]
+    for k in range(reps):
+        m[k][0].record(stream)
+        pk()
+        m[k][1].record(stream)
+        up()
+        m[k][2].record(stream)
+    m[-1][2].synchronize()
+    t = [1e3 * sum(m[k][d].elapsed_ms(m[k][d + 1]) for k in range(reps)) / (reps * lay) for d in (0, 1)]
+    out["copy_layers_engine_schedule"] = {
+        "layers": lay, "bytes_per_layer": 2 * n, "read_us_per_layer": round(t[0], 3),
+        "write_us_per_layer": round(t[1], 3), "step_gbs": round(4 * n / (t[0] + t[1]) / 1e3, 1)}
+    # one layer's copy stamped per workgroup: first start to last store completion vs the launch's events
+    tiles = -(-n // 32768)
+    stamps = torch.zeros(3 * tiles, dtype=torch.int64, device="cuda")
+    khz = cl.topkv_ceiling_wall_clock_khz()
+    e0, e1 = tk.HipEvent(), tk.HipEvent()
+    spans, durs, phases = [], [], []
+    for k in range(reps):
+        o = ((k * 7919 * n) % max(1, flat.numel() - n)) // 4096 * 4096
+        torch.cuda.synchronize()
+        e0.record(stream)
+        cl.topkv_ceiling_copy_timeline(flat[o:o + n], setup.packed[k % setup.ring], n, stamps, None)
+        e1.record(stream)
+        e1.synchronize()
+        s = stamps.view(tiles, 3).cpu().numpy().astype(np.int64)
+        spans.append((s[:, 2].max() - s[:, 0].min()) * 1e3 / khz)
+        phases.append(((s[:, 0].max() - s[:, 0].min()) * 1e3 / khz, (s[:, 1].max() - s[:, 0].min()) * 1e3 / khz))
+        durs.append(1e3 * e0.elapsed_ms(e1))
+    out["layer_copy_timeline"] = {
+        "bytes": 2 * n, "workgroups": tiles, "clock_khz": khz,
+        "first_start_to_last_store_us": round(float(np.median(spans)), 3),
+        "last_workgroup_start_us": round(float(np.median([p[0] for p in phases])), 3),
+        "last_load_return_us": round(float(np.median([p[1] for p in phases])), 3),
+        "launch_events_us": round(float(np.median(durs)), 3),
+        "active_window_gbs": round(2 * n / float(np.median(spans)) / 1e3, 1)}
+    return out
+
+
+def run(args):
+    import numpy as np
+    import torch
+
+    from paper_2607_28633_amd import topkv
+    from paper_2607_28633_amd.workloads import WORKLOADS, make_workload
+
+    torch.cuda.set_device(0)
+    wl = make_workload(args.workload)
+    log(f"[bench] workload {wl.describe()}")
+    st = Setup(wl, topkv)
+    L, R = wl.num_layers, wl.num_reqs
+    log(f"[bench] pools src {tuple(st.src.shape)} dst {tuple(st.dst.shape)}, packed {st.nbytes} B/layer, "
+        f"ring {st.ring}, engine launches per sweep {sum(1 for c in st.chunks if c[0] == 'engine')}")
+
+    # the timed run's output is checked: host copies of the checked layers' source slabs and of their
+    # destination slabs as generated, before any kernel has run
+    vlayers = verify_layers(wl, st.ring) if args.cpu_seconds > 0 else []
+
+    def words(t):   # device slab -> host uint16 words, bit-exact
+        return t.contiguous().view(torch.int16).cpu().numpy().view(np.uint16)
+
+    vsrc = {l: words(st.src[wl.kv_slab(l)]) for l in vlayers}
+    vdst0 = {wl.kv_slab(l): words(st.dst[wl.kv_slab(l)]) for l in vlayers}
+
+    def before_timed():
+        # everything the timed steps must produce is overwritten first
+        st.packed.fill_(0x5A5A)
+        for s, h in vdst0.items():
+            st.dst[s].view(torch.int16).copy_(torch.from_numpy(h.view(np.int16)))
+
+    ms_per_step, sweep_us, launches = time_sweeps(st, args.issue, args.steps, args.warmup, args.launch, before_timed)
+    got = {l: (words(st.packed[l % st.ring]), words(st.dst[wl.kv_slab(l)])) for l in vlayers}
+    log(f"[bench] {args.steps} timed steps ({args.issue}): {ms_per_step:.4f} ms per step")
+    kern = kernel_figures(wl, sweep_us, args.steps, launches)
+
+    other = "launches" if args.issue == "engine" else "engine"
+    o_ms, o_us, o_launches = time_sweeps(st, other, args.steps, args.warmup, args.launch)
+    o_kern = kernel_figures(wl, o_us, args.steps, o_launches)
+    log(f"[bench] {other}: {o_ms:.4f} ms per step")
 
     if args.kernel_events:
-        # diagnostic: each launch stamped with its own begin/end (host launch path is slower)
+        # diagnostic: each per-layer launch stamped with its own begin/end (host launch path is slower)
         evs = [[(topkv.HipEvent(), topkv.HipEvent()) for _ in range(L)] for _ in range(2)]
-        stamped = [sweep(0, evs[0]), sweep(1, evs[1])]
+        stamped = [st.sweep(0, "launches", evs[0]), st.sweep(1, "launches", evs[1])]
         per = [[], []]
         for _ in range(3):
-            run_calls(stamped[0])
-            run_calls(stamped[1])
+            for c in stamped[0] + stamped[1]:
+                c()
             torch.cuda.synchronize()
             for d in (0, 1):
                 per[d] += [evs[d][l][0].elapsed_ms(evs[d][l][1]) * 1e3 for l in range(L)]
+        tgt = kern if args.issue == "launches" else o_kern
         for d, name in ((0, "pack"), (1, "unpack")):
-            kern[name]["kernel_stamp_avg_us"] = round(float(np.mean(per[d])), 3)
-            kern[name]["kernel_stamp_median_us"] = round(float(np.median(per[d])), 3)
+            tgt[name]["kernel_stamp_avg_us"] = round(float(np.mean(per[d])), 3)
+            tgt[name]["kernel_stamp_median_us"] = round(float(np.median(per[d])), 3)
 
     dom = max(kern, key=lambda k: kern[k]["avg_us"] * kern[k]["launches"])
     traffic_vals = read_traffic(args.workload)
-    traffic = None
-    if traffic_vals and f"{dom}_hbm_bytes_per_launch" in traffic_vals:
-        traffic = float(traffic_vals[f"{dom}_hbm_bytes_per_launch"])
+    tkey = f"{'engine_' if args.issue == 'engine' else ''}{dom}_hbm_bytes_per_launch"
+    traffic = float(traffic_vals[tkey]) if traffic_vals and tkey in traffic_vals else None
     achieved = kern[dom]["gbs"]
+    kname = "kv_engine_kernel (layer engine)" if args.issue == "engine" else layer_kernel(wl, dom)
     roofline = {"bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s",
                 "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": traffic,
-                "kernel": f"{dom} launch: {layer_kernel(wl, dom)}", "bytes_per_launch": kern[dom]["bytes_per_launch"],
+                "kernel": f"{dom} launch: {kname}", "bytes_per_launch": kern[dom]["bytes_per_launch"],
                 "avg_launch_us": kern[dom]["avg_us"]}
 
-    # practical ceiling on this box: a plain device copy of one layer's bytes
-    # into as many distinct buffers as the pack sweep uses (same cache defeat)
-    flat = src.view(-1).view(torch.int16)
-    ce0, ce1 = topkv.HipEvent(), topkv.HipEvent()
-    n_el = nbytes // 2
-    for _ in range(2):
-        ce0.record(stream)
-        for l in range(L):
-            off = ((l * 7919 * n_el) % max(1, flat.numel() - n_el)) // 4096 * 4096
-            packed[l % ring].copy_(flat[off:off + n_el])
-        ce1.record(stream)
-        ce1.synchronize()
-    copy_gbs = 2 * nbytes * L / (ce0.elapsed_ms(ce1) * 1e-3) / 1e9
-
+    hs = host_slabs(wl, st.src, st.dst, st.states) if args.cpu_seconds > 0 else None
+    ceil = ceiling(st, args.steps) if not wl.layer_state else None
+    value = step_gbs(wl, ms_per_step)
     out = {
         "metric": "per-layer KV pack+unpack HBM GB/s (% of MI355X peak), 70B GQA 4K tokens",
-        "value": round(bytes_step / (ms_per_step * 1e-3) / 1e9, 1),
+        "value": round(value, 1),
         "unit": "GB/s", "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
         "ms_per_step": round(ms_per_step, 4), "higher_is_better": True, "scaling": "weak",
         "vs_baseline": None, "dtype": "bf16", "data": "synthetic",
         "config": {"workload": f"{wl.name}: {WORKLOADS[wl.name]}", "layers": L, "requests": R,
-                   "launch": args.launch,
+                   "issue": args.issue, "launch": args.launch,
                    "tokens": int(wl.seq_lens.astype(np.int64).sum()), "page_size": wl.page_size,
-                   "dst_page_size": wl.dst_page_size, "packed_bytes_per_layer": nbytes,
-                   **({"state_layers": sum(wl.layer_state), "packed_state_bytes_per_layer": slot_bytes}
+                   "dst_page_size": wl.dst_page_size, "packed_bytes_per_layer": st.nbytes,
+                   **({"state_layers": sum(wl.layer_state), "packed_state_bytes_per_layer": st.slot_bytes}
                       if wl.layer_state else {}),
-                   "step": "pack every layer (1 launch each), then unpack every layer",
-                   "seed": wl.seed, "packed_ring": ring, "phys_layers": wl.phys_layers},
-        "pct_of_peak": round(100 * bytes_step / (ms_per_step * 1e-3) / 1e9 / HBM_PEAK_GBS, 2),
+                   "step": ("pack every layer, then unpack every layer: "
+                            + ("the layer engine, one persistent launch per direction over each run of "
+                               "full-attention layers (every layer ready at launch), other layers one launch each"
+                               if args.issue == "engine" else "one launch per layer")),
+                   "seed": wl.seed, "packed_ring": st.ring, "phys_layers": wl.phys_layers},
+        "pct_of_peak": round(100 * value / HBM_PEAK_GBS, 2),
         "wall_us_per_layer": {"pack+unpack": round(1e3 * ms_per_step / L, 3)},
         "kernels": kern,
         "roofline": roofline,
-        "copy_ceiling_gbs": round(copy_gbs, 1),
+        other: {"value": round(step_gbs(wl, o_ms), 1), "ms_per_step": round(o_ms, 4),
+                "pct_of_peak": round(100 * step_gbs(wl, o_ms) / HBM_PEAK_GBS, 2), "kernels": o_kern},
+        "copy_ceiling_gbs": ceil["copy_per_launch"]["layer"]["gbs"] if ceil else None,
+        "ceiling": ceil,
     }
+    if args.configs and args.workload == "llama3-70b-4k":
+        del st
+        torch.cuda.empty_cache()
+        out["configs"] = config_block(args, topkv)
     if args.cpu_seconds > 0:
         log(f"[bench] CPU oracle sample (~{args.cpu_seconds} s)")
-        hs = host_slabs(wl, src, dst, states)
         refs = {}
-        out["cpu_baseline"] = cpu_baseline(wl, hs, args.cpu_seconds, refs)
+        out["cpu_baseline"] = cpu_baseline(wl, hs, args.cpu_seconds, refs, verify=(vlayers, vsrc, vdst0))
         log(f"[bench] threaded host pack/unpack (~{min(5.0, args.cpu_seconds / 2):.0f} s)")
-        out["cpu_threaded"] = cpu_threaded(wl, hs, min(5.0, args.cpu_seconds / 2), refs)
+        out["cpu_threaded"] = cpu_threaded(wl, hs, min(5.0, args.cpu_seconds / 2), refs, threads=args.threads)
+        ok = all(np.array_equal(got[l][0][:refs[("verify", l)][0].size], refs[("verify", l)][0]) and
+                 np.array_equal(got[l][1], refs[("verify", l)][1]) for l in vlayers)
+        out["verified"] = {"layers": vlayers, "bit_exact": bool(ok),
+                           "what": "packed slot and destination slab of each layer after the timed steps vs the "
+                                   "oracle results computed by the cpu_baseline leg (both overwritten before "
+                                   "the timed steps)"}
+        if not ok:
+            print(json.dumps(out), flush=True)
+            log("[bench] the timed run's output differs from the oracle")
+            sys.exit(1)
     else:
         out["cpu_baseline"] = None
         out["cpu_threaded"] = None
+        out["verified"] = None
     print(json.dumps(out), flush=True)
+
+
+def config_block(args, topkv):
+    """The batched configurations (70B batch of 8, DeepSeek-V3 MLA, 70B
+    re-blocking 16 -> 64) timed in the same run: a few graph-replayed steps
+    under each issue mode, pools freed between workloads."""
+    import torch
+    from paper_2607_28633_amd.workloads import make_workload
+    res = {}
+    for name in ("llama3-70b-batch8", "deepseek-v3-mla", "reblock-70b"):
+        wl = make_workload(name)
+        log(f"[bench] config {name}")
+        st = Setup(wl, topkv)
+        steps = max(2, args.steps // 3)
+        entry = {"requests": wl.num_reqs, "layers": wl.num_layers, "tokens": int(wl.seq_lens.sum()),
+                 "page_size": wl.page_size, "dst_page_size": wl.dst_page_size,
+                 "packed_bytes_per_layer": st.nbytes}
+        traffic = read_traffic(name)
+        for issue in ("engine", "launches"):
+            ms, us, launches = time_sweeps(st, issue, steps, 1, "graph")
+            kern = kernel_figures(wl, us, steps, launches)
+            for d in ("pack", "unpack"):
+                kern[d]["frac"] = round(kern[d]["gbs"] / HBM_PEAK_GBS, 4)
+                key = f"{'engine_' if issue == 'engine' else ''}{d}_traffic_over_algorithmic"
+                kern[d]["traffic_over_algorithmic"] = float(traffic[key]) if traffic and key in traffic else None
+            v = step_gbs(wl, ms)
+            entry[issue] = {"value": round(v, 1), "pct_of_peak": round(100 * v / HBM_PEAK_GBS, 2),
+                            "ms_per_step": round(ms, 4), "kernels": kern}
+        res[name] = entry
+        del st
+        torch.cuda.empty_cache()
+    return res
+
+
+def run_ceiling(args):
+    """The ceiling and floor of the workload's per-layer transfer on this machine
+    (see ceiling()), beside the workload's own sweeps under both issue
+    modes."""
+    import torch
+
+    from paper_2607_28633_amd import topkv
+    from paper_2607_28633_amd.workloads import WORKLOADS, make_workload
+    torch.cuda.set_device(0)
+    wl = make_workload(args.workload)
+    if wl.layer_state:
+        raise SystemExit("ceiling mode measures workloads without fixed-state layers")
+    st = Setup(wl, topkv)
+    res = {}
+    for issue in ("launches", "engine"):
+        ms, us, launches = time_sweeps(st, issue, args.steps, args.warmup, args.launch)
+        res[issue] = {"value": round(step_gbs(wl, ms), 1), "ms_per_step": round(ms, 4),
+                      "kernels": kernel_figures(wl, us, args.steps, launches)}
+    print(json.dumps({"metric": "per-layer transfer ceiling and floor", "mode": "ceiling", "unit": "GB/s",
+                      "n_gpus": 1, "steps": args.steps, "dtype": "bf16", "data": "synthetic",
+                      "config": {"workload": f"{wl.name}: {WORKLOADS[wl.name]}", "packed_bytes_per_layer": st.nbytes,
+                                 "packed_ring": st.ring},
+                      "sweeps": res, "ceiling": ceiling(st, args.steps)}), flush=True)
 
 
 def run_kvcache1(args):
@@ -1022,6 +1358,8 @@ def main():
         print(json.dumps(run_pipeline(args)), flush=True)
     elif args.mode == "reshard":
         run_reshard(args)
+    elif args.mode == "ceiling":
+        run_ceiling(args)
     else:
         run(args)
 

@@ -92,7 +92,9 @@ typedef enum topkv_status {
   TOPKV_ERR_LAUNCH = 3,       /* the HIP runtime refused the launch */
   TOPKV_ERR_BOUNDS = 4,       /* invalid device-side table, length, slot or capacity (checked path) */
   TOPKV_ERR_DEVICE = 5,       /* a HIP runtime query failed */
-  TOPKV_ERR_CHECKSUM = 6      /* topkv_kvcache1_verify: header or checksum mismatch */
+  TOPKV_ERR_CHECKSUM = 6,     /* topkv_kvcache1_verify: header or checksum mismatch */
+  TOPKV_ERR_TIMEOUT = 7,      /* layer engine: a layer's ready word did not arrive in time (device status) */
+  TOPKV_ERR_CANCELLED = 8     /* layer engine: the cancel word was set while a layer was awaited (device status) */
 } topkv_status_t;
 
 /* One paged KV pool.  The caller owns the memory.  All counts are elements
@@ -178,6 +180,80 @@ topkv_status_t topkv_unpack_layer_batched_ex(const void* src, int64_t src_bytes,
                                              int32_t num_reqs, const int32_t* block_tables,
                                              int32_t bt_stride, const int32_t* seq_lens,
                                              const topkv_launch_t* launch);
+
+/* Layer engine (Section 5.2: a prefill worker sends layer l while layers
+ * l+1 .. L-1 are still being computed, so the unit of transfer is one
+ * layer).  ONE persistent launch moves layers [first_layer, first_layer +
+ * num_layers) of a batch, each layer exactly as topkv_pack_layer_batched /
+ * topkv_unpack_layer_batched would move it, in layer order, and each layer
+ * only once its ready word allows.  The per-launch costs of one launch per
+ * layer (dispatch, the first table and length loads, each kernel's drain)
+ * are paid once per range.  The tables and lengths are shared by every layer
+ * of the range (one block table per request indexes every layer's pool).
+ *   layer z of the range (pool layer first_layer + z) uses the packed block
+ *   at packed + z * layer_stride, of min(layer_stride, packed_bytes -
+ *   z * layer_stride) bytes (packed_bytes when num_layers == 1); a request
+ *   whose packed block would cross that end is not moved in that layer, as
+ *   in the batched calls.  layer_stride > 0 when num_layers > 1, and
+ *   (num_layers - 1) * layer_stride <= packed_bytes.  Windowed and fixed-
+ *   state layers use their own per-layer calls.
+ *
+ * Waiting (engine->ready non-null): ready[z] has reached the epoch when
+ * (int32_t)(ready[z] - engine->epoch) >= 0, so the same words serve
+ * successive transfers with increasing epochs; layers move in order, so
+ * layer z may move once ready[0..z] have all reached it.  The words may
+ * sit in device memory or in host memory the device can reach (pinned,
+ * mapped); a producer publishes layer z by storing ready[z] with release
+ * ordering after the layer's data (a host store after the data's copy has
+ * completed, a kernel's release store, or a stream-ordered write after the
+ * producing kernel).  Each wait is bounded: after engine->timeout_us
+ * microseconds without the word, or as soon as the cancel word (optional,
+ * device or host memory) is non-zero, the waiting workgroups give up and
+ * exit: the layers before the first word that did not arrive are moved in
+ * full, that layer and every later one are not touched.  The first reason
+ * (TOPKV_ERR_TIMEOUT or TOPKV_ERR_CANCELLED) is written to *engine->status
+ * (device int32 that must hold 0 at launch; it stays 0 when every layer
+ * moved).  The status is written by the kernel: read it after the stream
+ * has completed.  engine == NULL, or engine->ready == NULL: every layer
+ * moves at once.
+ *
+ * Grids: without waiting, the launch is a hardware-dispatched grid with one
+ * workgroup per (layer, request, table entry, plane, tile) slot, as the
+ * batched calls use for one layer (slots past a request's pages exit at
+ * once); beyond that grid's limits (more than 1024 requests, 2^20 slots per
+ * layer, 65535 table entries or 65535 requests * layers) and whenever it
+ * waits, the engine is a persistent grid that keeps
+ * engine->workgroups_per_cu workgroups of 256 threads per compute unit (0: 8)
+ * for the whole launch, each working through its share of the items in
+ * layer order; a caller whose producer kernels must run beside a waiting
+ * engine on the same GPU leaves them room with a smaller value (e.g. 2).
+ * Returns synchronously: the host-
+ * side argument errors of the batched calls, TOPKV_ERR_INVALID_ARG for a bad
+ * layer range or layer_stride, a null status with ready set, or a timeout
+ * outside (0, 60 000 000] us, and TOPKV_ERR_UNSUPPORTED when num_layers *
+ * num_reqs * bt_stride * (items per page) reaches 2^31.  Checked mode
+ * validates the tables and lengths once for the range (the smallest layer
+ * block as capacity).  The call never synchronises otherwise and allocates
+ * nothing. */
+typedef struct topkv_engine {
+  const uint32_t* ready;      /* [num_layers] words, or NULL (no waiting) */
+  const uint32_t* cancel;     /* optional word; non-zero: waiting workgroups give up */
+  int32_t*        status;     /* device int32, 0 at launch; required with ready */
+  uint32_t        epoch;      /* value each ready word must reach */
+  int32_t         workgroups_per_cu;  /* 0: 8 */
+  int64_t         timeout_us; /* longest wait for one layer, in (0, 60e6]; ignored without ready */
+} topkv_engine_t;
+
+topkv_status_t topkv_engine_pack_layers(const topkv_pool_t* src, int32_t first_layer, int32_t num_layers,
+                                        int32_t num_reqs, const int32_t* block_tables, int32_t bt_stride,
+                                        const int32_t* seq_lens, void* packed, int64_t layer_stride,
+                                        int64_t packed_bytes, const topkv_engine_t* engine,
+                                        hipStream_t stream);
+topkv_status_t topkv_engine_unpack_layers(const void* packed, int64_t layer_stride, int64_t packed_bytes,
+                                          const topkv_pool_t* dst, int32_t first_layer, int32_t num_layers,
+                                          int32_t num_reqs, const int32_t* block_tables, int32_t bt_stride,
+                                          const int32_t* seq_lens, const topkv_engine_t* engine,
+                                          hipStream_t stream);
 
 /* Windowed layers (Section 2.2 extends Eq. 1 per layer kind: a sliding-
  * window attention layer holds only its last `window` tokens).  As the

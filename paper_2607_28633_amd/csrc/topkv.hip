@@ -106,7 +106,7 @@ struct MoveParams {
   int32_t tiles_per_plane;    // ceil(plane_bytes / tile bytes)
   int32_t batched;            // 1: lengths come from device seq_lens
   int32_t window;             // > 0: only the last `window` tokens of each request move
-  int32_t pad_;
+  int32_t z_layers;           // batched direct grid: layers on grid z (z = layer * num_reqs + request)
   int64_t plane_stride;       // single request only: > 0 places plane c at packed + c * plane_stride
   int64_t layer_bytes;        // single request, several layers: pool bytes per layer
   int64_t layer_stride;       // single request, several layers: packed bytes between consecutive layers
@@ -289,11 +289,20 @@ __device__ __forceinline__ void move_direct(char* __restrict__ pool, char* __res
                                             const int32_t* __restrict__ tables,
                                             const int32_t* __restrict__ seq_lens, const MoveParams& p) {
   constexpr int32_t kTile = kThreads * VPT * VB;
-  // grid: z = request (single request: z = layer after the first), y = table
-  // entry, x = plane * tiles_per_plane + tile
+  // grid: z = request (single request: z = layer after the first; a batch
+  // over several layers: z = layer * num_reqs + request), y = table entry,
+  // x = plane * tiles_per_plane + tile
   const uint3 b = grid_block();
-  const int32_t r = kBatched ? (int32_t)b.z : 0;
-  const int64_t lz = kBatched ? 0 : (int64_t)b.z;
+  int32_t r = 0;
+  int64_t lz = 0;
+  if (!kBatched) {
+    lz = (int64_t)b.z;
+  } else if (p.z_layers > 1) {
+    lz = (int64_t)(b.z / (uint32_t)p.num_reqs);
+    r = (int32_t)(b.z - (uint32_t)lz * (uint32_t)p.num_reqs);
+  } else {
+    r = (int32_t)b.z;
+  }
   const int32_t i = b.y;
   const int32_t c = (int32_t)(b.x / (uint32_t)p.tiles_per_plane);
   const int32_t k = (int32_t)(b.x - (uint32_t)c * p.tiles_per_plane);
@@ -345,6 +354,7 @@ __device__ __forceinline__ void move_direct(char* __restrict__ pool, char* __res
     end = ((int64_t)tok0 + cnt) * p.planes * p.row_bytes;
   }
   if (end + lz * p.layer_stride > p.packed_cap) return;
+  if (kBatched && p.z_layers > 1 && end > p.layer_stride) return;   // stays inside its layer's block
   char* packed_ptr = packed + lz * p.layer_stride + plane_off + (int64_t)(lo - start) * p.row_bytes + tstart;
   if (kPack) {
     store_tile<VB, VPT>(packed_ptr, v, nv);
@@ -352,6 +362,56 @@ __device__ __forceinline__ void move_direct(char* __restrict__ pool, char* __res
     load_tile<VB, VPT>(v, packed_ptr, nv);
     store_tile<VB, VPT>(pool_ptr, v, nv);
   }
+}
+
+// One item of the persistent mapping: page g of the batch's kept pages (in
+// request order), plane c, tile k.  tok / pg / st are the LDS prefix sums of
+// request_prefix (batched) and are not read for a single request.  The item
+// is skipped when its tile lies past the page's run, its request's packed
+// block would end past packed_cap, or its table entry is out of range.
+template <int VB, int VPT, bool kPack>
+__device__ __forceinline__ void strided_item(char* __restrict__ pool, char* __restrict__ packed,
+                                             const int32_t* __restrict__ tables, const MoveParams& p,
+                                             const int32_t* tok, const int32_t* pg, const int32_t* st,
+                                             bool batched, int64_t single_start, int64_t packed_cap, int32_t g,
+                                             int32_t c, int32_t k) {
+  constexpr int64_t kTile = (int64_t)kThreads * VPT * VB;
+  int32_t r = 0, tok0 = 0;
+  int64_t start = single_start, cnt = p.n_single - single_start;
+  int32_t i = (int32_t)(start / p.page_size) + g;
+  if (batched) {
+    int lo = 0, hi = p.num_reqs - 1;   // largest r with pg[r] <= g
+    while (lo < hi) {
+      const int mid = (lo + hi + 1) >> 1;
+      if (pg[mid] <= g) lo = mid; else hi = mid - 1;
+    }
+    r = uniform(lo);
+    tok0 = uniform(tok[r]);
+    cnt = uniform(tok[r + 1] - tok0);
+    start = uniform(st[r]);
+    i = uniform((int32_t)(start / p.page_size) + g - pg[r]);
+  }
+  const int64_t n = start + cnt;
+  const int64_t first = (int64_t)i * p.page_size;
+  const int64_t lo_t = first > start ? first : start;
+  const int64_t hi_t = first + p.page_size < n ? first + p.page_size : n;
+  const int64_t run = (hi_t - lo_t) * p.row_bytes;
+  const int64_t tstart = (int64_t)k * kTile;
+  if (tstart >= run) return;
+  const bool placed = !batched && p.plane_stride > 0;   // caller-placed planes (one request)
+  const int64_t req_end = placed ? (int64_t)(p.planes - 1) * p.plane_stride + cnt * p.row_bytes
+                                 : ((int64_t)tok0 + cnt) * p.planes * p.row_bytes;
+  if (req_end > packed_cap) return;
+  const int32_t page = tables[(int64_t)r * p.bt_stride + i];
+  if (page < 0 || (int64_t)page >= p.num_pages) return;
+  const int32_t len = (int32_t)(run - tstart < kTile ? run - tstart : kTile);
+  char* pool_ptr = pool + (int64_t)page * p.page_bytes + (int64_t)c * p.plane_bytes + (lo_t - first) * p.row_bytes +
+                   tstart;
+  const int64_t plane_off = placed ? (int64_t)c * p.plane_stride
+                                   : ((int64_t)tok0 * p.planes + (int64_t)c * cnt) * p.row_bytes;
+  char* packed_ptr = packed + plane_off + (lo_t - start) * p.row_bytes + tstart;
+  if (kPack) copy_tile<VB, VPT>(packed_ptr, pool_ptr, len);
+  else copy_tile<VB, VPT>(pool_ptr, packed_ptr, len);
 }
 
 // Persistent mapping for large batches: every workgroup scans the lengths
@@ -364,7 +424,6 @@ template <int VB, int VPT, bool kPack>
 __device__ __forceinline__ void move_strided(char* __restrict__ pool, char* __restrict__ packed,
                                            const int32_t* __restrict__ tables,
                                            const int32_t* __restrict__ seq_lens, const MoveParams& p) {
-  constexpr int64_t kTile = (int64_t)kThreads * VPT * VB;
   extern __shared__ uint64_t lds_u64[];
   uint64_t* wsum = lds_u64;                                      // [kWaves]
   int32_t* tok = reinterpret_cast<int32_t*>(lds_u64 + kWaves);   // [num_reqs + 1]
@@ -390,42 +449,173 @@ __device__ __forceinline__ void move_strided(char* __restrict__ pool, char* __re
     const int32_t rem = (int32_t)(w - (uint32_t)g * per_page);
     const int32_t c = uniform(rem / p.tiles_per_plane);
     const int32_t k = uniform(rem - c * p.tiles_per_plane);
-    int32_t r = 0, tok0 = 0;
-    int64_t start = single_start, cnt = p.n_single - single_start;
-    int32_t i = (int32_t)(start / p.page_size) + g;
-    if (batched) {
-      int lo = 0, hi = p.num_reqs - 1;   // largest r with pg[r] <= g
-      while (lo < hi) {
-        const int mid = (lo + hi + 1) >> 1;
-        if (pg[mid] <= g) lo = mid; else hi = mid - 1;
-      }
-      r = uniform(lo);
-      tok0 = uniform(tok[r]);
-      cnt = uniform(tok[r + 1] - tok0);
-      start = uniform(st[r]);
-      i = uniform((int32_t)(start / p.page_size) + g - pg[r]);
+    strided_item<VB, VPT, kPack>(pool, packed, tables, p, tok, pg, st, batched, single_start, p.packed_cap, g, c,
+                                 k);
+  }
+}
+
+// ---------------------------------------------------------------------------
+// Layer engine (Section 5.2: layer l leaves while later layers are still
+// being produced, so the unit of transfer is one layer).  One persistent
+// launch moves layers [first, first + layers) of a batch: the items of every
+// layer in layer order (layer z = w / items-per-layer of the flattened item
+// index w), each layer exactly as one batched launch would move it, and a
+// layer's items only once its ready word says the layer may move.  The
+// per-launch costs of one launch per layer (dispatch, the first table and
+// length loads, the drain at the end of each kernel) are paid once per
+// range instead of once per layer.
+// ---------------------------------------------------------------------------
+
+// How the engine waits.  ready == null: every layer may move at once.
+struct EngineWait {
+  const uint32_t* ready;     // [layers]: layer z may move once ready[z] has reached epoch
+  const uint32_t* cancel;    // optional: non-zero makes waiting waves give up
+  int32_t* status;           // non-null when ready is: 0, or why a wave gave up
+  int64_t timeout_ticks;     // longest one wait lasts, in wall-clock ticks
+  uint32_t epoch;
+  int32_t layers;
+};
+
+// Wait until layer z may move: layers move in order, so z may move once the
+// ready words of every layer up to z have reached the epoch.  *ready_below
+// is the first layer not yet seen ready (all before it are); each poll reads
+// the 64 words from there (one per lane) and raises *ready_below past the
+// run of consecutive ready ones.  The words are read with system-scope
+// atomic loads (they may live in host memory or be written by another
+// agent), then an acquire fence orders the layer's data loads after the
+// word.  Between polls that find nothing new the wave sleeps, longer after
+// the first few.  The wait gives up when the cancel word is non-zero
+// (TOPKV_ERR_CANCELLED), when it has lasted timeout_ticks
+// (TOPKV_ERR_TIMEOUT), or when another wave already gave up (status non-
+// zero); the first reason is stored in *status with a compare-and-swap from
+// 0, and the caller's wave then exits.  Returns true when layer z may move.
+__device__ __forceinline__ bool engine_wait(const EngineWait& e, int32_t z, int32_t* ready_below) {
+  const int lane = threadIdx.x & 63;
+  const uint64_t t0 = (uint64_t)wall_clock64();
+  int32_t below = *ready_below;
+  for (int32_t polls = 0;; ++polls) {
+    uint32_t word = e.epoch;
+    if (below + lane < e.layers)
+      word = __hip_atomic_load(const_cast<uint32_t*>(e.ready) + below + lane, __ATOMIC_RELAXED,
+                               __HIP_MEMORY_SCOPE_SYSTEM);
+    const uint64_t ok = __ballot((int32_t)(word - e.epoch) >= 0);
+    const int32_t run = ~ok ? __builtin_ctzll(~ok) : 64;
+    below += run;
+    if (below > z) {
+      *ready_below = below;
+      __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "");
+      return true;
     }
-    const int64_t n = start + cnt;
-    const int64_t first = (int64_t)i * p.page_size;
-    const int64_t lo_t = first > start ? first : start;
-    const int64_t hi_t = first + p.page_size < n ? first + p.page_size : n;
-    const int64_t run = (hi_t - lo_t) * p.row_bytes;
-    const int64_t tstart = (int64_t)k * kTile;
-    if (tstart >= run) continue;
-    const bool placed = !batched && p.plane_stride > 0;   // caller-placed planes (one request)
-    const int64_t req_end = placed ? (int64_t)(p.planes - 1) * p.plane_stride + cnt * p.row_bytes
-                                   : ((int64_t)tok0 + cnt) * p.planes * p.row_bytes;
-    if (req_end > p.packed_cap) continue;
-    const int32_t page = tables[(int64_t)r * p.bt_stride + i];
-    if (page < 0 || (int64_t)page >= p.num_pages) continue;
-    const int32_t len = (int32_t)(run - tstart < kTile ? run - tstart : kTile);
-    char* pool_ptr = pool + (int64_t)page * p.page_bytes + (int64_t)c * p.plane_bytes + (lo_t - first) * p.row_bytes +
-                     tstart;
-    const int64_t plane_off = placed ? (int64_t)c * p.plane_stride
-                                     : ((int64_t)tok0 * p.planes + (int64_t)c * cnt) * p.row_bytes;
-    char* packed_ptr = packed + plane_off + (lo_t - start) * p.row_bytes + tstart;
-    if (kPack) copy_tile<VB, VPT>(packed_ptr, pool_ptr, len);
-    else copy_tile<VB, VPT>(pool_ptr, packed_ptr, len);
+    if (run > 0) continue;        // progress: read the next words at once
+    int32_t why = 0;
+    if (lane == 0) {
+      if (__hip_atomic_load(e.status, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) != 0)
+        why = -1;
+      else if (e.cancel && __hip_atomic_load(const_cast<uint32_t*>(e.cancel), __ATOMIC_RELAXED,
+                                             __HIP_MEMORY_SCOPE_SYSTEM) != 0)
+        why = TOPKV_ERR_CANCELLED;
+      else if ((int64_t)((uint64_t)wall_clock64() - t0) > e.timeout_ticks)
+        why = TOPKV_ERR_TIMEOUT;
+      if (why > 0) atomicCAS(e.status, 0, why);
+    }
+    if (uniform(why) != 0) return false;
+    // short sleeps first (a word that is about to arrive), then long ones
+    // (~3 us at 2.4 GHz), so thousands of waiting waves do not keep the
+    // fabric busy with polls
+    if (polls < 16) __builtin_amdgcn_s_sleep(8);
+    else __builtin_amdgcn_s_sleep(127);
+  }
+}
+
+// One engine item (layer z, page g of the batch's pages, plane c, tile k)
+// located from the prefix sums alone: both offsets without the page's own
+// term, the table entry to read (-1: nothing to move) and the vectors to
+// move (no window: every request keeps all its tokens).
+struct EngineItem {
+  int64_t pool_off;    // from the first layer's slab, without page * page_bytes
+  int64_t packed_off;  // from the packed base
+  int32_t tidx;        // r * bt_stride + i, or -1
+  int32_t nv;          // vectors of VB bytes
+  int32_t z;           // layer of the range
+};
+
+template <int VB, int VPT>
+__device__ __forceinline__ EngineItem engine_locate(const MoveParams& p, const int32_t* tok, const int32_t* pg,
+                                                    uint32_t w, uint32_t work, uint32_t per_page, int32_t layers) {
+  constexpr int64_t kTile = (int64_t)kThreads * VPT * VB;
+  EngineItem it;
+  const int32_t z = uniform((int32_t)(w / work));
+  const uint32_t item = w - (uint32_t)z * work;
+  const int32_t g = uniform((int32_t)(item / per_page));
+  const int32_t rem = (int32_t)(item - (uint32_t)g * per_page);
+  const int32_t c = uniform(rem / p.tiles_per_plane);
+  const int32_t k = uniform(rem - c * p.tiles_per_plane);
+  int lo = 0, hi = p.num_reqs - 1;   // largest r with pg[r] <= g
+  while (lo < hi) {
+    const int mid = (lo + hi + 1) >> 1;
+    if (pg[mid] <= g) lo = mid; else hi = mid - 1;
+  }
+  const int32_t r = uniform(lo);
+  const int32_t tok0 = uniform(tok[r]);
+  const int32_t n = uniform(tok[r + 1] - tok0);
+  const int32_t i = uniform(g - pg[r]);
+  const int64_t first = (int64_t)i * p.page_size;
+  const int64_t last = first + p.page_size < n ? first + p.page_size : n;
+  const int64_t run = (last - first) * p.row_bytes;
+  const int64_t tstart = (int64_t)k * kTile;
+  const int64_t off = (int64_t)z * p.layer_stride;
+  int64_t cap = p.packed_cap - off;
+  if (layers > 1 && cap > p.layer_stride) cap = p.layer_stride;
+  const int64_t req_end = ((int64_t)tok0 + n) * p.planes * p.row_bytes;
+  it.z = z;
+  it.tidx = (tstart < run && req_end <= cap) ? r * p.bt_stride + i : -1;
+  it.nv = (int32_t)((run - tstart < kTile ? run - tstart : kTile) / VB);
+  it.pool_off = (int64_t)z * p.layer_bytes + (int64_t)c * p.plane_bytes + tstart;
+  it.packed_off = off + (((int64_t)tok0 * p.planes + (int64_t)c * n) + first) * p.row_bytes + tstart;
+  return it;
+}
+
+// The item's source and destination once its table entry is known; returns
+// the vectors to move (0: skipped, entry outside the pool or -1).
+template <bool kPack>
+__device__ __forceinline__ int32_t engine_address(const EngineItem& it, int32_t page, const MoveParams& p,
+                                                  char* pool, char* packed, const char** src, char** dst) {
+  if (it.tidx < 0 || page < 0 || (int64_t)page >= p.num_pages) return 0;
+  char* pool_ptr = pool + (int64_t)page * p.page_bytes + it.pool_off;
+  char* packed_ptr = packed + it.packed_off;
+  *src = kPack ? pool_ptr : packed_ptr;
+  *dst = kPack ? packed_ptr : pool_ptr;
+  return it.nv;
+}
+
+// pool: the first layer's slab; packed: layer z's block starts at packed +
+// z * layer_stride and holds min(layer_stride, packed_cap - z * layer_stride)
+// bytes (packed_cap alone for one layer).  Workgroup b runs items b,
+// b + gridDim.x, ... so the whole grid works through the layers in order
+// (a few layers in flight at a time).
+template <int VB, int VPT, bool kPack>
+__global__ __launch_bounds__(kThreads) void kv_engine_kernel(char* __restrict__ pool, char* __restrict__ packed,
+                                                             const int32_t* __restrict__ tables,
+                                                             const int32_t* __restrict__ seq_lens, MoveParams p,
+                                                             EngineWait e) {
+  extern __shared__ uint64_t lds_u64[];
+  uint64_t* wsum = lds_u64;
+  int32_t* tok = reinterpret_cast<int32_t*>(lds_u64 + kWaves);
+  int32_t* pg = tok + (p.num_reqs + 1);
+  int32_t* st = pg + (p.num_reqs + 1);
+  request_prefix(p, seq_lens, tok, pg, st, wsum);
+  const uint32_t per_page = (uint32_t)(p.planes * p.tiles_per_plane);
+  const uint32_t work = (uint32_t)pg[p.num_reqs] * per_page;     // items per layer
+  // the host keeps layers * num_reqs * bt_stride * per_page below 2^31
+  const uint32_t total = work * (uint32_t)e.layers;
+  int32_t ready_below = e.ready ? 0 : e.layers;
+  for (uint32_t w = blockIdx.x; w < total; w += gridDim.x) {
+    const EngineItem it = engine_locate<VB, VPT>(p, tok, pg, w, work, per_page, e.layers);
+    if (it.z >= ready_below && !engine_wait(e, it.z, &ready_below)) return;
+    const char* src = nullptr;
+    char* dst = nullptr;
+    const int32_t nv = engine_address<kPack>(it, it.tidx >= 0 ? tables[it.tidx] : -1, p, pool, packed, &src, &dst);
+    if (nv) copy_tile<VB, VPT>(dst, src, nv * VB);
   }
 }
 
@@ -661,7 +851,7 @@ topkv_status_t launch_move(bool pack, const topkv_pool_t* pool, int32_t layer, v
   p.tiles_per_plane = (int32_t)tpp;
   p.batched = seq_lens ? 1 : 0;
   p.window = window;
-  p.pad_ = 0;
+  p.z_layers = 1;
   p.plane_stride = plane_stride;
   p.layer_bytes = g.layer_bytes;
   p.layer_stride = layer_stride;
@@ -677,6 +867,160 @@ topkv_status_t launch_move(bool pack, const topkv_pool_t* pool, int32_t layer, v
   else
     e = hipLaunchKernel(fn, grid3, dim3(kThreads), args, lds, launch->stream);
   return e == hipSuccess ? TOPKV_OK : TOPKV_ERR_LAUNCH;
+}
+
+#ifndef TOPKV_ENGINE_WG_PER_CU
+#define TOPKV_ENGINE_WG_PER_CU 8   // layer engine: default workgroups kept per compute unit
+#endif
+
+typedef void (*EngineFn)(char*, char*, const int32_t*, const int32_t*, MoveParams, EngineWait);
+
+template <int VB, int VPT>
+EngineFn engine_for(bool pack) {
+  return pack ? kv_engine_kernel<VB, VPT, true> : kv_engine_kernel<VB, VPT, false>;
+}
+
+EngineFn pick_engine(bool pack, int vb, int vpt) {
+  switch (vb) {
+    case 16:
+      switch (vpt) {
+        case 8: return engine_for<16, 8>(pack);
+        case 4: return engine_for<16, 4>(pack);
+        case 2: return engine_for<16, 2>(pack);
+        default: return engine_for<16, 1>(pack);
+      }
+    case 8: return engine_for<8, TOPKV_VPT>(pack);
+    case 4: return engine_for<4, TOPKV_VPT>(pack);
+    case 2: return engine_for<2, TOPKV_VPT>(pack);
+    default: return engine_for<1, TOPKV_VPT>(pack);
+  }
+}
+
+// Wall-clock ticks per microsecond of the current device (the clock the
+// kernels read with wall_clock64), cached per device.
+std::atomic<int> g_clock_khz[kMaxDevices];
+
+topkv_status_t wall_clock_khz(int* out) {
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0) return TOPKV_ERR_DEVICE;
+  if (dev < kMaxDevices) {
+    const int cached = g_clock_khz[dev].load(std::memory_order_relaxed);
+    if (cached > 0) { *out = cached; return TOPKV_OK; }
+  }
+  int khz = 0;
+  if (hipDeviceGetAttribute(&khz, hipDeviceAttributeWallClockRate, dev) != hipSuccess || khz <= 0)
+    return TOPKV_ERR_DEVICE;
+  if (dev < kMaxDevices) g_clock_khz[dev].store(khz, std::memory_order_relaxed);
+  *out = khz;
+  return TOPKV_OK;
+}
+
+// The layer engine's launcher (both directions).  The argument rules are
+// those of the batched calls applied to every layer of the range, plus the
+// range, the layer stride and the wait options.
+topkv_status_t engine_move(bool pack, const topkv_pool_t* pool, int32_t first_layer, int32_t layers,
+                           void* packed, int64_t packed_cap, int64_t layer_stride, int32_t num_reqs,
+                           const int32_t* tables, int32_t bt_stride, const int32_t* seq_lens,
+                           const topkv_engine_t* opt, hipStream_t stream) {
+  Geometry g;
+  topkv_status_t st = pool_geometry(pool, first_layer, &g);
+  if (st != TOPKV_OK) return st;
+  if (layers < 1 || (int64_t)first_layer + layers > pool->num_layers) return TOPKV_ERR_INVALID_ARG;
+  if (num_reqs < 0 || packed_cap < 0 || layer_stride < 0 || (layers > 1 && layer_stride == 0))
+    return TOPKV_ERR_INVALID_ARG;
+  int64_t before_last;
+  if (__builtin_mul_overflow((int64_t)(layers - 1), layer_stride, &before_last) || before_last > packed_cap)
+    return TOPKV_ERR_INVALID_ARG;
+  const bool waits = opt && opt->ready;
+  if (waits && (!opt->status || opt->timeout_us <= 0 || opt->timeout_us > 60000000)) return TOPKV_ERR_INVALID_ARG;
+  if (opt && (opt->workgroups_per_cu < 0 || opt->workgroups_per_cu > 64)) return TOPKV_ERR_INVALID_ARG;
+  if (num_reqs > TOPKV_MAX_BATCH_REQS) return TOPKV_ERR_UNSUPPORTED;
+  if (num_reqs == 0) return TOPKV_OK;
+  if (!tables || !seq_lens || !packed || bt_stride <= 0) return TOPKV_ERR_INVALID_ARG;
+
+  if (topkv_internal::checked_mode()) {
+    // the last layer's block is the smallest
+    int64_t cap = packed_cap - before_last;
+    if (layers > 1 && cap > layer_stride) cap = layer_stride;
+    st = topkv_internal::checked_tables(pool, num_reqs, tables, bt_stride, seq_lens, 0, 0, !pack,
+                                        (int64_t)pool->planes * g.row_bytes, 0, cap, stream);
+    if (st != TOPKV_OK) return st;
+  }
+
+  int vb = vector_bytes(reinterpret_cast<uintptr_t>(pool->base), reinterpret_cast<uintptr_t>(packed), g.row_bytes);
+  while (layer_stride % vb) vb >>= 1;
+  const int vpt = vectors_per_lane(vb, g.plane_bytes);
+  const int64_t tile = (int64_t)kThreads * vpt * vb;
+  const int64_t tpp = (g.plane_bytes + tile - 1) / tile;
+  int64_t per_page, work, total;
+  const int64_t tok_cap = (int64_t)num_reqs * bt_stride * (int64_t)pool->page_size;
+  if (__builtin_mul_overflow(tpp, (int64_t)pool->planes, &per_page) || per_page > INT32_MAX ||
+      __builtin_mul_overflow((int64_t)num_reqs * bt_stride, per_page, &work) ||
+      __builtin_mul_overflow(work, (int64_t)layers, &total) || total > INT32_MAX || tok_cap > INT32_MAX)
+    return TOPKV_ERR_UNSUPPORTED;
+
+  char* pool_ptr = static_cast<char*>(pool->base) + (int64_t)first_layer * g.layer_bytes;
+  char* packed_ptr = static_cast<char*>(packed);
+  MoveParams p;
+  p.page_bytes = g.page_bytes;
+  p.plane_bytes = g.plane_bytes;
+  p.packed_cap = packed_cap;
+  p.num_pages = pool->num_pages;
+  p.row_bytes = (int32_t)g.row_bytes;
+  p.page_size = pool->page_size;
+  p.planes = pool->planes;
+  p.num_reqs = num_reqs;
+  p.bt_stride = bt_stride;
+  p.n_single = 0;
+  p.tiles_per_plane = (int32_t)tpp;
+  p.batched = 1;
+  p.window = 0;
+  p.z_layers = 1;
+  p.plane_stride = 0;
+  p.layer_bytes = g.layer_bytes;
+  p.layer_stride = layer_stride;
+
+  // Every layer ready at launch: the batched direct grid with the layers on
+  // grid z (z = layer * num_reqs + request), dispatched by the hardware - no
+  // waiting, so nothing needs to stay resident.  Same slot rules as one
+  // batched launch (slots past a request's pages exit at once).
+  if (!waits && work <= TOPKV_DIRECT_MAX && bt_stride <= 65535 && num_reqs <= TOPKV_DIRECT_MAX_REQS &&
+      (int64_t)num_reqs * layers <= 65535) {
+    p.z_layers = layers;
+    void* args[] = {&pool_ptr, &packed_ptr, &tables, &seq_lens, &p};
+    const void* fn = reinterpret_cast<const void*>(pick_kernel(pack, vb, vpt, true, true));
+    const dim3 grid3((unsigned)per_page, (unsigned)bt_stride, (unsigned)(num_reqs * layers));
+    return hipLaunchKernel(fn, grid3, dim3(kThreads), args, (size_t)TOPKV_DIRECT_LDS_PAD, stream) == hipSuccess
+               ? TOPKV_OK : TOPKV_ERR_LAUNCH;
+  }
+
+  int cus = 0;
+  st = cu_count(&cus);
+  if (st != TOPKV_OK) return st;
+  const int per_cu = (opt && opt->workgroups_per_cu > 0) ? opt->workgroups_per_cu : TOPKV_ENGINE_WG_PER_CU;
+  const int64_t cap_grid = (int64_t)cus * per_cu;
+  const unsigned grid = (unsigned)(total < cap_grid ? total : cap_grid);
+  if (grid == 0) return TOPKV_OK;
+
+  EngineWait e;
+  e.ready = waits ? opt->ready : nullptr;
+  e.cancel = waits ? opt->cancel : nullptr;
+  e.status = waits ? opt->status : nullptr;
+  e.epoch = waits ? opt->epoch : 0;
+  e.layers = layers;
+  e.timeout_ticks = 0;
+  if (waits) {
+    int khz = 0;
+    st = wall_clock_khz(&khz);
+    if (st != TOPKV_OK) return st;
+    e.timeout_ticks = opt->timeout_us * (int64_t)khz / 1000;
+  }
+
+  const size_t lds = sizeof(uint64_t) * kWaves + sizeof(int32_t) * 3 * ((size_t)num_reqs + 1);
+  void* args[] = {&pool_ptr, &packed_ptr, &tables, &seq_lens, &p, &e};
+  const void* fn = reinterpret_cast<const void*>(pick_engine(pack, vb, vpt));
+  return hipLaunchKernel(fn, dim3(grid), dim3(kThreads), args, lds, stream) == hipSuccess ? TOPKV_OK
+                                                                                         : TOPKV_ERR_LAUNCH;
 }
 
 int64_t single_bytes(const topkv_pool_t* pool, int32_t n) {
@@ -810,6 +1154,23 @@ topkv_status_t topkv_unpack_layer_batched(const void* src, int64_t src_bytes, co
                                        seq_lens, &l);
 }
 
+topkv_status_t topkv_engine_pack_layers(const topkv_pool_t* src, int32_t first_layer, int32_t num_layers,
+                                        int32_t num_reqs, const int32_t* block_tables, int32_t bt_stride,
+                                        const int32_t* seq_lens, void* packed, int64_t layer_stride,
+                                        int64_t packed_bytes, const topkv_engine_t* engine, hipStream_t stream) {
+  return topkv::engine_move(true, src, first_layer, num_layers, packed, packed_bytes, layer_stride, num_reqs,
+                            block_tables, bt_stride, seq_lens, engine, stream);
+}
+
+topkv_status_t topkv_engine_unpack_layers(const void* packed, int64_t layer_stride, int64_t packed_bytes,
+                                          const topkv_pool_t* dst, int32_t first_layer, int32_t num_layers,
+                                          int32_t num_reqs, const int32_t* block_tables, int32_t bt_stride,
+                                          const int32_t* seq_lens, const topkv_engine_t* engine,
+                                          hipStream_t stream) {
+  return topkv::engine_move(false, dst, first_layer, num_layers, const_cast<void*>(packed), packed_bytes,
+                            layer_stride, num_reqs, block_tables, bt_stride, seq_lens, engine, stream);
+}
+
 int64_t topkv_packed_window_bytes(const topkv_pool_t* pool, const int32_t* seq_lens_host, int32_t num_reqs,
                                   int32_t window) {
   if (!pool || num_reqs < 0 || window < 0 || (num_reqs > 0 && !seq_lens_host)) return -1;
@@ -842,6 +1203,8 @@ const char* topkv_status_string(topkv_status_t status) {
     case TOPKV_ERR_BOUNDS: return "TOPKV_ERR_BOUNDS: block table entry, length, slot or packed capacity out of range";
     case TOPKV_ERR_DEVICE: return "TOPKV_ERR_DEVICE: HIP device query failed";
     case TOPKV_ERR_CHECKSUM: return "TOPKV_ERR_CHECKSUM: serialized header or checksum mismatch";
+    case TOPKV_ERR_TIMEOUT: return "TOPKV_ERR_TIMEOUT: a layer's ready word did not arrive within the timeout";
+    case TOPKV_ERR_CANCELLED: return "TOPKV_ERR_CANCELLED: the cancel word was set while a layer was awaited";
   }
   return "TOPKV_ERR_UNKNOWN";
 }

@@ -32,6 +32,8 @@ TOPKV_ERR_LAUNCH = 3
 TOPKV_ERR_BOUNDS = 4
 TOPKV_ERR_DEVICE = 5
 TOPKV_ERR_CHECKSUM = 6
+TOPKV_ERR_TIMEOUT = 7
+TOPKV_ERR_CANCELLED = 8
 TOPKV_MAX_BATCH_REQS = 4096
 TOPKV_CHECK_RESULT_WORDS = 4
 
@@ -48,7 +50,8 @@ EXPORTS = ["topkv_pack_layer", "topkv_unpack_layer", "topkv_pack_layer_batched",
            "topkv_pack_layer_shards", "topkv_unpack_layer_shards", "topkv_packed_state_bytes",
            "topkv_pack_state_layer", "topkv_unpack_state_layer", "topkv_check_state_slots",
            "topkv_check_state_workspace_bytes", "topkv_kvcache1_pack_layers", "topkv_kvcache1_unpack_layers",
-           "topkv_kvcache1_pack_seal", "topkv_kvcache1_verify_unpack"]
+           "topkv_kvcache1_pack_seal", "topkv_kvcache1_verify_unpack", "topkv_engine_pack_layers",
+           "topkv_engine_unpack_layers"]
 
 TOPKV_LAYOUT_PACKED = 0
 TOPKV_LAYOUT_POOL = 1
@@ -76,6 +79,11 @@ class topkv_state_pool_t(ctypes.Structure):
 
 class topkv_launch_t(ctypes.Structure):
     _fields_ = [("stream", ctypes.c_void_p), ("start", ctypes.c_void_p), ("stop", ctypes.c_void_p)]
+
+
+class topkv_engine_t(ctypes.Structure):
+    _fields_ = [("ready", ctypes.c_void_p), ("cancel", ctypes.c_void_p), ("status", ctypes.c_void_p),
+                ("epoch", ctypes.c_uint32), ("workgroups_per_cu", ctypes.c_int32), ("timeout_us", ctypes.c_int64)]
 
 
 _P = ctypes.c_void_p
@@ -129,6 +137,10 @@ _SIGS = {
                                         ctypes.POINTER(topkv_launch_t)]),
     "topkv_check_state_slots": (_I32, [ctypes.POINTER(topkv_state_pool_t), _I32, _P, _I32, _P, _I64, _P, _P]),
     "topkv_check_state_workspace_bytes": (_I64, [ctypes.POINTER(topkv_state_pool_t)]),
+    "topkv_engine_pack_layers": (_I32, [_POOL, _I32, _I32, _I32, _P, _I32, _P, _P, _I64, _I64,
+                                        ctypes.POINTER(topkv_engine_t), _P]),
+    "topkv_engine_unpack_layers": (_I32, [_P, _I64, _I64, _POOL, _I32, _I32, _I32, _P, _I32, _P,
+                                          ctypes.POINTER(topkv_engine_t), _P]),
     "topkv_dma_create": (_I32, [ctypes.POINTER(_P)]),
     "topkv_dma_submit": (_I32, [_P, _P, _P, _P, _I64, ctypes.POINTER(_I64)]),
     "topkv_dma_wait": (_I32, [_P, _I64]),
@@ -472,11 +484,12 @@ def host_device_pointer(t: torch.Tensor) -> int:
     that write straight into it; raises for memory the device cannot map."""
     if t.is_cuda or not t.is_pinned():
         raise ValueError("expected a pinned host tensor")
+    base = t.untyped_storage().data_ptr()     # the mapping is looked up for the allocation's start
     d = ctypes.c_void_p()
-    rc = _hip.hipHostGetDevicePointer(ctypes.byref(d), ctypes.c_void_p(t.data_ptr()), 0)
+    rc = _hip.hipHostGetDevicePointer(ctypes.byref(d), ctypes.c_void_p(base), 0)
     if rc != 0 or not d.value:
         raise RuntimeError(f"hipHostGetDevicePointer failed ({rc}): host memory is not mapped")
-    return int(d.value)
+    return int(d.value) + (t.data_ptr() - base)
 
 
 def _any_ptr(x) -> int:
@@ -647,6 +660,62 @@ def prepare_pack_layer_shards(src, layer, num_reqs, block_tables, bt_stride, seq
             _I32(int(bt_stride)), _P(_table_ptr(seq_lens)), _I32(int(head_begin)), _I32(int(head_count)),
             _I32(int(shards)), _P(_ptr(dst)), _I64(int(shard_bytes)), _P(_stream(stream)))
     return PreparedCall("topkv_pack_layer_shards", args, (pool,))
+
+
+# --- layer engine ----------------------------------------------------------------
+
+def _word_ptr(x) -> int:
+    """Address of a ready / cancel word array: device memory, or pinned host
+    memory mapped for the device."""
+    if isinstance(x, torch.Tensor) and not x.is_cuda:
+        return host_device_pointer(x) if x.numel() else 0
+    return _ptr(x)
+
+
+def engine_options(ready=None, epoch=0, status=None, cancel=None, timeout_us=0, workgroups_per_cu=0) -> topkv_engine_t:
+    """topkv_engine_t for the engine calls: ready / cancel are int32 words in
+    device memory or pinned host memory (or addresses), status a device
+    int32 holding 0 at launch."""
+    return topkv_engine_t(_word_ptr(ready), _word_ptr(cancel), _ptr(status), ctypes.c_uint32(int(epoch) & 0xffffffff),
+                          int(workgroups_per_cu), int(timeout_us))
+
+
+def _engine_arg(engine):
+    return ctypes.byref(engine) if engine is not None else None
+
+
+def topkv_engine_pack_layers(src, first_layer, num_layers, num_reqs, block_tables, bt_stride, seq_lens, packed,
+                             layer_stride, packed_bytes=None, engine=None, stream=None) -> None:
+    _check(_lib.topkv_engine_pack_layers(ctypes.byref(_pool_arg(src)), int(first_layer), int(num_layers),
+                                         int(num_reqs), _table_ptr(block_tables), int(bt_stride), _table_ptr(seq_lens),
+                                         _ptr(packed), int(layer_stride), _nbytes(packed, packed_bytes),
+                                         _engine_arg(engine), _stream(stream)))
+
+
+def topkv_engine_unpack_layers(packed, layer_stride, dst, first_layer, num_layers, num_reqs, block_tables, bt_stride,
+                               seq_lens, packed_bytes=None, engine=None, stream=None) -> None:
+    _check(_lib.topkv_engine_unpack_layers(_ptr(packed), int(layer_stride), _nbytes(packed, packed_bytes),
+                                           ctypes.byref(_pool_arg(dst)), int(first_layer), int(num_layers),
+                                           int(num_reqs), _table_ptr(block_tables), int(bt_stride),
+                                           _table_ptr(seq_lens), _engine_arg(engine), _stream(stream)))
+
+
+def prepare_engine_pack_layers(src, first_layer, num_layers, num_reqs, block_tables, bt_stride, seq_lens, packed,
+                               layer_stride, packed_bytes=None, engine=None, stream=None) -> PreparedCall:
+    pool = _pool_arg(src)
+    args = (ctypes.byref(pool), _I32(int(first_layer)), _I32(int(num_layers)), _I32(int(num_reqs)),
+            _P(_table_ptr(block_tables)), _I32(int(bt_stride)), _P(_table_ptr(seq_lens)), _P(_ptr(packed)),
+            _I64(int(layer_stride)), _I64(_nbytes(packed, packed_bytes)), _engine_arg(engine), _P(_stream(stream)))
+    return PreparedCall("topkv_engine_pack_layers", args, (pool, engine))
+
+
+def prepare_engine_unpack_layers(packed, layer_stride, dst, first_layer, num_layers, num_reqs, block_tables,
+                                 bt_stride, seq_lens, packed_bytes=None, engine=None, stream=None) -> PreparedCall:
+    pool = _pool_arg(dst)
+    args = (_P(_ptr(packed)), _I64(int(layer_stride)), _I64(_nbytes(packed, packed_bytes)), ctypes.byref(pool),
+            _I32(int(first_layer)), _I32(int(num_layers)), _I32(int(num_reqs)), _P(_table_ptr(block_tables)),
+            _I32(int(bt_stride)), _P(_table_ptr(seq_lens)), _engine_arg(engine), _P(_stream(stream)))
+    return PreparedCall("topkv_engine_unpack_layers", args, (pool, engine))
 
 
 # --- fixed-state layers ---------------------------------------------------------

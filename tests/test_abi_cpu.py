@@ -39,7 +39,7 @@ def test_library_exports_every_declared_symbol(tk):
 
 
 def test_status_strings(tk):
-    for code in range(6):
+    for code in range(9):
         s = tk.topkv_status_string(code)
         assert s.startswith("TOPKV_")
     assert tk.topkv_status_string(99) == "TOPKV_ERR_UNKNOWN"
@@ -106,6 +106,39 @@ def test_empty_work_is_a_no_op(tk):
     tk.topkv_unpack_layer(0, good, 1, 0, 0, stream=0)
     tk.topkv_pack_layer_batched(good, 0, 0, 0, 1, 0, 0, dst_bytes=0, stream=0)
     tk.topkv_unpack_layer_batched(0, good, 0, 0, 0, 1, 0, src_bytes=0, stream=0)
+
+
+def test_engine_validation(tk):
+    """The layer engine refuses bad ranges, strides and wait options before
+    any runtime call; an empty batch launches nothing."""
+    INV, UNS = tk.TOPKV_ERR_INVALID_ARG, tk.TOPKV_ERR_UNSUPPORTED
+    bt, lens, buf, ready, status = 0x20000, 0x30000, 0x40000, 0x50000, 0x60000
+    good = _pool(tk)                     # 2 layers
+    stride = 1 << 20
+    pk, up = tk.topkv_engine_pack_layers, tk.topkv_engine_unpack_layers
+    for first, count in ((-1, 1), (0, 3), (1, 2), (2, 1), (0, 0)):
+        _expect(tk, INV, pk, good, first, count, 2, bt, 4, lens, buf, stride, packed_bytes=2 * stride)
+        _expect(tk, INV, up, buf, stride, good, first, count, 2, bt, 4, lens, packed_bytes=2 * stride)
+    _expect(tk, INV, pk, good, 0, 2, 2, bt, 4, lens, buf, 0, packed_bytes=2 * stride)           # no layer stride
+    _expect(tk, INV, pk, good, 0, 2, 2, bt, 4, lens, buf, stride, packed_bytes=stride - 1)       # last block outside
+    _expect(tk, INV, pk, good, 0, 2, 2, bt, 4, lens, buf, -stride, packed_bytes=2 * stride)
+    _expect(tk, INV, pk, good, 0, 2, -1, bt, 4, lens, buf, stride, packed_bytes=2 * stride)
+    _expect(tk, INV, pk, good, 0, 2, 2, 0, 4, lens, buf, stride, packed_bytes=2 * stride)        # null tables
+    _expect(tk, INV, pk, good, 0, 2, 2, bt, 4, 0, buf, stride, packed_bytes=2 * stride)          # null lengths
+    _expect(tk, INV, pk, good, 0, 2, 2, bt, 0, lens, buf, stride, packed_bytes=2 * stride)
+    _expect(tk, INV, up, 0, stride, good, 0, 2, 2, bt, 4, lens, packed_bytes=2 * stride)         # null packed
+    _expect(tk, UNS, pk, good, 0, 2, tk.TOPKV_MAX_BATCH_REQS + 1, bt, 4, lens, buf, stride, packed_bytes=2 * stride)
+    _expect(tk, UNS, pk, good, 0, 2, 4096, bt, 1 << 20, lens, buf, stride, packed_bytes=2 * stride)  # 2^31 items
+    for opt in (tk.engine_options(ready=ready, status=0, timeout_us=1000),          # ready without status
+                tk.engine_options(ready=ready, status=status, timeout_us=0),         # no timeout
+                tk.engine_options(ready=ready, status=status, timeout_us=60_000_001),
+                tk.engine_options(workgroups_per_cu=-1), tk.engine_options(workgroups_per_cu=65)):
+        _expect(tk, INV, pk, good, 0, 2, 2, bt, 4, lens, buf, stride, packed_bytes=2 * stride, engine=opt)
+        _expect(tk, INV, up, buf, stride, good, 0, 2, 2, bt, 4, lens, packed_bytes=2 * stride, engine=opt)
+    # no requests: nothing to launch, whatever the wait options
+    pk(good, 0, 2, 0, 0, 1, 0, 0, stride, packed_bytes=2 * stride,
+       engine=tk.engine_options(ready=ready, status=status, timeout_us=1000), stream=0)
+    up(0, stride, good, 1, 1, 0, 0, 1, 0, packed_bytes=0, stream=0)
 
 
 def test_check_tables_validation(tk):
@@ -262,3 +295,35 @@ def test_checked_mode_validates_arguments_first(tk, monkeypatch):
     _expect(tk, UNS, tk.topkv_pack_layer_batched, good, 0, tk.TOPKV_MAX_BATCH_REQS + 1, bt, 4, lens,
             buf, dst_bytes=1 << 20)
     tk.topkv_pack_layer(good, 0, 0, 0, 0, stream=0)            # zero tokens: still nothing to do
+
+
+CEILING_HEADER = os.path.join(ROOT, "include", "topkv_ceiling.h")
+
+
+def test_ceiling_library_exports_and_validation():
+    """The measurement kernels' library loads, exports what its header
+    declares under the binding's names, and refuses bad arguments before any
+    launch (no GPU needed)."""
+    from paper_2607_28633_amd.build import CEILING_LIBRARY, build_ceiling
+    if not os.path.exists(CEILING_LIBRARY):
+        build_ceiling()
+    from paper_2607_28633_amd import ceiling as cl
+    from paper_2607_28633_amd import topkv as tk
+    text = re.sub(r"/\*.*?\*/", "", open(CEILING_HEADER).read(), flags=re.S)
+    declared = sorted(set(re.findall(r"\b(topkv_ceiling_[a-z_0-9]+)\s*\(", text)))
+    assert declared == sorted(cl.EXPORTS)
+    lib = ctypes.CDLL(cl.LIBRARY)
+    assert all(hasattr(lib, n) for n in declared)
+    INV = tk.TOPKV_ERR_INVALID_ARG
+    a, b = 0x10000, 0x20000
+    for fn, args in ((cl.topkv_ceiling_copy, (0, b, 64)), (cl.topkv_ceiling_copy, (a, b, 17)),
+                     (cl.topkv_ceiling_copy, (a + 8, b, 64)), (cl.topkv_ceiling_copy, (a, b, -16)),
+                     (cl.topkv_ceiling_copy_layers, (a, 64, b, 64, 48, -1)),
+                     (cl.topkv_ceiling_copy_layers, (a, 60, b, 64, 48, 2)),
+                     (cl.topkv_ceiling_copy_layers, (a, 64, b, 64, 48, 2, 65)),
+                     (cl.topkv_ceiling_copy_timeline, (a, b, 64, 0))):
+        with pytest.raises(tk.TopkvError) as ei:
+            fn(*args, stream=0)
+        assert ei.value.status == INV, (fn.__name__, args)
+    cl.topkv_ceiling_copy(a, b, 0, stream=0)                       # nothing to copy: nothing launched
+    cl.topkv_ceiling_copy_layers(a, 64, b, 64, 0, 3, stream=0)
