@@ -47,8 +47,10 @@
 // current one is folded.
 #include <hip/hip_runtime.h>
 
+#include <atomic>
 #include <cstdint>
 #include <cstring>
+#include <mutex>
 
 #include "internal.h"
 #include "topkv.h"
@@ -691,9 +693,57 @@ topkv_status_t kv1_move_layers(bool pack, const topkv_pool_t* pool, int32_t firs
   return TOPKV_OK;
 }
 
+// The allocation-free CRC's workspace: one copy per GPU, held until the
+// process ends.  Host code never names it in a launch or a copy: the name is
+// a host-side stand-in, and its device address on each device comes from
+// hipGetSymbolAddress (scratch_words below).
+__device__ __align__(256) uint64_t scratch[kWsTables + kMaxSpans];
+static_assert(sizeof(scratch) == (size_t)TOPKV_CRC64_NOALLOC_SCRATCH_BYTES, "scratch size in topkv.h");
+
+constexpr int kMaxDevices = 64;
+std::atomic<uint64_t*> g_scratch[kMaxDevices];
+std::mutex g_scratch_mutex;
+
+// The current device's address of `scratch`, looked up once per device
+// (with that device current) and kept.
+topkv_status_t scratch_words(uint64_t** out) {
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDevices) return TOPKV_ERR_DEVICE;
+  uint64_t* p = g_scratch[dev].load(std::memory_order_acquire);
+  if (!p) {
+    std::lock_guard<std::mutex> lock(g_scratch_mutex);
+    p = g_scratch[dev].load(std::memory_order_relaxed);
+    if (!p) {
+      void* addr = nullptr;
+      if (hipGetSymbolAddress(&addr, HIP_SYMBOL(scratch)) != hipSuccess || !addr) return TOPKV_ERR_DEVICE;
+      p = static_cast<uint64_t*>(addr);
+      g_scratch[dev].store(p, std::memory_order_release);
+    }
+  }
+  *out = p;
+  return TOPKV_OK;
+}
+
 }  // namespace
 
 extern "C" {
+
+topkv_status_t topkv_crc64_noalloc(const void* data, int64_t nbytes, uint64_t* crc_out, hipStream_t stream) {
+  if (nbytes < 0 || !crc_out || (nbytes > 0 && !data)) return TOPKV_ERR_INVALID_ARG;
+  if (nbytes > 0 && !aligned16(data)) return TOPKV_ERR_UNSUPPORTED;
+  // every length fits: the workspace is the tables plus at most kMaxSpans span registers
+  if ((int64_t)sizeof(uint64_t) * crc_words(nbytes) > (int64_t)TOPKV_CRC64_NOALLOC_SCRATCH_BYTES)
+    return TOPKV_ERR_UNSUPPORTED;
+  uint64_t* ws = nullptr;
+  const topkv_status_t st = scratch_words(&ws);
+  if (st != TOPKV_OK) return st;
+  // the tables kernel writes every table word and each span kernel its own
+  // register before the finishing kernel reads them: nothing left by an
+  // earlier call is read
+  const topkv_status_t t = crc64_tables(ws, span_geometry(nbytes).span, stream);
+  if (t != TOPKV_OK) return t;
+  return crc64_launch(static_cast<const unsigned char*>(data), nbytes, ws, ws + kWsTables, crc_out, stream);
+}
 
 int64_t topkv_crc64_workspace_bytes(int64_t nbytes) {
   if (nbytes < 0) return -1;

@@ -51,7 +51,7 @@ EXPORTS = ["topkv_pack_layer", "topkv_unpack_layer", "topkv_pack_layer_batched",
            "topkv_pack_state_layer", "topkv_unpack_state_layer", "topkv_check_state_slots",
            "topkv_check_state_workspace_bytes", "topkv_kvcache1_pack_layers", "topkv_kvcache1_unpack_layers",
            "topkv_kvcache1_pack_seal", "topkv_kvcache1_verify_unpack", "topkv_engine_pack_layers",
-           "topkv_engine_unpack_layers"]
+           "topkv_engine_unpack_layers", "topkv_crc64_noalloc"]
 
 TOPKV_LAYOUT_PACKED = 0
 TOPKV_LAYOUT_POOL = 1
@@ -123,6 +123,7 @@ _SIGS = {
                                             _P, _P]),
     "topkv_crc64": (_I32, [_P, _I64, _P, _I64, _P, _P]),
     "topkv_crc64_workspace_bytes": (_I64, [_I64]),
+    "topkv_crc64_noalloc": (_I32, [_P, _I64, _P, _P]),
     "topkv_move_layer": (_I32, [ctypes.POINTER(topkv_view_t), ctypes.POINTER(topkv_view_t), _I32, _P, _I32,
                                 _I32, _P]),
     "topkv_pack_layer_heads": (_I32, [_POOL, _I32, _I32, _P, _I32, _P, _I32, _I32, _P, _I64, _P]),
@@ -403,6 +404,10 @@ def topkv_kvcache1_unpack_layers(blob, dst, first_layer, num_layers, block_table
 def topkv_crc64(data, nbytes, workspace, crc_out, workspace_bytes=None, stream=None) -> None:
     _check(_lib.topkv_crc64(_ptr(data), int(nbytes), _ptr(workspace), _nbytes(workspace, workspace_bytes),
                             _ptr(crc_out), _stream(stream)))
+
+
+def topkv_crc64_noalloc(data, nbytes, crc_out, stream=None) -> None:
+    _check(_lib.topkv_crc64_noalloc(_ptr(data), int(nbytes), _ptr(crc_out), _stream(stream)))
 
 
 def topkv_crc64_workspace_bytes(nbytes) -> int:

@@ -327,3 +327,14 @@ def test_ceiling_library_exports_and_validation():
         assert ei.value.status == INV, (fn.__name__, args)
     cl.topkv_ceiling_copy(a, b, 0, stream=0)                       # nothing to copy: nothing launched
     cl.topkv_ceiling_copy_layers(a, 64, b, 64, 0, 3, stream=0)
+
+
+def test_crc64_noalloc_validation(tk):
+    """The allocation-free CRC refuses bad arguments before touching the
+    runtime (its array's address is looked up only after them)."""
+    INV, UNS = tk.TOPKV_ERR_INVALID_ARG, tk.TOPKV_ERR_UNSUPPORTED
+    out = 0x50000
+    _expect(tk, INV, tk.topkv_crc64_noalloc, 0, 16, out)            # null data
+    _expect(tk, INV, tk.topkv_crc64_noalloc, 0x10000, -1, out)      # negative length
+    _expect(tk, INV, tk.topkv_crc64_noalloc, 0x10000, 16, 0)        # null result word
+    _expect(tk, UNS, tk.topkv_crc64_noalloc, 0x10008, 16, out)      # data off 16-byte alignment
