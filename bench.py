@@ -185,16 +185,35 @@ def layer_kernel(wl, direction):
     return f"kv_{direction}_kernel"
 
 
+def engine_kernel(wl, setup, direction):
+    """The kernel an engine launch of the workload runs (the library's
+    choice): with every layer ready, the batched direct grid with the layers
+    on grid z while it fits that grid's limits, else the persistent
+    kv_engine_kernel."""
+    runs = [n for kind, _, n in setup.chunks if kind == "engine"]
+    if not runs:
+        return "no engine launch (every layer has its own call)"
+    row = wl.num_heads * wl.head_dim * wl.elem_bytes
+    plane = (wl.page_size if direction == "pack" else wl.dst_page_size) * row
+    tiles = -(-plane // (256 * 8 * 16))
+    stride = (wl.block_tables if direction == "pack" else wl.dst_block_tables).shape[1]
+    direct = (wl.num_reqs * stride * wl.planes * tiles <= 1 << 20 and stride <= 65535 and wl.num_reqs <= 1024
+              and wl.num_reqs * max(runs) <= 65535)
+    name = f"kv_{direction}_kernel (batched direct grid, layers on grid z)" if direct else "kv_engine_kernel"
+    return f"{name}, layer engine over runs of {'/'.join(str(n) for n in sorted(set(runs)))} layers"
+
+
 def step_bytes(wl):
     """Algorithmic bytes of one pack and one unpack launch, averaged over layers."""
     per = [layer_bytes(wl, l) for l in range(wl.num_layers)]
     return (sum(p for p, _ in per) // wl.num_layers, sum(u for _, u in per) // wl.num_layers)
 
 
-def read_traffic(workload):
-    """HBM traffic per launch from the committed rocprofv3 --pmc summary, or
-    None when the kernels' code has changed since the counters were taken."""
-    path = os.path.join(PROFILES, f"kv_pack_unpack_{workload}_pmc.txt")
+def read_traffic(workload, engine=False):
+    """HBM traffic per launch from the committed rocprofv3 --pmc summary of
+    the workload's per-layer launches (or of its engine launches), or None
+    when the kernels' code has changed since the counters were taken."""
+    path = os.path.join(PROFILES, f"kv_{'engine' if engine else 'pack_unpack'}_{workload}_pmc.txt")
     if not os.path.exists(path):
         return None
     vals = {}
@@ -799,11 +818,11 @@ def run(args):
             tgt[name]["kernel_stamp_median_us"] = round(float(np.median(per[d])), 3)
 
     dom = max(kern, key=lambda k: kern[k]["avg_us"] * kern[k]["launches"])
-    traffic_vals = read_traffic(args.workload)
+    traffic_vals = read_traffic(args.workload, engine=args.issue == "engine")
     tkey = f"{'engine_' if args.issue == 'engine' else ''}{dom}_hbm_bytes_per_launch"
     traffic = float(traffic_vals[tkey]) if traffic_vals and tkey in traffic_vals else None
     achieved = kern[dom]["gbs"]
-    kname = "kv_engine_kernel (layer engine)" if args.issue == "engine" else layer_kernel(wl, dom)
+    kname = engine_kernel(wl, st, dom) if args.issue == "engine" else layer_kernel(wl, dom)
     roofline = {"bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s",
                 "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": traffic,
                 "kernel": f"{dom} launch: {kname}", "bytes_per_launch": kern[dom]["bytes_per_launch"],
@@ -880,8 +899,8 @@ def config_block(args, topkv):
         entry = {"requests": wl.num_reqs, "layers": wl.num_layers, "tokens": int(wl.seq_lens.sum()),
                  "page_size": wl.page_size, "dst_page_size": wl.dst_page_size,
                  "packed_bytes_per_layer": st.nbytes}
-        traffic = read_traffic(name)
         for issue in ("engine", "launches"):
+            traffic = read_traffic(name, engine=issue == "engine")
             ms, us, launches = time_sweeps(st, issue, steps, 1, "graph")
             kern = kernel_figures(wl, us, steps, launches)
             for d in ("pack", "unpack"):
