@@ -404,7 +404,9 @@ topkv_status_t topkv_kvcache1_verify_unpack(const void* blob, int64_t blob_bytes
                                             hipStream_t stream);
 
 /* CRC-64/XZ (as above) of nbytes of device memory at data (16-byte aligned,
- * any length), written to the device word *crc_out on the stream.
+ * any length up to 256 spans of 2 GiB - 64 KiB, about 512 GiB, beyond any
+ * one device's memory: TOPKV_ERR_UNSUPPORTED above that), written to the
+ * device word *crc_out on the stream.
  * workspace: topkv_crc64_workspace_bytes(nbytes) bytes of device memory,
  * 8-byte aligned, caller-owned. */
 topkv_status_t topkv_crc64(const void* data, int64_t nbytes, void* workspace,

@@ -43,6 +43,11 @@ topkv_status_t topkv_ceiling_copy_layers(const void* src, int64_t src_stride, vo
                                          int64_t layer_bytes, int32_t layers, int32_t workgroups_per_cu,
                                          hipStream_t stream);
 
+/* Read `bytes` at src, one 32 KiB tile per workgroup, and write the XOR of
+ * tile b's 32-bit words to sink[b] (device memory, ceil(bytes / 32 KiB)
+ * words): the read-only ceiling a checksum pass is read against. */
+topkv_status_t topkv_ceiling_read(const void* src, int64_t bytes, uint32_t* sink, hipStream_t stream);
+
 /* One workgroup of 64 lanes that touches no memory: the cost of a launch. */
 topkv_status_t topkv_ceiling_empty(hipStream_t stream);
 

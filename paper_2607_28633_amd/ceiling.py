@@ -16,12 +16,13 @@ if not os.path.exists(LIBRARY):
     raise ImportError(f"{LIBRARY} is missing: build it with `python -m paper_2607_28633_amd.build`")
 _lib = ctypes.CDLL(LIBRARY)
 
-EXPORTS = ["topkv_ceiling_copy", "topkv_ceiling_copy_layers", "topkv_ceiling_empty", "topkv_ceiling_copy_timeline",
-           "topkv_ceiling_wall_clock_khz"]
+EXPORTS = ["topkv_ceiling_copy", "topkv_ceiling_copy_layers", "topkv_ceiling_read", "topkv_ceiling_empty",
+           "topkv_ceiling_copy_timeline", "topkv_ceiling_wall_clock_khz"]
 _P, _I32, _I64 = ctypes.c_void_p, ctypes.c_int32, ctypes.c_int64
 _SIGS = {
     "topkv_ceiling_copy": [_P, _P, _I64, _P],
     "topkv_ceiling_copy_layers": [_P, _I64, _P, _I64, _I64, _I32, _I32, _P],
+    "topkv_ceiling_read": [_P, _I64, _P, _P],
     "topkv_ceiling_empty": [_P],
     "topkv_ceiling_copy_timeline": [_P, _P, _I64, _P, _P],
     "topkv_ceiling_wall_clock_khz": [ctypes.POINTER(_I32)],
@@ -45,6 +46,10 @@ def topkv_ceiling_copy_layers(src, src_stride, dst, dst_stride, layer_bytes, lay
                               stream=None) -> None:
     _check(_lib.topkv_ceiling_copy_layers(_ptr(src), int(src_stride), _ptr(dst), int(dst_stride), int(layer_bytes),
                                           int(layers), int(workgroups_per_cu), _stream(stream)))
+
+
+def topkv_ceiling_read(src, nbytes, sink, stream=None) -> None:
+    _check(_lib.topkv_ceiling_read(_ptr(src), int(nbytes), _ptr(sink), _stream(stream)))
 
 
 def topkv_ceiling_empty(stream=None) -> None:

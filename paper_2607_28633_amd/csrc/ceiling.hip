@@ -58,6 +58,22 @@ __global__ __launch_bounds__(kThreads) void ceiling_copy_layers_kernel(const cha
   }
 }
 
+// Read-only: each workgroup reads its 32 KiB tile and writes the XOR of it
+// as one word to sink[blockIdx.x] (so the loads cannot be dropped).
+__global__ __launch_bounds__(kThreads) void ceiling_read_kernel(const V* __restrict__ s, int64_t n16,
+                                                                uint32_t* __restrict__ sink) {
+  __shared__ uint32_t part[kThreads / 64];
+  V v[kVpt];
+  load_tile(v, s, (int64_t)blockIdx.x * kThreads * kVpt, n16);
+  uint32_t x = 0;
+#pragma unroll
+  for (int j = 0; j < kVpt; ++j) x ^= v[j].x ^ v[j].y ^ v[j].z ^ v[j].w;
+  for (int o = 32; o > 0; o >>= 1) x ^= __shfl_xor(x, o);
+  if ((threadIdx.x & 63) == 0) part[threadIdx.x >> 6] = x;
+  __syncthreads();
+  if (threadIdx.x == 0) sink[blockIdx.x] = part[0] ^ part[1] ^ part[2] ^ part[3];
+}
+
 __global__ void ceiling_empty_kernel() {}
 
 __global__ __launch_bounds__(kThreads) void ceiling_timeline_kernel(const V* __restrict__ s, V* __restrict__ d,
@@ -125,6 +141,17 @@ topkv_status_t topkv_ceiling_copy_layers(const void* src, int64_t src_stride, vo
   hipLaunchKernelGGL(ceiling_copy_layers_kernel, dim3((unsigned)(total < cap ? total : cap)), dim3(kThreads), 0,
                      stream, static_cast<const char*>(src), src_stride, static_cast<char*>(dst), dst_stride,
                      layer_bytes / 16, tiles, total);
+  return hipGetLastError() == hipSuccess ? TOPKV_OK : TOPKV_ERR_LAUNCH;
+}
+
+topkv_status_t topkv_ceiling_read(const void* src, int64_t bytes, uint32_t* sink, hipStream_t stream) {
+  using namespace topkv_ceiling;
+  if (!src || !sink || bytes < 0 || bytes % 16 || !aligned(src)) return TOPKV_ERR_INVALID_ARG;
+  const int64_t tiles = (bytes + kTile - 1) / kTile;
+  if (tiles == 0) return TOPKV_OK;
+  if (tiles > INT32_MAX) return TOPKV_ERR_UNSUPPORTED;
+  hipLaunchKernelGGL(ceiling_read_kernel, dim3((unsigned)tiles), dim3(kThreads), 0, stream,
+                     static_cast<const V*>(src), bytes / 16, sink);
   return hipGetLastError() == hipSuccess ? TOPKV_OK : TOPKV_ERR_LAUNCH;
 }
 

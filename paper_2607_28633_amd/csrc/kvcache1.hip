@@ -22,17 +22,19 @@
 //     the lanes inside a span and of the spans;
 //   kernel 1: the data, front-padded with zero bytes (free, by the property
 //     above), is cut into at most 256 equal spans of whole 64 KiB
-//     sub-chunks, one 1024-lane workgroup per span.  Lane t takes bytes
-//     [64t, 64t + 64) of every sub-chunk: a wave loads its 4 KiB slice with
-//     fully coalesced 16-byte loads (the next sub-chunk's in flight while
-//     this one is folded) and hands each lane its 64 bytes through an LDS
-//     staging area; lanes run them through slicing-by-4 tables held in LDS
-//     in 8 replicas (lane t reads replica t mod 8, which spreads a wave's
-//     random lookups over the LDS banks),
-//     and advances its running register by one sub-chunk per step; a tree of
-//     table multiplies joins the lanes at the end of the span;
-//   kernel 2: one workgroup joins the span registers the same way, appends
-//     the sub-16-byte tail and applies the preset and complement.
+//     sub-chunks, one 1024-lane workgroup per span (several inputs of one
+//     length, such as a blob's K and V tensors, share one launch, each with
+//     its share of the spans).  Lane t takes bytes [64t, 64t + 64) of every
+//     sub-chunk: a wave loads its 4 KiB slice with fully coalesced 16-byte
+//     buffer loads (the next two sub-chunks' in flight while this one is
+//     folded; a load in the front padding lies outside the buffer and returns
+//     zeros) and hands each lane its 64 bytes through an LDS staging area;
+//     lanes run them through slicing-by-4 tables held in LDS in 16 replicas
+//     arranged so that the 32 lanes an LDS cycle serves never share a bank
+//     (crc_word4), and advance their running register by one sub-chunk per
+//     step; a tree of table multiplies joins the lanes at the end of the span;
+//   kernel 2: one workgroup per input joins its span registers the same way,
+//     appends the sub-16-byte tail and applies the preset and complement.
 // Shift constants x^(8n) mod P are computed on the host.
 //
 // One-pass serialization: kernel 1 also runs with the pool as its source
@@ -64,12 +66,13 @@ constexpr int kLoads = kPiece / 16;                             // 16-byte loads
 constexpr int kSubLog2 = 16;                                    // 64 KiB sub-chunk = 1024 lanes x 64 B
 constexpr int64_t kSub = (int64_t)1 << kSubLog2;
 constexpr int kMaxSpans = 256;                                  // span workgroups per CRC at most
+constexpr int64_t kMaxSpanSubs = 32767;                         // sub-chunks per span at most (span < 2 GiB)
 constexpr int kLaneLevels = 10;                                 // log2(kCrcThreads)
 constexpr int kSpanLevels = 8;                                  // log2(kMaxSpans)
 constexpr int kTableWords = 8 * 256;                            // one set of 8 byte tables (16 KiB)
-constexpr int kCopies = 8;                                      // LDS replicas of the slicing tables
+constexpr int kCopies = 16;                                     // LDS replicas of the slicing tables
 constexpr int kWaves = kCrcThreads / 64;
-constexpr int kStageWords = kWaves * 64 * kPiece / 8;           // per-wave staging of one sub-chunk slice
+constexpr int kStageWords = kWaves * 64 * 16 / 8;               // per-wave staging of one 1 KiB row
 // workspace table sets: 0 slicing, 1 sub-chunk advance, 2.. lane levels, then span levels
 constexpr int kSetSlice = 0, kSetSub = 1, kSetLane = 2, kSetSpan = kSetLane + kLaneLevels;
 constexpr int kSets = kSetSpan + kSpanLevels;
@@ -138,17 +141,45 @@ __device__ inline uint64_t lookup8(uint64_t v, const uint64_t* t) {   // t: 8 x 
          t[6 * 256 + ((v >> 48) & 0xff)] ^ t[7 * 256 + (v >> 56)];
 }
 
-// Four bytes (little-endian word w) into the register with slicing-by-4
-// tables in replicated layout: entry (k, b) of this lane's replica is
-// tc[(k * 256 + b) * kCopies]; byte 0 is followed by 3 more bytes, byte 3 by
-// none.
-__device__ inline uint64_t crc_word4(uint64_t reg, uint32_t w, const uint64_t* tc) {
-  reg ^= w;
-  return tc[(3 * 256 + (reg & 0xff)) * kCopies] ^ tc[(2 * 256 + ((reg >> 8) & 0xff)) * kCopies] ^
-         tc[(1 * 256 + ((reg >> 16) & 0xff)) * kCopies] ^ tc[((reg >> 24) & 0xff) * kCopies] ^ (reg >> 32);
+// Four bytes (little-endian word w) into the register (lo, hi) with
+// slicing-by-4 tables held in LDS in kCopies = 16 replicas.  Layout (byte
+// offsets in the 128 KiB table region): tables 2h and 2h + 1 share the 64 KiB
+// region h; entry b of table t, replica r sits at h * 65536 + b * 256 +
+// (t % 2) * 128 + r * 8.  So, with the LDS's 64 four-byte banks, replica r of
+// an even table occupies only banks 2r and 2r + 1, and of an odd table banks
+// 32 + 2r and 33 + 2r.  A ds_read_b64 serves 32 lanes at a time; lanes r and
+// r + 16 of such a group share replica r, so they look up the two tables of a
+// pair in the opposite order (lanes 16..31 of every 32 take table t ^ 1 where
+// lanes 0..15 take table t): in every instruction the 32 lanes touch 64
+// different banks whatever bytes they look up.  Every address is one byte
+// permute of the lane's L = r << 3 | (r << 3 | 128) << 8 | 1 << 24 (the two
+// half-row bytes, then the region bytes 0 and 1) and x = lo ^ w: sel[k] puts
+// the half byte of its table in byte 0, the looked-up byte of x in byte 1 and
+// the region in byte 2.  Byte 0 of the word is followed by 3 more bytes
+// (table 3), byte 3 by none (table 0).
+// a ^ b ^ c in one instruction: gfx950's three-input bitwise operation, truth table 0x96 (bit i of
+// the table is the parity of i, the XOR of the three input bits).
+__device__ __forceinline__ uint32_t xor3(uint32_t a, uint32_t b, uint32_t c) {
+  return __builtin_amdgcn_bitop3_b32(a, b, c, 0x96);
+}
+
+__device__ __forceinline__ void crc_word4(uint32_t& lo, uint32_t& hi, uint32_t w, const char* tab, uint32_t L,
+                                          const uint32_t (&sel)[4]) {
+  const uint32_t x = lo ^ w;
+  const uint2 e0 = *reinterpret_cast<const uint2*>(tab + __builtin_amdgcn_perm(L, x, sel[0]));
+  const uint2 e1 = *reinterpret_cast<const uint2*>(tab + __builtin_amdgcn_perm(L, x, sel[1]));
+  const uint2 e2 = *reinterpret_cast<const uint2*>(tab + __builtin_amdgcn_perm(L, x, sel[2]));
+  const uint2 e3 = *reinterpret_cast<const uint2*>(tab + __builtin_amdgcn_perm(L, x, sel[3]));
+  lo = xor3(xor3(e0.x, e1.x, e2.x), e3.x, hi);
+  hi = xor3(e0.y, e1.y, e2.y) ^ e3.y;
 }
 
 typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
+
+// Buffer resource word 3 of an untyped buffer (32-bit data format), and the cache-policy bit of a
+// non-temporal buffer access.
+constexpr int kBufferWord3 = 0x00020000;
+constexpr int kBufferNt = 2;
 
 // Copy `words` words (a multiple of nthreads * kBatch) from global memory
 // into LDS with kBatch loads in flight per thread before their stores.
@@ -192,47 +223,72 @@ struct PoolSide {
   char* pool;             // pool base (layer 0)
   u32x4* blob;            // the tensor's first byte in the blob
   const int32_t* table;   // the request's block table
-  int64_t layer_bytes, page_bytes, plane_off, num_pages;
+  int64_t layer_bytes, page_bytes, num_pages;
+  int64_t plane_off;      // the tensor's plane inside a page row (set per tensor by the kernel)
+  int64_t plane_stride;   // between the planes of consecutive tensors
   int64_t step_q;         // kSub / row_bytes
   int32_t step_r;         // kSub mod row_bytes
   int32_t row_bytes, seq_len, page_size, first_layer;
   Div32 d_row, d_seq, d_page;
 };
 
-// Kernel 1: raw register of each span of the front-padded stream.  The
-// tensor (or data) has `head` bytes (a multiple of 16); `pad` leading zero
-// bytes (a multiple of 16) make head + pad = gridDim.x spans of span_subs
-// sub-chunks.
+// Kernel 1: raw register of each span of the front-padded streams of
+// gridDim.x / spans_per_buf inputs (tensors) of `head` bytes each (a multiple
+// of 16), input i at data + i * buf_stride bytes (pool modes: the blob tensor
+// of plane i); `pad` leading zero bytes (a multiple of 16) make head + pad =
+// spans_per_buf spans of span_subs sub-chunks.  Workgroup w takes span
+// w % spans_per_buf of input w / spans_per_buf and writes its register to
+// partial[input * kMaxSpans + span].
 template <int kMode>
-__global__ __launch_bounds__(kCrcThreads) void crc64_span_kernel(const u32x4* __restrict__ data, int64_t pad,
-                                                                 int64_t span_subs,
+__global__ __launch_bounds__(kCrcThreads) void crc64_span_kernel(const u32x4* __restrict__ data, int64_t buf_stride,
+                                                                 int64_t pad, int64_t span_subs,
+                                                                 int32_t spans_per_buf,
                                                                  const uint64_t* __restrict__ tables,
-                                                                 uint64_t* __restrict__ partial, PoolSide ps) {
-  // [0, 8192): slicing tables 0..3 in kCopies replicas (64 KiB); [8192, 16384): per-wave staging
-  // (64 KiB); after the span, all 128 KiB hold join levels 0..7
-  __shared__ __attribute__((aligned(16))) uint64_t big[4 * 256 * kCopies + kStageWords];
-  __shared__ uint64_t t_sub[kTableWords];
-  __shared__ uint64_t acc[kCrcThreads];
-  static_assert(4 * 256 * kCopies + kStageWords == 8 * kTableWords, "join levels 0..7 fill the region");
-  uint64_t* t_slice = big;
-  {
-    // thread e writes entry e = (k, b) of tables 0..3 into all kCopies replicas
-    static_assert(4 * 256 == kCrcThreads, "one slicing entry per thread");
-    const uint64_t v = tables[kSetSlice * kTableWords + threadIdx.x];
+                                                                 uint64_t* __restrict__ partial, PoolSide ps_in) {
+  // big: slicing tables 0..3 in kCopies replicas (128 KiB), then the lane-join levels 0..7;
+  // small: per-wave staging of one 1 KiB row (16 KiB) and the sub-chunk advance table (16 KiB), then
+  // the join registers and level 8.
+  __shared__ __attribute__((aligned(16))) uint64_t big[4 * 256 * kCopies];
+  __shared__ __attribute__((aligned(16))) uint64_t small[kStageWords + kTableWords];
+  static_assert(4 * 256 * kCopies == 8 * kTableWords, "join levels 0..7 fill the table region");
+  static_assert(kStageWords + kTableWords >= kCrcThreads + kTableWords, "join registers and level 8 fit");
+  // The table words this thread places in LDS are loaded first; the LDS is filled once the first
+  // sub-chunks' loads are also on their way (below), so their latency overlaps the fill.
+  static_assert(4 * 256 == kCrcThreads, "one slicing entry per thread");
+  static_assert(kTableWords == 2 * kCrcThreads, "two sub-chunk advance words per thread");
+  const uint64_t slice_word = tables[kSetSlice * kTableWords + threadIdx.x];
+  const uint64_t sub_word0 = tables[kSetSub * kTableWords + threadIdx.x];
+  const uint64_t sub_word1 = tables[kSetSub * kTableWords + kCrcThreads + threadIdx.x];
+  __builtin_amdgcn_sched_barrier(0);
+  // this workgroup's input and span
+  const int32_t buf_idx = (int32_t)blockIdx.x / spans_per_buf;
+  const int32_t span_idx = (int32_t)blockIdx.x - buf_idx * spans_per_buf;
+  PoolSide ps = ps_in;
+  ps.plane_off = buf_idx * ps_in.plane_stride;
+  if (kMode != kStream) ps.blob += buf_idx * (buf_stride / 16);
+  data += buf_idx * (buf_stride / 16);
+  const char* tab = reinterpret_cast<const char*>(big);
+  // this lane's replica bytes and the permute selectors of crc_word4's four lookups: lookup k reads
+  // table (3 - k) ^ grp (selector bytes: 4 + half -> L.b0 / L.b1, 3 - t -> x.b(3 - t), 6 + region
+  // -> L.b2 / L.b3, 0x0c -> zero)
+  const uint32_t rr = (threadIdx.x % kCopies) << 3;
+  const uint32_t L = rr | (rr | 128u) << 8 | 1u << 24;
+  const uint32_t grp = (threadIdx.x >> 4) & 1;                     // lanes 16..31 of every 32
+  uint32_t sel[4];
 #pragma unroll
-    for (int c = 0; c < kCopies; ++c) t_slice[threadIdx.x * kCopies + c] = v;
-    stage<2>(t_sub, tables + kSetSub * kTableWords, kTableWords, kCrcThreads);
+  for (int k = 0; k < 4; ++k) {
+    const uint32_t t = (uint32_t)(3 - k) ^ grp;
+    sel[k] = 0x0c000000u | (6u + (t >> 1)) << 16 | (3u - t) << 8 | (4u + (t & 1));
   }
-  __syncthreads();
-  const uint64_t* tc = t_slice + (threadIdx.x % kCopies);
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  // this wave's 4 KiB staging area: 4 rows of 64 16-byte slots; slot (row j, lane l) holds the
-  // wave's bytes [1024 j + 16 l, +16) at position l ^ ((l >> 4) & 3), which keeps both the
-  // row-wise writes and the lane-piece reads free of bank conflicts
-  u32x4* stage_area = reinterpret_cast<u32x4*>(big + 4 * 256 * kCopies) + wave * 4 * 64;
+  // this wave's 1 KiB staging area: one row of 64 16-byte slots, used once per row of the wave's
+  // 4 KiB of a sub-chunk; slot l holds the row's bytes [16 l, +16) at position l ^ ((l >> 4) & 3),
+  // which keeps both the row writes and the lane-piece reads free of bank conflicts
+  u32x4* stage_area = reinterpret_cast<u32x4*>(small) + wave * 64;
+  const uint64_t* t_sub = small + kStageWords;                     // the sub-chunk advance (LDS)
   // this lane's 16-byte column within a sub-chunk, and the first sub-chunk's data offset
   const int32_t local = wave * 64 * kPiece + 16 * lane;
-  const int64_t span0 = (int64_t)blockIdx.x * span_subs * kSub - pad;
+  const int64_t span0 = (int64_t)span_idx * span_subs * kSub - pad;
   const int64_t base = span0 + local;
 
   // Pool side.  A sub-chunk's first tensor byte sb is tracked as the floor
@@ -272,20 +328,20 @@ __global__ __launch_bounds__(kCrcThreads) void crc64_span_kernel(const u32x4* __
   // plane, slot and byte; -1 in the padding), worked out once per piece
   // together with its table index, and the page entry pg loaded from the
   // table: offset = pb + pg * page_bytes (one 32 x 32 -> 64-bit multiply-add).
+  // (Every piece loads an entry - a padding piece row 0's - and the padding is marked in pb alone, so
+  // no branch surrounds a load and nothing waits for the entries until a piece's slot is needed.)
   auto lookup = [&](int64_t (&pb)[kLoads], int32_t (&pg)[kLoads], const RowPos& p) {
 #pragma unroll
     for (int j = 0; j < kLoads; ++j) {
-      uint32_t row, inrow;
-      pb[j] = -1;
-      pg[j] = -1;
-      if (row_of(p, j, &row, &inrow)) {
-        const uint32_t l = div32(row, ps.d_seq);
-        const uint32_t t = row - l * (uint32_t)ps.seq_len;
-        const uint32_t i = div32(t, ps.d_page);
-        pg[j] = ps.table[i];
-        pb[j] = (int64_t)(ps.first_layer + (int32_t)l) * ps.layer_bytes + ps.plane_off +
-                (int64_t)((uint64_t)(t - i * (uint32_t)ps.page_size) * (uint32_t)ps.row_bytes) + inrow;
-      }
+      uint32_t row = 0, inrow = 0;
+      const bool in_tensor = row_of(p, j, &row, &inrow);
+      const uint32_t l = div32(row, ps.d_seq);
+      const uint32_t t = row - l * (uint32_t)ps.seq_len;
+      const uint32_t i = div32(t, ps.d_page);                    // < ceil(seq_len / page_size)
+      pg[j] = ps.table[i];
+      pb[j] = in_tensor ? (int64_t)(ps.first_layer + (int32_t)l) * ps.layer_bytes + ps.plane_off +
+                              (int64_t)((uint64_t)(t - i * (uint32_t)ps.page_size) * (uint32_t)ps.row_bytes) + inrow
+                        : -1;
     }
   };
   // pool byte of a piece: -1 in the padding, -2 when its page entry is out of range
@@ -297,30 +353,42 @@ __global__ __launch_bounds__(kCrcThreads) void crc64_span_kernel(const u32x4* __
   const u32x4 zero = {0u, 0u, 0u, 0u};
   const u32x4* in = kMode == kScatter ? ps.blob : data;
 
-  u32x4 cur[kLoads], nxt[kLoads];
-  int32_t pg_a[kLoads] = {}, pg_b[kLoads] = {};
-  int64_t pb_a[kLoads] = {}, pb_b[kLoads] = {};
   // kStream / kScatter: contiguous input (the data, or the blob tensor)
-  auto load = [&](u32x4 (&v)[kLoads], int64_t sub) {
+  // Every load is issued (the front padding's at offset 0: no branch around a load, so the compiler
+  // counts outstanding loads exactly); bit j of *pad marks a piece of the padding, which the staging
+  // step replaces by zeros when the data is used.
+  // Buffer loads relative to the workgroup's first input byte, with a 32-bit lane offset (spans are
+  // shorter than 2 GiB).  In the front padding the offset is negative, i.e. above the resource's
+  // size as an unsigned number, and such a load returns zeros without touching memory: the padding's
+  // zero bytes come from the load itself.
+  const int64_t in_lo = span0 > 0 ? span0 : 0;
+  const __amdgpu_buffer_rsrc_t in_rsrc = __builtin_amdgcn_make_buffer_rsrc(
+      const_cast<char*>(reinterpret_cast<const char*>(in)) + in_lo, (short)0,
+      (int)(span0 + span_subs * kSub - in_lo), kBufferWord3);
+  const int32_t lane_off = local + (int32_t)(span0 - in_lo);
+  auto load = [&](u32x4 (&v)[kLoads], int64_t sub, uint32_t* pad) {
+    *pad = 0;
 #pragma unroll
     for (int j = 0; j < kLoads; ++j) {
-      const int64_t off = base + (sub << kSubLog2) + 1024 * j;
-      v[j] = off >= 0 ? __builtin_nontemporal_load(in + off / 16) : zero;   // off < head
+      const int32_t off = lane_off + ((int32_t)sub << kSubLog2) + 1024 * j;
+      v[j] = __builtin_amdgcn_raw_buffer_load_b128(in_rsrc, (uint32_t)off, 0, kBufferNt);
     }
   };
   // kGather: pool pieces (page entries pg loaded an iteration earlier); bad pages read the blob.
   // Bit j of *moved: piece j came from the pool (so the blob store writes it).
   auto gather = [&](u32x4 (&v)[kLoads], int64_t sub, const int64_t (&pb)[kLoads], const int32_t (&pg)[kLoads],
-                    uint32_t* moved) {
+                    uint32_t* moved, uint32_t* pad) {
     *moved = 0;
+    *pad = 0;
 #pragma unroll
     for (int j = 0; j < kLoads; ++j) {
       const int64_t po = slot_of(pb[j], pg[j]);
       const int64_t off = base + (sub << kSubLog2) + 1024 * j;
-      v[j] = po >= 0    ? __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(ps.pool + po))
-             : po == -2 ? ps.blob[off / 16]
-                        : zero;
+      // one load per piece whatever its source (the padding's from the blob's start)
+      const u32x4* src = po >= 0 ? reinterpret_cast<const u32x4*>(ps.pool + po) : ps.blob + (po == -2 ? off / 16 : 0);
+      v[j] = __builtin_nontemporal_load(src);
       *moved |= (po >= 0 ? 1u : 0u) << j;
+      *pad |= (po == -1 ? 1u : 0u) << j;
     }
   };
   auto put_blob = [&](const u32x4 (&v)[kLoads], int64_t sub, uint32_t moved) {
@@ -335,71 +403,120 @@ __global__ __launch_bounds__(kCrcThreads) void crc64_span_kernel(const u32x4* __
       if (po >= 0) __builtin_nontemporal_store(v[j], reinterpret_cast<u32x4*>(ps.pool + po));
     }
   };
-  uint32_t moved_cur = 0, moved_nxt = 0;
-
-  RowPos pos = pos0;   // this sub-chunk's row position (pool modes)
   const int wr = lane ^ ((lane >> 4) & 3);                        // write slot of this lane in each row
   const int rrow = lane >> 4, rcol = 4 * (lane & 15);             // this lane's piece: row, first column
   uint64_t fold = 0;
+  // Per-sub-chunk state in kDepth sets used in turn, so a step never copies a later sub-chunk's
+  // registers (a copy would wait for its loads): the pieces, the padding and moved masks, and (pool
+  // modes) the page-independent offsets and page entries.  The streaming mode keeps two sub-chunks'
+  // loads in flight while it folds a third; the pool modes, which need more registers per piece, one.
+  constexpr int kDepth = kMode == kStream ? 3 : 2;
+  u32x4 buf[kDepth][kLoads];
+  int64_t pb[kDepth][kLoads] = {};
+  int32_t pg[kDepth][kLoads] = {};
+  uint32_t zp[kDepth] = {}, mv[kDepth] = {};
+  RowPos pos = pos0;   // row position of the sub-chunk the next step folds (pool modes)
   if (kMode == kGather) {
-    lookup(pb_a, pg_a, pos);
-    gather(cur, 0, pb_a, pg_a, &moved_cur);
-    if (span_subs > 1) lookup(pb_b, pg_b, advance(pos));
+    lookup(pb[0], pg[0], pos);
+    gather(buf[0], 0, pb[0], pg[0], &mv[0], &zp[0]);
+    if (span_subs > 1) lookup(pb[1], pg[1], advance(pos));
   } else {
-    load(cur, 0);
-    if (kMode == kScatter) lookup(pb_a, pg_a, pos);
+    // in set order, as the loop issues them (kept apart so the scheduler cannot interleave the sets:
+    // the loop's waits count loads in issue order, and a set issued later than the loop assumes would
+    // make every iteration wait for it)
+#pragma unroll
+    for (int k = 0; k + 1 < kDepth; ++k) {
+      load(buf[k], k < span_subs ? k : span_subs - 1, &zp[k]);
+      __builtin_amdgcn_sched_barrier(0);
+    }
+    if (kMode == kScatter) lookup(pb[0], pg[0], pos);
   }
-  for (int64_t sub = 0; sub < span_subs; ++sub) {
+  {
+    // thread e writes entry b = e mod 256 of slicing table t = e / 256 into every replica (layout at
+    // crc_word4), replica (i + lane) % kCopies at step i, so a wave's writes spread over the banks
+    static_assert(kCopies == 16, "16 replicas of 8 bytes fill a 128-byte half row");
+    const int t = threadIdx.x >> 8, b = threadIdx.x & 255;
+    char* row = reinterpret_cast<char*>(big) + (t >> 1) * 65536 + b * 256 + (t & 1) * 128;
+#pragma unroll
+    for (int i = 0; i < kCopies; ++i)
+      *reinterpret_cast<uint64_t*>(row + ((i + threadIdx.x) % kCopies) * 8) = slice_word;
+    small[kStageWords + threadIdx.x] = sub_word0;
+    small[kStageWords + kCrcThreads + threadIdx.x] = sub_word1;
+  }
+  __syncthreads();
+  // One step: fold sub-chunk `sub` (set c) while the loads of sub-chunk sub + kDepth - 1 go into set n
+  // (the set the previous step folded).  Every step of a loop iteration runs, also past the span's
+  // end: such a step's loads reread the span's last sub-chunk (so no branch surrounds a load and the
+  // compiler's count of outstanding loads is exact on every path) and the rest of it is skipped.
+  auto step = [&](int64_t sub, int c, int n) {
+    const bool live = sub < span_subs;
+    // the advance of the running register by one sub-chunk (LDS lookups; they return while this
+    // sub-chunk's bytes are folded)
+    const uint64_t adv = lookup8(fold, t_sub);
+    const int64_t ahead = sub + kDepth - 1;
     if (kMode == kGather) {
-      // pg_a: this sub-chunk's entries, pg_b: the next one's (loaded a sub-chunk ago)
-      const RowPos p1 = advance(pos);
-      if (sub + 1 < span_subs) gather(nxt, sub + 1, pb_b, pg_b, &moved_nxt);
-      put_blob(cur, sub, moved_cur);
-      moved_cur = moved_nxt;
-      if (sub + 2 < span_subs) lookup(pb_b, pg_b, advance(p1));
-      pos = p1;
+      // entries of sub + 1 were looked up a step ago into set n; set c's entries are free once sub's
+      // pieces are in, and take those of sub + 2
+      if (live) {
+        const RowPos p1 = advance(pos);
+        if (sub + 1 < span_subs) gather(buf[n], sub + 1, pb[n], pg[n], &mv[n], &zp[n]);
+        put_blob(buf[c], sub, mv[c]);
+        if (sub + 2 < span_subs) lookup(pb[c], pg[c], advance(p1));
+        pos = p1;
+      }
     } else {
-      if (sub + 1 < span_subs) {
-        load(nxt, sub + 1);
-        if (kMode == kScatter) lookup(pb_b, pg_b, advance(pos));
-      }
-      if (kMode == kScatter) {
-        put_pool(cur, pb_a, pg_a);
-#pragma unroll
-        for (int j = 0; j < kLoads; ++j) {
-          pg_a[j] = pg_b[j];
-          pb_a[j] = pb_b[j];
-        }
-        pos = advance(pos);
+      load(buf[n], ahead < span_subs ? ahead : span_subs - 1, &zp[n]);
+      if (kMode == kScatter && live) {
+        // the next sub-chunk's entries (on a span's last step past the tensor's end: in-range table
+        // indices whose entries are never used), then this sub-chunk's pieces to their pool slots
+        const RowPos p1 = advance(pos);
+        lookup(pb[n], pg[n], p1);
+        put_pool(buf[c], pb[c], pg[c]);
+        pos = p1;
       }
     }
-#pragma unroll
-    for (int j = 0; j < kLoads; ++j) stage_area[j * 64 + wr] = cur[j];
-    __builtin_amdgcn_wave_barrier();
+    if (!live) return;
     u32x4 piece[kLoads];
+    // (kGather) pieces of the front padding, only in a sub-chunk that starts before the data (the same
+    // for the whole workgroup), are staged as zeros
+    const bool front = kMode == kGather && span0 + (sub << kSubLog2) < 0;
 #pragma unroll
-    for (int m = 0; m < kLoads; ++m) {
-      const int l = rcol + m;
-      piece[m] = stage_area[rrow * 64 + (l ^ ((l >> 4) & 3))];
+    for (int h = 0; h < kLoads; ++h) {   // row h: lanes 16h .. 16h + 15 take their pieces
+      if (front)
+        stage_area[wr] = (zp[c] >> h & 1) ? zero : buf[c][h];
+      else
+        stage_area[wr] = buf[c][h];
+      __builtin_amdgcn_wave_barrier();
+      if (rrow == h) {
+#pragma unroll
+        for (int m = 0; m < kLoads; ++m) {
+          const int l = rcol + m;
+          piece[m] = stage_area[l ^ ((l >> 4) & 3)];
+        }
+      }
+      __builtin_amdgcn_wave_barrier();   // reads done before the next writes
     }
-    __builtin_amdgcn_wave_barrier();   // reads done before the next sub-chunk's writes
-    uint64_t reg = 0;
+    uint32_t lo = 0, hi = 0;
 #pragma unroll
     for (int j = 0; j < kLoads; ++j) {
-      reg = crc_word4(reg, piece[j].x, tc);
-      reg = crc_word4(reg, piece[j].y, tc);
-      reg = crc_word4(reg, piece[j].z, tc);
-      reg = crc_word4(reg, piece[j].w, tc);
+      crc_word4(lo, hi, piece[j].x, tab, L, sel);
+      crc_word4(lo, hi, piece[j].y, tab, L, sel);
+      crc_word4(lo, hi, piece[j].z, tab, L, sel);
+      crc_word4(lo, hi, piece[j].w, tab, L, sel);
     }
-    fold = lookup8(fold, t_sub) ^ reg;
+    fold = adv ^ ((uint64_t)hi << 32 | lo);
+  };
+  for (int64_t sub = 0; sub < span_subs; sub += kDepth) {
 #pragma unroll
-    for (int j = 0; j < kLoads; ++j) cur[j] = nxt[j];
+    for (int k = 0; k < kDepth; ++k) step(sub + k, k, (k + kDepth - 1) % kDepth);
   }
-  acc[threadIdx.x] = fold;
-  __syncthreads();   // every lane is done with the slicing tables: their LDS holds the join levels now
+  __syncthreads();   // every lane is done with the slicing tables and the staging area
+  uint64_t* acc = small;                                         // join registers
+  uint64_t* lvl8 = small + kCrcThreads;                          // level 8 (16 KiB)
   uint64_t* lvl_tab = big;                                       // levels 0..7 (8 x 16 KiB)
+  acc[threadIdx.x] = fold;
   stage<16>(lvl_tab, tables + kSetLane * kTableWords, 8 * kTableWords, kCrcThreads);
-  stage<2>(t_sub, tables + (kSetLane + 8) * kTableWords, kTableWords, kCrcThreads);   // level 8
+  stage<2>(lvl8, tables + (kSetLane + 8) * kTableWords, kTableWords, kCrcThreads);
   __syncthreads();
   // join lanes t and t + s: the later group holds s lanes x kPiece bytes of every sub-chunk
   for (int lvl = 0; lvl < kLaneLevels; ++lvl) {
@@ -407,23 +524,28 @@ __global__ __launch_bounds__(kCrcThreads) void crc64_span_kernel(const u32x4* __
     const int t = threadIdx.x;
     if ((t & (2 * s - 1)) == 0) {
       const uint64_t* tab = lvl < 8 ? lvl_tab + lvl * kTableWords
-                                    : lvl == 8 ? t_sub : tables + (kSetLane + lvl) * kTableWords;
+                                    : lvl == 8 ? lvl8 : tables + (kSetLane + lvl) * kTableWords;
       acc[t] = lookup8(acc[t], tab) ^ acc[t + s];
     }
     __syncthreads();
   }
-  if (threadIdx.x == 0) partial[blockIdx.x] = acc[0];
+  if (threadIdx.x == 0) partial[buf_idx * kMaxSpans + span_idx] = acc[0];
 }
 
-// Kernel 2 (one workgroup of kMaxSpans lanes): lane t holds span register
-// t - lead (the first `lead` lanes hold zero spans, i.e. more leading zero
-// bytes), a tree of table multiplies joins them, then the tail bytes are
-// appended and the CRC finished: out = ~(preset_shift + R).
+// Kernel 2 (one workgroup of kMaxSpans lanes per input i: its span registers
+// at partial + i * kMaxSpans, its tail at tail + i * buf_stride, its CRC to
+// out[i]): lane t holds span register t - lead (the first `lead` lanes hold
+// zero spans, i.e. more leading zero bytes), a tree of table multiplies joins
+// them, then the tail bytes are appended and the CRC finished:
+// out = ~(preset_shift + R).
 __global__ __launch_bounds__(kMaxSpans) void crc64_finish_kernel(const uint64_t* __restrict__ tables,
                                                                  const uint64_t* __restrict__ partial, int spans,
                                                                  const unsigned char* __restrict__ tail,
-                                                                 int tail_len, uint64_t preset_shift,
-                                                                 uint64_t* __restrict__ out) {
+                                                                 int64_t buf_stride, int tail_len,
+                                                                 uint64_t preset_shift, uint64_t* __restrict__ out) {
+  partial += blockIdx.x * kMaxSpans;
+  tail += blockIdx.x * buf_stride;
+  out += blockIdx.x;
   __shared__ uint64_t lvl_tab[kSpanLevels * kTableWords];       // 128 KiB
   __shared__ uint64_t t0[256];
   __shared__ uint64_t acc[kMaxSpans];
@@ -448,17 +570,20 @@ __global__ __launch_bounds__(kMaxSpans) void crc64_finish_kernel(const uint64_t*
 // Workspace words one CRC needs: tables + span registers.
 int64_t crc_words(int64_t) { return kWsTables + kMaxSpans; }
 
-// Span geometry of a CRC over n bytes: the 16-byte-aligned head is cut into
-// `spans` spans of `span_subs` sub-chunks each (spans <= kMaxSpans).
+// Span geometry of CRCs over `inputs` inputs of n bytes each, launched
+// together: each 16-byte-aligned head is cut into `spans` spans of
+// `span_subs` sub-chunks (spans <= kMaxSpans / inputs, so all inputs' spans
+// fill one launch of at most kMaxSpans workgroups).
 struct Spans {
   int64_t head, span_subs, span, spans;
 };
 
-Spans span_geometry(int64_t n) {
+Spans span_geometry(int64_t n, int inputs = 1) {
   Spans g;
+  const int64_t max_spans = kMaxSpans / inputs;
   g.head = n - n % 16;
   const int64_t subs = (g.head + kSub - 1) / kSub;
-  g.span_subs = subs > 0 ? (subs + kMaxSpans - 1) / kMaxSpans : 1;
+  g.span_subs = subs > 0 ? (subs + max_spans - 1) / max_spans : 1;
   g.span = g.span_subs * kSub;
   g.spans = (g.head + g.span - 1) / g.span;
   return g;
@@ -477,21 +602,23 @@ topkv_status_t crc64_tables(uint64_t* ws, int64_t span, hipStream_t stream) {
   return hipGetLastError() == hipSuccess ? TOPKV_OK : TOPKV_ERR_LAUNCH;
 }
 
-// Queue the CRC-64/XZ of data[0, n) into out (device).  data 16-byte aligned;
-// `tables` were queued by crc64_tables for this n's span; partial has room
-// for kMaxSpans words.
-topkv_status_t crc64_launch(const unsigned char* data, int64_t n, const uint64_t* tables, uint64_t* partial,
-                            uint64_t* out, hipStream_t stream) {
+// Queue the CRC-64/XZ of each of `inputs` inputs of n bytes, input i at
+// data + i * stride, into out[i] (device).  data and stride 16-byte aligned;
+// `tables` were queued by crc64_tables for span_geometry(n, inputs).span;
+// partial has room for inputs * kMaxSpans words.
+topkv_status_t crc64_launch(const unsigned char* data, int64_t n, int inputs, int64_t stride, const uint64_t* tables,
+                            uint64_t* partial, uint64_t* out, hipStream_t stream) {
   const ShiftConsts& sc = shift_consts();
-  const Spans g = span_geometry(n);
+  const Spans g = span_geometry(n, inputs);
+  if (g.span_subs > kMaxSpanSubs) return TOPKV_ERR_UNSUPPORTED;   // spans of 2 GiB and more
   if (g.spans > 0) {
-    hipLaunchKernelGGL(crc64_span_kernel<kStream>, dim3((unsigned)g.spans), dim3(kCrcThreads), 0, stream,
-                       reinterpret_cast<const u32x4*>(data), g.spans * g.span - g.head, g.span_subs, tables, partial,
-                       PoolSide{});
+    hipLaunchKernelGGL(crc64_span_kernel<kStream>, dim3((unsigned)(g.spans * inputs)), dim3(kCrcThreads), 0, stream,
+                       reinterpret_cast<const u32x4*>(data), stride, g.spans * g.span - g.head, g.span_subs,
+                       (int32_t)g.spans, tables, partial, PoolSide{});
     if (hipGetLastError() != hipSuccess) return TOPKV_ERR_LAUNCH;
   }
-  hipLaunchKernelGGL(crc64_finish_kernel, dim3(1), dim3(kMaxSpans), 0, stream, tables, partial, (int)g.spans,
-                     data + g.head, (int)(n - g.head), mulmod(x8n(sc, (uint64_t)n), ~0ull), out);
+  hipLaunchKernelGGL(crc64_finish_kernel, dim3((unsigned)inputs), dim3(kMaxSpans), 0, stream, tables, partial,
+                     (int)g.spans, data + g.head, stride, (int)(n - g.head), mulmod(x8n(sc, (uint64_t)n), ~0ull), out);
   return hipGetLastError() == hipSuccess ? TOPKV_OK : TOPKV_ERR_LAUNCH;
 }
 
@@ -594,16 +721,21 @@ topkv_status_t blob_crcs(const unsigned char* blob, const Blob& b, uint64_t* ws,
   uint64_t* tables = ws + 2;
   uint64_t* partial_k = tables + kWsTables;
   uint64_t* partial_v = partial_k + crc_words(b.k_bytes) - kWsTables;
+  if (b.v_bytes == b.k_bytes) {   // both tensors in one launch of each kernel
+    const topkv_status_t st = crc64_tables(tables, span_geometry(b.k_bytes, 2).span, stream);
+    if (st != TOPKV_OK) return st;
+    return crc64_launch(blob + kHeaderBytes, b.k_bytes, 2, b.k_bytes, tables, partial_k, ws, stream);
+  }
   const int64_t span_k = span_geometry(b.k_bytes).span, span_v = span_geometry(b.v_bytes).span;
   topkv_status_t st = crc64_tables(tables, span_k, stream);
   if (st != TOPKV_OK) return st;
-  st = crc64_launch(blob + kHeaderBytes, b.k_bytes, tables, partial_k, ws, stream);
+  st = crc64_launch(blob + kHeaderBytes, b.k_bytes, 1, 0, tables, partial_k, ws, stream);
   if (st != TOPKV_OK) return st;
   if (span_v != span_k) {   // stream order: K's kernels are done with the tables before they change
     st = crc64_tables(tables, span_v, stream);
     if (st != TOPKV_OK) return st;
   }
-  return crc64_launch(blob + kHeaderBytes + b.k_bytes, b.v_bytes, tables, partial_v, ws + 1, stream);
+  return crc64_launch(blob + kHeaderBytes + b.k_bytes, b.v_bytes, 1, 0, tables, partial_v, ws + 1, stream);
 }
 
 int64_t blob_ws_bytes(const Blob& b) {
@@ -616,7 +748,8 @@ bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15) == 
 // and the blob themselves (32-bit row and token arithmetic, 16-byte pieces).
 bool fused_fits(const topkv_pool_t* pool, int32_t seq_len, const Blob& b) {
   return seq_len > 0 && (int64_t)pool->num_layers * seq_len < INT32_MAX && b.row < INT32_MAX - 2 * kSub &&
-         (int64_t)pool->planes * pool->page_size * b.row <= UINT32_MAX && aligned16(pool->base);
+         (int64_t)pool->planes * pool->page_size * b.row <= UINT32_MAX && aligned16(pool->base) &&
+         span_geometry(b.k_bytes, pool->planes).span_subs <= kMaxSpanSubs;
 }
 
 // Both checksums of the blob body into ws[0..1] while the K and V tensors of
@@ -643,23 +776,23 @@ topkv_status_t fused_blob_crcs(const topkv_pool_t* pool, const int32_t* table, i
   ps.d_row = make_div32((uint32_t)b.row);
   ps.d_seq = make_div32((uint32_t)seq_len);
   ps.d_page = make_div32((uint32_t)pool->page_size);
-  const Spans g = span_geometry(b.k_bytes);                 // K and V tensors have the same size
+  // every plane's tensor (K, V) in one launch of each kernel; the tensors have the same size
+  const Spans g = span_geometry(b.k_bytes, pool->planes);
   topkv_status_t st = crc64_tables(tables, g.span, stream);
   if (st != TOPKV_OK) return st;
-  for (int c = 0; c < pool->planes; ++c) {
-    ps.plane_off = (int64_t)c * pool->page_size * b.row;
-    ps.blob = reinterpret_cast<u32x4*>(blob + kHeaderBytes + c * b.k_bytes);
-    hipLaunchKernelGGL(crc64_span_kernel<kMode>, dim3((unsigned)g.spans), dim3(kCrcThreads), 0, stream, ps.blob,
-                       g.spans * g.span - g.head, g.span_subs, tables, partial[c], ps);
-    if (hipGetLastError() != hipSuccess) return TOPKV_ERR_LAUNCH;
-    hipLaunchKernelGGL(crc64_finish_kernel, dim3(1), dim3(kMaxSpans), 0, stream, tables, partial[c], (int)g.spans,
-                       reinterpret_cast<const unsigned char*>(ps.blob) + g.head, 0,
-                       mulmod(x8n(sc, (uint64_t)b.k_bytes), ~0ull), ws + c);
-    if (hipGetLastError() != hipSuccess) return TOPKV_ERR_LAUNCH;
-  }
+  ps.plane_stride = (int64_t)pool->page_size * b.row;
+  ps.blob = reinterpret_cast<u32x4*>(blob + kHeaderBytes);
+  hipLaunchKernelGGL(crc64_span_kernel<kMode>, dim3((unsigned)(g.spans * pool->planes)), dim3(kCrcThreads), 0, stream,
+                     ps.blob, b.k_bytes, g.spans * g.span - g.head, g.span_subs, (int32_t)g.spans, tables, partial[0],
+                     ps);
+  if (hipGetLastError() != hipSuccess) return TOPKV_ERR_LAUNCH;
+  hipLaunchKernelGGL(crc64_finish_kernel, dim3((unsigned)pool->planes), dim3(kMaxSpans), 0, stream, tables,
+                     partial[0], (int)g.spans, reinterpret_cast<const unsigned char*>(ps.blob) + g.head, b.k_bytes, 0,
+                     mulmod(x8n(sc, (uint64_t)b.k_bytes), ~0ull), ws);
+  if (hipGetLastError() != hipSuccess) return TOPKV_ERR_LAUNCH;
   if (pool->planes == 1) {     // an MLA cache has no V tensor: its checksum is that of no bytes
     hipLaunchKernelGGL(crc64_finish_kernel, dim3(1), dim3(kMaxSpans), 0, stream, tables, partial[1], 0,
-                       blob + kHeaderBytes + b.k_bytes, 0, mulmod(x8n(sc, 0), ~0ull), ws + 1);
+                       blob + kHeaderBytes + b.k_bytes, (int64_t)0, 0, mulmod(x8n(sc, 0), ~0ull), ws + 1);
     if (hipGetLastError() != hipSuccess) return TOPKV_ERR_LAUNCH;
   }
   return TOPKV_OK;
@@ -742,7 +875,7 @@ topkv_status_t topkv_crc64_noalloc(const void* data, int64_t nbytes, uint64_t* c
   // earlier call is read
   const topkv_status_t t = crc64_tables(ws, span_geometry(nbytes).span, stream);
   if (t != TOPKV_OK) return t;
-  return crc64_launch(static_cast<const unsigned char*>(data), nbytes, ws, ws + kWsTables, crc_out, stream);
+  return crc64_launch(static_cast<const unsigned char*>(data), nbytes, 1, 0, ws, ws + kWsTables, crc_out, stream);
 }
 
 int64_t topkv_crc64_workspace_bytes(int64_t nbytes) {
@@ -758,7 +891,7 @@ topkv_status_t topkv_crc64(const void* data, int64_t nbytes, void* workspace, in
   uint64_t* ws = static_cast<uint64_t*>(workspace);
   const topkv_status_t st = crc64_tables(ws, span_geometry(nbytes).span, stream);
   if (st != TOPKV_OK) return st;
-  return crc64_launch(static_cast<const unsigned char*>(data), nbytes, ws, ws + kWsTables, crc_out, stream);
+  return crc64_launch(static_cast<const unsigned char*>(data), nbytes, 1, 0, ws, ws + kWsTables, crc_out, stream);
 }
 
 int64_t topkv_kvcache1_bytes(const topkv_pool_t* geometry, int32_t seq_len) {

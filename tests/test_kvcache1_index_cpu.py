@@ -1,6 +1,7 @@
 """CPU model of the one-pass KVCACHE1 span kernels' addressing (the kGather /
 kScatter source of crc64_span_kernel): every 16-byte piece of a tensor,
-visited in the kernel's order (span, sub-chunk, wave, lane, row j), must land
+visited in the kernel's order (plane, span, sub-chunk, wave, lane, row j; the
+planes' tensors share one launch, kMaxSpans / planes spans each), must land
 on the pool byte the KVCACHE1 definition gives -- tensor byte o is layer
 o // (s * row), token (o // row) % s, byte o % row of that token's row in its
 page -- exactly once, inside the pool, with the front padding skipped.  The
@@ -30,10 +31,11 @@ def div32(n, f):
     return (((n * m) >> 32) + n) >> s
 
 
-def span_geometry(n):
+def span_geometry(n, inputs=1):
+    max_spans = K_MAX_SPANS // inputs
     head = n - n % 16
     subs = (head + K_SUB - 1) // K_SUB
-    span_subs = (subs + K_MAX_SPANS - 1) // K_MAX_SPANS if subs > 0 else 1
+    span_subs = (subs + max_spans - 1) // max_spans if subs > 0 else 1
     span = span_subs * K_SUB
     return head, span_subs, span, (head + span - 1) // span
 
@@ -57,7 +59,8 @@ def _check(L, NP, C, P, H, D, eb, s, seed=0):
     layer_bytes = NP * page_bytes
     table = rng.permutation(NP)[:-(-s // P)]
     tensor = L * s * row
-    head, span_subs, span, spans = span_geometry(tensor)
+    head, span_subs, span, spans = span_geometry(tensor, C)
+    assert spans * C <= K_MAX_SPANS
     pad = spans * span - head
     d_row, d_seq, d_page = make_div32(row), make_div32(s), make_div32(P)
     step_q, step_r = K_SUB // row, K_SUB % row
@@ -69,13 +72,21 @@ def _check(L, NP, C, P, H, D, eb, s, seed=0):
             q = span0 // row                                     # floor quotient (span0 < 0 in the padding)
             r0, in0 = q, span0 - q * row
             assert 0 <= in0 < row
-            for sub in range(span_subs):
+            # every piece's table entry is loaded, a padding piece's as row 0's, and the receiver also
+            # looks up the sub-chunk after a span's last one (past the tensor on the last span):
+            # every such index lies within the request's table
+            for sub in range(span_subs + 1):
                 for j in range(K_LOADS):
                     for loc in local.tolist():
                         off = span0 + (sub << K_SUB_LOG2) + loc + 1024 * j
                         x = in0 + loc + 1024 * j
                         qq = div32(x, d_row)
                         r = r0 + qq
+                        rr = max(r, 0)
+                        i_any = div32(rr - div32(rr, d_seq) * s, d_page)
+                        assert 0 <= i_any < len(table)
+                        if sub == span_subs:
+                            continue
                         if r < 0:
                             assert off < 0
                             continue
