@@ -416,8 +416,8 @@ int64_t topkv_crc64_workspace_bytes(int64_t nbytes);
 /* topkv_crc64 for callers that cannot allocate (code under HIP graph
  * capture, tight serving loops, harnesses that forbid hipMalloc): no
  * workspace argument, and nothing is allocated or freed.  The workspace is a
- * file-scope device array of TOPKV_CRC64_NOALLOC_SCRATCH_BYTES bytes (the
- * tables plus at most 256 span registers), one copy per GPU the library runs
+ * file-scope device array of TOPKV_CRC64_NOALLOC_SCRATCH_BYTES bytes (at most
+ * 256 span registers), one copy per GPU the library runs
  * on, held until the process ends; the first call on a device looks its
  * address up (hipGetSymbolAddress, device current), so make that call before
  * any capture on that device.  Every length fits that
@@ -427,7 +427,7 @@ int64_t topkv_crc64_workspace_bytes(int64_t nbytes);
  * Calls on one GPU share its array: calls whose kernels overlap in time
  * (other streams, other threads) race and may write wrong checksums; calls
  * ordered on one stream are safe (each rewrites every word it reads). */
-#define TOPKV_CRC64_NOALLOC_SCRATCH_BYTES 329728
+#define TOPKV_CRC64_NOALLOC_SCRATCH_BYTES 2048
 topkv_status_t topkv_crc64_noalloc(const void* data, int64_t nbytes, uint64_t* crc_out,
                                    hipStream_t stream);
 

@@ -17,9 +17,9 @@
 // ~(~0 * x^(8N) + R(data)).  Multiplying a register by a fixed power of x is
 // linear, so it is the XOR of one lookup per register byte in a table of
 // that constant.  Work split:
-//   kernel 0: the tables, into the caller's workspace: slicing tables, the
-//     constant that advances a register by one sub-chunk, the join levels of
-//     the lanes inside a span and of the spans;
+//   tables: the slicing tables, the constant that advances a register by
+//     one sub-chunk and the join levels of the lanes inside a span do not
+//     depend on the data; the compiler computes them (kConstTables);
 //   kernel 1: the data, front-padded with zero bytes (free, by the property
 //     above), is cut into at most 256 equal spans of whole 64 KiB
 //     sub-chunks, one 1024-lane workgroup per span (several inputs of one
@@ -32,9 +32,13 @@
 //     lanes run them through slicing-by-4 tables held in LDS in 16 replicas
 //     arranged so that the 32 lanes an LDS cycle serves never share a bank
 //     (crc_word4), and advance their running register by one sub-chunk per
-//     step; a tree of table multiplies joins the lanes at the end of the span;
-//   kernel 2: one workgroup per input joins its span registers the same way,
-//     appends the sub-16-byte tail and applies the preset and complement.
+//     step; a tree of table multiplies joins the lanes at the end of the
+//     span, and the span's register is multiplied into its place in the
+//     input (a GF(2) product per bit of its distance to the end, done across
+//     a wave);
+//   kernel 2: one workgroup XORs each input's placed span registers,
+//     appends the sub-16-byte tail, applies the preset and complement, and
+//     writes (seal) or checks (verify) a blob's header.
 // Shift constants x^(8n) mod P are computed on the host.
 //
 // One-pass serialization: kernel 1 also runs with the pool as its source
@@ -73,23 +77,17 @@ constexpr int kTableWords = 8 * 256;                            // one set of 8 
 constexpr int kCopies = 16;                                     // LDS replicas of the slicing tables
 constexpr int kWaves = kCrcThreads / 64;
 constexpr int kStageWords = kWaves * 64 * 16 / 8;               // per-wave staging of one 1 KiB row
-// workspace table sets: 0 slicing, 1 sub-chunk advance, 2.. lane levels, then span levels
-constexpr int kSetSlice = 0, kSetSub = 1, kSetLane = 2, kSetSpan = kSetLane + kLaneLevels;
-constexpr int kSets = kSetSpan + kSpanLevels;
-constexpr int64_t kWsTables = (int64_t)kSets * kTableWords;     // then the span registers
+// constant table sets: 0 slicing, 1 sub-chunk advance, 2.. lane-join levels
+constexpr int kSetSlice = 0, kSetSub = 1, kSetLane = 2, kConstSets = kSetLane + kLaneLevels;
 
 struct ShiftConsts {
   uint64_t x8pow2[64];    // x^(8 * 2^k) mod P, reflected
 };
 
-struct TableConsts {
-  uint64_t shift[kSets];  // the constant of each multiply set (unused for the slicing set)
-};
-
-__host__ __device__ inline uint64_t mul_x(uint64_t w) { return (w >> 1) ^ ((w & 1) ? kPolyReflected : 0); }
+__host__ __device__ constexpr uint64_t mul_x(uint64_t w) { return (w >> 1) ^ ((w & 1) ? kPolyReflected : 0); }
 
 // a * b mod P in the reflected representation (bit 63 of a is its x^0 term).
-__host__ __device__ inline uint64_t mulmod(uint64_t a, uint64_t b) {
+__host__ __device__ constexpr uint64_t mulmod(uint64_t a, uint64_t b) {
   uint64_t prod = 0;
   for (int i = 0; i < 64 && a; ++i) {
     if (a >> 63) prod ^= b;
@@ -119,21 +117,59 @@ uint64_t x8n(const ShiftConsts& c, uint64_t n) {
   return r;
 }
 
-// Kernel 0: table set g / 2048, table k, byte b:
-//   slicing set: byte b followed by k zero bytes;
-//   multiply sets: (b << 8k) times the set's constant.
-__global__ __launch_bounds__(256) void crc64_tables_kernel(uint64_t* __restrict__ tables, TableConsts tc) {
-  const int g = blockIdx.x * 256 + threadIdx.x;              // grid covers exactly kSets * 2048 entries
-  const int set = g / kTableWords, k = (g / 256) % 8, b = g % 256;
-  uint64_t v;
-  if (set == kSetSlice) {
-    v = (uint64_t)b;
-    for (int i = 0; i < 8 * (k + 1); ++i) v = mul_x(v);
-  } else {
-    v = mulmod((uint64_t)b << (8 * k), tc.shift[set]);
+// A set of 8 byte tables is linear in the byte: entry (k, b) is the XOR of
+// m[8k + i] over the set bits i of b, for the set's basis m[0..63].  Slicing
+// set: entry (k, b) is byte b followed by k zero bytes, b * x^(8(k + 1)), so
+// m[8k + i] = x^(63 - i) * x^(8k + 8).  Multiply set of constant c: entry
+// (k, b) is (b << 8k) * c, so m[j] = x^(63 - j) * c, i.e. m[63] = c and
+// m[j - 1] = x * m[j].  Each entry is built from the one with its lowest set
+// bit cleared.
+__host__ __device__ constexpr void fill_set(uint64_t* set, const uint64_t (&m)[64]) {
+  for (int k = 0; k < 8; ++k) {
+    set[k * 256] = 0;
+    for (int b = 1; b < 256; ++b) {
+      int low = 0;
+      while (!((b >> low) & 1)) ++low;
+      set[k * 256 + b] = set[k * 256 + (b & (b - 1))] ^ m[8 * k + low];
+    }
   }
-  tables[g] = v;
 }
+
+__host__ __device__ constexpr void multiply_basis(uint64_t (&m)[64], uint64_t c) {
+  m[63] = c;
+  for (int j = 63; j > 0; --j) m[j - 1] = mul_x(m[j]);
+}
+
+// The span-independent table sets, computed by the compiler: slicing, the
+// advance by one sub-chunk (x^(8 * 64 Ki)), and the lane-join levels
+// (x^(8 * kPiece * 2^l)).
+struct ConstTables {
+  uint64_t w[kConstSets * kTableWords];
+};
+
+constexpr ConstTables make_const_tables() {
+  ConstTables t{};
+  uint64_t p[128] = {};                                      // p[n] = x^n
+  p[0] = 1ull << 63;
+  for (int n = 1; n < 128; ++n) p[n] = mul_x(p[n - 1]);
+  uint64_t m[64] = {};
+  for (int k = 0; k < 8; ++k)
+    for (int i = 0; i < 8; ++i) m[8 * k + i] = p[71 + 8 * k - i];
+  fill_set(t.w + kSetSlice * kTableWords, m);
+  uint64_t x8p[kSubLog2 + 1] = {};                           // x8p[k] = x^(8 * 2^k)
+  x8p[0] = p[8];
+  for (int k = 1; k <= kSubLog2; ++k) x8p[k] = mulmod(x8p[k - 1], x8p[k - 1]);
+  multiply_basis(m, x8p[kSubLog2]);
+  fill_set(t.w + kSetSub * kTableWords, m);
+  static_assert(kPiece == 64 && 6 + kLaneLevels - 1 <= kSubLog2, "lane levels are x^(8 * 2^(6 + l))");
+  for (int l = 0; l < kLaneLevels; ++l) {
+    multiply_basis(m, x8p[6 + l]);
+    fill_set(t.w + (kSetLane + l) * kTableWords, m);
+  }
+  return t;
+}
+
+__device__ const ConstTables kConstTables = make_const_tables();
 
 __device__ inline uint64_t lookup8(uint64_t v, const uint64_t* t) {   // t: 8 x 256 words
   return t[0 * 256 + (v & 0xff)] ^ t[1 * 256 + ((v >> 8) & 0xff)] ^ t[2 * 256 + ((v >> 16) & 0xff)] ^
@@ -232,19 +268,33 @@ struct PoolSide {
   Div32 d_row, d_seq, d_page;
 };
 
+// The factors that place a span's register in its input:
+// level[b] = x^(8 * span * 2^b).
+struct SpanShift {
+  uint64_t level[kSpanLevels];
+};
+
+__device__ __forceinline__ uint64_t shfl_xor64(uint64_t v, int mask) {
+  const uint32_t lo = (uint32_t)__shfl_xor((int)(uint32_t)v, mask);
+  const uint32_t hi = (uint32_t)__shfl_xor((int)(uint32_t)(v >> 32), mask);
+  return (uint64_t)hi << 32 | lo;
+}
+
 // Kernel 1: raw register of each span of the front-padded streams of
 // gridDim.x / spans_per_buf inputs (tensors) of `head` bytes each (a multiple
 // of 16), input i at data + i * buf_stride bytes (pool modes: the blob tensor
 // of plane i); `pad` leading zero bytes (a multiple of 16) make head + pad =
 // spans_per_buf spans of span_subs sub-chunks.  Workgroup w takes span
-// w % spans_per_buf of input w / spans_per_buf and writes its register to
+// w % spans_per_buf of input w / spans_per_buf and writes its register,
+// multiplied into its place in the input, to
 // partial[input * kMaxSpans + span].
 template <int kMode>
 __global__ __launch_bounds__(kCrcThreads) void crc64_span_kernel(const u32x4* __restrict__ data, int64_t buf_stride,
                                                                  int64_t pad, int64_t span_subs,
                                                                  int32_t spans_per_buf,
-                                                                 const uint64_t* __restrict__ tables,
-                                                                 uint64_t* __restrict__ partial, PoolSide ps_in) {
+                                                                 uint64_t* __restrict__ partial, SpanShift sh,
+                                                                 PoolSide ps_in) {
+  const uint64_t* tables = kConstTables.w;
   // big: slicing tables 0..3 in kCopies replicas (128 KiB), then the lane-join levels 0..7;
   // small: per-wave staging of one 1 KiB row (16 KiB) and the sub-chunk advance table (16 KiB), then
   // the join registers and level 8.
@@ -529,46 +579,128 @@ __global__ __launch_bounds__(kCrcThreads) void crc64_span_kernel(const u32x4* __
     }
     __syncthreads();
   }
-  if (threadIdx.x == 0) partial[buf_idx * kMaxSpans + span_idx] = acc[0];
-}
-
-// Kernel 2 (one workgroup of kMaxSpans lanes per input i: its span registers
-// at partial + i * kMaxSpans, its tail at tail + i * buf_stride, its CRC to
-// out[i]): lane t holds span register t - lead (the first `lead` lanes hold
-// zero spans, i.e. more leading zero bytes), a tree of table multiplies joins
-// them, then the tail bytes are appended and the CRC finished:
-// out = ~(preset_shift + R).
-__global__ __launch_bounds__(kMaxSpans) void crc64_finish_kernel(const uint64_t* __restrict__ tables,
-                                                                 const uint64_t* __restrict__ partial, int spans,
-                                                                 const unsigned char* __restrict__ tail,
-                                                                 int64_t buf_stride, int tail_len,
-                                                                 uint64_t preset_shift, uint64_t* __restrict__ out) {
-  partial += blockIdx.x * kMaxSpans;
-  tail += blockIdx.x * buf_stride;
-  out += blockIdx.x;
-  __shared__ uint64_t lvl_tab[kSpanLevels * kTableWords];       // 128 KiB
-  __shared__ uint64_t t0[256];
-  __shared__ uint64_t acc[kMaxSpans];
-  const int lead = kMaxSpans - spans;
-  acc[threadIdx.x] = (int)threadIdx.x >= lead ? partial[threadIdx.x - lead] : 0ull;
-  t0[threadIdx.x] = tables[kSetSlice * kTableWords + threadIdx.x];   // slicing table 0 (kMaxSpans == 256)
-  stage<16>(lvl_tab, tables + kSetSpan * kTableWords, kSpanLevels * kTableWords, kMaxSpans);
+  // The span's register times X^k, X = x^(8 * span), k = spans_per_buf - 1 - span_idx: its place in
+  // the input, so that the registers of an input's spans just XOR together.  One factor
+  // x^(8 * span * 2^b) per set bit b of k, each a GF(2) product across a wave: lane p holds
+  // x^(63 - p) times the factor (the basis of mulmod), the product is the XOR over the set bits p of
+  // the register of lane p's word.  Wave b builds factor b's basis (the join's tables are free now).
+  const int k = spans_per_buf - 1 - span_idx;
+  uint64_t* basis = big;
+  if (wave < kSpanLevels && ((k >> wave) & 1)) {
+    uint64_t v = sh.level[wave];
+    for (int it = 0; it < 63; ++it)
+      if (it < 63 - lane) v = mul_x(v);
+    basis[wave * 64 + lane] = v;
+  }
   __syncthreads();
-  for (int lvl = 0; lvl < kSpanLevels; ++lvl) {
-    const int s = 1 << lvl;
-    const int t = threadIdx.x;
-    if ((t & (2 * s - 1)) == 0) acc[t] = lookup8(acc[t], lvl_tab + lvl * kTableWords) ^ acc[t + s];
-    __syncthreads();
-  }
-  if (threadIdx.x == 0) {
+  if (wave == 0) {
     uint64_t r = acc[0];
-    for (int b = 0; b < tail_len; ++b) r = t0[(r ^ tail[b]) & 0xff] ^ (r >> 8);
-    out[0] = ~(preset_shift ^ r);
+    for (int b = 0; b < kSpanLevels; ++b) {
+      if (!((k >> b) & 1)) continue;
+      uint64_t t = ((r >> lane) & 1) ? basis[b * 64 + lane] : 0ull;
+      for (int o = 32; o > 0; o >>= 1) t ^= shfl_xor64(t, o);
+      r = t;
+    }
+    if (lane == 0) partial[buf_idx * kMaxSpans + span_idx] = r;
   }
 }
 
-// Workspace words one CRC needs: tables + span registers.
-int64_t crc_words(int64_t) { return kWsTables + kMaxSpans; }
+// The KVCACHE1 header (written by seal, checked by verify): sixteen
+// little-endian 8-byte words, words 8 and 9 the checksums of K and V.
+struct HeaderFields {
+  uint64_t request_id, model_id;
+  uint32_t seq_len, layers, kv_heads, head_dim, elem_bytes, planes;
+  uint64_t k_bytes, v_bytes;
+};
+
+__device__ uint64_t header_word(const HeaderFields& f, int w, const uint64_t* crcs) {
+  switch (w) {
+    case 0: {
+      uint64_t magic;
+      memcpy(&magic, "KVCACHE1", 8);
+      return magic;
+    }
+    case 1: return f.request_id;
+    case 2: return f.model_id;
+    case 3: return (uint64_t)f.seq_len | ((uint64_t)f.layers << 32);
+    case 4: return (uint64_t)f.kv_heads | ((uint64_t)f.head_dim << 32);
+    case 5: return (uint64_t)f.elem_bytes | ((uint64_t)f.planes << 32);
+    case 6: return f.k_bytes;
+    case 7: return f.v_bytes;
+    case 8: return crcs[0];
+    case 9: return crcs[1];
+    default: return 0;
+  }
+}
+
+// What kernel 2 does with the checksums: write them out, also write a blob's
+// header with them (seal), or also check a blob's header against them
+// (verify: result[0] = TOPKV_OK or TOPKV_ERR_CHECKSUM, result[1] = mask of
+// bad header words 0..7, result[2] / [3] = K / V checksum mismatch).
+enum { kFinishCrcs = 0, kFinishSeal = 1, kFinishVerify = 2 };
+
+struct FinishArgs {
+  int32_t inputs;                       // inputs with data (span registers and tails)
+  int32_t outputs;                      // checksums produced (inputs, then empty ones: CRC 0)
+  int32_t spans, tail_len;
+  int64_t stride;                       // between the inputs' tails
+  uint64_t preset_shift;                // ~0 * x^(8n): the preset carried over the n bytes
+  int32_t what;
+  HeaderFields f;
+};
+
+// Kernel 2 (one workgroup of kMaxSpans lanes): each input's span registers,
+// already in place, XOR into its raw register R; the tail bytes are appended
+// and the CRC finished, out[i] = ~(preset_shift + R); then the header is
+// written or checked.
+__global__ __launch_bounds__(kMaxSpans) void crc64_finish_kernel(const uint64_t* __restrict__ partial,
+                                                                 const unsigned char* __restrict__ tail,
+                                                                 FinishArgs a, uint64_t* __restrict__ out,
+                                                                 unsigned char* __restrict__ blob,
+                                                                 int32_t* __restrict__ result) {
+  __shared__ uint64_t t0[256];
+  __shared__ uint64_t part[2][kMaxSpans / 64];
+  __shared__ uint64_t crcs[2];
+  static_assert(kMaxSpans == 256, "one slicing-table entry per lane");
+  const int i = threadIdx.x, lane = i & 63, wave = i >> 6;
+  t0[i] = kConstTables.w[kSetSlice * kTableWords + i];           // slicing table 0
+  for (int in = 0; in < a.inputs; ++in) {
+    uint64_t v = i < a.spans ? partial[in * kMaxSpans + i] : 0ull;
+    for (int o = 32; o > 0; o >>= 1) v ^= shfl_xor64(v, o);
+    if (lane == 0) part[in][wave] = v;
+  }
+  __syncthreads();
+  if (i < a.outputs) {
+    uint64_t c = 0;                                             // the CRC of no bytes
+    if (i < a.inputs) {
+      uint64_t r = part[i][0] ^ part[i][1] ^ part[i][2] ^ part[i][3];
+      const unsigned char* tl = tail + i * a.stride;
+      for (int b = 0; b < a.tail_len; ++b) r = t0[(r ^ tl[b]) & 0xff] ^ (r >> 8);
+      c = ~(a.preset_shift ^ r);
+    }
+    out[i] = c;
+    crcs[i] = c;
+  }
+  if (a.what == kFinishCrcs) return;
+  __syncthreads();
+  if (a.what == kFinishSeal) {
+    if (i < 16) reinterpret_cast<uint64_t*>(blob)[i] = header_word(a.f, i, crcs);
+  } else if (i == 0) {
+    const uint64_t* h = reinterpret_cast<const uint64_t*>(blob);
+    int32_t bad = 0;
+    for (int w = 0; w < 8; ++w)
+      if (h[w] != header_word(a.f, w, crcs)) bad |= 1 << w;
+    const int32_t ck = h[8] != crcs[0];
+    const int32_t cv = h[9] != crcs[1];
+    result[0] = (bad | ck | cv) ? (int32_t)TOPKV_ERR_CHECKSUM : (int32_t)TOPKV_OK;
+    result[1] = bad;
+    result[2] = ck;
+    result[3] = cv;
+  }
+}
+
+// Workspace words one CRC needs: its span registers.
+int64_t crc_words(int64_t) { return kMaxSpans; }
 
 // Span geometry of CRCs over `inputs` inputs of n bytes each, launched
 // together: each 16-byte-aligned head is cut into `spans` spans of
@@ -589,36 +721,45 @@ Spans span_geometry(int64_t n, int inputs = 1) {
   return g;
 }
 
-// Queue the tables for CRCs whose spans have `span` bytes into ws (first
-// kWsTables words).
-topkv_status_t crc64_tables(uint64_t* ws, int64_t span, hipStream_t stream) {
-  const ShiftConsts& sc = shift_consts();
-  TableConsts tc;
-  tc.shift[kSetSlice] = 0;
-  tc.shift[kSetSub] = sc.x8pow2[kSubLog2];                                     // x^(8 * sub-chunk)
-  for (int l = 0; l < kLaneLevels; ++l) tc.shift[kSetLane + l] = x8n(sc, (uint64_t)kPiece << l);
-  for (int l = 0; l < kSpanLevels; ++l) tc.shift[kSetSpan + l] = x8n(sc, (uint64_t)span << l);
-  hipLaunchKernelGGL(crc64_tables_kernel, dim3((unsigned)(kWsTables / 256)), dim3(256), 0, stream, ws, tc);
-  return hipGetLastError() == hipSuccess ? TOPKV_OK : TOPKV_ERR_LAUNCH;
-}
-
-// Queue the CRC-64/XZ of each of `inputs` inputs of n bytes, input i at
-// data + i * stride, into out[i] (device).  data and stride 16-byte aligned;
-// `tables` were queued by crc64_tables for span_geometry(n, inputs).span;
-// partial has room for inputs * kMaxSpans words.
-topkv_status_t crc64_launch(const unsigned char* data, int64_t n, int inputs, int64_t stride, const uint64_t* tables,
-                            uint64_t* partial, uint64_t* out, hipStream_t stream) {
+// Kernel 2's arguments for CRCs of `inputs` inputs of n bytes, `stride` apart,
+// whose spans follow span_geometry(n, inputs): checksums only.
+FinishArgs finish_args(int64_t n, int inputs, int64_t stride) {
   const ShiftConsts& sc = shift_consts();
   const Spans g = span_geometry(n, inputs);
+  FinishArgs a{};
+  a.inputs = inputs;
+  a.outputs = inputs;
+  a.spans = (int32_t)g.spans;
+  a.tail_len = (int32_t)(n - g.head);
+  a.stride = stride;
+  a.preset_shift = mulmod(x8n(sc, (uint64_t)n), ~0ull);
+  a.what = kFinishCrcs;
+  return a;
+}
+
+SpanShift span_shift(int64_t span) {
+  SpanShift s;
+  s.level[0] = x8n(shift_consts(), (uint64_t)span);
+  for (int b = 1; b < kSpanLevels; ++b) s.level[b] = mulmod(s.level[b - 1], s.level[b - 1]);
+  return s;
+}
+
+// Queue the CRC-64/XZ of each of a.inputs inputs of n bytes, input i at
+// data + i * a.stride (16-byte aligned), into out[0 .. a.outputs) (device),
+// then what a.what asks for (blob: the header; result: verify's four words).
+// partial has room for a.inputs * kMaxSpans words.
+topkv_status_t crc64_launch(const unsigned char* data, int64_t n, const FinishArgs& a, uint64_t* partial,
+                            uint64_t* out, unsigned char* blob, int32_t* result, hipStream_t stream) {
+  const Spans g = span_geometry(n, a.inputs);
   if (g.span_subs > kMaxSpanSubs) return TOPKV_ERR_UNSUPPORTED;   // spans of 2 GiB and more
   if (g.spans > 0) {
-    hipLaunchKernelGGL(crc64_span_kernel<kStream>, dim3((unsigned)(g.spans * inputs)), dim3(kCrcThreads), 0, stream,
-                       reinterpret_cast<const u32x4*>(data), stride, g.spans * g.span - g.head, g.span_subs,
-                       (int32_t)g.spans, tables, partial, PoolSide{});
+    hipLaunchKernelGGL(crc64_span_kernel<kStream>, dim3((unsigned)(g.spans * a.inputs)), dim3(kCrcThreads), 0,
+                       stream, reinterpret_cast<const u32x4*>(data), a.stride, g.spans * g.span - g.head,
+                       g.span_subs, (int32_t)g.spans, partial, span_shift(g.span), PoolSide{});
     if (hipGetLastError() != hipSuccess) return TOPKV_ERR_LAUNCH;
   }
-  hipLaunchKernelGGL(crc64_finish_kernel, dim3((unsigned)inputs), dim3(kMaxSpans), 0, stream, tables, partial,
-                     (int)g.spans, data + g.head, stride, (int)(n - g.head), mulmod(x8n(sc, (uint64_t)n), ~0ull), out);
+  hipLaunchKernelGGL(crc64_finish_kernel, dim3(1), dim3(kMaxSpans), 0, stream, partial, data + g.head, a, out, blob,
+                     result);
   return hipGetLastError() == hipSuccess ? TOPKV_OK : TOPKV_ERR_LAUNCH;
 }
 
@@ -649,57 +790,6 @@ topkv_status_t blob_geometry(const topkv_pool_t* g, int32_t seq_len, Blob* b) {
   return TOPKV_OK;
 }
 
-struct HeaderFields {
-  uint64_t request_id, model_id;
-  uint32_t seq_len, layers, kv_heads, head_dim, elem_bytes, planes;
-  uint64_t k_bytes, v_bytes;
-};
-
-// Writes the 128-byte header: 16 lanes each store one little-endian 8-byte
-// word (vector stores); words 8 and 9 are the two checksums from `crcs`.
-__global__ void kv1_header_kernel(unsigned char* __restrict__ blob, HeaderFields f,
-                                  const uint64_t* __restrict__ crcs) {
-  const int w = threadIdx.x;
-  if (w >= 16) return;
-  uint64_t v = 0;
-  switch (w) {
-    case 0: memcpy(&v, "KVCACHE1", 8); break;
-    case 1: v = f.request_id; break;
-    case 2: v = f.model_id; break;
-    case 3: v = (uint64_t)f.seq_len | ((uint64_t)f.layers << 32); break;
-    case 4: v = (uint64_t)f.kv_heads | ((uint64_t)f.head_dim << 32); break;
-    case 5: v = (uint64_t)f.elem_bytes | ((uint64_t)f.planes << 32); break;
-    case 6: v = f.k_bytes; break;
-    case 7: v = f.v_bytes; break;
-    case 8: v = crcs[0]; break;
-    case 9: v = crcs[1]; break;
-    default: v = 0; break;
-  }
-  reinterpret_cast<uint64_t*>(blob)[w] = v;
-}
-
-// result[0] status, [1] header fields differing from the expected geometry
-// (bit mask over header words 0-7), [2] K checksum mismatch, [3] V mismatch.
-__global__ void kv1_verify_kernel(const unsigned char* __restrict__ blob, HeaderFields f,
-                                  const uint64_t* __restrict__ crcs, int32_t* __restrict__ result) {
-  if (threadIdx.x != 0) return;
-  const uint64_t* h = reinterpret_cast<const uint64_t*>(blob);
-  uint64_t magic;
-  memcpy(&magic, "KVCACHE1", 8);
-  const uint64_t want[8] = {magic, f.request_id, f.model_id, (uint64_t)f.seq_len | ((uint64_t)f.layers << 32),
-                            (uint64_t)f.kv_heads | ((uint64_t)f.head_dim << 32),
-                            (uint64_t)f.elem_bytes | ((uint64_t)f.planes << 32), f.k_bytes, f.v_bytes};
-  int32_t bad = 0;
-  for (int w = 0; w < 8; ++w)
-    if (h[w] != want[w]) bad |= 1 << w;
-  const int32_t ck = h[8] != crcs[0];
-  const int32_t cv = h[9] != crcs[1];
-  result[0] = (bad | ck | cv) ? (int32_t)TOPKV_ERR_CHECKSUM : (int32_t)TOPKV_OK;
-  result[1] = bad;
-  result[2] = ck;
-  result[3] = cv;
-}
-
 HeaderFields fields(const topkv_pool_t* g, int32_t seq_len, uint64_t request_id, uint64_t model_id, const Blob& b) {
   HeaderFields f;
   f.request_id = request_id;
@@ -715,31 +805,20 @@ HeaderFields fields(const topkv_pool_t* g, int32_t seq_len, uint64_t request_id,
   return f;
 }
 
-// Both checksums of a blob body into ws[0..1]; then the tables, then the
-// span registers of K and of V.
-topkv_status_t blob_crcs(const unsigned char* blob, const Blob& b, uint64_t* ws, hipStream_t stream) {
-  uint64_t* tables = ws + 2;
-  uint64_t* partial_k = tables + kWsTables;
-  uint64_t* partial_v = partial_k + crc_words(b.k_bytes) - kWsTables;
-  if (b.v_bytes == b.k_bytes) {   // both tensors in one launch of each kernel
-    const topkv_status_t st = crc64_tables(tables, span_geometry(b.k_bytes, 2).span, stream);
-    if (st != TOPKV_OK) return st;
-    return crc64_launch(blob + kHeaderBytes, b.k_bytes, 2, b.k_bytes, tables, partial_k, ws, stream);
-  }
-  const int64_t span_k = span_geometry(b.k_bytes).span, span_v = span_geometry(b.v_bytes).span;
-  topkv_status_t st = crc64_tables(tables, span_k, stream);
-  if (st != TOPKV_OK) return st;
-  st = crc64_launch(blob + kHeaderBytes, b.k_bytes, 1, 0, tables, partial_k, ws, stream);
-  if (st != TOPKV_OK) return st;
-  if (span_v != span_k) {   // stream order: K's kernels are done with the tables before they change
-    st = crc64_tables(tables, span_v, stream);
-    if (st != TOPKV_OK) return st;
-  }
-  return crc64_launch(blob + kHeaderBytes + b.k_bytes, b.v_bytes, 1, 0, tables, partial_v, ws + 1, stream);
+// Both checksums of a blob body into ws[0..1] (then the span registers), and
+// the header written (kFinishSeal) or checked (kFinishVerify, into result).
+topkv_status_t blob_crcs(unsigned char* blob, const Blob& b, const HeaderFields& f, int what, int32_t* result,
+                         uint64_t* ws, hipStream_t stream) {
+  const int inputs = b.v_bytes == b.k_bytes ? 2 : 1;   // an MLA blob has no V tensor
+  FinishArgs a = finish_args(b.k_bytes, inputs, b.k_bytes);
+  a.outputs = 2;
+  a.what = what;
+  a.f = f;
+  return crc64_launch(blob + kHeaderBytes, b.k_bytes, a, ws + 2, ws, blob, result, stream);
 }
 
 int64_t blob_ws_bytes(const Blob& b) {
-  return (int64_t)sizeof(uint64_t) * (2 + crc_words(b.k_bytes) + crc_words(b.v_bytes) - kWsTables);
+  return (int64_t)sizeof(uint64_t) * (2 + 2 * kMaxSpans);
 }
 
 bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15) == 0; }
@@ -757,10 +836,8 @@ bool fused_fits(const topkv_pool_t* pool, int32_t seq_len, const Blob& b) {
 // (kGather: pool -> blob, kScatter: blob -> pool).
 template <int kMode>
 topkv_status_t fused_blob_crcs(const topkv_pool_t* pool, const int32_t* table, int32_t seq_len, unsigned char* blob,
-                               const Blob& b, uint64_t* ws, hipStream_t stream) {
-  uint64_t* tables = ws + 2;
-  uint64_t* partial[2] = {tables + kWsTables, tables + kWsTables + kMaxSpans};
-  const ShiftConsts& sc = shift_consts();
+                               const Blob& b, const HeaderFields& f, int what, int32_t* result, uint64_t* ws,
+                               hipStream_t stream) {
   PoolSide ps{};
   ps.pool = static_cast<char*>(pool->base);
   ps.table = table;
@@ -776,26 +853,22 @@ topkv_status_t fused_blob_crcs(const topkv_pool_t* pool, const int32_t* table, i
   ps.d_row = make_div32((uint32_t)b.row);
   ps.d_seq = make_div32((uint32_t)seq_len);
   ps.d_page = make_div32((uint32_t)pool->page_size);
-  // every plane's tensor (K, V) in one launch of each kernel; the tensors have the same size
+  // every plane's tensor (K, V) in one launch of each kernel; the tensors have the same size (tensors
+  // are whole 16-byte rows: no tail); an MLA cache has no V tensor: its checksum is that of no bytes
   const Spans g = span_geometry(b.k_bytes, pool->planes);
-  topkv_status_t st = crc64_tables(tables, g.span, stream);
-  if (st != TOPKV_OK) return st;
+  FinishArgs a = finish_args(b.k_bytes, pool->planes, b.k_bytes);
+  a.outputs = 2;
+  a.what = what;
+  a.f = f;
   ps.plane_stride = (int64_t)pool->page_size * b.row;
   ps.blob = reinterpret_cast<u32x4*>(blob + kHeaderBytes);
   hipLaunchKernelGGL(crc64_span_kernel<kMode>, dim3((unsigned)(g.spans * pool->planes)), dim3(kCrcThreads), 0, stream,
-                     ps.blob, b.k_bytes, g.spans * g.span - g.head, g.span_subs, (int32_t)g.spans, tables, partial[0],
-                     ps);
+                     ps.blob, b.k_bytes, g.spans * g.span - g.head, g.span_subs, (int32_t)g.spans, ws + 2,
+                     span_shift(g.span), ps);
   if (hipGetLastError() != hipSuccess) return TOPKV_ERR_LAUNCH;
-  hipLaunchKernelGGL(crc64_finish_kernel, dim3((unsigned)pool->planes), dim3(kMaxSpans), 0, stream, tables,
-                     partial[0], (int)g.spans, reinterpret_cast<const unsigned char*>(ps.blob) + g.head, b.k_bytes, 0,
-                     mulmod(x8n(sc, (uint64_t)b.k_bytes), ~0ull), ws);
-  if (hipGetLastError() != hipSuccess) return TOPKV_ERR_LAUNCH;
-  if (pool->planes == 1) {     // an MLA cache has no V tensor: its checksum is that of no bytes
-    hipLaunchKernelGGL(crc64_finish_kernel, dim3(1), dim3(kMaxSpans), 0, stream, tables, partial[1], 0,
-                       blob + kHeaderBytes + b.k_bytes, (int64_t)0, 0, mulmod(x8n(sc, 0), ~0ull), ws + 1);
-    if (hipGetLastError() != hipSuccess) return TOPKV_ERR_LAUNCH;
-  }
-  return TOPKV_OK;
+  hipLaunchKernelGGL(crc64_finish_kernel, dim3(1), dim3(kMaxSpans), 0, stream, ws + 2,
+                     reinterpret_cast<const unsigned char*>(ps.blob) + g.head, a, ws, blob, result);
+  return hipGetLastError() == hipSuccess ? TOPKV_OK : TOPKV_ERR_LAUNCH;
 }
 
 // Layers [first_layer, first_layer + num_layers) of one request into (pack) or
@@ -830,7 +903,7 @@ topkv_status_t kv1_move_layers(bool pack, const topkv_pool_t* pool, int32_t firs
 // process ends.  Host code never names it in a launch or a copy: the name is
 // a host-side stand-in, and its device address on each device comes from
 // hipGetSymbolAddress (scratch_words below).
-__device__ __align__(256) uint64_t scratch[kWsTables + kMaxSpans];
+__device__ __align__(256) uint64_t scratch[kMaxSpans];
 static_assert(sizeof(scratch) == (size_t)TOPKV_CRC64_NOALLOC_SCRATCH_BYTES, "scratch size in topkv.h");
 
 constexpr int kMaxDevices = 64;
@@ -870,12 +943,11 @@ topkv_status_t topkv_crc64_noalloc(const void* data, int64_t nbytes, uint64_t* c
   uint64_t* ws = nullptr;
   const topkv_status_t st = scratch_words(&ws);
   if (st != TOPKV_OK) return st;
-  // the tables kernel writes every table word and each span kernel its own
-  // register before the finishing kernel reads them: nothing left by an
-  // earlier call is read
-  const topkv_status_t t = crc64_tables(ws, span_geometry(nbytes).span, stream);
-  if (t != TOPKV_OK) return t;
-  return crc64_launch(static_cast<const unsigned char*>(data), nbytes, 1, 0, ws, ws + kWsTables, crc_out, stream);
+  // each span kernel writes its own register before the finishing kernel
+  // reads it, which reads no other word: nothing left by an earlier call is
+  // read
+  return crc64_launch(static_cast<const unsigned char*>(data), nbytes, finish_args(nbytes, 1, 0), ws, crc_out,
+                      nullptr, nullptr, stream);
 }
 
 int64_t topkv_crc64_workspace_bytes(int64_t nbytes) {
@@ -888,10 +960,8 @@ topkv_status_t topkv_crc64(const void* data, int64_t nbytes, void* workspace, in
   if (nbytes < 0 || !crc_out || (nbytes > 0 && !data) || !workspace) return TOPKV_ERR_INVALID_ARG;
   if (workspace_bytes < topkv_crc64_workspace_bytes(nbytes)) return TOPKV_ERR_INVALID_ARG;
   if (nbytes > 0 && !aligned16(data)) return TOPKV_ERR_UNSUPPORTED;
-  uint64_t* ws = static_cast<uint64_t*>(workspace);
-  const topkv_status_t st = crc64_tables(ws, span_geometry(nbytes).span, stream);
-  if (st != TOPKV_OK) return st;
-  return crc64_launch(static_cast<const unsigned char*>(data), nbytes, 1, 0, ws, ws + kWsTables, crc_out, stream);
+  return crc64_launch(static_cast<const unsigned char*>(data), nbytes, finish_args(nbytes, 1, 0),
+                      static_cast<uint64_t*>(workspace), crc_out, nullptr, nullptr, stream);
 }
 
 int64_t topkv_kvcache1_bytes(const topkv_pool_t* geometry, int32_t seq_len) {
@@ -925,13 +995,8 @@ topkv_status_t topkv_kvcache1_seal(const topkv_pool_t* geometry, int32_t seq_len
   if (st != TOPKV_OK) return st;
   if (!blob || blob_bytes < b.total || !workspace || workspace_bytes < blob_ws_bytes(b)) return TOPKV_ERR_INVALID_ARG;
   if (!aligned16(blob)) return TOPKV_ERR_UNSUPPORTED;
-  uint64_t* ws = static_cast<uint64_t*>(workspace);
-  unsigned char* bytes = static_cast<unsigned char*>(blob);
-  st = blob_crcs(bytes, b, ws, stream);
-  if (st != TOPKV_OK) return st;
-  hipLaunchKernelGGL(kv1_header_kernel, dim3(1), dim3(64), 0, stream, bytes,
-                     fields(geometry, seq_len, request_id, model_id, b), (const uint64_t*)ws);
-  return hipGetLastError() == hipSuccess ? TOPKV_OK : TOPKV_ERR_LAUNCH;
+  return blob_crcs(static_cast<unsigned char*>(blob), b, fields(geometry, seq_len, request_id, model_id, b),
+                   kFinishSeal, nullptr, static_cast<uint64_t*>(workspace), stream);
 }
 
 topkv_status_t topkv_kvcache1_verify(const topkv_pool_t* geometry, int32_t seq_len, uint64_t request_id,
@@ -943,13 +1008,10 @@ topkv_status_t topkv_kvcache1_verify(const topkv_pool_t* geometry, int32_t seq_l
   if (!blob || blob_bytes < b.total || !workspace || workspace_bytes < blob_ws_bytes(b) || !result)
     return TOPKV_ERR_INVALID_ARG;
   if (!aligned16(blob)) return TOPKV_ERR_UNSUPPORTED;
-  uint64_t* ws = static_cast<uint64_t*>(workspace);
-  const unsigned char* bytes = static_cast<const unsigned char*>(blob);
-  st = blob_crcs(bytes, b, ws, stream);
-  if (st != TOPKV_OK) return st;
-  hipLaunchKernelGGL(kv1_verify_kernel, dim3(1), dim3(64), 0, stream, bytes,
-                     fields(geometry, seq_len, request_id, model_id, b), (const uint64_t*)ws, result);
-  return hipGetLastError() == hipSuccess ? TOPKV_OK : TOPKV_ERR_LAUNCH;
+  // (kernel 2 only reads the blob on this path: kFinishVerify writes no header)
+  return blob_crcs(static_cast<unsigned char*>(const_cast<void*>(blob)), b,
+                   fields(geometry, seq_len, request_id, model_id, b), kFinishVerify, result,
+                   static_cast<uint64_t*>(workspace), stream);
 }
 
 topkv_status_t topkv_kvcache1_unpack_layer(const void* blob, int64_t blob_bytes, const topkv_pool_t* dst,
@@ -988,13 +1050,9 @@ topkv_status_t topkv_kvcache1_pack_seal(const topkv_pool_t* src, const int32_t* 
                                         nullptr, seq_len, 0, false, 0, 0, INT64_MAX, stream);
     if (st != TOPKV_OK) return st;
   }
-  uint64_t* ws = static_cast<uint64_t*>(workspace);
-  unsigned char* bytes = static_cast<unsigned char*>(blob);
-  st = fused_blob_crcs<kGather>(src, block_table, seq_len, bytes, b, ws, stream);
-  if (st != TOPKV_OK) return st;
-  hipLaunchKernelGGL(kv1_header_kernel, dim3(1), dim3(64), 0, stream, bytes,
-                     fields(src, seq_len, request_id, model_id, b), (const uint64_t*)ws);
-  return hipGetLastError() == hipSuccess ? TOPKV_OK : TOPKV_ERR_LAUNCH;
+  return fused_blob_crcs<kGather>(src, block_table, seq_len, static_cast<unsigned char*>(blob), b,
+                                  fields(src, seq_len, request_id, model_id, b), kFinishSeal, nullptr,
+                                  static_cast<uint64_t*>(workspace), stream);
 }
 
 topkv_status_t topkv_kvcache1_verify_unpack(const void* blob, int64_t blob_bytes, const topkv_pool_t* dst,
@@ -1021,13 +1079,9 @@ topkv_status_t topkv_kvcache1_verify_unpack(const void* blob, int64_t blob_bytes
                                         nullptr, seq_len, 0, true, 0, 0, INT64_MAX, stream);
     if (st != TOPKV_OK) return st;
   }
-  uint64_t* ws = static_cast<uint64_t*>(workspace);
-  unsigned char* bytes = static_cast<unsigned char*>(const_cast<void*>(blob));
-  st = fused_blob_crcs<kScatter>(dst, block_table, seq_len, bytes, b, ws, stream);
-  if (st != TOPKV_OK) return st;
-  hipLaunchKernelGGL(kv1_verify_kernel, dim3(1), dim3(64), 0, stream, bytes,
-                     fields(dst, seq_len, request_id, model_id, b), (const uint64_t*)ws, result);
-  return hipGetLastError() == hipSuccess ? TOPKV_OK : TOPKV_ERR_LAUNCH;
+  return fused_blob_crcs<kScatter>(dst, block_table, seq_len, static_cast<unsigned char*>(const_cast<void*>(blob)), b,
+                                   fields(dst, seq_len, request_id, model_id, b), kFinishVerify, result,
+                                   static_cast<uint64_t*>(workspace), stream);
 }
 
 topkv_status_t topkv_kvcache1_pack_layers(const topkv_pool_t* src, int32_t first_layer, int32_t num_layers,
