@@ -129,6 +129,11 @@ def parse():
     ap.add_argument("--issue", choices=["engine", "launches"], default="engine",
                     help="engine: one layer-engine launch per direction over each run of full-attention layers "
                          "(value); launches: one launch per layer.  The other mode is timed beside it")
+    ap.add_argument("--tables", choices=["random", "sorted", "consecutive"], default="random",
+                    help="page layout of the block tables: random (each request the next pages of a seeded "
+                         "permutation of the pool: the workloads' fragmented pools, measured by default), sorted "
+                         "(the same pages, each request's in ascending pool order), consecutive (each request's "
+                         "pages one contiguous run of the pool)")
     ap.add_argument("--no-configs", dest="configs", action="store_false",
                     help="skip the batched configurations (batch of 8, MLA, re-blocking) of the default run")
     ap.add_argument("--threads", type=int, default=0,
@@ -183,6 +188,27 @@ def layer_kernel(wl, direction):
     if full_bound and not any(wl.window(l) for l in range(wl.num_layers)) and row % (64 * 16) == 0:
         return "kv_reshard_single_kernel"
     return f"kv_{direction}_kernel"
+
+
+def table_layout(wl, layout):
+    """Re-lay both pools' block tables of a workload: "sorted" keeps every
+    request's pages and sorts them by pool index; "consecutive" hands the
+    requests consecutive runs of the pool in request order; "random" leaves
+    the workload's tables."""
+    import numpy as np
+    if layout == "random":
+        return
+    for attr, P in (("block_tables", wl.page_size), ("dst_block_tables", wl.dst_page_size)):
+        tab = getattr(wl, attr).copy()
+        nxt = 0
+        for r, n in enumerate(wl.seq_lens):
+            k = -(-int(n) // P)
+            if layout == "sorted":
+                tab[r, :k] = np.sort(tab[r, :k])
+            else:
+                tab[r, :k] = np.arange(nxt, nxt + k)
+                nxt += k
+        setattr(wl, attr, tab)
 
 
 def engine_kernel(wl, setup, direction):
@@ -769,7 +795,8 @@ def run(args):
 
     torch.cuda.set_device(0)
     wl = make_workload(args.workload)
-    log(f"[bench] workload {wl.describe()}")
+    table_layout(wl, args.tables)
+    log(f"[bench] workload {wl.describe()}, tables {args.tables}")
     st = Setup(wl, topkv)
     L, R = wl.num_layers, wl.num_reqs
     log(f"[bench] pools src {tuple(st.src.shape)} dst {tuple(st.dst.shape)}, packed {st.nbytes} B/layer, "
@@ -838,13 +865,13 @@ def run(args):
         "ms_per_step": round(ms_per_step, 4), "higher_is_better": True, "scaling": "weak",
         "vs_baseline": None, "dtype": "bf16", "data": "synthetic",
         "config": {"workload": f"{wl.name}: {WORKLOADS[wl.name]}", "layers": L, "requests": R,
-                   "issue": args.issue, "launch": args.launch,
+                   "issue": args.issue, "launch": args.launch, "tables": args.tables,
                    "tokens": int(wl.seq_lens.astype(np.int64).sum()), "page_size": wl.page_size,
                    "dst_page_size": wl.dst_page_size, "packed_bytes_per_layer": st.nbytes,
                    **({"state_layers": sum(wl.layer_state), "packed_state_bytes_per_layer": st.slot_bytes}
                       if wl.layer_state else {}),
                    "step": ("pack every layer, then unpack every layer: "
-                            + ("the layer engine, one persistent launch per direction over each run of "
+                            + ("the layer engine, one launch per direction over each run of "
                                "full-attention layers (every layer ready at launch), other layers one launch each"
                                if args.issue == "engine" else "one launch per layer")),
                    "seed": wl.seed, "packed_ring": st.ring, "phys_layers": wl.phys_layers},

@@ -183,7 +183,7 @@ topkv_status_t topkv_unpack_layer_batched_ex(const void* src, int64_t src_bytes,
 
 /* Layer engine (Section 5.2: a prefill worker sends layer l while layers
  * l+1 .. L-1 are still being computed, so the unit of transfer is one
- * layer).  ONE persistent launch moves layers [first_layer, first_layer +
+ * layer).  ONE launch moves layers [first_layer, first_layer +
  * num_layers) of a batch, each layer exactly as topkv_pack_layer_batched /
  * topkv_unpack_layer_batched would move it, in layer order, and each layer
  * only once its ready word allows.  The per-launch costs of one launch per

@@ -31,6 +31,31 @@ def test_windowed_bytes_count_kept_tokens_only():
         (int(n) - 1) // 16 - max(0, int(n) - 128) // 16 + 1 for n in wl.seq_lens)
 
 
+def test_table_layouts_keep_the_pages_valid():
+    """--tables sorted keeps every request's pages (sorted); consecutive gives
+    each request its own run of the pool; both stay inside the pool."""
+    import bench
+    from paper_2607_28633_amd.workloads import make_workload
+    base = make_workload("llama3-70b-batch8")
+    for layout in ("sorted", "consecutive"):
+        wl = make_workload("llama3-70b-batch8")
+        bench.table_layout(wl, layout)
+        for attr, P, NP in (("block_tables", wl.page_size, wl.num_pages),
+                            ("dst_block_tables", wl.dst_page_size, wl.dst_num_pages)):
+            tab, ref = getattr(wl, attr), getattr(base, attr)
+            seen = []
+            for r, n in enumerate(wl.seq_lens):
+                k = -(-int(n) // P)
+                row = tab[r, :k]
+                assert row.min() >= 0 and row.max() < NP
+                if layout == "sorted":
+                    assert (np.diff(row) > 0).all() and sorted(ref[r, :k].tolist()) == row.tolist()
+                else:
+                    assert (np.diff(row) == 1).all()
+                seen += row.tolist()
+            assert len(set(seen)) == len(seen)          # no page shared by two requests
+
+
 def test_more_than_one_gpu_is_refused():
     r = subprocess.run([sys.executable, os.path.join(ROOT, "bench.py"), "--gpus", "2"],
                        capture_output=True, text=True, cwd=ROOT, timeout=120)
