@@ -680,7 +680,9 @@ def ceiling(setup, steps):
     the same cache defeat): the empty kernel, the per-layer pack grid with
     every length 0, the hand-written streaming copy of one layer's packed
     bytes per launch into each layer's own slot, that copy at 64 MiB, 256 MiB
-    and 1 GiB, and the layer engine's schedule without tables
+    and 1 GiB, a read-only pass over the same sources at the same sizes
+    (the ceiling of a checksum pass), and the layer engine's schedule
+    without tables
     (topkv_ceiling_copy_layers: pool slab prefixes -> packed slots -> a
     second pool's slab prefixes, one launch per direction)."""
     import numpy as np
@@ -720,7 +722,7 @@ def ceiling(setup, steps):
         for l in range(L)], L), 3)
     flat = setup.src.view(-1).view(torch.uint8)
     slab = flat.numel() // setup.src.shape[0]
-    copies = {}
+    copies, reads = {}, {}
     for size, count in ((n, max(2, min(L, (2 << 30) // n))), (64 << 20, 20), (256 << 20, 6), (1 << 30, 2)):
         if size > flat.numel() // 2:
             continue
@@ -733,10 +735,19 @@ def ceiling(setup, steps):
                     for l, o in enumerate(offs)]
 
         us = graph_us(make, count)
-        copies[f"{size >> 20}MiB" if size != n else "layer"] = {"bytes": size, "us_per_launch": round(us, 3),
-                                                               "gbs": round(2 * size / us / 1e3, 1)}
-        del dst
+        key = f"{size >> 20}MiB" if size != n else "layer"
+        copies[key] = {"bytes": size, "us_per_launch": round(us, 3), "gbs": round(2 * size / us / 1e3, 1)}
+        # the read-only ceiling of a checksum pass: the same sources, each workgroup's XOR to one word
+        sink = torch.empty(-(-size // 32768), dtype=torch.int32, device="cuda")
+
+        def make_read(size=size, offs=offs, sink=sink):
+            return [(lambda s=flat[o:o + size]: cl.topkv_ceiling_read(s, size, sink, None)) for o in offs]
+
+        us = graph_us(make_read, count)
+        reads[key] = {"bytes": size, "us_per_launch": round(us, 3), "gbs": round(size / us / 1e3, 1)}
+        del dst, sink
     out["copy_per_launch"] = copies
+    out["read_per_launch"] = reads
     # the engine's schedule without tables: read each slab's first n bytes into the packed slots, then
     # write them to the second pool's slabs, one launch per direction, alternating as the step does
     lay = min(L, setup.ring, setup.src.shape[0], setup.dst.shape[0])
