@@ -64,10 +64,12 @@ __global__ __launch_bounds__(kThreads) void ceiling_read_kernel(const V* __restr
                                                                 uint32_t* __restrict__ sink) {
   __shared__ uint32_t part[kThreads / 64];
   V v[kVpt];
-  load_tile(v, s, (int64_t)blockIdx.x * kThreads * kVpt, n16);
+  const int64_t base = (int64_t)blockIdx.x * kThreads * kVpt;
+  load_tile(v, s, base, n16);
   uint32_t x = 0;
 #pragma unroll
-  for (int j = 0; j < kVpt; ++j) x ^= v[j].x ^ v[j].y ^ v[j].z ^ v[j].w;
+  for (int j = 0; j < kVpt; ++j)   // a ragged tile's clamped loads repeat its last vector: count it once
+    if (base + j * kThreads + threadIdx.x < n16) x ^= v[j].x ^ v[j].y ^ v[j].z ^ v[j].w;
   for (int o = 32; o > 0; o >>= 1) x ^= __shfl_xor(x, o);
   if ((threadIdx.x & 63) == 0) part[threadIdx.x >> 6] = x;
   __syncthreads();
