@@ -178,7 +178,9 @@ __device__ inline uint64_t lookup8(uint64_t v, const uint64_t* t) {   // t: 8 x 
 }
 
 // Four bytes (little-endian word w) into the register (lo, hi) with
-// slicing-by-4 tables held in LDS in kCopies = 16 replicas.  Layout (byte
+// slicing-by-4 tables (the slicing-by-N method of Kounavis and Berry: one
+// table per byte position of the word, the byte's effect after the bytes
+// that follow it) held in LDS in kCopies = 16 replicas.  Layout (byte
 // offsets in the 128 KiB table region): tables 2h and 2h + 1 share the 64 KiB
 // region h; entry b of table t, replica r sits at h * 65536 + b * 256 +
 // (t % 2) * 128 + r * 8.  So, with the LDS's 64 four-byte banks, replica r of
@@ -380,18 +382,40 @@ __global__ __launch_bounds__(kCrcThreads) void crc64_span_kernel(const u32x4* __
   // table: offset = pb + pg * page_bytes (one 32 x 32 -> 64-bit multiply-add).
   // (Every piece loads an entry - a padding piece row 0's - and the padding is marked in pb alone, so
   // no branch surrounds a load and nothing waits for the entries until a piece's slot is needed.)
+  auto piece = [&](const RowPos& p, int j, uint32_t* idx) -> int64_t {
+    uint32_t row = 0, inrow = 0;
+    const bool in_tensor = row_of(p, j, &row, &inrow);
+    const uint32_t l = div32(row, ps.d_seq);
+    const uint32_t t = row - l * (uint32_t)ps.seq_len;
+    const uint32_t i = div32(t, ps.d_page);                      // < ceil(seq_len / page_size)
+    *idx = i;
+    return in_tensor ? (int64_t)(ps.first_layer + (int32_t)l) * ps.layer_bytes + ps.plane_off +
+                           (int64_t)((uint64_t)(t - i * (uint32_t)ps.page_size) * (uint32_t)ps.row_bytes) + inrow
+                     : -1;
+  };
   auto lookup = [&](int64_t (&pb)[kLoads], int32_t (&pg)[kLoads], const RowPos& p) {
 #pragma unroll
     for (int j = 0; j < kLoads; ++j) {
-      uint32_t row = 0, inrow = 0;
-      const bool in_tensor = row_of(p, j, &row, &inrow);
-      const uint32_t l = div32(row, ps.d_seq);
-      const uint32_t t = row - l * (uint32_t)ps.seq_len;
-      const uint32_t i = div32(t, ps.d_page);                    // < ceil(seq_len / page_size)
+      uint32_t i = 0;
+      pb[j] = piece(p, j, &i);
       pg[j] = ps.table[i];
-      pb[j] = in_tensor ? (int64_t)(ps.first_layer + (int32_t)l) * ps.layer_bytes + ps.plane_off +
-                              (int64_t)((uint64_t)(t - i * (uint32_t)ps.page_size) * (uint32_t)ps.row_bytes) + inrow
-                        : -1;
+    }
+  };
+  // (kScatter) the entries alone, loaded a step ahead, and the page-independent offsets worked out
+  // again where the pieces are stored: fewer registers carried from step to step
+  auto entries = [&](int32_t (&pg)[kLoads], const RowPos& p) {
+#pragma unroll
+    for (int j = 0; j < kLoads; ++j) {
+      uint32_t i = 0;
+      (void)piece(p, j, &i);
+      pg[j] = ps.table[i];
+    }
+  };
+  auto offsets = [&](int64_t (&pb)[kLoads], const RowPos& p) {
+#pragma unroll
+    for (int j = 0; j < kLoads; ++j) {
+      uint32_t i = 0;
+      pb[j] = piece(p, j, &i);
     }
   };
   // pool byte of a piece: -1 in the padding, -2 when its page entry is out of range
@@ -458,7 +482,7 @@ __global__ __launch_bounds__(kCrcThreads) void crc64_span_kernel(const u32x4* __
   uint64_t fold = 0;
   // Per-sub-chunk state in kDepth sets used in turn, so a step never copies a later sub-chunk's
   // registers (a copy would wait for its loads): the pieces, the padding and moved masks, and (pool
-  // modes) the page-independent offsets and page entries.  The streaming mode keeps two sub-chunks'
+  // modes) the page entries and (kGather) the page-independent offsets.  The streaming mode keeps two sub-chunks'
   // loads in flight while it folds a third; the pool modes, which need more registers per piece, one.
   constexpr int kDepth = kMode == kStream ? 3 : 2;
   u32x4 buf[kDepth][kLoads];
@@ -479,7 +503,7 @@ __global__ __launch_bounds__(kCrcThreads) void crc64_span_kernel(const u32x4* __
       load(buf[k], k < span_subs ? k : span_subs - 1, &zp[k]);
       __builtin_amdgcn_sched_barrier(0);
     }
-    if (kMode == kScatter) lookup(pb[0], pg[0], pos);
+    if (kMode == kScatter) entries(pg[0], pos);
   }
   {
     // thread e writes entry b = e mod 256 of slicing table t = e / 256 into every replica (layout at
@@ -520,8 +544,10 @@ __global__ __launch_bounds__(kCrcThreads) void crc64_span_kernel(const u32x4* __
         // the next sub-chunk's entries (on a span's last step past the tensor's end: in-range table
         // indices whose entries are never used), then this sub-chunk's pieces to their pool slots
         const RowPos p1 = advance(pos);
-        lookup(pb[n], pg[n], p1);
-        put_pool(buf[c], pb[c], pg[c]);
+        entries(pg[n], p1);
+        int64_t pbc[kLoads];
+        offsets(pbc, pos);
+        put_pool(buf[c], pbc, pg[c]);
         pos = p1;
       }
     }
