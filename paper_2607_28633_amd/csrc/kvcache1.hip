@@ -15,8 +15,8 @@
 // complement), R(A || B) = R(A) * x^(8|B|) + R(B) over GF(2), leading zero
 // bytes leave R unchanged, and the CRC proper is
 // ~(~0 * x^(8N) + R(data)).  Multiplying a register by a fixed power of x is
-// linear, so it is the XOR of one lookup per register byte in a table of
-// that constant.  Work split:
+// linear, so it is the XOR of one lookup per register byte (or nibble) in a
+// table of that constant.  Work split:
 //   tables: the slicing tables, the constant that advances a register by
 //     one sub-chunk and the join levels of the lanes inside a span do not
 //     depend on the data; the compiler computes them (kConstTables);
@@ -32,10 +32,14 @@
 //     lanes run them through slicing-by-4 tables held in LDS in 16 replicas
 //     arranged so that the 32 lanes an LDS cycle serves never share a bank
 //     (crc_word4), and advance their running register by one sub-chunk per
-//     step; a tree of table multiplies joins the lanes at the end of the
-//     span, and the span's register is multiplied into its place in the
-//     input (a GF(2) product per bit of its distance to the end, done across
-//     a wave);
+//     step (a byte-table multiply); a tree of nibble-table multiplies joins
+//     the lanes at the end of the span (inside each wave by shuffles, then
+//     across the 16 waves), and the span's register is multiplied into its
+//     place in the input (one nibble-table multiply per set bit of its
+//     distance to the end, in spans).  Nibble sets take twice the lookups of
+//     byte sets but an eighth of the room, so they serve where tables are
+//     staged or built after the loop, and the byte set where a lookup runs
+//     every step;
 //   kernel 2: one workgroup XORs each input's placed span registers,
 //     appends the sub-16-byte tail, applies the preset and complement, and
 //     writes (seal) or checks (verify) a blob's header.
@@ -77,8 +81,9 @@ constexpr int kTableWords = 8 * 256;                            // one set of 8 
 constexpr int kCopies = 16;                                     // LDS replicas of the slicing tables
 constexpr int kWaves = kCrcThreads / 64;
 constexpr int kStageWords = kWaves * 64 * 16 / 8;               // per-wave staging of one 1 KiB row
-// constant table sets: 0 slicing, 1 sub-chunk advance, 2.. lane-join levels
-constexpr int kSetSlice = 0, kSetSub = 1, kSetLane = 2, kConstSets = kSetLane + kLaneLevels;
+constexpr int kNibWords = 16 * 16;                              // one nibble table set (2 KiB)
+// nibble table sets: the lane-join levels
+constexpr int kNibSets = kLaneLevels;
 
 struct ShiftConsts {
   uint64_t x8pow2[64];    // x^(8 * 2^k) mod P, reflected
@@ -117,20 +122,26 @@ uint64_t x8n(const ShiftConsts& c, uint64_t n) {
   return r;
 }
 
-// A set of 8 byte tables is linear in the byte: entry (k, b) is the XOR of
-// m[8k + i] over the set bits i of b, for the set's basis m[0..63].  Slicing
-// set: entry (k, b) is byte b followed by k zero bytes, b * x^(8(k + 1)), so
-// m[8k + i] = x^(63 - i) * x^(8k + 8).  Multiply set of constant c: entry
-// (k, b) is (b << 8k) * c, so m[j] = x^(63 - j) * c, i.e. m[63] = c and
-// m[j - 1] = x * m[j].  Each entry is built from the one with its lowest set
-// bit cleared.
+// A set of tables is linear in the register's bits: bit j of a 64-bit value
+// stands for the basis word m[j], and an entry is the XOR of m[j] over the
+// set bits j of the part of the value it indexes.  Byte sets: entry (k, b) of
+// 8 tables covers bits 8k .. 8k + 7; nibble sets: entry (k, n) of 16 tables
+// covers bits 4k .. 4k + 3 (16 entries of 8 bytes: one table is 128 bytes, so
+// the lanes of an LDS cycle looking up one table never share a bank).
+// Slicing set: entry (k, b) is byte b followed by k zero bytes,
+// b * x^(8(k + 1)), so m[8k + i] = x^(63 - i) * x^(8k + 8).  Multiply set of
+// constant c: entry (k, .) is (value << 8k or 4k) * c, so
+// m[j] = x^(63 - j) * c, i.e. m[63] = c and m[j - 1] = x * m[j].  Each entry
+// is built from the one with its lowest set bit cleared.
+template <int kBits>
 __host__ __device__ constexpr void fill_set(uint64_t* set, const uint64_t (&m)[64]) {
-  for (int k = 0; k < 8; ++k) {
-    set[k * 256] = 0;
-    for (int b = 1; b < 256; ++b) {
+  constexpr int kEntries = 1 << kBits;
+  for (int k = 0; k < 64 / kBits; ++k) {
+    set[k * kEntries] = 0;
+    for (int b = 1; b < kEntries; ++b) {
       int low = 0;
       while (!((b >> low) & 1)) ++low;
-      set[k * 256 + b] = set[k * 256 + (b & (b - 1))] ^ m[8 * k + low];
+      set[k * kEntries + b] = set[k * kEntries + (b & (b - 1))] ^ m[kBits * k + low];
     }
   }
 }
@@ -140,11 +151,13 @@ __host__ __device__ constexpr void multiply_basis(uint64_t (&m)[64], uint64_t c)
   for (int j = 63; j > 0; --j) m[j - 1] = mul_x(m[j]);
 }
 
-// The span-independent table sets, computed by the compiler: slicing, the
-// advance by one sub-chunk (x^(8 * 64 Ki)), and the lane-join levels
-// (x^(8 * kPiece * 2^l)).
+// The span-independent table sets, computed by the compiler: the slicing
+// bytes, the advance by one sub-chunk (x^(8 * 64 Ki), bytes) and the
+// lane-join levels (x^(8 * kPiece * 2^l), nibbles).
 struct ConstTables {
-  uint64_t w[kConstSets * kTableWords];
+  uint64_t slice[kTableWords];
+  uint64_t sub[kTableWords];
+  uint64_t nib[kNibSets * kNibWords];
 };
 
 constexpr ConstTables make_const_tables() {
@@ -155,23 +168,24 @@ constexpr ConstTables make_const_tables() {
   uint64_t m[64] = {};
   for (int k = 0; k < 8; ++k)
     for (int i = 0; i < 8; ++i) m[8 * k + i] = p[71 + 8 * k - i];
-  fill_set(t.w + kSetSlice * kTableWords, m);
+  fill_set<8>(t.slice, m);
   uint64_t x8p[kSubLog2 + 1] = {};                           // x8p[k] = x^(8 * 2^k)
   x8p[0] = p[8];
   for (int k = 1; k <= kSubLog2; ++k) x8p[k] = mulmod(x8p[k - 1], x8p[k - 1]);
   multiply_basis(m, x8p[kSubLog2]);
-  fill_set(t.w + kSetSub * kTableWords, m);
+  fill_set<8>(t.sub, m);
   static_assert(kPiece == 64 && 6 + kLaneLevels - 1 <= kSubLog2, "lane levels are x^(8 * 2^(6 + l))");
   for (int l = 0; l < kLaneLevels; ++l) {
     multiply_basis(m, x8p[6 + l]);
-    fill_set(t.w + (kSetLane + l) * kTableWords, m);
+    fill_set<4>(t.nib + l * kNibWords, m);
   }
   return t;
 }
 
 __device__ const ConstTables kConstTables = make_const_tables();
 
-__device__ inline uint64_t lookup8(uint64_t v, const uint64_t* t) {   // t: 8 x 256 words
+// v times the constant of a byte set t (8 x 256 words): one lookup per byte of v.
+__device__ __forceinline__ uint64_t lookup8(uint64_t v, const uint64_t* t) {
   return t[0 * 256 + (v & 0xff)] ^ t[1 * 256 + ((v >> 8) & 0xff)] ^ t[2 * 256 + ((v >> 16) & 0xff)] ^
          t[3 * 256 + ((v >> 24) & 0xff)] ^ t[4 * 256 + ((v >> 32) & 0xff)] ^ t[5 * 256 + ((v >> 40) & 0xff)] ^
          t[6 * 256 + ((v >> 48) & 0xff)] ^ t[7 * 256 + (v >> 56)];
@@ -201,6 +215,22 @@ __device__ __forceinline__ uint32_t xor3(uint32_t a, uint32_t b, uint32_t c) {
   return __builtin_amdgcn_bitop3_b32(a, b, c, 0x96);
 }
 
+// v times the constant of a nibble set t (16 x 16 words in LDS): one lookup per nibble of v.
+__device__ __forceinline__ uint64_t nib_mul(uint64_t v, const uint64_t* t) {
+  const uint32_t lo = (uint32_t)v, hi = (uint32_t)(v >> 32);
+  uint2 e[16];
+#pragma unroll
+  for (int k = 0; k < 16; ++k)
+    e[k] = *reinterpret_cast<const uint2*>(t + 16 * k + (((k < 8 ? lo : hi) >> (4 * (k & 7))) & 15));
+  uint32_t rl = 0, rh = 0;
+#pragma unroll
+  for (int k = 0; k < 16; k += 2) {
+    rl = xor3(rl, e[k].x, e[k + 1].x);
+    rh = xor3(rh, e[k].y, e[k + 1].y);
+  }
+  return (uint64_t)rh << 32 | rl;
+}
+
 __device__ __forceinline__ void crc_word4(uint32_t& lo, uint32_t& hi, uint32_t w, const char* tab, uint32_t L,
                                           const uint32_t (&sel)[4]) {
   const uint32_t x = lo ^ w;
@@ -218,19 +248,6 @@ typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
 // non-temporal buffer access.
 constexpr int kBufferWord3 = 0x00020000;
 constexpr int kBufferNt = 2;
-
-// Copy `words` words (a multiple of nthreads * kBatch) from global memory
-// into LDS with kBatch loads in flight per thread before their stores.
-template <int kBatch>
-__device__ inline void stage(uint64_t* lds, const uint64_t* __restrict__ src, int words, int nthreads) {
-  for (int base = 0; base < words; base += nthreads * kBatch) {
-    uint64_t v[kBatch];
-#pragma unroll
-    for (int j = 0; j < kBatch; ++j) v[j] = src[base + j * nthreads + threadIdx.x];
-#pragma unroll
-    for (int j = 0; j < kBatch; ++j) lds[base + j * nthreads + threadIdx.x] = v[j];
-  }
-}
 
 // n / d for 0 <= n < 2^31 by a multiply-high (Granlund and Montgomery,
 // 1994): s = ceil(log2 d), m = floor(2^32 (2^s - d) / d) + 1, and the
@@ -282,6 +299,13 @@ __device__ __forceinline__ uint64_t shfl_xor64(uint64_t v, int mask) {
   return (uint64_t)hi << 32 | lo;
 }
 
+// v of lane + d (lanes past the wave's end keep their own)
+__device__ __forceinline__ uint64_t shfl_down64(uint64_t v, int d) {
+  const uint32_t lo = (uint32_t)__shfl_down((int)(uint32_t)v, d);
+  const uint32_t hi = (uint32_t)__shfl_down((int)(uint32_t)(v >> 32), d);
+  return (uint64_t)hi << 32 | lo;
+}
+
 // Kernel 1: raw register of each span of the front-padded streams of
 // gridDim.x / spans_per_buf inputs (tensors) of `head` bytes each (a multiple
 // of 16), input i at data + i * buf_stride bytes (pool modes: the blob tensor
@@ -296,21 +320,18 @@ __global__ __launch_bounds__(kCrcThreads) void crc64_span_kernel(const u32x4* __
                                                                  int32_t spans_per_buf,
                                                                  uint64_t* __restrict__ partial, SpanShift sh,
                                                                  PoolSide ps_in) {
-  const uint64_t* tables = kConstTables.w;
-  // big: slicing tables 0..3 in kCopies replicas (128 KiB), then the lane-join levels 0..7;
-  // small: per-wave staging of one 1 KiB row (16 KiB) and the sub-chunk advance table (16 KiB), then
-  // the join registers and level 8.
+  // big: slicing tables 0..3 in kCopies replicas (128 KiB); once every wave has left the loop, the
+  // join's tables, the span placement's tables and the waves' registers (layout at the join).
+  // small: per-wave staging of one 1 KiB row (16 KiB), then the sub-chunk advance set (16 KiB).
   __shared__ __attribute__((aligned(16))) uint64_t big[4 * 256 * kCopies];
   __shared__ __attribute__((aligned(16))) uint64_t small[kStageWords + kTableWords];
-  static_assert(4 * 256 * kCopies == 8 * kTableWords, "join levels 0..7 fill the table region");
-  static_assert(kStageWords + kTableWords >= kCrcThreads + kTableWords, "join registers and level 8 fit");
   // The table words this thread places in LDS are loaded first; the LDS is filled once the first
   // sub-chunks' loads are also on their way (below), so their latency overlaps the fill.
   static_assert(4 * 256 == kCrcThreads, "one slicing entry per thread");
   static_assert(kTableWords == 2 * kCrcThreads, "two sub-chunk advance words per thread");
-  const uint64_t slice_word = tables[kSetSlice * kTableWords + threadIdx.x];
-  const uint64_t sub_word0 = tables[kSetSub * kTableWords + threadIdx.x];
-  const uint64_t sub_word1 = tables[kSetSub * kTableWords + kCrcThreads + threadIdx.x];
+  const uint64_t slice_word = kConstTables.slice[threadIdx.x];
+  const uint64_t sub_word0 = kConstTables.sub[threadIdx.x];
+  const uint64_t sub_word1 = kConstTables.sub[kCrcThreads + threadIdx.x];
   __builtin_amdgcn_sched_barrier(0);
   // this workgroup's input and span
   const int32_t buf_idx = (int32_t)blockIdx.x / spans_per_buf;
@@ -524,9 +545,6 @@ __global__ __launch_bounds__(kCrcThreads) void crc64_span_kernel(const u32x4* __
   // compiler's count of outstanding loads is exact on every path) and the rest of it is skipped.
   auto step = [&](int64_t sub, int c, int n) {
     const bool live = sub < span_subs;
-    // the advance of the running register by one sub-chunk (LDS lookups; they return while this
-    // sub-chunk's bytes are folded)
-    const uint64_t adv = lookup8(fold, t_sub);
     const int64_t ahead = sub + kDepth - 1;
     if (kMode == kGather) {
       // entries of sub + 1 were looked up a step ago into set n; set c's entries are free once sub's
@@ -552,6 +570,9 @@ __global__ __launch_bounds__(kCrcThreads) void crc64_span_kernel(const u32x4* __
       }
     }
     if (!live) return;
+    // the advance of the running register by one sub-chunk (LDS lookups; they return while this
+    // sub-chunk's bytes are folded)
+    const uint64_t adv = lookup8(fold, t_sub);
     u32x4 piece[kLoads];
     // (kGather) pieces of the front padding, only in a sub-chunk that starts before the data (the same
     // for the whole workgroup), are staged as zeros
@@ -586,47 +607,77 @@ __global__ __launch_bounds__(kCrcThreads) void crc64_span_kernel(const u32x4* __
 #pragma unroll
     for (int k = 0; k < kDepth; ++k) step(sub + k, k, (k + kDepth - 1) % kDepth);
   }
-  __syncthreads();   // every lane is done with the slicing tables and the staging area
-  uint64_t* acc = small;                                         // join registers
-  uint64_t* lvl8 = small + kCrcThreads;                          // level 8 (16 KiB)
-  uint64_t* lvl_tab = big;                                       // levels 0..7 (8 x 16 KiB)
-  acc[threadIdx.x] = fold;
-  stage<16>(lvl_tab, tables + kSetLane * kTableWords, 8 * kTableWords, kCrcThreads);
-  stage<2>(lvl8, tables + (kSetLane + 8) * kTableWords, kTableWords, kCrcThreads);
-  __syncthreads();
-  // join lanes t and t + s: the later group holds s lanes x kPiece bytes of every sub-chunk
-  for (int lvl = 0; lvl < kLaneLevels; ++lvl) {
-    const int s = 1 << lvl;
-    const int t = threadIdx.x;
-    if ((t & (2 * s - 1)) == 0) {
-      const uint64_t* tab = lvl < 8 ? lvl_tab + lvl * kTableWords
-                                    : lvl == 8 ? lvl8 : tables + (kSetLane + lvl) * kTableWords;
-      acc[t] = lookup8(acc[t], tab) ^ acc[t + s];
-    }
-    __syncthreads();
+  // Join the lanes: lanes t and t + s (the later s lanes x kPiece bytes of every sub-chunk) give t's
+  // register times x^(8 * kPiece * s) plus t + s's register, s = 1, 2, ..., 512 lanes: levels 0..5
+  // inside each wave by shuffles, levels 6..9 across the 16 waves, with the levels' nibble sets.
+  // Then the span's register times X^k, X = x^(8 * span), k = spans_per_buf - 1 - span_idx: its place
+  // in the input, so that the registers of an input's spans just XOR together.  One factor
+  // x^(8 * span * 2^b) per set bit b of k; wave b works out the basis of factor b (lane p holds
+  // x^(63 - p) times it) and turns it into the factor's nibble set.  The join's sets and the bases are
+  // loaded and worked out as each wave leaves the loop, while others may still be folding.
+  static_assert(kNibSets * kNibWords <= 3 * kCrcThreads, "three join words per thread");
+  uint64_t jw[3];
+#pragma unroll
+  for (int j = 0; j < 3; ++j) {
+    const int e = j * kCrcThreads + threadIdx.x;
+    jw[j] = e < kNibSets * kNibWords ? kConstTables.nib[e] : 0ull;
   }
-  // The span's register times X^k, X = x^(8 * span), k = spans_per_buf - 1 - span_idx: its place in
-  // the input, so that the registers of an input's spans just XOR together.  One factor
-  // x^(8 * span * 2^b) per set bit b of k, each a GF(2) product across a wave: lane p holds
-  // x^(63 - p) times the factor (the basis of mulmod), the product is the XOR over the set bits p of
-  // the register of lane p's word.  Wave b builds factor b's basis (the join's tables are free now).
   const int k = spans_per_buf - 1 - span_idx;
-  uint64_t* basis = big;
-  if (wave < kSpanLevels && ((k >> wave) & 1)) {
-    uint64_t v = sh.level[wave];
+  const bool place = wave < kSpanLevels && ((k >> wave) & 1);
+  uint64_t bw = 0;
+  if (place) {
+    bw = sh.level[wave];
     for (int it = 0; it < 63; ++it)
-      if (it < 63 - lane) v = mul_x(v);
-    basis[wave * 64 + lane] = v;
+      if (it < 63 - lane) bw = mul_x(bw);
+  }
+  __syncthreads();   // every lane is done with the slicing tables and the staging area
+  // big (words): [0, 2560) the join's nibble sets, [3072, 5120) the placement factors' nibble sets,
+  // [5120, 5632) their bases, [5632, 5648) the waves' registers
+  uint64_t* lane_nib = big;
+  uint64_t* place_nib = big + 3072;
+  uint64_t* basis = big + 5120;
+  uint64_t* wave_reg = big + 5632;
+  static_assert(kNibSets * kNibWords <= 3072 && 3072 + kSpanLevels * kNibWords <= 5120 &&
+                    5120 + kSpanLevels * 64 <= 5632 && 5632 + kWaves <= 4 * 256 * kCopies,
+                "join and placement layout fits the table region");
+#pragma unroll
+  for (int j = 0; j < 3; ++j) {
+    const int e = j * kCrcThreads + threadIdx.x;
+    if (e < kNibSets * kNibWords) lane_nib[e] = jw[j];
+  }
+  if (place) basis[wave * 64 + lane] = bw;
+  __syncthreads();
+  uint64_t acc = fold;
+#pragma unroll
+  for (int l = 0; l < 6; ++l) {
+    const uint64_t later = shfl_down64(acc, 1 << l);
+    acc = nib_mul(acc, lane_nib + l * kNibWords) ^ later;
+  }
+  if (lane == 0) wave_reg[wave] = acc;
+  if (place) {
+    // entries 4 lane .. 4 lane + 3 of factor `wave`'s nibble set: entry (q, n), q = lane / 4,
+    // n = 4 (lane % 4) + j, is the XOR of basis words 4q + i over the set bits i of n
+    const uint64_t* m = basis + wave * 64 + 4 * (lane >> 2);
+    const uint64_t m0 = m[0], m1 = m[1], m2 = m[2], m3 = m[3];
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const int n = 4 * (lane & 3) + j;
+      place_nib[wave * kNibWords + 4 * lane + j] =
+          ((n & 1) ? m0 : 0ull) ^ ((n & 2) ? m1 : 0ull) ^ ((n & 4) ? m2 : 0ull) ^ ((n & 8) ? m3 : 0ull);
+    }
   }
   __syncthreads();
   if (wave == 0) {
-    uint64_t r = acc[0];
-    for (int b = 0; b < kSpanLevels; ++b) {
-      if (!((k >> b) & 1)) continue;
-      uint64_t t = ((r >> lane) & 1) ? basis[b * 64 + lane] : 0ull;
-      for (int o = 32; o > 0; o >>= 1) t ^= shfl_xor64(t, o);
-      r = t;
+    // lanes 0..15 hold the waves' registers (wave w: bytes [4 KiB w, 4 KiB (w + 1)) of every sub-chunk)
+    uint64_t a = wave_reg[lane & (kWaves - 1)];
+#pragma unroll
+    for (int l = 6; l < kLaneLevels; ++l) {
+      const uint64_t later = shfl_down64(a, 1 << (l - 6));
+      a = nib_mul(a, lane_nib + l * kNibWords) ^ later;
     }
+    uint64_t r = a;
+    for (int bit = 0; bit < kSpanLevels; ++bit)
+      if ((k >> bit) & 1) r = nib_mul(r, place_nib + bit * kNibWords);
     if (lane == 0) partial[buf_idx * kMaxSpans + span_idx] = r;
   }
 }
@@ -689,7 +740,7 @@ __global__ __launch_bounds__(kMaxSpans) void crc64_finish_kernel(const uint64_t*
   __shared__ uint64_t crcs[2];
   static_assert(kMaxSpans == 256, "one slicing-table entry per lane");
   const int i = threadIdx.x, lane = i & 63, wave = i >> 6;
-  t0[i] = kConstTables.w[kSetSlice * kTableWords + i];           // slicing table 0
+  t0[i] = kConstTables.slice[i];                                  // slicing table 0
   for (int in = 0; in < a.inputs; ++in) {
     uint64_t v = i < a.spans ? partial[in * kMaxSpans + i] : 0ull;
     for (int o = 32; o > 0; o >>= 1) v ^= shfl_xor64(v, o);
