@@ -29,10 +29,12 @@
 //     buffer loads (the next two sub-chunks' in flight while this one is
 //     folded; a load in the front padding lies outside the buffer and returns
 //     zeros) and hands each lane its 64 bytes through an LDS staging area;
-//     lanes run them through slicing-by-4 tables held in LDS in 16 replicas
+//     lanes run them through slicing-by-4 tables held in LDS in 8 replicas
 //     arranged so that the 32 lanes an LDS cycle serves never share a bank
 //     (crc_word4), and advance their running register by one sub-chunk per
-//     step (a byte-table multiply); a tree of nibble-table multiplies joins
+//     step (a byte-table multiply, its tables in 4 replicas arranged the
+//     same way: no LDS lookup of the loop can conflict); a tree of
+//     nibble-table multiplies joins
 //     the lanes at the end of the span (inside each wave by shuffles, then
 //     across the 16 waves), and the span's register is multiplied into its
 //     place in the input (one nibble-table multiply per set bit of its
@@ -78,7 +80,8 @@ constexpr int64_t kMaxSpanSubs = 32767;                         // sub-chunks pe
 constexpr int kLaneLevels = 10;                                 // log2(kCrcThreads)
 constexpr int kSpanLevels = 8;                                  // log2(kMaxSpans)
 constexpr int kTableWords = 8 * 256;                            // one set of 8 byte tables (16 KiB)
-constexpr int kCopies = 16;                                     // LDS replicas of the slicing tables
+constexpr int kCopies = 8;                                      // LDS replicas of the slicing tables
+constexpr int kSubCopies = 4;                                   // LDS replicas of the advance's tables
 constexpr int kWaves = kCrcThreads / 64;
 constexpr int kStageWords = kWaves * 64 * 16 / 8;               // per-wave staging of one 1 KiB row
 constexpr int kNibWords = 16 * 16;                              // one nibble table set (2 KiB)
@@ -184,31 +187,22 @@ constexpr ConstTables make_const_tables() {
 
 __device__ const ConstTables kConstTables = make_const_tables();
 
-// v times the constant of a byte set t (8 x 256 words): one lookup per byte of v.
-__device__ __forceinline__ uint64_t lookup8(uint64_t v, const uint64_t* t) {
-  return t[0 * 256 + (v & 0xff)] ^ t[1 * 256 + ((v >> 8) & 0xff)] ^ t[2 * 256 + ((v >> 16) & 0xff)] ^
-         t[3 * 256 + ((v >> 24) & 0xff)] ^ t[4 * 256 + ((v >> 32) & 0xff)] ^ t[5 * 256 + ((v >> 40) & 0xff)] ^
-         t[6 * 256 + ((v >> 48) & 0xff)] ^ t[7 * 256 + (v >> 56)];
-}
 
 // Four bytes (little-endian word w) into the register (lo, hi) with
 // slicing-by-4 tables (the slicing-by-N method of Kounavis and Berry: one
 // table per byte position of the word, the byte's effect after the bytes
-// that follow it) held in LDS in kCopies = 16 replicas.  Layout (byte
-// offsets in the 128 KiB table region): tables 2h and 2h + 1 share the 64 KiB
-// region h; entry b of table t, replica r sits at h * 65536 + b * 256 +
-// (t % 2) * 128 + r * 8.  So, with the LDS's 64 four-byte banks, replica r of
-// an even table occupies only banks 2r and 2r + 1, and of an odd table banks
-// 32 + 2r and 33 + 2r.  A ds_read_b64 serves 32 lanes at a time; lanes r and
-// r + 16 of such a group share replica r, so they look up the two tables of a
-// pair in the opposite order (lanes 16..31 of every 32 take table t ^ 1 where
-// lanes 0..15 take table t): in every instruction the 32 lanes touch 64
+// that follow it) held in LDS in kCopies = 8 replicas.  Layout (byte offsets
+// in the 64 KiB table region): entry b of table t, replica r sits at
+// b * 256 + t * 64 + r * 8, so with the LDS's 64 four-byte banks each (table,
+// replica) pair owns banks 16t + 2r and 16t + 2r + 1 whatever the entry.  A
+// ds_read_b64 serves 32 lanes at a time; lane l of such a group uses replica
+// r = l % 8 and belongs to group g = (l / 8) % 4, and lookup k of group g
+// reads table (3 - k + g) % 4: in every instruction the 32 lanes touch 64
 // different banks whatever bytes they look up.  Every address is one byte
-// permute of the lane's L = r << 3 | (r << 3 | 128) << 8 | 1 << 24 (the two
-// half-row bytes, then the region bytes 0 and 1) and x = lo ^ w: sel[k] puts
-// the half byte of its table in byte 0, the looked-up byte of x in byte 1 and
-// the region in byte 2.  Byte 0 of the word is followed by 3 more bytes
-// (table 3), byte 3 by none (table 0).
+// permute of the lane's L (byte k: table and replica bytes of lookup k) and
+// x = lo ^ w: sel[k] puts L's byte k in byte 0 and the byte of x that table
+// looks up in byte 1.  Byte 0 of the word is followed by 3 more bytes (table
+// 3), byte 3 by none (table 0).
 // a ^ b ^ c in one instruction: gfx950's three-input bitwise operation, truth table 0x96 (bit i of
 // the table is the parity of i, the XOR of the three input bits).
 __device__ __forceinline__ uint32_t xor3(uint32_t a, uint32_t b, uint32_t c) {
@@ -225,6 +219,35 @@ __device__ __forceinline__ uint64_t nib_mul(uint64_t v, const uint64_t* t) {
   uint32_t rl = 0, rh = 0;
 #pragma unroll
   for (int k = 0; k < 16; k += 2) {
+    rl = xor3(rl, e[k].x, e[k + 1].x);
+    rh = xor3(rh, e[k].y, e[k + 1].y);
+  }
+  return (uint64_t)rh << 32 | rl;
+}
+
+// v times the sub-chunk advance: one lookup per byte of v in the advance's byte set, held in LDS in
+// kSubCopies = 4 replicas.  Layout (byte offsets in its 64 KiB region): entry b of table t (the table
+// of byte t of v), replica r sits at b * 256 + t * 32 + r * 8, so each (table, replica) pair owns one
+// pair of the 64 four-byte banks whatever the entry.  Of the 32 lanes an LDS cycle serves, lane l
+// uses replica r = l % 4 and belongs to group g = (l / 4) % 8, and lookup k of group g reads table
+// (k + g) % 8: in every instruction the 32 lanes sit in 32 different bank pairs.  The lane first
+// rotates v right by 8g bits (swap the words when g >= 4, then align by 8 (g % 4)), so lookup k
+// always takes byte k of the rotated value; its address is then one byte permute of that word and
+// the lane's la / lb (byte k % 4: (32 k + 32 g + 8 r) mod 256, the table and replica bytes).
+__device__ __forceinline__ uint64_t sub_advance(uint64_t v, const char* t, uint32_t la, uint32_t lb, bool swap,
+                                            uint32_t sh) {
+  const uint32_t lo = (uint32_t)v, hi = (uint32_t)(v >> 32);
+  const uint32_t a = swap ? hi : lo, b = swap ? lo : hi;
+  const uint32_t w[2] = {__builtin_amdgcn_alignbit(b, a, sh), __builtin_amdgcn_alignbit(a, b, sh)};
+  uint2 e[8];
+#pragma unroll
+  for (int k = 0; k < 8; ++k) {
+    const uint32_t sel = 0x0c0c0000u | (uint32_t)(k & 3) << 8 | (uint32_t)(4 + (k & 3));
+    e[k] = *reinterpret_cast<const uint2*>(t + __builtin_amdgcn_perm(k < 4 ? la : lb, w[k >> 2], sel));
+  }
+  uint32_t rl = 0, rh = 0;
+#pragma unroll
+  for (int k = 0; k < 8; k += 2) {
     rl = xor3(rl, e[k].x, e[k + 1].x);
     rh = xor3(rh, e[k].y, e[k + 1].y);
   }
@@ -320,18 +343,27 @@ __global__ __launch_bounds__(kCrcThreads) void crc64_span_kernel(const u32x4* __
                                                                  int32_t spans_per_buf,
                                                                  uint64_t* __restrict__ partial, SpanShift sh,
                                                                  PoolSide ps_in) {
-  // big: slicing tables 0..3 in kCopies replicas (128 KiB); once every wave has left the loop, the
-  // join's tables, the span placement's tables and the waves' registers (layout at the join).
-  // small: per-wave staging of one 1 KiB row (16 KiB), then the sub-chunk advance set (16 KiB).
-  __shared__ __attribute__((aligned(16))) uint64_t big[4 * 256 * kCopies];
-  __shared__ __attribute__((aligned(16))) uint64_t small[kStageWords + kTableWords];
+  // One LDS block, laid out by hand so the slicing tables start below 64 KiB (their lookups' table
+  // offset then fits the LDS instructions' 16-bit offset field: no address add per lookup):
+  // stage_lds: per-wave staging of one 1 KiB row (16 KiB);
+  // big: slicing tables 0..3 in kCopies replicas (64 KiB); once every wave has left the loop, the
+  // join's tables, the span placement's tables and the waves' registers (layout at the join);
+  // sub_lds: the sub-chunk advance's 8 tables in kSubCopies replicas (64 KiB; one OR per lookup).
+  __shared__ __attribute__((aligned(16))) uint64_t lds[4 * 256 * kCopies + kTableWords * kSubCopies + kStageWords];
+  uint64_t* const stage_lds = lds;
+  uint64_t* const big = lds + kStageWords;
+  uint64_t* const sub_lds = big + 4 * 256 * kCopies;
   // The table words this thread places in LDS are loaded first; the LDS is filled once the first
-  // sub-chunks' loads are also on their way (below), so their latency overlaps the fill.
+  // sub-chunks' loads are also on their way (below), so their latency overlaps the fill.  Thread e
+  // places entry e / 4 of slicing table e % 4 and entries (e + 1024 j) / 8 of advance table e % 8
+  // (j = 0, 1), so a wave's 32-lane halves write 32 different bank pairs at every step of the fill.
   static_assert(4 * 256 == kCrcThreads, "one slicing entry per thread");
   static_assert(kTableWords == 2 * kCrcThreads, "two sub-chunk advance words per thread");
-  const uint64_t slice_word = kConstTables.slice[threadIdx.x];
-  const uint64_t sub_word0 = kConstTables.sub[threadIdx.x];
-  const uint64_t sub_word1 = kConstTables.sub[kCrcThreads + threadIdx.x];
+  const uint32_t fill_t = threadIdx.x & 3, fill_b = threadIdx.x >> 2;
+  const uint32_t fill_u = threadIdx.x & 7, fill_c = threadIdx.x >> 3;
+  const uint64_t slice_word = kConstTables.slice[fill_t * 256 + fill_b];
+  const uint64_t sub_word0 = kConstTables.sub[fill_u * 256 + fill_c];
+  const uint64_t sub_word1 = kConstTables.sub[fill_u * 256 + fill_c + kCrcThreads / 8];
   __builtin_amdgcn_sched_barrier(0);
   // this workgroup's input and span
   const int32_t buf_idx = (int32_t)blockIdx.x / spans_per_buf;
@@ -341,24 +373,36 @@ __global__ __launch_bounds__(kCrcThreads) void crc64_span_kernel(const u32x4* __
   if (kMode != kStream) ps.blob += buf_idx * (buf_stride / 16);
   data += buf_idx * (buf_stride / 16);
   const char* tab = reinterpret_cast<const char*>(big);
-  // this lane's replica bytes and the permute selectors of crc_word4's four lookups: lookup k reads
-  // table (3 - k) ^ grp (selector bytes: 4 + half -> L.b0 / L.b1, 3 - t -> x.b(3 - t), 6 + region
-  // -> L.b2 / L.b3, 0x0c -> zero)
-  const uint32_t rr = (threadIdx.x % kCopies) << 3;
-  const uint32_t L = rr | (rr | 128u) << 8 | 1u << 24;
-  const uint32_t grp = (threadIdx.x >> 4) & 1;                     // lanes 16..31 of every 32
+  // this lane's table-and-replica bytes and the permute selectors of crc_word4's four lookups:
+  // lookup k reads table t = (3 - k + g) % 4 (selector bytes: 4 + k -> L.b(k), 3 - t -> x.b(3 - t),
+  // 0x0c -> zero)
+  static_assert(kCopies == 8, "8 replicas x 4 groups = the 32 lanes of an LDS cycle");
+  const uint32_t rep8 = threadIdx.x & 7, grp4 = (threadIdx.x >> 3) & 3;
+  uint32_t L = 0;
   uint32_t sel[4];
 #pragma unroll
   for (int k = 0; k < 4; ++k) {
-    const uint32_t t = (uint32_t)(3 - k) ^ grp;
-    sel[k] = 0x0c000000u | (6u + (t >> 1)) << 16 | (3u - t) << 8 | (4u + (t & 1));
+    const uint32_t t = (3u - (uint32_t)k + grp4) & 3u;
+    L |= (t * 64u + rep8 * 8u) << (8 * k);
+    sel[k] = 0x0c0c0000u | (3u - t) << 8 | (4u + (uint32_t)k);
+  }
+  // the advance's lane constants (layout at sub_advance): replica l % 4, group (l / 4) % 8
+  static_assert(kSubCopies == 4, "4 replicas x 8 groups = the 32 lanes of an LDS cycle");
+  const uint32_t rep4 = threadIdx.x & 3, grp8 = (threadIdx.x >> 2) & 7;
+  const bool adv_swap = grp8 >= 4;
+  const uint32_t adv_sh = 8u * (grp8 & 3u);
+  uint32_t adv_la = 0, adv_lb = 0;
+#pragma unroll
+  for (int k = 0; k < 4; ++k) {
+    adv_la |= ((32u * (uint32_t)k + 32u * grp8 + 8u * rep4) & 255u) << (8 * k);
+    adv_lb |= ((32u * (uint32_t)(k + 4) + 32u * grp8 + 8u * rep4) & 255u) << (8 * k);
   }
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   // this wave's 1 KiB staging area: one row of 64 16-byte slots, used once per row of the wave's
   // 4 KiB of a sub-chunk; slot l holds the row's bytes [16 l, +16) at position l ^ ((l >> 4) & 3),
   // which keeps both the row writes and the lane-piece reads free of bank conflicts
-  u32x4* stage_area = reinterpret_cast<u32x4*>(small) + wave * 64;
-  const uint64_t* t_sub = small + kStageWords;                     // the sub-chunk advance (LDS)
+  u32x4* stage_area = reinterpret_cast<u32x4*>(stage_lds) + wave * 64;
+  const char* t_sub = reinterpret_cast<const char*>(sub_lds);      // the sub-chunk advance (LDS)
   // this lane's 16-byte column within a sub-chunk, and the first sub-chunk's data offset
   const int32_t local = wave * 64 * kPiece + 16 * lane;
   const int64_t span0 = (int64_t)span_idx * span_subs * kSub - pad;
@@ -527,16 +571,19 @@ __global__ __launch_bounds__(kCrcThreads) void crc64_span_kernel(const u32x4* __
     if (kMode == kScatter) entries(pg[0], pos);
   }
   {
-    // thread e writes entry b = e mod 256 of slicing table t = e / 256 into every replica (layout at
-    // crc_word4), replica (i + lane) % kCopies at step i, so a wave's writes spread over the banks
-    static_assert(kCopies == 16, "16 replicas of 8 bytes fill a 128-byte half row");
-    const int t = threadIdx.x >> 8, b = threadIdx.x & 255;
-    char* row = reinterpret_cast<char*>(big) + (t >> 1) * 65536 + b * 256 + (t & 1) * 128;
+    // every replica of this thread's entries (layouts at crc_word4 and sub_advance), replica
+    // (i + lane / 4) % 8 resp. (i + lane / 8) % 4 at step i
+    char* srow = reinterpret_cast<char*>(big) + fill_b * 256 + fill_t * 64;
 #pragma unroll
     for (int i = 0; i < kCopies; ++i)
-      *reinterpret_cast<uint64_t*>(row + ((i + threadIdx.x) % kCopies) * 8) = slice_word;
-    small[kStageWords + threadIdx.x] = sub_word0;
-    small[kStageWords + kCrcThreads + threadIdx.x] = sub_word1;
+      *reinterpret_cast<uint64_t*>(srow + ((i + (threadIdx.x >> 2)) & (kCopies - 1)) * 8) = slice_word;
+    char* arow = reinterpret_cast<char*>(sub_lds) + fill_c * 256 + fill_u * 32;
+#pragma unroll
+    for (int i = 0; i < kSubCopies; ++i) {
+      const int r = (i + (threadIdx.x >> 3)) & (kSubCopies - 1);
+      *reinterpret_cast<uint64_t*>(arow + r * 8) = sub_word0;
+      *reinterpret_cast<uint64_t*>(arow + (kCrcThreads / 8) * 256 + r * 8) = sub_word1;
+    }
   }
   __syncthreads();
   // One step: fold sub-chunk `sub` (set c) while the loads of sub-chunk sub + kDepth - 1 go into set n
@@ -571,8 +618,9 @@ __global__ __launch_bounds__(kCrcThreads) void crc64_span_kernel(const u32x4* __
     }
     if (!live) return;
     // the advance of the running register by one sub-chunk (LDS lookups; they return while this
-    // sub-chunk's bytes are folded)
-    const uint64_t adv = lookup8(fold, t_sub);
+    // sub-chunk's bytes are folded; the sender, shortest of registers, takes it after the fold)
+    uint64_t adv = 0;
+    if (kMode != kGather) adv = sub_advance(fold, t_sub, adv_la, adv_lb, adv_swap, adv_sh);
     u32x4 piece[kLoads];
     // (kGather) pieces of the front padding, only in a sub-chunk that starts before the data (the same
     // for the whole workgroup), are staged as zeros
@@ -601,6 +649,7 @@ __global__ __launch_bounds__(kCrcThreads) void crc64_span_kernel(const u32x4* __
       crc_word4(lo, hi, piece[j].z, tab, L, sel);
       crc_word4(lo, hi, piece[j].w, tab, L, sel);
     }
+    if (kMode == kGather) adv = sub_advance(fold, t_sub, adv_la, adv_lb, adv_swap, adv_sh);
     fold = adv ^ ((uint64_t)hi << 32 | lo);
   };
   for (int64_t sub = 0; sub < span_subs; sub += kDepth) {
