@@ -135,7 +135,7 @@ def parse():
                          "(the same pages, each request's in ascending pool order), consecutive (each request's "
                          "pages one contiguous run of the pool)")
     ap.add_argument("--no-configs", dest="configs", action="store_false",
-                    help="skip the batched configurations (batch of 8, MLA, re-blocking) of the default run")
+                    help="skip the other full-size configurations (Llama-3-8B, batch of 8, MLA, re-blocking) of the default run")
     ap.add_argument("--threads", type=int, default=0,
                     help="threaded host baseline: thread count (0: sweep powers of two up to the cores)")
     ap.add_argument("--kernel-events", action="store_true",
@@ -923,13 +923,14 @@ def run(args):
 
 
 def config_block(args, topkv):
-    """The batched configurations (70B batch of 8, DeepSeek-V3 MLA, 70B
-    re-blocking 16 -> 64) timed in the same run: a few graph-replayed steps
-    under each issue mode, pools freed between workloads."""
+    """The other full-size configurations (Llama-3-8B one 4096-token request,
+    70B batch of 8, DeepSeek-V3 MLA, 70B re-blocking 16 -> 64) timed in the
+    same run: a few graph-replayed steps under each issue mode, pools freed
+    between workloads."""
     import torch
     from paper_2607_28633_amd.workloads import make_workload
     res = {}
-    for name in ("llama3-70b-batch8", "deepseek-v3-mla", "reblock-70b"):
+    for name in ("llama3-8b", "llama3-70b-batch8", "deepseek-v3-mla", "reblock-70b"):
         wl = make_workload(name)
         log(f"[bench] config {name}")
         st = Setup(wl, topkv)
