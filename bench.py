@@ -681,10 +681,14 @@ def ceiling(setup, steps):
     every length 0, the hand-written streaming copy of one layer's packed
     bytes per launch into each layer's own slot, that copy at 64 MiB, 256 MiB
     and 1 GiB, a read-only pass over the same sources at the same sizes
-    (the ceiling of a checksum pass), and the layer engine's schedule
+    (the ceiling of a checksum pass), the layer engine's schedule
     without tables
     (topkv_ceiling_copy_layers: pool slab prefixes -> packed slots -> a
-    second pool's slab prefixes, one launch per direction)."""
+    second pool's slab prefixes, one launch per direction), and the same
+    transfer over the workload's own scattered pages with the tables'
+    lookups done beforehand (topkv_ceiling_copy_tiles: every 32 KiB page
+    plane from its pool page to its packed slot and on to its destination
+    page, one launch per direction)."""
     import numpy as np
     import torch
 
@@ -770,6 +774,53 @@ def ceiling(setup, steps):
     out["copy_layers_engine_schedule"] = {
         "layers": lay, "bytes_per_layer": 2 * n, "read_us_per_layer": round(t[0], 3),
         "write_us_per_layer": round(t[1], 3), "step_gbs": round(4 * n / (t[0] + t[1]) / 1e3, 1)}
+    # the same scattered pages with the table lookups and length arithmetic taken out: one 32 KiB
+    # tile per workgroup, every tile's pool and packed offsets worked out here from the block tables
+    # (full pages of planes that are whole tiles), one launch per direction over every layer,
+    # alternating as the step does
+    row = wl.num_heads * wl.head_dim * wl.elem_bytes
+    plane = wl.page_size * row
+    if plane % 32768 == 0 and wl.dst_page_size == wl.page_size and not wl.layer_windows and not wl.layer_state:
+        tpp = plane // 32768
+        tok0 = np.concatenate([[0], np.cumsum(wl.seq_lens.astype(np.int64))])
+        so, po, do = [], [], []
+        for l in range(L):
+            slab, base = wl.kv_slab(l), (l % setup.ring) * setup.slice
+            for r in range(R):
+                nr = int(wl.seq_lens[r])
+                for i in range(nr // wl.page_size):
+                    p1, p2 = int(wl.block_tables[r, i]), int(wl.dst_block_tables[r, i])
+                    for c in range(wl.planes):
+                        for t in range(tpp):
+                            so.append(((slab * wl.num_pages + p1) * wl.planes + c) * plane + t * 32768)
+                            do.append(((slab * wl.dst_num_pages + p2) * wl.planes + c) * plane + t * 32768)
+                            po.append(base + (int(tok0[r]) * wl.planes + c * nr + i * wl.page_size) * row + t * 32768)
+        so_t, po_t, do_t = (torch.tensor(x, dtype=torch.int64, device="cuda") for x in (so, po, do))
+        T = len(so)
+        nb = lambda x: x.numel() * x.element_size()
+        pk = lambda: cl.topkv_ceiling_copy_tiles(setup.src, nb(setup.src), so_t, setup.packed, nb(setup.packed), po_t,
+                                                 T, None)
+        up = lambda: cl.topkv_ceiling_copy_tiles(setup.packed, nb(setup.packed), po_t, setup.dst, nb(setup.dst), do_t,
+                                                 T, None)
+        for _ in range(2):
+            pk()
+            up()
+        torch.cuda.synchronize()
+        m = [[tk.HipEvent() for _ in range(3)] for _ in range(reps)]
+        for k in range(reps):
+            m[k][0].record(stream)
+            pk()
+            m[k][1].record(stream)
+            up()
+            m[k][2].record(stream)
+        m[-1][2].synchronize()
+        t = [1e3 * sum(m[k][d].elapsed_ms(m[k][d + 1]) for k in range(reps)) / reps for d in (0, 1)]
+        moved = 2 * T * 32768
+        out["copy_tiles_scattered_pages"] = {
+            "tiles_per_direction": T, "bytes_per_direction": moved, "pack_like_us": round(t[0], 2),
+            "unpack_like_us": round(t[1], 2), "pack_like_gbs": round(moved / t[0] / 1e3, 1),
+            "unpack_like_gbs": round(moved / t[1] / 1e3, 1), "step_gbs": round(2 * moved / (t[0] + t[1]) / 1e3, 1)}
+        del so_t, po_t, do_t
     # one layer's copy stamped per workgroup: first start to last store completion vs the launch's events
     tiles = -(-n // 32768)
     stamps = torch.zeros(3 * tiles, dtype=torch.int64, device="cuda")

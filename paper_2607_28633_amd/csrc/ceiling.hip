@@ -76,6 +76,19 @@ __global__ __launch_bounds__(kThreads) void ceiling_read_kernel(const V* __restr
   if (threadIdx.x == 0) sink[blockIdx.x] = part[0] ^ part[1] ^ part[2] ^ part[3];
 }
 
+// Tile w: 32 KiB from src + src_off[w] to dst + dst_off[w] (byte offsets); a tile whose offsets are
+// not 16-byte aligned or whose 32 KiB would leave either buffer is skipped.
+__global__ __launch_bounds__(kThreads) void ceiling_copy_tiles_kernel(const char* __restrict__ src, int64_t src_bytes,
+                                                                      const int64_t* __restrict__ src_off,
+                                                                      char* __restrict__ dst, int64_t dst_bytes,
+                                                                      const int64_t* __restrict__ dst_off) {
+  const int64_t so = src_off[blockIdx.x], d0 = dst_off[blockIdx.x];
+  if (((so | d0) & 15) || so < 0 || d0 < 0 || so > src_bytes - kTile || d0 > dst_bytes - kTile) return;
+  V v[kVpt];
+  load_tile(v, reinterpret_cast<const V*>(src + so), 0, kTile / 16);
+  store_tile(v, reinterpret_cast<V*>(dst + d0), 0, kTile / 16);
+}
+
 __global__ void ceiling_empty_kernel() {}
 
 __global__ __launch_bounds__(kThreads) void ceiling_timeline_kernel(const V* __restrict__ s, V* __restrict__ d,
@@ -154,6 +167,19 @@ topkv_status_t topkv_ceiling_read(const void* src, int64_t bytes, uint32_t* sink
   if (tiles > INT32_MAX) return TOPKV_ERR_UNSUPPORTED;
   hipLaunchKernelGGL(ceiling_read_kernel, dim3((unsigned)tiles), dim3(kThreads), 0, stream,
                      static_cast<const V*>(src), bytes / 16, sink);
+  return hipGetLastError() == hipSuccess ? TOPKV_OK : TOPKV_ERR_LAUNCH;
+}
+
+topkv_status_t topkv_ceiling_copy_tiles(const void* src, int64_t src_bytes, const int64_t* src_off, void* dst,
+                                        int64_t dst_bytes, const int64_t* dst_off, int32_t tiles,
+                                        hipStream_t stream) {
+  using namespace topkv_ceiling;
+  if (!src || !dst || !src_off || !dst_off || src_bytes < 0 || dst_bytes < 0 || tiles < 0 || !aligned(src) ||
+      !aligned(dst))
+    return TOPKV_ERR_INVALID_ARG;
+  if (tiles == 0) return TOPKV_OK;
+  hipLaunchKernelGGL(ceiling_copy_tiles_kernel, dim3((unsigned)tiles), dim3(kThreads), 0, stream,
+                     static_cast<const char*>(src), src_bytes, src_off, static_cast<char*>(dst), dst_bytes, dst_off);
   return hipGetLastError() == hipSuccess ? TOPKV_OK : TOPKV_ERR_LAUNCH;
 }
 

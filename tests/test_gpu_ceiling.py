@@ -1,8 +1,10 @@
 """The measurement kernels the bench reads the product against
 (libtopkv_ceiling.so) do what they are reported as: the copies move exactly
 the bytes named (ragged sizes too, nothing past them), the engine-schedule
-copy moves every layer between its own strided blocks, the read-only pass
-writes each 32 KiB tile's XOR, and the timeline's stamps are ordered."""
+copy moves every layer between its own strided blocks, the scattered-tile
+copy moves each 32 KiB tile between the offsets it is given and skips tiles
+whose offsets are misaligned or out of range, the read-only pass writes each
+32 KiB tile's XOR, and the timeline's stamps are ordered."""
 import numpy as np
 import pytest
 import torch
@@ -44,6 +46,28 @@ def test_copy_layers_engine_schedule(cl):
         for z in range(layers):
             assert torch.equal(dst[z * ds:z * ds + lb], src[z * ss:z * ss + lb]), (per_cu, z)
             assert (dst[z * ds + lb:(z + 1) * ds] == 0x3C).all(), (per_cu, z)
+
+
+def test_copy_tiles_follows_the_offsets(cl):
+    n_src, n_dst, tiles = 40 * TILE + 48, 30 * TILE + 16, 24
+    src = _bytes(n_src, 4)
+    dst = torch.full((n_dst,), 0x5A, dtype=torch.uint8, device="cuda")
+    rng = np.random.default_rng(9)
+    so = rng.integers(0, (n_src - TILE) // 16, size=tiles) * 16
+    do = rng.permutation(np.arange(0, (n_dst - TILE) // TILE + 1) * TILE)[:tiles - 4]   # non-overlapping
+    do = np.concatenate([do, [8, n_dst - TILE + 16, -TILE, n_dst]])   # misaligned, past the end, negative, past
+    so[-1] = n_src - TILE + 32                                            # source past the end
+    so_t, do_t = torch.tensor(so, device="cuda"), torch.tensor(do, device="cuda")
+    cl.topkv_ceiling_copy_tiles(src, n_src, so_t, dst, n_dst, do_t, tiles)
+    torch.cuda.synchronize()
+    want = np.full(n_dst, 0x5A, dtype=np.uint8)
+    h = src.cpu().numpy()
+    for k in range(tiles):
+        s0, d0 = int(so[k]), int(do[k])
+        if (s0 | d0) % 16 or s0 < 0 or d0 < 0 or s0 > n_src - TILE or d0 > n_dst - TILE:
+            continue
+        want[d0:d0 + TILE] = h[s0:s0 + TILE]
+    assert np.array_equal(dst.cpu().numpy(), want)
 
 
 @pytest.mark.parametrize("n", [16, TILE, 3 * TILE + 4096 + 16, (8 << 20) + 160])
