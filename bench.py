@@ -674,6 +674,84 @@ def verify_layers(wl, ring):
     return sorted({cand[0], cand[len(cand) // 2], cand[-1]})
 
 
+def scattered_tiles(setup, direction):
+    """Tiles of at most 32 KiB covering one direction's page runs over every
+    layer, as (pool offsets, packed offsets, lengths) in bytes: pack from the
+    source pool's pages (block_tables, page_size), unpack into the
+    destination pool's (dst_block_tables, dst_page_size); packed offsets in
+    the bench's ring of layer slots.  None for windowed or fixed-state
+    workloads."""
+    import numpy as np
+    wl = setup.wl
+    if wl.layer_windows or wl.layer_state:
+        return None
+    row = wl.num_heads * wl.head_dim * wl.elem_bytes
+    tables, P, npages = ((wl.block_tables, wl.page_size, wl.num_pages) if direction == 0
+                         else (wl.dst_block_tables, wl.dst_page_size, wl.dst_num_pages))
+    plane = P * row
+    pool_rel, pk_rel, lens = [], [], []
+    tok0 = 0
+    for r in range(wl.num_reqs):
+        n = int(wl.seq_lens[r])
+        npg = -(-n // P)
+        i = np.arange(npg, dtype=np.int64)
+        run = (np.minimum(n, (i + 1) * P) - i * P) * row
+        nt = -(-run // 32768)
+        ii = np.repeat(i, nt)
+        tt = np.arange(int(nt.sum()), dtype=np.int64) - np.repeat(np.cumsum(nt) - nt, nt)
+        pages = tables[r, :npg].astype(np.int64)[ii]
+        for c in range(wl.planes):
+            pool_rel.append((pages * wl.planes + c) * plane + tt * 32768)
+            pk_rel.append((tok0 * wl.planes + c * n + ii * P) * row + tt * 32768)
+            lens.append(np.minimum(32768, run[ii] - tt * 32768))
+        tok0 += n
+    pool_rel, pk_rel, lens = (np.concatenate(x) for x in (pool_rel, pk_rel, lens))
+    layer_pool = np.array([wl.kv_slab(l) * npages * wl.planes * plane for l in range(wl.num_layers)], dtype=np.int64)
+    layer_pk = np.array([(l % setup.ring) * setup.slice for l in range(wl.num_layers)], dtype=np.int64)
+    return ((layer_pool[:, None] + pool_rel[None, :]).reshape(-1), (layer_pk[:, None] + pk_rel[None, :]).reshape(-1),
+            np.tile(lens, wl.num_layers).astype(np.int32))
+
+
+def scattered_copy(setup, reps):
+    """The workload's transfer with the table lookups and the length
+    arithmetic done beforehand (topkv_ceiling_copy_tiles over scattered_tiles):
+    pool pages -> packed slots, then packed slots -> destination pages, one
+    launch per direction, alternating as the step does."""
+    import torch
+
+    from paper_2607_28633_amd import ceiling as cl
+    tk = setup.tk
+    sides = [scattered_tiles(setup, d) for d in (0, 1)]
+    if sides[0] is None or any(len(x[0]) > 2**31 - 1 for x in sides):
+        return None
+    dev = [[torch.from_numpy(a).cuda() for a in x] for x in sides]
+    nb = lambda x: x.numel() * x.element_size()
+    pk = lambda: cl.topkv_ceiling_copy_tiles(setup.src, nb(setup.src), dev[0][0], setup.packed, nb(setup.packed),
+                                             dev[0][1], dev[0][2], len(sides[0][0]), None)
+    up = lambda: cl.topkv_ceiling_copy_tiles(setup.packed, nb(setup.packed), dev[1][1], setup.dst, nb(setup.dst),
+                                             dev[1][0], dev[1][2], len(sides[1][0]), None)
+    stream = torch.cuda.current_stream()
+    for _ in range(2):
+        pk()
+        up()
+    torch.cuda.synchronize()
+    m = [[tk.HipEvent() for _ in range(3)] for _ in range(reps)]
+    for k in range(reps):
+        m[k][0].record(stream)
+        pk()
+        m[k][1].record(stream)
+        up()
+        m[k][2].record(stream)
+    m[-1][2].synchronize()
+    t = [1e3 * sum(m[k][d].elapsed_ms(m[k][d + 1]) for k in range(reps)) / reps for d in (0, 1)]
+    moved = [2 * int(sides[d][2].astype("int64").sum()) for d in (0, 1)]
+    del dev
+    return {"tiles": [len(sides[0][0]), len(sides[1][0])], "bytes": moved,
+            "pack_like_us": round(t[0], 2), "unpack_like_us": round(t[1], 2),
+            "pack_like_gbs": round(moved[0] / t[0] / 1e3, 1), "unpack_like_gbs": round(moved[1] / t[1] / 1e3, 1),
+            "step_gbs": round((moved[0] + moved[1]) / (t[0] + t[1]) / 1e3, 1)}
+
+
 def ceiling(setup, steps):
     """The practical ceiling and floor on this machine, measured like the
     headline (graph replays of L launches, or one launch per direction, with
@@ -774,53 +852,9 @@ def ceiling(setup, steps):
     out["copy_layers_engine_schedule"] = {
         "layers": lay, "bytes_per_layer": 2 * n, "read_us_per_layer": round(t[0], 3),
         "write_us_per_layer": round(t[1], 3), "step_gbs": round(4 * n / (t[0] + t[1]) / 1e3, 1)}
-    # the same scattered pages with the table lookups and length arithmetic taken out: one 32 KiB
-    # tile per workgroup, every tile's pool and packed offsets worked out here from the block tables
-    # (full pages of planes that are whole tiles), one launch per direction over every layer,
-    # alternating as the step does
-    row = wl.num_heads * wl.head_dim * wl.elem_bytes
-    plane = wl.page_size * row
-    if plane % 32768 == 0 and wl.dst_page_size == wl.page_size and not wl.layer_windows and not wl.layer_state:
-        tpp = plane // 32768
-        tok0 = np.concatenate([[0], np.cumsum(wl.seq_lens.astype(np.int64))])
-        so, po, do = [], [], []
-        for l in range(L):
-            slab, base = wl.kv_slab(l), (l % setup.ring) * setup.slice
-            for r in range(R):
-                nr = int(wl.seq_lens[r])
-                for i in range(nr // wl.page_size):
-                    p1, p2 = int(wl.block_tables[r, i]), int(wl.dst_block_tables[r, i])
-                    for c in range(wl.planes):
-                        for t in range(tpp):
-                            so.append(((slab * wl.num_pages + p1) * wl.planes + c) * plane + t * 32768)
-                            do.append(((slab * wl.dst_num_pages + p2) * wl.planes + c) * plane + t * 32768)
-                            po.append(base + (int(tok0[r]) * wl.planes + c * nr + i * wl.page_size) * row + t * 32768)
-        so_t, po_t, do_t = (torch.tensor(x, dtype=torch.int64, device="cuda") for x in (so, po, do))
-        T = len(so)
-        nb = lambda x: x.numel() * x.element_size()
-        pk = lambda: cl.topkv_ceiling_copy_tiles(setup.src, nb(setup.src), so_t, setup.packed, nb(setup.packed), po_t,
-                                                 T, None)
-        up = lambda: cl.topkv_ceiling_copy_tiles(setup.packed, nb(setup.packed), po_t, setup.dst, nb(setup.dst), do_t,
-                                                 T, None)
-        for _ in range(2):
-            pk()
-            up()
-        torch.cuda.synchronize()
-        m = [[tk.HipEvent() for _ in range(3)] for _ in range(reps)]
-        for k in range(reps):
-            m[k][0].record(stream)
-            pk()
-            m[k][1].record(stream)
-            up()
-            m[k][2].record(stream)
-        m[-1][2].synchronize()
-        t = [1e3 * sum(m[k][d].elapsed_ms(m[k][d + 1]) for k in range(reps)) / reps for d in (0, 1)]
-        moved = 2 * T * 32768
-        out["copy_tiles_scattered_pages"] = {
-            "tiles_per_direction": T, "bytes_per_direction": moved, "pack_like_us": round(t[0], 2),
-            "unpack_like_us": round(t[1], 2), "pack_like_gbs": round(moved / t[0] / 1e3, 1),
-            "unpack_like_gbs": round(moved / t[1] / 1e3, 1), "step_gbs": round(2 * moved / (t[0] + t[1]) / 1e3, 1)}
-        del so_t, po_t, do_t
+    sp = scattered_copy(setup, reps)
+    if sp:
+        out["copy_tiles_scattered_pages"] = sp
     # one layer's copy stamped per workgroup: first start to last store completion vs the launch's events
     tiles = -(-n // 32768)
     stamps = torch.zeros(3 * tiles, dtype=torch.int64, device="cuda")
@@ -976,8 +1010,9 @@ def run(args):
 def config_block(args, topkv):
     """The other full-size configurations (Llama-3-8B one 4096-token request,
     70B batch of 8, DeepSeek-V3 MLA, 70B re-blocking 16 -> 64) timed in the
-    same run: a few graph-replayed steps under each issue mode, pools freed
-    between workloads."""
+    same run: a few graph-replayed steps under each issue mode, and the
+    table-free copy over the same scattered pages (scattered_copy); pools
+    freed between workloads."""
     import torch
     from paper_2607_28633_amd.workloads import make_workload
     res = {}
@@ -1000,6 +1035,8 @@ def config_block(args, topkv):
             v = step_gbs(wl, ms)
             entry[issue] = {"value": round(v, 1), "pct_of_peak": round(100 * v / HBM_PEAK_GBS, 2),
                             "ms_per_step": round(ms, 4), "kernels": kern}
+        # the ceiling of the same transfer over the same scattered pages (table lookups done beforehand)
+        entry["scattered_copy"] = scattered_copy(st, max(3, steps))
         res[name] = entry
         del st
         torch.cuda.empty_cache()

@@ -48,17 +48,19 @@ topkv_status_t topkv_ceiling_copy_layers(const void* src, int64_t src_stride, vo
  * words): the read-only ceiling a checksum pass is read against. */
 topkv_status_t topkv_ceiling_read(const void* src, int64_t bytes, uint32_t* sink, hipStream_t stream);
 
-/* Copy `tiles` tiles of 32 KiB in ONE launch, one workgroup per tile: tile
- * k from src + src_off[k] to dst + dst_off[k] (src_off, dst_off: device
- * int64 arrays of byte offsets).  A tile whose offsets are not multiples of
- * 16 or whose 32 KiB would leave [0, src_bytes) or [0, dst_bytes) is
- * skipped.  With the offsets of a workload's page planes (the pages its
- * block tables name) this is the paged transfer with the table lookups and
- * the length arithmetic taken out: the ceiling of a pack or unpack over the
- * same scattered pages. */
+/* Copy `tiles` tiles in ONE launch, one workgroup per tile: tile k moves
+ * lens[k] bytes (every tile 32 KiB when lens is null) from src + src_off[k]
+ * to dst + dst_off[k] (src_off, dst_off: device int64 arrays of byte
+ * offsets; lens: device int32 array or null).  A tile whose offsets or
+ * length are not multiples of 16, whose length is not in [16, 32 KiB], or
+ * whose bytes would leave [0, src_bytes) or [0, dst_bytes) is skipped.
+ * With the offsets of a workload's page runs (the pages its block tables
+ * name) this is the paged transfer with the table lookups and the length
+ * arithmetic taken out: the ceiling of a pack or unpack over the same
+ * scattered pages. */
 topkv_status_t topkv_ceiling_copy_tiles(const void* src, int64_t src_bytes, const int64_t* src_off, void* dst,
-                                        int64_t dst_bytes, const int64_t* dst_off, int32_t tiles,
-                                        hipStream_t stream);
+                                        int64_t dst_bytes, const int64_t* dst_off, const int32_t* lens,
+                                        int32_t tiles, hipStream_t stream);
 
 /* One workgroup of 64 lanes that touches no memory: the cost of a launch. */
 topkv_status_t topkv_ceiling_empty(hipStream_t stream);

@@ -26,7 +26,7 @@ _SIGS = {
     "topkv_ceiling_empty": [_P],
     "topkv_ceiling_copy_timeline": [_P, _P, _I64, _P, _P],
     "topkv_ceiling_wall_clock_khz": [ctypes.POINTER(_I32)],
-    "topkv_ceiling_copy_tiles": [_P, _I64, _P, _P, _I64, _P, _I32, _P],
+    "topkv_ceiling_copy_tiles": [_P, _I64, _P, _P, _I64, _P, _P, _I32, _P],
 }
 for _name, _args in _SIGS.items():
     _fn = getattr(_lib, _name)
@@ -53,9 +53,9 @@ def topkv_ceiling_read(src, nbytes, sink, stream=None) -> None:
     _check(_lib.topkv_ceiling_read(_ptr(src), int(nbytes), _ptr(sink), _stream(stream)))
 
 
-def topkv_ceiling_copy_tiles(src, src_bytes, src_off, dst, dst_bytes, dst_off, tiles, stream=None) -> None:
+def topkv_ceiling_copy_tiles(src, src_bytes, src_off, dst, dst_bytes, dst_off, lens, tiles, stream=None) -> None:
     _check(_lib.topkv_ceiling_copy_tiles(_ptr(src), int(src_bytes), _ptr(src_off), _ptr(dst), int(dst_bytes),
-                                         _ptr(dst_off), int(tiles), _stream(stream)))
+                                         _ptr(dst_off), _ptr(lens), int(tiles), _stream(stream)))
 
 
 def topkv_ceiling_empty(stream=None) -> None:

@@ -76,17 +76,22 @@ __global__ __launch_bounds__(kThreads) void ceiling_read_kernel(const V* __restr
   if (threadIdx.x == 0) sink[blockIdx.x] = part[0] ^ part[1] ^ part[2] ^ part[3];
 }
 
-// Tile w: 32 KiB from src + src_off[w] to dst + dst_off[w] (byte offsets); a tile whose offsets are
-// not 16-byte aligned or whose 32 KiB would leave either buffer is skipped.
+// Tile w: lens[w] bytes (32 KiB when lens is null) from src + src_off[w] to dst + dst_off[w] (byte
+// offsets); a tile whose offsets or length are not multiples of 16, whose length is not in
+// [16, 32 KiB], or whose bytes would leave either buffer is skipped.
 __global__ __launch_bounds__(kThreads) void ceiling_copy_tiles_kernel(const char* __restrict__ src, int64_t src_bytes,
                                                                       const int64_t* __restrict__ src_off,
                                                                       char* __restrict__ dst, int64_t dst_bytes,
-                                                                      const int64_t* __restrict__ dst_off) {
+                                                                      const int64_t* __restrict__ dst_off,
+                                                                      const int32_t* __restrict__ lens) {
   const int64_t so = src_off[blockIdx.x], d0 = dst_off[blockIdx.x];
-  if (((so | d0) & 15) || so < 0 || d0 < 0 || so > src_bytes - kTile || d0 > dst_bytes - kTile) return;
+  const int64_t len = lens ? lens[blockIdx.x] : kTile;
+  if (((so | d0 | len) & 15) || len < 16 || len > kTile || so < 0 || d0 < 0 || so > src_bytes - len ||
+      d0 > dst_bytes - len)
+    return;
   V v[kVpt];
-  load_tile(v, reinterpret_cast<const V*>(src + so), 0, kTile / 16);
-  store_tile(v, reinterpret_cast<V*>(dst + d0), 0, kTile / 16);
+  load_tile(v, reinterpret_cast<const V*>(src + so), 0, len / 16);
+  store_tile(v, reinterpret_cast<V*>(dst + d0), 0, len / 16);
 }
 
 __global__ void ceiling_empty_kernel() {}
@@ -171,15 +176,16 @@ topkv_status_t topkv_ceiling_read(const void* src, int64_t bytes, uint32_t* sink
 }
 
 topkv_status_t topkv_ceiling_copy_tiles(const void* src, int64_t src_bytes, const int64_t* src_off, void* dst,
-                                        int64_t dst_bytes, const int64_t* dst_off, int32_t tiles,
-                                        hipStream_t stream) {
+                                        int64_t dst_bytes, const int64_t* dst_off, const int32_t* lens,
+                                        int32_t tiles, hipStream_t stream) {
   using namespace topkv_ceiling;
   if (!src || !dst || !src_off || !dst_off || src_bytes < 0 || dst_bytes < 0 || tiles < 0 || !aligned(src) ||
       !aligned(dst))
     return TOPKV_ERR_INVALID_ARG;
   if (tiles == 0) return TOPKV_OK;
   hipLaunchKernelGGL(ceiling_copy_tiles_kernel, dim3((unsigned)tiles), dim3(kThreads), 0, stream,
-                     static_cast<const char*>(src), src_bytes, src_off, static_cast<char*>(dst), dst_bytes, dst_off);
+                     static_cast<const char*>(src), src_bytes, src_off, static_cast<char*>(dst), dst_bytes, dst_off,
+                     lens);
   return hipGetLastError() == hipSuccess ? TOPKV_OK : TOPKV_ERR_LAUNCH;
 }
 

@@ -324,17 +324,17 @@ def test_ceiling_library_exports_and_validation():
                      (cl.topkv_ceiling_copy_timeline, (a, b, 64, 0)),
                      (cl.topkv_ceiling_read, (a, 64, 0)), (cl.topkv_ceiling_read, (a, 24, b)),
                      (cl.topkv_ceiling_read, (a + 8, 64, b)),
-                     (cl.topkv_ceiling_copy_tiles, (a, 64, 0, b, 64, a, 1)),
-                     (cl.topkv_ceiling_copy_tiles, (a, 64, a, b, 64, b, -1)),
-                     (cl.topkv_ceiling_copy_tiles, (a, -1, a, b, 64, b, 1)),
-                     (cl.topkv_ceiling_copy_tiles, (a + 8, 64, a, b, 64, b, 1))):
+                     (cl.topkv_ceiling_copy_tiles, (a, 64, 0, b, 64, a, None, 1)),
+                     (cl.topkv_ceiling_copy_tiles, (a, 64, a, b, 64, b, None, -1)),
+                     (cl.topkv_ceiling_copy_tiles, (a, -1, a, b, 64, b, None, 1)),
+                     (cl.topkv_ceiling_copy_tiles, (a + 8, 64, a, b, 64, b, None, 1))):
         with pytest.raises(tk.TopkvError) as ei:
             fn(*args, stream=0)
         assert ei.value.status == INV, (fn.__name__, args)
     cl.topkv_ceiling_copy(a, b, 0, stream=0)                       # nothing to copy: nothing launched
     cl.topkv_ceiling_copy_layers(a, 64, b, 64, 0, 3, stream=0)
     cl.topkv_ceiling_read(a, 0, b, stream=0)
-    cl.topkv_ceiling_copy_tiles(a, 64, a, b, 64, b, 0, stream=0)
+    cl.topkv_ceiling_copy_tiles(a, 64, a, b, 64, b, None, 0, stream=0)
 
 
 def test_crc64_noalloc_validation(tk):

@@ -56,6 +56,47 @@ def test_table_layouts_keep_the_pages_valid():
             assert len(set(seen)) == len(seen)          # no page shared by two requests
 
 
+def test_scattered_tiles_cover_every_page_run_once():
+    """The ceiling's scattered-page copy (bench.scattered_tiles) moves exactly
+    the workload's transfer: in each direction the tiles' packed intervals
+    tile every layer's packed block once, and each tile's pool interval lies
+    inside the page plane its table entry names, over the rows its request
+    holds (five configurations; the re-blocking one unpacks into 64-token
+    pages)."""
+    import types
+
+    import bench
+    from paper_2607_28633_amd.workloads import make_workload
+    for name in ("tiny", "llama3-70b-4k", "llama3-70b-batch8", "deepseek-v3-mla", "reblock-70b"):
+        wl = make_workload(name)
+        row = wl.num_heads * wl.head_dim * wl.elem_bytes
+        layer_packed = int(wl.seq_lens.sum()) * wl.planes * row
+        ring = bench.ring_slots(wl, layer_packed)
+        st = types.SimpleNamespace(wl=wl, ring=ring, slice=layer_packed)
+        for d, (tables, P, npages) in enumerate(((wl.block_tables, wl.page_size, wl.num_pages),
+                                                 (wl.dst_block_tables, wl.dst_page_size, wl.dst_num_pages))):
+            pool, packed, lens = bench.scattered_tiles(st, d)
+            assert len(pool) == len(packed) == len(lens) and (lens >= 16).all() and (lens <= 32768).all()
+            assert not ((pool | packed | lens.astype(np.int64)) % 16).any()
+            per = len(pool) // wl.num_layers
+            plane = P * row
+            slab_bytes = npages * wl.planes * plane
+            for l in sorted({0, wl.num_layers // 2, wl.num_layers - 1}):
+                sl = slice(l * per, (l + 1) * per)
+                o, n = packed[sl] - (l % ring) * layer_packed, lens[sl].astype(np.int64)
+                k = np.argsort(o)
+                assert o[k][0] == 0 and (o[k][1:] == (o[k] + n[k])[:-1]).all() and int((o + n).max()) == layer_packed
+                # pool side: page plane of the tile, offset inside it, and the rows the request owns there
+                q = pool[sl] - wl.kv_slab(l) * slab_bytes
+                page, c, within = q // (wl.planes * plane), (q // plane) % wl.planes, q % plane
+                tok = np.concatenate([[0], np.cumsum(wl.seq_lens.astype(np.int64))])
+                r = np.searchsorted(tok, o // (wl.planes * row), side="right") - 1   # request of each tile
+                first = (o - tok[r] * wl.planes * row - c * wl.seq_lens[r].astype(np.int64) * row) // row
+                i = first // P                                                 # table entry of the tile
+                assert (tables[r, i] == page).all() and (within == first % P * row + (o % row)).all()
+                assert (within + n <= plane).all() and ((first * row + o % row + n) <= wl.seq_lens[r] * row).all()
+
+
 def test_more_than_one_gpu_is_refused():
     r = subprocess.run([sys.executable, os.path.join(ROOT, "bench.py"), "--gpus", "2"],
                        capture_output=True, text=True, cwd=ROOT, timeout=120)

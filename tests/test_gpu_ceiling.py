@@ -57,17 +57,22 @@ def test_copy_tiles_follows_the_offsets(cl):
     do = rng.permutation(np.arange(0, (n_dst - TILE) // TILE + 1) * TILE)[:tiles - 4]   # non-overlapping
     do = np.concatenate([do, [8, n_dst - TILE + 16, -TILE, n_dst]])   # misaligned, past the end, negative, past
     so[-1] = n_src - TILE + 32                                            # source past the end
-    so_t, do_t = torch.tensor(so, device="cuda"), torch.tensor(do, device="cuda")
-    cl.topkv_ceiling_copy_tiles(src, n_src, so_t, dst, n_dst, do_t, tiles)
-    torch.cuda.synchronize()
-    want = np.full(n_dst, 0x5A, dtype=np.uint8)
-    h = src.cpu().numpy()
-    for k in range(tiles):
-        s0, d0 = int(so[k]), int(do[k])
-        if (s0 | d0) % 16 or s0 < 0 or d0 < 0 or s0 > n_src - TILE or d0 > n_dst - TILE:
-            continue
-        want[d0:d0 + TILE] = h[s0:s0 + TILE]
-    assert np.array_equal(dst.cpu().numpy(), want)
+    for lens in (None, rng.integers(1, TILE // 16 + 1, size=tiles) * 16):
+        if lens is not None:
+            lens[3], lens[5], lens[7] = 0, TILE + 16, 24                  # too short, too long, misaligned
+        dst.fill_(0x5A)
+        so_t, do_t = torch.tensor(so, device="cuda"), torch.tensor(do, device="cuda")
+        ln_t = None if lens is None else torch.tensor(lens, dtype=torch.int32, device="cuda")
+        cl.topkv_ceiling_copy_tiles(src, n_src, so_t, dst, n_dst, do_t, ln_t, tiles)
+        torch.cuda.synchronize()
+        want = np.full(n_dst, 0x5A, dtype=np.uint8)
+        h = src.cpu().numpy()
+        for k in range(tiles):
+            s0, d0, n = int(so[k]), int(do[k]), TILE if lens is None else int(lens[k])
+            if (s0 | d0 | n) % 16 or n < 16 or n > TILE or s0 < 0 or d0 < 0 or s0 > n_src - n or d0 > n_dst - n:
+                continue
+            want[d0:d0 + n] = h[s0:s0 + n]
+        assert np.array_equal(dst.cpu().numpy(), want), lens is None
 
 
 @pytest.mark.parametrize("n", [16, TILE, 3 * TILE + 4096 + 16, (8 << 20) + 160])
