@@ -129,11 +129,12 @@ def parse():
     ap.add_argument("--issue", choices=["engine", "launches"], default="engine",
                     help="engine: one layer-engine launch per direction over each run of full-attention layers "
                          "(value); launches: one launch per layer.  The other mode is timed beside it")
-    ap.add_argument("--tables", choices=["random", "sorted", "consecutive"], default="random",
+    ap.add_argument("--tables", type=tables_arg, default="random",
                     help="page layout of the block tables: random (each request the next pages of a seeded "
                          "permutation of the pool: the workloads' fragmented pools, measured by default), sorted "
                          "(the same pages, each request's in ascending pool order), consecutive (each request's "
-                         "pages one contiguous run of the pool)")
+                         "pages one contiguous run of the pool), runsN (each request's pages random runs of N "
+                         "consecutive pool pages)")
     ap.add_argument("--no-configs", dest="configs", action="store_false",
                     help="skip the other full-size configurations (Llama-3-8B, batch of 8, MLA, re-blocking) of the default run")
     ap.add_argument("--threads", type=int, default=0,
@@ -193,22 +194,45 @@ def layer_kernel(wl, direction):
 def table_layout(wl, layout):
     """Re-lay both pools' block tables of a workload: "sorted" keeps every
     request's pages and sorts them by pool index; "consecutive" hands the
-    requests consecutive runs of the pool in request order; "random" leaves
-    the workload's tables."""
+    requests consecutive runs of the pool in request order; "runsN" hands
+    each request random runs of N consecutive pool pages (run slots drawn
+    from a seeded permutation of the pool's N-page slots, none shared);
+    "random" leaves the workload's tables."""
     import numpy as np
     if layout == "random":
         return
-    for attr, P in (("block_tables", wl.page_size), ("dst_block_tables", wl.dst_page_size)):
+    run = int(layout[4:]) if layout.startswith("runs") else 0
+    for attr, P, NP in (("block_tables", wl.page_size, wl.num_pages),
+                        ("dst_block_tables", wl.dst_page_size, wl.dst_num_pages)):
         tab = getattr(wl, attr).copy()
         nxt = 0
+        if run:
+            pages_of = [-(-int(n) // P) for n in wl.seq_lens]
+            need = sum(-(-k // run) for k in pages_of)
+            if need > NP // run:
+                raise SystemExit(f"--tables {layout}: {need} runs of {run} pages do not fit a pool of {NP} pages")
+            slots = np.random.default_rng(wl.seed + run).permutation(NP // run)
         for r, n in enumerate(wl.seq_lens):
             k = -(-int(n) // P)
             if layout == "sorted":
                 tab[r, :k] = np.sort(tab[r, :k])
+            elif run:
+                m = -(-k // run)
+                pages = (slots[nxt:nxt + m, None] * run + np.arange(run)[None, :]).reshape(-1)
+                tab[r, :k] = pages[:k]
+                nxt += m
             else:
                 tab[r, :k] = np.arange(nxt, nxt + k)
                 nxt += k
         setattr(wl, attr, tab)
+
+
+def tables_arg(v):
+    """--tables: random, sorted, consecutive or runsN (N >= 1 pages per run)."""
+    import argparse
+    if v in ("random", "sorted", "consecutive") or (v.startswith("runs") and v[4:].isdigit() and int(v[4:]) >= 1):
+        return v
+    raise argparse.ArgumentTypeError(f"{v!r}: expected random, sorted, consecutive or runsN")
 
 
 def engine_kernel(wl, setup, direction):

@@ -33,11 +33,12 @@ def test_windowed_bytes_count_kept_tokens_only():
 
 def test_table_layouts_keep_the_pages_valid():
     """--tables sorted keeps every request's pages (sorted); consecutive gives
-    each request its own run of the pool; both stay inside the pool."""
+    each request its own run of the pool; runs8 gives each request runs of 8
+    consecutive pages; all stay inside the pool, no page shared."""
     import bench
     from paper_2607_28633_amd.workloads import make_workload
     base = make_workload("llama3-70b-batch8")
-    for layout in ("sorted", "consecutive"):
+    for layout in ("sorted", "consecutive", "runs8"):
         wl = make_workload("llama3-70b-batch8")
         bench.table_layout(wl, layout)
         for attr, P, NP in (("block_tables", wl.page_size, wl.num_pages),
@@ -50,6 +51,10 @@ def test_table_layouts_keep_the_pages_valid():
                 assert row.min() >= 0 and row.max() < NP
                 if layout == "sorted":
                     assert (np.diff(row) > 0).all() and sorted(ref[r, :k].tolist()) == row.tolist()
+                elif layout == "runs8":
+                    assert (row[::8] % 8 == 0).all()                      # runs start on 8-page slots
+                    runs = [row[j:j + 8] for j in range(0, k, 8)]
+                    assert all((np.diff(x) == 1).all() for x in runs)
                 else:
                     assert (np.diff(row) == 1).all()
                 seen += row.tolist()
