@@ -6,10 +6,11 @@ buffer), then unpack every layer (send buffer -> destination pool): the
 per-layer transfer unit of the paper's pipelined layer-by-layer KV transfer
 (Section 5.2) at both ends.  Two ways of issuing a sweep are timed:
   engine   - the layer engine (topkv_engine_pack_layers / _unpack_layers):
-             one persistent launch per direction over each run of
-             full-attention layers, each layer moved as one batched launch
-             would move it, every layer ready at launch (windowed and
-             fixed-state layers keep one launch each);
+             one call per direction over each run of full-attention layers,
+             each layer moved as one batched launch would move it, every
+             layer ready at launch, issued by the library as grids of about
+             512 MiB of packed blocks (topkv_engine_layers_per_grid);
+             windowed and fixed-state layers keep one launch each;
   launches - one batched launch per layer.
 --issue picks the one that gives `value` (engine by default); the other is
 reported beside it.  Each sweep is replayed from a captured HIP graph
@@ -127,7 +128,7 @@ def parse():
     ap.add_argument("--launch", choices=["eager", "graph"], default="graph",
                     help="issue each sweep from the host, or replay it as a captured HIP graph")
     ap.add_argument("--issue", choices=["engine", "launches"], default="engine",
-                    help="engine: one layer-engine launch per direction over each run of full-attention layers "
+                    help="engine: one layer-engine call per direction over each run of full-attention layers "
                          "(value); launches: one launch per layer.  The other mode is timed beside it")
     ap.add_argument("--tables", type=tables_arg, default="random",
                     help="page layout of the block tables: random (each request the next pages of a seeded "
@@ -135,6 +136,9 @@ def parse():
                          "(the same pages, each request's in ascending pool order), consecutive (each request's "
                          "pages one contiguous run of the pool), runsN (each request's pages random runs of N "
                          "consecutive pool pages)")
+    ap.add_argument("--single-mode", action="store_true",
+                    help="time only the --issue mode (profiler runs: every pack/unpack dispatch before the "
+                         "ceiling block is then that mode's)")
     ap.add_argument("--no-configs", dest="configs", action="store_false",
                     help="skip the other full-size configurations (Llama-3-8B, batch of 8, MLA, re-blocking) of the default run")
     ap.add_argument("--threads", type=int, default=0,
@@ -235,21 +239,51 @@ def tables_arg(v):
     raise argparse.ArgumentTypeError(f"{v!r}: expected random, sorted, consecutive or runsN")
 
 
-def engine_kernel(wl, setup, direction):
-    """The kernel an engine launch of the workload runs (the library's
-    choice): with every layer ready, the batched direct grid with the layers
-    on grid z while it fits that grid's limits, else the persistent
-    kv_engine_kernel."""
-    runs = [n for kind, _, n in setup.chunks if kind == "engine"]
-    if not runs:
-        return "no engine launch (every layer has its own call)"
+def engine_direct(wl, direction, layers):
+    """Whether an engine call over `layers` layers with every layer ready
+    runs the hardware-dispatched grid (the library's rule: the batched
+    direct grid's slot, table-width and request limits, layers * requests
+    within grid z) rather than the persistent kv_engine_kernel."""
     row = wl.num_heads * wl.head_dim * wl.elem_bytes
     plane = (wl.page_size if direction == "pack" else wl.dst_page_size) * row
     tiles = -(-plane // (256 * 8 * 16))
     stride = (wl.block_tables if direction == "pack" else wl.dst_block_tables).shape[1]
-    direct = (wl.num_reqs * stride * wl.planes * tiles <= 1 << 20 and stride <= 65535 and wl.num_reqs <= 1024
-              and wl.num_reqs * max(runs) <= 65535)
-    name = f"kv_{direction}_kernel (batched direct grid, layers on grid z)" if direct else "kv_engine_kernel"
+    return (wl.num_reqs * stride * wl.planes * tiles <= 1 << 20 and stride <= 65535 and wl.num_reqs <= 1024
+            and wl.num_reqs * layers <= 65535)
+
+
+def sweep_grids(setup, issue, direction):
+    """Kernel launches in one sweep of a direction: one per per-layer call;
+    an engine call over n layers issues ceil(n / layers per grid) grids
+    (topkv_engine_layers_per_grid) when it runs the hardware-dispatched
+    grid, one persistent grid otherwise."""
+    if issue == "launches":
+        return setup.wl.num_layers
+    d = ("pack", "unpack")[direction]
+    total = 0
+    for kind, _, n in setup.chunks:
+        if kind == "engine" and engine_direct(setup.wl, d, n):
+            total += -(-n // setup.tk.topkv_engine_layers_per_grid(n, setup.slice))
+        else:
+            total += 1
+    return total
+
+
+def engine_kernel(wl, setup, direction):
+    """The kernel an engine launch of the workload runs (the library's
+    choice): with every layer ready, the batched direct grid with the layers
+    on grid z while it fits that grid's limits, issued as grids of
+    topkv_engine_layers_per_grid layers each, else the persistent
+    kv_engine_kernel."""
+    runs = [n for kind, _, n in setup.chunks if kind == "engine"]
+    if not runs:
+        return "no engine launch (every layer has its own call)"
+    per = sorted({setup.tk.topkv_engine_layers_per_grid(n, setup.slice) for n in runs})
+    if all(engine_direct(wl, direction, n) for n in runs):
+        name = (f"kv_{direction}_kernel (batched direct grid, layers on grid z, "
+                f"{'/'.join(str(x) for x in per)} layers per grid)")
+    else:
+        name = "kv_engine_kernel"
     return f"{name}, layer engine over runs of {'/'.join(str(n) for n in sorted(set(runs)))} layers"
 
 
@@ -621,7 +655,7 @@ def time_sweeps(setup, issue, steps, warmup, launch="graph", before_timed=None):
     """Warm up, then time `steps` steps (pack sweep, then unpack sweep) with
     HIP events on the launch stream at the sweep boundaries.  Returns
     (ms per step, [pack sweep us, unpack sweep us] summed over the steps,
-    launches per sweep)."""
+    [kernel launches per pack sweep, per unpack sweep])."""
     import torch
     tk = setup.tk
     stream = torch.cuda.current_stream()
@@ -664,20 +698,21 @@ def time_sweeps(setup, issue, steps, warmup, launch="graph", before_timed=None):
     torch.cuda.synchronize()
     wall_ms = marks[0][0].elapsed_ms(marks[-1][2])
     sweep_us = [1e3 * sum(marks[k][d].elapsed_ms(marks[k][d + 1]) for k in range(steps)) for d in (0, 1)]
-    return wall_ms / steps, sweep_us, len(sweeps[0])
+    return wall_ms / steps, sweep_us, [sweep_grids(setup, issue, d) for d in (0, 1)]
 
 
 def kernel_figures(wl, sweep_us, steps, launches):
-    """Per-launch figures of each direction: algorithmic bytes per launch,
-    average launch duration (sweep time / launches, so it includes the
-    sub-microsecond gaps between launches), GB/s."""
+    """Per-launch figures of each direction: algorithmic bytes per kernel
+    launch, average launch duration (sweep time / kernel launches, so it
+    includes the sub-microsecond gaps between launches), GB/s.  launches:
+    kernel launches per pack sweep and per unpack sweep."""
     per_layer = [layer_bytes(wl, l) for l in range(wl.num_layers)]
     out = {}
     for d, name in ((0, "pack"), (1, "unpack")):
-        b = sum(x[d] for x in per_layer) / launches
-        us = sweep_us[d] / (steps * launches)
+        b = sum(x[d] for x in per_layer) / launches[d]
+        us = sweep_us[d] / (steps * launches[d])
         out[name] = {"bytes_per_launch": int(round(b)), "avg_us": round(us, 3), "gbs": round(b / us / 1e3, 1),
-                     "launches": steps * launches,
+                     "launches": steps * launches[d],
                      "us_per_layer": round(sweep_us[d] / (steps * wl.num_layers), 3)}
     return out
 
@@ -736,24 +771,46 @@ def scattered_tiles(setup, direction):
             np.tile(lens, wl.num_layers).astype(np.int32))
 
 
+def layer_groups(setup):
+    """(first layer, layers) of the grids the engine splits the whole sweep
+    into (topkv_engine_layers_per_grid over every layer), so the ceiling
+    copies run in launches of the engine's length."""
+    L = setup.wl.num_layers
+    per = setup.tk.topkv_engine_layers_per_grid(L, setup.slice)
+    return [(j, min(per, L - j)) for j in range(0, L, per)]
+
+
 def scattered_copy(setup, reps):
     """The workload's transfer with the table lookups and the length
     arithmetic done beforehand (topkv_ceiling_copy_tiles over scattered_tiles):
-    pool pages -> packed slots, then packed slots -> destination pages, one
-    launch per direction, alternating as the step does."""
+    pool pages -> packed slots, then packed slots -> destination pages, in
+    launches over the engine's layer groups (layer_groups), alternating
+    direction as the step does."""
     import torch
 
     from paper_2607_28633_amd import ceiling as cl
-    tk = setup.tk
+    tk, L = setup.tk, setup.wl.num_layers
     sides = [scattered_tiles(setup, d) for d in (0, 1)]
     if sides[0] is None or any(len(x[0]) > 2**31 - 1 for x in sides):
         return None
     dev = [[torch.from_numpy(a).cuda() for a in x] for x in sides]
     nb = lambda x: x.numel() * x.element_size()
-    pk = lambda: cl.topkv_ceiling_copy_tiles(setup.src, nb(setup.src), dev[0][0], setup.packed, nb(setup.packed),
-                                             dev[0][1], dev[0][2], len(sides[0][0]), None)
-    up = lambda: cl.topkv_ceiling_copy_tiles(setup.packed, nb(setup.packed), dev[1][1], setup.dst, nb(setup.dst),
-                                             dev[1][0], dev[1][2], len(sides[1][0]), None)
+    groups = layer_groups(setup)
+    per_layer = [len(x[0]) // L for x in sides]          # tiles are layer-major, the same count per layer
+
+    def go(d):
+        T = per_layer[d]
+        for j, n in groups:
+            a, b = j * T, (j + n) * T
+            if d == 0:
+                cl.topkv_ceiling_copy_tiles(setup.src, nb(setup.src), dev[0][0][a:b], setup.packed,
+                                            nb(setup.packed), dev[0][1][a:b], dev[0][2][a:b], b - a, None)
+            else:
+                cl.topkv_ceiling_copy_tiles(setup.packed, nb(setup.packed), dev[1][1][a:b], setup.dst,
+                                            nb(setup.dst), dev[1][0][a:b], dev[1][2][a:b], b - a, None)
+
+    pk = lambda: go(0)
+    up = lambda: go(1)
     stream = torch.cuda.current_stream()
     for _ in range(2):
         pk()
@@ -770,7 +827,7 @@ def scattered_copy(setup, reps):
     t = [1e3 * sum(m[k][d].elapsed_ms(m[k][d + 1]) for k in range(reps)) / reps for d in (0, 1)]
     moved = [2 * int(sides[d][2].astype("int64").sum()) for d in (0, 1)]
     del dev
-    return {"tiles": [len(sides[0][0]), len(sides[1][0])], "bytes": moved,
+    return {"tiles": [len(sides[0][0]), len(sides[1][0])], "bytes": moved, "launches": len(groups),
             "pack_like_us": round(t[0], 2), "unpack_like_us": round(t[1], 2),
             "pack_like_gbs": round(moved[0] / t[0] / 1e3, 1), "unpack_like_gbs": round(moved[1] / t[1] / 1e3, 1),
             "step_gbs": round((moved[0] + moved[1]) / (t[0] + t[1]) / 1e3, 1)}
@@ -778,19 +835,19 @@ def scattered_copy(setup, reps):
 
 def ceiling(setup, steps):
     """The practical ceiling and floor on this machine, measured like the
-    headline (graph replays of L launches, or one launch per direction, with
-    the same cache defeat): the empty kernel, the per-layer pack grid with
+    headline (graph replays of L launches, or launches over the engine's
+    layer groups, with the same cache defeat): the empty kernel, the per-layer pack grid with
     every length 0, the hand-written streaming copy of one layer's packed
     bytes per launch into each layer's own slot, that copy at 64 MiB, 256 MiB
     and 1 GiB, a read-only pass over the same sources at the same sizes
     (the ceiling of a checksum pass), the layer engine's schedule
     without tables
     (topkv_ceiling_copy_layers: pool slab prefixes -> packed slots -> a
-    second pool's slab prefixes, one launch per direction), and the same
-    transfer over the workload's own scattered pages with the tables'
-    lookups done beforehand (topkv_ceiling_copy_tiles: every 32 KiB page
-    plane from its pool page to its packed slot and on to its destination
-    page, one launch per direction)."""
+    second pool's slab prefixes), and the same transfer over the workload's
+    own scattered pages with the tables' lookups done beforehand
+    (topkv_ceiling_copy_tiles: every 32 KiB page plane from its pool page to
+    its packed slot and on to its destination page); these two run in
+    launches over the engine's layer groups (layer_groups)."""
     import numpy as np
     import torch
 
@@ -855,11 +912,21 @@ def ceiling(setup, steps):
     out["copy_per_launch"] = copies
     out["read_per_launch"] = reads
     # the engine's schedule without tables: read each slab's first n bytes into the packed slots, then
-    # write them to the second pool's slabs, one launch per direction, alternating as the step does
+    # write them to the second pool's slabs, in launches over the engine's layer groups, alternating
+    # direction as the step does
     lay = min(L, setup.ring, setup.src.shape[0], setup.dst.shape[0])
-    pk = lambda: cl.topkv_ceiling_copy_layers(setup.src, slab, setup.packed, setup.slice, n, lay, 0, None)
     dslab = setup.dst.view(-1).numel() * 2 // setup.dst.shape[0]
-    up = lambda: cl.topkv_ceiling_copy_layers(setup.packed, setup.slice, setup.dst, dslab, n, lay, 0, None)
+    per = tk.topkv_engine_layers_per_grid(lay, setup.slice)
+    lgroups = [(j, min(per, lay - j)) for j in range(0, lay, per)]
+    sp_, pp_, dp_ = setup.src.data_ptr(), setup.packed.data_ptr(), setup.dst.data_ptr()
+
+    def pk():
+        for j, k in lgroups:
+            cl.topkv_ceiling_copy_layers(sp_ + j * slab, slab, pp_ + j * setup.slice, setup.slice, n, k, 0, None)
+
+    def up():
+        for j, k in lgroups:
+            cl.topkv_ceiling_copy_layers(pp_ + j * setup.slice, setup.slice, dp_ + j * dslab, dslab, n, k, 0, None)
     for _ in range(2):
         pk()
         up()
@@ -874,7 +941,7 @@ def ceiling(setup, steps):
     m[-1][2].synchronize()
     t = [1e3 * sum(m[k][d].elapsed_ms(m[k][d + 1]) for k in range(reps)) / (reps * lay) for d in (0, 1)]
     out["copy_layers_engine_schedule"] = {
-        "layers": lay, "bytes_per_layer": 2 * n, "read_us_per_layer": round(t[0], 3),
+        "layers": lay, "launches": len(lgroups), "bytes_per_layer": 2 * n, "read_us_per_layer": round(t[0], 3),
         "write_us_per_layer": round(t[1], 3), "step_gbs": round(4 * n / (t[0] + t[1]) / 1e3, 1)}
     sp = scattered_copy(setup, reps)
     if sp:
@@ -920,7 +987,8 @@ def run(args):
     st = Setup(wl, topkv)
     L, R = wl.num_layers, wl.num_reqs
     log(f"[bench] pools src {tuple(st.src.shape)} dst {tuple(st.dst.shape)}, packed {st.nbytes} B/layer, "
-        f"ring {st.ring}, engine launches per sweep {sum(1 for c in st.chunks if c[0] == 'engine')}")
+        f"ring {st.ring}, engine calls per sweep {sum(1 for c in st.chunks if c[0] == 'engine')}, "
+        f"kernel launches per sweep {sweep_grids(st, 'engine', 0)}")
 
     # the timed run's output is checked: host copies of the checked layers' source slabs and of their
     # destination slabs as generated, before any kernel has run
@@ -944,11 +1012,13 @@ def run(args):
     kern = kernel_figures(wl, sweep_us, args.steps, launches)
 
     other = "launches" if args.issue == "engine" else "engine"
-    o_ms, o_us, o_launches = time_sweeps(st, other, args.steps, args.warmup, args.launch)
-    o_kern = kernel_figures(wl, o_us, args.steps, o_launches)
-    log(f"[bench] {other}: {o_ms:.4f} ms per step")
+    o_ms = o_kern = None
+    if not args.single_mode:
+        o_ms, o_us, o_launches = time_sweeps(st, other, args.steps, args.warmup, args.launch)
+        o_kern = kernel_figures(wl, o_us, args.steps, o_launches)
+        log(f"[bench] {other}: {o_ms:.4f} ms per step")
 
-    if args.kernel_events:
+    if args.kernel_events and (args.issue == "launches" or o_kern is not None):
         # diagnostic: each per-layer launch stamped with its own begin/end (host launch path is slower)
         evs = [[(topkv.HipEvent(), topkv.HipEvent()) for _ in range(L)] for _ in range(2)]
         stamped = [st.sweep(0, "launches", evs[0]), st.sweep(1, "launches", evs[1])]
@@ -991,16 +1061,18 @@ def run(args):
                    **({"state_layers": sum(wl.layer_state), "packed_state_bytes_per_layer": st.slot_bytes}
                       if wl.layer_state else {}),
                    "step": ("pack every layer, then unpack every layer: "
-                            + ("the layer engine, one launch per direction over each run of "
-                               "full-attention layers (every layer ready at launch), other layers one launch each"
+                            + ("the layer engine, one call per direction over each run of "
+                               "full-attention layers (every layer ready at launch; grids of about 512 MiB of "
+                               "packed blocks), other layers one launch each"
                                if args.issue == "engine" else "one launch per layer")),
                    "seed": wl.seed, "packed_ring": st.ring, "phys_layers": wl.phys_layers},
         "pct_of_peak": round(100 * value / HBM_PEAK_GBS, 2),
         "wall_us_per_layer": {"pack+unpack": round(1e3 * ms_per_step / L, 3)},
         "kernels": kern,
         "roofline": roofline,
-        other: {"value": round(step_gbs(wl, o_ms), 1), "ms_per_step": round(o_ms, 4),
-                "pct_of_peak": round(100 * step_gbs(wl, o_ms) / HBM_PEAK_GBS, 2), "kernels": o_kern},
+        other: None if o_ms is None else {
+            "value": round(step_gbs(wl, o_ms), 1), "ms_per_step": round(o_ms, 4),
+            "pct_of_peak": round(100 * step_gbs(wl, o_ms) / HBM_PEAK_GBS, 2), "kernels": o_kern},
         "copy_ceiling_gbs": ceil["copy_per_launch"]["layer"]["gbs"] if ceil else None,
         "ceiling": ceil,
     }

@@ -220,7 +220,10 @@ topkv_status_t topkv_unpack_layer_batched_ex(const void* src, int64_t src_bytes,
  * Grids: without waiting, the launch is a hardware-dispatched grid with one
  * workgroup per (layer, request, table entry, plane, tile) slot, as the
  * batched calls use for one layer (slots past a request's pages exit at
- * once); beyond that grid's limits (more than 1024 requests, 2^20 slots per
+ * once), issued as consecutive grids of topkv_engine_layers_per_grid layers
+ * each (engine->layers_per_grid when non-zero, else about 512 MiB of packed
+ * blocks per grid: a single grid over a long range was measured slower on
+ * MI355X); beyond that grid's limits (more than 1024 requests, 2^20 slots per
  * layer, 65535 table entries or 65535 requests * layers) and whenever it
  * waits, the engine is a persistent grid that keeps
  * engine->workgroups_per_cu workgroups of 256 threads per compute unit (0: 8)
@@ -230,7 +233,8 @@ topkv_status_t topkv_unpack_layer_batched_ex(const void* src, int64_t src_bytes,
  * Returns synchronously: the host-
  * side argument errors of the batched calls, TOPKV_ERR_INVALID_ARG for a bad
  * layer range or layer_stride, a null status with ready set, or a timeout
- * outside (0, 60 000 000] us, and TOPKV_ERR_UNSUPPORTED when num_layers *
+ * outside (0, 60 000 000] us or a negative layers_per_grid, and
+ * TOPKV_ERR_UNSUPPORTED when num_layers *
  * num_reqs * bt_stride * (items per page) reaches 2^31.  Checked mode
  * validates the tables and lengths once for the range (the smallest layer
  * block as capacity).  The call never synchronises otherwise and allocates
@@ -242,7 +246,18 @@ typedef struct topkv_engine {
   uint32_t        epoch;      /* value each ready word must reach */
   int32_t         workgroups_per_cu;  /* 0: 8 */
   int64_t         timeout_us; /* longest wait for one layer, in (0, 60e6]; ignored without ready */
+  int32_t         layers_per_grid;    /* without ready: layers per hardware-dispatched grid, 0: the library's */
 } topkv_engine_t;
+
+/* Layers that each hardware-dispatched grid of an engine call without
+ * waiting covers (the call's last grid may cover fewer): engine->
+ * layers_per_grid when engine is non-null and it is non-zero (at most
+ * num_layers), else num_layers cut into ceil(num_layers * layer_stride /
+ * 512 MiB) grids of equal layer count, rounded up.  Host-only, no device
+ * access; the persistent grid (waiting, or a range past the direct grid's
+ * limits) is always one launch.  Returns -1 for num_layers < 1, a negative
+ * layer_stride or a negative engine->layers_per_grid. */
+int32_t topkv_engine_layers_per_grid(int32_t num_layers, int64_t layer_stride, const topkv_engine_t* engine);
 
 topkv_status_t topkv_engine_pack_layers(const topkv_pool_t* src, int32_t first_layer, int32_t num_layers,
                                         int32_t num_reqs, const int32_t* block_tables, int32_t bt_stride,

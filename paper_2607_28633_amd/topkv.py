@@ -51,7 +51,7 @@ EXPORTS = ["topkv_pack_layer", "topkv_unpack_layer", "topkv_pack_layer_batched",
            "topkv_pack_state_layer", "topkv_unpack_state_layer", "topkv_check_state_slots",
            "topkv_check_state_workspace_bytes", "topkv_kvcache1_pack_layers", "topkv_kvcache1_unpack_layers",
            "topkv_kvcache1_pack_seal", "topkv_kvcache1_verify_unpack", "topkv_engine_pack_layers",
-           "topkv_engine_unpack_layers", "topkv_crc64_noalloc"]
+           "topkv_engine_unpack_layers", "topkv_engine_layers_per_grid", "topkv_crc64_noalloc"]
 
 TOPKV_LAYOUT_PACKED = 0
 TOPKV_LAYOUT_POOL = 1
@@ -83,7 +83,8 @@ class topkv_launch_t(ctypes.Structure):
 
 class topkv_engine_t(ctypes.Structure):
     _fields_ = [("ready", ctypes.c_void_p), ("cancel", ctypes.c_void_p), ("status", ctypes.c_void_p),
-                ("epoch", ctypes.c_uint32), ("workgroups_per_cu", ctypes.c_int32), ("timeout_us", ctypes.c_int64)]
+                ("epoch", ctypes.c_uint32), ("workgroups_per_cu", ctypes.c_int32), ("timeout_us", ctypes.c_int64),
+                ("layers_per_grid", ctypes.c_int32)]
 
 
 _P = ctypes.c_void_p
@@ -142,6 +143,7 @@ _SIGS = {
                                         ctypes.POINTER(topkv_engine_t), _P]),
     "topkv_engine_unpack_layers": (_I32, [_P, _I64, _I64, _POOL, _I32, _I32, _I32, _P, _I32, _P,
                                           ctypes.POINTER(topkv_engine_t), _P]),
+    "topkv_engine_layers_per_grid": (_I32, [_I32, _I64, ctypes.POINTER(topkv_engine_t)]),
     "topkv_dma_create": (_I32, [ctypes.POINTER(_P)]),
     "topkv_dma_submit": (_I32, [_P, _P, _P, _P, _I64, ctypes.POINTER(_I64)]),
     "topkv_dma_wait": (_I32, [_P, _I64]),
@@ -677,12 +679,22 @@ def _word_ptr(x) -> int:
     return _ptr(x)
 
 
-def engine_options(ready=None, epoch=0, status=None, cancel=None, timeout_us=0, workgroups_per_cu=0) -> topkv_engine_t:
+def engine_options(ready=None, epoch=0, status=None, cancel=None, timeout_us=0, workgroups_per_cu=0,
+                   layers_per_grid=0) -> topkv_engine_t:
     """topkv_engine_t for the engine calls: ready / cancel are int32 words in
     device memory or pinned host memory (or addresses), status a device
     int32 holding 0 at launch."""
     return topkv_engine_t(_word_ptr(ready), _word_ptr(cancel), _ptr(status), ctypes.c_uint32(int(epoch) & 0xffffffff),
-                          int(workgroups_per_cu), int(timeout_us))
+                          int(workgroups_per_cu), int(timeout_us), int(layers_per_grid))
+
+
+def topkv_engine_layers_per_grid(num_layers, layer_stride, engine=None) -> int:
+    """Layers per hardware-dispatched grid of an engine call without waits
+    (host-only)."""
+    n = _lib.topkv_engine_layers_per_grid(int(num_layers), int(layer_stride), _engine_arg(engine))
+    if n < 0:
+        raise TopkvError(TOPKV_ERR_INVALID_ARG)
+    return n
 
 
 def _engine_arg(engine):

@@ -132,13 +132,36 @@ def test_engine_validation(tk):
     for opt in (tk.engine_options(ready=ready, status=0, timeout_us=1000),          # ready without status
                 tk.engine_options(ready=ready, status=status, timeout_us=0),         # no timeout
                 tk.engine_options(ready=ready, status=status, timeout_us=60_000_001),
-                tk.engine_options(workgroups_per_cu=-1), tk.engine_options(workgroups_per_cu=65)):
+                tk.engine_options(workgroups_per_cu=-1), tk.engine_options(workgroups_per_cu=65),
+                tk.engine_options(layers_per_grid=-1)):
         _expect(tk, INV, pk, good, 0, 2, 2, bt, 4, lens, buf, stride, packed_bytes=2 * stride, engine=opt)
         _expect(tk, INV, up, buf, stride, good, 0, 2, 2, bt, 4, lens, packed_bytes=2 * stride, engine=opt)
     # no requests: nothing to launch, whatever the wait options
     pk(good, 0, 2, 0, 0, 1, 0, 0, stride, packed_bytes=2 * stride,
        engine=tk.engine_options(ready=ready, status=status, timeout_us=1000), stream=0)
     up(0, stride, good, 1, 1, 0, 0, 1, 0, packed_bytes=0, stream=0)
+
+
+def test_engine_layers_per_grid(tk):
+    """The engine's split of a range into hardware-dispatched grids: about
+    512 MiB of packed blocks per grid in grids of equal layer count (rounded
+    up), or the caller's count capped at the range."""
+    f = tk.topkv_engine_layers_per_grid
+    mib = 1 << 20
+    assert f(80, 16 * mib) == 27                  # 1280 MiB: 3 grids of 27, 27, 26 layers
+    assert f(80, 139685888) == 4                  # the 70B batch of 8: 21 grids
+    assert f(61, 204800000) == 3                  # 200 MB layers: 23 grids
+    assert f(32, 16 * mib) == 32                  # exactly 512 MiB: one grid
+    assert f(33, 16 * mib) == 17                  # just past it: two grids
+    assert f(8, 5 << 30) == 1                     # layers past the target: one each
+    assert f(1, 0) == 1 and f(5, 0) == 5          # no stride: one grid
+    assert f(3, 1 << 62) == 1                     # the product overflows int64: one layer per grid
+    assert f(7, 16 * mib, tk.engine_options(layers_per_grid=3)) == 3
+    assert f(7, 16 * mib, tk.engine_options(layers_per_grid=9)) == 7
+    assert f(7, 16 * mib, tk.engine_options()) == 7
+    for bad in ((0, mib, None), (2, -1, None), (2, mib, tk.engine_options(layers_per_grid=-1))):
+        with pytest.raises(tk.TopkvError):
+            f(*bad)
 
 
 def test_check_tables_validation(tk):

@@ -128,6 +128,50 @@ def test_engine_sub_range_and_one_layer(tk):
     assert np.array_equal(to_host(dst), want_dst)
 
 
+@pytest.mark.parametrize("per", [1, 2, 3, 0], ids=["grids1", "grids2", "grids3", "library"])
+@pytest.mark.parametrize("short", [False, True], ids=["fit", "short_stride"])
+def test_engine_grids_of_a_few_layers(tk, per, short):
+    """A range issued as consecutive hardware-dispatched grids of `per`
+    layers (0: the library's split, one grid at this size) moves every layer
+    as one grid would.  With a layer stride one word short of a layer's
+    packed batch, every layer - the first and last of each grid included,
+    and a one-layer grid's - leaves its last request unmoved (its block
+    would cross the layer's end), with the buffer sized past the last block
+    so that only the stride bounds it."""
+    wl = make_workload("llama3-70b-batch8", num_layers=7, seq_lens=[300, 17, 1000, 64, 33])
+    say(f"[engine grids] {wl.describe()} layers per grid {per or 'library'}, short stride {short}")
+    src_h, dst_h = host_src_pool(wl), host_dst_prefill(wl)
+    src, dst = to_dev(src_h), to_dev(dst_h)
+    bt, bt2, lens = to_dev(wl.block_tables), to_dev(wl.dst_block_tables), to_dev(wl.seq_lens)
+    nbytes = tk.topkv_packed_layer_bytes(src, wl.seq_lens)
+    L, R = wl.num_layers, wl.num_reqs
+    stride = nbytes - 2 if short else nbytes + 512
+    total = L * stride + 4096
+    buf = torch.full((total // 2,), SENTINEL, dtype=torch.int16, device="cuda")
+    opt = tk.engine_options(layers_per_grid=per)
+    assert tk.topkv_engine_layers_per_grid(L, stride, opt) == (per or L)
+    tk.topkv_engine_pack_layers(src, 0, L, R, bt, bt.shape[1], lens, buf, stride, packed_bytes=total, engine=opt)
+    torch.cuda.synchronize()
+    row_bytes = wl.planes * wl.num_heads * wl.head_dim * 2
+    keep = (nbytes - int(wl.seq_lens[-1]) * row_bytes) if short else nbytes   # bytes of the requests moved
+    h = to_host(buf)
+    want_dst = dst_h.copy()
+    for z in range(L):
+        want = oracle.pack_layer(src_h, z, wl.block_tables, wl.seq_lens)
+        got = h[z * stride // 2:z * stride // 2 + min(stride, nbytes) // 2]
+        assert np.array_equal(got[:keep // 2], want[:keep // 2]), f"layer {z}: moved requests differ from the oracle"
+        assert (got[keep // 2:] == SENTINEL).all(), f"layer {z}: the request crossing the stride was moved"
+        if not short:
+            oracle.unpack_layer(want, want_dst, z, wl.dst_block_tables, wl.seq_lens)
+    assert (h[(L - 1) * stride // 2 + min(stride, nbytes) // 2:] == SENTINEL).all(), "bytes past the last block"
+    if not short:
+        assert _gaps_untouched(buf[:L * stride // 2], stride, L, nbytes)
+        tk.topkv_engine_unpack_layers(buf, stride, dst, 0, L, R, bt2, bt2.shape[1], lens, packed_bytes=total,
+                                      engine=opt)
+        torch.cuda.synchronize()
+        assert np.array_equal(to_host(dst), want_dst), "unpacked pool differs from the oracle"
+
+
 def test_engine_fullsize_headline_every_layer(tk):
     """The 70B / 4096-token request at full size, all 80 layers in one engine
     launch per direction (the benchmark's configuration): every layer's
