@@ -347,9 +347,11 @@ topkv_status_t topkv_kvcache1_pack_layer(const topkv_pool_t* src, int32_t layer,
                                          int64_t blob_bytes, hipStream_t stream);
 
 /* Layers [first_layer, first_layer + num_layers) of one request packed into
- * their rows of the blob's K and V tensors in one launch (a whole request at
- * once, when it is not shipped layer by layer); when one layer's work is too
- * large for that launch, one launch per layer.  The same result as
+ * their rows of the blob's K and V tensors in a few launches (a whole request
+ * at once, when it is not shipped layer by layer): grids of
+ * topkv_engine_layers_per_grid(num_layers, planes * seq_len * row bytes)
+ * layers each, as the layer engine issues them; when one layer's work is too
+ * large for such a grid, one launch per layer.  The same result as
  * topkv_kvcache1_pack_layer for each layer.  TOPKV_ERR_INVALID_ARG for a
  * layer range outside [0, src->num_layers), otherwise as
  * topkv_kvcache1_pack_layer; num_layers == 0 queues nothing. */
@@ -384,7 +386,7 @@ topkv_status_t topkv_kvcache1_unpack_layer(const void* blob, int64_t blob_bytes,
                                            hipStream_t stream);
 
 /* Layers [first_layer, first_layer + num_layers) of a blob scattered into a
- * pool, in one launch where it fits (see topkv_kvcache1_pack_layers). */
+ * pool, in the same grids (see topkv_kvcache1_pack_layers). */
 topkv_status_t topkv_kvcache1_unpack_layers(const void* blob, int64_t blob_bytes, const topkv_pool_t* dst,
                                             int32_t first_layer, int32_t num_layers, const int32_t* block_table,
                                             int32_t seq_len, hipStream_t stream);

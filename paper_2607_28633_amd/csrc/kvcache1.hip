@@ -998,8 +998,9 @@ topkv_status_t fused_blob_crcs(const topkv_pool_t* pool, const int32_t* table, i
 }
 
 // Layers [first_layer, first_layer + num_layers) of one request into (pack) or
-// out of (unpack) their rows of the blob's K and V tensors: one launch when
-// the layer dimension fits the direct grid, else one launch per layer.
+// out of (unpack) their rows of the blob's K and V tensors: grids of
+// topkv_engine_layers_per_grid layers when the layer dimension fits the
+// direct grid, else one launch per layer.
 topkv_status_t kv1_move_layers(bool pack, const topkv_pool_t* pool, int32_t first_layer, int32_t num_layers,
                                       const int32_t* block_table, int32_t seq_len, void* blob, int64_t blob_bytes,
                                       hipStream_t stream) {
@@ -1014,8 +1015,17 @@ topkv_status_t kv1_move_layers(bool pack, const topkv_pool_t* pool, int32_t firs
   const int64_t layer_rows = (int64_t)seq_len * b.row;                 // one layer's rows in one tensor
   unsigned char* k = static_cast<unsigned char*>(blob) + kHeaderBytes + first_layer * layer_rows;
   const int64_t cap = blob_bytes - (kHeaderBytes + first_layer * layer_rows);
-  st = topkv_internal::placed_layers_move(pack, pool, first_layer, num_layers, k, cap, b.k_bytes, layer_rows,
-                                          block_table, seq_len, stream);
+  // grids of the layer engine's length (the same measured effect: one grid over a long range of
+  // layers moves them slower than a few shorter grids back to back)
+  const int32_t per = topkv_engine_layers_per_grid(num_layers, (int64_t)pool->planes * layer_rows, nullptr);
+  if (per < 1) return TOPKV_ERR_INVALID_ARG;
+  for (int32_t j = 0; j < num_layers; j += per) {
+    const int32_t n = num_layers - j < per ? num_layers - j : per;
+    st = topkv_internal::placed_layers_move(pack, pool, first_layer + j, n, k + j * layer_rows, cap - j * layer_rows,
+                                            b.k_bytes, layer_rows, block_table, seq_len, stream);
+    if (st == TOPKV_ERR_UNSUPPORTED && j == 0) break;                   // too large for the layer grid
+    if (st != TOPKV_OK) return st;
+  }
   if (st != TOPKV_ERR_UNSUPPORTED) return st;
   for (int32_t l = 0; l < num_layers; ++l) {                            // too large for one grid
     st = topkv_internal::placed_layers_move(pack, pool, first_layer + l, 1, k + l * layer_rows, cap - l * layer_rows,

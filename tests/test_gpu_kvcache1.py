@@ -124,7 +124,7 @@ def test_kvcache1_fullsize_70b(tk):
     say(f"[kvcache1] full size: {wl.describe()}")
     src, dst = device_src_pool(wl), device_dst_prefill(wl)
     n = int(wl.seq_lens[0])
-    blob, ws = _blob_run(tk, wl, src, dst, 0, rid=42, mid=70, whole=True)   # all 80 layers in one launch
+    blob, ws = _blob_run(tk, wl, src, dst, 0, rid=42, mid=70, whole=True)   # all 80 layers in one call
     assert blob.numel() == 128 + 1_342_177_280
     hdr = okv.parse_header(blob[:128].cpu().numpy().tobytes())
     body = blob[128:].cpu().numpy()
