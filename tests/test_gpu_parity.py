@@ -86,6 +86,61 @@ def test_parity_batched(tk, case):
     _sweep_and_check(tk, wl, host_src_pool(wl), host_dst_prefill(wl), case)
 
 
+@pytest.mark.parametrize("short", [False, True], ids=["exact_cap", "cap_one_word_short"])
+def test_uneven_batch_hostile(tk, short):
+    """A batch whose requests differ widely in length (one of 512 pages, the
+    rest 0 to 129 pages): the direct grid's slots past each short request's
+    pages move nothing, invalid table entries deep in the long requests are
+    skipped, a capacity one word short leaves the last request unmoved, and
+    an unpack through a table with invalid entries writes nothing for them;
+    all else equals the oracle."""
+    lens = [8192, 0, 1, 17, 16, 33, 2049, 100]
+    wl = make_workload("llama3-70b-batch8", num_layers=1, seq_lens=lens, seed=13)
+    src_h, dst_h = host_src_pool(wl), host_dst_prefill(wl)
+    src, dst = to_dev(src_h), to_dev(dst_h)
+    P, NP, H, D = wl.page_size, wl.num_pages, wl.num_heads, wl.head_dim
+    nbytes = tk.topkv_packed_layer_bytes(src, wl.seq_lens)
+    cap = nbytes - 2 if short else nbytes
+    bt = wl.block_tables.copy()
+    assert bt.shape[1] == 512
+    say(f"[uneven_batch] {wl.describe()} cap {'short' if short else 'exact'}")
+    bad = [(0, 100), (0, 301), (0, 511), (6, 128)]            # entries deep in the two long requests
+    bt[0, 100], bt[0, 301], bt[0, 511], bt[6, 128] = -1, NP, -9, NP + 5
+    packed = torch.full((nbytes // 2 + 64,), 0x2B2B, dtype=torch.int16, device="cuda")
+    tk.topkv_pack_layer_batched(src, 0, wl.num_reqs, to_dev(bt), bt.shape[1], to_dev(wl.seq_lens), packed,
+                                dst_bytes=cap)
+    torch.cuda.synchronize()
+    got = to_host(packed)
+    want = oracle.pack_layer(src_h, 0, wl.block_tables, wl.seq_lens).copy()
+    row_words = wl.planes * H * D
+    offs = np.concatenate([[0], np.cumsum(wl.seq_lens.astype(np.int64) * row_words)])
+    for r, i in bad:
+        n = int(wl.seq_lens[r])
+        for c in range(wl.planes):
+            want[offs[r] + (c * n + i * P) * H * D:offs[r] + (c * n + min(n, (i + 1) * P)) * H * D] = 0x2B2B
+    if short:
+        want[offs[-2]:] = 0x2B2B                                # the last request's block would cross the end
+    assert np.array_equal(got[:want.size], want), f"pack: {int((got[:want.size] != want).sum())} words differ"
+    assert (got[want.size:] == 0x2B2B).all(), "write past the batch"
+    # unpack of the oracle's batch through a destination table with invalid entries in the long requests
+    full = oracle.pack_layer(src_h, 0, wl.block_tables, wl.seq_lens)
+    bt2 = wl.dst_block_tables.copy()
+    keep = {(0, 200): bt2[0, 200], (6, 120): bt2[6, 120]}
+    bt2[0, 200], bt2[6, 120] = -3, wl.dst_num_pages
+    tk.topkv_unpack_layer_batched(torch.from_numpy(full.view(np.int16)).cuda(), dst, 0, wl.num_reqs, to_dev(bt2),
+                                  bt2.shape[1], to_dev(wl.seq_lens), src_bytes=cap)
+    torch.cuda.synchronize()
+    want_dst = dst_h.copy()
+    saved = {k: want_dst[0, v].copy() for k, v in keep.items()}
+    lens_used = wl.seq_lens.copy()
+    if short:
+        lens_used[-1] = 0                                       # not moved: its block crosses the capacity
+    oracle.unpack_layer(full[:offs[-2]] if short else full, want_dst, 0, wl.dst_block_tables, lens_used)
+    for k, v in keep.items():
+        want_dst[0, v] = saved[k]
+    assert np.array_equal(to_host(dst), want_dst), "unpack differs from the oracle"
+
+
 @pytest.mark.parametrize("case", ["tiny", "deepseek-v3-mla-div16", "reblock-70b-div32", "odd-row-5B-u8"])
 def test_parity_single_request(tk, case):
     """topkv_pack_layer / topkv_unpack_layer, one call per request."""
