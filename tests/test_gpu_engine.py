@@ -174,13 +174,15 @@ def test_engine_grids_of_a_few_layers(tk, per, short):
 
 def test_engine_fullsize_headline_every_layer(tk):
     """The 70B / 4096-token request at full size, all 80 layers in one engine
-    launch per direction (the benchmark's configuration): every layer's
-    packed block and every destination layer slab against the oracle."""
+    call per direction (the benchmark's configuration: the library issues
+    it as three grids of 27, 27 and 26 layers): every layer's packed block
+    and every destination layer slab against the oracle."""
     wl = make_workload("llama3-70b-4k")
     say(f"[engine fullsize] {wl.describe()}")
     src, dst, bt, bt2, lens, nbytes = _setup(tk, wl, host_pools=False)
     L, R = wl.num_layers, wl.num_reqs
     packed = torch.empty((L, nbytes // 2), dtype=torch.int16, device="cuda")
+    assert tk.topkv_engine_layers_per_grid(L, nbytes) == 27     # the grids meet at layers 27 and 54
     before = dst.clone()
     tk.topkv_engine_pack_layers(src, 0, L, R, bt, bt.shape[1], lens, packed, nbytes)
     tk.topkv_engine_unpack_layers(packed, nbytes, dst, 0, L, R, bt2, bt2.shape[1], lens)
