@@ -148,3 +148,40 @@ def test_threaded_host_baseline_matches_oracle():
         bench.cpu_baseline(wl, hs, 0.05, refs)          # the oracle's results the threaded leg checks against
         res = bench.cpu_threaded(wl, hs, 0.05, refs, threads=3)
         assert res["value"] > 0 and res["threads"] == 3, wl.name
+
+
+def test_kernel_launches_per_sweep():
+    """The per-launch figures divide a sweep's time by its kernel launches:
+    one per layer in the per-layer mode; in the engine mode, the grids the
+    library issues for each engine call (topkv_engine_layers_per_grid over
+    the call's layers and the packed slot size) and one launch for every
+    layer that keeps its own call.  The ceiling copies run in the same layer
+    groups."""
+    import types
+
+    import bench
+    from paper_2607_28633_amd import topkv
+    from paper_2607_28633_amd.workloads import make_workload
+
+    def fake_setup(name):
+        wl = make_workload(name)
+        row = wl.num_heads * wl.head_dim * wl.elem_bytes
+        nbytes = wl.planes * row * int(wl.seq_lens.astype(np.int64).sum())
+        sl = max(nbytes, wl.num_reqs * wl.state_bytes if wl.layer_state else 0)
+        ring = bench.ring_slots(wl, sl)
+        return types.SimpleNamespace(wl=wl, tk=topkv, slice=sl, ring=ring, chunks=bench.engine_chunks(wl, ring))
+
+    want = {"llama3-70b-4k": 3, "llama3-70b-batch8": 20, "deepseek-v3-mla": 21, "reblock-70b": 80,
+            "llama3-8b": 1, "llama3-70b-tp8": 1}
+    for name, grids in want.items():
+        st = fake_setup(name)
+        assert [bench.sweep_grids(st, "engine", d) for d in (0, 1)] == [grids, grids], name
+        assert [bench.sweep_grids(st, "launches", d) for d in (0, 1)] == [st.wl.num_layers] * 2, name
+    st = fake_setup("llama3-70b-4k")
+    assert bench.layer_groups(st) == [(0, 27), (27, 27), (54, 26)]
+    assert "27 layers per grid" in bench.engine_kernel(st.wl, st, "unpack")
+    # windowed layers keep their own calls: gpt-oss alternates windowed and full-attention layers
+    st = fake_setup("gpt-oss-120b")
+    n_engine = sum(1 for kind, _, _ in st.chunks if kind == "engine")
+    n_layer = sum(1 for kind, _, _ in st.chunks if kind == "layer")
+    assert n_layer == 18 and bench.sweep_grids(st, "engine", 0) >= n_engine + n_layer

@@ -317,9 +317,12 @@ def test_engine_cancel_from_host(tk):
     assert np.all(to_host(buf) == SENTINEL)
 
 
-def test_engine_graph_replays(tk):
-    """Both directions captured into one HIP graph: every replay (with eager
-    work and synchronisation between replays) equals the eager result."""
+@pytest.mark.parametrize("per", [0, 1, 3], ids=["one_grid", "grids_of_1", "grids_of_3"])
+def test_engine_graph_replays(tk, per):
+    """Both directions captured into one HIP graph, the engine call issued as
+    one grid or as several (layers_per_grid 1 and 3 over 4 layers: several
+    kernel nodes per call): every replay (with eager work and
+    synchronisation between replays) equals the oracle."""
     wl = make_workload("llama3-70b-batch8", num_layers=4, seq_lens=[4096, 1000, 17, 2049])
     src_h, dst_h = host_src_pool(wl), host_dst_prefill(wl)
     src, dst = to_dev(src_h), to_dev(dst_h)
@@ -327,10 +330,11 @@ def test_engine_graph_replays(tk):
     nbytes = tk.topkv_packed_layer_bytes(src, wl.seq_lens)
     L, R = wl.num_layers, wl.num_reqs
     packed = torch.empty((L, nbytes // 2), dtype=torch.int16, device="cuda")
+    opt = tk.engine_options(layers_per_grid=per)
     g = torch.cuda.CUDAGraph()
     with torch.cuda.graph(g):
-        tk.topkv_engine_pack_layers(src, 0, L, R, bt, bt.shape[1], lens, packed, nbytes)
-        tk.topkv_engine_unpack_layers(packed, nbytes, dst, 0, L, R, bt2, bt2.shape[1], lens)
+        tk.topkv_engine_pack_layers(src, 0, L, R, bt, bt.shape[1], lens, packed, nbytes, engine=opt)
+        tk.topkv_engine_unpack_layers(packed, nbytes, dst, 0, L, R, bt2, bt2.shape[1], lens, engine=opt)
     want_dst = dst_h.copy()
     want = [oracle.pack_layer(src_h, z, wl.block_tables, wl.seq_lens) for z in range(L)]
     for z in range(L):
