@@ -1271,6 +1271,8 @@ def run_reshard(args):
     beside the full-head pack; unpack into a
     head-major pool beside the slot-major unpack; and pool-to-pool re-blocking
     (P -> P', one launch, no staging buffer) beside the pack + unpack pair.
+    The *_layers sweeps make the shards pack, the head-major unpack and the
+    re-block over runs of layers, one topkv_move_layers call per run.
     GB/s counts algorithmic bytes: each moved byte read once and written once
     per launch that moves it (the pair moves every byte twice)."""
     import torch
@@ -1299,6 +1301,12 @@ def run_reshard(args):
     def slab(l):
         return l % wl.phys_layers
 
+    def runs(k):
+        """(first layer, layers) of runs of at most k layers that start on a multiple of k (k divides the
+        packed ring and the slab count, so a run never wraps either)."""
+        assert ring % k == 0 or k == wl.phys_layers, (ring, k)
+        return [(l, min(k, L - l)) for l in range(0, L, k)]
+
     sweeps = {
         "pack_full": lambda: [topkv.prepare_pack_layer_batched_ex(
             src, slab(l), R, bt, bt.shape[1], lens, packed[l % ring], stream=None) for l in range(L)],
@@ -1315,6 +1323,17 @@ def run_reshard(args):
         "reblock_fused": lambda: [topkv.prepare_move_layer(
             topkv.pool_view(src, slab(l), bt, bt.shape[1]), topkv.pool_view(dst, slab(l), bt2, bt2.shape[1]),
             R, lens, H) for l in range(L)],
+        # the same moves over runs of layers in one call each (topkv_move_layers): runs of consecutive
+        # pool slabs and, where a packed side takes part, consecutive packed slots
+        "pack_shards_tp2_layers": lambda: [topkv.prepare_move_layers(
+            topkv.pool_view(src, slab(l), bt, bt.shape[1]), topkv.packed_view(half[l % ring], nbytes // 2, shards=2),
+            n, nbytes, R, lens, H) for l, n in runs(min(ring, wl.phys_layers))],
+        "unpack_head_major_layers": lambda: [topkv.prepare_move_layers(
+            topkv.packed_view(packed[l % ring]), topkv.pool_view(hm, slab(l), bt2, bt2.shape[1], head_major=True),
+            n, nbytes, R, lens, H) for l, n in runs(min(ring, wl.phys_layers))],
+        "reblock_fused_layers": lambda: [topkv.prepare_move_layers(
+            topkv.pool_view(src, slab(l), bt, bt.shape[1]), topkv.pool_view(dst, slab(l), bt2, bt2.shape[1]),
+            n, 0, R, lens, H) for l, n in runs(wl.phys_layers)],
     }
     graphs = {}
     for name, make in sweeps.items():

@@ -542,6 +542,27 @@ topkv_status_t topkv_move_layer(const topkv_view_t* src, const topkv_view_t* dst
                                 const int32_t* seq_lens, int32_t head_count, int32_t window,
                                 hipStream_t stream);
 
+/* A range of layers moved as topkv_move_layer moves one (same views, rules
+ * and errors), in a few launches instead of one per layer (a whole request
+ * resharded, re-blocked or re-laid out at once, when it is not moved layer
+ * by layer as the layers are produced, Section 5.2).  Layer z < num_layers
+ * of a pool view is pool layer view.layer + z (so view.layer + num_layers
+ * <= pool.num_layers); layer z of a packed view starts at data +
+ * z * packed_layer_stride and holds that view's region(s) (`bytes`, or S
+ * shard regions of `bytes` each), so with num_layers > 1 the stride is at
+ * least max(1, shards) * bytes and the buffer spans (num_layers - 1) *
+ * packed_layer_stride plus one layer's regions.  The layers go out as
+ * hardware-dispatched grids of topkv_engine_layers_per_grid layers (the
+ * bytes of one layer's packed regions, or for pool to pool the source
+ * tables' capacity) where a direct grid applies (no window, whole wave
+ * spans per token), else one launch per layer.  num_layers == 0 or
+ * num_reqs == 0 queues nothing.  Extra errors: TOPKV_ERR_INVALID_ARG for a
+ * negative num_layers or stride, a layer range outside a pool, or a stride
+ * that would overlap consecutive layers' packed regions. */
+topkv_status_t topkv_move_layers(const topkv_view_t* src, const topkv_view_t* dst, int32_t num_layers,
+                                 int64_t packed_layer_stride, int32_t num_reqs, const int32_t* seq_lens,
+                                 int32_t head_count, int32_t window, hipStream_t stream);
+
 /* Head-sliced pack: heads [head_begin, head_begin + head_count) of layer
  * `layer` of a slot-major pool into dst ([planes][n_r][head_count][dim] per
  * request, requests concatenated; dst_bytes is its capacity).  Same as

@@ -91,6 +91,7 @@ __device__ __forceinline__ uint32_t fdiv(uint32_t n, const FastDiv& f) {
 // One side of a move (kernel argument, by value).
 struct Side {
   char* base;               // pool: the layer slab; packed: the buffer
+  int64_t layer_stride;     // several layers on grid z: bytes from one layer's base to the next
   const int32_t* tables;    // pool: [num_reqs][bt_stride]
   int64_t page_bytes;
   int64_t plane_bytes;
@@ -115,7 +116,7 @@ struct Params {
   int32_t window;
   int32_t max_tok;          // lengths are clamped to [0, max_tok]
   int32_t n_host;           // one request with a host-side length: its tokens (else unused)
-  int32_t pad_;
+  int32_t layers;           // direct grids: layers on grid z (1: one layer)
 };
 
 // Per-request kept-token counts and first kept tokens, and the exclusive
@@ -376,7 +377,19 @@ __device__ __forceinline__ void direct_move(const Params& p, const int32_t* __re
   const uint32_t wave_first = __builtin_amdgcn_readfirstlane(threadIdx.x & ~63u);
   const uint3 b = grid_block();
   const uint32_t c = b.y;
-  const int32_t r = kBatch ? (int32_t)b.z : 0;
+  // grid z: the layer (one request), or layer * num_reqs + request (a batch over several layers)
+  uint32_t lz = 0;
+  int32_t r = 0;
+  if (!kBatch) {
+    lz = b.z;
+  } else if (p.layers > 1) {
+    lz = b.z / (uint32_t)p.num_reqs;
+    r = (int32_t)(b.z - lz * (uint32_t)p.num_reqs);
+  } else {
+    r = (int32_t)b.z;
+  }
+  const char* const src_base = p.src.base + (int64_t)lz * p.src.layer_stride;
+  char* const dst_base = p.dst.base + (int64_t)lz * p.dst.layer_stride;
   const uint32_t base = b.x * kTile;
   PageCache src_pc, dst_pc;
   {
@@ -432,11 +445,11 @@ __device__ __forceinline__ void direct_move(const Params& p, const int32_t* __re
       soff = ok[j] ? so : 0;
       doff[j] = o;
     }
-    v[j] = __builtin_nontemporal_load(reinterpret_cast<const V*>(p.src.base + soff));
+    v[j] = __builtin_nontemporal_load(reinterpret_cast<const V*>(src_base + soff));
   }
 #pragma unroll
   for (int j = 0; j < kVpt; ++j)
-    if (ok[j]) __builtin_nontemporal_store(v[j], reinterpret_cast<V*>(p.dst.base + doff[j]));
+    if (ok[j]) __builtin_nontemporal_store(v[j], reinterpret_cast<V*>(dst_base + doff[j]));
 }
 
 template <int VB, bool kHostLen>
@@ -545,11 +558,16 @@ KernelFn direct_kernel_for(int vb) {
 }
 
 // single_only: launch only the one-request direct grid (and report whether it
-// did through *launched); otherwise whichever grid applies.
+// did through *launched); otherwise whichever grid applies.  layers > 1: the
+// views' layers and the next layers - 1 on grid z of a direct grid (a pool
+// side's layer slabs follow each other; a packed side's layer z starts at
+// data + z * packed_layer_stride), launched only when a direct grid applies:
+// *launched stays false otherwise, with nothing queued.  The caller has
+// checked the layer ranges and the stride.
 topkv_status_t move_layer_impl(const topkv_view_t* src, const topkv_view_t* dst, int32_t num_reqs,
                                const int32_t* seq_lens, int32_t head_count, int32_t window,
                                const topkv_launch_t& launch, bool single_only, bool* launched,
-                               int32_t n_host = -1) {
+                               int32_t n_host = -1, int32_t layers = 1, int64_t packed_layer_stride = 0) {
   *launched = false;
   if (!src || !dst || !valid_layout(src->layout) || !valid_layout(dst->layout)) return TOPKV_ERR_INVALID_ARG;
   if (src->layout == TOPKV_LAYOUT_PACKED && dst->layout == TOPKV_LAYOUT_PACKED) return TOPKV_ERR_INVALID_ARG;
@@ -620,7 +638,8 @@ topkv_status_t move_layer_impl(const topkv_view_t* src, const topkv_view_t* dst,
     for (int i = 0; i < 2 && fits; ++i) {
       const topkv_view_t* v = sides[i];
       if (v->layout == TOPKV_LAYOUT_PACKED) {
-        fits = reinterpret_cast<uintptr_t>(v->data) % vb == 0 && (shards == 1 || packed_cap % vb == 0);
+        fits = reinterpret_cast<uintptr_t>(v->data) % vb == 0 && (shards == 1 || packed_cap % vb == 0) &&
+               packed_layer_stride % vb == 0;
       } else {
         const uintptr_t b = reinterpret_cast<uintptr_t>(v->pool.base);
         fits = b % vb == 0 && info[i].layer_bytes % vb == 0 && info[i].page_bytes % vb == 0 &&
@@ -647,11 +666,13 @@ topkv_status_t move_layer_impl(const topkv_view_t* src, const topkv_view_t* dst,
     Side& s = i == 0 ? p.src : p.dst;
     if (v->layout == TOPKV_LAYOUT_PACKED) {
       s.base = static_cast<char*>(v->data);
+      s.layer_stride = packed_layer_stride;
       s.packed = 1;
       s.page = make_div(1);
       continue;
     }
     s.base = static_cast<char*>(v->pool.base) + (int64_t)v->layer * info[i].layer_bytes;
+    s.layer_stride = info[i].layer_bytes;
     s.tables = v->block_tables;
     s.page_bytes = info[i].page_bytes;
     s.plane_bytes = info[i].plane_bytes;
@@ -672,6 +693,7 @@ topkv_status_t move_layer_impl(const topkv_view_t* src, const topkv_view_t* dst,
   p.window = window;
   p.max_tok = (int32_t)max_tok;
   p.n_host = host_len ? (n_host < max_tok ? n_host : (int32_t)max_tok) : 0;
+  p.layers = layers;
 
   int cus = 0;
   const topkv_status_t st = cu_count(&cus);
@@ -692,8 +714,9 @@ topkv_status_t move_layer_impl(const topkv_view_t* src, const topkv_view_t* dst,
   const bool direct = !single && TOPKV_RS_DIRECT && num_reqs > 1 && num_reqs <= 1024 && window == 0 && wave &&
                       geo->planes <= 65535 && plane_tiles * geo->planes * num_reqs <= ((int64_t)1 << 20);
   if (single_only && !single) return TOPKV_OK;
-  const dim3 grid = single   ? dim3((unsigned)plane_tiles, (unsigned)geo->planes)
-                    : direct ? dim3((unsigned)plane_tiles, (unsigned)geo->planes, (unsigned)num_reqs)
+  if (layers > 1 && !((single && layers <= 65535) || (direct && (int64_t)num_reqs * layers <= 65535))) return TOPKV_OK;
+  const dim3 grid = single   ? dim3((unsigned)plane_tiles, (unsigned)geo->planes, (unsigned)layers)
+                    : direct ? dim3((unsigned)plane_tiles, (unsigned)geo->planes, (unsigned)(num_reqs * layers))
                              : dim3((unsigned)blocks);
   if (plane_tiles == 0) return TOPKV_OK;   // a host-side length of 0: nothing to move
   const KernelFn fn = single   ? (host_len ? single_kernel_for<true>(vb) : single_kernel_for<false>(vb))
@@ -714,6 +737,75 @@ topkv_status_t move_layer(const topkv_view_t* src, const topkv_view_t* dst, int3
   topkv_launch_t launch = {stream, nullptr, nullptr};
   bool launched = false;
   return move_layer_impl(src, dst, num_reqs, seq_lens, head_count, window, launch, false, &launched);
+}
+
+// Layers [view.layer, view.layer + num_layers) of each pool side (a packed
+// side's layer z at data + z * packed_layer_stride), in grids of
+// topkv_engine_layers_per_grid layers (the bytes a layer moves: the packed
+// side's regions, or for pool to pool the source tables' capacity); a move
+// no direct grid takes runs one launch per layer.
+topkv_status_t move_layers(const topkv_view_t* src, const topkv_view_t* dst, int32_t num_layers,
+                           int64_t packed_layer_stride, int32_t num_reqs, const int32_t* seq_lens,
+                           int32_t head_count, int32_t window, hipStream_t stream) {
+  if (!src || !dst || num_layers < 0 || packed_layer_stride < 0 || head_count <= 0) return TOPKV_ERR_INVALID_ARG;
+  if (!valid_layout(src->layout) || !valid_layout(dst->layout)) return TOPKV_ERR_INVALID_ARG;
+  const topkv_view_t* sides[2] = {src, dst};
+  int64_t layer_bytes = 0;   // bytes one layer moves, at most (sizes the grids only)
+  for (int i = 0; i < 2; ++i) {
+    const topkv_view_t* v = sides[i];
+    if (v->layout == TOPKV_LAYOUT_PACKED) {
+      const int64_t regions = v->shards > 1 ? v->shards : 1;
+      int64_t span;
+      if (v->bytes < 0 || v->shards < 0 || __builtin_mul_overflow(regions, v->bytes, &span))
+        return TOPKV_ERR_INVALID_ARG;
+      if (num_layers > 1 && packed_layer_stride < span) return TOPKV_ERR_INVALID_ARG;   // layers would overlap
+      layer_bytes = span;
+      continue;
+    }
+    if (v->layer < 0 || num_layers > v->pool.num_layers - v->layer) return TOPKV_ERR_INVALID_ARG;
+  }
+  if (num_layers == 0 || num_reqs == 0) return TOPKV_OK;
+  if (layer_bytes == 0) {   // pool to pool: the source tables' capacity in tokens, every moved head
+    const topkv_pool_t& g = src->pool;
+    if (__builtin_mul_overflow((int64_t)num_reqs * src->bt_stride, (int64_t)g.page_size, &layer_bytes) ||
+        __builtin_mul_overflow(layer_bytes, (int64_t)g.planes * head_count * g.head_dim * g.elem_bytes,
+                               &layer_bytes))
+      layer_bytes = INT64_MAX;
+  }
+  const int32_t per = topkv_engine_layers_per_grid(num_layers, layer_bytes, nullptr);
+  if (per < 1) return TOPKV_ERR_INVALID_ARG;
+  topkv_launch_t launch = {stream, nullptr, nullptr};
+  for (int32_t j = 0; j < num_layers; j += per) {
+    const int32_t n = num_layers - j < per ? num_layers - j : per;
+    topkv_view_t s = *src, d = *dst;
+    topkv_view_t* moved[2] = {&s, &d};
+    for (topkv_view_t* v : moved) {
+      if (v->layout == TOPKV_LAYOUT_PACKED)
+        v->data = v->data ? static_cast<char*>(v->data) + (int64_t)j * packed_layer_stride : nullptr;
+      else
+        v->layer += j;
+    }
+    bool launched = false;
+    topkv_status_t st = n > 1 ? move_layer_impl(&s, &d, num_reqs, seq_lens, head_count, window, launch, false,
+                                                &launched, -1, n, packed_layer_stride)
+                              : TOPKV_OK;
+    if (st != TOPKV_OK) return st;
+    if (launched) continue;
+    // one launch per layer (one layer in this group, or a move no direct grid takes)
+    for (int32_t l = 0; l < n; ++l) {
+      topkv_view_t s1 = s, d1 = d;
+      topkv_view_t* one[2] = {&s1, &d1};
+      for (topkv_view_t* v : one) {
+        if (v->layout == TOPKV_LAYOUT_PACKED)
+          v->data = v->data ? static_cast<char*>(v->data) + (int64_t)l * packed_layer_stride : nullptr;
+        else
+          v->layer += l;
+      }
+      st = move_layer_impl(&s1, &d1, num_reqs, seq_lens, head_count, window, launch, false, &launched);
+      if (st != TOPKV_OK) return st;
+    }
+  }
+  return TOPKV_OK;
 }
 
 topkv_view_t pool_view(int32_t layout, const topkv_pool_t* pool, int32_t layer, const int32_t* tables,
@@ -770,6 +862,12 @@ topkv_status_t topkv_move_layer(const topkv_view_t* src, const topkv_view_t* dst
                                 const int32_t* seq_lens, int32_t head_count, int32_t window,
                                 hipStream_t stream) {
   return move_layer(src, dst, num_reqs, seq_lens, head_count, window, stream);
+}
+
+topkv_status_t topkv_move_layers(const topkv_view_t* src, const topkv_view_t* dst, int32_t num_layers,
+                                 int64_t packed_layer_stride, int32_t num_reqs, const int32_t* seq_lens,
+                                 int32_t head_count, int32_t window, hipStream_t stream) {
+  return move_layers(src, dst, num_layers, packed_layer_stride, num_reqs, seq_lens, head_count, window, stream);
 }
 
 topkv_status_t topkv_pack_layer_heads(const topkv_pool_t* src, int32_t layer, int32_t num_reqs,

@@ -45,7 +45,7 @@ EXPORTS = ["topkv_pack_layer", "topkv_unpack_layer", "topkv_pack_layer_batched",
            "topkv_unpack_layer_planes", "topkv_kvcache1_bytes", "topkv_kvcache1_workspace_bytes",
            "topkv_kvcache1_pack_layer", "topkv_kvcache1_seal", "topkv_kvcache1_verify",
            "topkv_kvcache1_unpack_layer", "topkv_crc64", "topkv_crc64_workspace_bytes", "topkv_dma_create",
-           "topkv_dma_submit", "topkv_dma_wait", "topkv_dma_destroy", "topkv_move_layer",
+           "topkv_dma_submit", "topkv_dma_wait", "topkv_dma_destroy", "topkv_move_layer", "topkv_move_layers",
            "topkv_pack_layer_heads", "topkv_unpack_layer_heads", "topkv_reblock_layer",
            "topkv_pack_layer_shards", "topkv_unpack_layer_shards", "topkv_packed_state_bytes",
            "topkv_pack_state_layer", "topkv_unpack_state_layer", "topkv_check_state_slots",
@@ -127,6 +127,8 @@ _SIGS = {
     "topkv_crc64_noalloc": (_I32, [_P, _I64, _P, _P]),
     "topkv_move_layer": (_I32, [ctypes.POINTER(topkv_view_t), ctypes.POINTER(topkv_view_t), _I32, _P, _I32,
                                 _I32, _P]),
+    "topkv_move_layers": (_I32, [ctypes.POINTER(topkv_view_t), ctypes.POINTER(topkv_view_t), _I32, _I64, _I32, _P,
+                                 _I32, _I32, _P]),
     "topkv_pack_layer_heads": (_I32, [_POOL, _I32, _I32, _P, _I32, _P, _I32, _I32, _P, _I64, _P]),
     "topkv_unpack_layer_heads": (_I32, [_P, _I64, _POOL, _I32, _I32, _P, _I32, _P, _I32, _I32, _P]),
     "topkv_reblock_layer": (_I32, [_POOL, _I32, _P, _I32, _POOL, _I32, _P, _I32, _I32, _P, _P]),
@@ -516,6 +518,12 @@ def topkv_move_layer(src: topkv_view_t, dst: topkv_view_t, num_reqs, seq_lens, h
                                  int(head_count), int(window), _stream(stream)))
 
 
+def topkv_move_layers(src: topkv_view_t, dst: topkv_view_t, num_layers, packed_layer_stride, num_reqs, seq_lens,
+                      head_count, window=0, stream=None) -> None:
+    _check(_lib.topkv_move_layers(ctypes.byref(src), ctypes.byref(dst), int(num_layers), int(packed_layer_stride),
+                                  int(num_reqs), _table_ptr(seq_lens), int(head_count), int(window), _stream(stream)))
+
+
 def topkv_pack_layer_heads(src, layer, num_reqs, block_tables, bt_stride, seq_lens, head_begin, head_count, dst,
                            dst_bytes=None, stream=None) -> None:
     _check(_lib.topkv_pack_layer_heads(ctypes.byref(_pool_arg(src)), int(layer), int(num_reqs),
@@ -649,6 +657,14 @@ def prepare_pack_layer_heads(src, layer, num_reqs, block_tables, bt_stride, seq_
             _I32(int(bt_stride)), _P(_table_ptr(seq_lens)), _I32(int(head_begin)), _I32(int(head_count)),
             _P(_ptr(dst)), _I64(_nbytes(dst, dst_bytes)), _P(_stream(stream)))
     return PreparedCall("topkv_pack_layer_heads", args, (pool,))
+
+
+def prepare_move_layers(src: topkv_view_t, dst: topkv_view_t, num_layers, packed_layer_stride, num_reqs, seq_lens,
+                        head_count, window=0, stream=None) -> PreparedCall:
+    args = (ctypes.byref(src), ctypes.byref(dst), _I32(int(num_layers)), _I64(int(packed_layer_stride)),
+            _I32(int(num_reqs)), _P(_table_ptr(seq_lens)), _I32(int(head_count)), _I32(int(window)),
+            _P(_stream(stream)))
+    return PreparedCall("topkv_move_layers", args, (src, dst))
 
 
 def prepare_move_layer(src: topkv_view_t, dst: topkv_view_t, num_reqs, seq_lens, head_count, window=0,

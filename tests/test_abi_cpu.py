@@ -223,6 +223,20 @@ def test_move_layer_validation(tk):
     _expect(tk, INV, tk.topkv_pack_layer_shards, good, 1, 2, bt, 4, lens, 0, 8, 0, buf, shard_bytes=1 << 20)
     _expect(tk, INV, tk.topkv_unpack_layer_shards, buf, good, 1, 2, bt, 4, lens, 0, 6, 4, shard_bytes=1 << 20)
     tk.topkv_move_layer(pv, pk, 0, 0, 8, stream=0)                             # no requests: nothing to launch
+    # layer ranges: a pool side's layers past the pool, negative counts or strides, overlapping packed layers
+    p0 = tk.pool_view(good, 0, bt, 4)
+    mv = tk.topkv_move_layers
+    _expect(tk, INV, mv, p0, pk, -1, 1 << 20, 2, lens, 8)
+    _expect(tk, INV, mv, p0, pk, 2, -1, 2, lens, 8)
+    _expect(tk, INV, mv, pv, pk, 2, 1 << 20, 2, lens, 8)                       # layers 1..2 of a 2-layer pool
+    _expect(tk, INV, mv, p0, pk, 2, (1 << 20) - 16, 2, lens, 8)                # layer 1 would overlap layer 0
+    _expect(tk, INV, mv, p0, tk.packed_view(buf, 1 << 20, shards=2), 2, 1 << 20, 2, lens, 8)   # two regions
+    _expect(tk, INV, mv, pk, p0, 2, (1 << 20) - 16, 2, lens, 8)
+    _expect(tk, INV, mv, bad, pk, 2, 1 << 20, 2, lens, 8)
+    _expect(tk, INV, mv, p0, pk, 2, 1 << 20, 2, lens, 0)                       # head_count 0
+    _expect(tk, INV, mv, p0, tk.pool_view(_pool(tk, base=0x900000), 1, bt, 4), 2, 0, 2, lens, 8)  # dst layers 1..2
+    mv(p0, pk, 2, 1 << 20, 0, 0, 8, stream=0)                                  # no requests: nothing to launch
+    mv(p0, pk, 0, 0, 2, lens, 8, stream=0)                                     # no layers: nothing to launch
 
 
 def test_state_layer_validation(tk):

@@ -307,3 +307,110 @@ def test_fullsize_head_major_70b(tk):
     assert np.array_equal(to_host(hm[0, page0]), want[0, page0]), "head-major page vs oracle"
     del src, hm
     torch.cuda.empty_cache()
+
+
+MULTI_CASES = [("h8-d128-p16-p64", 0), ("h8-d128-p16-p64", 40), ("h8-d16", 0), ("mla-p64-p16", 0)]
+
+
+@pytest.mark.parametrize("case,window", MULTI_CASES)
+def test_move_layers_matches_oracle(tk, case, window):
+    """topkv_move_layers over every layer of a range equals the oracle's move
+    of each layer: head-sliced pack into packed layers `stride` apart (slack
+    between them untouched), two shards per layer, the unpack back into a
+    pool, and pool-to-pool re-blocking from a later source layer.  With 2 KiB
+    rows the direct grid carries the layers on grid z (one request: the
+    one-request grid; a batch: the batched one); with 256-byte rows, or a
+    window, every layer takes its own launch."""
+    wl = WORKLOADS[case]()
+    C, H, D = _geom(wl)
+    L = wl.num_layers + 1
+    wl = make_workload(wl.name, num_layers=L, num_heads=H, head_dim=D, seq_lens=wl.seq_lens,
+                       page_size=wl.page_size, dst_page_size=wl.dst_page_size, elem_bytes=wl.elem_bytes)
+    say(f"[reshard] move_layers {case} W={window}: {wl.describe()}")
+    src_h, dst_h = host_src_pool(wl), host_dst_prefill(wl)
+    src, dst = to_dev(src_h), to_dev(dst_h)
+    bt, bt2, lens = to_dev(wl.block_tables), to_dev(wl.dst_block_tables), to_dev(wl.seq_lens)
+    E = wl.elem_bytes
+    for sub in ([(0, wl.num_reqs)] if wl.num_reqs == 1 else [(0, 1), (0, wl.num_reqs)]):
+        R = sub[1]
+        lens_r = wl.seq_lens[:R]
+        h0, hc, S = (0, H, 2) if H % 2 == 0 else (0, H, 1)
+        per = rs.packed_heads_elems(C, hc // S, D, lens_r, window)
+        cap = per + 32 // E                                     # each shard region with slack
+        stride = S * cap + 64 // E                              # and slack between layers
+        n_lay = L - 1
+        out = torch.full((n_lay * stride,), SENTINEL, dtype=src.dtype, device="cuda")
+        tk.topkv_move_layers(tk.pool_view(src, 1, bt, bt.shape[1], h0),
+                             tk.packed_view(out, cap * E, shards=S), n_lay, stride * E, R, lens, hc, window)
+        torch.cuda.synchronize()
+        got = to_host(out)
+        for z in range(n_lay):
+            want = rs.move_layer(rs.View(rs.POOL, src_h, 1 + z, wl.block_tables, h0),
+                                 rs.View(rs.PACKED, np.full(S * cap, SENTINEL, dtype=np.int16).view(src_h.dtype),
+                                         shards=S, shard_elems=cap), lens_r, hc, window)
+            assert np.array_equal(got[z * stride:z * stride + S * cap], want), f"R={R} pack layer {z}"
+            assert (got[z * stride + S * cap:(z + 1) * stride].view(np.int16) == SENTINEL).all(), \
+                f"R={R} layer {z}: slack between layers written"
+        # the packed layers back into pool layers 0.. of the destination
+        back = dst.clone()
+        tk.topkv_move_layers(tk.packed_view(out, cap * E, shards=S),
+                             tk.pool_view(back, 0, bt2, bt2.shape[1], h0), n_lay, stride * E, R, lens, hc, window)
+        # pool to pool: source layers 1.., destination layers 0..
+        rb = dst.clone()
+        tk.topkv_move_layers(tk.pool_view(src, 1, bt, bt.shape[1]), tk.pool_view(rb, 0, bt2, bt2.shape[1]),
+                             n_lay, 0, R, lens, H, window)
+        torch.cuda.synchronize()
+        want_back, want_rb = dst_h.copy(), dst_h.copy()
+        for z in range(n_lay):
+            rs.move_layer(rs.View(rs.PACKED, got[z * stride:z * stride + S * cap], shards=S, shard_elems=cap),
+                          rs.View(rs.POOL, want_back, z, wl.dst_block_tables, h0), lens_r, hc, window)
+            rs.move_layer(rs.View(rs.POOL, src_h, 1 + z, wl.block_tables, 0),
+                          rs.View(rs.POOL, want_rb, z, wl.dst_block_tables, 0), lens_r, H, window)
+        assert np.array_equal(to_host(back), want_back), f"R={R}: unpacked layers differ"
+        assert np.array_equal(to_host(rb), want_rb), f"R={R}: re-blocked layers differ"
+
+
+def test_fullsize_70b_move_layers(tk):
+    """70B, 4096 tokens, all 80 layers in one call (three grids of 27, 27 and
+    26 layers): both tensor-parallel shards of every layer equal the
+    per-layer shards calls, the unpack of those shards equals the per-layer
+    unpacks, and the pool-to-pool re-block (page 16 -> 64) equals the
+    per-layer re-block; one layer of each against the oracle."""
+    wl = make_workload("llama3-70b-4k", dst_page_size=64)
+    say(f"[reshard] move_layers full size: {wl.describe()}")
+    src, dst = device_src_pool(wl), device_dst_prefill(wl)
+    bt, bt2, lens = to_dev(wl.block_tables), to_dev(wl.dst_block_tables), to_dev(wl.seq_lens)
+    n, L = int(wl.seq_lens[0]), wl.num_layers
+    half = 2 * n * 4 * 128                                    # one shard of one layer, int16 words
+    layer_words = 2 * half
+    assert tk.topkv_engine_layers_per_grid(L, layer_words * 2) == 27
+    many = torch.empty(L * layer_words, dtype=torch.int16, device="cuda")
+    tk.topkv_move_layers(tk.pool_view(src, 0, bt, bt.shape[1]), tk.packed_view(many, half * 2, shards=2), L,
+                         layer_words * 2, 1, lens, 8)
+    one = torch.empty(layer_words, dtype=torch.int16, device="cuda")
+    for layer in range(L):
+        tk.topkv_pack_layer_shards(src, layer, 1, bt, bt.shape[1], lens, 0, 8, 2, one)
+        assert torch.equal(many[layer * layer_words:(layer + 1) * layer_words], one), f"shards layer {layer}"
+    want = oracle.pack_layer(to_host(src[40])[None], 0, wl.block_tables, wl.seq_lens).reshape(2, n, 8, 128)
+    got = to_host(many[40 * layer_words:41 * layer_words]).reshape(2, 2, n, 4, 128)   # shard, plane, token
+    assert np.array_equal(np.concatenate([got[0], got[1]], axis=-2), want), "layer 40 shards vs oracle"
+    # the shards back into a second pool (page 64) in one call, and layer by layer
+    a, b = dst.clone(), dst.clone()
+    tk.topkv_move_layers(tk.packed_view(many, half * 2, shards=2), tk.pool_view(a, 0, bt2, bt2.shape[1]), L,
+                         layer_words * 2, 1, lens, 8)
+    for layer in range(L):
+        tk.topkv_unpack_layer_shards(many[layer * layer_words:], b, layer, 1, bt2, bt2.shape[1], lens, 0, 8, 2,
+                                     shard_bytes=half * 2)
+    torch.cuda.synchronize()
+    assert torch.equal(a.view(torch.int16), b.view(torch.int16)), "unpacked shards differ from per-layer unpacks"
+    # pool to pool, every layer
+    tk.topkv_move_layers(tk.pool_view(src, 0, bt, bt.shape[1]), tk.pool_view(a, 0, bt2, bt2.shape[1]), L, 0, 1,
+                         lens, 8)
+    for layer in range(L):
+        tk.topkv_reblock_layer(src, layer, bt, bt.shape[1], b, layer, bt2, bt2.shape[1], 1, lens)
+    torch.cuda.synchronize()
+    assert torch.equal(a.view(torch.int16), b.view(torch.int16)), "re-blocked layers differ from per-layer re-blocks"
+    again = oracle.pack_layer(to_host(a[79])[None], 0, wl.dst_block_tables, wl.seq_lens)
+    assert np.array_equal(again, oracle.pack_layer(to_host(src[79])[None], 0, wl.block_tables, wl.seq_lens))
+    del src, dst, a, b, many, one
+    torch.cuda.empty_cache()
