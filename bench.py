@@ -270,14 +270,14 @@ def sweep_grids(setup, issue, direction):
 
 
 def engine_kernel(wl, setup, direction):
-    """The kernel an engine launch of the workload runs (the library's
+    """The kernel an engine call of the workload runs (the library's
     choice): with every layer ready, the batched direct grid with the layers
     on grid z while it fits that grid's limits, issued as grids of
     topkv_engine_layers_per_grid layers each, else the persistent
     kv_engine_kernel."""
     runs = [n for kind, _, n in setup.chunks if kind == "engine"]
     if not runs:
-        return "no engine launch (every layer has its own call)"
+        return "no engine call (every layer has its own call)"
     per = sorted({setup.tk.topkv_engine_layers_per_grid(n, setup.slice) for n in runs})
     if all(engine_direct(wl, direction, n) for n in runs):
         name = (f"kv_{direction}_kernel (batched direct grid, layers on grid z, "
@@ -295,7 +295,7 @@ def step_bytes(wl):
 
 def read_traffic(workload, engine=False):
     """HBM traffic per launch from the committed rocprofv3 --pmc summary of
-    the workload's per-layer launches (or of its engine launches), or None
+    the workload's per-layer launches (or of its engine grids), or None
     when the kernels' code has changed since the counters were taken."""
     path = os.path.join(PROFILES, f"kv_{'engine' if engine else 'pack_unpack'}_{workload}_pmc.txt")
     if not os.path.exists(path):
@@ -570,7 +570,7 @@ def ring_slots(wl, slice_bytes):
 def engine_chunks(wl, ring):
     """The sweep's launches under the layer engine: maximal runs of
     consecutive full-attention layers (no window, no fixed state) whose pool
-    slabs and packed slots are both consecutive, one engine launch each
+    slabs and packed slots are both consecutive, one engine call each
     ("engine", first layer, count); every other layer keeps its own call
     ("layer", l, 1)."""
     L, out, l = wl.num_layers, [], 0
