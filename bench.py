@@ -568,7 +568,7 @@ def ring_slots(wl, slice_bytes):
 
 
 def engine_chunks(wl, ring):
-    """The sweep's launches under the layer engine: maximal runs of
+    """The sweep's calls under the layer engine: maximal runs of
     consecutive full-attention layers (no window, no fixed state) whose pool
     slabs and packed slots are both consecutive, one engine call each
     ("engine", first layer, count); every other layer keeps its own call
