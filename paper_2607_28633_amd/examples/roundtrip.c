@@ -2,7 +2,9 @@
  * paged pool is packed (gather into the wire order [plane][token][head][dim]),
  * unpacked into a pool with another page size, packed again and compared; the
  * destination pool is then re-blocked back pool-to-pool and two head halves
- * are packed and checked against the full-head packed layer.  Then a
+ * are packed and checked against the full-head packed layer; the layer
+ * engine packs both layers in one call and is checked against the per-layer
+ * packs.  Then a
  * fixed-state layer: two requests' states are packed from a state cache and
  * unpacked into other slots of a second cache; and the device CRC-64 of
  * "123456789" is checked against the published CRC-64/XZ check value.
@@ -119,6 +121,25 @@ int main(void) {
                 return 1;
             }
     }
+
+    /* the layer engine: both layers in one call per direction, layer z's packed block at z * packed_bytes;
+     * block 1 is the layer packed above, block 0 the same as a single-layer pack of layer 0 */
+    void* d_two;
+    uint16_t* two = malloc(2 * packed_bytes);
+    if (!two) return 1;
+    HIP_OK(hipMalloc(&d_two, 2 * packed_bytes));
+    TOPKV_OK_OR_FAIL(topkv_engine_pack_layers(&src, 0, LAYERS, 1, d_bt_src, PAGES, d_len, d_two,
+                                              (int64_t)packed_bytes, (int64_t)(2 * packed_bytes), NULL, 0));
+    TOPKV_OK_OR_FAIL(topkv_pack_layer(&src, 0, d_bt_src, TOKENS, d_b, 0));
+    HIP_OK(hipDeviceSynchronize());
+    HIP_OK(hipMemcpy(two, d_two, 2 * packed_bytes, hipMemcpyDeviceToHost));
+    HIP_OK(hipMemcpy(b, d_b, packed_bytes, hipMemcpyDeviceToHost));
+    if (memcmp((const char*)two + packed_bytes, a, packed_bytes) != 0 || memcmp(two, b, packed_bytes) != 0) {
+        fprintf(stderr, "layer engine blocks differ from the per-layer packs\n");
+        return 1;
+    }
+    hipFree(d_two);
+    free(two);
 
     /* fixed-state layer: states of slots {3, 1} of layer 1, unpacked into slots {0, 2} of a second cache */
     enum { SLOTS = 4, STATE = 1000 };
