@@ -764,6 +764,9 @@ topkv_status_t move_layers(const topkv_view_t* src, const topkv_view_t* dst, int
     }
     if (v->layer < 0 || num_layers > v->pool.num_layers - v->layer) return TOPKV_ERR_INVALID_ARG;
   }
+  int64_t last;   // the last layer's offset on a packed side
+  if (num_layers > 1 && __builtin_mul_overflow((int64_t)(num_layers - 1), packed_layer_stride, &last))
+    return TOPKV_ERR_INVALID_ARG;
   if (num_layers == 0 || num_reqs == 0) return TOPKV_OK;
   if (layer_bytes == 0) {   // pool to pool: the source tables' capacity in tokens, every moved head
     const topkv_pool_t& g = src->pool;

@@ -235,6 +235,8 @@ def test_move_layer_validation(tk):
     _expect(tk, INV, mv, bad, pk, 2, 1 << 20, 2, lens, 8)
     _expect(tk, INV, mv, p0, pk, 2, 1 << 20, 2, lens, 0)                       # head_count 0
     _expect(tk, INV, mv, p0, tk.pool_view(_pool(tk, base=0x900000), 1, bt, 4), 2, 0, 2, lens, 8)  # dst layers 1..2
+    p4 = tk.pool_view(_pool(tk, num_layers=4), 0, bt, 4)
+    _expect(tk, INV, mv, p4, pk, 4, 1 << 62, 2, lens, 8)                       # 3 * stride overflows int64
     mv(p0, pk, 2, 1 << 20, 0, 0, 8, stream=0)                                  # no requests: nothing to launch
     mv(p0, pk, 0, 0, 2, lens, 8, stream=0)                                     # no layers: nothing to launch
 
