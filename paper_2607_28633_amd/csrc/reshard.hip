@@ -770,10 +770,13 @@ topkv_status_t move_layers(const topkv_view_t* src, const topkv_view_t* dst, int
   if (num_layers == 0 || num_reqs == 0) return TOPKV_OK;
   if (layer_bytes == 0) {   // pool to pool: the source tables' capacity in tokens, every moved head
     const topkv_pool_t& g = src->pool;
-    if (__builtin_mul_overflow((int64_t)num_reqs * src->bt_stride, (int64_t)g.page_size, &layer_bytes) ||
-        __builtin_mul_overflow(layer_bytes, (int64_t)g.planes * head_count * g.head_dim * g.elem_bytes,
-                               &layer_bytes))
-      layer_bytes = INT64_MAX;
+    const int64_t factors[] = {src->bt_stride, g.page_size, g.planes, head_count, g.head_dim, g.elem_bytes};
+    layer_bytes = num_reqs;
+    for (const int64_t f : factors)
+      if (f < 0 || __builtin_mul_overflow(layer_bytes, f, &layer_bytes)) {
+        layer_bytes = INT64_MAX;   // only sizes the grids; the move itself validates the pool
+        break;
+      }
   }
   const int32_t per = topkv_engine_layers_per_grid(num_layers, layer_bytes, nullptr);
   if (per < 1) return TOPKV_ERR_INVALID_ARG;
