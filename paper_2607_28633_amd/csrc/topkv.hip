@@ -1020,7 +1020,7 @@ topkv_status_t engine_move(bool pack, const topkv_pool_t* pool, int32_t first_la
       MoveParams q = p;
       q.z_layers = n;
       q.packed_cap = packed_cap - (int64_t)j * layer_stride;          // >= 0: j <= layers - 1
-      int64_t span;   // this grid's layers' blocks: n * layer_stride (no overflow: at most packed_cap + layer_stride)
+      int64_t span;   // this grid's layers' blocks, n * layer_stride
       if (layers > 1 && !__builtin_mul_overflow((int64_t)n, layer_stride, &span) && q.packed_cap > span)
         q.packed_cap = span;
       char* pool_j = pool_ptr + (int64_t)j * g.layer_bytes;
