@@ -75,6 +75,9 @@
 #ifndef TOPKV_THREADS
 #define TOPKV_THREADS 256     // threads per workgroup (a multiple of 64)
 #endif
+#ifndef TOPKV_SMALL_THREADS
+#define TOPKV_SMALL_THREADS 128  // direct grids over 4-8 KiB page planes (TOPKV_THREADS: off)
+#endif
 #ifndef TOPKV_ENGINE_GRID_BYTES
 #define TOPKV_ENGINE_GRID_BYTES (512ll << 20)  // engine without waits: packed bytes per hardware-dispatched grid
 #endif
@@ -83,6 +86,8 @@ namespace topkv {
 
 constexpr int kThreads = TOPKV_THREADS;
 constexpr int kWaves = kThreads / 64;
+constexpr int kSmallThreads = TOPKV_SMALL_THREADS;
+static_assert(kSmallThreads % 64 == 0 && kSmallThreads <= kThreads, "small-plane workgroups are whole waves");
 
 template <int B> struct Vec;
 template <> struct Vec<16> { typedef unsigned int type __attribute__((ext_vector_type(4))); };
@@ -186,52 +191,53 @@ __device__ void request_prefix(const MoveParams& p, const int32_t* __restrict__ 
   __syncthreads();
 }
 
-// A tile is up to kThreads * VPT vectors of VB bytes.  Lane t handles vectors
-// t, t + kThreads, ... so each wave instruction covers one contiguous span.
-template <int VB, int VPT>
+// A tile is up to NT * VPT vectors of VB bytes, NT the workgroup's threads.
+// Lane t handles vectors t, t + NT, ... so each wave instruction covers one
+// contiguous span.
+template <int VB, int VPT, int NT = kThreads>
 __device__ __forceinline__ void load_tile(typename Vec<VB>::type (&v)[VPT], const char* __restrict__ src,
                                           int32_t nv) {
   typedef typename Vec<VB>::type V;
   const V* __restrict__ s = reinterpret_cast<const V*>(src);
-  if (nv == kThreads * VPT) {
+  if (nv == NT * VPT) {
 #pragma unroll
     for (int j = 0; j < VPT; ++j) {
 #if TOPKV_NT_LOADS
-      v[j] = __builtin_nontemporal_load(s + j * kThreads + threadIdx.x);
+      v[j] = __builtin_nontemporal_load(s + j * NT + threadIdx.x);
 #else
-      v[j] = s[j * kThreads + threadIdx.x];
+      v[j] = s[j * NT + threadIdx.x];
 #endif
     }
   } else {
-    // Ragged tile (1 <= nv < kThreads * VPT): every lane still issues all VPT
+    // Ragged tile (1 <= nv < NT * VPT): every lane still issues all VPT
     // loads back to back (indices clamped into the tile, so they stay in
     // bounds); only the stores are predicated.
 #pragma unroll
     for (int j = 0; j < VPT; ++j) {
-      const int idx = j * kThreads + threadIdx.x;
+      const int idx = j * NT + threadIdx.x;
       v[j] = s[idx < nv ? idx : nv - 1];
     }
   }
 }
 
-template <int VB, int VPT>
+template <int VB, int VPT, int NT = kThreads>
 __device__ __forceinline__ void store_tile(char* __restrict__ dst, const typename Vec<VB>::type (&v)[VPT],
                                            int32_t nv) {
   typedef typename Vec<VB>::type V;
   V* __restrict__ d = reinterpret_cast<V*>(dst);
-  if (nv == kThreads * VPT) {
+  if (nv == NT * VPT) {
 #pragma unroll
     for (int j = 0; j < VPT; ++j) {
 #if TOPKV_NT_STORES
-      __builtin_nontemporal_store(v[j], d + j * kThreads + threadIdx.x);
+      __builtin_nontemporal_store(v[j], d + j * NT + threadIdx.x);
 #else
-      d[j * kThreads + threadIdx.x] = v[j];
+      d[j * NT + threadIdx.x] = v[j];
 #endif
     }
   } else {
 #pragma unroll
     for (int j = 0; j < VPT; ++j) {
-      const int idx = j * kThreads + threadIdx.x;
+      const int idx = j * NT + threadIdx.x;
       if (idx < nv) d[idx] = v[j];
     }
   }
@@ -287,11 +293,11 @@ __device__ __forceinline__ uint3 grid_block() {
 #endif
 }
 
-template <int VB, int VPT, bool kPack, bool kBatched>
+template <int VB, int VPT, bool kPack, bool kBatched, int NT>
 __device__ __forceinline__ void move_direct(char* __restrict__ pool, char* __restrict__ packed,
                                             const int32_t* __restrict__ tables,
                                             const int32_t* __restrict__ seq_lens, const MoveParams& p) {
-  constexpr int32_t kTile = kThreads * VPT * VB;
+  constexpr int32_t kTile = NT * VPT * VB;
   // grid: z = request (single request: z = layer after the first; a batch
   // over several layers: z = layer * num_reqs + request), y = table entry,
   // x = plane * tiles_per_plane + tile
@@ -346,7 +352,7 @@ __device__ __forceinline__ void move_direct(char* __restrict__ pool, char* __res
   typename Vec<VB>::type v[VPT];
   // Pack: the pool loads go out before the token offset is known (their
   // addresses do not depend on it), so the offset sum overlaps them.
-  if (kPack) load_tile<VB, VPT>(v, pool_ptr, nv);
+  if (kPack) load_tile<VB, VPT, NT>(v, pool_ptr, nv);
   const int32_t tok0 = (kBatched && r > 0) ? tokens_before(seq_lens, r, max_tok, p.window, mine) : 0;
   int64_t plane_off, end;
   if (!kBatched && p.plane_stride > 0) {          // caller-placed planes (one request)
@@ -360,10 +366,10 @@ __device__ __forceinline__ void move_direct(char* __restrict__ pool, char* __res
   if (kBatched && p.z_layers > 1 && end > p.layer_stride) return;   // stays inside its layer's block
   char* packed_ptr = packed + lz * p.layer_stride + plane_off + (int64_t)(lo - start) * p.row_bytes + tstart;
   if (kPack) {
-    store_tile<VB, VPT>(packed_ptr, v, nv);
+    store_tile<VB, VPT, NT>(packed_ptr, v, nv);
   } else {
-    load_tile<VB, VPT>(v, packed_ptr, nv);
-    store_tile<VB, VPT>(pool_ptr, v, nv);
+    load_tile<VB, VPT, NT>(v, packed_ptr, nv);
+    store_tile<VB, VPT, NT>(pool_ptr, v, nv);
   }
 }
 
@@ -626,22 +632,26 @@ __global__ __launch_bounds__(kThreads) void kv_engine_kernel(char* __restrict__ 
 // a host-side length, 2 = direct grid for a batch with device lengths.
 enum { kStrided = 0, kDirectSingle = 1, kDirectBatched = 2 };
 
-// VB: bytes per vector (16 on the fast path); VPT: vectors per lane per tile,
-// so a tile is kThreads * VPT * VB bytes (chosen per launch to fit a page plane).
-template <int VB, int VPT, int kMode>
-__global__ __launch_bounds__(kThreads) void kv_pack_kernel(char* __restrict__ pool, char* __restrict__ packed,
-                                                           const int32_t* __restrict__ tables,
-                                                           const int32_t* __restrict__ seq_lens, MoveParams p) {
+// VB: bytes per vector (16 on the fast path); VPT: vectors per lane per tile;
+// NT: threads per workgroup (kThreads, or kSmallThreads for direct grids over
+// small page planes), so a tile is NT * VPT * VB bytes (chosen per launch to
+// fit a page plane).  The persistent grid runs kThreads only.
+template <int VB, int VPT, int kMode, int NT>
+__global__ __launch_bounds__(NT) void kv_pack_kernel(char* __restrict__ pool, char* __restrict__ packed,
+                                                     const int32_t* __restrict__ tables,
+                                                     const int32_t* __restrict__ seq_lens, MoveParams p) {
+  static_assert(kMode != kStrided || NT == kThreads, "the persistent grid runs kThreads-wide workgroups");
   if (kMode == kStrided) move_strided<VB, VPT, true>(pool, packed, tables, seq_lens, p);
-  else move_direct<VB, VPT, true, kMode == kDirectBatched>(pool, packed, tables, seq_lens, p);
+  else move_direct<VB, VPT, true, kMode == kDirectBatched, NT>(pool, packed, tables, seq_lens, p);
 }
 
-template <int VB, int VPT, int kMode>
-__global__ __launch_bounds__(kThreads) void kv_unpack_kernel(char* __restrict__ pool, char* __restrict__ packed,
-                                                             const int32_t* __restrict__ tables,
-                                                             const int32_t* __restrict__ seq_lens, MoveParams p) {
+template <int VB, int VPT, int kMode, int NT>
+__global__ __launch_bounds__(NT) void kv_unpack_kernel(char* __restrict__ pool, char* __restrict__ packed,
+                                                       const int32_t* __restrict__ tables,
+                                                       const int32_t* __restrict__ seq_lens, MoveParams p) {
+  static_assert(kMode != kStrided || NT == kThreads, "the persistent grid runs kThreads-wide workgroups");
   if (kMode == kStrided) move_strided<VB, VPT, false>(pool, packed, tables, seq_lens, p);
-  else move_direct<VB, VPT, false, kMode == kDirectBatched>(pool, packed, tables, seq_lens, p);
+  else move_direct<VB, VPT, false, kMode == kDirectBatched, NT>(pool, packed, tables, seq_lens, p);
 }
 
 // ---------------------------------------------------------------------------
@@ -702,9 +712,9 @@ int vector_bytes(uintptr_t a, uintptr_t b, int64_t row) {
 
 typedef void (*KernelFn)(char*, char*, const int32_t*, const int32_t*, MoveParams);
 
-template <int VB, int VPT, int kMode>
+template <int VB, int VPT, int kMode, int NT = kThreads>
 KernelFn kernel_for(bool pack) {
-  return pack ? kv_pack_kernel<VB, VPT, kMode> : kv_unpack_kernel<VB, VPT, kMode>;
+  return pack ? kv_pack_kernel<VB, VPT, kMode, NT> : kv_unpack_kernel<VB, VPT, kMode, NT>;
 }
 
 template <int kMode>
@@ -725,19 +735,49 @@ KernelFn pick_kernel_mode(bool pack, int vb, int vpt) {
   }
 }
 
-KernelFn pick_kernel(bool pack, int vb, int vpt, bool direct, bool batched) {
+// threads: kThreads, or kSmallThreads as launch_threads chose it (then the
+// tile is 2 vectors of 16 bytes per lane; null for any other combination).
+KernelFn pick_kernel(bool pack, int vb, int vpt, bool direct, bool batched, int threads = kThreads) {
+  if (threads != kThreads) {
+    if (!direct || vb != 16 || vpt != 2 || threads != kSmallThreads) return nullptr;
+    return batched ? kernel_for<16, 2, kDirectBatched, kSmallThreads>(pack)
+                   : kernel_for<16, 2, kDirectSingle, kSmallThreads>(pack);
+  }
   if (!direct) return pick_kernel_mode<kStrided>(pack, vb, vpt);
   return batched ? pick_kernel_mode<kDirectBatched>(pack, vb, vpt) : pick_kernel_mode<kDirectSingle>(pack, vb, vpt);
 }
 
 // Vectors per lane for 16-byte vectors: the largest of TOPKV_VPT, 4, 2, 1
-// whose tile still fits in one page plane, so small planes (e.g. 16 KiB for
-// 1 KiB rows in 16-token pages) get full tiles instead of half-empty ones.
-int vectors_per_lane(int vb, int64_t plane_bytes) {
+// whose tile of `threads` lanes still fits in one page plane, so small planes
+// (e.g. 16 KiB for 1 KiB rows in 16-token pages) get full tiles instead of
+// half-empty ones.
+int vectors_per_lane(int vb, int64_t plane_bytes, int threads = kThreads) {
   if (vb != 16) return TOPKV_VPT;
   for (int v = TOPKV_VPT; v > 1; v >>= 1)
-    if ((int64_t)kThreads * v * 16 <= plane_bytes) return v;
+    if ((int64_t)threads * v * 16 <= plane_bytes) return v;
   return 1;
+}
+
+// Threads per workgroup of a launch.  A direct grid over page planes of 4 to
+// 8 KiB (one KV head of 128 bf16 in 16-token pages: 4 KiB) runs
+// kSmallThreads-wide workgroups with two 16-byte vectors per lane, where
+// kThreads lanes would hold one vector each: half the waves per tile, each
+// with twice the loads in flight.  Pack and unpack both take it (a pack
+// grid runs at its best after an unpack grid of the same width).  Larger
+// planes, and the persistent grid, run kThreads.
+int launch_threads(bool direct, int vb, int64_t plane_bytes) {
+  if (direct && vb == 16 && kSmallThreads < kThreads && plane_bytes >= (int64_t)kSmallThreads * 2 * 16 &&
+      plane_bytes < (int64_t)kThreads * 2 * 16)
+    return kSmallThreads;
+  return kThreads;
+}
+
+// launch_threads for a launch whose grid is already laid out in tiles of
+// `tile` bytes (kThreads lanes): the narrower workgroup is taken only when its
+// own tile has the same size, so the grid and tiles_per_plane stand.
+int narrow_threads(bool direct, int vb, int64_t plane_bytes, int64_t tile) {
+  const int t = launch_threads(direct, vb, plane_bytes);
+  return (int64_t)t * vectors_per_lane(vb, plane_bytes, t) * vb == tile ? t : kThreads;
 }
 
 // Shared launcher for the four movement entry points.
@@ -862,13 +902,16 @@ topkv_status_t launch_move(bool pack, const topkv_pool_t* pool, int32_t layer, v
   const size_t lds = (seq_lens && !direct) ? sizeof(uint64_t) * kWaves + sizeof(int32_t) * 3 * ((size_t)num_reqs + 1)
                                            : (direct ? (size_t)TOPKV_DIRECT_LDS_PAD : 0);
   void* args[] = {&pool_ptr, &packed_ptr, &tables, &seq_lens, &p};
-  const void* fn = reinterpret_cast<const void*>(pick_kernel(pack, vb, vpt, direct, seq_lens != nullptr));
+  const int threads = narrow_threads(direct, vb, g.plane_bytes, tile);
+  const void* fn = reinterpret_cast<const void*>(
+      pick_kernel(pack, vb, vectors_per_lane(vb, g.plane_bytes, threads), direct, seq_lens != nullptr, threads));
+  if (!fn) return TOPKV_ERR_UNSUPPORTED;
   hipError_t e;
   if (launch->start || launch->stop)
-    e = hipExtLaunchKernel(fn, grid3, dim3(kThreads), args, lds, launch->stream, launch->start,
+    e = hipExtLaunchKernel(fn, grid3, dim3(threads), args, lds, launch->stream, launch->start,
                            launch->stop, 0);
   else
-    e = hipLaunchKernel(fn, grid3, dim3(kThreads), args, lds, launch->stream);
+    e = hipLaunchKernel(fn, grid3, dim3(threads), args, lds, launch->stream);
   return e == hipSuccess ? TOPKV_OK : TOPKV_ERR_LAUNCH;
 }
 
@@ -1014,7 +1057,10 @@ topkv_status_t engine_move(bool pack, const topkv_pool_t* pool, int32_t first_la
   if (!waits && work <= TOPKV_DIRECT_MAX && bt_stride <= 65535 && num_reqs <= TOPKV_DIRECT_MAX_REQS &&
       (int64_t)num_reqs * layers <= 65535) {
     const int32_t per = engine_layers_per_grid(layers, layer_stride, opt);
-    const void* fn = reinterpret_cast<const void*>(pick_kernel(pack, vb, vpt, true, true));
+    const int threads = narrow_threads(true, vb, g.plane_bytes, tile);
+    const void* fn = reinterpret_cast<const void*>(
+        pick_kernel(pack, vb, vectors_per_lane(vb, g.plane_bytes, threads), true, true, threads));
+    if (!fn) return TOPKV_ERR_UNSUPPORTED;
     for (int32_t j = 0; j < layers; j += per) {
       const int32_t n = layers - j < per ? layers - j : per;
       MoveParams q = p;
@@ -1027,7 +1073,7 @@ topkv_status_t engine_move(bool pack, const topkv_pool_t* pool, int32_t first_la
       char* packed_j = packed_ptr + (int64_t)j * layer_stride;
       void* args[] = {&pool_j, &packed_j, &tables, &seq_lens, &q};
       const dim3 grid3((unsigned)per_page, (unsigned)bt_stride, (unsigned)(num_reqs * n));
-      if (hipLaunchKernel(fn, grid3, dim3(kThreads), args, (size_t)TOPKV_DIRECT_LDS_PAD, stream) != hipSuccess)
+      if (hipLaunchKernel(fn, grid3, dim3(threads), args, (size_t)TOPKV_DIRECT_LDS_PAD, stream) != hipSuccess)
         return TOPKV_ERR_LAUNCH;
     }
     return TOPKV_OK;

@@ -67,6 +67,9 @@ ENGINE_CASES = [
     (dict(name="llama3-70b-batch8", num_layers=3, seq_lens=[4096, 1000, 17, 0, 2049, 16, 33, 8192]), 0),
     (dict(name="deepseek-v3-mla", num_layers=3, seq_lens=[512, 4096, 65, 7000]), 4),
     (dict(name="reblock-70b", num_layers=2, seq_lens=[256, 4095, 999, 3000, 64]), 0),
+    (dict(name="tiny", num_layers=3, num_heads=3, seq_lens=[64, 48, 33, 17, 1]), 0),     # 6 KiB planes
+    (dict(name="tiny", num_layers=3, num_heads=1, head_dim=248, seq_lens=[64, 31, 16]), 0),   # 7.75 KiB
+    (dict(name="llama3-70b-tp8", num_layers=5, seq_lens=[4096]), 0),                    # 4 KiB, one request
 ]
 
 

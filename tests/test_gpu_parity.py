@@ -43,6 +43,11 @@ SMALL = {
     "odd-row-5B-u8": lambda: make_workload("tiny", num_heads=1, head_dim=5, elem_bytes=1, seq_lens=[19, 64]),
     "row-12B-u32": lambda: make_workload("tiny", num_heads=1, head_dim=3, elem_bytes=4, seq_lens=[5, 77]),
     "row-24B-u64": lambda: make_workload("tiny", num_heads=3, head_dim=1, elem_bytes=8, seq_lens=[31, 2, 17]),
+    # page planes of 6 KiB and 7.75 KiB: direct grids run 128-thread workgroups below 8 KiB planes, with a
+    # ragged second tile here; 8 KiB planes switch back to 256 threads
+    "plane-6k": lambda: make_workload("tiny", num_heads=3, seq_lens=[64, 48, 33, 17, 1]),
+    "plane-7.75k": lambda: make_workload("tiny", num_heads=1, head_dim=248, seq_lens=[64, 31, 16]),
+    "plane-8k": lambda: make_workload("tiny", num_heads=4, seq_lens=[64, 40, 9]),
     "page256-big-planes": lambda: make_workload("llama3-8b", num_layers=1, page_size=256, dst_page_size=16,
                                                 seq_lens=[1000, 513, 256]),
 }
