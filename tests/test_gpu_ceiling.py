@@ -55,7 +55,8 @@ def test_copy_tiles_follows_the_offsets(cl):
     rng = np.random.default_rng(9)
     so = rng.integers(0, (n_src - TILE) // 16, size=tiles) * 16
     do = rng.permutation(np.arange(0, (n_dst - TILE) // TILE + 1) * TILE)[:tiles - 4]   # non-overlapping
-    do = np.concatenate([do, [8, n_dst - TILE + 16, -TILE, n_dst]])   # misaligned, past the end, negative, past
+    # misaligned, past the end (fits a 16-byte tile only, after every slot), negative, past
+    do = np.concatenate([do, [8, n_dst - 16, -TILE, n_dst]])
     so[-1] = n_src - TILE + 32                                            # source past the end
     for lens in (None, rng.integers(1, TILE // 16 + 1, size=tiles) * 16):
         if lens is not None:
@@ -67,10 +68,13 @@ def test_copy_tiles_follows_the_offsets(cl):
         torch.cuda.synchronize()
         want = np.full(n_dst, 0x5A, dtype=np.uint8)
         h = src.cpu().numpy()
+        hit = np.zeros(n_dst, dtype=bool)
         for k in range(tiles):
             s0, d0, n = int(so[k]), int(do[k]), TILE if lens is None else int(lens[k])
             if (s0 | d0 | n) % 16 or n < 16 or n > TILE or s0 < 0 or d0 < 0 or s0 > n_src - n or d0 > n_dst - n:
                 continue
+            assert not hit[d0:d0 + n].any(), "copied tiles overlap: the result would depend on workgroup order"
+            hit[d0:d0 + n] = True
             want[d0:d0 + n] = h[s0:s0 + n]
         assert np.array_equal(dst.cpu().numpy(), want), lens is None
 
